@@ -1,0 +1,693 @@
+/*
+ * Reference oracle for the HAPMoE planner hot path -- TEST INFRASTRUCTURE ONLY.
+ * (Only tests, the smoke check and the bench's CPU-baseline leg use it.)
+ *
+ * Plain single-threaded C, fp64, IEEE + - * / and ceil only; build with
+ * -O2 -ffp-contract=off -fno-fast-math.  Each function names the passage of the
+ * paper it restates.  Readings of passages the paper leaves open are listed in
+ * the design notes of the repository and restated next to the code here.
+ */
+#include "hapmoe_oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+static int64_t q(double x) { return (int64_t)ceil(x); }   /* ns / bytes are whole numbers, rounded up */
+static int64_t min64(int64_t a, int64_t b) { return a < b ? a : b; }
+static int64_t max64(int64_t a, int64_t b) { return a > b ? a : b; }
+static int lg2(int v) { int r = 0; while ((1 << r) < v) r++; return r; }
+static int popc(int v) { int c = 0; while (v) { c += v & 1; v >>= 1; } return c; }
+
+int32_t orc_validate(const orc_problem *p)
+{
+    int N = p->n_layers, T = p->n_types;
+    if (N < 1 || N > 255 || T < 1 || T > ORC_MAX_TYPES) return -1;
+    if (p->seq_len < 1 || p->hidden < 1 || p->micro_batch_size < 1 || p->elem_bytes < 0) return -1;
+    if (p->n_experts < 0 || (p->n_experts > 0 && (p->top_k < 1 || p->top_k > p->n_experts))) return -1;
+    for (int l = 0; l < N; l++)
+        if (p->is_moe[l] && p->n_experts == 0) return -1;
+    for (int h = 0; h < T; h++) {
+        if (p->count[h] < 1 || p->speed[h] < 1 || p->mem_bytes[h] < 0 || !(p->eff[h] > 0.0)) return -1;
+        if (!(p->route_coef[h] >= 0.0)) return -1;
+        for (int g = 0; g < T; g++)
+            if (!(p->bw[h * ORC_MAX_TYPES + g] > 0.0) || !(p->alpha[h * ORC_MAX_TYPES + g] >= 0.0)) return -1;
+    }
+    for (int64_t i = 0; i < (int64_t)T * 16 * N; i++)
+        if (p->t_ffn[i] < 0 || p->t_ffn[i] > p->t_dense[i]) return -1;
+    if (!(p->rc_time >= 1.0) || !(p->rc_act >= 0.0 && p->rc_act <= 1.0)) return -1;
+    if (!(p->gamma >= 0.0 && p->gamma <= 1.0) || !(p->opt_coef >= 0.0) || !(p->moe_ffn_mult >= 0.0)) return -1;
+    if (p->delta_den < 1 || p->delta_num < 0 || p->delta_num >= p->delta_den || p->eta_prune < 0) return -1;
+    if (p->n_micro < 1 || p->n_micro > ORC_MAX_MICRO) return -1;
+    if (p->pp_max < 1 || p->pp_max > ORC_MAX_STAGES || p->mode < 0 || p->mode > 1) return -1;
+    for (int i = 0; i < p->n_micro; i++)
+        if (p->micro[i] < 1 || p->micro[i] > (1 << 20)) return -1;
+    return 0;
+}
+
+/* ------------------------------------------------------------------------
+ * Candidate set.  Section 3.1 output pi = (PP, TP, DP, EP, TPE, CP); the
+ * search of Section 3.4 / Algorithm 1 runs over a configuration set Pi.
+ * Reading: every stage is a group of G/PP devices (G = sum_h m_h); TP and CP
+ * split a stage group, DP = group / (TP*CP); the expert dimensions fold
+ * inside the group (EP*TPE divides it).  mode 1 instead takes the literal
+ * product PP*DP*TP*CP*EP*TPE = G.  Dense models use EP = TPE = 1.
+ * Loop order PP, TP, CP, EP, TPE ascending; candidate index
+ * ((config * n_orders) + order) * n_micro + micro_index.
+ * ---------------------------------------------------------------------- */
+int64_t orc_enumerate(const orc_problem *p, orc_config *out, int64_t cap)
+{
+    int G = 0;
+    for (int h = 0; h < p->n_types; h++) G += p->count[h];
+    int dense = (p->n_experts == 0);
+    int64_t n = 0;
+    for (int PP = 1; PP <= G; PP++) {
+        if (G % PP != 0 || PP > p->pp_max || PP > p->n_layers) continue;
+        int g = G / PP;
+        for (int i = 0; i < 4; i++) {
+            int TP = 1 << i;
+            if (!((p->tp_mask >> i) & 1) || g % TP != 0 || p->hidden % TP != 0) continue;
+            for (int j = 0; j < 4; j++) {
+                int CP = 1 << j;
+                if (!((p->cp_mask >> j) & 1) || p->seq_len % CP != 0) continue;
+                for (int EP = 1; EP <= (dense ? 1 : p->ep_max); EP *= 2) {
+                    if (!dense && p->n_experts % EP != 0) continue;
+                    for (int m = 0; m < 4; m++) {
+                        int TPE = 1 << m;
+                        if (dense ? (TPE != 1) : !((p->tpe_mask >> m) & 1)) continue;
+                        int DP;
+                        if (p->mode == 0) {
+                            if (g % (TP * CP) != 0 || g % (EP * TPE) != 0) continue;
+                            DP = g / (TP * CP);
+                        } else {
+                            int prod = TP * CP * EP * TPE;
+                            if (g % prod != 0) continue;
+                            DP = g / prod;
+                        }
+                        if (out && n < cap) {
+                            orc_config c = {PP, TP, CP, DP, EP, TPE};
+                            out[n] = c;
+                        }
+                        n++;
+                    }
+                }
+            }
+        }
+    }
+    return n;
+}
+
+/* Device-type orderings: all permutations of the type indices, lexicographic. */
+int32_t orc_n_orders(const orc_problem *p)
+{
+    int f = 1;
+    for (int i = 2; i <= p->n_types; i++) f *= i;
+    return f;
+}
+
+void orc_order(const orc_problem *p, int32_t o, int32_t *perm)
+{
+    /* o-th permutation in lexicographic order (factorial number system) */
+    int T = p->n_types, used[ORC_MAX_TYPES] = {0};
+    int fact = orc_n_orders(p);
+    for (int pos = 0; pos < T; pos++) {
+        fact /= (T - pos);
+        int k = o / fact;
+        o %= fact;
+        for (int h = 0; h < T; h++) {
+            if (used[h]) continue;
+            if (k == 0) { perm[pos] = h; used[h] = 1; break; }
+            k--;
+        }
+    }
+}
+
+int64_t orc_n_instances(const orc_problem *p)
+{
+    return orc_enumerate(p, NULL, 0) * orc_n_orders(p) * p->n_micro;
+}
+
+int32_t orc_instance(const orc_problem *p, int64_t idx, orc_config *cfg, int32_t *order, int32_t *micro)
+{
+    int64_t ncfg = orc_enumerate(p, NULL, 0);
+    int64_t per = (int64_t)orc_n_orders(p) * p->n_micro;
+    if (idx < 0 || idx >= ncfg * per) return -1;
+    orc_config *all = (orc_config *)malloc(sizeof(orc_config) * (size_t)ncfg);
+    orc_enumerate(p, all, ncfg);
+    *cfg = all[idx / per];
+    free(all);
+    *order = (int32_t)((idx / p->n_micro) % orc_n_orders(p));
+    *micro = p->micro[idx % p->n_micro];
+    return 0;
+}
+
+/* ------------------------------------------------------------------------
+ * Link model.  Section 3.2: collective time is a primitive-specific function
+ * of (bytes, world, link type).  Reading: an alpha-beta model per pair of
+ * device types; a group spanning several types runs at the slowest pair
+ * (largest latency, smallest bandwidth).  Ring all-reduce over w ranks moves
+ * 2(w-1)/w of the buffer in 2(w-1) steps.
+ * ---------------------------------------------------------------------- */
+static void mask_link(const orc_problem *p, int mask, double *alpha, double *bw)
+{
+    double a = 0.0, b = 0.0;
+    int first = 1;
+    for (int h = 0; h < p->n_types; h++) {
+        if (!((mask >> h) & 1)) continue;
+        for (int g = 0; g < p->n_types; g++) {
+            if (!((mask >> g) & 1)) continue;
+            double al = p->alpha[h * ORC_MAX_TYPES + g], bb = p->bw[h * ORC_MAX_TYPES + g];
+            if (first || al > a) a = al;
+            if (first || bb < b) b = bb;
+            first = 0;
+        }
+    }
+    *alpha = a;
+    *bw = b;
+}
+
+static double ring_allreduce(double bytes, int w, double alpha, double bw)
+{
+    if (w == 1) return 0.0;
+    double steps = (double)(2 * (w - 1));
+    return steps * alpha + ((steps * bytes) / (double)w) / bw;
+}
+
+/* tokens per rank of one micro-batch: S * micro_batch_size / CP */
+static double tokens(const orc_problem *p, const orc_config *c)
+{
+    return (double)((int64_t)p->seq_len * p->micro_batch_size / c->cp);
+}
+
+/* activation bytes of one micro-batch on one rank: tokens * H * beta */
+static double act_tensor(const orc_problem *p, const orc_config *c)
+{
+    return (tokens(p, c) * (double)p->hidden) * (double)p->elem_bytes;
+}
+
+/* Load-imbalance factor (Section 3.2): rho = max_e |T_e| / mean_e |T_e|,
+ * applied as 1 + gamma (rho - 1). */
+static double skew(const orc_problem *p, int layer)
+{
+    int E = p->n_experts;
+    int64_t sum = 0, mx = 0;
+    for (int e = 0; e < E; e++) {
+        int64_t v = p->expert_tokens[(int64_t)layer * E + e];
+        sum += v;
+        if (v > mx) mx = v;
+    }
+    double rho = sum > 0 ? (double)(mx * E) / (double)sum : 1.0;
+    return 1.0 + p->gamma * (rho - 1.0);
+}
+
+/* Eq. 2 (Section 3.2): per-layer compute on device type h,
+ *   t = t_base - t_ffn + mult * t_ffn / (eta_h * EP * TPE) + t_route(h),
+ * with t_route = route_coef_h * tokens * H and the expert part scaled by the
+ * load-imbalance factor.  Dense layers take t_base from the table. */
+void orc_type_terms_eval(const orc_problem *p, const orc_config *c, int32_t layer, int32_t h, orc_type_terms *o)
+{
+    int64_t off = (((int64_t)h * 4 + lg2(c->tp)) * 4 + lg2(c->cp)) * p->n_layers + layer;
+    double td = (double)p->t_dense[off], tf = (double)p->t_ffn[off];
+    if (!p->is_moe[layer]) {
+        o->comp = td;
+        o->expert = 0.0;
+    } else {
+        double route = p->route_coef[h] * (tokens(p, c) * (double)p->hidden);
+        o->comp = (td - tf) + route;
+        double xexp = (p->moe_ffn_mult * tf) / ((p->eff[h] * (double)c->ep) * (double)c->tpe);
+        o->expert = skew(p, layer) * xexp;
+    }
+    o->q_comp = q(o->comp);
+    o->q_expert = q(o->expert);
+}
+
+/* Communication of one layer on a stage whose devices span type set `mask`.
+ *  - dispatch/combine (Eq. 3): D_moe = tokens * H * beta * k * (1 - 1/EP) per
+ *    all-to-all; the all-gather dispatcher moves tokens * H * beta * (EP-1);
+ *    the cheaper primitive is used (all-to-all on ties), 4 transfers per
+ *    micro-batch (dispatch + combine, forward + backward), scaled by the
+ *    load-imbalance factor (the MoE critical path);
+ *  - TP: 4 ring all-reduces of the activation (2 for MoE layers, plus 2 over
+ *    the TPE group);
+ *  - CP: CP-1 ring steps exchanging K and V, forward + 2x backward. */
+void orc_mask_terms_eval(const orc_problem *p, const orc_config *c, int32_t layer, int32_t mask, orc_mask_terms *o)
+{
+    double alpha, bw;
+    mask_link(p, mask, &alpha, &bw);
+    double D = act_tensor(p, c);
+    if (!p->is_moe[layer]) {
+        o->a2a = 0.0;
+        o->tp = 4.0 * ring_allreduce(D, c->tp, alpha, bw);
+    } else {
+        double s = skew(p, layer);
+        double dm = (D * (double)p->top_k) * (1.0 - 1.0 / (double)c->ep);
+        double f_a2a = (double)(c->ep - 1) * alpha + dm / bw;
+        double f_ag = (double)(c->ep - 1) * alpha + (D * (double)(c->ep - 1)) / bw;
+        double sel = f_ag < f_a2a ? f_ag : f_a2a;
+        o->a2a = s * (4.0 * sel);
+        o->tp = 2.0 * ring_allreduce(D, c->tp, alpha, bw) + 2.0 * ring_allreduce(D, c->tpe, alpha, bw);
+    }
+    o->cp = c->cp == 1 ? 0.0 : 3.0 * ((double)(c->cp - 1) * (alpha + ((2.0 * D) / (double)c->tp) / bw));
+    o->q_a2a = q(o->a2a);
+    o->q_tp = q(o->tp);
+    o->q_cp = q(o->cp);
+    o->comm = o->q_a2a + o->q_tp + o->q_cp;
+    /* a stage spanning several types runs at its slowest type */
+    int64_t ce = -1;
+    for (int h = 0; h < p->n_types; h++) {
+        if (!((mask >> h) & 1)) continue;
+        orc_type_terms t;
+        orc_type_terms_eval(p, c, layer, h, &t);
+        if (t.q_comp + t.q_expert > ce) ce = t.q_comp + t.q_expert;
+    }
+    o->t_r0 = ce + o->comm;
+    o->t_r1 = q(p->rc_time * (double)o->t_r0);   /* recomputation: time x rc_time */
+}
+
+/* Stage memory model (Section 3.2): weights + gradients + optimizer states
+ * sharded by (TP, DP, EP, TPE); ZeRO-1 bf16 training keeps 2 + 4 bytes per
+ * parameter plus 12 bytes of fp32 optimizer state split over DP; activations
+ * split by TP and CP, times xi(r) = rc_act under recomputation. */
+void orc_mem_terms_eval(const orc_problem *p, const orc_config *c, int32_t layer, orc_mem_terms *o)
+{
+    double beta_opt = 6.0 + 12.0 / (double)c->dp;
+    o->w = ((double)p->params_dense[layer] / (double)c->tp +
+            (double)p->params_expert[layer] / (double)(c->ep * c->tpe)) * beta_opt;
+    o->a0 = (double)p->act_bytes[layer] / (double)(c->tp * c->cp);
+    o->q_w = q(o->w);
+    o->q_a0 = q(o->a0);
+    o->q_a1 = q(p->rc_act * (double)o->q_a0);
+}
+
+/* Per-configuration terms:
+ *  - X: routing metadata (8 bytes per token and choice) plus the dispatch
+ *    and combine buffers (2 D_moe), held once by a stage with an MoE layer;
+ *  - tbar: mean compute per stage, ceil(sum_l max_h (comp + expert) / PP),
+ *    the T_comp-bar of pruning 3 bounded independently of the partition;
+ *  - p_avg: parameters per device, averaged over stages. */
+void orc_pi_terms_eval(const orc_problem *p, const orc_config *c, orc_pi_terms *o)
+{
+    int64_t pd = 0, pe = 0;
+    for (int l = 0; l < p->n_layers; l++) {
+        pd += p->params_dense[l];
+        pe += p->params_expert[l];
+    }
+    o->p_avg = ((double)pd / (double)c->tp + (double)pe / (double)(c->ep * c->tpe)) / (double)c->pp;
+    double D = act_tensor(p, c);
+    double dm = (D * (double)p->top_k) * (1.0 - 1.0 / (double)c->ep);
+    o->x_f = ((8.0 * tokens(p, c)) * (double)p->top_k) + 2.0 * dm;
+    o->x_bytes = q(o->x_f);
+    int64_t s = 0;
+    for (int l = 0; l < p->n_layers; l++) {
+        int64_t m = 0;
+        for (int h = 0; h < p->n_types; h++) {
+            orc_type_terms t;
+            orc_type_terms_eval(p, c, l, h, &t);
+            m = max64(m, t.q_comp + t.q_expert);
+        }
+        s += m;
+    }
+    o->tbar = (s + c->pp - 1) / c->pp;
+    o->dp_const_f = 0.0;
+}
+
+/* T_comm(h, h', k, j) of the DP transition (Section 3.4): the activation sent
+ * forward and its gradient sent back between adjacent stages, one message of
+ * tokens * H * beta / TP bytes each way over the boundary link. */
+int64_t orc_p2p(const orc_problem *p, const orc_config *c, int32_t h_from, int32_t h_to)
+{
+    double al = p->alpha[h_from * ORC_MAX_TYPES + h_to], bw = p->bw[h_from * ORC_MAX_TYPES + h_to];
+    return q(2.0 * (al + (act_tensor(p, c) / (double)c->tp) / bw));
+}
+
+/* device type of device d under an ordering */
+static int dev_type(const orc_problem *p, const int *perm, int d)
+{
+    int start = 0;
+    for (int j = 0; j < p->n_types; j++) {
+        int h = perm[j];
+        if (d < start + p->count[h]) return h;
+        start += p->count[h];
+    }
+    return perm[p->n_types - 1];
+}
+
+/* Device layout of a (configuration, ordering): the devices are listed type by
+ * type in the ordering (m_h devices each) and stage i takes the i-th group of
+ * G/PP consecutive devices.  This fixes {h_i} per candidate (the state m of
+ * the DP of Section 3.4 is enumerated through the orderings instead). */
+int32_t orc_stages(const orc_problem *p, const orc_config *c, int32_t order, int32_t micro, orc_stage *st)
+{
+    int perm[ORC_MAX_TYPES];
+    orc_order(p, order, perm);
+    int G = 0;
+    for (int h = 0; h < p->n_types; h++) G += p->count[h];
+    int PP = c->pp, g = G / PP;
+    int64_t sum_speed = 0;
+    for (int s = 0; s < PP; s++) {
+        orc_stage *x = &st[s];
+        int lo = s * g, hi = lo + g;
+        x->mask = 0;
+        for (int d = lo; d < hi; d++) x->mask |= 1 << dev_type(p, perm, d);
+        x->first_type = dev_type(p, perm, lo);
+        x->last_type = dev_type(p, perm, hi - 1);
+        x->cap = -1;
+        x->speed = 0;
+        for (int h = 0; h < p->n_types; h++) {
+            if (!((x->mask >> h) & 1)) continue;
+            if (x->cap < 0 || p->mem_bytes[h] < x->cap) x->cap = p->mem_bytes[h];
+            if (x->speed == 0 || p->speed[h] < x->speed) x->speed = p->speed[h];
+        }
+        mask_link(p, x->mask, &x->alpha, &x->bw);
+        x->mixed = popc(x->mask) > 1;
+        if (s < PP - 1) {
+            int nt = dev_type(p, perm, hi);
+            x->bdiff = nt != x->last_type;
+            x->p2p = orc_p2p(p, c, x->last_type, nt);
+        } else {
+            x->bdiff = 0;
+            x->p2p = 0;
+        }
+        /* 1F1B: stage i (1-based) holds the activations of PP - i + 1 micro-batches */
+        x->m_store = min64(PP - s, micro);
+        sum_speed += x->speed;
+    }
+    /* Pruning 1 (Section 3.4): n_i within [(1-delta) w_i N, (1+delta) w_i N],
+     * w_i = the stage's share of the summed stage speeds; integer floor / ceil. */
+    int64_t dn = p->delta_num, dd = p->delta_den, N = p->n_layers;
+    for (int s = 0; s < PP; s++) {
+        if (!p->prune_window) {
+            st[s].lo = 1;
+            st[s].hi = (int32_t)N;
+            continue;
+        }
+        int64_t den = dd * sum_speed;
+        int64_t lo = ((dd - dn) * st[s].speed * N) / den;
+        int64_t hi = ((dd + dn) * st[s].speed * N + den - 1) / den;
+        st[s].lo = (int32_t)max64(1, lo);
+        st[s].hi = (int32_t)min64(N, hi);
+    }
+    return 0;
+}
+
+/* T_dp-sync + T_opt of Eq. 4: a ring all-reduce of fp32 gradients over DP at
+ * the slowest link of the candidate's stages plus an optimizer step
+ * proportional to the parameters each rank updates.  Partition-independent. */
+int64_t orc_dp_const(const orc_problem *p, const orc_config *c, int32_t order)
+{
+    orc_stage st[ORC_MAX_STAGES];
+    orc_stages(p, c, order, 1, st);
+    double al = 0.0, bw = 0.0;
+    for (int s = 0; s < c->pp; s++) {
+        if (s == 0 || st[s].alpha > al) al = st[s].alpha;
+        if (s == 0 || st[s].bw < bw) bw = st[s].bw;
+    }
+    orc_pi_terms t;
+    orc_pi_terms_eval(p, c, &t);
+    return q(ring_allreduce(4.0 * t.p_avg, c->dp, al, bw) + (p->opt_coef * t.p_avg) / (double)c->dp);
+}
+
+/* ------------------------------------------------------------------------
+ * Segment cost c_i(a, b) of putting layers [a, b) on stage i (Algorithm 1 inner
+ * body): pruning 1 window; the smallest recomputation choice that fits the
+ * stage's memory (pruning 2); pruning 3 on cross-type communication; then
+ * T_stage + T_comm.
+ * ---------------------------------------------------------------------- */
+int32_t orc_segment_costs(const orc_problem *p, int64_t idx, int64_t *cost, uint8_t *rflag)
+{
+    orc_config c;
+    int32_t order, micro;
+    if (orc_instance(p, idx, &c, &order, &micro)) return -1;
+    int N = p->n_layers, PP = c.pp, W = N + 1;
+    orc_stage st[ORC_MAX_STAGES];
+    orc_stages(p, &c, order, micro, st);
+    orc_pi_terms pt;
+    orc_pi_terms_eval(p, &c, &pt);
+
+    int64_t *Wp = calloc((size_t)W, 8), *A0 = calloc((size_t)W, 8), *A1 = calloc((size_t)W, 8);
+    int64_t *MO = calloc((size_t)W, 8), *T0 = calloc((size_t)W, 8), *T1 = calloc((size_t)W, 8);
+    int64_t *CM = calloc((size_t)W, 8);
+    for (int l = 0; l < N; l++) {
+        orc_mem_terms m;
+        orc_mem_terms_eval(p, &c, l, &m);
+        Wp[l + 1] = Wp[l] + m.q_w;
+        A0[l + 1] = A0[l] + m.q_a0;
+        A1[l + 1] = A1[l] + m.q_a1;
+        MO[l + 1] = MO[l] + (p->is_moe[l] ? 1 : 0);
+    }
+    for (int i = 0; i < PP; i++) {
+        for (int l = 0; l < N; l++) {
+            orc_mask_terms m;
+            orc_mask_terms_eval(p, &c, l, st[i].mask, &m);
+            T0[l + 1] = T0[l] + m.t_r0;
+            T1[l + 1] = T1[l] + m.t_r1;
+            CM[l + 1] = CM[l] + m.comm;
+        }
+        for (int a = 0; a < W; a++) {
+            for (int b = 0; b < W; b++) {
+                int64_t at = ((int64_t)i * W + a) * W + b;
+                cost[at] = ORC_INF;
+                rflag[at] = 0;
+                if (b <= a) continue;
+                int n = b - a;
+                if (n < st[i].lo || n > st[i].hi) continue;                        /* pruning 1 */
+                int64_t extra = (MO[b] - MO[a]) > 0 ? pt.x_bytes : 0;
+                int64_t m0 = (Wp[b] - Wp[a]) + st[i].m_store * (A0[b] - A0[a]) + extra;
+                int64_t m1 = (Wp[b] - Wp[a]) + st[i].m_store * (A1[b] - A1[a]) + extra;
+                int64_t t;
+                int r;
+                if (m0 <= st[i].cap) {
+                    t = T0[b] - T0[a];
+                    r = 0;
+                } else if (p->allow_recompute && m1 <= st[i].cap) {
+                    t = T1[b] - T1[a];
+                    r = 1;
+                } else {
+                    continue;                                                     /* pruning 2 */
+                }
+                if (p->prune_hetero) {
+                    int64_t hc = (st[i].mixed ? CM[b] - CM[a] : 0) + (st[i].bdiff ? st[i].p2p : 0);
+                    if (hc > (int64_t)p->eta_prune * pt.tbar) continue;            /* pruning 3 */
+                }
+                cost[at] = t + st[i].p2p;
+                rflag[at] = (uint8_t)r;
+            }
+        }
+    }
+    free(Wp); free(A0); free(A1); free(MO); free(T0); free(T1); free(CM);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------
+ * Stage DP (Section 3.4 transition; Algorithm 1).  F[i][b] = the least sum of
+ * stage costs placing layers [0, b) on stages 1..i, every stage cost <= t.
+ * Ties keep the smallest split point a.
+ * ---------------------------------------------------------------------- */
+static int64_t dp_pass(int pp, int n, const int64_t *cost, int64_t t, int64_t *F, int16_t *arg)
+{
+    int W = n + 1;
+    for (int b = 0; b < W; b++) F[b] = b == 0 ? 0 : ORC_INF;
+    for (int i = 1; i <= pp; i++) {
+        for (int b = 0; b < W; b++) {
+            int64_t best = ORC_INF;
+            int ba = -1;
+            for (int a = 0; a < b; a++) {
+                int64_t prev = F[(int64_t)(i - 1) * W + a];
+                int64_t c = cost[((int64_t)(i - 1) * W + a) * W + b];
+                if (prev == ORC_INF || c == ORC_INF || c > t) continue;
+                if (prev + c < best) {
+                    best = prev + c;
+                    ba = a;
+                }
+            }
+            F[(int64_t)i * W + b] = best;
+            arg[(int64_t)i * W + b] = (int16_t)ba;
+        }
+    }
+    return F[(int64_t)pp * W + n];
+}
+
+static int cmp_i64(const void *x, const void *y)
+{
+    int64_t a = *(const int64_t *)x, b = *(const int64_t *)y;
+    return (a > b) - (a < b);
+}
+
+/* Threshold form of the 1F1B objective: with every stage <= t,
+ *   score(t) = F_t + (B-1) t,  OPT = min_t score(t)
+ * over t in the set of distinct finite stage costs, ascending; t* is the
+ * smallest t reaching OPT and the partition is the back-trace of F at t*.
+ * The sweep stops once F_inf + (B-1) t >= best (no larger t can do better). */
+int32_t orc_dp(int32_t pp, int32_t n, int64_t micro, const int64_t *cost, orc_result *r)
+{
+    int W = n + 1;
+    int64_t ncost = (int64_t)pp * W * W;
+    memset(r, 0, sizeof(*r));
+    r->pp = pp;
+    int64_t *theta = malloc(sizeof(int64_t) * (size_t)(ncost + 1));
+    int64_t nt = 0;
+    for (int64_t i = 0; i < ncost; i++)
+        if (cost[i] != ORC_INF) theta[nt++] = cost[i];
+    qsort(theta, (size_t)nt, sizeof(int64_t), cmp_i64);
+    int64_t u = 0;
+    for (int64_t i = 0; i < nt; i++)
+        if (u == 0 || theta[i] != theta[u - 1]) theta[u++] = theta[i];
+    int64_t *F = malloc(sizeof(int64_t) * (size_t)(pp + 1) * W);
+    int16_t *arg = malloc(sizeof(int16_t) * (size_t)(pp + 1) * W);
+
+    int64_t finf = dp_pass(pp, n, cost, ORC_INF, F, arg);
+    int64_t best = ORC_INF, tstar = -1, swept = 0;
+    if (finf != ORC_INF) {
+        for (int64_t k = 0; k < u; k++) {
+            int64_t t = theta[k];
+            if (finf + (micro - 1) * t >= best) break;
+            int64_t f = dp_pass(pp, n, cost, t, F, arg);
+            swept++;
+            if (f == ORC_INF) continue;
+            int64_t score = f + (micro - 1) * t;
+            if (score < best) {
+                best = score;
+                tstar = t;
+            }
+        }
+    }
+    r->thresholds = swept;
+    if (tstar < 0) {
+        r->status = 1;
+        r->opt = r->sum = r->tmax = ORC_INF;
+    } else {
+        r->sum = dp_pass(pp, n, cost, tstar, F, arg);
+        r->tmax = tstar;
+        r->opt = best;
+        int b = n;
+        for (int i = pp; i >= 1; i--) {
+            int a = arg[(int64_t)i * W + b];
+            r->layers[i - 1] = (uint8_t)(b - a);
+            b = a;
+        }
+    }
+    free(theta);
+    free(F);
+    free(arg);
+    return 0;
+}
+
+/* Brute force over every composition of n layers into pp non-empty stages.
+ * Order: (sum + (B-1) max, max, b_{pp-1}, b_{pp-2}, ..., b_1) ascending, where
+ * b_i is the end layer of stage i -- the same canonical choice as orc_dp. */
+typedef struct brute_state {
+    int pp, n, W;
+    int64_t micro;
+    const int64_t *cost;
+    int b[ORC_MAX_STAGES + 1];
+    int best_b[ORC_MAX_STAGES + 1];
+    int64_t best_obj, best_max, best_sum;
+    int found;
+} brute_state;
+
+static int brute_better(const brute_state *s, int64_t obj, int64_t mx)
+{
+    if (!s->found) return 1;
+    if (obj != s->best_obj) return obj < s->best_obj;
+    if (mx != s->best_max) return mx < s->best_max;
+    for (int i = s->pp - 1; i >= 1; i--)
+        if (s->b[i] != s->best_b[i]) return s->b[i] < s->best_b[i];
+    return 0;
+}
+
+static void brute_rec(brute_state *s, int i)
+{
+    if (i == s->pp) {
+        int64_t sum = 0, mx = 0;
+        for (int k = 0; k < s->pp; k++) {
+            int64_t c = s->cost[((int64_t)k * s->W + s->b[k]) * s->W + s->b[k + 1]];
+            if (c == ORC_INF) return;
+            sum += c;
+            if (c > mx) mx = c;
+        }
+        int64_t obj = sum + (s->micro - 1) * mx;
+        if (brute_better(s, obj, mx)) {
+            s->found = 1;
+            s->best_obj = obj;
+            s->best_max = mx;
+            s->best_sum = sum;
+            memcpy(s->best_b, s->b, sizeof(s->b));
+        }
+        return;
+    }
+    if (i == s->pp - 1) {
+        s->b[i + 1] = s->n;
+        if (s->b[i] < s->n) brute_rec(s, i + 1);
+        return;
+    }
+    for (int e = s->b[i] + 1; e <= s->n - (s->pp - 1 - i); e++) {
+        s->b[i + 1] = e;
+        brute_rec(s, i + 1);
+    }
+}
+
+int32_t orc_brute(int32_t pp, int32_t n, int64_t micro, const int64_t *cost, orc_result *r)
+{
+    memset(r, 0, sizeof(*r));
+    r->pp = pp;
+    brute_state s;
+    memset(&s, 0, sizeof(s));
+    s.pp = pp;
+    s.n = n;
+    s.W = n + 1;
+    s.micro = micro;
+    s.cost = cost;
+    s.b[0] = 0;
+    if (pp <= n) brute_rec(&s, 0);
+    if (!s.found) {
+        r->status = 1;
+        r->opt = r->sum = r->tmax = ORC_INF;
+        return 0;
+    }
+    r->opt = s.best_obj;
+    r->sum = s.best_sum;
+    r->tmax = s.best_max;
+    for (int i = 0; i < pp; i++) r->layers[i] = (uint8_t)(s.best_b[i + 1] - s.best_b[i]);
+    return 0;
+}
+
+static int32_t solve_with(const orc_problem *p, int64_t idx, orc_result *r, int brute)
+{
+    orc_config c;
+    int32_t order, micro;
+    if (orc_instance(p, idx, &c, &order, &micro)) return -1;
+    int W = p->n_layers + 1;
+    int64_t *cost = malloc(sizeof(int64_t) * (size_t)c.pp * W * W);
+    uint8_t *rf = malloc((size_t)c.pp * W * W);
+    orc_segment_costs(p, idx, cost, rf);
+    if (brute)
+        orc_brute(c.pp, p->n_layers, micro, cost, r);
+    else
+        orc_dp(c.pp, p->n_layers, micro, cost, r);
+    orc_stage st[ORC_MAX_STAGES];
+    orc_stages(p, &c, order, micro, st);
+    for (int i = 0; i < c.pp; i++) r->stage_mask[i] = (uint8_t)st[i].mask;
+    r->dp_const = orc_dp_const(p, &c, order);
+    if (r->status == 0) {
+        r->opt += r->dp_const;
+        int a = 0;
+        for (int i = 0; i < c.pp; i++) {
+            int b = a + r->layers[i];
+            r->recompute[i] = rf[((int64_t)i * W + a) * W + b];
+            a = b;
+        }
+    }
+    free(cost);
+    free(rf);
+    return 0;
+}
+
+int32_t orc_solve(const orc_problem *p, int64_t idx, orc_result *r) { return solve_with(p, idx, r, 0); }
+int32_t orc_solve_brute(const orc_problem *p, int64_t idx, orc_result *r) { return solve_with(p, idx, r, 1); }
+
+int32_t orc_solve_many(const orc_problem *p, const int64_t *idx, int64_t n, orc_result *r)
+{
+    for (int64_t i = 0; i < n; i++)
+        if (orc_solve(p, idx[i], &r[i])) return -1;
+    return 0;
+}

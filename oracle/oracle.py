@@ -1,0 +1,309 @@
+"""ctypes front-end of the CPU oracle -- TEST INFRASTRUCTURE ONLY.
+
+Only the test-suite, ``__graft_entry__.smoke()`` and the bench's CPU-baseline
+leg import this module.  It marshals a problem dictionary (see the package's
+``workloads`` module for the fields) into the oracle's own flat C struct and
+calls the plain C implementation in ``hapmoe_oracle.c``.  It imports nothing
+from the HIP library's package.
+"""
+from __future__ import annotations
+
+import ctypes as C
+
+import numpy as np
+
+from . import build as _build
+
+MAX_TYPES = 4
+MAX_STAGES = 64
+MAX_MICRO = 64
+INF = np.iinfo(np.int64).max
+
+
+class OrcProblem(C.Structure):
+    _fields_ = [
+        ("n_layers", C.c_int32), ("seq_len", C.c_int32), ("hidden", C.c_int32),
+        ("n_experts", C.c_int32), ("top_k", C.c_int32), ("micro_batch_size", C.c_int32),
+        ("elem_bytes", C.c_int32),
+        ("moe_ffn_mult", C.c_double),
+        ("is_moe", C.c_void_p), ("expert_tokens", C.c_void_p), ("params_dense", C.c_void_p),
+        ("params_expert", C.c_void_p), ("act_bytes", C.c_void_p),
+        ("n_types", C.c_int32),
+        ("count", C.c_int32 * MAX_TYPES), ("speed", C.c_int32 * MAX_TYPES),
+        ("mem_bytes", C.c_int64 * MAX_TYPES),
+        ("eff", C.c_double * MAX_TYPES), ("route_coef", C.c_double * MAX_TYPES),
+        ("bw", C.c_double * (MAX_TYPES * MAX_TYPES)), ("alpha", C.c_double * (MAX_TYPES * MAX_TYPES)),
+        ("t_dense", C.c_void_p), ("t_ffn", C.c_void_p),
+        ("gamma", C.c_double), ("rc_time", C.c_double), ("rc_act", C.c_double), ("opt_coef", C.c_double),
+        ("delta_num", C.c_int32), ("delta_den", C.c_int32), ("eta_prune", C.c_int32),
+        ("prune_window", C.c_int32), ("prune_hetero", C.c_int32), ("allow_recompute", C.c_int32),
+        ("pp_max", C.c_int32), ("tp_mask", C.c_int32), ("cp_mask", C.c_int32), ("ep_max", C.c_int32),
+        ("tpe_mask", C.c_int32), ("mode", C.c_int32),
+        ("n_micro", C.c_int32), ("micro", C.c_int32 * MAX_MICRO),
+    ]
+
+
+class OrcConfig(C.Structure):
+    _fields_ = [(n, C.c_int32) for n in ("pp", "tp", "cp", "dp", "ep", "tpe")]
+
+
+class OrcStage(C.Structure):
+    _fields_ = [("mask", C.c_int32), ("speed", C.c_int32), ("lo", C.c_int32), ("hi", C.c_int32),
+                ("mixed", C.c_int32), ("bdiff", C.c_int32), ("first_type", C.c_int32),
+                ("last_type", C.c_int32), ("cap", C.c_int64), ("p2p", C.c_int64),
+                ("m_store", C.c_int64), ("alpha", C.c_double), ("bw", C.c_double)]
+
+
+class OrcTypeTerms(C.Structure):
+    _fields_ = [("comp", C.c_double), ("expert", C.c_double), ("q_comp", C.c_int64),
+                ("q_expert", C.c_int64)]
+
+
+class OrcMaskTerms(C.Structure):
+    _fields_ = [("a2a", C.c_double), ("tp", C.c_double), ("cp", C.c_double), ("q_a2a", C.c_int64),
+                ("q_tp", C.c_int64), ("q_cp", C.c_int64), ("comm", C.c_int64), ("t_r0", C.c_int64),
+                ("t_r1", C.c_int64)]
+
+
+class OrcMemTerms(C.Structure):
+    _fields_ = [("w", C.c_double), ("a0", C.c_double), ("q_w", C.c_int64), ("q_a0", C.c_int64),
+                ("q_a1", C.c_int64)]
+
+
+class OrcPiTerms(C.Structure):
+    _fields_ = [("p_avg", C.c_double), ("dp_const_f", C.c_double), ("x_f", C.c_double),
+                ("x_bytes", C.c_int64), ("tbar", C.c_int64)]
+
+
+class OrcResult(C.Structure):
+    _fields_ = [("status", C.c_int32), ("pp", C.c_int32), ("opt", C.c_int64), ("sum", C.c_int64),
+                ("tmax", C.c_int64), ("dp_const", C.c_int64), ("thresholds", C.c_int64),
+                ("layers", C.c_uint8 * MAX_STAGES), ("recompute", C.c_uint8 * MAX_STAGES),
+                ("stage_mask", C.c_uint8 * MAX_STAGES)]
+
+
+_LIB = None
+
+
+def lib():
+    """Load liboracle.so, compiling it first if it is not there."""
+    global _LIB
+    if _LIB is None:
+        path = _build.build(force=False)
+        L = C.CDLL(path)
+        P = C.POINTER
+        L.orc_validate.argtypes = [P(OrcProblem)]
+        L.orc_enumerate.argtypes = [P(OrcProblem), P(OrcConfig), C.c_int64]
+        L.orc_enumerate.restype = C.c_int64
+        L.orc_n_orders.argtypes = [P(OrcProblem)]
+        L.orc_order.argtypes = [P(OrcProblem), C.c_int32, P(C.c_int32)]
+        L.orc_order.restype = None
+        L.orc_n_instances.argtypes = [P(OrcProblem)]
+        L.orc_n_instances.restype = C.c_int64
+        for name, T in (("orc_mask_terms_eval", OrcMaskTerms),):
+            getattr(L, name).argtypes = [P(OrcProblem), P(OrcConfig), C.c_int32, C.c_int32, P(T)]
+            getattr(L, name).restype = None
+        L.orc_type_terms_eval.argtypes = [P(OrcProblem), P(OrcConfig), C.c_int32, C.c_int32,
+                                          P(OrcTypeTerms)]
+        L.orc_type_terms_eval.restype = None
+        L.orc_mem_terms_eval.argtypes = [P(OrcProblem), P(OrcConfig), C.c_int32, P(OrcMemTerms)]
+        L.orc_mem_terms_eval.restype = None
+        L.orc_pi_terms_eval.argtypes = [P(OrcProblem), P(OrcConfig), P(OrcPiTerms)]
+        L.orc_pi_terms_eval.restype = None
+        L.orc_p2p.argtypes = [P(OrcProblem), P(OrcConfig), C.c_int32, C.c_int32]
+        L.orc_p2p.restype = C.c_int64
+        L.orc_dp_const.argtypes = [P(OrcProblem), P(OrcConfig), C.c_int32]
+        L.orc_dp_const.restype = C.c_int64
+        L.orc_stages.argtypes = [P(OrcProblem), P(OrcConfig), C.c_int32, C.c_int32, P(OrcStage)]
+        L.orc_segment_costs.argtypes = [P(OrcProblem), C.c_int64, C.c_void_p, C.c_void_p]
+        L.orc_dp.argtypes = [C.c_int32, C.c_int32, C.c_int64, C.c_void_p, P(OrcResult)]
+        L.orc_brute.argtypes = [C.c_int32, C.c_int32, C.c_int64, C.c_void_p, P(OrcResult)]
+        L.orc_solve.argtypes = [P(OrcProblem), C.c_int64, P(OrcResult)]
+        L.orc_solve_brute.argtypes = [P(OrcProblem), C.c_int64, P(OrcResult)]
+        L.orc_solve_many.argtypes = [P(OrcProblem), C.c_void_p, C.c_int64, P(OrcResult)]
+        _LIB = L
+    return _LIB
+
+
+def _ptr(a):
+    return a.ctypes.data_as(C.c_void_p)
+
+
+def result_dict(r: OrcResult) -> dict:
+    pp = r.pp
+    return {"status": r.status, "pp": pp, "opt": r.opt, "sum": r.sum, "tmax": r.tmax,
+            "dp_const": r.dp_const, "thresholds": r.thresholds,
+            "layers": list(r.layers[:pp]), "recompute": list(r.recompute[:pp]),
+            "stage_mask": list(r.stage_mask[:pp])}
+
+
+class Oracle:
+    """Oracle bound to one problem dictionary."""
+
+    def __init__(self, problem: dict):
+        m, c, pa, sp = problem["model"], problem["cluster"], problem["params"], problem["space"]
+        T = int(c["n_types"])
+        self._keep = {
+            "is_moe": np.ascontiguousarray(m["is_moe"], dtype=np.uint8),
+            "expert_tokens": np.ascontiguousarray(m["expert_tokens"], dtype=np.int64),
+            "params_dense": np.ascontiguousarray(m["params_dense"], dtype=np.int64),
+            "params_expert": np.ascontiguousarray(m["params_expert"], dtype=np.int64),
+            "act_bytes": np.ascontiguousarray(m["act_bytes"], dtype=np.int64),
+            "t_dense": np.ascontiguousarray(c["t_dense"], dtype=np.int64),
+            "t_ffn": np.ascontiguousarray(c["t_ffn"], dtype=np.int64),
+        }
+        P = OrcProblem()
+        P.n_layers, P.seq_len, P.hidden = m["n_layers"], m["seq_len"], m["hidden"]
+        P.n_experts, P.top_k, P.micro_batch_size = m["n_experts"], m["top_k"], m["micro_batch_size"]
+        P.elem_bytes = m["elem_bytes"]
+        P.moe_ffn_mult = float(m["moe_ffn_mult"])
+        for name in ("is_moe", "expert_tokens", "params_dense", "params_expert", "act_bytes",
+                     "t_dense", "t_ffn"):
+            setattr(P, name, _ptr(self._keep[name]))
+        P.n_types = T
+        for h in range(T):
+            P.count[h] = int(c["count"][h])
+            P.speed[h] = int(c["speed"][h])
+            P.mem_bytes[h] = int(c["mem_bytes"][h])
+            P.eff[h] = float(c["eff"][h])
+            P.route_coef[h] = float(c["route_coef"][h])
+            for g in range(T):
+                P.bw[h * MAX_TYPES + g] = float(c["bw"][h][g])
+                P.alpha[h * MAX_TYPES + g] = float(c["alpha"][h][g])
+        for name in ("gamma", "rc_time", "rc_act", "opt_coef"):
+            setattr(P, name, float(pa[name]))
+        for name in ("delta_num", "delta_den", "eta_prune", "prune_window", "prune_hetero",
+                     "allow_recompute"):
+            setattr(P, name, int(pa[name]))
+        for name in ("pp_max", "tp_mask", "cp_mask", "ep_max", "tpe_mask", "mode"):
+            setattr(P, name, int(sp[name]))
+        micro = list(sp["micro"])
+        P.n_micro = len(micro)
+        for i, b in enumerate(micro):
+            P.micro[i] = int(b)
+        self.P = P
+        self.problem = problem
+        self.L = lib()
+        if self.L.orc_validate(C.byref(P)) != 0:
+            raise ValueError("oracle: invalid problem")
+
+    # ---- enumeration -------------------------------------------------------
+    def configs(self):
+        n = self.L.orc_enumerate(C.byref(self.P), None, 0)
+        arr = (OrcConfig * max(n, 1))()
+        self.L.orc_enumerate(C.byref(self.P), arr, n)
+        return [(x.pp, x.tp, x.cp, x.dp, x.ep, x.tpe) for x in arr[:n]]
+
+    def n_orders(self):
+        return self.L.orc_n_orders(C.byref(self.P))
+
+    def order(self, o):
+        perm = (C.c_int32 * MAX_TYPES)()
+        self.L.orc_order(C.byref(self.P), o, perm)
+        return list(perm[: self.P.n_types])
+
+    def n_instances(self):
+        return self.L.orc_n_instances(C.byref(self.P))
+
+    # ---- cost model --------------------------------------------------------
+    @staticmethod
+    def _cfg(cfg):
+        return OrcConfig(*[int(v) for v in cfg])
+
+    def type_terms(self, cfg, layer, h):
+        o = OrcTypeTerms()
+        self.L.orc_type_terms_eval(C.byref(self.P), C.byref(self._cfg(cfg)), layer, h, C.byref(o))
+        return {k: getattr(o, k) for k, _ in o._fields_}
+
+    def mask_terms(self, cfg, layer, mask):
+        o = OrcMaskTerms()
+        self.L.orc_mask_terms_eval(C.byref(self.P), C.byref(self._cfg(cfg)), layer, mask, C.byref(o))
+        return {k: getattr(o, k) for k, _ in o._fields_}
+
+    def mem_terms(self, cfg, layer):
+        o = OrcMemTerms()
+        self.L.orc_mem_terms_eval(C.byref(self.P), C.byref(self._cfg(cfg)), layer, C.byref(o))
+        return {k: getattr(o, k) for k, _ in o._fields_}
+
+    def pi_terms(self, cfg):
+        o = OrcPiTerms()
+        self.L.orc_pi_terms_eval(C.byref(self.P), C.byref(self._cfg(cfg)), C.byref(o))
+        return {k: getattr(o, k) for k, _ in o._fields_}
+
+    def p2p(self, cfg, h_from, h_to):
+        return self.L.orc_p2p(C.byref(self.P), C.byref(self._cfg(cfg)), h_from, h_to)
+
+    def dp_const(self, cfg, order):
+        return self.L.orc_dp_const(C.byref(self.P), C.byref(self._cfg(cfg)), order)
+
+    def stages(self, cfg, order, micro):
+        st = (OrcStage * MAX_STAGES)()
+        self.L.orc_stages(C.byref(self.P), C.byref(self._cfg(cfg)), order, micro, st)
+        return [{k: getattr(s, k) for k, _ in s._fields_} for s in st[: int(cfg[0])]]
+
+    def segment_costs(self, idx):
+        cfgs = self.configs()
+        per = self.n_orders() * self.P.n_micro
+        pp = cfgs[idx // per][0]
+        W = self.P.n_layers + 1
+        cost = np.zeros((pp, W, W), dtype=np.int64)
+        rflag = np.zeros((pp, W, W), dtype=np.uint8)
+        if self.L.orc_segment_costs(C.byref(self.P), idx, _ptr(cost), _ptr(rflag)) != 0:
+            raise IndexError(idx)
+        return cost, rflag
+
+    # ---- search ------------------------------------------------------------
+    def solve(self, idx):
+        r = OrcResult()
+        if self.L.orc_solve(C.byref(self.P), int(idx), C.byref(r)) != 0:
+            raise IndexError(idx)
+        return result_dict(r)
+
+    def solve_brute(self, idx):
+        r = OrcResult()
+        if self.L.orc_solve_brute(C.byref(self.P), int(idx), C.byref(r)) != 0:
+            raise IndexError(idx)
+        return result_dict(r)
+
+    def solve_many(self, idx):
+        idx = np.ascontiguousarray(idx, dtype=np.int64)
+        res = (OrcResult * max(len(idx), 1))()
+        if self.L.orc_solve_many(C.byref(self.P), _ptr(idx), len(idx), res) != 0:
+            raise IndexError("instance out of range")
+        return [result_dict(r) for r in res[: len(idx)]]
+
+    def best(self):
+        """Global arg-min over all instances of (objective, instance index)."""
+        best = None
+        for i in range(self.n_instances()):
+            r = self.solve(i)
+            if r["status"] == 0 and (best is None or r["opt"] < best[1]["opt"]):
+                best = (i, r)
+        return best
+
+
+def dp(pp, n, micro, cost):
+    """Threshold DP on an explicit cost tensor [pp][n+1][n+1] (INF = infeasible)."""
+    cost = np.ascontiguousarray(cost, dtype=np.int64)
+    assert cost.shape == (pp, n + 1, n + 1)
+    r = OrcResult()
+    lib().orc_dp(pp, n, micro, _ptr(cost), C.byref(r))
+    return result_dict(r)
+
+
+def brute(pp, n, micro, cost):
+    """Brute force over all compositions on an explicit cost tensor."""
+    cost = np.ascontiguousarray(cost, dtype=np.int64)
+    assert cost.shape == (pp, n + 1, n + 1)
+    r = OrcResult()
+    lib().orc_brute(pp, n, micro, _ptr(cost), C.byref(r))
+    return result_dict(r)
+
+
+def solve_worker(args):
+    """multiprocessing helper: (problem, instance indices) -> results."""
+    problem, idx = args
+    return Oracle(problem).solve_many(idx)
+
+
+__all__ = ["Oracle", "dp", "brute", "INF", "lib", "solve_worker"]
