@@ -1,0 +1,145 @@
+#!/usr/bin/env python3
+"""Planner hot-path benchmark on one MI355X.
+
+One step = the whole hot path over the candidate set of the workload:
+cost-table kernel -> stage-DP kernel -> segmented arg-min (best plan), with
+the problem image and candidate array already resident in HBM.  The metric is
+candidates evaluated per second.  Each kernel is timed with HIP events on the
+stream it runs on; the stage-DP kernel (the dominant one) is reported against
+the VALU issue roofline of the chip.  The CPU oracle is timed on a bounded
+stride sample of the same workload (single core) as a reported baseline.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 4]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "candidate plans evaluated/sec (cost model + stage DP), % HBM/VALU roofline"
+
+# MI355X: 256 CUs x 4 SIMD x 16 lanes at 2.4 GHz -> 32-bit VALU lane operations per second
+VALU_PEAK_OPS = 256 * 64 * 2.4e9
+# one DP relaxation = 3 int64 operations (stage cost <= threshold, F + c, compare with the
+# running minimum) = 6 32-bit lane operations
+OPS_PER_RELAXATION = 6
+
+WORKLOADS = {
+    1: "tiny: 8-layer MoE (H1024, E8 top-2, S2048), 4+4 devices of 2 types, B=8",
+    2: "32-layer MoE (H4096, E64 top-8, S4096), 64 devices 32/16/16 of 3 types, B in {8,16,32}",
+    3: "61-layer MoE (3 dense, H7168, E256 top-8, 1 shared, S4096), 4x64 devices of 4 types, B in {16,32,64}",
+    4: "96-layer MoE (H8192, E128 top-4, S8192, CP<=8), 4x256 devices of 4 types, 24 orderings, B=1..64",
+    5: "adversarial: 61-layer shape, +-1% near-tied layer costs, tight memory, Zipf s=2",
+}
+
+
+def cpu_baseline(problem, n_total, n_sample):
+    """The oracle as it stands, single thread, on a fixed stride sample."""
+    from oracle.oracle import Oracle
+    o = Oracle(problem)
+    stride = max(1, n_total // n_sample)
+    idx = list(range(stride // 2, n_total, stride))[:n_sample]
+    t0 = time.perf_counter()
+    o.solve_many(idx)
+    dt = time.perf_counter() - t0
+    return {"value": len(idx) / dt, "unit": "candidates/s", "cores": 1, "kind": "oracle",
+            "sample": f"{len(idx)} candidates at stride {stride} of {n_total} (every {stride}th), "
+                      f"{dt:.1f} s on one host core"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", type=int, default=4)
+    ap.add_argument("--cpu-sample", type=int, default=200)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the planner's candidates are independent and this build "
+              "has no multi-GPU path (see DESIGN.md for how it would shard). Run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2609_39350_amd import binding, workloads
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    problem = workloads.config(args.config)
+    pl = binding.Planner(problem, dev)
+    n = pl.n
+    stream = torch.cuda.current_stream()
+
+    # untimed: relaxation / pass counts of one stage-DP launch (deterministic per launch)
+    pl.eval_cost_tables()
+    pl.stage_dp(stats=True)
+    st = pl.stats()
+    relax = int(st[:, 1].astype(np.int64).sum())
+    passes = st[:, 0]
+    feasible = int((pl.results()["status"] == 0).sum())
+
+    for _ in range(args.warmup):
+        pl.run()
+    torch.cuda.synchronize()
+
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    plan = None
+    for k in range(args.steps):
+        e = ev[k]
+        e[0].record(stream)
+        pl.eval_cost_tables()
+        e[1].record(stream)
+        pl.stage_dp()
+        e[2].record(stream)
+        plan = pl.best_plan()        # waits for the stream
+        e[3].record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    elapsed = t1 - t0
+    ms = {name: float(np.mean([ev[k][j].elapsed_time(ev[k][j + 1]) for k in range(args.steps)]))
+          for j, name in enumerate(("cost_tables", "stage_dp", "best_plan"))}
+
+    dp_s = ms["stage_dp"] / 1e3
+    achieved = relax * OPS_PER_RELAXATION / dp_s
+    out = {
+        "metric": METRIC,
+        "value": n * args.steps / elapsed,
+        "unit": "candidates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed * 1e3 / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic",
+        "config": {"workload": f"config {args.config}: {WORKLOADS[args.config]}", "candidates": n,
+                   "configs_6d": pl.n_configs, "feasible_candidates": feasible},
+        "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK_OPS / 1e12,
+                     "unit": "TOP/s", "frac": achieved / VALU_PEAK_OPS, "traffic": None,
+                     "kernel": "stage_dp", "ops_per_relaxation": OPS_PER_RELAXATION,
+                     "relaxations_per_launch": relax},
+        "kernels_ms": ms,
+        "dp_cell_updates_per_s": relax / dp_s,
+        "threshold_passes_per_candidate": {"mean": float(passes.mean()), "max": int(passes.max())},
+        "best_plan": {"instance": plan["instance"], "objective_ns": plan["objective"],
+                      "config": plan["config"], "order": plan["order"], "B": plan["n_micro"],
+                      "layers": plan["layers"], "recompute": plan["recompute"]},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(problem, n, args.cpu_sample)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

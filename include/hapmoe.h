@@ -1,0 +1,249 @@
+/*
+ * hapmoe.h -- C ABI of the MI355X (gfx950) planner hot path of HAPMoE
+ * ("Heterogeneity-Aware Automatic Parallelism Planning for Mixture-of-Experts
+ * Models Training").
+ *
+ * The library evaluates the paper's MoE-aware cost model (Section 3.2) over the
+ * 6D candidate space (DP, PP, TP, CP, EP, TPE) on a heterogeneous cluster and
+ * runs, for every candidate, the pruning-enhanced stage DP of Section 3.4
+ * (Algorithm 1) that picks a non-uniform layer-to-stage partition and a
+ * per-stage recomputation choice.  Pipeline of calls:
+ *
+ *   hapmoe_enumerate_candidates   host   the candidate set (pi, device ordering, B)
+ *   hapmoe_pack_image             host   flatten the problem for the device
+ *   hapmoe_eval_cost_tables       GPU    cost-table kernel
+ *   hapmoe_stage_dp               GPU    stage-DP kernel, one result per candidate
+ *   hapmoe_best_plan              GPU    segmented arg-min -> the best plan (syncs)
+ *
+ * Conventions
+ *  - Every call returns an int32_t status: HAPMOE_OK (0) or a negative
+ *    HAPMOE_E_* code; hapmoe_strerror() names it.  Nothing throws.
+ *  - The caller owns all memory.  Pointers named h_* / host structs are host
+ *    memory; d_* are device memory of the current HIP device.  The library
+ *    never allocates device memory; buffer sizes come from the *_bytes queries.
+ *  - `stream` is a hipStream_t passed as void* (0 = the null stream).  GPU calls
+ *    enqueue work and return; only hapmoe_best_plan waits for its stream.
+ *  - Times are int64 nanoseconds, memory sizes int64 bytes, bandwidths bytes/ns
+ *    (= GB/s), latencies ns.  Costs are rounded up to whole ns / bytes once per
+ *    modelled term.
+ *  - The device calls need a gfx950 device (HAPMOE_E_ARCH otherwise).
+ */
+#ifndef HAPMOE_H
+#define HAPMOE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HAPMOE_MAX_TYPES 4     /* device types |H| */
+#define HAPMOE_MAX_STAGES 32   /* pipeline stages PP */
+#define HAPMOE_MAX_LAYERS 127  /* transformer layers N */
+#define HAPMOE_MAX_MICRO 64    /* entries of the microbatch-count list */
+
+enum {
+    HAPMOE_OK = 0,
+    HAPMOE_E_INVAL = -1,      /* malformed problem or argument */
+    HAPMOE_E_CAPACITY = -2,   /* output array too small; the required count is returned */
+    HAPMOE_E_WORKSPACE = -3,  /* device buffer smaller than the *_bytes query says */
+    HAPMOE_E_HIP = -4,        /* a HIP runtime call failed */
+    HAPMOE_E_ARCH = -5,       /* current device is not gfx950 */
+    HAPMOE_E_INFEASIBLE = -6, /* no candidate has a memory-feasible partition */
+    HAPMOE_E_RANGE = -7       /* candidate sub-range outside [0, n) */
+};
+
+/* Per-candidate status in hapmoe_dp_result.status */
+enum {
+    HAPMOE_STATUS_OK = 0,
+    HAPMOE_STATUS_INFEASIBLE = 1, /* no partition passes the three prunings */
+    HAPMOE_STATUS_OVERFLOW = 2    /* a modelled term left the int64 range the DP allows */
+};
+
+/* Model and training hyper-parameters (Section 3.1 "Input": N, S, H, E, k,
+ * batch sizes, optimizer).  Arrays are host memory, N = n_layers entries. */
+typedef struct hapmoe_model {
+    int32_t n_layers;          /* N, 1..HAPMOE_MAX_LAYERS */
+    int32_t seq_len;           /* S */
+    int32_t hidden;            /* H */
+    int32_t n_experts;         /* E (0 = dense model) */
+    int32_t top_k;             /* k */
+    int32_t micro_batch_size;  /* tokens per microbatch = seq_len * micro_batch_size */
+    int32_t elem_bytes;        /* beta of Eq. 3 */
+    double moe_ffn_mult;       /* the factor 2 of Eq. 2: expert work relative to t_ffn */
+    const uint8_t *is_moe;          /* [N] 1 = MoE layer */
+    const int64_t *expert_tokens;   /* [N][E] router statistics |T_e| (Section 3.2) */
+    const int64_t *params_dense;    /* [N] non-expert parameters */
+    const int64_t *params_expert;   /* [N] parameters of all experts of the layer */
+    const int64_t *act_bytes;       /* [N] activation bytes of one microbatch at TP = CP = 1 */
+} hapmoe_model;
+
+/* Device types (Section 3.1: type h has (P_h, C_h, B_h) and m_h devices) and
+ * the profiled tables of Section 3.3. */
+typedef struct hapmoe_cluster {
+    int32_t n_types;                          /* |H|, 1..4 */
+    int32_t count[HAPMOE_MAX_TYPES];          /* m_h */
+    int32_t speed[HAPMOE_MAX_TYPES];          /* P_h, relative compute speed (integer) */
+    int64_t mem_bytes[HAPMOE_MAX_TYPES];      /* C_h */
+    double eff[HAPMOE_MAX_TYPES];             /* eta_h of Eq. 2, in (0, 1] */
+    double route_coef[HAPMOE_MAX_TYPES];      /* router ns per (token x hidden) */
+    double bw[HAPMOE_MAX_TYPES][HAPMOE_MAX_TYPES];     /* link bandwidth h -> h', bytes/ns */
+    double alpha[HAPMOE_MAX_TYPES][HAPMOE_MAX_TYPES];  /* link latency h -> h', ns */
+    const int64_t *t_dense;  /* [T][4][4][N] dense layer time at TP = 2^i, CP = 2^j, ns */
+    const int64_t *t_ffn;    /* [T][4][4][N] its FFN part (0 <= t_ffn <= t_dense) */
+} hapmoe_cluster;
+
+/* Method parameters (Sections 3.2 and 3.4). */
+typedef struct hapmoe_params {
+    double gamma;            /* load-imbalance weight, [0, 1] */
+    double rc_time;          /* recomputation time factor (>= 1) */
+    double rc_act;           /* xi(r = 1): activation factor under recomputation, [0, 1] */
+    double opt_coef;         /* optimizer step, ns per parameter */
+    int32_t delta_num;       /* pruning-1 tolerance delta = delta_num / delta_den */
+    int32_t delta_den;
+    int32_t eta_prune;       /* pruning-3 factor eta */
+    int32_t prune_window;    /* pruning 1 on/off */
+    int32_t prune_hetero;    /* pruning 3 on/off */
+    int32_t allow_recompute; /* r in {0, 1} (1) or r = 0 only (0) */
+} hapmoe_params;
+
+/* Candidate space (Section 3.4: configuration set Pi; Algorithm 1 input). */
+typedef struct hapmoe_space {
+    int32_t pp_max;      /* PP <= pp_max <= HAPMOE_MAX_STAGES */
+    int32_t tp_mask;     /* bit i: TP = 2^i allowed (i < 4) */
+    int32_t cp_mask;     /* bit i: CP = 2^i allowed */
+    int32_t ep_max;      /* EP = powers of two dividing E, <= ep_max */
+    int32_t tpe_mask;    /* bit i: TPE = 2^i allowed */
+    int32_t mode;        /* 0: EP*TPE folds inside the stage group (DP = group/(TP*CP));
+                            1: literal product PP*DP*TP*CP*EP*TPE = sum_h m_h */
+    int32_t n_micro;     /* entries of micro[] */
+    int32_t micro[HAPMOE_MAX_MICRO]; /* microbatch counts B, 1..1024 */
+} hapmoe_space;
+
+typedef struct hapmoe_problem {
+    hapmoe_model model;
+    hapmoe_cluster cluster;
+    hapmoe_params params;
+    hapmoe_space space;
+} hapmoe_problem;
+
+/* One candidate: the 6D configuration pi (Section 3.1 output), the device-type
+ * ordering that places the stages on devices, and the microbatch count B. */
+typedef struct hapmoe_candidate {
+    int32_t pp, tp, cp, dp, ep, tpe;
+    int32_t order;      /* rank of the type permutation in lexicographic order */
+    int32_t n_micro;    /* B */
+} hapmoe_candidate;     /* 32 bytes */
+
+/* Stage-DP result of one candidate (64 bytes). */
+typedef struct hapmoe_dp_result {
+    int64_t objective;        /* sum_i c_i + (B-1) max_i c_i + C(pi), INT64_MAX if not OK */
+    int64_t stage_sum;        /* sum_i c_i */
+    int64_t t_max;            /* max_i c_i (the threshold t*) */
+    int32_t status;           /* HAPMOE_STATUS_* */
+    uint32_t recompute_mask;  /* bit i = r_i */
+    uint8_t layers[HAPMOE_MAX_STAGES]; /* n_i */
+} hapmoe_dp_result;
+
+/* The best plan (Section 3.1 output (pi*, L*, {h_i*}, {r_i*})). */
+typedef struct hapmoe_plan {
+    int64_t instance;         /* index of the winning candidate */
+    int64_t objective, stage_sum, t_max, dp_const;
+    hapmoe_candidate cand;
+    int32_t n_stages;
+    uint32_t recompute_mask;
+    uint8_t layers[HAPMOE_MAX_STAGES];      /* n_i */
+    uint8_t stage_types[HAPMOE_MAX_STAGES]; /* bit h set = stage uses device type h */
+} hapmoe_plan;
+
+/* Name of a status code (static string). */
+const char *hapmoe_strerror(int32_t code);
+
+/* Check a problem against the limits above.  HAPMOE_OK or HAPMOE_E_INVAL. */
+int32_t hapmoe_validate(const hapmoe_problem *p);
+
+/* Candidate set (Section 3.1 output pi; Section 3.4 / Algorithm 1 loop over
+ * Pi, device types and the microbatch list).  Order: PP, TP, CP, EP, TPE
+ * ascending, then the type ordering, then micro[] in the given order; the index
+ * of a candidate is ((config * n_orders) + order) * n_micro + micro_index.
+ * Host only.  Writes min(capacity, total) candidates to `out` (may be NULL) and
+ * the total to *n_total; returns HAPMOE_E_CAPACITY if out is NULL or too small. */
+int32_t hapmoe_enumerate_candidates(const hapmoe_problem *p, hapmoe_candidate *out,
+                                    int64_t capacity, int64_t *n_total);
+
+/* Problem image: a flat copy of the problem that the kernels read.  The caller
+ * copies the packed host image to device memory once and passes that device
+ * pointer to the GPU calls together with the same host problem. */
+int32_t hapmoe_image_bytes(const hapmoe_problem *p, int64_t *bytes);
+int32_t hapmoe_pack_image(const hapmoe_problem *p, void *h_image, int64_t bytes);
+
+/* Size of the cost-table buffer for the full candidate array, and of the
+ * optional fp64 debug buffer (pre-rounding terms). */
+int32_t hapmoe_tables_bytes(const hapmoe_problem *p, int64_t *bytes);
+int32_t hapmoe_debug_bytes(const hapmoe_problem *p, int64_t *bytes);
+
+/* Cost-table buffer format (for inspection; the stage DP reads it):
+ *   out[0..8] = n_configs, n_orders, n_masks (= 2^T - 1), np (prefix stride
+ *   >= N + 1), off_pi, off_key, off_mem, off_time, total bytes.
+ *   pi   [n_configs] 152-byte records {int64 x_bytes, int64 tbar,
+ *        int64 p2p[4][4], int32 status, uint32 used_masks}
+ *   key  [n_configs * n_orders] 136-byte records {int64 dp_const,
+ *        uint8 mask[32], lo[32], hi[32], bpair[32]}
+ *   mem  [n_configs][4][np] int64 prefix sums over layers of weights, r = 0
+ *        activations, r = 1 activations, and the count of MoE layers
+ *   time [n_configs][n_masks][3][np] int64 prefix sums of the stage time
+ *        without / with recomputation and of its communication part, for the
+ *        device-type set m at index m - 1 (only sets some stage uses are
+ *        written).
+ * Debug buffer (fp64, per configuration, out[0..3] = doubles per
+ * configuration, offsets of the type, set and memory blocks):
+ *   type [N][T][2] (Eq. 2 compute, expert), set [n_masks][N][3] (all-to-all,
+ *   TP, CP), mem [N][2] (weights, activations). */
+int32_t hapmoe_tables_layout(const hapmoe_problem *p, int64_t out[9]);
+int32_t hapmoe_debug_layout(const hapmoe_problem *p, int64_t out[4]);
+
+/* Cost-table kernel (Section 3.2 Eq. 2, Eq. 3, load imbalance, stage memory;
+ * Section 3.3 compute / primitive tables; Section 3.4 pruning windows and the
+ * constants of Eq. 4).  Per configuration and device-type set it writes prefix
+ * sums over layers of the stage time without (r = 0) and with (r = 1)
+ * recomputation and of the communication part, per configuration the weight /
+ * activation prefix sums, and per (configuration, ordering) the stage layout.
+ * d_cand must be the full array of hapmoe_enumerate_candidates (n_cand
+ * entries); d_tables has hapmoe_tables_bytes bytes.  d_debug (may be NULL)
+ * receives the fp64 terms before rounding (hapmoe_debug_bytes).  Asynchronous. */
+int32_t hapmoe_eval_cost_tables(const hapmoe_problem *p, const void *d_image,
+                                const hapmoe_candidate *d_cand, int64_t n_cand,
+                                void *d_tables, int64_t tables_bytes,
+                                double *d_debug, int64_t debug_bytes, void *stream);
+
+/* Stage-DP kernel (Section 3.4 DP transition, prunings 1-3, Algorithm 1 with
+ * backtrace) for candidates [first, first + count): for each, the partition
+ * minimising sum_i c_i + (B-1) max_i c_i subject to every stage fitting its
+ * memory with the least recomputation.  Ties: lowest threshold t*, then the
+ * smallest split point at each backtrace step (from the last stage).  Writes
+ * d_res[0 .. count).  d_stats (may be NULL) receives per candidate two int32:
+ * threshold passes and DP relaxations.  Asynchronous. */
+int32_t hapmoe_stage_dp(const hapmoe_problem *p, const void *d_image,
+                        const hapmoe_candidate *d_cand, int64_t n_cand,
+                        const void *d_tables, int64_t tables_bytes,
+                        int64_t first, int64_t count,
+                        hapmoe_dp_result *d_res, int32_t *d_stats, void *stream);
+
+/* Workspace of hapmoe_best_plan for n results. */
+int32_t hapmoe_best_plan_ws_bytes(const hapmoe_problem *p, int64_t n, int64_t *bytes);
+
+/* Segmented arg-min (Eq. 1 objective): per configuration pi the best of its
+ * candidates (d_config_best, n_configs int64 entries: candidate index or -1;
+ * may be NULL), then the global best by (objective, candidate index).  d_res
+ * holds the results of candidates [0, n).  Waits for `stream`, fills *h_plan.
+ * Returns HAPMOE_E_INFEASIBLE if no candidate is feasible. */
+int32_t hapmoe_best_plan(const hapmoe_problem *p, const hapmoe_candidate *d_cand,
+                         const void *d_tables, int64_t tables_bytes,
+                         const hapmoe_dp_result *d_res, int64_t n,
+                         int64_t *d_config_best, void *d_ws, int64_t ws_bytes,
+                         hapmoe_plan *h_plan, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HAPMOE_H */

@@ -1,0 +1,464 @@
+// Host side of the C ABI declared in include/hapmoe.h: argument checks, the
+// candidate enumeration, the device problem image, buffer-size queries and the
+// kernel launches.  No device memory is allocated here.
+#include <algorithm>
+#include <array>
+#include <cmath>
+#include <cstring>
+#include <vector>
+
+#include "internal.h"
+
+using namespace hapmoe;
+
+namespace {
+
+bool finite_nonneg(double x) { return std::isfinite(x) && x >= 0.0; }
+
+int32_t check_problem(const hapmoe_problem *p)
+{
+    if (!p) return HAPMOE_E_INVAL;
+    const hapmoe_model &m = p->model;
+    const hapmoe_cluster &c = p->cluster;
+    const hapmoe_params &q = p->params;
+    const hapmoe_space &s = p->space;
+    const int N = m.n_layers, T = c.n_types;
+    if (N < 1 || N > kMaxLayers || T < 1 || T > kMaxTypes) return HAPMOE_E_INVAL;
+    if (m.seq_len < 1 || m.hidden < 1 || m.micro_batch_size < 1 || m.elem_bytes < 0) return HAPMOE_E_INVAL;
+    if ((int64_t)m.seq_len * m.micro_batch_size > (int64_t(1) << 31)) return HAPMOE_E_INVAL;
+    if (m.n_experts < 0 || m.n_experts > 65536) return HAPMOE_E_INVAL;
+    if (m.n_experts > 0 && (m.top_k < 1 || m.top_k > m.n_experts)) return HAPMOE_E_INVAL;
+    if (!finite_nonneg(m.moe_ffn_mult)) return HAPMOE_E_INVAL;
+    if (!m.is_moe || !m.params_dense || !m.params_expert || !m.act_bytes) return HAPMOE_E_INVAL;
+    if (m.n_experts > 0 && !m.expert_tokens) return HAPMOE_E_INVAL;
+    const int64_t big = int64_t(1) << 50;
+    for (int l = 0; l < N; ++l) {
+        if (m.is_moe[l] > 1 || (m.is_moe[l] && m.n_experts == 0)) return HAPMOE_E_INVAL;
+        if (m.params_dense[l] < 0 || m.params_dense[l] > big) return HAPMOE_E_INVAL;
+        if (m.params_expert[l] < 0 || m.params_expert[l] > big) return HAPMOE_E_INVAL;
+        if (m.act_bytes[l] < 0 || m.act_bytes[l] > big) return HAPMOE_E_INVAL;
+        for (int e = 0; e < m.n_experts; ++e) {
+            const int64_t v = m.expert_tokens[(int64_t)l * m.n_experts + e];
+            if (v < 0 || v > (int64_t(1) << 40)) return HAPMOE_E_INVAL;
+        }
+    }
+    int64_t G = 0;
+    for (int h = 0; h < T; ++h) {
+        if (c.count[h] < 1 || c.speed[h] < 1 || c.speed[h] > 1000000 || c.mem_bytes[h] < 0) return HAPMOE_E_INVAL;
+        if (!(std::isfinite(c.eff[h]) && c.eff[h] > 0.0) || !finite_nonneg(c.route_coef[h])) return HAPMOE_E_INVAL;
+        for (int g = 0; g < T; ++g)
+            if (!(std::isfinite(c.bw[h][g]) && c.bw[h][g] > 0.0) || !finite_nonneg(c.alpha[h][g]))
+                return HAPMOE_E_INVAL;
+        G += c.count[h];
+    }
+    if (G > (1 << 20)) return HAPMOE_E_INVAL;
+    if (!c.t_dense || !c.t_ffn) return HAPMOE_E_INVAL;
+    for (int64_t i = 0; i < (int64_t)T * 16 * N; ++i)
+        if (c.t_dense[i] < 0 || c.t_dense[i] > (int64_t(1) << 40) || c.t_ffn[i] < 0 || c.t_ffn[i] > c.t_dense[i])
+            return HAPMOE_E_INVAL;
+    if (!(q.rc_time >= 1.0 && q.rc_time <= 16.0) || !(q.rc_act >= 0.0 && q.rc_act <= 1.0)) return HAPMOE_E_INVAL;
+    if (!(q.gamma >= 0.0 && q.gamma <= 1.0) || !finite_nonneg(q.opt_coef)) return HAPMOE_E_INVAL;
+    if (q.delta_den < 1 || q.delta_den > 1000000 || q.delta_num < 0 || q.delta_num >= q.delta_den)
+        return HAPMOE_E_INVAL;
+    if (q.eta_prune < 0 || q.eta_prune > 1000000) return HAPMOE_E_INVAL;
+    if (s.pp_max < 1 || s.pp_max > kMaxStages || s.mode < 0 || s.mode > 1 || s.ep_max < 1) return HAPMOE_E_INVAL;
+    if (s.tp_mask < 0 || s.tp_mask > 15 || s.cp_mask < 0 || s.cp_mask > 15 || s.tpe_mask < 0 || s.tpe_mask > 15)
+        return HAPMOE_E_INVAL;
+    if (s.n_micro < 1 || s.n_micro > HAPMOE_MAX_MICRO) return HAPMOE_E_INVAL;
+    for (int i = 0; i < s.n_micro; ++i)
+        if (s.micro[i] < 1 || s.micro[i] > kMaxMicroValue) return HAPMOE_E_INVAL;
+    return HAPMOE_OK;
+}
+
+// The configuration set, the type orderings and the LDS bounds of the DP kernel.
+struct Space {
+    std::vector<std::array<int32_t, 6>> cfg;   // pp, tp, cp, dp, ep, tpe
+    std::vector<std::array<int8_t, kMaxTypes>> perm;
+    int kmax = 1;    // distinct device-type sets over the stages of any candidate
+    int ppmax = 1;
+};
+
+void build_space(const hapmoe_problem *p, Space &S)
+{
+    const hapmoe_model &m = p->model;
+    const hapmoe_cluster &c = p->cluster;
+    const hapmoe_space &sp = p->space;
+    const int T = c.n_types;
+    int G = 0;
+    for (int h = 0; h < T; ++h) G += c.count[h];
+
+    std::vector<int> tps, cps, tpes, eps;
+    for (int i = 0; i < 4; ++i) {
+        if ((sp.tp_mask >> i) & 1) tps.push_back(1 << i);
+        if ((sp.cp_mask >> i) & 1) cps.push_back(1 << i);
+        if ((sp.tpe_mask >> i) & 1) tpes.push_back(1 << i);
+    }
+    const bool dense = m.n_experts == 0;
+    if (dense) {
+        eps = {1};
+        tpes = {1};
+    } else {
+        for (int e = 1; e <= sp.ep_max && e <= m.n_experts; e *= 2)
+            if (m.n_experts % e == 0) eps.push_back(e);
+    }
+    S.cfg.clear();
+    S.kmax = 1;
+    S.ppmax = 1;
+    for (int PP = 1; PP <= std::min(G, std::min(sp.pp_max, m.n_layers)); ++PP) {
+        if (G % PP) continue;
+        const int g = G / PP;
+        bool any = false;
+        for (int TP : tps) {
+            if (g % TP || m.hidden % TP) continue;
+            for (int CP : cps) {
+                if (m.seq_len % CP) continue;
+                for (int EP : eps)
+                    for (int TPE : tpes) {
+                        int DP;
+                        if (sp.mode == 0) {
+                            if (g % (TP * CP) || g % (EP * TPE)) continue;
+                            DP = g / (TP * CP);
+                        } else {
+                            const int prod = TP * CP * EP * TPE;
+                            if (g % prod) continue;
+                            DP = g / prod;
+                        }
+                        S.cfg.push_back({PP, TP, CP, DP, EP, TPE});
+                        any = true;
+                    }
+            }
+        }
+        if (any) {
+            // pure stages use at most T sets; a stage straddling a type boundary
+            // (possible only if some m_h is not a multiple of the group) adds at most T-1
+            bool straddle = false;
+            for (int h = 0; h < T; ++h) straddle |= (c.count[h] % g) != 0;
+            S.kmax = std::max(S.kmax, std::min(PP, T + (straddle ? T - 1 : 0)));
+            S.ppmax = std::max(S.ppmax, PP);
+        }
+    }
+    std::array<int8_t, kMaxTypes> cur{};
+    for (int h = 0; h < T; ++h) cur[h] = (int8_t)h;
+    S.perm.clear();
+    do {
+        S.perm.push_back(cur);
+    } while (std::next_permutation(cur.begin(), cur.begin() + T));
+}
+
+int check_arch()
+{
+    static int cache[64] = {0};   // 0 unknown, 1 gfx950, 2 other
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return HAPMOE_E_HIP;
+    if (dev >= 0 && dev < 64 && cache[dev]) return cache[dev] == 1 ? HAPMOE_OK : HAPMOE_E_ARCH;
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return HAPMOE_E_HIP;
+    const bool ok = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+    if (dev >= 0 && dev < 64) cache[dev] = ok ? 1 : 2;
+    return ok ? HAPMOE_OK : HAPMOE_E_ARCH;
+}
+
+struct ImageLayout {
+    int64_t off_is_moe, off_tokens, off_pdense, off_pexp, off_act, off_tdense, off_tffn, total;
+};
+
+ImageLayout image_layout(const hapmoe_problem *p)
+{
+    const int64_t N = p->model.n_layers, E = p->model.n_experts, T = p->cluster.n_types;
+    ImageLayout I;
+    I.off_is_moe = align256((int64_t)sizeof(ImageHeader));
+    I.off_tokens = align256(I.off_is_moe + N);
+    I.off_pdense = align256(I.off_tokens + N * E * 8);
+    I.off_pexp = align256(I.off_pdense + N * 8);
+    I.off_act = align256(I.off_pexp + N * 8);
+    I.off_tdense = align256(I.off_act + N * 8);
+    I.off_tffn = align256(I.off_tdense + T * 16 * N * 8);
+    I.total = align256(I.off_tffn + T * 16 * N * 8);
+    return I;
+}
+
+int64_t per_config(const hapmoe_problem *p, const Space &S)
+{
+    return (int64_t)S.perm.size() * p->space.n_micro;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *hapmoe_strerror(int32_t code)
+{
+    switch (code) {
+    case HAPMOE_OK: return "ok";
+    case HAPMOE_E_INVAL: return "invalid problem or argument";
+    case HAPMOE_E_CAPACITY: return "output array too small";
+    case HAPMOE_E_WORKSPACE: return "device buffer too small";
+    case HAPMOE_E_HIP: return "HIP runtime error";
+    case HAPMOE_E_ARCH: return "current device is not gfx950";
+    case HAPMOE_E_INFEASIBLE: return "no candidate has a feasible partition";
+    case HAPMOE_E_RANGE: return "candidate range out of bounds";
+    default: return "unknown status";
+    }
+}
+
+int32_t hapmoe_validate(const hapmoe_problem *p) { return check_problem(p); }
+
+int32_t hapmoe_enumerate_candidates(const hapmoe_problem *p, hapmoe_candidate *out, int64_t capacity,
+                                    int64_t *n_total)
+{
+    if (n_total) *n_total = 0;
+    if (const int32_t e = check_problem(p)) return e;
+    if (!n_total || capacity < 0) return HAPMOE_E_INVAL;
+    Space S;
+    build_space(p, S);
+    const int64_t total = (int64_t)S.cfg.size() * per_config(p, S);
+    *n_total = total;
+    if (out) {
+        int64_t k = 0;
+        for (const auto &cf : S.cfg)
+            for (int o = 0; o < (int)S.perm.size(); ++o)
+                for (int b = 0; b < p->space.n_micro; ++b) {
+                    if (k >= capacity) break;
+                    hapmoe_candidate &x = out[k++];
+                    x.pp = cf[0];
+                    x.tp = cf[1];
+                    x.cp = cf[2];
+                    x.dp = cf[3];
+                    x.ep = cf[4];
+                    x.tpe = cf[5];
+                    x.order = o;
+                    x.n_micro = p->space.micro[b];
+                }
+    }
+    return (!out || capacity < total) ? HAPMOE_E_CAPACITY : HAPMOE_OK;
+}
+
+int32_t hapmoe_image_bytes(const hapmoe_problem *p, int64_t *bytes)
+{
+    if (const int32_t e = check_problem(p)) return e;
+    if (!bytes) return HAPMOE_E_INVAL;
+    *bytes = image_layout(p).total;
+    return HAPMOE_OK;
+}
+
+int32_t hapmoe_pack_image(const hapmoe_problem *p, void *h_image, int64_t bytes)
+{
+    if (const int32_t e = check_problem(p)) return e;
+    if (!h_image) return HAPMOE_E_INVAL;
+    const ImageLayout I = image_layout(p);
+    if (bytes < I.total) return HAPMOE_E_WORKSPACE;
+    Space S;
+    build_space(p, S);
+    unsigned char *base = static_cast<unsigned char *>(h_image);
+    std::memset(base, 0, (size_t)I.total);
+    ImageHeader &H = *reinterpret_cast<ImageHeader *>(base);
+    const hapmoe_model &m = p->model;
+    const hapmoe_cluster &c = p->cluster;
+    const hapmoe_params &q = p->params;
+    H.n_layers = m.n_layers;
+    H.seq_len = m.seq_len;
+    H.hidden = m.hidden;
+    H.n_experts = m.n_experts;
+    H.top_k = m.top_k;
+    H.mbs = m.micro_batch_size;
+    H.elem_bytes = m.elem_bytes;
+    H.n_types = c.n_types;
+    H.total_devices = 0;
+    for (int h = 0; h < kMaxTypes; ++h) {
+        const bool on = h < c.n_types;
+        H.count[h] = on ? c.count[h] : 0;
+        H.speed[h] = on ? c.speed[h] : 0;
+        H.mem_bytes[h] = on ? c.mem_bytes[h] : 0;
+        H.eff[h] = on ? c.eff[h] : 1.0;
+        H.route_coef[h] = on ? c.route_coef[h] : 0.0;
+        H.total_devices += H.count[h];
+        for (int g = 0; g < kMaxTypes; ++g) {
+            const bool on2 = on && g < c.n_types;
+            H.bw[h * kMaxTypes + g] = on2 ? c.bw[h][g] : 1.0;
+            H.alpha[h * kMaxTypes + g] = on2 ? c.alpha[h][g] : 0.0;
+        }
+    }
+    H.moe_ffn_mult = m.moe_ffn_mult;
+    H.gamma = q.gamma;
+    H.rc_time = q.rc_time;
+    H.rc_act = q.rc_act;
+    H.opt_coef = q.opt_coef;
+    H.delta_num = q.delta_num;
+    H.delta_den = q.delta_den;
+    H.eta_prune = q.eta_prune;
+    H.prune_window = q.prune_window ? 1 : 0;
+    H.prune_hetero = q.prune_hetero ? 1 : 0;
+    H.allow_recompute = q.allow_recompute ? 1 : 0;
+    H.n_orders = (int32_t)S.perm.size();
+    H.n_micro = p->space.n_micro;
+    H.n_configs = (int32_t)S.cfg.size();
+    for (size_t o = 0; o < S.perm.size(); ++o)
+        for (int j = 0; j < kMaxTypes; ++j) H.perm[o][j] = S.perm[o][j];
+    for (int i = 0; i < p->space.n_micro; ++i) H.micro[i] = p->space.micro[i];
+    H.off_is_moe = I.off_is_moe;
+    H.off_tokens = I.off_tokens;
+    H.off_pdense = I.off_pdense;
+    H.off_pexp = I.off_pexp;
+    H.off_act = I.off_act;
+    H.off_tdense = I.off_tdense;
+    H.off_tffn = I.off_tffn;
+    H.image_bytes = I.total;
+    const int64_t N = m.n_layers, E = m.n_experts, T = c.n_types;
+    std::memcpy(base + I.off_is_moe, m.is_moe, (size_t)N);
+    if (E > 0) std::memcpy(base + I.off_tokens, m.expert_tokens, (size_t)(N * E * 8));
+    std::memcpy(base + I.off_pdense, m.params_dense, (size_t)(N * 8));
+    std::memcpy(base + I.off_pexp, m.params_expert, (size_t)(N * 8));
+    std::memcpy(base + I.off_act, m.act_bytes, (size_t)(N * 8));
+    std::memcpy(base + I.off_tdense, c.t_dense, (size_t)(T * 16 * N * 8));
+    std::memcpy(base + I.off_tffn, c.t_ffn, (size_t)(T * 16 * N * 8));
+    return HAPMOE_OK;
+}
+
+int32_t hapmoe_tables_bytes(const hapmoe_problem *p, int64_t *bytes)
+{
+    if (const int32_t e = check_problem(p)) return e;
+    if (!bytes) return HAPMOE_E_INVAL;
+    Space S;
+    build_space(p, S);
+    *bytes = tables_layout((int64_t)S.cfg.size(), (int)S.perm.size(), p->cluster.n_types, p->model.n_layers).total;
+    return HAPMOE_OK;
+}
+
+int32_t hapmoe_tables_layout(const hapmoe_problem *p, int64_t out[9])
+{
+    if (const int32_t e = check_problem(p)) return e;
+    if (!out) return HAPMOE_E_INVAL;
+    Space S;
+    build_space(p, S);
+    const TablesLayout L = tables_layout((int64_t)S.cfg.size(), (int)S.perm.size(), p->cluster.n_types,
+                                         p->model.n_layers);
+    const int64_t v[9] = {L.n_configs, L.n_orders, L.n_masks, L.np, L.off_pi, L.off_key, L.off_mem, L.off_time,
+                          L.total};
+    for (int i = 0; i < 9; ++i) out[i] = v[i];
+    return HAPMOE_OK;
+}
+
+int32_t hapmoe_debug_layout(const hapmoe_problem *p, int64_t out[4])
+{
+    if (const int32_t e = check_problem(p)) return e;
+    if (!out) return HAPMOE_E_INVAL;
+    const DebugLayout D = debug_layout(p->cluster.n_types, p->model.n_layers);
+    out[0] = D.per_cfg;
+    out[1] = D.off_type;
+    out[2] = D.off_mask;
+    out[3] = D.off_mem;
+    return HAPMOE_OK;
+}
+
+int32_t hapmoe_debug_bytes(const hapmoe_problem *p, int64_t *bytes)
+{
+    if (const int32_t e = check_problem(p)) return e;
+    if (!bytes) return HAPMOE_E_INVAL;
+    Space S;
+    build_space(p, S);
+    *bytes = (int64_t)S.cfg.size() * debug_layout(p->cluster.n_types, p->model.n_layers).per_cfg * 8;
+    return HAPMOE_OK;
+}
+
+int32_t hapmoe_eval_cost_tables(const hapmoe_problem *p, const void *d_image, const hapmoe_candidate *d_cand,
+                                int64_t n_cand, void *d_tables, int64_t tables_bytes, double *d_debug,
+                                int64_t debug_bytes, void *stream)
+{
+    if (const int32_t e = check_problem(p)) return e;
+    if (!d_image || !d_cand || !d_tables) return HAPMOE_E_INVAL;
+    Space S;
+    build_space(p, S);
+    const int64_t per = per_config(p, S);
+    if (n_cand != (int64_t)S.cfg.size() * per) return HAPMOE_E_INVAL;
+    const TablesLayout L = tables_layout((int64_t)S.cfg.size(), (int)S.perm.size(), p->cluster.n_types,
+                                         p->model.n_layers);
+    if (tables_bytes < L.total) return HAPMOE_E_WORKSPACE;
+    const DebugLayout D = debug_layout(p->cluster.n_types, p->model.n_layers);
+    if (d_debug && debug_bytes < (int64_t)S.cfg.size() * D.per_cfg * 8) return HAPMOE_E_WORKSPACE;
+    if (const int e = check_arch()) return e;
+    if (launch_cost_tables(d_image, d_cand, per, L, d_tables, d_debug, D, (hipStream_t)stream) != hipSuccess)
+        return HAPMOE_E_HIP;
+    return HAPMOE_OK;
+}
+
+int32_t hapmoe_stage_dp(const hapmoe_problem *p, const void *d_image, const hapmoe_candidate *d_cand,
+                        int64_t n_cand, const void *d_tables, int64_t tables_bytes, int64_t first, int64_t count,
+                        hapmoe_dp_result *d_res, int32_t *d_stats, void *stream)
+{
+    if (const int32_t e = check_problem(p)) return e;
+    if (!d_image || !d_cand || !d_tables || !d_res) return HAPMOE_E_INVAL;
+    Space S;
+    build_space(p, S);
+    const int64_t per = per_config(p, S);
+    if (n_cand != (int64_t)S.cfg.size() * per) return HAPMOE_E_INVAL;
+    if (first < 0 || count < 0 || first + count > n_cand || count > INT32_MAX) return HAPMOE_E_RANGE;
+    const TablesLayout L = tables_layout((int64_t)S.cfg.size(), (int)S.perm.size(), p->cluster.n_types,
+                                         p->model.n_layers);
+    if (tables_bytes < L.total) return HAPMOE_E_WORKSPACE;
+    if (const int e = check_arch()) return e;
+    if (launch_stage_dp(d_image, d_cand, p->model.n_layers, p->space.n_micro, (int)S.perm.size(), L, d_tables,
+                        first, count, S.kmax, S.ppmax, d_res, d_stats, (hipStream_t)stream) != hipSuccess)
+        return HAPMOE_E_HIP;
+    return HAPMOE_OK;
+}
+
+int32_t hapmoe_best_plan_ws_bytes(const hapmoe_problem *p, int64_t n, int64_t *bytes)
+{
+    if (const int32_t e = check_problem(p)) return e;
+    if (!bytes || n < 0) return HAPMOE_E_INVAL;
+    Space S;
+    build_space(p, S);
+    *bytes = best_plan_ws_bytes(n, per_config(p, S), (int64_t)S.cfg.size());
+    return HAPMOE_OK;
+}
+
+int32_t hapmoe_best_plan(const hapmoe_problem *p, const hapmoe_candidate *d_cand, const void *d_tables,
+                         int64_t tables_bytes, const hapmoe_dp_result *d_res, int64_t n, int64_t *d_config_best,
+                         void *d_ws, int64_t ws_bytes, hapmoe_plan *h_plan, void *stream)
+{
+    if (const int32_t e = check_problem(p)) return e;
+    if (!d_cand || !d_tables || !d_res || !d_ws || !h_plan) return HAPMOE_E_INVAL;
+    Space S;
+    build_space(p, S);
+    const int64_t per = per_config(p, S), ncfg = (int64_t)S.cfg.size();
+    if (n < 1 || n > ncfg * per) return HAPMOE_E_RANGE;
+    const TablesLayout L = tables_layout(ncfg, (int)S.perm.size(), p->cluster.n_types, p->model.n_layers);
+    if (tables_bytes < L.total) return HAPMOE_E_WORKSPACE;
+    if (ws_bytes < best_plan_ws_bytes(n, per, ncfg)) return HAPMOE_E_WORKSPACE;
+    if (const int e = check_arch()) return e;
+    hipStream_t s = (hipStream_t)stream;
+    if (launch_best_plan(d_res, n, per, ncfg, d_config_best, d_ws, s) != hipSuccess) return HAPMOE_E_HIP;
+    int64_t best[2];
+    if (hipMemcpyAsync(best, d_ws, sizeof(best), hipMemcpyDeviceToHost, s) != hipSuccess) return HAPMOE_E_HIP;
+    if (hipStreamSynchronize(s) != hipSuccess) return HAPMOE_E_HIP;
+    std::memset(h_plan, 0, sizeof(*h_plan));
+    h_plan->instance = -1;
+    if (best[0] == kInf) return HAPMOE_E_INFEASIBLE;
+    const int64_t idx = best[1];
+    hapmoe_dp_result r;
+    hapmoe_candidate cd;
+    KeyInfo ki;
+    const int64_t key = idx / p->space.n_micro;
+    const auto *tab = static_cast<const unsigned char *>(d_tables);
+    if (hipMemcpyAsync(&r, d_res + idx, sizeof(r), hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipMemcpyAsync(&cd, d_cand + idx, sizeof(cd), hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipMemcpyAsync(&ki, tab + L.off_key + key * (int64_t)sizeof(KeyInfo), sizeof(ki), hipMemcpyDeviceToHost,
+                       s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+        return HAPMOE_E_HIP;
+    h_plan->instance = idx;
+    h_plan->objective = r.objective;
+    h_plan->stage_sum = r.stage_sum;
+    h_plan->t_max = r.t_max;
+    h_plan->dp_const = ki.dp_const;
+    h_plan->cand = cd;
+    h_plan->n_stages = cd.pp;
+    h_plan->recompute_mask = r.recompute_mask;
+    for (int i = 0; i < kMaxStages; ++i) {
+        h_plan->layers[i] = i < cd.pp ? r.layers[i] : 0;
+        h_plan->stage_types[i] = i < cd.pp ? ki.mask[i] : 0;
+    }
+    return HAPMOE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,353 @@
+// Cost-table kernel: the MoE-aware per-layer cost model of the paper
+// (Section 3.2: Eq. 2 compute, Eq. 3 dispatch/combine volume with the best of
+// the all-to-all and all-gather primitives, the load-imbalance factor, the
+// stage memory model; Section 3.3: compute and primitive tables) evaluated
+// for every configuration pi, quantised to int64 ns / bytes and stored as
+// prefix sums over layers for the stage DP.  It also lays out the stages of
+// every (pi, device-type ordering): device-type set, pruning-1 window,
+// boundary link, and the partition-independent T_dp-sync + T_opt of Eq. 4.
+//
+// One workgroup (4 wave64) per configuration.  Arithmetic is fp64 with IEEE
+// + - * / and ceil only, in a fixed order, compiled with -ffp-contract=off so
+// every rounded value is reproducible bit for bit.
+#include "internal.h"
+
+namespace hapmoe {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kLayerSlots = 128;   // >= kMaxLayers + 1
+
+__device__ inline int lg2i(int v) { return 31 - __clz(v); }
+
+// Rounded-up term; values at or above the int64 budget of the DP set the
+// overflow flag instead (and are clamped so the conversion stays defined).
+__device__ inline int64_t qterm(double x, unsigned *flag)
+{
+    if (!(x < (double)kTermLimit)) {
+        atomicOr(flag, 1u);
+        return kTermLimit;
+    }
+    return (int64_t)ceil(x);
+}
+
+// Slowest link inside a device-type set: largest latency, smallest bandwidth
+// over all (h, h') pairs of the set.
+__device__ inline void set_link(const ImageHeader &H, int mask, double &alpha, double &bw)
+{
+    bool first = true;
+    alpha = 0.0;
+    bw = 0.0;
+    for (int h = 0; h < H.n_types; ++h) {
+        if (!((mask >> h) & 1)) continue;
+        for (int g = 0; g < H.n_types; ++g) {
+            if (!((mask >> g) & 1)) continue;
+            const double a = H.alpha[h * kMaxTypes + g], b = H.bw[h * kMaxTypes + g];
+            if (first || a > alpha) alpha = a;
+            if (first || b < bw) bw = b;
+            first = false;
+        }
+    }
+}
+
+// Ring all-reduce over w ranks: 2(w-1) latency steps, 2(w-1)/w of the bytes.
+__device__ inline double ring_ar(double bytes, int w, double alpha, double bw)
+{
+    if (w == 1) return 0.0;
+    const double steps = (double)(2 * (w - 1));
+    return steps * alpha + ((steps * bytes) / (double)w) / bw;
+}
+
+__device__ inline int64_t wave_excl_scan(int64_t x, int lane)
+{
+    int64_t inc = x;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int64_t y = __shfl_up(inc, d, 64);
+        if (lane >= d) inc += y;
+    }
+    return inc - x;
+}
+
+__device__ inline int64_t wave_sum(int64_t x)
+{
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) x += __shfl_xor(x, d, 64);
+    return x;
+}
+
+__global__ __launch_bounds__(kThreads) void k_cost_tables(const unsigned char *__restrict__ img,
+                                                          const hapmoe_candidate *__restrict__ cand,
+                                                          int64_t per_config, TablesLayout L,
+                                                          unsigned char *__restrict__ tab,
+                                                          double *__restrict__ dbg, DebugLayout D)
+{
+    const ImageHeader &H = *reinterpret_cast<const ImageHeader *>(img);
+    const uint8_t *is_moe = img + H.off_is_moe;
+    const int64_t *tokens = reinterpret_cast<const int64_t *>(img + H.off_tokens);
+    const int64_t *pdense = reinterpret_cast<const int64_t *>(img + H.off_pdense);
+    const int64_t *pexp = reinterpret_cast<const int64_t *>(img + H.off_pexp);
+    const int64_t *act = reinterpret_cast<const int64_t *>(img + H.off_act);
+    const int64_t *tdense = reinterpret_cast<const int64_t *>(img + H.off_tdense);
+    const int64_t *tffn = reinterpret_cast<const int64_t *>(img + H.off_tffn);
+
+    const int64_t cfg = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const hapmoe_candidate c = cand[cfg * per_config];
+    const int N = H.n_layers, T = H.n_types, E = H.n_experts;
+    double *dcfg = dbg ? dbg + cfg * D.per_cfg : nullptr;
+
+    __shared__ int64_t s_qce[kMaxTypes][kLayerSlots];   // q(comp) + q(expert) per type, layer
+    __shared__ int64_t s_maxce[kLayerSlots];
+    __shared__ double s_skew[kLayerSlots];
+    __shared__ int64_t s_w[kLayerSlots], s_a0[kLayerSlots], s_a1[kLayerSlots];
+    __shared__ double s_pavg;
+    __shared__ unsigned s_used, s_flag;
+    __shared__ int64_t s_tbar;
+
+    // tokens of one micro-batch per rank, activation tensor bytes, D_moe (Eq. 3)
+    const double tok = (double)((int64_t)H.seq_len * H.mbs / c.cp);
+    const double Dact = (tok * (double)H.hidden) * (double)H.elem_bytes;
+    const double dmoe = (Dact * (double)H.top_k) * (1.0 - 1.0 / (double)c.ep);
+
+    if (tid == 0) {
+        s_used = 0;
+        s_flag = 0;
+        int64_t pd = 0, pe = 0;
+        for (int l = 0; l < N; ++l) {
+            pd += pdense[l];
+            pe += pexp[l];
+        }
+        // parameters per device, averaged over the stages
+        s_pavg = ((double)pd / (double)c.tp + (double)pe / (double)(c.ep * c.tpe)) / (double)c.pp;
+    }
+    __syncthreads();
+
+    // ---- stage layout of every device-type ordering (one thread each) ----
+    if (tid < H.n_orders) {
+        const int o = tid;
+        int pos_type[kMaxTypes], pos_start[kMaxTypes], pos_end[kMaxTypes];
+        int acc = 0;
+        for (int j = 0; j < T; ++j) {
+            pos_type[j] = H.perm[o][j];
+            pos_start[j] = acc;
+            acc += H.count[pos_type[j]];
+            pos_end[j] = acc;
+        }
+        auto type_of = [&](int d) {
+            int t = pos_type[T - 1];
+            for (int j = T - 1; j >= 0; --j)
+                if (d < pos_end[j]) t = pos_type[j];
+            return t;
+        };
+        const int g = H.total_devices / c.pp;
+        KeyInfo *K = reinterpret_cast<KeyInfo *>(tab + L.off_key) + (cfg * L.n_orders + o);
+        int spd[kMaxStages];
+        int64_t sum_speed = 0;
+        double al_k = 0.0, bw_k = 0.0;
+        for (int s = 0; s < c.pp; ++s) {
+            const int d0 = s * g, d1 = d0 + g;
+            int mask = 0;
+            for (int j = 0; j < T; ++j)
+                if (pos_start[j] < d1 && pos_end[j] > d0) mask |= 1 << pos_type[j];
+            int bpair = 0;
+            if (s < c.pp - 1) bpair = (type_of(d1 - 1) << 2) | type_of(d1);
+            int sp = 0;
+            for (int h = 0; h < T; ++h)
+                if ((mask >> h) & 1) sp = (sp == 0 || H.speed[h] < sp) ? H.speed[h] : sp;
+            spd[s] = sp;
+            sum_speed += sp;
+            double a, b;
+            set_link(H, mask, a, b);
+            if (s == 0 || a > al_k) al_k = a;
+            if (s == 0 || b < bw_k) bw_k = b;
+            atomicOr(&s_used, 1u << (mask - 1));
+            K->mask[s] = (uint8_t)mask;
+            K->bpair[s] = (uint8_t)bpair;
+        }
+        // pruning-1 window: n_s in [(1-delta) w_s N, (1+delta) w_s N], w_s = P_s / sum P
+        const int64_t dn = H.delta_num, dd = H.delta_den;
+        const int64_t den = dd * sum_speed;
+        for (int s = 0; s < c.pp; ++s) {
+            int64_t lo = 1, hi = N;
+            if (H.prune_window) {
+                lo = ((dd - dn) * spd[s] * (int64_t)N) / den;
+                hi = ((dd + dn) * spd[s] * (int64_t)N + den - 1) / den;
+                lo = lo < 1 ? 1 : lo;
+                hi = hi > N ? N : hi;
+            }
+            K->lo[s] = (uint8_t)lo;
+            K->hi[s] = (uint8_t)hi;
+        }
+        const double pavg = s_pavg;
+        K->dp_const = qterm(ring_ar(4.0 * pavg, c.dp, al_k, bw_k) + (H.opt_coef * pavg) / (double)c.dp, &s_flag);
+    }
+
+    // ---- per-layer terms: Eq. 2 per device type, load imbalance, memory ----
+    for (int l = tid; l < N; l += kThreads) {
+        const bool moe = is_moe[l] != 0;
+        double sk = 1.0;
+        if (moe) {
+            int64_t sum = 0, mx = 0;
+            for (int e = 0; e < E; ++e) {
+                const int64_t v = tokens[(int64_t)l * E + e];
+                sum += v;
+                mx = v > mx ? v : mx;
+            }
+            const double rho = sum > 0 ? (double)(mx * E) / (double)sum : 1.0;
+            sk = 1.0 + H.gamma * (rho - 1.0);
+        }
+        s_skew[l] = sk;
+        int64_t mce = 0;
+        for (int h = 0; h < T; ++h) {
+            const int64_t off = (((int64_t)h * 4 + lg2i(c.tp)) * 4 + lg2i(c.cp)) * N + l;
+            const double td = (double)tdense[off], tf = (double)tffn[off];
+            double comp, expert;
+            if (!moe) {
+                comp = td;
+                expert = 0.0;
+            } else {
+                const double route = H.route_coef[h] * (tok * (double)H.hidden);
+                comp = (td - tf) + route;
+                const double xexp = (H.moe_ffn_mult * tf) / ((H.eff[h] * (double)c.ep) * (double)c.tpe);
+                expert = sk * xexp;
+            }
+            const int64_t q = qterm(comp, &s_flag) + qterm(expert, &s_flag);
+            s_qce[h][l] = q;
+            mce = q > mce ? q : mce;
+            if (dcfg) {
+                dcfg[D.off_type + ((int64_t)l * T + h) * 2 + 0] = comp;
+                dcfg[D.off_type + ((int64_t)l * T + h) * 2 + 1] = expert;
+            }
+        }
+        s_maxce[l] = mce;
+        const double beta_opt = 6.0 + 12.0 / (double)c.dp;
+        const double w = ((double)pdense[l] / (double)c.tp + (double)pexp[l] / (double)(c.ep * c.tpe)) * beta_opt;
+        const double a0 = (double)act[l] / (double)(c.tp * c.cp);
+        const int64_t qa0 = qterm(a0, &s_flag);
+        s_w[l] = qterm(w, &s_flag);
+        s_a0[l] = qa0;
+        s_a1[l] = qterm(H.rc_act * (double)qa0, &s_flag);
+        if (dcfg) {
+            dcfg[D.off_mem + (int64_t)l * 2 + 0] = w;
+            dcfg[D.off_mem + (int64_t)l * 2 + 1] = a0;
+        }
+    }
+    __syncthreads();
+
+    const int64_t np = L.np;
+    // ---- memory prefix sums and the pruning-3 compute bound (wave 0) ----
+    if (wave == 0) {
+        int64_t *mem = reinterpret_cast<int64_t *>(tab + L.off_mem) + cfg * 4 * np;
+        const int l0 = 2 * lane, l1 = 2 * lane + 1;
+        int64_t v[4][2];
+        for (int k = 0; k < 2; ++k) {
+            const int l = k ? l1 : l0;
+            const bool ok = l < N;
+            v[0][k] = ok ? s_w[l] : 0;
+            v[1][k] = ok ? s_a0[l] : 0;
+            v[2][k] = ok ? s_a1[l] : 0;
+            v[3][k] = ok ? (int64_t)(is_moe[l] != 0) : 0;
+        }
+        for (int f = 0; f < 4; ++f) {
+            const int64_t ex = wave_excl_scan(v[f][0] + v[f][1], lane);
+            if (lane == 0) mem[f * np] = 0;
+            if (l0 < N) mem[f * np + l0 + 1] = ex + v[f][0];
+            if (l1 < N) mem[f * np + l1 + 1] = ex + v[f][0] + v[f][1];
+        }
+        const int64_t tot = wave_sum((l0 < N ? s_maxce[l0] : 0) + (l1 < N ? s_maxce[l1] : 0));
+        if (lane == 0) s_tbar = (tot + c.pp - 1) / c.pp;
+    }
+
+    // ---- per device-type set: communication and stage times (all waves) ----
+    const unsigned used = s_used;
+    int k = 0;
+    for (int m = 1; m <= (int)L.n_masks; ++m) {
+        if (!((used >> (m - 1)) & 1)) continue;
+        if ((k++ & 3) != wave) continue;
+        double alpha, bw;
+        set_link(H, m, alpha, bw);
+        int64_t *P = reinterpret_cast<int64_t *>(tab + L.off_time) + (cfg * L.n_masks + (m - 1)) * 3 * np;
+        int64_t v[3][2];
+        for (int kk = 0; kk < 2; ++kk) {
+            const int l = 2 * lane + kk;
+            v[0][kk] = v[1][kk] = v[2][kk] = 0;
+            if (l >= N) continue;
+            double a2a, tp;
+            if (!is_moe[l]) {
+                a2a = 0.0;
+                tp = 4.0 * ring_ar(Dact, c.tp, alpha, bw);
+            } else {
+                const double sk = s_skew[l];
+                const double f_a2a = (double)(c.ep - 1) * alpha + dmoe / bw;
+                const double f_ag = (double)(c.ep - 1) * alpha + (Dact * (double)(c.ep - 1)) / bw;
+                const double sel = f_ag < f_a2a ? f_ag : f_a2a;
+                a2a = sk * (4.0 * sel);
+                tp = 2.0 * ring_ar(Dact, c.tp, alpha, bw) + 2.0 * ring_ar(Dact, c.tpe, alpha, bw);
+            }
+            const double cpt = c.cp == 1 ? 0.0
+                                         : 3.0 * ((double)(c.cp - 1) * (alpha + ((2.0 * Dact) / (double)c.tp) / bw));
+            const int64_t comm = qterm(a2a, &s_flag) + qterm(tp, &s_flag) + qterm(cpt, &s_flag);
+            int64_t ce = 0;
+            for (int h = 0; h < T; ++h)
+                if ((m >> h) & 1) ce = s_qce[h][l] > ce ? s_qce[h][l] : ce;
+            const int64_t t0 = ce + comm;
+            v[0][kk] = t0;
+            v[1][kk] = qterm(H.rc_time * (double)t0, &s_flag);
+            v[2][kk] = comm;
+            if (dcfg) {
+                double *dm = dcfg + D.off_mask + ((int64_t)(m - 1) * N + l) * 3;
+                dm[0] = a2a;
+                dm[1] = tp;
+                dm[2] = cpt;
+            }
+        }
+        const int l0 = 2 * lane, l1 = 2 * lane + 1;
+        for (int f = 0; f < 3; ++f) {
+            const int64_t ex = wave_excl_scan(v[f][0] + v[f][1], lane);
+            if (lane == 0) P[f * np] = 0;
+            if (l0 < N) P[f * np + l0 + 1] = ex + v[f][0];
+            if (l1 < N) P[f * np + l1 + 1] = ex + v[f][0] + v[f][1];
+        }
+    }
+
+    __syncthreads();
+
+    // ---- per-configuration record (after every overflow flag is in) ----
+    if (tid == 0) {
+        PiInfo *pi = reinterpret_cast<PiInfo *>(tab + L.off_pi) + cfg;
+        // boundary transfer: activation forward + gradient back, tokens*H*beta/TP each way
+        for (int h = 0; h < kMaxTypes; ++h)
+            for (int g = 0; g < kMaxTypes; ++g) {
+                int64_t v = 0;
+                if (h < T && g < T) {
+                    const double a = H.alpha[h * kMaxTypes + g], b = H.bw[h * kMaxTypes + g];
+                    v = qterm(2.0 * (a + (Dact / (double)c.tp) / b), &s_flag);
+                }
+                pi->p2p[h * kMaxTypes + g] = v;
+            }
+        // routing metadata (8 bytes per token and choice) + dispatch and combine buffers
+        pi->x_bytes = qterm(((8.0 * tok) * (double)H.top_k) + 2.0 * dmoe, &s_flag);
+        pi->tbar = s_tbar;
+        pi->used_masks = s_used;
+        pi->status = s_flag ? HAPMOE_STATUS_OVERFLOW : HAPMOE_STATUS_OK;
+    }
+}
+
+}  // namespace
+}  // namespace hapmoe
+
+namespace hapmoe {
+
+hipError_t launch_cost_tables(const void *d_image, const hapmoe_candidate *d_cand, int64_t per_config,
+                              const TablesLayout &L, void *d_tables, double *d_debug,
+                              const DebugLayout &D, hipStream_t s)
+{
+    if (L.n_configs == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_cost_tables, dim3((unsigned)L.n_configs), dim3(kThreads), 0, s,
+                       static_cast<const unsigned char *>(d_image), d_cand, per_config, L,
+                       static_cast<unsigned char *>(d_tables), d_debug, D);
+    return hipGetLastError();
+}
+
+}  // namespace hapmoe

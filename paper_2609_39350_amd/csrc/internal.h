@@ -1,0 +1,121 @@
+// Internal layouts of the HAPMoE planner library: the device problem image and
+// the cost-table buffer.  Shared by the host API and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "hapmoe.h"
+
+namespace hapmoe {
+
+constexpr int kMaxTypes = HAPMOE_MAX_TYPES;
+constexpr int kMaxStages = HAPMOE_MAX_STAGES;
+constexpr int kMaxLayers = HAPMOE_MAX_LAYERS;
+constexpr int kMaxMasks = (1 << kMaxTypes) - 1;   // non-empty device-type sets
+constexpr int kMaxOrders = 24;                      // 4!
+constexpr int64_t kInf = INT64_MAX;
+// Every rounded per-layer term must stay below 2^44 so that prefix sums,
+// memory totals (x M_store <= 32) and (B-1) * t_max (B <= 1024) fit in int64.
+constexpr int64_t kTermLimit = int64_t(1) << 44;
+constexpr int kMaxMicroValue = 1024;
+
+// Flat problem image (host packs it, device reads it).  Arrays follow the
+// header at the offsets below (bytes from the image start, 256-byte aligned).
+struct ImageHeader {
+    int32_t n_layers, seq_len, hidden, n_experts, top_k, mbs, elem_bytes, n_types;
+    int32_t count[kMaxTypes];
+    int32_t speed[kMaxTypes];
+    int64_t mem_bytes[kMaxTypes];
+    double eff[kMaxTypes];
+    double route_coef[kMaxTypes];
+    double bw[kMaxTypes * kMaxTypes];
+    double alpha[kMaxTypes * kMaxTypes];
+    double moe_ffn_mult, gamma, rc_time, rc_act, opt_coef;
+    int32_t delta_num, delta_den, eta_prune, prune_window, prune_hetero, allow_recompute;
+    int32_t n_orders, n_micro, n_configs, total_devices;
+    int8_t perm[kMaxOrders][kMaxTypes];   // orderings, lexicographic
+    int32_t micro[HAPMOE_MAX_MICRO];
+    int64_t off_is_moe, off_tokens, off_pdense, off_pexp, off_act, off_tdense, off_tffn;
+    int64_t image_bytes;
+};
+
+// Per configuration pi.
+struct PiInfo {
+    int64_t x_bytes;                 // MoE buffers of a stage holding an MoE layer
+    int64_t tbar;                    // pruning-3 compute bound
+    int64_t p2p[kMaxTypes * kMaxTypes];  // boundary transfer cost, [from][to]
+    int32_t status;                  // HAPMOE_STATUS_OK or _OVERFLOW
+    uint32_t used_masks;             // bit (m-1): device-type set m occurs in some stage
+};
+
+// Per (configuration, ordering): the stage layout.
+struct KeyInfo {
+    int64_t dp_const;                // T_dp-sync + T_opt
+    uint8_t mask[kMaxStages];        // device types of stage s
+    uint8_t lo[kMaxStages];          // pruning-1 window on n_s
+    uint8_t hi[kMaxStages];
+    uint8_t bpair[kMaxStages];       // (type of last device << 2) | type of next stage's first
+};
+
+// Byte layout of the cost-table buffer.  np = prefix stride (>= N + 1).
+//   pi   [n_configs] PiInfo
+//   key  [n_configs * n_orders] KeyInfo
+//   mem  [n_configs][4][np] int64   W, A0, A1 prefix sums and MoE-layer count
+//   time [n_configs][n_masks][3][np] int64   T0, T1, comm prefix sums
+struct TablesLayout {
+    int64_t n_configs, n_orders, n_masks, np;
+    int64_t off_pi, off_key, off_mem, off_time, total;
+};
+
+// fp64 debug buffer: per configuration
+//   type [N][T][2] (comp, expert), mask [n_masks][N][3] (a2a, tp, cp), mem [N][2] (w, a0)
+struct DebugLayout {
+    int64_t per_cfg, off_type, off_mask, off_mem;
+};
+
+static_assert(sizeof(PiInfo) == 152, "PiInfo layout is part of the documented table format");
+static_assert(sizeof(KeyInfo) == 136, "KeyInfo layout is part of the documented table format");
+static_assert(sizeof(hapmoe_candidate) == 32 && sizeof(hapmoe_dp_result) == 64, "ABI record sizes");
+
+inline int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
+
+inline TablesLayout tables_layout(int64_t n_configs, int n_orders, int n_types, int n_layers)
+{
+    TablesLayout L;
+    L.n_configs = n_configs;
+    L.n_orders = n_orders;
+    L.n_masks = (1 << n_types) - 1;
+    L.np = (n_layers + 1 + 7) & ~7;
+    L.off_pi = 0;
+    L.off_key = align256(L.off_pi + n_configs * (int64_t)sizeof(PiInfo));
+    L.off_mem = align256(L.off_key + n_configs * n_orders * (int64_t)sizeof(KeyInfo));
+    L.off_time = align256(L.off_mem + n_configs * 4 * L.np * 8);
+    L.total = align256(L.off_time + n_configs * L.n_masks * 3 * L.np * 8);
+    return L;
+}
+
+inline DebugLayout debug_layout(int n_types, int n_layers)
+{
+    DebugLayout D;
+    int64_t M = (1 << n_types) - 1;
+    D.off_type = 0;
+    D.off_mask = D.off_type + (int64_t)n_layers * n_types * 2;
+    D.off_mem = D.off_mask + M * n_layers * 3;
+    D.per_cfg = D.off_mem + (int64_t)n_layers * 2;
+    return D;
+}
+
+// Kernel launchers (stream = hipStream_t).
+hipError_t launch_cost_tables(const void *d_image, const hapmoe_candidate *d_cand, int64_t per_config,
+                              const TablesLayout &L, void *d_tables, double *d_debug,
+                              const DebugLayout &D, hipStream_t s);
+hipError_t launch_stage_dp(const void *d_image, const hapmoe_candidate *d_cand, int n_layers,
+                           int n_micro, int n_orders, const TablesLayout &L, const void *d_tables,
+                           int64_t first, int64_t count, int kmax, int ppmax, hapmoe_dp_result *d_res,
+                           int32_t *d_stats, hipStream_t s);
+hipError_t launch_best_plan(const hapmoe_dp_result *d_res, int64_t n, int64_t per_config,
+                            int64_t n_configs, int64_t *d_config_best, void *d_ws, hipStream_t s);
+int64_t best_plan_ws_bytes(int64_t n, int64_t per_config, int64_t n_configs);
+
+}  // namespace hapmoe

@@ -9,3 +9,13 @@ if ROOT not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
     config.addinivalue_line("markers", "slow: longer CPU run")
+
+
+def pytest_sessionfinish(session, exitstatus):
+    try:
+        from tests import test_gpu_parity as g
+    except Exception:
+        return
+    if getattr(g, "_POOL", None) is not None:
+        g._POOL.terminate()
+        g._POOL = None

@@ -1,0 +1,108 @@
+"""C-ABI checks that need no GPU: the library loads, exports every declared
+symbol, validates its input and enumerates the same candidate set as the
+oracle (host-only calls)."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import oracle as orc
+from paper_2609_39350_amd import binding, workloads
+from tests.problems import variant, worked_problem
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "hapmoe.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(hapmoe_\w+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = _declared()
+    assert len(names) >= 12
+    L = binding.lib()
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_strerror_names_every_code():
+    for code in range(-7, 1):
+        assert binding.lib().hapmoe_strerror(code).decode() not in ("", "unknown status")
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 4, 5])
+def test_enumeration_matches_oracle(n):
+    p = workloads.config(n)
+    cand = binding.enumerate_candidates(p)
+    o = orc.Oracle(p)
+    assert len(cand) == o.n_instances()
+    cfgs = o.configs()
+    per = o.n_orders() * len(p["space"]["micro"])
+    got = np.stack([cand[f] for f in ("pp", "tp", "cp", "dp", "ep", "tpe")], axis=1)[::per]
+    assert [tuple(int(v) for v in r) for r in got] == cfgs
+    # ordering and B fields follow the documented index formula
+    k = np.arange(len(cand))
+    assert np.array_equal(cand["order"], (k // len(p["space"]["micro"])) % o.n_orders())
+    assert np.array_equal(cand["n_micro"], np.array(p["space"]["micro"])[k % len(p["space"]["micro"])])
+
+
+def test_enumeration_random_and_literal_mode():
+    for s in range(30):
+        p = workloads.random_tiny(s)
+        cand = binding.enumerate_candidates(p)
+        assert len(cand) == orc.Oracle(p).n_instances()
+    assert len(binding.enumerate_candidates(workloads.config(1, mode=1))) == 110
+
+
+def test_validation_rejects_bad_input():
+    base = worked_problem()
+    bad = [
+        {"model.n_layers": 0},
+        {"model.top_k": 9},
+        {"cluster.t_ffn": base["cluster"]["t_dense"] + 1},
+        {"params.rc_time": 0.5},
+        {"params.gamma": 1.5},
+        {"params.delta_num": 5},
+        {"space.pp_max": 33},
+        {"space.micro": [0]},
+        {"space.micro": [2000]},
+        {"cluster.bw": np.zeros((2, 2))},
+        {"model.is_moe": np.array([2, 1], dtype=np.uint8)},
+    ]
+    for ch in bad:
+        with pytest.raises(binding.HapmoeError) as e:
+            binding.validate(variant(base, **ch))
+        assert e.value.code == -1, ch
+    binding.validate(base)
+
+
+def test_capacity_and_sizes():
+    p = workloads.config(2)
+    hp = binding.HostProblem(p)
+    import ctypes as C
+    n = C.c_int64(0)
+    assert binding.lib().hapmoe_enumerate_candidates(hp.ref, None, 0, C.byref(n)) == -2
+    assert n.value == 16272
+    small = np.zeros(10, dtype=binding.CANDIDATE_DTYPE)
+    assert binding.lib().hapmoe_enumerate_candidates(hp.ref, small.ctypes.data, 10, C.byref(n)) == -2
+    assert n.value == 16272 and small["pp"][0] == 1
+    L = binding.tables_layout(p)
+    assert L["n_configs"] == 904 and L["n_orders"] == 6 and L["n_masks"] == 7 and L["np"] >= 33
+    assert binding.tables_bytes(p) == L["total"]
+    img = binding.pack_image(p)
+    assert img.nbytes == binding.image_bytes(p)
+
+
+def test_device_calls_refuse_bad_sizes_before_touching_the_gpu():
+    # argument checks run before any HIP call: wrong candidate count is rejected
+    p = worked_problem()
+    hp = binding.HostProblem(p)
+    code = binding.lib().hapmoe_stage_dp(hp.ref, 1, 1, 5, 1, 10**9, 0, 1, 1, None, None)
+    assert code == -1
+    code = binding.lib().hapmoe_stage_dp(hp.ref, 1, 1, 90, 1, 10**9, 80, 20, 1, None, None)
+    assert code == -7
+    code = binding.lib().hapmoe_stage_dp(hp.ref, 1, 1, 90, 1, 10, 0, 1, 1, None, None)
+    assert code == -3

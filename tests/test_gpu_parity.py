@@ -1,0 +1,284 @@
+"""GPU path vs the CPU oracle, through the C ABI (needs an MI355X).
+
+The bar (integer/index work): bit-exact objective, stage sum, t*, partition,
+recomputation choice and status for every compared candidate; fp64 terms
+before rounding within 1e-12 relative.  Small problems are compared in full;
+the large configurations on a fixed stride sample plus the chosen best plan.
+"""
+import multiprocessing as mp
+import os
+
+import numpy as np
+import pytest
+
+from oracle import oracle as orc
+from paper_2609_39350_amd import binding, workloads
+from tests.problems import variant, worked_problem
+
+pytestmark = pytest.mark.gpu
+
+_POOL = None
+
+
+def _pool():
+    """Oracle worker processes (spawned: they never touch the GPU)."""
+    global _POOL
+    if _POOL is None:
+        n = max(1, min(16, os.cpu_count() or 1))
+        _POOL = mp.get_context("spawn").Pool(n)
+    return _POOL
+
+
+def oracle_many(problem, idx):
+    idx = [int(i) for i in idx]
+    if len(idx) < 64:
+        return orc.Oracle(problem).solve_many(idx)
+    n = _pool()._processes
+    parts = [idx[k::n] for k in range(n)]
+    outs = _pool().map(orc.solve_worker, [(problem, part) for part in parts])
+    res = [None] * len(idx)
+    for k, out in enumerate(outs):
+        for j, r in enumerate(out):
+            res[k + j * n] = r
+    return res
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    if not t.cuda.is_available():
+        pytest.skip("no GPU")
+    return t
+
+
+def compare(problem, planner, idx, res=None):
+    """Element-by-element parity of the DP results at candidate indices idx."""
+    res = planner.results() if res is None else res
+    ref = oracle_many(problem, idx)
+    bad = []
+    for i, r in zip(idx, ref):
+        g = res[i]
+        st = int(g["status"])
+        if st != r["status"]:
+            bad.append((int(i), "status", st, r["status"]))
+            continue
+        if st != 0:
+            assert int(g["objective"]) == np.iinfo(np.int64).max
+            continue
+        pp = r["pp"]
+        got = (int(g["objective"]), int(g["stage_sum"]), int(g["t_max"]), list(g["layers"][:pp]),
+               [(int(g["recompute_mask"]) >> s) & 1 for s in range(pp)])
+        exp = (r["opt"], r["sum"], r["tmax"], r["layers"], r["recompute"])
+        if got != exp:
+            bad.append((int(i), got, exp))
+        assert all(v == 0 for v in g["layers"][pp:])
+    assert not bad, f"{len(bad)} mismatches, first: {bad[:3]}"
+    return sum(r["status"] == 0 for r in ref)
+
+
+# --------------------------------------------------------------- cost tables
+def _check_tables(problem, planner, cfg_sample):
+    t = binding.decode_tables(problem, planner.tables())
+    dbg = planner.debug()
+    DL = binding.debug_layout(problem)
+    o = orc.Oracle(problem)
+    cfgs = o.configs()
+    N, T = problem["model"]["n_layers"], problem["cluster"]["n_types"]
+    micro0 = problem["space"]["micro"][0]
+    for k in cfg_sample:
+        cfg = cfgs[k]
+        pi = t["pi"][k]
+        assert int(pi["status"]) == 0
+        pt = o.pi_terms(cfg)
+        assert int(pi["x_bytes"]) == pt["x_bytes"] and int(pi["tbar"]) == pt["tbar"]
+        for h in range(T):
+            for g in range(T):
+                assert int(pi["p2p"][h * 4 + g]) == o.p2p(cfg, h, g)
+        d = dbg[k * DL["per_cfg"]:(k + 1) * DL["per_cfg"]]
+        mem = t["mem"][k]
+        for layer in range(N):
+            mt = o.mem_terms(cfg, layer)
+            assert [int(mem[f, layer + 1] - mem[f, layer]) for f in range(3)] == \
+                   [mt["q_w"], mt["q_a0"], mt["q_a1"]]
+            assert int(mem[3, layer + 1] - mem[3, layer]) == int(problem["model"]["is_moe"][layer])
+            for v, ref in ((d[DL["off_mem"] + 2 * layer], mt["w"]), (d[DL["off_mem"] + 2 * layer + 1], mt["a0"])):
+                assert abs(v - ref) <= 1e-12 * abs(ref)
+            for h in range(T):
+                tt = o.type_terms(cfg, layer, h)
+                for j, f in enumerate(("comp", "expert")):
+                    v = d[DL["off_type"] + (layer * T + h) * 2 + j]
+                    assert abs(v - tt[f]) <= 1e-12 * abs(tt[f]), (k, layer, h, f)
+        used = int(pi["used_masks"])
+        masks = [m for m in range(1, 2 ** T) if (used >> (m - 1)) & 1]
+        for m in masks:
+            tm = t["time"][k, m - 1]
+            for layer in range(N):
+                mt = o.mask_terms(cfg, layer, m)
+                got = [int(tm[f, layer + 1] - tm[f, layer]) for f in range(3)]
+                assert got == [mt["t_r0"], mt["t_r1"], mt["comm"]], (k, m, layer)
+                for j, f in enumerate(("a2a", "tp", "cp")):
+                    v = d[DL["off_mask"] + ((m - 1) * N + layer) * 3 + j]
+                    assert abs(v - mt[f]) <= 1e-12 * abs(mt[f]), (k, m, layer, f)
+        for oi in range(o.n_orders()):
+            key = t["key"][k, oi]
+            st = o.stages(cfg, oi, micro0)
+            assert int(key["dp_const"]) == o.dp_const(cfg, oi)
+            for s, x in enumerate(st):
+                assert (int(key["mask"][s]), int(key["lo"][s]), int(key["hi"][s])) == (x["mask"], x["lo"], x["hi"])
+                assert (used >> (x["mask"] - 1)) & 1
+
+
+@pytest.mark.parametrize("which", ["w1", "cfg1", "cfg2", "cfg3", "tiny"])
+def test_cost_tables_match_oracle(torch, which):
+    if which == "w1":
+        probs = [worked_problem()]
+    elif which == "tiny":
+        probs = [workloads.random_tiny(s) for s in range(12)]
+    else:
+        probs = [workloads.config(int(which[-1]))]
+    for p in probs:
+        print(f"cost tables: {p['name']}", flush=True)
+        pl = binding.Planner(p, "cuda:0", debug=True)
+        pl.eval_cost_tables()
+        ncfg = pl.n_configs
+        sample = range(ncfg) if ncfg <= 200 else sorted(set(np.linspace(0, ncfg - 1, 60).astype(int)))
+        _check_tables(p, pl, sample)
+
+
+# ----------------------------------------------------------------- stage DP
+def test_worked_example_on_gpu(torch):
+    p = worked_problem()
+    pl = binding.Planner(p, "cuda:0")
+    plan = pl.run()
+    res = pl.results()
+    assert int(res[88]["objective"]) == 2030366 and int(res[89]["objective"]) == 1316910
+    compare(p, pl, range(pl.n))
+    assert plan["objective"] == min(int(r["objective"]) for r in res)
+
+
+@pytest.mark.parametrize("n", [1, 2])
+def test_small_configs_every_candidate(torch, n):
+    p = workloads.config(n)
+    print(f"config {n}: all candidates", flush=True)
+    pl = binding.Planner(p, "cuda:0")
+    plan = pl.run()
+    feas = compare(p, pl, range(pl.n))
+    assert feas > 0
+    res = pl.results()
+    obj = np.where(res["status"] == 0, res["objective"], np.iinfo(np.int64).max)
+    assert plan["instance"] == int(np.argmin(obj)) and plan["objective"] == int(obj.min())
+    # per-configuration segmented minimum
+    per = pl.n // pl.n_configs
+    cb = pl.config_best()
+    for k in range(pl.n_configs):
+        seg = obj[k * per:(k + 1) * per]
+        exp = -1 if seg.min() == np.iinfo(np.int64).max else k * per + int(np.argmin(seg))
+        assert cb[k] == exp
+
+
+def test_config1_literal_mode(torch):
+    p = workloads.config(1, mode=1)
+    pl = binding.Planner(p, "cuda:0")
+    pl.run()
+    compare(p, pl, range(pl.n))
+
+
+@pytest.mark.parametrize("n,stride", [(3, 61), (5, 37)])
+def test_large_configs_sampled(torch, n, stride):
+    p = workloads.config(n)
+    print(f"config {n}: stride-{stride} sample", flush=True)
+    pl = binding.Planner(p, "cuda:0")
+    plan = pl.run()
+    idx = list(range(0, pl.n, stride)) + [pl.n - 1]
+    if plan["instance"] >= 0:
+        idx.append(plan["instance"])
+    compare(p, pl, sorted(set(idx)))
+    res = pl.results()
+    obj = np.where(res["status"] == 0, res["objective"], np.iinfo(np.int64).max)
+    assert plan["instance"] == int(np.argmin(obj))
+
+
+def test_random_tiny_every_candidate(torch):
+    total = 0
+    for s in range(40):
+        p = workloads.random_tiny(s)
+        pl = binding.Planner(p, "cuda:0")
+        pl.eval_cost_tables()
+        pl.stage_dp()
+        total += compare(p, pl, range(pl.n))
+    assert total > 100
+
+
+def test_subranges_and_repeat_are_identical(torch):
+    p = workloads.config(2)
+    pl = binding.Planner(p, "cuda:0")
+    pl.eval_cost_tables()
+    pl.stage_dp()
+    full = pl.results().copy()
+    pl.d_res.fill_(0)
+    step = 1777   # ragged chunks
+    for first in range(0, pl.n, step):
+        pl.stage_dp(first=first, count=min(step, pl.n - first))
+    assert np.array_equal(full.view(np.uint8), pl.results().view(np.uint8))
+
+
+def test_stats_count_passes(torch):
+    p = workloads.config(2)
+    pl = binding.Planner(p, "cuda:0")
+    pl.eval_cost_tables()
+    pl.stage_dp(stats=True)
+    st = pl.stats()
+    res = pl.results()
+    ok = res["status"] == 0
+    assert (st[ok, 0] >= 2).all() and (st[~ok, 0] <= 1).all()
+    assert (st[:, 1] >= 0).all() and st[ok, 1].sum() > 0
+
+
+def test_all_infeasible_reports_infeasible(torch):
+    p = variant(workloads.config(1), **{"cluster.mem_bytes": np.array([10**6, 10**6], dtype=np.int64)})
+    pl = binding.Planner(p, "cuda:0")
+    with pytest.raises(binding.HapmoeError) as e:
+        pl.run()
+    assert e.value.code == -6
+    res = pl.results()
+    assert (res["status"] == 1).all()
+
+
+def test_degenerate_shapes(torch):
+    # N = PP (one layer per stage), B = 1, dense model, single device type
+    for s in range(6):
+        p = workloads.random_tiny(100 + s, n_layers=4, max_pp=4, micro=[1, 5],
+                                  flags={"prune_window": 0, "prune_hetero": 0, "allow_recompute": 1})
+        pl = binding.Planner(p, "cuda:0")
+        pl.eval_cost_tables()
+        pl.stage_dp()
+        compare(p, pl, range(pl.n))
+    p = workloads.random_tiny(7, n_types=1)
+    p["model"]["n_experts"] = 0
+    p["model"]["is_moe"][:] = 0
+    p["model"]["expert_tokens"] = np.zeros((p["model"]["n_layers"], 0), dtype=np.int64)
+    p["model"]["params_expert"][:] = 0
+    pl = binding.Planner(p, "cuda:0")
+    pl.eval_cost_tables()
+    pl.stage_dp()
+    compare(p, pl, range(pl.n))
+
+
+def test_config4_full_launch_sampled(torch):
+    """The bench workload (3.86 M candidates, one launch): sampled parity + properties."""
+    p = workloads.config(4)
+    print("config 4: full launch, stride sample", flush=True)
+    pl = binding.Planner(p, "cuda:0")
+    plan = pl.run()
+    res = pl.results()
+    ok = res["status"] == 0
+    N = p["model"]["n_layers"]
+    cand = pl.cand_host
+    sums = res["layers"].astype(np.int64).sum(axis=1)
+    assert (sums[ok] == N).all()
+    pp = cand["pp"]
+    assert all((res["layers"][ok][:, :] > 0).sum(axis=1) == pp[ok])
+    obj = np.where(ok, res["objective"], np.iinfo(np.int64).max)
+    assert plan["instance"] == int(np.argmin(obj))
+    idx = list(range(11, pl.n, 25013)) + [plan["instance"]]
+    compare(p, pl, sorted(set(idx)), res)
