@@ -216,18 +216,26 @@ int32_t hapmoe_eval_cost_tables(const hapmoe_problem *p, const void *d_image,
                                 void *d_tables, int64_t tables_bytes,
                                 double *d_debug, int64_t debug_bytes, void *stream);
 
+/* Workspace of hapmoe_stage_dp (its work-queue counter). */
+int32_t hapmoe_stage_dp_ws_bytes(const hapmoe_problem *p, int64_t *bytes);
+
 /* Stage-DP kernel (Section 3.4 DP transition, prunings 1-3, Algorithm 1 with
  * backtrace) for candidates [first, first + count): for each, the partition
  * minimising sum_i c_i + (B-1) max_i c_i subject to every stage fitting its
  * memory with the least recomputation.  Ties: lowest threshold t*, then the
  * smallest split point at each backtrace step (from the last stage).  Writes
  * d_res[0 .. count).  d_stats (may be NULL) receives per candidate two int32:
- * threshold passes and DP relaxations.  Asynchronous. */
+ * threshold passes of its sweep and the DP relaxations (a sweep shared by the
+ * candidates of one (pi, ordering) that differ only in B >= PP counts its
+ * relaxations once, on the first of them).  d_ws (hapmoe_stage_dp_ws_bytes)
+ * holds the kernel's work queue: calls that may overlap need their own d_ws.
+ * Asynchronous. */
 int32_t hapmoe_stage_dp(const hapmoe_problem *p, const void *d_image,
                         const hapmoe_candidate *d_cand, int64_t n_cand,
                         const void *d_tables, int64_t tables_bytes,
                         int64_t first, int64_t count,
-                        hapmoe_dp_result *d_res, int32_t *d_stats, void *stream);
+                        hapmoe_dp_result *d_res, int32_t *d_stats,
+                        void *d_ws, int64_t ws_bytes, void *stream);
 
 /* Workspace of hapmoe_best_plan for n results. */
 int32_t hapmoe_best_plan_ws_bytes(const hapmoe_problem *p, int64_t n, int64_t *bytes);

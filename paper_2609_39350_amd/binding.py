@@ -96,13 +96,14 @@ def lib():
         L.hapmoe_tables_bytes.argtypes = [P(Problem), P(i64)]
         L.hapmoe_debug_bytes.argtypes = [P(Problem), P(i64)]
         L.hapmoe_eval_cost_tables.argtypes = [P(Problem), vp, vp, i64, vp, i64, vp, i64, vp]
-        L.hapmoe_stage_dp.argtypes = [P(Problem), vp, vp, i64, vp, i64, i64, i64, vp, vp, vp]
+        L.hapmoe_stage_dp.argtypes = [P(Problem), vp, vp, i64, vp, i64, i64, i64, vp, vp, vp, i64, vp]
+        L.hapmoe_stage_dp_ws_bytes.argtypes = [P(Problem), P(i64)]
         L.hapmoe_tables_layout.argtypes = [P(Problem), P(i64)]
         L.hapmoe_debug_layout.argtypes = [P(Problem), P(i64)]
         L.hapmoe_best_plan_ws_bytes.argtypes = [P(Problem), i64, P(i64)]
         L.hapmoe_best_plan.argtypes = [P(Problem), vp, vp, i64, vp, i64, vp, vp, i64, P(Plan), vp]
         for f in ("hapmoe_validate", "hapmoe_enumerate_candidates", "hapmoe_image_bytes", "hapmoe_pack_image",
-                  "hapmoe_tables_bytes", "hapmoe_debug_bytes", "hapmoe_tables_layout", "hapmoe_debug_layout", "hapmoe_eval_cost_tables", "hapmoe_stage_dp",
+                  "hapmoe_tables_bytes", "hapmoe_debug_bytes", "hapmoe_tables_layout", "hapmoe_debug_layout", "hapmoe_eval_cost_tables", "hapmoe_stage_dp", "hapmoe_stage_dp_ws_bytes",
                   "hapmoe_best_plan_ws_bytes", "hapmoe_best_plan"):
             getattr(L, f).restype = C.c_int32
         _LIB = L
@@ -276,10 +277,16 @@ def eval_cost_tables(problem, d_image, d_cand, n_cand, d_tables, d_debug=None, s
                                          _stream(stream)), "hapmoe_eval_cost_tables")
 
 
-def stage_dp(problem, d_image, d_cand, n_cand, d_tables, first, count, d_res, d_stats=None, stream=None):
+def stage_dp_ws_bytes(problem) -> int:
+    n = C.c_int64(0)
+    _check(lib().hapmoe_stage_dp_ws_bytes(_hp(problem).ref, C.byref(n)), "hapmoe_stage_dp_ws_bytes")
+    return n.value
+
+
+def stage_dp(problem, d_image, d_cand, n_cand, d_tables, first, count, d_res, d_ws, d_stats=None, stream=None):
     _check(lib().hapmoe_stage_dp(_hp(problem).ref, _dptr(d_image), _dptr(d_cand), int(n_cand), _dptr(d_tables),
                                  _nbytes(d_tables), int(first), int(count), _dptr(d_res), _dptr(d_stats),
-                                 _stream(stream)), "hapmoe_stage_dp")
+                                 _dptr(d_ws), _nbytes(d_ws), _stream(stream)), "hapmoe_stage_dp")
 
 
 def best_plan(problem, d_cand, d_tables, d_res, n, d_ws, d_config_best=None, stream=None) -> dict:
@@ -320,6 +327,7 @@ class Planner:
         self.d_res = torch.empty(max(self.n, 1) * RESULT_DTYPE.itemsize, **u8)
         self.d_stats = None
         self.d_ws = torch.empty(best_plan_ws_bytes(self.hp, max(self.n, 1)), **u8)
+        self.d_dp_ws = torch.empty(stage_dp_ws_bytes(self.hp), **u8)
         n_cfg = tables_layout(self.hp)["n_configs"]
         self.n_configs = n_cfg
         self.d_config_best = torch.empty(max(n_cfg, 1), dtype=torch.int64, device=self.device)
@@ -335,7 +343,8 @@ class Planner:
             self.d_stats = d_stats
         res = self.d_res[first * RESULT_DTYPE.itemsize:]
         st = None if d_stats is None else d_stats[2 * first:]
-        stage_dp(self.hp, self.d_image, self.d_cand, self.n, self.d_tables, first, count, res, st, stream)
+        stage_dp(self.hp, self.d_image, self.d_cand, self.n, self.d_tables, first, count, res, self.d_dp_ws, st,
+                 stream)
 
     def best_plan(self, stream=None):
         return best_plan(self.hp, self.d_cand, self.d_tables, self.d_res, self.n, self.d_ws, self.d_config_best,

@@ -381,12 +381,20 @@ int32_t hapmoe_eval_cost_tables(const hapmoe_problem *p, const void *d_image, co
     return HAPMOE_OK;
 }
 
-int32_t hapmoe_stage_dp(const hapmoe_problem *p, const void *d_image, const hapmoe_candidate *d_cand,
-                        int64_t n_cand, const void *d_tables, int64_t tables_bytes, int64_t first, int64_t count,
-                        hapmoe_dp_result *d_res, int32_t *d_stats, void *stream)
+int32_t hapmoe_stage_dp_ws_bytes(const hapmoe_problem *p, int64_t *bytes)
 {
     if (const int32_t e = check_problem(p)) return e;
-    if (!d_image || !d_cand || !d_tables || !d_res) return HAPMOE_E_INVAL;
+    if (!bytes) return HAPMOE_E_INVAL;
+    *bytes = stage_dp_ws_bytes();
+    return HAPMOE_OK;
+}
+
+int32_t hapmoe_stage_dp(const hapmoe_problem *p, const void *d_image, const hapmoe_candidate *d_cand,
+                        int64_t n_cand, const void *d_tables, int64_t tables_bytes, int64_t first, int64_t count,
+                        hapmoe_dp_result *d_res, int32_t *d_stats, void *d_ws, int64_t ws_bytes, void *stream)
+{
+    if (const int32_t e = check_problem(p)) return e;
+    if (!d_image || !d_cand || !d_tables || !d_res || !d_ws) return HAPMOE_E_INVAL;
     Space S;
     build_space(p, S);
     const int64_t per = per_config(p, S);
@@ -394,10 +402,13 @@ int32_t hapmoe_stage_dp(const hapmoe_problem *p, const void *d_image, const hapm
     if (first < 0 || count < 0 || first + count > n_cand || count > INT32_MAX) return HAPMOE_E_RANGE;
     const TablesLayout L = tables_layout((int64_t)S.cfg.size(), (int)S.perm.size(), p->cluster.n_types,
                                          p->model.n_layers);
-    if (tables_bytes < L.total) return HAPMOE_E_WORKSPACE;
+    if (tables_bytes < L.total || ws_bytes < stage_dp_ws_bytes()) return HAPMOE_E_WORKSPACE;
     if (const int e = check_arch()) return e;
-    if (launch_stage_dp(d_image, d_cand, p->model.n_layers, p->space.n_micro, (int)S.perm.size(), L, d_tables,
-                        first, count, S.kmax, S.ppmax, d_res, d_stats, (hipStream_t)stream) != hipSuccess)
+    std::vector<int32_t> cfg_pp(S.cfg.size());
+    for (size_t i = 0; i < S.cfg.size(); ++i) cfg_pp[i] = S.cfg[i][0];
+    if (launch_stage_dp(d_image, d_cand, p->model.n_layers, p->space.n_micro, cfg_pp, (int)S.perm.size(), L,
+                        d_tables, first, count, S.kmax, S.ppmax, d_res, d_stats, d_ws, p->space.micro,
+                        (hipStream_t)stream) != hipSuccess)
         return HAPMOE_E_HIP;
     return HAPMOE_OK;
 }

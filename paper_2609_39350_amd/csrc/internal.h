@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <vector>
+
 #include "hapmoe.h"
 
 namespace hapmoe {
@@ -110,10 +112,12 @@ inline DebugLayout debug_layout(int n_types, int n_layers)
 hipError_t launch_cost_tables(const void *d_image, const hapmoe_candidate *d_cand, int64_t per_config,
                               const TablesLayout &L, void *d_tables, double *d_debug,
                               const DebugLayout &D, hipStream_t s);
-hipError_t launch_stage_dp(const void *d_image, const hapmoe_candidate *d_cand, int n_layers,
-                           int n_micro, int n_orders, const TablesLayout &L, const void *d_tables,
-                           int64_t first, int64_t count, int kmax, int ppmax, hapmoe_dp_result *d_res,
-                           int32_t *d_stats, hipStream_t s);
+hipError_t launch_stage_dp(const void *d_image, const hapmoe_candidate *d_cand, int n_layers, int n_micro,
+                           const std::vector<int32_t> &config_pp, int n_orders, const TablesLayout &L,
+                           const void *d_tables, int64_t first, int64_t count, int kmax, int ppmax,
+                           hapmoe_dp_result *d_res, int32_t *d_stats, void *d_ws, const int32_t *micro,
+                           hipStream_t s);
+int64_t stage_dp_ws_bytes();
 hipError_t launch_best_plan(const hapmoe_dp_result *d_res, int64_t n, int64_t per_config,
                             int64_t n_configs, int64_t *d_config_best, void *d_ws, hipStream_t s);
 int64_t best_plan_ws_bytes(int64_t n, int64_t per_config, int64_t n_configs);

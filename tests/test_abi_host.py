@@ -100,9 +100,9 @@ def test_device_calls_refuse_bad_sizes_before_touching_the_gpu():
     # argument checks run before any HIP call: wrong candidate count is rejected
     p = worked_problem()
     hp = binding.HostProblem(p)
-    code = binding.lib().hapmoe_stage_dp(hp.ref, 1, 1, 5, 1, 10**9, 0, 1, 1, None, None)
-    assert code == -1
-    code = binding.lib().hapmoe_stage_dp(hp.ref, 1, 1, 90, 1, 10**9, 80, 20, 1, None, None)
-    assert code == -7
-    code = binding.lib().hapmoe_stage_dp(hp.ref, 1, 1, 90, 1, 10, 0, 1, 1, None, None)
-    assert code == -3
+    f = binding.lib().hapmoe_stage_dp
+    assert f(hp.ref, 1, 1, 5, 1, 10**9, 0, 1, 1, None, 1, 256, None) == -1
+    assert f(hp.ref, 1, 1, 90, 1, 10**9, 80, 20, 1, None, 1, 256, None) == -7
+    assert f(hp.ref, 1, 1, 90, 1, 10, 0, 1, 1, None, 1, 256, None) == -3
+    assert f(hp.ref, 1, 1, 90, 1, 10**9, 0, 1, 1, None, 1, 8, None) == -3
+    assert f(hp.ref, 1, 1, 90, 1, 10**9, 0, 1, 1, None, None, 256, None) == -1
