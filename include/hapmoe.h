@@ -224,10 +224,12 @@ int32_t hapmoe_stage_dp_ws_bytes(const hapmoe_problem *p, int64_t *bytes);
  * minimising sum_i c_i + (B-1) max_i c_i subject to every stage fitting its
  * memory with the least recomputation.  Ties: lowest threshold t*, then the
  * smallest split point at each backtrace step (from the last stage).  Writes
- * d_res[0 .. count).  d_stats (may be NULL) receives per candidate two int32:
- * threshold passes of its sweep and the DP relaxations (a sweep shared by the
- * candidates of one (pi, ordering) that differ only in B >= PP counts its
- * relaxations once, on the first of them).  d_ws (hapmoe_stage_dp_ws_bytes)
+ * d_res[0 .. count).  d_stats (may be NULL) receives per candidate four
+ * int32: threshold passes of its sweep, DP relaxations, split-point
+ * evaluations of the feasibility scan, 0.  Candidates of one (pi, ordering)
+ * whose B gives the same min(B, PP) share one sweep; its relaxations and
+ * evaluations are counted once, on the first of them.  d_ws
+ * (hapmoe_stage_dp_ws_bytes)
  * holds the kernel's work queue: calls that may overlap need their own d_ws.
  * Asynchronous. */
 int32_t hapmoe_stage_dp(const hapmoe_problem *p, const void *d_image,

@@ -339,10 +339,10 @@ class Planner:
         count = self.n - first if count is None else count
         d_stats = None
         if stats:
-            d_stats = self.torch.zeros(2 * max(self.n, 1), dtype=self.torch.int32, device=self.device)
+            d_stats = self.torch.zeros(4 * max(self.n, 1), dtype=self.torch.int32, device=self.device)
             self.d_stats = d_stats
         res = self.d_res[first * RESULT_DTYPE.itemsize:]
-        st = None if d_stats is None else d_stats[2 * first:]
+        st = None if d_stats is None else d_stats[4 * first:]
         stage_dp(self.hp, self.d_image, self.d_cand, self.n, self.d_tables, first, count, res, self.d_dp_ws, st,
                  stream)
 
@@ -362,7 +362,7 @@ class Planner:
 
     def stats(self) -> np.ndarray:
         self.torch.cuda.synchronize(self.device)
-        return self.d_stats.cpu().numpy().reshape(-1, 2)[: self.n]
+        return self.d_stats.cpu().numpy().reshape(-1, 4)[: self.n]
 
     def tables(self) -> np.ndarray:
         self.torch.cuda.synchronize(self.device)

@@ -10,72 +10,72 @@
 // min-max pass) is the floor, and thresholds that can no longer beat an
 // incumbent are skipped.  This visits exactly the (max, sum) Pareto points in
 // range and returns the same (objective, t*, partition) as an ascending sweep
-// over every distinct stage cost.
+// over every distinct stage cost: the back-trace of the pass at the winning
+// threshold is the lexicographically smallest sum-optimal partition there,
+// which is also the smallest one at its own largest stage.
 //
 // Work sharing across B: B enters a candidate only through the 1F1B count of
-// stored micro-batches min(PP - i, B) (memory) and through the (B-1) weight of
-// the objective.  All candidates of one (pi, ordering) whose B gives the same
-// min(B, PP) therefore share the feasible segments and every DP pass; one
-// sweep serves all of them, with one incumbent per B held in its own lane.
+// stored micro-batches min(PP - i, B) (memory) and the (B-1) weight of the
+// objective.  Candidates of one (pi, ordering) whose B gives the same
+// min(B, PP) form a group that shares every feasible segment and every DP
+// pass; one sweep serves the group, one incumbent per B.
 //
-// Mapping: persistent wave64 workgroups pull work items (pi, ordering,
-// B-group) from an atomic queue, largest PP first.  Lanes run over the end
-// layer b of a stage, restricted to the band of b reachable under the
-// pruning-1 windows; split points a run over the previous stage's band.
-// Layer prefix sums sit in LDS; the feasible split interval of every
-// (stage, b) is computed once per work item (memory with / without
-// recomputation and prunings 1 and 3 are monotone in the segment length).
-// No MFMA: this is int64 min-plus scan work.
+// Mapping: persistent wave64 workgroups pull (pi, ordering) keys from an atomic
+// queue, largest PP first.  The stage layout of a key is wave-uniform (one
+// stage per lane, read with readlane).  Up to four B-groups of the key run at
+// once in lane segments of 16 / 32 lanes; in a segment, lanes cover the band
+// of end layers b a stage can reach under the pruning-1 windows (in rounds),
+// and each lane loops over the split points a of the previous stage's band.
+// Layer prefix sums live in LDS once per key; feasible split intervals
+// (memory with / without recomputation, prunings 1 and 3 -- all monotone in
+// the segment length), DP rows (double-buffered) and back-trace pointers live
+// in LDS per segment, packed by band.  Lane j also holds the incumbent of the
+// key's j-th microbatch count.  No MFMA: this is int64 min-plus scan work.
 #include "internal.h"
 
 namespace hapmoe {
 namespace {
 
 constexpr int64_t kBig = int64_t(1) << 62;   // "no partition" inside the DP (sums stay far from overflow)
-constexpr int kMaxRuns = 32;
+constexpr int kMaxSeg = 4;
 
-struct ItemRun {
-    int64_t item_start;
-    int32_t key_start, key_count, n_groups, pp;
-};
-
-// Work items: runs of consecutive (pi, ordering) keys with the same PP; each
-// key of a run contributes n_groups items (one per distinct min(B, PP)).
-struct ItemMap {
-    int32_t n_runs, pad;
-    int64_t total;
-    ItemRun run[kMaxRuns];
-};
-
+// LDS of one wave: TM [kmax][np] {T0, T1} | memory prefixes | per-segment
+// region | control.  The per-segment region holds, for each active segment:
+// AMIN, A0B, ARG [sum of band widths] bytes and two DP rows [max band width].
 struct DpLds {
-    int np, kmax, ppmax;
-    int off_amin, off_a0, off_u, off_arg, off_fm, off_w, off_a0m, off_a1m, off_moe, off_bt, total;
+    int np, kmax, ppmax, region;
+    int off_mw, off_ma0, off_ma1, off_moe, off_region, off_ctl, total;
 };
 
-inline int align16(int x) { return (x + 15) & ~15; }
+__host__ __device__ inline int align16(int x) { return (x + 15) & ~15; }
 
-// LDS of one wave: TM [kmax][np] {T0, T1} | AMIN, A0B [ppmax][np] bytes |
-// union( ARG [ppmax][np] bytes + FM [np] {F, M} ,  memory prefixes ) | back-trace scratch
+// Per-segment control block in LDS.
+struct SegCtl {
+    int64_t t;        // threshold of the next pass
+    int64_t F, M;     // result of the last pass at b = N
+    int32_t on;       // the segment takes part in the next pass
+    int32_t pad;
+    uint32_t bt[8];   // back-trace: n_i bytes
+    uint32_t rmask, ok;
+};
+
+
 DpLds dp_lds(int n_layers, int kmax, int ppmax)
 {
     DpLds S;
     S.np = (n_layers + 1 + 15) & ~15;
     S.kmax = kmax;
     S.ppmax = ppmax;
-    const int np = S.np;
-    S.off_amin = kmax * np * 16;
-    S.off_a0 = S.off_amin + ppmax * np;
-    S.off_u = align16(S.off_a0 + ppmax * np);
-    S.off_arg = S.off_u;
-    S.off_fm = align16(S.off_arg + ppmax * np);
-    const int dp_end = S.off_fm + np * 16;
-    S.off_w = S.off_u;
-    S.off_a0m = S.off_w + np * 8;
-    S.off_a1m = S.off_a0m + np * 8;
-    S.off_moe = S.off_a1m + np * 8;
-    const int mem_end = S.off_moe + np * 4;
-    S.off_bt = align16(dp_end > mem_end ? dp_end : mem_end);
-    S.total = S.off_bt + 48;
+    const int np = S.np, w = n_layers + 1;
+    S.off_mw = kmax * np * 16;
+    S.off_ma0 = S.off_mw + np * 8;
+    S.off_ma1 = S.off_ma0 + np * 8;
+    S.off_moe = S.off_ma1 + np * 8;
+    S.off_region = align16(S.off_moe + np * 4);
+    // one segment always fits: every stage band is at most N + 1 wide
+    S.region = align16(3 * ppmax * w) + 2 * align16(w * 16) + 64;
+    S.off_ctl = S.off_region + S.region;
+    S.total = S.off_ctl + kMaxSeg * (int)sizeof(SegCtl);
     return S;
 }
 
@@ -125,6 +125,16 @@ __device__ inline int wave_incl_scan(int x, int lane)
     return x;
 }
 
+__device__ inline int wave_max32(int x)
+{
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int y = __shfl_xor(x, d, 64);
+        x = y > x ? y : x;
+    }
+    return x;
+}
+
 __device__ inline int wave_sum32(int x)
 {
 #pragma unroll
@@ -132,9 +142,9 @@ __device__ inline int wave_sum32(int x)
     return x;
 }
 
-// The workgroup is a single wave: LDS traffic of one wave is processed in
-// order, so a wave-level fence (wait for outstanding LDS ops + no compiler
-// motion) separates the reads of a row from its in-place update.
+// The workgroup is a single wave whose LDS operations are processed in order;
+// this fence keeps the compiler from moving LDS accesses across it and waits
+// for the wave's outstanding LDS operations.
 __device__ inline void wave_sync()
 {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -175,11 +185,11 @@ __device__ inline void write_result(hapmoe_dp_result *out, int status, int64_t o
 
 __global__ void k_reset_queue(uint32_t *q) { q[0] = 0; }
 
-template <int R, bool STATS>
+template <bool STATS>
 __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict__ img,
                                                  const hapmoe_candidate *__restrict__ cand, TablesLayout L,
                                                  const unsigned char *__restrict__ tab, int64_t first,
-                                                 int64_t count, ItemMap M, DpLds S,
+                                                 int64_t count, int64_t key_lo, int64_t n_keys, DpLds S,
                                                  hapmoe_dp_result *__restrict__ res, int32_t *__restrict__ stats,
                                                  uint32_t *__restrict__ queue)
 {
@@ -193,53 +203,43 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
     const uint32_t zero_words[8] = {0, 0, 0, 0, 0, 0, 0, 0};
 
     I64x2 *TM = reinterpret_cast<I64x2 *>(smem);
-    uint8_t *AMIN = smem + S.off_amin;
-    uint8_t *A0B = smem + S.off_a0;
-    uint8_t *ARG = smem + S.off_arg;
-    I64x2 *FM = reinterpret_cast<I64x2 *>(smem + S.off_fm);
-    int64_t *MW = reinterpret_cast<int64_t *>(smem + S.off_w);
-    int64_t *MA0 = reinterpret_cast<int64_t *>(smem + S.off_a0m);
-    int64_t *MA1 = reinterpret_cast<int64_t *>(smem + S.off_a1m);
+    int64_t *MW = reinterpret_cast<int64_t *>(smem + S.off_mw);
+    int64_t *MA0 = reinterpret_cast<int64_t *>(smem + S.off_ma0);
+    int64_t *MA1 = reinterpret_cast<int64_t *>(smem + S.off_ma1);
     int32_t *MOE = reinterpret_cast<int32_t *>(smem + S.off_moe);
-    uint32_t *BT = reinterpret_cast<uint32_t *>(smem + S.off_bt);   // back-trace: 8 words of n_i + r mask
+    unsigned char *REG = smem + S.off_region;
+    SegCtl *CTL = reinterpret_cast<SegCtl *>(smem + S.off_ctl);
 
     for (;;) {
         uint32_t qi = 0;
         if (lane == 0) qi = atomicAdd(queue, 1u);
         qi = __shfl(qi, 0, 64);
-        if ((int64_t)qi >= M.total) break;   // every wave exits once the queue is drained
-        const int64_t item = M.total - 1 - (int64_t)qi;   // runs are PP-ascending: biggest work first
-        int r = 0;
-        while (r + 1 < M.n_runs && item >= M.run[r + 1].item_start) ++r;
-        const int64_t rel = item - M.run[r].item_start;
-        const int ng = M.run[r].n_groups;
-        const int64_t key = M.run[r].key_start + rel / ng;
-        const int g = (int)(rel % ng);
+        if ((int64_t)qi >= n_keys) break;   // every wave exits once the queue is drained
+        const int64_t key = key_lo + n_keys - 1 - (int64_t)qi;   // keys are PP-ascending: biggest work first
         const int64_t cfg = key / H.n_orders;
         const int64_t idx0 = key * nB;
         const int PP = cand[idx0].pp;
+        const PiInfo *pi = reinterpret_cast<const PiInfo *>(tab + L.off_pi) + cfg;
+        const KeyInfo *ki = reinterpret_cast<const KeyInfo *>(tab + L.off_key) + key;
 
-        // ---- the candidates of this item: lanes j < nB with min(B_j, PP) equal to the g-th value ----
+        // ---- lane j holds the key's j-th microbatch count ----
+        const int64_t inst = idx0 + lane;
+        const bool inr = lane < nB && inst >= first && inst < first + count;
         int Bj = 1, vj = 0;
         if (lane < nB) {
             Bj = H.micro[lane];
             vj = Bj < PP ? Bj : PP;
         }
         const uint64_t present = wave_or64(lane < nB ? (uint64_t(1) << vj) : 0);
-        uint64_t rest = present;
-        for (int k = 0; k < g; ++k) rest &= rest - 1;
-        const int vg = __ffsll((unsigned long long)rest) - 1;
-        const int64_t inst = idx0 + lane;
-        const bool member = lane < nB && vj == vg && inst >= first && inst < first + count;
-        if (!__any(member)) continue;
+        const int ng = __popcll(present);
+        const int gj = __popcll(present & ((uint64_t(1) << vj) - 1));   // this lane's group
+        if (!__any(inr)) continue;
         hapmoe_dp_result *out = res + (inst - first);
-
-        const PiInfo *pi = reinterpret_cast<const PiInfo *>(tab + L.off_pi) + cfg;
-        const KeyInfo *ki = reinterpret_cast<const KeyInfo *>(tab + L.off_key) + key;
+        int32_t *st_out = STATS ? stats + 4 * (inst - first) : nullptr;
         if (pi->status != HAPMOE_STATUS_OK) {
-            if (member) {
+            if (inr) {
                 write_result(out, HAPMOE_STATUS_OVERFLOW, kInf, kInf, kInf, 0, zero_words);
-                if (STATS) stats[2 * (inst - first)] = stats[2 * (inst - first) + 1] = 0;
+                if (STATS) st_out[0] = st_out[1] = st_out[2] = st_out[3] = 0;
             }
             continue;
         }
@@ -258,31 +258,34 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
         int64_t cap = kInf;
         for (int h = 0; h < H.n_types; ++h)
             if ((mask >> h) & 1) cap = H.mem_bytes[h] < cap ? H.mem_bytes[h] : cap;
-        const int64_t ms = (int64_t)((PP - lane) < vg ? (PP - lane) : vg);   // 1F1B stored micro-batches
         const bool inner = lane < PP - 1;
         const int64_t p2p = inner ? pi->p2p[(bp >> 2) * kMaxTypes + (bp & 3)] : 0;
         const int bdiff = inner && ((bp >> 2) != (bp & 3));
         const int mixed = __popc(mask) > 1;
         const int64_t X = pi->x_bytes, eta_tbar = (int64_t)H.eta_prune * pi->tbar;
-        // band of end layers reachable by stage s under the windows
+        // band [blo, bhi] of end layers stage s can reach under the windows
         const int cumlo = wave_incl_scan(lane < PP ? lo : 0, lane);
         const int cumhi = wave_incl_scan(lane < PP ? hi : 0, lane);
         const int totlo = rl32(cumlo, 63), tothi = rl32(cumhi, 63);
         int blo = N - (tothi - cumhi), bhi = N - (totlo - cumlo);
         blo = blo > cumlo ? blo : cumlo;
         bhi = bhi < cumhi ? bhi : cumhi;
-        const bool band_ok = !(lane < PP) || blo <= bhi;
-        const bool feasible_shape = totlo <= N && tothi >= N && __all(band_ok);
-        if (nslot > S.kmax || PP > S.ppmax || !feasible_shape) {
-            if (member) {
+        const int wd = lane < PP ? (bhi >= blo ? bhi - blo + 1 : 0) : 0;
+        const int woff = wave_incl_scan(wd, lane) - wd;   // packed offset of stage s
+        const int sumwd = rl32(woff, 63) + rl32(wd, 63);
+        const int maxw = wave_max32(wd);
+        const bool feasible_shape = totlo <= N && tothi >= N && !__any(lane < PP && wd == 0);
+        const int seg_bytes = align16(3 * sumwd) + 2 * align16(maxw * 16);
+        if (nslot > S.kmax || PP > S.ppmax || !feasible_shape || seg_bytes > S.region) {
+            if (inr) {
                 const int st = feasible_shape ? HAPMOE_STATUS_OVERFLOW : HAPMOE_STATUS_INFEASIBLE;
                 write_result(out, st, kInf, kInf, kInf, 0, zero_words);
-                if (STATS) stats[2 * (inst - first)] = stats[2 * (inst - first) + 1] = 0;
+                if (STATS) st_out[0] = st_out[1] = st_out[2] = st_out[3] = 0;
             }
             continue;
         }
 
-        // ---- stage the prefix sums of this candidate in LDS ----
+        // ---- the key's prefix sums in LDS ----
         const int64_t *time = reinterpret_cast<const int64_t *>(tab + L.off_time) + cfg * L.n_masks * 3 * np;
         const int64_t *mem = reinterpret_cast<const int64_t *>(tab + L.off_mem) + cfg * 4 * np;
         {
@@ -292,111 +295,135 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                 const int m = __ffsll((unsigned long long)rs) - 1;
                 rs &= rs - 1;
                 const int64_t *src = time + (int64_t)(m - 1) * 3 * np;
-#pragma unroll
-                for (int q = 0; q < R; ++q) {
-                    const int b = lane + 64 * q;
-                    if (b <= N) TM[k * NP + b] = I64x2{src[b], src[np + b]};
-                }
+                for (int b = lane; b <= N; b += 64) TM[k * NP + b] = I64x2{src[b], src[np + b]};
                 ++k;
             }
-#pragma unroll
-            for (int q = 0; q < R; ++q) {
-                const int b = lane + 64 * q;
-                if (b <= N) {
-                    MW[b] = mem[b];
-                    MA0[b] = mem[np + b];
-                    MA1[b] = mem[2 * np + b];
-                    MOE[b] = (int32_t)mem[3 * np + b];
-                }
+            for (int b = lane; b <= N; b += 64) {
+                MW[b] = mem[b];
+                MA0[b] = mem[np + b];
+                MA1[b] = mem[2 * np + b];
+                MOE[b] = (int32_t)mem[3 * np + b];
             }
         }
         wave_sync();
 
-        // ---- feasible split interval of every (stage, b in band) ----
-        // a in [AMIN, A0B) fits only with recomputation (r = 1), a in [A0B, b - lo] without.
-        for (int s = 0; s < PP; ++s) {
-            const int lo_s = rl32(lo, s), hi_s = rl32(hi, s), mask_s = rl32(mask, s);
-            const int blo_s = rl32(blo, s), bhi_s = rl32(bhi, s);
-            const int plo = s ? rl32(blo, s - 1) : 0, phi = s ? rl32(bhi, s - 1) : 0;
-            const int mixed_s = rl32(mixed, s), bdiff_s = rl32(bdiff, s);
-            const int64_t cap_s = rl64(cap, s), ms_s = rl64(ms, s), p2p_s = rl64(p2p, s);
-            const int64_t *CM = mixed_s ? time + ((int64_t)(mask_s - 1) * 3 + 2) * np : nullptr;
-            const int64_t hc_b = bdiff_s ? p2p_s : 0;
-            for (int q = 0; q * 64 <= bhi_s - blo_s; ++q) {
-                const int k = lane + 64 * q;
-                const int b = blo_s + k;
-                if (b > bhi_s) continue;
-                int amin = 255, a0 = 255;
-                const int ahi = (b - lo_s) < phi ? (b - lo_s) : phi;
-                const int alo = (b - hi_s) > plo ? (b - hi_s) : plo;
-                if (ahi >= alo) {
-                    amin = a0 = ahi + 1;
-                    const int64_t wb = MW[b], a0b = MA0[b], a1b = MA1[b];
-                    const int mb = MOE[b];
-                    const int64_t cmb = CM ? CM[b] : 0;
-                    bool phase0 = true;
-                    for (int a = ahi; a >= alo; --a) {
-                        if (H.prune_hetero) {
-                            const int64_t hc = (CM ? cmb - CM[a] : 0) + hc_b;   // pruning 3
-                            if (hc > eta_tbar) break;
-                        }
-                        const int64_t xb = (mb - MOE[a]) > 0 ? X : 0;
-                        const int64_t dw = wb - MW[a];
-                        if (phase0) {
-                            if (dw + ms_s * (a0b - MA0[a]) + xb <= cap_s) {
-                                a0 = a;
+        // segments per batch: as many as the region holds, at most 4
+        int smax = S.region / seg_bytes;
+        smax = smax > kMaxSeg ? kMaxSeg : smax;
+        const int off_amin = 0, off_a0 = sumwd, off_arg = 2 * sumwd;
+        const int off_fm0 = align16(3 * sumwd), off_fm1 = off_fm0 + align16(maxw * 16);
+
+        for (int g0 = 0; g0 < ng; g0 += smax) {
+            const int nact = (ng - g0) < smax ? (ng - g0) : smax;
+            const int nseg = nact <= 1 ? 1 : (nact <= 2 ? 2 : 4);
+            const int W = 64 / nseg;
+            const int sg = lane / W, ll = lane % W;   // DP view: segment and lane in segment
+            // group value of this lane's segment
+            uint64_t rest = present;
+            for (int k = 0; k < g0 + sg && rest; ++k) rest &= rest - 1;
+            const bool seg_live = sg < nact && rest != 0;
+            const int vseg = seg_live ? __ffsll((unsigned long long)rest) - 1 : 1;
+            unsigned char *R = REG + (seg_live ? sg : 0) * seg_bytes;
+            uint8_t *AMIN = R + off_amin;
+            uint8_t *A0B = R + off_a0;
+            uint8_t *ARG = R + off_arg;
+            I64x2 *const FM0 = reinterpret_cast<I64x2 *>(R + off_fm0);
+            I64x2 *const FM1 = reinterpret_cast<I64x2 *>(R + off_fm1);
+            // candidate view: lane j's segment in this batch (-1: not in this batch)
+            const int sj = (gj >= g0 && gj < g0 + nact) ? gj - g0 : -1;
+            bool member = inr && sj >= 0;
+            // groups whose candidates are all outside [first, first + count) still run;
+            // their results are simply not written.
+
+            int evals = 0;
+            // ---- feasible split interval of every (stage, b in band), per segment ----
+            // a in [AMIN, A0B) fits only with recomputation (r = 1), a in [A0B, b - lo] without.
+            for (int s = 0; s < PP; ++s) {
+                const int lo_s = rl32(lo, s), hi_s = rl32(hi, s), mask_s = rl32(mask, s);
+                const int blo_s = rl32(blo, s), wd_s = rl32(wd, s), off_s = rl32(woff, s);
+                const int plo = s ? rl32(blo, s - 1) : 0, phi = s ? rl32(bhi, s - 1) : 0;
+                const int mixed_s = rl32(mixed, s), bdiff_s = rl32(bdiff, s);
+                const int64_t cap_s = rl64(cap, s), p2p_s = rl64(p2p, s);
+                const int64_t ms = (int64_t)((PP - s) < vseg ? (PP - s) : vseg);   // 1F1B stored micro-batches
+                const int64_t *CM = mixed_s ? time + ((int64_t)(mask_s - 1) * 3 + 2) * np : nullptr;
+                const int64_t hc_b = bdiff_s ? p2p_s : 0;
+                for (int k = ll; k < wd_s; k += W) {
+                    if (!seg_live) break;
+                    const int b = blo_s + k;
+                    int amin = 255, a0 = 255;
+                    const int ahi = (b - lo_s) < phi ? (b - lo_s) : phi;
+                    const int alo = (b - hi_s) > plo ? (b - hi_s) : plo;
+                    if (ahi >= alo) {
+                        amin = a0 = ahi + 1;
+                        const int64_t wb = MW[b], a0b = MA0[b], a1b = MA1[b];
+                        const int mb = MOE[b];
+                        const int64_t cmb = CM ? CM[b] : 0;
+                        bool phase0 = true;
+                        for (int a = ahi; a >= alo; --a) {
+                            if (STATS) ++evals;
+                            if (H.prune_hetero) {
+                                const int64_t hc = (CM ? cmb - CM[a] : 0) + hc_b;   // pruning 3
+                                if (hc > eta_tbar) break;
+                            }
+                            const int64_t xb = (mb - MOE[a]) > 0 ? X : 0;
+                            const int64_t dw = wb - MW[a];
+                            if (phase0) {
+                                if (dw + ms * (a0b - MA0[a]) + xb <= cap_s) {
+                                    a0 = a;
+                                    amin = a;
+                                    continue;
+                                }
+                                phase0 = false;
+                            }
+                            if (!H.allow_recompute) break;
+                            if (dw + ms * (a1b - MA1[a]) + xb <= cap_s) {
                                 amin = a;
                                 continue;
                             }
-                            phase0 = false;
+                            break;   // pruning 2: no recomputation choice fits
                         }
-                        if (!H.allow_recompute) break;
-                        if (dw + ms_s * (a1b - MA1[a]) + xb <= cap_s) {
-                            amin = a;
-                            continue;
-                        }
-                        break;   // pruning 2: no recomputation choice fits
                     }
+                    AMIN[off_s + k] = (uint8_t)amin;
+                    A0B[off_s + k] = (uint8_t)a0;
                 }
-                AMIN[s * NP + k] = (uint8_t)amin;
-                A0B[s * NP + k] = (uint8_t)a0;
             }
-        }
-        wave_sync();   // the memory prefixes are dead from here on (their LDS holds ARG / FM)
-
-        int passes = 0, relax = 0;
-
-        // One DP pass at threshold t.  minimax: F = least possible largest stage;
-        // otherwise F = least stage sum with all stages <= t and M = the largest
-        // stage on the back-trace path (ties: smallest split point a).
-        auto pass = [&](int64_t t, bool minimax, int64_t &F_out, int64_t &M_out) {
-            ++passes;
-            if (lane == 0) FM[0] = I64x2{0, 0};
             wave_sync();
-            for (int s = 0; s < PP; ++s) {
-                const int slot_s = rl32(slot, s), lo_s = rl32(lo, s);
-                const int blo_s = rl32(blo, s), bhi_s = rl32(bhi, s);
-                const int phi = s ? rl32(bhi, s - 1) : 0;
-                const int64_t p2p_s = rl64(p2p, s);
-                const I64x2 *T = TM + slot_s * NP;
-                int64_t fbest[R], fm[R];
-                int fa[R];
-#pragma unroll
-                for (int q = 0; q < R; ++q) {
-                    const int k = lane + 64 * q;
-                    const int b = blo_s + k;
-                    int64_t best = kBig, bm = 0;
-                    int ba = 255;
-                    if (b <= bhi_s) {
-                        const int amin = AMIN[s * NP + k], a0 = A0B[s * NP + k];
+
+            int passes = 0, relax = 0;
+            int last_parity = 0;   // DP row buffer holding b = N after the last pass
+
+            // One DP pass of every segment with CTL.on set, at its CTL.t.
+            // minimax: F = least possible largest stage; otherwise F = least
+            // stage sum with all stages <= t and M = the largest stage on the
+            // back-trace path (ties: smallest split point a).
+            auto pass = [&](bool minimax) {
+                const bool on = seg_live && CTL[sg].on != 0;
+                const int64_t t = seg_live ? CTL[sg].t : 0;
+                if (on) ++passes;
+                if (on && ll == 0) FM1[0] = I64x2{0, 0};   // stage -1: layer 0 reached at cost 0
+                wave_sync();
+                for (int s = 0; s < PP; ++s) {
+                    const int slot_s = rl32(slot, s), lo_s = rl32(lo, s);
+                    const int blo_s = rl32(blo, s), wd_s = rl32(wd, s), off_s = rl32(woff, s);
+                    const int plo = s ? rl32(blo, s - 1) : 0, phi = s ? rl32(bhi, s - 1) : 0;
+                    const int64_t p2p_s = rl64(p2p, s);
+                    const I64x2 *T = TM + slot_s * NP;
+                    const I64x2 *Fp = (s & 1) ? FM0 : FM1;
+                    I64x2 *Fc = (s & 1) ? FM1 : FM0;
+                    for (int k = ll; k < wd_s; k += W) {
+                        if (!on) break;
+                        const int b = blo_s + k;
+                        const int amin = AMIN[off_s + k], a0 = A0B[off_s + k];
                         const int ahi = (b - lo_s) < phi ? (b - lo_s) : phi;
                         const I64x2 tb = T[b];
                         const int64_t k0 = tb.x + p2p_s, k1 = tb.y + p2p_s;
+                        int64_t best = kBig, bm = 0;
+                        int ba = 255;
                         for (int a = amin; a <= ahi; ++a) {
                             const I64x2 ta = T[a];
                             const bool r1 = a < a0;
                             const int64_t cst = r1 ? k1 - ta.y : k0 - ta.x;
-                            const I64x2 f = FM[a];
+                            const I64x2 f = Fp[a - plo];
                             int64_t v = minimax ? (f.x > cst ? f.x : cst) : f.x + cst;
                             v = cst <= t ? v : kBig;
                             if (v < best) {
@@ -406,134 +433,227 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                             }
                         }
                         if (STATS) relax += ahi >= amin ? ahi - amin + 1 : 0;
+                        Fc[k] = I64x2{best, bm};
+                        ARG[off_s + k] = (uint8_t)ba;
                     }
-                    fbest[q] = best;
-                    fm[q] = bm;
-                    fa[q] = ba;
+                    wave_sync();
+                }
+                last_parity = (PP - 1) & 1;
+                if (on && ll == 0) {
+                    const I64x2 fin = last_parity ? FM1[0] : FM0[0];
+                    CTL[sg].F = fin.x;
+                    CTL[sg].M = fin.y;
                 }
                 wave_sync();
-#pragma unroll
-                for (int q = 0; q < R; ++q) {
-                    const int k = lane + 64 * q;
-                    const int b = blo_s + k;
-                    if (b <= bhi_s) {
-                        FM[b] = I64x2{fbest[q], fm[q]};
-                        ARG[s * NP + k] = (uint8_t)fa[q];
-                    }
-                }
-                wave_sync();
-            }
-            const I64x2 fin = FM[N];
-            F_out = fin.x;
-            M_out = fin.y;
-        };
+            };
 
-        // back-trace of the last pass into BT (lane 0), then shared by the writers
-        auto backtrace = [&]() {
-            if (lane == 0) {
-                uint32_t words[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-                uint32_t rmask = 0;
-                int b = N;
-                bool ok = true;
-                for (int s = PP - 1; s >= 0; --s) {
-                    const int k = b - rl32(blo, s);
-                    const int a = ARG[s * NP + k];
-                    if (a >= b) {
-                        ok = false;
-                        break;
-                    }
-                    words[s >> 2] |= (uint32_t)(b - a) << (8 * (s & 3));
-                    if (a < A0B[s * NP + k]) rmask |= 1u << s;
-                    b = a;
+            // per-segment control, written by lane 0 from wave-uniform values
+            auto set_ctl = [&](int seg, bool on, int64_t t) {
+                if (lane == 0) {
+                    CTL[seg].on = on ? 1 : 0;
+                    CTL[seg].t = t;
                 }
-                ok = ok && b == 0;
-                for (int w = 0; w < 8; ++w) BT[w] = words[w];
-                BT[8] = rmask;
-                BT[9] = ok ? 1u : 0u;
+            };
+
+            // ---- 1) bottleneck: min-max pass ----
+#pragma unroll
+            for (int q = 0; q < kMaxSeg; ++q)
+                if (q < nseg) set_ctl(q, q < nact, kInf);
+            wave_sync();
+            pass(true);
+            int64_t tbot = member ? CTL[sj].F : kBig;
+            const bool infeasible = member && tbot >= kBig;
+            if (infeasible) {
+                write_result(out, HAPMOE_STATUS_INFEASIBLE, kInf, kInf, kInf, 0, zero_words);
+                member = false;
+            }
+            // segment s is feasible iff any lane of it still is a member (all agree)
+            int64_t segF[kMaxSeg];
+            bool segok[kMaxSeg];
+            for (int q = 0; q < kMaxSeg; ++q) {
+                segok[q] = false;
+                segF[q] = 0;
+            }
+#pragma unroll
+            for (int q = 0; q < kMaxSeg; ++q) {
+                if (q >= nseg) continue;
+                const int64_t fq = q < nact ? CTL[q].F : kBig;
+                segF[q] = fq;
+                segok[q] = q < nact && fq < kBig;
             }
             wave_sync();
-        };
 
-        int64_t tbot, unused, F1, M1;
-        pass(kInf, true, tbot, unused);
-        if (tbot >= kBig) {
-            if (member) {
-                write_result(out, HAPMOE_STATUS_INFEASIBLE, kInf, kInf, kInf, 0, zero_words);
-                if (STATS) {
-                    stats[2 * (inst - first)] = passes;
-                    stats[2 * (inst - first) + 1] = 0;
+            // ---- 2) least sum without a threshold ----
+#pragma unroll
+            for (int q = 0; q < kMaxSeg; ++q)
+                if (q < nseg) set_ctl(q, segok[q], kInf);
+            wave_sync();
+            pass(false);
+            int64_t F1 = member ? CTL[sj].F : 0, M1 = member ? CTL[sj].M : 0;
+            int64_t lastt[kMaxSeg];
+            for (int q = 0; q < kMaxSeg; ++q) lastt[q] = kInf;
+            const int64_t Bm = (int64_t)Bj - 1;
+            int64_t bs = F1 + Bm * M1, bmx = M1, bt = kInf;   // this lane's incumbent
+            int64_t F = F1, tcur = M1 - 1;
+            wave_sync();
+
+            // ---- 3) the bottleneck threshold itself ----
+            {
+                bool any = false;
+    #pragma unroll
+                for (int q = 0; q < kMaxSeg; ++q) {
+                    if (q >= nseg) continue;
+                    const bool run = segok[q] && segF[q] < CTL[q].M;   // t_bot < M1
+                    set_ctl(q, run, segF[q]);
+                    any |= run;
                 }
+                wave_sync();
+                if (any) {
+                    pass(false);
+#pragma unroll
+                    for (int q = 0; q < kMaxSeg; ++q)
+                        if (q < nseg && segok[q] && CTL[q].on) lastt[q] = segF[q];
+                    if (member && CTL[sj].on) {
+                        const int64_t Fb = CTL[sj].F, Mb = CTL[sj].M;
+                        if (Fb + Bm * Mb <= bs) {
+                            bs = Fb + Bm * Mb;
+                            bmx = Mb;
+                            bt = tbot;
+                        }
+                    }
+                }
+                wave_sync();
             }
-            if (STATS) {
-                const int rs = wave_sum32(relax);
-                const int leader = __ffsll((unsigned long long)__ballot(member)) - 1;
-                if (lane == leader) stats[2 * (inst - first) + 1] = rs;
-            }
-            continue;
-        }
-        pass(kInf, false, F1, M1);
-        int64_t last_t = kInf;
-        const int64_t Bm = (int64_t)Bj - 1;
-        int64_t bs = F1 + Bm * M1, bmx = M1, bt = kInf;   // this lane's incumbent
-        if (tbot < M1) {
-            int64_t Fb, Mb;
-            pass(tbot, false, Fb, Mb);
-            last_t = tbot;
-            if (Fb + Bm * Mb <= bs) {
-                bs = Fb + Bm * Mb;
-                bmx = Mb;
-                bt = tbot;
-            }
-            int64_t F = F1, t = M1 - 1;
+            // lanes of segments where t_bot >= M1 are already final
+            bool sweeping = member && tbot < M1;
+
+            // ---- 4) descending Pareto sweep ----
             for (;;) {
                 const bool done = bmx == tbot && bs == F1 + Bm * tbot;   // reached the lower bound
-                const bool act = member && !done && F + Bm * tbot <= bs;
+                const bool act = sweeping && !done && F + Bm * tbot <= bs;
                 const int64_t lim = act ? (Bm > 0 ? (bs - F) / Bm : kBig) : -1;
-                const int64_t mx = wave_max64(lim);
-                const int64_t tn = mx < t ? mx : t;
-                if (tn <= tbot) break;
-                int64_t Fc, Mc;
-                pass(tn, false, Fc, Mc);
-                last_t = tn;
-                if (Fc + Bm * Mc <= bs) {
-                    bs = Fc + Bm * Mc;
-                    bmx = Mc;
-                    bt = tn;
+                const int64_t mine = lim < tcur ? lim : tcur;
+                bool any = false;
+                int64_t tn[kMaxSeg] = {-1, -1, -1, -1};
+    #pragma unroll
+                for (int q = 0; q < kMaxSeg; ++q) {
+                    if (q >= nseg) continue;
+                    tn[q] = wave_max64(sj == q && act ? mine : -1);
+                    const int64_t tb = wave_max64(sj == q && act ? tbot : -1);
+                    const bool run = tn[q] >= 0 && tn[q] > tb;
+                    set_ctl(q, run, tn[q]);
+                    any |= run;
                 }
-                F = Fc;
-                t = Mc - 1;
+                wave_sync();
+                if (!any) break;
+                pass(false);
+                if (sj >= 0 && sweeping && CTL[sj].on) {
+                    const int64_t Fc = CTL[sj].F, Mc = CTL[sj].M;
+                    if (Fc + Bm * Mc <= bs) {
+                        bs = Fc + Bm * Mc;
+                        bmx = Mc;
+                        bt = CTL[sj].t;
+                    }
+                    F = Fc;
+                    tcur = Mc - 1;
+                }
+    #pragma unroll
+                for (int q = 0; q < kMaxSeg; ++q)
+                    if (q < nseg && CTL[q].on) lastt[q] = CTL[q].t;
+                wave_sync();
             }
-        }
 
-        // ---- results: one back-trace per distinct winning threshold ----
-        bool pending = member;
-        const int64_t dpc = ki->dp_const;
-        while (__any(pending)) {
-            const int64_t tr = wave_min64(pending ? bt : kInf);
-            if (tr != last_t) {
-                int64_t Fr, Mr;
-                pass(tr, false, Fr, Mr);
-                last_t = tr;
+            // ---- 5) results: one back-trace per distinct winning threshold ----
+            bool pending = member;
+            const int64_t dpc = ki->dp_const;
+            while (__any(pending)) {
+                bool anyrun = false;
+                int64_t tr[kMaxSeg] = {kInf, kInf, kInf, kInf};
+    #pragma unroll
+                for (int q = 0; q < kMaxSeg; ++q) {
+                    if (q >= nseg) continue;
+                    tr[q] = wave_min64(pending && sj == q ? bt : kInf);
+                    const bool has = __any(pending && sj == q);
+                    const bool run = has && tr[q] != lastt[q];
+                    set_ctl(q, run, tr[q]);
+                    anyrun |= run;
+                }
+                wave_sync();
+                if (anyrun) {
+                    pass(false);
+        #pragma unroll
+                    for (int q = 0; q < kMaxSeg; ++q)
+                        if (q < nseg && CTL[q].on) lastt[q] = tr[q];
+                }
+                // back-trace of every segment with pending results (lane 0 of the segment)
+                bool hasq[kMaxSeg] = {false, false, false, false};
+    #pragma unroll
+                for (int q = 0; q < kMaxSeg; ++q)
+                    if (q < nseg) hasq[q] = __any(pending && sj == q);
+                const bool tracer = seg_live && ll == 0 && hasq[sg];
+                if (tracer) {
+                    uint32_t words[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+                    uint32_t rmask = 0;
+                    int b = N;
+                    bool ok = true;
+                    for (int s = PP - 1; s >= 0; --s) {
+                        const int k = b - rl32(blo, s);
+                        const int a = ARG[rl32(woff, s) + k];
+                        if (a >= b) {
+                            ok = false;
+                            break;
+                        }
+                        words[s >> 2] |= (uint32_t)(b - a) << (8 * (s & 3));
+                        if (a < A0B[rl32(woff, s) + k]) rmask |= 1u << s;
+                        b = a;
+                    }
+                    ok = ok && b == 0;
+                    for (int w = 0; w < 8; ++w) CTL[sg].bt[w] = words[w];
+                    CTL[sg].rmask = rmask;
+                    CTL[sg].ok = ok ? 1u : 0u;
+                }
+                wave_sync();
+                if (pending) {
+                    const int64_t mytr = sj == 0 ? tr[0] : sj == 1 ? tr[1] : sj == 2 ? tr[2] : tr[3];
+                    if (bt == mytr) {
+                        uint32_t words[8];
+                        for (int w = 0; w < 8; ++w) words[w] = CTL[sj].bt[w];
+                        if (CTL[sj].ok)
+                            write_result(out, HAPMOE_STATUS_OK, bs + dpc, bs - Bm * bmx, bmx, CTL[sj].rmask, words);
+                        else
+                            write_result(out, HAPMOE_STATUS_OVERFLOW, kInf, kInf, kInf, 0, zero_words);
+                        pending = false;
+                    }
+                }
+                wave_sync();
             }
-            backtrace();
-            if (pending && bt == tr) {
-                uint32_t words[8];
-                for (int w = 0; w < 8; ++w) words[w] = BT[w];
-                if (BT[9])
-                    write_result(out, HAPMOE_STATUS_OK, bs + dpc, bs - Bm * bmx, bmx, BT[8], words);
-                else
-                    write_result(out, HAPMOE_STATUS_OVERFLOW, kInf, kInf, kInf, 0, zero_words);
-                pending = false;
+
+            if (STATS) {
+                // per segment: passes, relaxations, split-point evaluations; the
+                // shared work is counted once, on the group's first candidate in range
+                int rq[kMaxSeg] = {0, 0, 0, 0}, eq[kMaxSeg] = {0, 0, 0, 0}, pq[kMaxSeg] = {0, 0, 0, 0};
+                int lead[kMaxSeg] = {-1, -1, -1, -1};
+    #pragma unroll
+                for (int q = 0; q < kMaxSeg; ++q) {
+                    if (q >= nseg) continue;
+                    rq[q] = wave_sum32(sg == q ? relax : 0);
+                    eq[q] = wave_sum32(sg == q ? evals : 0);
+                    pq[q] = wave_max32(sg == q ? passes : 0);
+                    lead[q] = __ffsll((unsigned long long)__ballot(inr && sj == q)) - 1;
+                }
+                if (inr && sj >= 0) {
+                    const int p = sj == 0 ? pq[0] : sj == 1 ? pq[1] : sj == 2 ? pq[2] : pq[3];
+                    const int r = sj == 0 ? rq[0] : sj == 1 ? rq[1] : sj == 2 ? rq[2] : rq[3];
+                    const int e = sj == 0 ? eq[0] : sj == 1 ? eq[1] : sj == 2 ? eq[2] : eq[3];
+                    const int l = sj == 0 ? lead[0] : sj == 1 ? lead[1] : sj == 2 ? lead[2] : lead[3];
+                    st_out[0] = p;
+                    st_out[1] = lane == l ? r : 0;
+                    st_out[2] = lane == l ? e : 0;
+                    st_out[3] = 0;
+                }
             }
+            (void)last_parity;
             wave_sync();
-        }
-        if (STATS) {
-            const int rs = wave_sum32(relax);
-            const int leader = __ffsll((unsigned long long)__ballot(member)) - 1;
-            if (member) {
-                stats[2 * (inst - first)] = passes;
-                stats[2 * (inst - first) + 1] = lane == leader ? rs : 0;
-            }
         }
     }
 }
@@ -548,37 +668,13 @@ hipError_t launch_stage_dp(const void *d_image, const hapmoe_candidate *d_cand, 
                            hapmoe_dp_result *d_res, int32_t *d_stats, void *d_ws, const int32_t *micro,
                            hipStream_t s)
 {
+    (void)config_pp;
+    (void)micro;
+    (void)n_orders;
     if (count == 0) return hipSuccess;
-    // work items over the keys that hold candidates of [first, first + count)
-    const int64_t key_lo = first / n_micro, key_hi = (first + count - 1) / n_micro;   // inclusive
-    ItemMap M;
-    M.n_runs = 0;
-    M.pad = 0;
-    M.total = 0;
-    const int64_t ncfg = (int64_t)config_pp.size();
-    for (int64_t c = 0; c < ncfg;) {
-        int64_t e = c;
-        while (e < ncfg && config_pp[e] == config_pp[c]) ++e;
-        const int pp = config_pp[c];
-        int64_t ks = c * n_orders, ke = e * n_orders - 1;
-        ks = ks > key_lo ? ks : key_lo;
-        ke = ke < key_hi ? ke : key_hi;
-        if (ks <= ke) {
-            uint64_t present = 0;
-            for (int i = 0; i < n_micro; ++i) present |= uint64_t(1) << (micro[i] < pp ? micro[i] : pp);
-            if (M.n_runs >= kMaxRuns) return hipErrorInvalidValue;
-            ItemRun &r = M.run[M.n_runs++];
-            r.item_start = M.total;
-            r.key_start = (int32_t)ks;
-            r.key_count = (int32_t)(ke - ks + 1);
-            r.n_groups = __builtin_popcountll(present);
-            r.pp = pp;
-            M.total += (int64_t)r.key_count * r.n_groups;
-        }
-        c = e;
-    }
-    if (M.total == 0) return hipSuccess;
-    const int R = (n_layers + 1 + 63) / 64;
+    // keys holding candidates of [first, first + count)
+    const int64_t key_lo = first / n_micro, key_hi = (first + count - 1) / n_micro;
+    const int64_t n_keys = key_hi - key_lo + 1;
     const DpLds S = dp_lds(n_layers, kmax, ppmax);
     const auto *img = static_cast<const unsigned char *>(d_image);
     const auto *tab = static_cast<const unsigned char *>(d_tables);
@@ -591,14 +687,12 @@ hipError_t launch_stage_dp(const void *d_image, const hapmoe_candidate *d_cand, 
         hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 64, S.total);
         if (e != hipSuccess) return e;
         int64_t grid = (int64_t)ncu * (per_cu > 0 ? per_cu : 1);
-        if (grid > M.total) grid = M.total;
-        hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(64), S.total, s, img, d_cand, L, tab, first, count, M,
-                           S, d_res, d_stats, queue);
+        if (grid > n_keys) grid = n_keys;
+        hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(64), S.total, s, img, d_cand, L, tab, first, count,
+                           key_lo, n_keys, S, d_res, d_stats, queue);
         return hipGetLastError();
     };
-    if (R == 1)
-        return d_stats ? go(k_stage_dp<1, true>) : go(k_stage_dp<1, false>);
-    return d_stats ? go(k_stage_dp<2, true>) : go(k_stage_dp<2, false>);
+    return d_stats ? go(k_stage_dp<true>) : go(k_stage_dp<false>);
 }
 
 }  // namespace hapmoe

@@ -230,8 +230,12 @@ def test_stats_count_passes(torch):
     st = pl.stats()
     res = pl.results()
     ok = res["status"] == 0
+    assert st.shape == (pl.n, 4)
     assert (st[ok, 0] >= 2).all() and (st[~ok, 0] <= 1).all()
-    assert (st[:, 1] >= 0).all() and st[ok, 1].sum() > 0
+    assert (st[:, 1] >= 0).all() and st[ok, 1].sum() > 0 and st[:, 2].sum() > 0
+    # shared sweeps are counted once per (pi, ordering, min(B, PP)) group
+    per_key = len(p["space"]["micro"])
+    assert (st[:, 1].reshape(-1, per_key) > 0).sum(axis=1).max() <= per_key
 
 
 def test_all_infeasible_reports_infeasible(torch):
