@@ -73,7 +73,7 @@ DpLds dp_lds(int n_layers, int kmax, int ppmax)
     S.off_moe = S.off_ma1 + np * 8;
     S.off_region = align16(S.off_moe + np * 4);
     // one segment always fits: every stage band is at most N + 1 wide
-    S.region = align16(3 * ppmax * w) + 2 * align16(w * 16) + 64;
+    S.region = align16(3 * ppmax * w) + 2 * align16(w * 8) + 64;
     S.off_ctl = S.off_region + S.region;
     S.total = S.off_ctl + kMaxSeg * (int)sizeof(SegCtl);
     return S;
@@ -275,7 +275,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
         const int sumwd = rl32(woff, 63) + rl32(wd, 63);
         const int maxw = wave_max32(wd);
         const bool feasible_shape = totlo <= N && tothi >= N && !__any(lane < PP && wd == 0);
-        const int seg_bytes = align16(3 * sumwd) + 2 * align16(maxw * 16);
+        const int seg_bytes = align16(3 * sumwd) + 2 * align16(maxw * 8);
         if (nslot > S.kmax || PP > S.ppmax || !feasible_shape || seg_bytes > S.region) {
             if (inr) {
                 const int st = feasible_shape ? HAPMOE_STATUS_OVERFLOW : HAPMOE_STATUS_INFEASIBLE;
@@ -311,7 +311,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
         int smax = S.region / seg_bytes;
         smax = smax > kMaxSeg ? kMaxSeg : smax;
         const int off_amin = 0, off_a0 = sumwd, off_arg = 2 * sumwd;
-        const int off_fm0 = align16(3 * sumwd), off_fm1 = off_fm0 + align16(maxw * 16);
+        const int off_fm0 = align16(3 * sumwd), off_fm1 = off_fm0 + align16(maxw * 8);
 
         for (int g0 = 0; g0 < ng; g0 += smax) {
             const int nact = (ng - g0) < smax ? (ng - g0) : smax;
@@ -327,8 +327,8 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
             uint8_t *AMIN = R + off_amin;
             uint8_t *A0B = R + off_a0;
             uint8_t *ARG = R + off_arg;
-            I64x2 *const FM0 = reinterpret_cast<I64x2 *>(R + off_fm0);
-            I64x2 *const FM1 = reinterpret_cast<I64x2 *>(R + off_fm1);
+            int64_t *const FM0 = reinterpret_cast<int64_t *>(R + off_fm0);
+            int64_t *const FM1 = reinterpret_cast<int64_t *>(R + off_fm1);
             // candidate view: lane j's segment in this batch (-1: not in this batch)
             const int sj = (gj >= g0 && gj < g0 + nact) ? gj - g0 : -1;
             bool member = inr && sj >= 0;
@@ -354,33 +354,22 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                     const int ahi = (b - lo_s) < phi ? (b - lo_s) : phi;
                     const int alo = (b - hi_s) > plo ? (b - hi_s) : plo;
                     if (ahi >= alo) {
+                        // the feasible split points form a suffix [amin, ahi] (memory and
+                        // pruning 3 grow with the segment), so both bounds are minima over
+                        // independent evaluations -- no early exit, loads pipeline freely
                         amin = a0 = ahi + 1;
                         const int64_t wb = MW[b], a0b = MA0[b], a1b = MA1[b];
                         const int mb = MOE[b];
                         const int64_t cmb = CM ? CM[b] : 0;
-                        bool phase0 = true;
-                        for (int a = ahi; a >= alo; --a) {
+                        for (int a = alo; a <= ahi; ++a) {
                             if (STATS) ++evals;
-                            if (H.prune_hetero) {
-                                const int64_t hc = (CM ? cmb - CM[a] : 0) + hc_b;   // pruning 3
-                                if (hc > eta_tbar) break;
-                            }
                             const int64_t xb = (mb - MOE[a]) > 0 ? X : 0;
                             const int64_t dw = wb - MW[a];
-                            if (phase0) {
-                                if (dw + ms * (a0b - MA0[a]) + xb <= cap_s) {
-                                    a0 = a;
-                                    amin = a;
-                                    continue;
-                                }
-                                phase0 = false;
-                            }
-                            if (!H.allow_recompute) break;
-                            if (dw + ms * (a1b - MA1[a]) + xb <= cap_s) {
-                                amin = a;
-                                continue;
-                            }
-                            break;   // pruning 2: no recomputation choice fits
+                            const bool ok3 = !H.prune_hetero || (CM ? cmb - CM[a] : 0) + hc_b <= eta_tbar;
+                            const bool f0 = ok3 && dw + ms * (a0b - MA0[a]) + xb <= cap_s;
+                            const bool f1 = ok3 && H.allow_recompute && dw + ms * (a1b - MA1[a]) + xb <= cap_s;
+                            a0 = f0 && a < a0 ? a : a0;
+                            amin = (f0 || f1) && a < amin ? a : amin;
                         }
                     }
                     AMIN[off_s + k] = (uint8_t)amin;
@@ -390,17 +379,17 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
             wave_sync();
 
             int passes = 0, relax = 0;
-            int last_parity = 0;   // DP row buffer holding b = N after the last pass
 
             // One DP pass of every segment with CTL.on set, at its CTL.t.
-            // minimax: F = least possible largest stage; otherwise F = least
-            // stage sum with all stages <= t and M = the largest stage on the
-            // back-trace path (ties: smallest split point a).
+            // minimax: F = least possible largest stage.  Otherwise F = least
+            // stage sum with all stages <= t (ties: smallest split point a);
+            // lane 0 of the segment then back-traces the partition and its
+            // largest stage M into the segment's control block.
             auto pass = [&](bool minimax) {
                 const bool on = seg_live && CTL[sg].on != 0;
                 const int64_t t = seg_live ? CTL[sg].t : 0;
                 if (on) ++passes;
-                if (on && ll == 0) FM1[0] = I64x2{0, 0};   // stage -1: layer 0 reached at cost 0
+                if (on && ll == 0) FM1[0] = 0;   // stage -1: layer 0 reached at cost 0
                 wave_sync();
                 for (int s = 0; s < PP; ++s) {
                     const int slot_s = rl32(slot, s), lo_s = rl32(lo, s);
@@ -408,8 +397,8 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                     const int plo = s ? rl32(blo, s - 1) : 0, phi = s ? rl32(bhi, s - 1) : 0;
                     const int64_t p2p_s = rl64(p2p, s);
                     const I64x2 *T = TM + slot_s * NP;
-                    const I64x2 *Fp = (s & 1) ? FM0 : FM1;
-                    I64x2 *Fc = (s & 1) ? FM1 : FM0;
+                    const int64_t *Fp = (s & 1) ? FM0 : FM1;
+                    int64_t *Fc = (s & 1) ? FM1 : FM0;
                     for (int k = ll; k < wd_s; k += W) {
                         if (!on) break;
                         const int b = blo_s + k;
@@ -417,32 +406,71 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                         const int ahi = (b - lo_s) < phi ? (b - lo_s) : phi;
                         const I64x2 tb = T[b];
                         const int64_t k0 = tb.x + p2p_s, k1 = tb.y + p2p_s;
-                        int64_t best = kBig, bm = 0;
+                        int64_t best = kBig;
                         int ba = 255;
-                        for (int a = amin; a <= ahi; ++a) {
-                            const I64x2 ta = T[a];
-                            const bool r1 = a < a0;
-                            const int64_t cst = r1 ? k1 - ta.y : k0 - ta.x;
-                            const I64x2 f = Fp[a - plo];
-                            int64_t v = minimax ? (f.x > cst ? f.x : cst) : f.x + cst;
-                            v = cst <= t ? v : kBig;
-                            if (v < best) {
-                                best = v;
-                                ba = a;
-                                bm = f.y > cst ? f.y : cst;
+                        int trips = 0;
+                        if (amin <= ahi) {
+                            // a runs downwards: the stage cost only grows as the segment
+                            // grows, so the first cost above t ends the scan; "<=" keeps
+                            // the smallest split point among equal values.  The loads of
+                            // a - 1 are issued before a is evaluated (clamped index).
+                            int a = ahi;
+                            I64x2 ta = T[a];
+                            int64_t f = Fp[a - plo];
+                            for (;;) {
+                                const int an = a > amin ? a - 1 : a;
+                                const I64x2 ta_n = T[an];
+                                const int64_t f_n = Fp[an - plo];
+                                const int64_t cst = a < a0 ? k1 - ta.y : k0 - ta.x;
+                                if (cst > t) break;
+                                ++trips;
+                                const int64_t v = minimax ? (f > cst ? f : cst) : f + cst;
+                                const bool le = v <= best;
+                                best = le ? v : best;
+                                ba = le ? a : ba;
+                                if (a == amin) break;
+                                a = an;
+                                ta = ta_n;
+                                f = f_n;
                             }
                         }
-                        if (STATS) relax += ahi >= amin ? ahi - amin + 1 : 0;
-                        Fc[k] = I64x2{best, bm};
-                        ARG[off_s + k] = (uint8_t)ba;
+                        if (STATS) relax += trips;
+                        Fc[k] = best;
+                        if (!minimax) ARG[off_s + k] = (uint8_t)ba;
                     }
                     wave_sync();
                 }
-                last_parity = (PP - 1) & 1;
+                const int64_t fin = ((PP - 1) & 1) ? FM1[0] : FM0[0];
                 if (on && ll == 0) {
-                    const I64x2 fin = last_parity ? FM1[0] : FM0[0];
-                    CTL[sg].F = fin.x;
-                    CTL[sg].M = fin.y;
+                    CTL[sg].F = fin;
+                    if (!minimax) {
+                        uint32_t words[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+                        uint32_t rmask = 0;
+                        int64_t m = 0;
+                        int b = N;
+                        bool ok = fin < kBig;
+                        for (int s = PP - 1; s >= 0 && ok; --s) {
+                            const int k = b - rl32(blo, s), off_s = rl32(woff, s);
+                            const int a = ARG[off_s + k];
+                            if (a >= b) {
+                                ok = false;
+                                break;
+                            }
+                            const I64x2 *T = TM + rl32(slot, s) * NP;
+                            const I64x2 ta = T[a], tb = T[b];
+                            const bool r1 = a < A0B[off_s + k];
+                            const int64_t c = (r1 ? tb.y - ta.y : tb.x - ta.x) + rl64(p2p, s);
+                            m = c > m ? c : m;
+                            words[s >> 2] |= (uint32_t)(b - a) << (8 * (s & 3));
+                            if (r1) rmask |= 1u << s;
+                            b = a;
+                        }
+                        ok = ok && b == 0;
+                        CTL[sg].M = m;
+                        for (int w = 0; w < 8; ++w) CTL[sg].bt[w] = words[w];
+                        CTL[sg].rmask = rmask;
+                        CTL[sg].ok = ok ? 1u : 0u;
+                    }
                 }
                 wave_sync();
             };
@@ -455,31 +483,40 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                 }
             };
 
+            // this lane's incumbent and its partition
+            int64_t bs = 0, bmx = 0;
+            uint32_t pw[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+            uint32_t prm = 0, pok = 0;
+            const int64_t Bm = (int64_t)Bj - 1;
+            auto take = [&](int64_t Fx, int64_t Mx) {   // offer the segment's last pass
+                const int64_t sc = Fx + Bm * Mx;
+                if (sc <= bs) {
+                    bs = sc;
+                    bmx = Mx;
+                    for (int w = 0; w < 8; ++w) pw[w] = CTL[sj].bt[w];
+                    prm = CTL[sj].rmask;
+                    pok = CTL[sj].ok;
+                }
+            };
+
             // ---- 1) bottleneck: min-max pass ----
 #pragma unroll
             for (int q = 0; q < kMaxSeg; ++q)
                 if (q < nseg) set_ctl(q, q < nact, kInf);
             wave_sync();
             pass(true);
-            int64_t tbot = member ? CTL[sj].F : kBig;
-            const bool infeasible = member && tbot >= kBig;
-            if (infeasible) {
+            const int64_t tbot = member ? CTL[sj].F : kBig;
+            if (member && tbot >= kBig) {
                 write_result(out, HAPMOE_STATUS_INFEASIBLE, kInf, kInf, kInf, 0, zero_words);
                 member = false;
             }
-            // segment s is feasible iff any lane of it still is a member (all agree)
-            int64_t segF[kMaxSeg];
-            bool segok[kMaxSeg];
-            for (int q = 0; q < kMaxSeg; ++q) {
-                segok[q] = false;
-                segF[q] = 0;
-            }
+            int64_t segF[kMaxSeg] = {kBig, kBig, kBig, kBig};
+            bool segok[kMaxSeg] = {false, false, false, false};
 #pragma unroll
             for (int q = 0; q < kMaxSeg; ++q) {
-                if (q >= nseg) continue;
-                const int64_t fq = q < nact ? CTL[q].F : kBig;
-                segF[q] = fq;
-                segok[q] = q < nact && fq < kBig;
+                if (q >= nact) continue;
+                segF[q] = CTL[q].F;
+                segok[q] = segF[q] < kBig;
             }
             wave_sync();
 
@@ -489,18 +526,20 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                 if (q < nseg) set_ctl(q, segok[q], kInf);
             wave_sync();
             pass(false);
-            int64_t F1 = member ? CTL[sj].F : 0, M1 = member ? CTL[sj].M : 0;
-            int64_t lastt[kMaxSeg];
-            for (int q = 0; q < kMaxSeg; ++q) lastt[q] = kInf;
-            const int64_t Bm = (int64_t)Bj - 1;
-            int64_t bs = F1 + Bm * M1, bmx = M1, bt = kInf;   // this lane's incumbent
+            int64_t F1 = 0, M1 = 0;
+            if (member) {
+                F1 = CTL[sj].F;
+                M1 = CTL[sj].M;
+                bs = kInf;
+                take(F1, M1);
+            }
             int64_t F = F1, tcur = M1 - 1;
             wave_sync();
 
             // ---- 3) the bottleneck threshold itself ----
             {
                 bool any = false;
-    #pragma unroll
+#pragma unroll
                 for (int q = 0; q < kMaxSeg; ++q) {
                     if (q >= nseg) continue;
                     const bool run = segok[q] && segF[q] < CTL[q].M;   // t_bot < M1
@@ -510,22 +549,12 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                 wave_sync();
                 if (any) {
                     pass(false);
-#pragma unroll
-                    for (int q = 0; q < kMaxSeg; ++q)
-                        if (q < nseg && segok[q] && CTL[q].on) lastt[q] = segF[q];
-                    if (member && CTL[sj].on) {
-                        const int64_t Fb = CTL[sj].F, Mb = CTL[sj].M;
-                        if (Fb + Bm * Mb <= bs) {
-                            bs = Fb + Bm * Mb;
-                            bmx = Mb;
-                            bt = tbot;
-                        }
-                    }
+                    if (member && CTL[sj].on) take(CTL[sj].F, CTL[sj].M);
                 }
                 wave_sync();
             }
             // lanes of segments where t_bot >= M1 are already final
-            bool sweeping = member && tbot < M1;
+            const bool sweeping = member && tbot < M1;
 
             // ---- 4) descending Pareto sweep ----
             for (;;) {
@@ -534,98 +563,33 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                 const int64_t lim = act ? (Bm > 0 ? (bs - F) / Bm : kBig) : -1;
                 const int64_t mine = lim < tcur ? lim : tcur;
                 bool any = false;
-                int64_t tn[kMaxSeg] = {-1, -1, -1, -1};
-    #pragma unroll
+#pragma unroll
                 for (int q = 0; q < kMaxSeg; ++q) {
                     if (q >= nseg) continue;
-                    tn[q] = wave_max64(sj == q && act ? mine : -1);
+                    const int64_t tn = wave_max64(sj == q && act ? mine : -1);
                     const int64_t tb = wave_max64(sj == q && act ? tbot : -1);
-                    const bool run = tn[q] >= 0 && tn[q] > tb;
-                    set_ctl(q, run, tn[q]);
+                    const bool run = tn >= 0 && tn > tb;
+                    set_ctl(q, run, tn);
                     any |= run;
                 }
                 wave_sync();
                 if (!any) break;
                 pass(false);
-                if (sj >= 0 && sweeping && CTL[sj].on) {
+                if (sweeping && CTL[sj].on) {
                     const int64_t Fc = CTL[sj].F, Mc = CTL[sj].M;
-                    if (Fc + Bm * Mc <= bs) {
-                        bs = Fc + Bm * Mc;
-                        bmx = Mc;
-                        bt = CTL[sj].t;
-                    }
+                    take(Fc, Mc);
                     F = Fc;
                     tcur = Mc - 1;
                 }
-    #pragma unroll
-                for (int q = 0; q < kMaxSeg; ++q)
-                    if (q < nseg && CTL[q].on) lastt[q] = CTL[q].t;
                 wave_sync();
             }
 
-            // ---- 5) results: one back-trace per distinct winning threshold ----
-            bool pending = member;
-            const int64_t dpc = ki->dp_const;
-            while (__any(pending)) {
-                bool anyrun = false;
-                int64_t tr[kMaxSeg] = {kInf, kInf, kInf, kInf};
-    #pragma unroll
-                for (int q = 0; q < kMaxSeg; ++q) {
-                    if (q >= nseg) continue;
-                    tr[q] = wave_min64(pending && sj == q ? bt : kInf);
-                    const bool has = __any(pending && sj == q);
-                    const bool run = has && tr[q] != lastt[q];
-                    set_ctl(q, run, tr[q]);
-                    anyrun |= run;
-                }
-                wave_sync();
-                if (anyrun) {
-                    pass(false);
-        #pragma unroll
-                    for (int q = 0; q < kMaxSeg; ++q)
-                        if (q < nseg && CTL[q].on) lastt[q] = tr[q];
-                }
-                // back-trace of every segment with pending results (lane 0 of the segment)
-                bool hasq[kMaxSeg] = {false, false, false, false};
-    #pragma unroll
-                for (int q = 0; q < kMaxSeg; ++q)
-                    if (q < nseg) hasq[q] = __any(pending && sj == q);
-                const bool tracer = seg_live && ll == 0 && hasq[sg];
-                if (tracer) {
-                    uint32_t words[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-                    uint32_t rmask = 0;
-                    int b = N;
-                    bool ok = true;
-                    for (int s = PP - 1; s >= 0; --s) {
-                        const int k = b - rl32(blo, s);
-                        const int a = ARG[rl32(woff, s) + k];
-                        if (a >= b) {
-                            ok = false;
-                            break;
-                        }
-                        words[s >> 2] |= (uint32_t)(b - a) << (8 * (s & 3));
-                        if (a < A0B[rl32(woff, s) + k]) rmask |= 1u << s;
-                        b = a;
-                    }
-                    ok = ok && b == 0;
-                    for (int w = 0; w < 8; ++w) CTL[sg].bt[w] = words[w];
-                    CTL[sg].rmask = rmask;
-                    CTL[sg].ok = ok ? 1u : 0u;
-                }
-                wave_sync();
-                if (pending) {
-                    const int64_t mytr = sj == 0 ? tr[0] : sj == 1 ? tr[1] : sj == 2 ? tr[2] : tr[3];
-                    if (bt == mytr) {
-                        uint32_t words[8];
-                        for (int w = 0; w < 8; ++w) words[w] = CTL[sj].bt[w];
-                        if (CTL[sj].ok)
-                            write_result(out, HAPMOE_STATUS_OK, bs + dpc, bs - Bm * bmx, bmx, CTL[sj].rmask, words);
-                        else
-                            write_result(out, HAPMOE_STATUS_OVERFLOW, kInf, kInf, kInf, 0, zero_words);
-                        pending = false;
-                    }
-                }
-                wave_sync();
+            // ---- 5) results ----
+            if (member) {
+                if (pok)
+                    write_result(out, HAPMOE_STATUS_OK, bs + ki->dp_const, bs - Bm * bmx, bmx, prm, pw);
+                else
+                    write_result(out, HAPMOE_STATUS_OVERFLOW, kInf, kInf, kInf, 0, zero_words);
             }
 
             if (STATS) {
@@ -652,7 +616,6 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                     st_out[3] = 0;
                 }
             }
-            (void)last_parity;
             wave_sync();
         }
     }
