@@ -44,7 +44,7 @@ constexpr int kMaxSeg = 4;
 // AMIN, A0B, ARG [sum of band widths] bytes and two DP rows [max band width].
 struct DpLds {
     int np, kmax, ppmax, region;
-    int off_mw, off_ma0, off_ma1, off_moe, off_region, off_ctl, total;
+    int off_region, off_ctl, total;
 };
 
 __host__ __device__ inline int align16(int x) { return (x + 15) & ~15; }
@@ -52,7 +52,8 @@ __host__ __device__ inline int align16(int x) { return (x + 15) & ~15; }
 // Per-segment control block in LDS.
 struct SegCtl {
     int64_t t;        // threshold of the next pass
-    int64_t F, M;     // result of the last pass at b = N
+    int64_t F, M;     // result of the last pass at b = N: stage sum, largest stage
+    int64_t G;        // min-max value of the fused pass
     int32_t on;       // the segment takes part in the next pass
     int32_t pad;
     uint32_t bt[8];   // back-trace: n_i bytes
@@ -60,20 +61,26 @@ struct SegCtl {
 };
 
 
+// Bytes of the memory prefix sums (W, A0, A1 as int64, MoE count as int32).
+__host__ __device__ inline int mem_bytes(int n_layers)
+{
+    const int w = n_layers + 1;
+    return 3 * align16(w * 8) + align16(w * 4);
+}
+
 DpLds dp_lds(int n_layers, int kmax, int ppmax)
 {
     DpLds S;
     S.np = (n_layers + 1 + 15) & ~15;
     S.kmax = kmax;
     S.ppmax = ppmax;
-    const int np = S.np, w = n_layers + 1;
-    S.off_mw = kmax * np * 16;
-    S.off_ma0 = S.off_mw + np * 8;
-    S.off_ma1 = S.off_ma0 + np * 8;
-    S.off_moe = S.off_ma1 + np * 8;
-    S.off_region = align16(S.off_moe + np * 4);
-    // one segment always fits: every stage band is at most N + 1 wide
-    S.region = align16(3 * ppmax * w) + 2 * align16(w * 8) + 64;
+    const int w = n_layers + 1;
+    S.off_region = kmax * S.np * 16;
+    // one segment always fits: every stage band is at most N + 1 wide; the
+    // memory prefix sums share the space of the DP rows (they are only read
+    // before the first DP pass of a batch)
+    const int rows = 2 * align16(w * 16), mb = mem_bytes(n_layers);
+    S.region = align16(3 * ppmax * w) + (rows > mb ? rows : mb) + 64;
     S.off_ctl = S.off_region + S.region;
     S.total = S.off_ctl + kMaxSeg * (int)sizeof(SegCtl);
     return S;
@@ -203,10 +210,6 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
     const uint32_t zero_words[8] = {0, 0, 0, 0, 0, 0, 0, 0};
 
     I64x2 *TM = reinterpret_cast<I64x2 *>(smem);
-    int64_t *MW = reinterpret_cast<int64_t *>(smem + S.off_mw);
-    int64_t *MA0 = reinterpret_cast<int64_t *>(smem + S.off_ma0);
-    int64_t *MA1 = reinterpret_cast<int64_t *>(smem + S.off_ma1);
-    int32_t *MOE = reinterpret_cast<int32_t *>(smem + S.off_moe);
     unsigned char *REG = smem + S.off_region;
     SegCtl *CTL = reinterpret_cast<SegCtl *>(smem + S.off_ctl);
 
@@ -275,8 +278,15 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
         const int sumwd = rl32(woff, 63) + rl32(wd, 63);
         const int maxw = wave_max32(wd);
         const bool feasible_shape = totlo <= N && tothi >= N && !__any(lane < PP && wd == 0);
-        const int seg_bytes = align16(3 * sumwd) + 2 * align16(maxw * 8);
-        if (nslot > S.kmax || PP > S.ppmax || !feasible_shape || seg_bytes > S.region) {
+        // region: [per-segment AMIN | A0B | ARG] [per-segment DP rows  or  memory prefixes]
+        const int arr_bytes = align16(3 * sumwd), row_bytes = 2 * align16(maxw * 16);
+        const int mbytes = mem_bytes(N);
+        int smax = 0;
+        for (int q = 1; q <= kMaxSeg; ++q) {
+            const int need = q * arr_bytes + (q * row_bytes > mbytes ? q * row_bytes : mbytes);
+            if (need <= S.region) smax = q;
+        }
+        if (nslot > S.kmax || PP > S.ppmax || !feasible_shape || smax == 0) {
             if (inr) {
                 const int st = feasible_shape ? HAPMOE_STATUS_OVERFLOW : HAPMOE_STATUS_INFEASIBLE;
                 write_result(out, st, kInf, kInf, kInf, 0, zero_words);
@@ -298,20 +308,14 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                 for (int b = lane; b <= N; b += 64) TM[k * NP + b] = I64x2{src[b], src[np + b]};
                 ++k;
             }
-            for (int b = lane; b <= N; b += 64) {
-                MW[b] = mem[b];
-                MA0[b] = mem[np + b];
-                MA1[b] = mem[2 * np + b];
-                MOE[b] = (int32_t)mem[3 * np + b];
-            }
         }
         wave_sync();
 
-        // segments per batch: as many as the region holds, at most 4
-        int smax = S.region / seg_bytes;
-        smax = smax > kMaxSeg ? kMaxSeg : smax;
-        const int off_amin = 0, off_a0 = sumwd, off_arg = 2 * sumwd;
-        const int off_fm0 = align16(3 * sumwd), off_fm1 = off_fm0 + align16(maxw * 8);
+        const int off_rows = smax * arr_bytes;   // start of the DP rows / memory prefixes
+        int64_t *MW = reinterpret_cast<int64_t *>(REG + off_rows);
+        int64_t *MA0 = MW + align16((N + 1) * 8) / 8;
+        int64_t *MA1 = MA0 + align16((N + 1) * 8) / 8;
+        int32_t *MOE = reinterpret_cast<int32_t *>(MA1 + align16((N + 1) * 8) / 8);
 
         for (int g0 = 0; g0 < ng; g0 += smax) {
             const int nact = (ng - g0) < smax ? (ng - g0) : smax;
@@ -323,12 +327,23 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
             for (int k = 0; k < g0 + sg && rest; ++k) rest &= rest - 1;
             const bool seg_live = sg < nact && rest != 0;
             const int vseg = seg_live ? __ffsll((unsigned long long)rest) - 1 : 1;
-            unsigned char *R = REG + (seg_live ? sg : 0) * seg_bytes;
-            uint8_t *AMIN = R + off_amin;
-            uint8_t *A0B = R + off_a0;
-            uint8_t *ARG = R + off_arg;
-            int64_t *const FM0 = reinterpret_cast<int64_t *>(R + off_fm0);
-            int64_t *const FM1 = reinterpret_cast<int64_t *>(R + off_fm1);
+            const int segi = seg_live ? sg : 0;
+            uint8_t *AMIN = REG + segi * arr_bytes;
+            uint8_t *A0B = AMIN + sumwd;
+            uint8_t *ARG = AMIN + 2 * sumwd;
+            unsigned char *RW = REG + off_rows + segi * row_bytes;
+            int64_t *const FM0 = reinterpret_cast<int64_t *>(RW);
+            int64_t *const FM1 = reinterpret_cast<int64_t *>(RW + row_bytes / 2);
+            I64x2 *const FG0 = reinterpret_cast<I64x2 *>(RW);   // fused pass: {sum, min-max}
+            I64x2 *const FG1 = reinterpret_cast<I64x2 *>(RW + row_bytes / 2);
+            // memory prefix sums for the feasibility scan (they share the DP-row space)
+            for (int b = lane; b <= N; b += 64) {
+                MW[b] = mem[b];
+                MA0[b] = mem[np + b];
+                MA1[b] = mem[2 * np + b];
+                MOE[b] = (int32_t)mem[3 * np + b];
+            }
+            wave_sync();
             // candidate view: lane j's segment in this batch (-1: not in this batch)
             const int sj = (gj >= g0 && gj < g0 + nact) ? gj - g0 : -1;
             bool member = inr && sj >= 0;
@@ -380,16 +395,21 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
 
             int passes = 0, relax = 0;
 
-            // One DP pass of every segment with CTL.on set, at its CTL.t.
-            // minimax: F = least possible largest stage.  Otherwise F = least
-            // stage sum with all stages <= t (ties: smallest split point a);
-            // lane 0 of the segment then back-traces the partition and its
-            // largest stage M into the segment's control block.
-            auto pass = [&](bool minimax) {
+            // One DP pass of every segment with CTL.on set, at its CTL.t: F = least
+            // stage sum with all stages <= t (ties: smallest split point a); lane
+            // 0 of the segment then back-traces the partition and its largest
+            // stage M into the segment's control block.  The fused pass (t = inf)
+            // also carries the min-max row: G = least possible largest stage.
+            auto pass = [&](bool fused) {
                 const bool on = seg_live && CTL[sg].on != 0;
                 const int64_t t = seg_live ? CTL[sg].t : 0;
                 if (on) ++passes;
-                if (on && ll == 0) FM1[0] = 0;   // stage -1: layer 0 reached at cost 0
+                if (on && ll == 0) {   // stage -1: layer 0 reached at cost 0
+                    if (fused)
+                        FG1[0] = I64x2{0, 0};
+                    else
+                        FM1[0] = 0;
+                }
                 wave_sync();
                 for (int s = 0; s < PP; ++s) {
                     const int slot_s = rl32(slot, s), lo_s = rl32(lo, s);
@@ -399,6 +419,8 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                     const I64x2 *T = TM + slot_s * NP;
                     const int64_t *Fp = (s & 1) ? FM0 : FM1;
                     int64_t *Fc = (s & 1) ? FM1 : FM0;
+                    const I64x2 *Gp = (s & 1) ? FG0 : FG1;
+                    I64x2 *Gc = (s & 1) ? FG1 : FG0;
                     for (int k = ll; k < wd_s; k += W) {
                         if (!on) break;
                         const int b = blo_s + k;
@@ -406,7 +428,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                         const int ahi = (b - lo_s) < phi ? (b - lo_s) : phi;
                         const I64x2 tb = T[b];
                         const int64_t k0 = tb.x + p2p_s, k1 = tb.y + p2p_s;
-                        int64_t best = kBig;
+                        int64_t best = kBig, gbest = kBig;
                         int ba = 255;
                         int trips = 0;
                         if (amin <= ahi) {
@@ -416,18 +438,22 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                             // a - 1 are issued before a is evaluated (clamped index).
                             int a = ahi;
                             I64x2 ta = T[a];
-                            int64_t f = Fp[a - plo];
+                            I64x2 f = fused ? Gp[a - plo] : I64x2{Fp[a - plo], 0};
                             for (;;) {
                                 const int an = a > amin ? a - 1 : a;
                                 const I64x2 ta_n = T[an];
-                                const int64_t f_n = Fp[an - plo];
+                                const I64x2 f_n = fused ? Gp[an - plo] : I64x2{Fp[an - plo], 0};
                                 const int64_t cst = a < a0 ? k1 - ta.y : k0 - ta.x;
                                 if (cst > t) break;
                                 ++trips;
-                                const int64_t v = minimax ? (f > cst ? f : cst) : f + cst;
+                                const int64_t v = f.x + cst;
                                 const bool le = v <= best;
                                 best = le ? v : best;
                                 ba = le ? a : ba;
+                                if (fused) {
+                                    const int64_t g = f.y > cst ? f.y : cst;
+                                    gbest = g < gbest ? g : gbest;
+                                }
                                 if (a == amin) break;
                                 a = an;
                                 ta = ta_n;
@@ -435,42 +461,45 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                             }
                         }
                         if (STATS) relax += trips;
-                        Fc[k] = best;
-                        if (!minimax) ARG[off_s + k] = (uint8_t)ba;
+                        if (fused)
+                            Gc[k] = I64x2{best, gbest};
+                        else
+                            Fc[k] = best;
+                        ARG[off_s + k] = (uint8_t)ba;
                     }
                     wave_sync();
                 }
-                const int64_t fin = ((PP - 1) & 1) ? FM1[0] : FM0[0];
+                const bool odd = ((PP - 1) & 1) != 0;
+                const int64_t fin = fused ? (odd ? FG1[0].x : FG0[0].x) : (odd ? FM1[0] : FM0[0]);
                 if (on && ll == 0) {
                     CTL[sg].F = fin;
-                    if (!minimax) {
-                        uint32_t words[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-                        uint32_t rmask = 0;
-                        int64_t m = 0;
-                        int b = N;
-                        bool ok = fin < kBig;
-                        for (int s = PP - 1; s >= 0 && ok; --s) {
-                            const int k = b - rl32(blo, s), off_s = rl32(woff, s);
-                            const int a = ARG[off_s + k];
-                            if (a >= b) {
-                                ok = false;
-                                break;
-                            }
-                            const I64x2 *T = TM + rl32(slot, s) * NP;
-                            const I64x2 ta = T[a], tb = T[b];
-                            const bool r1 = a < A0B[off_s + k];
-                            const int64_t c = (r1 ? tb.y - ta.y : tb.x - ta.x) + rl64(p2p, s);
-                            m = c > m ? c : m;
-                            words[s >> 2] |= (uint32_t)(b - a) << (8 * (s & 3));
-                            if (r1) rmask |= 1u << s;
-                            b = a;
+                    if (fused) CTL[sg].G = odd ? FG1[0].y : FG0[0].y;
+                    uint32_t words[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+                    uint32_t rmask = 0;
+                    int64_t m = 0;
+                    int b = N;
+                    bool ok = fin < kBig;
+                    for (int s = PP - 1; s >= 0 && ok; --s) {
+                        const int k = b - rl32(blo, s), off_s = rl32(woff, s);
+                        const int a = ARG[off_s + k];
+                        if (a >= b) {
+                            ok = false;
+                            break;
                         }
-                        ok = ok && b == 0;
-                        CTL[sg].M = m;
-                        for (int w = 0; w < 8; ++w) CTL[sg].bt[w] = words[w];
-                        CTL[sg].rmask = rmask;
-                        CTL[sg].ok = ok ? 1u : 0u;
+                        const I64x2 *T = TM + rl32(slot, s) * NP;
+                        const I64x2 ta = T[a], tb = T[b];
+                        const bool r1 = a < A0B[off_s + k];
+                        const int64_t c = (r1 ? tb.y - ta.y : tb.x - ta.x) + rl64(p2p, s);
+                        m = c > m ? c : m;
+                        words[s >> 2] |= (uint32_t)(b - a) << (8 * (s & 3));
+                        if (r1) rmask |= 1u << s;
+                        b = a;
                     }
+                    ok = ok && b == 0;
+                    CTL[sg].M = m;
+                    for (int w = 0; w < 8; ++w) CTL[sg].bt[w] = words[w];
+                    CTL[sg].rmask = rmask;
+                    CTL[sg].ok = ok ? 1u : 0u;
                 }
                 wave_sync();
             };
@@ -499,33 +528,25 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                 }
             };
 
-            // ---- 1) bottleneck: min-max pass ----
+            // ---- 1) least sum without a threshold, fused with the min-max pass ----
 #pragma unroll
             for (int q = 0; q < kMaxSeg; ++q)
                 if (q < nseg) set_ctl(q, q < nact, kInf);
             wave_sync();
             pass(true);
-            const int64_t tbot = member ? CTL[sj].F : kBig;
+            const int64_t tbot = member ? CTL[sj].G : kBig;
             if (member && tbot >= kBig) {
                 write_result(out, HAPMOE_STATUS_INFEASIBLE, kInf, kInf, kInf, 0, zero_words);
                 member = false;
             }
-            int64_t segF[kMaxSeg] = {kBig, kBig, kBig, kBig};
+            int64_t segF[kMaxSeg] = {kBig, kBig, kBig, kBig};   // t_bot of each segment
             bool segok[kMaxSeg] = {false, false, false, false};
 #pragma unroll
             for (int q = 0; q < kMaxSeg; ++q) {
                 if (q >= nact) continue;
-                segF[q] = CTL[q].F;
+                segF[q] = CTL[q].G;
                 segok[q] = segF[q] < kBig;
             }
-            wave_sync();
-
-            // ---- 2) least sum without a threshold ----
-#pragma unroll
-            for (int q = 0; q < kMaxSeg; ++q)
-                if (q < nseg) set_ctl(q, segok[q], kInf);
-            wave_sync();
-            pass(false);
             int64_t F1 = 0, M1 = 0;
             if (member) {
                 F1 = CTL[sj].F;
