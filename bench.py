@@ -87,6 +87,7 @@ def main():
     st = pl.stats()
     relax = int(st[:, 1].astype(np.int64).sum())
     evals = int(st[:, 2].astype(np.int64).sum())
+    slots = int(st[:, 3].astype(np.int64).sum())
     passes = st[:, 0]
     feasible = int((pl.results()["status"] == 0).sum())
 
@@ -136,6 +137,7 @@ def main():
                      "relaxations_per_launch": relax, "evaluations_per_launch": evals},
         "kernels_ms": ms,
         "dp_cell_updates_per_s": relax / dp_s,
+        "relaxation_lane_utilisation": relax / max(slots, 1),
         "threshold_passes_per_candidate": {"mean": float(passes.mean()), "max": int(passes.max())},
         "best_plan": {"instance": plan["instance"], "objective_ns": plan["objective"],
                       "config": plan["config"], "order": plan["order"], "B": plan["n_micro"],

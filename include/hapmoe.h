@@ -226,9 +226,11 @@ int32_t hapmoe_stage_dp_ws_bytes(const hapmoe_problem *p, int64_t *bytes);
  * smallest split point at each backtrace step (from the last stage).  Writes
  * d_res[0 .. count).  d_stats (may be NULL) receives per candidate four
  * int32: threshold passes of its sweep, DP relaxations, split-point
- * evaluations of the feasibility scan, 0.  Candidates of one (pi, ordering)
- * whose B gives the same min(B, PP) share one sweep; its relaxations and
- * evaluations are counted once, on the first of them.  d_ws
+ * evaluations of the feasibility scan, and the lane slots the relaxation
+ * loops issued for the sweep (relaxations / slots is the SIMD-lane
+ * utilisation of those loops).  Candidates of one (pi, ordering) whose B
+ * gives the same min(B, PP) share one sweep; its relaxations, evaluations
+ * and slots are counted once, on the first of them.  d_ws
  * (hapmoe_stage_dp_ws_bytes)
  * holds the kernel's work queue: calls that may overlap need their own d_ws.
  * Asynchronous. */

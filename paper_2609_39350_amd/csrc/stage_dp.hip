@@ -37,6 +37,11 @@ namespace hapmoe {
 namespace {
 
 constexpr int64_t kBig = int64_t(1) << 62;   // "no partition" inside the DP (sums stay far from overflow)
+constexpr int64_t kNegInf = INT64_MIN;        // a threshold no stage cost meets
+#ifndef HAPMOE_RELAX_UNROLL
+#define HAPMOE_RELAX_UNROLL 2
+#endif
+constexpr int kRelaxUnroll = HAPMOE_RELAX_UNROLL;   // split points per relaxation-loop trip
 constexpr int kMaxSeg = 4;
 
 // LDS of one wave: TM [kmax][np] {T0, T1} | memory prefixes | per-segment
@@ -95,31 +100,84 @@ __device__ inline int64_t rl64(int64_t v, int src)
     return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
 }
 
-__device__ inline uint64_t wave_or64(uint64_t x)
+// Wave-wide reductions for a full wave (all 64 lanes active).  Each 16-lane
+// row is all-reduced with DPP row rotations (register-to-register, no LDS round
+// trip), then the four row results are combined from lanes 0/16/32/48 in scalar
+// registers, so the result is wave-uniform.
+template <int CTRL>
+__device__ inline int dpp32(int x)
 {
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) x |= __shfl_xor(x, d, 64);
-    return x;
+    return __builtin_amdgcn_update_dpp(0, x, CTRL, 0xf, 0xf, false);
+}
+
+template <int CTRL>
+__device__ inline int64_t dpp64(int64_t x)
+{
+    const int lo = dpp32<CTRL>((int)(uint32_t)(uint64_t)x);
+    const int hi = dpp32<CTRL>((int)(uint32_t)((uint64_t)x >> 32));
+    return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+constexpr int kRowRor8 = 0x128, kRowRor4 = 0x124, kRowRor2 = 0x122, kRowRor1 = 0x121;
+
+__device__ inline int64_t rows_max64(int64_t x)
+{
+    int64_t y = dpp64<kRowRor8>(x);
+    x = y > x ? y : x;
+    y = dpp64<kRowRor4>(x);
+    x = y > x ? y : x;
+    y = dpp64<kRowRor2>(x);
+    x = y > x ? y : x;
+    y = dpp64<kRowRor1>(x);
+    return y > x ? y : x;
 }
 
 __device__ inline int64_t wave_max64(int64_t x)
 {
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const int64_t y = __shfl_xor(x, d, 64);
-        x = y > x ? y : x;
-    }
-    return x;
+    x = rows_max64(x);
+    const int64_t r0 = rl64(x, 0), r1 = rl64(x, 16), r2 = rl64(x, 32), r3 = rl64(x, 48);
+    const int64_t a = r0 > r1 ? r0 : r1, b = r2 > r3 ? r2 : r3;
+    return a > b ? a : b;
 }
 
-__device__ inline int64_t wave_min64(int64_t x)
+__device__ inline int wave_max32(int x)
 {
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const int64_t y = __shfl_xor(x, d, 64);
-        x = y < x ? y : x;
-    }
-    return x;
+    int y = dpp32<kRowRor8>(x);
+    x = y > x ? y : x;
+    y = dpp32<kRowRor4>(x);
+    x = y > x ? y : x;
+    y = dpp32<kRowRor2>(x);
+    x = y > x ? y : x;
+    y = dpp32<kRowRor1>(x);
+    x = y > x ? y : x;
+    const int r0 = rl32(x, 0), r1 = rl32(x, 16), r2 = rl32(x, 32), r3 = rl32(x, 48);
+    const int a = r0 > r1 ? r0 : r1, b = r2 > r3 ? r2 : r3;
+    return a > b ? a : b;
+}
+
+__device__ inline int wave_sum32(int x)
+{
+    x += dpp32<kRowRor8>(x);
+    x += dpp32<kRowRor4>(x);
+    x += dpp32<kRowRor2>(x);
+    x += dpp32<kRowRor1>(x);
+    return rl32(x, 0) + rl32(x, 16) + rl32(x, 32) + rl32(x, 48);
+}
+
+__device__ inline uint64_t wave_or64(uint64_t x)
+{
+    int lo = (int)(uint32_t)x, hi = (int)(uint32_t)(x >> 32);
+    lo |= dpp32<kRowRor8>(lo);
+    hi |= dpp32<kRowRor8>(hi);
+    lo |= dpp32<kRowRor4>(lo);
+    hi |= dpp32<kRowRor4>(hi);
+    lo |= dpp32<kRowRor2>(lo);
+    hi |= dpp32<kRowRor2>(hi);
+    lo |= dpp32<kRowRor1>(lo);
+    hi |= dpp32<kRowRor1>(hi);
+    const uint32_t l = (uint32_t)(rl32(lo, 0) | rl32(lo, 16) | rl32(lo, 32) | rl32(lo, 48));
+    const uint32_t h = (uint32_t)(rl32(hi, 0) | rl32(hi, 16) | rl32(hi, 32) | rl32(hi, 48));
+    return ((uint64_t)h << 32) | l;
 }
 
 __device__ inline int wave_incl_scan(int x, int lane)
@@ -129,23 +187,6 @@ __device__ inline int wave_incl_scan(int x, int lane)
         const int y = __shfl_up(x, d, 64);
         if (lane >= d) x += y;
     }
-    return x;
-}
-
-__device__ inline int wave_max32(int x)
-{
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const int y = __shfl_xor(x, d, 64);
-        x = y > x ? y : x;
-    }
-    return x;
-}
-
-__device__ inline int wave_sum32(int x)
-{
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) x += __shfl_xor(x, d, 64);
     return x;
 }
 
@@ -266,6 +307,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
         const int bdiff = inner && ((bp >> 2) != (bp & 3));
         const int mixed = __popc(mask) > 1;
         const int64_t X = pi->x_bytes, eta_tbar = (int64_t)H.eta_prune * pi->tbar;
+        const bool prune_het = H.prune_hetero != 0, recomp = H.allow_recompute != 0;
         // band [blo, bhi] of end layers stage s can reach under the windows
         const int cumlo = wave_incl_scan(lane < PP ? lo : 0, lane);
         const int cumhi = wave_incl_scan(lane < PP ? hi : 0, lane);
@@ -362,38 +404,59 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                 const int64_t ms = (int64_t)((PP - s) < vseg ? (PP - s) : vseg);   // 1F1B stored micro-batches
                 const int64_t *CM = mixed_s ? time + ((int64_t)(mask_s - 1) * 3 + 2) * np : nullptr;
                 const int64_t hc_b = bdiff_s ? p2p_s : 0;
-                for (int k = ll; k < wd_s; k += W) {
-                    if (!seg_live) break;
-                    const int b = blo_s + k;
-                    int amin = 255, a0 = 255;
+                const int rounds = (wd_s + W - 1) / W;   // wave-uniform
+                for (int r = 0; r < rounds; ++r) {
+                    const int k = ll + r * W;
+                    const bool act = seg_live && k < wd_s;
+                    const int b = blo_s + (act ? k : 0);
                     const int ahi = (b - lo_s) < phi ? (b - lo_s) : phi;
                     const int alo = (b - hi_s) > plo ? (b - hi_s) : plo;
-                    if (ahi >= alo) {
-                        // the feasible split points form a suffix [amin, ahi] (memory and
-                        // pruning 3 grow with the segment), so both bounds are minima over
-                        // independent evaluations -- no early exit, loads pipeline freely
-                        amin = a0 = ahi + 1;
-                        const int64_t wb = MW[b], a0b = MA0[b], a1b = MA1[b];
-                        const int mb = MOE[b];
-                        const int64_t cmb = CM ? CM[b] : 0;
-                        for (int a = alo; a <= ahi; ++a) {
-                            if (STATS) ++evals;
-                            const int64_t xb = (mb - MOE[a]) > 0 ? X : 0;
-                            const int64_t dw = wb - MW[a];
-                            const bool ok3 = !H.prune_hetero || (CM ? cmb - CM[a] : 0) + hc_b <= eta_tbar;
-                            const bool f0 = ok3 && dw + ms * (a0b - MA0[a]) + xb <= cap_s;
-                            const bool f1 = ok3 && H.allow_recompute && dw + ms * (a1b - MA1[a]) + xb <= cap_s;
-                            a0 = f0 && a < a0 ? a : a0;
-                            amin = (f0 || f1) && a < amin ? a : amin;
-                        }
+                    const bool has = act && ahi >= alo;
+                    // the feasible split points form a suffix [amin, ahi] of the window
+                    // (memory and pruning 3 only grow with the segment), and so do those
+                    // feasible without recomputation, [a0, ahi]: scanning a upwards, the
+                    // first hit of each is its bound, and a lane is done at its first
+                    // split point that fits without recomputation
+                    int amin = has ? ahi + 1 : 255, a0 = amin;
+                    const int64_t wb = MW[b], a0b = MA0[b], a1b = MA1[b];
+                    const int mb = MOE[b];
+                    const int64_t cmb = CM ? CM[b] : 0;
+                    const int aend = has ? ahi : plo;
+                    bool open = has;
+                    // one split point's test, gated by the lane still being open
+                    auto test = [&](int a, int64_t mwa, int64_t ma0, int64_t ma1, int moea, int64_t cma) {
+                        const int64_t xb = (mb - moea) > 0 ? X : 0;
+                        const int64_t base = wb - mwa + xb;
+                        const bool ok3 = !prune_het | (cmb - cma + hc_b <= eta_tbar);
+                        const bool f0 = open & ok3 & (base + ms * (a0b - ma0) <= cap_s);
+                        const bool f1 = open & ok3 & recomp & (base + ms * (a1b - ma1) <= cap_s);
+                        if (STATS) evals += open ? 1 : 0;
+                        amin = ((f0 | f1) & (a < amin)) ? a : amin;
+                        a0 = f0 ? a : a0;
+                        open = open & !f0 & (a < aend);
+                    };
+                    // two split points per trip, all loads issued before either test
+                    int a = has ? alo : plo;
+                    for (;;) {   // a lane closes at aend at the latest
+                        const int a2 = a < aend ? a + 1 : a;
+                        const int64_t w1 = MW[a], w2 = MW[a2], p1 = MA0[a], p2 = MA0[a2];
+                        const int64_t q1 = MA1[a], q2 = MA1[a2];
+                        const int m1 = MOE[a], m2 = MOE[a2];
+                        const int64_t c1 = CM ? CM[a] : 0, c2 = CM ? CM[a2] : 0;
+                        test(a, w1, p1, q1, m1, c1);
+                        test(a2, w2, p2, q2, m2, c2);
+                        if (__builtin_amdgcn_ballot_w64(open) == 0) break;
+                        a = a2 < aend ? a2 + 1 : a2;   // stays inside the window
                     }
-                    AMIN[off_s + k] = (uint8_t)amin;
-                    A0B[off_s + k] = (uint8_t)a0;
+                    if (act) {
+                        AMIN[off_s + k] = (uint8_t)amin;
+                        A0B[off_s + k] = (uint8_t)a0;
+                    }
                 }
             }
             wave_sync();
 
-            int passes = 0, relax = 0;
+            int passes = 0, relax = 0, slots = 0;
 
             // One DP pass of every segment with CTL.on set, at its CTL.t: F = least
             // stage sum with all stages <= t (ties: smallest split point a); lane
@@ -421,51 +484,74 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                     int64_t *Fc = (s & 1) ? FM1 : FM0;
                     const I64x2 *Gp = (s & 1) ? FG0 : FG1;
                     I64x2 *Gc = (s & 1) ? FG1 : FG0;
-                    for (int k = ll; k < wd_s; k += W) {
-                        if (!on) break;
-                        const int b = blo_s + k;
-                        const int amin = AMIN[off_s + k], a0 = A0B[off_s + k];
-                        const int ahi = (b - lo_s) < phi ? (b - lo_s) : phi;
+                    // wave-uniform rounds and split-point loop: a lane with less to do
+                    // runs masked (clamped, in-range loads; predicated stores only)
+                    const int rounds = (wd_s + W - 1) / W;
+                    for (int r = 0; r < rounds; ++r) {
+                        const int k = ll + r * W;
+                        const bool act = on && k < wd_s;
+                        const int kk = act ? k : 0;
+                        const int b = blo_s + kk;
+                        const int amin0 = AMIN[off_s + kk], a0 = A0B[off_s + kk];
+                        const int ahi0 = (b - lo_s) < phi ? (b - lo_s) : phi;
+                        const bool has = act && amin0 <= ahi0;
+                        int left = has ? ahi0 - amin0 + 1 : 0;   // split points not yet relaxed
+                        // a lane without a window reads split point plo under a
+                        // threshold no stage cost meets
+                        const int amin = has ? amin0 : plo;
+                        const int64_t tl = has ? t : kNegInf;
                         const I64x2 tb = T[b];
                         const int64_t k0 = tb.x + p2p_s, k1 = tb.y + p2p_s;
                         int64_t best = kBig, gbest = kBig;
                         int ba = 255;
-                        int trips = 0;
-                        if (amin <= ahi) {
-                            // a runs downwards: the stage cost only grows as the segment
-                            // grows, so the first cost above t ends the scan; "<=" keeps
-                            // the smallest split point among equal values.  The loads of
-                            // a - 1 are issued before a is evaluated (clamped index).
-                            int a = ahi;
-                            I64x2 ta = T[a];
-                            I64x2 f = fused ? Gp[a - plo] : I64x2{Fp[a - plo], 0};
-                            for (;;) {
-                                const int an = a > amin ? a - 1 : a;
-                                const I64x2 ta_n = T[an];
-                                const I64x2 f_n = fused ? Gp[an - plo] : I64x2{Fp[an - plo], 0};
-                                const int64_t cst = a < a0 ? k1 - ta.y : k0 - ta.x;
-                                if (cst > t) break;
-                                ++trips;
-                                const int64_t v = f.x + cst;
-                                const bool le = v <= best;
-                                best = le ? v : best;
-                                ba = le ? a : ba;
-                                if (fused) {
-                                    const int64_t g = f.y > cst ? f.y : cst;
-                                    gbest = g < gbest ? g : gbest;
-                                }
-                                if (a == amin) break;
-                                a = an;
-                                ta = ta_n;
-                                f = f_n;
+                        // a runs downwards from b - lo and then stays at amin: repeating
+                        // the last split point changes nothing ("<=" keeps the smallest
+                        // split point among equal values, which is the current one)
+                        // kRelaxUnroll split points per trip: every load is issued before
+                        // the first use, one exit test per trip; the trip count is bounded
+                        // by the longest window, as a lane only goes on while a > amin
+                        int a = has ? ahi0 : plo;
+                        for (;;) {
+                            int au[kRelaxUnroll];
+                            I64x2 tu[kRelaxUnroll], fu[kRelaxUnroll];
+#pragma unroll
+                            for (int u = 0; u < kRelaxUnroll; ++u) {
+                                au[u] = u == 0 ? a : (au[u - 1] > amin ? au[u - 1] - 1 : au[u - 1]);
+                                tu[u] = T[au[u]];
+                                fu[u] = fused ? Gp[au[u] - plo] : I64x2{Fp[au[u] - plo], 0};
                             }
+                            bool ok = false;
+#pragma unroll
+                            for (int u = 0; u < kRelaxUnroll; ++u) {
+                                const int64_t cst = au[u] < a0 ? k1 - tu[u].y : k0 - tu[u].x;
+                                ok = cst <= tl;
+                                const int64_t v = fu[u].x + cst;
+                                const bool le = ok && v <= best;
+                                best = le ? v : best;
+                                ba = le ? au[u] : ba;
+                                if (fused) {
+                                    const int64_t g = fu[u].y > cst ? fu[u].y : cst;
+                                    gbest = ok && g < gbest ? g : gbest;
+                                }
+                                if (STATS) {
+                                    relax += ok && left > 0 ? 1 : 0;
+                                    slots += on ? 1 : 0;
+                                    --left;
+                                }
+                            }
+                            // the stage cost only grows as a falls: the wave is done once
+                            // no lane is both under its threshold and short of amin
+                            const int al = au[kRelaxUnroll - 1];
+                            if (__builtin_amdgcn_ballot_w64(ok && al > amin) == 0) break;
+                            a = al > amin ? al - 1 : al;
                         }
-                        if (STATS) relax += trips;
-                        if (fused)
-                            Gc[k] = I64x2{best, gbest};
-                        else
-                            Fc[k] = best;
-                        ARG[off_s + k] = (uint8_t)ba;
+                        if (act) {
+                            if (fused)
+                                Gc[k] = I64x2{best, gbest};
+                            else
+                                Fc[k] = best;
+                            ARG[off_s + k] = (uint8_t)ba;
+                        }
                     }
                     wave_sync();
                 }
@@ -614,15 +700,18 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
             }
 
             if (STATS) {
-                // per segment: passes, relaxations, split-point evaluations; the
-                // shared work is counted once, on the group's first candidate in range
+                // per segment: passes, relaxations, split-point evaluations and the
+                // lane slots the relaxation loops issued while the segment took part;
+                // the shared work is counted once, on the group's first candidate in range
                 int rq[kMaxSeg] = {0, 0, 0, 0}, eq[kMaxSeg] = {0, 0, 0, 0}, pq[kMaxSeg] = {0, 0, 0, 0};
+                int sq[kMaxSeg] = {0, 0, 0, 0};
                 int lead[kMaxSeg] = {-1, -1, -1, -1};
     #pragma unroll
                 for (int q = 0; q < kMaxSeg; ++q) {
                     if (q >= nseg) continue;
                     rq[q] = wave_sum32(sg == q ? relax : 0);
                     eq[q] = wave_sum32(sg == q ? evals : 0);
+                    sq[q] = wave_sum32(sg == q ? slots : 0);
                     pq[q] = wave_max32(sg == q ? passes : 0);
                     lead[q] = __ffsll((unsigned long long)__ballot(inr && sj == q)) - 1;
                 }
@@ -631,10 +720,11 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                     const int r = sj == 0 ? rq[0] : sj == 1 ? rq[1] : sj == 2 ? rq[2] : rq[3];
                     const int e = sj == 0 ? eq[0] : sj == 1 ? eq[1] : sj == 2 ? eq[2] : eq[3];
                     const int l = sj == 0 ? lead[0] : sj == 1 ? lead[1] : sj == 2 ? lead[2] : lead[3];
+                    const int z = sj == 0 ? sq[0] : sj == 1 ? sq[1] : sj == 2 ? sq[2] : sq[3];
                     st_out[0] = p;
                     st_out[1] = lane == l ? r : 0;
                     st_out[2] = lane == l ? e : 0;
-                    st_out[3] = 0;
+                    st_out[3] = lane == l ? z : 0;
                 }
             }
             wave_sync();

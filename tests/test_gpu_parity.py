@@ -233,6 +233,8 @@ def test_stats_count_passes(torch):
     assert st.shape == (pl.n, 4)
     assert (st[ok, 0] >= 1).all() and (st[~ok, 0] <= 1).all()
     assert (st[:, 1] >= 0).all() and st[ok, 1].sum() > 0 and st[:, 2].sum() > 0
+    # lane slots of the relaxation loops bound the relaxations, group by group
+    assert (st[:, 3] >= st[:, 1]).all() and st[:, 3].sum() > st[:, 1].sum()
     # shared sweeps are counted once per (pi, ordering, min(B, PP)) group
     per_key = len(p["space"]["micro"])
     assert (st[:, 1].reshape(-1, per_key) > 0).sum(axis=1).max() <= per_key
