@@ -190,6 +190,22 @@ __device__ inline int wave_incl_scan(int x, int lane)
     return x;
 }
 
+// Bit m set for the m in [1, mtop] with m = floor(room / act): the largest count
+// of stored micro-batches whose activations still fit into room (none if room <
+// 0, act = 0 or the count exceeds mtop).  Exact: an fp32 estimate is corrected
+// by one integer step either way (its error is far below 1 for counts < 64).
+__device__ inline uint64_t cap_step(int64_t room, int64_t act, int mtop)
+{
+    if (room < act || act <= 0 || room >= act * 64) return 0;   // count 0, unbounded or >= 64
+    int m = (int)((float)room / (float)act);
+    m = m > 63 ? 63 : m;
+    if ((int64_t)m * act > room)
+        --m;
+    else if ((int64_t)(m + 1) * act <= room)
+        ++m;
+    return (m >= 1 && m <= mtop) ? (uint64_t(1) << m) : 0;
+}
+
 // The workgroup is a single wave whose LDS operations are processed in order;
 // this fence keeps the compiler from moving LDS accesses across it and waits
 // for the wave's outstanding LDS operations.
@@ -274,9 +290,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
             Bj = H.micro[lane];
             vj = Bj < PP ? Bj : PP;
         }
-        const uint64_t present = wave_or64(lane < nB ? (uint64_t(1) << vj) : 0);
-        const int ng = __popcll(present);
-        const int gj = __popcll(present & ((uint64_t(1) << vj) - 1));   // this lane's group
+        const uint64_t present = wave_or64(lane < nB ? (uint64_t(1) << vj) : 0);   // group values
         if (!__any(inr)) continue;
         hapmoe_dp_result *out = res + (inst - first);
         int32_t *st_out = STATS ? stats + 4 * (inst - first) : nullptr;
@@ -359,13 +373,75 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
         int64_t *MA1 = MA0 + align16((N + 1) * 8) / 8;
         int32_t *MOE = reinterpret_cast<int32_t *>(MA1 + align16((N + 1) * 8) / 8);
 
+        // ---- classes of groups with identical feasible windows ----
+        // Stage s of group v stores ms = min(PP - s, v) micro-batches.  For a fixed
+        // (s, b) and split point a, the largest ms that still fits is cap(a) =
+        // floor(room / activation), with and without recomputation, and it does
+        // not fall as a grows; so the window bounds of (s, b), as functions of ms,
+        // step exactly at the cap values of the window's split points.  Groups v <
+        // v' see identical windows everywhere -- hence identical DP results at any
+        // threshold -- unless some stage steps at an m in [v, min(PP - s, v') - 1]:
+        // collect every step m <= PP - s - 1 into brk, then a present group value
+        // opens a new class iff brk has a bit between the previous value and it.
+        for (int b = lane; b <= N; b += 64) {
+            MW[b] = mem[b];
+            MA0[b] = mem[np + b];
+            MA1[b] = mem[2 * np + b];
+            MOE[b] = (int32_t)mem[3 * np + b];
+        }
+        wave_sync();
+        uint64_t brk = 0;
+        int cls_evals = 0;
+        for (int s = 0; s + 1 < PP; ++s) {
+            const int mtop = PP - s - 1;   // steps that matter: m in [1, mtop]
+            const int lo_s = rl32(lo, s), hi_s = rl32(hi, s), mask_s = rl32(mask, s);
+            const int blo_s = rl32(blo, s), wd_s = rl32(wd, s);
+            const int plo = s ? rl32(blo, s - 1) : 0, phi = s ? rl32(bhi, s - 1) : 0;
+            const int mixed_s = rl32(mixed, s), bdiff_s = rl32(bdiff, s);
+            const int64_t cap_s = rl64(cap, s), p2p_s = rl64(p2p, s);
+            const int64_t *CM = mixed_s ? time + ((int64_t)(mask_s - 1) * 3 + 2) * np : nullptr;
+            const int64_t hc_b = bdiff_s ? p2p_s : 0;
+            for (int k = lane; k < wd_s; k += 64) {
+                const int b = blo_s + k;
+                const int ahi = (b - lo_s) < phi ? (b - lo_s) : phi;
+                const int alo = (b - hi_s) > plo ? (b - hi_s) : plo;
+                const int64_t wb = MW[b], a0b = MA0[b], a1b = MA1[b];
+                const int mb = MOE[b];
+                const int64_t cmb = CM ? CM[b] : 0;
+                for (int a = alo; a <= ahi; ++a) {
+                    if (STATS) ++cls_evals;
+                    const int64_t xb = (mb - MOE[a]) > 0 ? X : 0;
+                    const int64_t room = cap_s - (wb - MW[a] + xb);
+                    const bool ok3 = !prune_het || (CM ? cmb - CM[a] : 0) + hc_b <= eta_tbar;
+                    if (!ok3) continue;
+                    brk |= cap_step(room, a0b - MA0[a], mtop);
+                    if (recomp) brk |= cap_step(room, a1b - MA1[a], mtop);
+                }
+            }
+        }
+        brk = wave_or64(brk);
+        const int cls_sum = STATS ? wave_sum32(cls_evals) : 0;
+        uint64_t bnd;   // first group value of every class
+        {
+            const uint64_t below = present & ((uint64_t(1) << lane) - 1);
+            bool first = true;
+            if (below) {
+                const int vprev = 63 - __clzll((long long)below);
+                const uint64_t range = ((uint64_t(1) << lane) - 1) & ~((uint64_t(1) << vprev) - 1);
+                first = (brk & range) != 0;
+            }
+            bnd = __builtin_amdgcn_ballot_w64(((present >> lane) & 1) && first);
+        }
+        const int ng = __popcll(bnd);   // classes
+        const int gj = __popcll(bnd & ((uint64_t(2) << vj) - 1)) - 1;   // this lane's class
+
         for (int g0 = 0; g0 < ng; g0 += smax) {
             const int nact = (ng - g0) < smax ? (ng - g0) : smax;
             const int nseg = nact <= 1 ? 1 : (nact <= 2 ? 2 : 4);
             const int W = 64 / nseg;
             const int sg = lane / W, ll = lane % W;   // DP view: segment and lane in segment
             // group value of this lane's segment
-            uint64_t rest = present;
+            uint64_t rest = bnd;
             for (int k = 0; k < g0 + sg && rest; ++k) rest &= rest - 1;
             const bool seg_live = sg < nact && rest != 0;
             const int vseg = seg_live ? __ffsll((unsigned long long)rest) - 1 : 1;
@@ -392,7 +468,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
             // groups whose candidates are all outside [first, first + count) still run;
             // their results are simply not written.
 
-            int evals = 0;
+            int evals = (STATS && g0 == 0 && lane == 0) ? cls_sum : 0;   // classification counted once
             // ---- feasible split interval of every (stage, b in band), per segment ----
             // a in [AMIN, A0B) fits only with recomputation (r = 1), a in [A0B, b - lo] without.
             for (int s = 0; s < PP; ++s) {
