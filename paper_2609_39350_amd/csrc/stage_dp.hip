@@ -206,6 +206,34 @@ __device__ inline uint64_t cap_step(int64_t room, int64_t act, int mtop)
     return (m >= 1 && m <= mtop) ? (uint64_t(1) << m) : 0;
 }
 
+// Entry e of a stage's (segment, end layer) list: segment q = e / wd and
+// k = e % wd.  The fp32 quotient is off by at most one for e < 2^10 and is
+// corrected by one integer step.
+__device__ inline void split_entry(int e, int wd, float inv_wd, int &q, int &k)
+{
+    q = (int)((float)e * inv_wd);
+    if (q * wd > e)
+        --q;
+    else if ((q + 1) * wd <= e)
+        ++q;
+    k = e - q * wd;
+}
+
+// Per-segment values held in registers, selected / updated without dynamic
+// register indexing.
+__device__ inline int sel4(const int (&v)[4], int q)
+{
+    return q == 0 ? v[0] : q == 1 ? v[1] : q == 2 ? v[2] : v[3];
+}
+
+__device__ inline void add4(int (&v)[4], int q, int x)
+{
+    v[0] += q == 0 ? x : 0;
+    v[1] += q == 1 ? x : 0;
+    v[2] += q == 2 ? x : 0;
+    v[3] += q == 3 ? x : 0;
+}
+
 // The workgroup is a single wave whose LDS operations are processed in order;
 // this fence keeps the compiler from moving LDS accesses across it and waits
 // for the wave's outstanding LDS operations.
@@ -440,11 +468,20 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
             const int nseg = nact <= 1 ? 1 : (nact <= 2 ? 2 : 4);
             const int W = 64 / nseg;
             const int sg = lane / W, ll = lane % W;   // DP view: segment and lane in segment
-            // group value of this lane's segment
-            uint64_t rest = bnd;
-            for (int k = 0; k < g0 + sg && rest; ++k) rest &= rest - 1;
-            const bool seg_live = sg < nact && rest != 0;
-            const int vseg = seg_live ? __ffsll((unsigned long long)rest) - 1 : 1;
+            // class value (its smallest group value) of every segment of the batch
+            int vq[kMaxSeg] = {1, 1, 1, 1};
+            {
+                uint64_t rest = bnd;
+                for (int k = 0; k < g0 && rest; ++k) rest &= rest - 1;
+#pragma unroll
+                for (int q = 0; q < kMaxSeg; ++q) {
+                    if (q < nact && rest) {
+                        vq[q] = __ffsll((unsigned long long)rest) - 1;
+                        rest &= rest - 1;
+                    }
+                }
+            }
+            const bool seg_live = sg < nact;
             const int segi = seg_live ? sg : 0;
             uint8_t *AMIN = REG + segi * arr_bytes;
             uint8_t *A0B = AMIN + sumwd;
@@ -468,23 +505,30 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
             // groups whose candidates are all outside [first, first + count) still run;
             // their results are simply not written.
 
-            int evals = (STATS && g0 == 0 && lane == 0) ? cls_sum : 0;   // classification counted once
+            // split-point evaluations per segment (stats); the classification counts once
+            int evq[kMaxSeg] = {(STATS && g0 == 0 && lane == 0) ? cls_sum : 0, 0, 0, 0};
             // ---- feasible split interval of every (stage, b in band), per segment ----
             // a in [AMIN, A0B) fits only with recomputation (r = 1), a in [A0B, b - lo] without.
+            // The (segment, b) entries of a stage are spread over all 64 lanes.
             for (int s = 0; s < PP; ++s) {
                 const int lo_s = rl32(lo, s), hi_s = rl32(hi, s), mask_s = rl32(mask, s);
                 const int blo_s = rl32(blo, s), wd_s = rl32(wd, s), off_s = rl32(woff, s);
                 const int plo = s ? rl32(blo, s - 1) : 0, phi = s ? rl32(bhi, s - 1) : 0;
                 const int mixed_s = rl32(mixed, s), bdiff_s = rl32(bdiff, s);
                 const int64_t cap_s = rl64(cap, s), p2p_s = rl64(p2p, s);
-                const int64_t ms = (int64_t)((PP - s) < vseg ? (PP - s) : vseg);   // 1F1B stored micro-batches
                 const int64_t *CM = mixed_s ? time + ((int64_t)(mask_s - 1) * 3 + 2) * np : nullptr;
                 const int64_t hc_b = bdiff_s ? p2p_s : 0;
-                const int rounds = (wd_s + W - 1) / W;   // wave-uniform
-                for (int r = 0; r < rounds; ++r) {
-                    const int k = ll + r * W;
-                    const bool act = seg_live && k < wd_s;
-                    const int b = blo_s + (act ? k : 0);
+                const int total = nact * wd_s;
+                const float inv_wd = 1.0f / (float)wd_s;
+                for (int e0 = 0; e0 < total; e0 += 64) {   // wave-uniform
+                    const int e = e0 + lane;
+                    const bool act = e < total;
+                    int q, k;
+                    split_entry(act ? e : 0, wd_s, inv_wd, q, k);
+                    const int vs = sel4(vq, q);
+                    const int64_t ms = (int64_t)((PP - s) < vs ? (PP - s) : vs);   // 1F1B stored micro-batches
+                    uint8_t *const AMq = REG + q * arr_bytes;
+                    const int b = blo_s + k;
                     const int ahi = (b - lo_s) < phi ? (b - lo_s) : phi;
                     const int alo = (b - hi_s) > plo ? (b - hi_s) : plo;
                     const bool has = act && ahi >= alo;
@@ -506,7 +550,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                         const bool ok3 = !prune_het | (cmb - cma + hc_b <= eta_tbar);
                         const bool f0 = open & ok3 & (base + ms * (a0b - ma0) <= cap_s);
                         const bool f1 = open & ok3 & recomp & (base + ms * (a1b - ma1) <= cap_s);
-                        if (STATS) evals += open ? 1 : 0;
+                        if (STATS) add4(evq, q, open ? 1 : 0);
                         amin = ((f0 | f1) & (a < amin)) ? a : amin;
                         a0 = f0 ? a : a0;
                         open = open & !f0 & (a < aend);
@@ -525,14 +569,15 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                         a = a2 < aend ? a2 + 1 : a2;   // stays inside the window
                     }
                     if (act) {
-                        AMIN[off_s + k] = (uint8_t)amin;
-                        A0B[off_s + k] = (uint8_t)a0;
+                        AMq[off_s + k] = (uint8_t)amin;
+                        AMq[sumwd + off_s + k] = (uint8_t)a0;
                     }
                 }
             }
             wave_sync();
 
-            int passes = 0, relax = 0, slots = 0;
+            int passes = 0;
+            int relq[kMaxSeg] = {0, 0, 0, 0}, slq[kMaxSeg] = {0, 0, 0, 0};   // per segment (stats)
 
             // One DP pass of every segment with CTL.on set, at its CTL.t: F = least
             // stage sum with all stages <= t (ties: smallest split point a); lane
@@ -541,13 +586,22 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
             // also carries the min-max row: G = least possible largest stage.
             auto pass = [&](bool fused) {
                 const bool on = seg_live && CTL[sg].on != 0;
-                const int64_t t = seg_live ? CTL[sg].t : 0;
                 if (on) ++passes;
                 if (on && ll == 0) {   // stage -1: layer 0 reached at cost 0
                     if (fused)
                         FG1[0] = I64x2{0, 0};
                     else
                         FM1[0] = 0;
+                }
+                // the running segments, in order (wave-uniform)
+                int nq = 0, qmap = 0;
+#pragma unroll
+                for (int q = 0; q < kMaxSeg; ++q) {
+                    const int o = q < nseg ? __builtin_amdgcn_readfirstlane(CTL[q].on) : 0;
+                    if (o) {
+                        qmap |= q << (2 * nq);
+                        ++nq;
+                    }
                 }
                 wave_sync();
                 for (int s = 0; s < PP; ++s) {
@@ -556,19 +610,27 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                     const int plo = s ? rl32(blo, s - 1) : 0, phi = s ? rl32(bhi, s - 1) : 0;
                     const int64_t p2p_s = rl64(p2p, s);
                     const I64x2 *T = TM + slot_s * NP;
-                    const int64_t *Fp = (s & 1) ? FM0 : FM1;
-                    int64_t *Fc = (s & 1) ? FM1 : FM0;
-                    const I64x2 *Gp = (s & 1) ? FG0 : FG1;
-                    I64x2 *Gc = (s & 1) ? FG1 : FG0;
-                    // wave-uniform rounds and split-point loop: a lane with less to do
-                    // runs masked (clamped, in-range loads; predicated stores only)
-                    const int rounds = (wd_s + W - 1) / W;
-                    for (int r = 0; r < rounds; ++r) {
-                        const int k = ll + r * W;
-                        const bool act = on && k < wd_s;
-                        const int kk = act ? k : 0;
-                        const int b = blo_s + kk;
-                        const int amin0 = AMIN[off_s + kk], a0 = A0B[off_s + kk];
+                    const int poff = (s & 1) ? 0 : row_bytes / 2, coff = row_bytes / 2 - poff;
+                    // wave-uniform rounds over the (running segment, b) entries of the
+                    // stage, and a wave-uniform split-point loop: a lane with less to
+                    // do runs masked (clamped, in-range loads; predicated stores only)
+                    const int total = nq * wd_s;
+                    const float inv_wd = 1.0f / (float)wd_s;
+                    for (int e0 = 0; e0 < total; e0 += 64) {
+                        const int e = e0 + lane;
+                        const bool act = e < total;
+                        int qi = 0, k = act ? e : 0;
+                        if (nq > 1) split_entry(k, wd_s, inv_wd, qi, k);   // wave-uniform branch
+                        const int q = (qmap >> (2 * qi)) & 3;
+                        const int64_t t = CTL[q].t;
+                        uint8_t *const AMq = REG + q * arr_bytes;
+                        unsigned char *const RWq = REG + off_rows + q * row_bytes;
+                        const int64_t *Fp = reinterpret_cast<const int64_t *>(RWq + poff);
+                        int64_t *Fc = reinterpret_cast<int64_t *>(RWq + coff);
+                        const I64x2 *Gp = reinterpret_cast<const I64x2 *>(RWq + poff);
+                        I64x2 *Gc = reinterpret_cast<I64x2 *>(RWq + coff);
+                        const int b = blo_s + k;
+                        const int amin0 = AMq[off_s + k], a0 = AMq[sumwd + off_s + k];
                         const int ahi0 = (b - lo_s) < phi ? (b - lo_s) : phi;
                         const bool has = act && amin0 <= ahi0;
                         int left = has ? ahi0 - amin0 + 1 : 0;   // split points not yet relaxed
@@ -610,8 +672,8 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                                     gbest = ok && g < gbest ? g : gbest;
                                 }
                                 if (STATS) {
-                                    relax += ok && left > 0 ? 1 : 0;
-                                    slots += on ? 1 : 0;
+                                    add4(relq, q, ok && left > 0 ? 1 : 0);
+                                    add4(slq, q, 1);
                                     --left;
                                 }
                             }
@@ -626,7 +688,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                                 Gc[k] = I64x2{best, gbest};
                             else
                                 Fc[k] = best;
-                            ARG[off_s + k] = (uint8_t)ba;
+                            AMq[2 * sumwd + off_s + k] = (uint8_t)ba;
                         }
                     }
                     wave_sync();
@@ -679,9 +741,13 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
             uint32_t pw[8] = {0, 0, 0, 0, 0, 0, 0, 0};
             uint32_t prm = 0, pok = 0;
             const int64_t Bm = (int64_t)Bj - 1;
-            auto take = [&](int64_t Fx, int64_t Mx) {   // offer the segment's last pass
+            // offer the segment's last pass: a lower objective wins, and on equal
+            // objectives the lower largest stage (the least threshold reaching the
+            // optimum), whatever order the passes ran in; equal (objective, M)
+            // points share the partition of threshold M
+            auto take = [&](int64_t Fx, int64_t Mx) {
                 const int64_t sc = Fx + Bm * Mx;
-                if (sc <= bs) {
+                if (sc < bs || (sc == bs && Mx < bmx)) {
                     bs = sc;
                     bmx = Mx;
                     for (int w = 0; w < 8; ++w) pw[w] = CTL[sj].bt[w];
@@ -785,9 +851,9 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
     #pragma unroll
                 for (int q = 0; q < kMaxSeg; ++q) {
                     if (q >= nseg) continue;
-                    rq[q] = wave_sum32(sg == q ? relax : 0);
-                    eq[q] = wave_sum32(sg == q ? evals : 0);
-                    sq[q] = wave_sum32(sg == q ? slots : 0);
+                    rq[q] = wave_sum32(relq[q]);
+                    eq[q] = wave_sum32(evq[q]);
+                    sq[q] = wave_sum32(slq[q]);
                     pq[q] = wave_max32(sg == q ? passes : 0);
                     lead[q] = __ffsll((unsigned long long)__ballot(inr && sj == q)) - 1;
                 }

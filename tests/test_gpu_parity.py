@@ -198,6 +198,48 @@ def test_large_configs_sampled(torch, n, stride):
     assert plan["instance"] == int(np.argmin(obj))
 
 
+@pytest.mark.parametrize("n,scale,stride", [(2, 0.35, 1), (3, 0.5, 97)])
+def test_tight_memory_many_micro_counts(torch, n, scale, stride):
+    """Memory binds at many stored micro-batch counts and B runs over 1..32, so
+    the micro-batch groups of a key split into several classes of identical
+    feasible windows (and merge inside each): every result must still be the
+    oracle's."""
+    p = workloads.config(n)
+    p = variant(p, **{"cluster.mem_bytes": (p["cluster"]["mem_bytes"] * scale).astype(np.int64),
+                      "space.micro": np.arange(1, 33, dtype=np.int32)})
+    print(f"config {n}: memory x{scale}, B = 1..32, stride {stride}", flush=True)
+    pl = binding.Planner(p, "cuda:0")
+    pl.eval_cost_tables()
+    pl.stage_dp()
+    idx = list(range(0, pl.n, stride)) + [pl.n - 1]
+    assert compare(p, pl, sorted(set(idx))) > 0
+
+
+def _uniform_layers(problem):
+    """Every layer a copy of layer 0: stage costs become multiples of one layer's
+    cost, so equal objectives (ties in sum + (B-1) max) are everywhere."""
+    q = variant(problem)
+    m, c = q["model"], q["cluster"]
+    for key in ("is_moe", "params_dense", "params_expert", "act_bytes"):
+        m[key][:] = m[key][0]
+    m["expert_tokens"][:] = m["expert_tokens"][0]
+    for key in ("t_dense", "t_ffn"):
+        c[key][...] = c[key][..., :1]
+    return q
+
+
+@pytest.mark.parametrize("n,micro", [(1, None), (2, list(range(1, 17)))])
+def test_tied_objectives_every_candidate(torch, n, micro):
+    p = _uniform_layers(workloads.config(n))
+    if micro is not None:
+        p["space"]["micro"] = np.array(micro, dtype=np.int32)
+    print(f"config {n}: uniform layers", flush=True)
+    pl = binding.Planner(p, "cuda:0")
+    pl.eval_cost_tables()
+    pl.stage_dp()
+    assert compare(p, pl, range(pl.n)) > 0
+
+
 def test_random_tiny_every_candidate(torch):
     total = 0
     for s in range(40):
