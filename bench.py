@@ -12,6 +12,7 @@ stride sample of the same workload (single core) as a reported baseline.
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 4]
 """
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -40,6 +41,48 @@ WORKLOADS = {
 }
 
 
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "stage_dp_moe96_traffic.json")
+STAGE_DP_SOURCE = os.path.join(ROOT, "paper_2609_39350_amd", "csrc", "stage_dp.hip")
+
+
+def kernel_code_sha256(path=STAGE_DP_SOURCE):
+    """SHA-256 of a kernel source with its // comments and blank lines removed
+    (the kernel source has no string literal holding //)."""
+    lines = []
+    with open(path) as f:
+        for line in f:
+            code = line.split("//", 1)[0].rstrip()
+            if code:
+                lines.append(code)
+    return hashlib.sha256("\n".join(lines).encode()).hexdigest()
+
+
+def measured_traffic(config):
+    """HBM bytes per stage-DP launch from the committed counter record, or None
+    when the record is for another workload or the kernel code has changed
+    since the counters were taken."""
+    try:
+        with open(TRAFFIC_RECORD) as f:
+            rec = json.load(f)
+        sha = kernel_code_sha256()
+    except OSError:
+        return None
+    if rec.get("config") != config or rec.get("kernel_sha256") != sha:
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def copy_calibration(torch, dev, nbytes=1 << 30, reps=3):
+    """A plain device-to-device copy of known size, for scaling the FETCH_SIZE /
+    WRITE_SIZE counters (run under rocprofv3 --pmc next to the kernels)."""
+    src = torch.ones(nbytes, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    return nbytes
+
+
 def cpu_baseline(problem, n_total, n_sample):
     """The oracle as it stands, single thread, on a fixed stride sample."""
     from oracle.oracle import Oracle
@@ -62,6 +105,8 @@ def main():
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--cpu-sample", type=int, default=200)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a 1 GiB device copy (counter scaling for HBM traffic)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the planner's candidates are independent and this build "
@@ -90,6 +135,8 @@ def main():
     slots = int(st[:, 3].astype(np.int64).sum())
     passes = st[:, 0]
     feasible = int((pl.results()["status"] == 0).sum())
+
+    calib = copy_calibration(torch, dev) if args.copy_calibration else None
 
     for _ in range(args.warmup):
         pl.run()
@@ -131,7 +178,8 @@ def main():
         "config": {"workload": f"config {args.config}: {WORKLOADS[args.config]}", "candidates": n,
                    "configs_6d": pl.n_configs, "feasible_candidates": feasible},
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK_OPS / 1e12,
-                     "unit": "TOP/s", "frac": achieved / VALU_PEAK_OPS, "traffic": None,
+                     "unit": "TOP/s", "frac": achieved / VALU_PEAK_OPS,
+                     "traffic": measured_traffic(args.config),
                      "kernel": "stage_dp", "ops_per_relaxation": OPS_PER_RELAXATION,
                      "ops_per_evaluation": OPS_PER_EVALUATION,
                      "relaxations_per_launch": relax, "evaluations_per_launch": evals},
@@ -143,6 +191,8 @@ def main():
                       "config": plan["config"], "order": plan["order"], "B": plan["n_micro"],
                       "layers": plan["layers"], "recompute": plan["recompute"]},
     }
+    if calib is not None:
+        out["copy_calibration_bytes"] = calib
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(problem, n, args.cpu_sample)
     print(json.dumps(out), flush=True)

@@ -14,23 +14,35 @@
 // threshold is the lexicographically smallest sum-optimal partition there,
 // which is also the smallest one at its own largest stage.
 //
+// Passes per sweep: one fused pass at t = inf that also carries the min-max
+// row (t_bot = least possible largest stage), one pass at t_bot, then the
+// descending sweep.  An incumbent is replaced by a lower objective, or by an
+// equal one with a lower largest stage, so the result does not depend on the
+// order of the passes.
+//
 // Work sharing across B: B enters a candidate only through the 1F1B count of
 // stored micro-batches min(PP - i, B) (memory) and the (B-1) weight of the
-// objective.  Candidates of one (pi, ordering) whose B gives the same
-// min(B, PP) form a group that shares every feasible segment and every DP
-// pass; one sweep serves the group, one incumbent per B.
+// objective.  Candidates of one (pi, ordering) whose B values lead to identical
+// feasible split intervals at every (stage, end layer) share every DP pass:
+// one sweep serves them, one incumbent per B.  The groups of equal min(B, PP)
+// are merged further into classes: the intervals of a (stage, end layer) change
+// with the stored count m only at the m where some split point's memory stops
+// fitting (m = floor(room / activation), computed exactly), so neighbouring
+// group values fall into one class unless such a step lies between them.
 //
 // Mapping: persistent wave64 workgroups pull (pi, ordering) keys from an atomic
 // queue, largest PP first.  The stage layout of a key is wave-uniform (one
-// stage per lane, read with readlane).  Up to four B-groups of the key run at
-// once in lane segments of 16 / 32 lanes; in a segment, lanes cover the band
-// of end layers b a stage can reach under the pruning-1 windows (in rounds),
-// and each lane loops over the split points a of the previous stage's band.
-// Layer prefix sums live in LDS once per key; feasible split intervals
-// (memory with / without recomputation, prunings 1 and 3 -- all monotone in
-// the segment length), DP rows (double-buffered) and back-trace pointers live
-// in LDS per segment, packed by band.  Lane j also holds the incumbent of the
-// key's j-th microbatch count.  No MFMA: this is int64 min-plus scan work.
+// stage per lane, read with readlane).  Up to four classes of the key run at
+// once as segments; the (segment, end layer b) entries of a stage -- b over the
+// band a stage can reach under the pruning-1 windows -- are spread over the 64
+// lanes in rounds, and each lane loops over the split points a of the previous
+// stage's band (two per trip, wave-uniform trip count).  Layer prefix sums live
+// in LDS once per key; feasible split intervals (memory with / without
+// recomputation, prunings 1 and 3 -- all monotone in the segment length), DP
+// rows (double-buffered) and back-trace pointers live in LDS per segment,
+// packed by band.  Lane j also holds the incumbent of the key's j-th
+// microbatch count.  Wave-wide reductions use DPP row rotations.  No MFMA:
+// this is int64 min-plus scan work.
 #include "internal.h"
 
 namespace hapmoe {
