@@ -50,10 +50,7 @@ namespace {
 
 constexpr int64_t kBig = int64_t(1) << 62;   // "no partition" inside the DP (sums stay far from overflow)
 constexpr int64_t kNegInf = INT64_MIN;        // a threshold no stage cost meets
-#ifndef HAPMOE_RELAX_UNROLL
-#define HAPMOE_RELAX_UNROLL 2
-#endif
-constexpr int kRelaxUnroll = HAPMOE_RELAX_UNROLL;   // split points per relaxation-loop trip
+constexpr int kRelaxUnroll = 2;   // split points per relaxation-loop trip
 constexpr int kMaxSeg = 4;
 
 // LDS of one wave: TM [kmax][np] {T0, T1} | memory prefixes | per-segment
@@ -373,6 +370,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
         const int woff = wave_incl_scan(wd, lane) - wd;   // packed offset of stage s
         const int sumwd = rl32(woff, 63) + rl32(wd, 63);
         const int maxw = wave_max32(wd);
+
         const bool feasible_shape = totlo <= N && tothi >= N && !__any(lane < PP && wd == 0);
         // region: [per-segment AMIN | A0B | ARG] [per-segment DP rows  or  memory prefixes]
         const int arr_bytes = align16(3 * sumwd), row_bytes = 2 * align16(maxw * 16);
@@ -401,7 +399,8 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                 const int m = __ffsll((unsigned long long)rs) - 1;
                 rs &= rs - 1;
                 const int64_t *src = time + (int64_t)(m - 1) * 3 * np;
-                for (int b = lane; b <= N; b += 64) TM[k * NP + b] = I64x2{src[b], src[np + b]};
+                // negated, so that a stage cost T[b] - T[a] is one 64-bit add
+                for (int b = lane; b <= N; b += 64) TM[k * NP + b] = I64x2{-src[b], -src[np + b]};
                 ++k;
             }
         }
@@ -650,16 +649,18 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                         // threshold no stage cost meets
                         const int amin = has ? amin0 : plo;
                         const int64_t tl = has ? t : kNegInf;
-                        const I64x2 tb = T[b];
-                        const int64_t k0 = tb.x + p2p_s, k1 = tb.y + p2p_s;
+                        const I64x2 tb = T[b];   // negated prefix sums
+                        const int64_t k0 = p2p_s - tb.x, k1 = p2p_s - tb.y;
                         int64_t best = kBig, gbest = kBig;
                         int ba = 255;
                         // a runs downwards from b - lo and then stays at amin: repeating
                         // the last split point changes nothing ("<=" keeps the smallest
                         // split point among equal values, which is the current one)
-                        // kRelaxUnroll split points per trip: every load is issued before
-                        // the first use, one exit test per trip; the trip count is bounded
-                        // by the longest window, as a lane only goes on while a > amin
+                        // kRelaxUnroll split points per trip (more only add work: the
+                        // threshold leaves most windows one or two points long): every
+                        // load is issued before the first use, one exit test per trip;
+                        // the trip count is bounded by the longest window, as a lane only
+                        // goes on while a > amin
                         int a = has ? ahi0 : plo;
                         for (;;) {
                             int au[kRelaxUnroll];
@@ -671,9 +672,11 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                                 fu[u] = fused ? Gp[au[u] - plo] : I64x2{Fp[au[u] - plo], 0};
                             }
                             bool ok = false;
+                            int al = a;
 #pragma unroll
                             for (int u = 0; u < kRelaxUnroll; ++u) {
-                                const int64_t cst = au[u] < a0 ? k1 - tu[u].y : k0 - tu[u].x;
+                                al = au[u];
+                                const int64_t cst = au[u] < a0 ? k1 + tu[u].y : k0 + tu[u].x;
                                 ok = cst <= tl;
                                 const int64_t v = fu[u].x + cst;
                                 const bool le = ok && v <= best;
@@ -691,7 +694,6 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                             }
                             // the stage cost only grows as a falls: the wave is done once
                             // no lane is both under its threshold and short of amin
-                            const int al = au[kRelaxUnroll - 1];
                             if (__builtin_amdgcn_ballot_w64(ok && al > amin) == 0) break;
                             a = al > amin ? al - 1 : al;
                         }
@@ -713,23 +715,34 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                     uint32_t words[8] = {0, 0, 0, 0, 0, 0, 0, 0};
                     uint32_t rmask = 0;
                     int64_t m = 0;
+                    // the reads of the next stage (pointer and recomputation bound at
+                    // the split point just found) go out with this stage's prefix sums:
+                    // one LDS round trip a stage
                     int b = N;
                     bool ok = fin < kBig;
+                    int k = b - rl32(blo, PP - 1);
+                    int a = ARG[rl32(woff, PP - 1) + k], a0 = A0B[rl32(woff, PP - 1) + k];
                     for (int s = PP - 1; s >= 0 && ok; --s) {
-                        const int k = b - rl32(blo, s), off_s = rl32(woff, s);
-                        const int a = ARG[off_s + k];
                         if (a >= b) {
                             ok = false;
                             break;
                         }
+                        int an = 0, a0n = 0;
+                        if (s > 0) {
+                            const int kn = a - rl32(blo, s - 1), offn = rl32(woff, s - 1);
+                            an = ARG[offn + kn];
+                            a0n = A0B[offn + kn];
+                        }
                         const I64x2 *T = TM + rl32(slot, s) * NP;
-                        const I64x2 ta = T[a], tb = T[b];
-                        const bool r1 = a < A0B[off_s + k];
-                        const int64_t c = (r1 ? tb.y - ta.y : tb.x - ta.x) + rl64(p2p, s);
+                        const I64x2 ta = T[a], tb = T[b];   // negated prefix sums
+                        const bool r1 = a < a0;
+                        const int64_t c = (r1 ? ta.y - tb.y : ta.x - tb.x) + rl64(p2p, s);
                         m = c > m ? c : m;
                         words[s >> 2] |= (uint32_t)(b - a) << (8 * (s & 3));
                         if (r1) rmask |= 1u << s;
                         b = a;
+                        a = an;
+                        a0 = a0n;
                     }
                     ok = ok && b == 0;
                     CTL[sg].M = m;
