@@ -199,19 +199,26 @@ __device__ inline int wave_incl_scan(int x, int lane)
     return x;
 }
 
-// Bit m set for the m in [1, mtop] with m = floor(room / act): the largest count
-// of stored micro-batches whose activations still fit into room (none if room <
-// 0, act = 0 or the count exceeds mtop).  Exact: an fp32 estimate is corrected
-// by one integer step either way (its error is far below 1 for counts < 64).
-__device__ inline uint64_t cap_step(int64_t room, int64_t act, int mtop)
+// The largest count m of stored micro-batches whose activations (act each) still
+// fit into room: floor(room / act), -1 if room < 0, 64 for "64 or more" (also
+// act = 0).  Exact: an fp32 estimate is corrected by one integer step either way
+// (its error is far below 1 for counts < 64).
+__device__ inline int cap_count(int64_t room, int64_t act)
 {
-    if (room < act || act <= 0 || room >= act * 64) return 0;   // count 0, unbounded or >= 64
+    if (room < 0) return -1;
+    if (act <= 0 || room >= act * 64) return 64;
+    if (room < act) return 0;
     int m = (int)((float)room / (float)act);
     m = m > 63 ? 63 : m;
     if ((int64_t)m * act > room)
         --m;
     else if ((int64_t)(m + 1) * act <= room)
         ++m;
+    return m;
+}
+
+__device__ inline uint64_t step_bit(int m, int mtop)
+{
     return (m >= 1 && m <= mtop) ? (uint64_t(1) << m) : 0;
 }
 
@@ -447,14 +454,18 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                 const int64_t wb = MW[b], a0b = MA0[b], a1b = MA1[b];
                 const int mb = MOE[b];
                 const int64_t cmb = CM ? CM[b] : 0;
+                // the counts do not fall as a grows: once both exceed mtop, so do
+                // all the later ones
                 for (int a = alo; a <= ahi; ++a) {
                     if (STATS) ++cls_evals;
                     const int64_t xb = (mb - MOE[a]) > 0 ? X : 0;
                     const int64_t room = cap_s - (wb - MW[a] + xb);
                     const bool ok3 = !prune_het || (CM ? cmb - CM[a] : 0) + hc_b <= eta_tbar;
                     if (!ok3) continue;
-                    brk |= cap_step(room, a0b - MA0[a], mtop);
-                    if (recomp) brk |= cap_step(room, a1b - MA1[a], mtop);
+                    const int m0 = cap_count(room, a0b - MA0[a]);
+                    const int m1 = recomp ? cap_count(room, a1b - MA1[a]) : 64;
+                    brk |= step_bit(m0, mtop) | (recomp ? step_bit(m1, mtop) : 0);
+                    if (m0 > mtop && m1 > mtop) break;
                 }
             }
         }
