@@ -375,6 +375,11 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
         bhi = bhi < cumhi ? bhi : cumhi;
         const int wd = lane < PP ? (bhi >= blo ? bhi - blo + 1 : 0) : 0;
         const int woff = wave_incl_scan(wd, lane) - wd;   // packed offset of stage s
+        // stage s's band fields packed in lane s (one readlane each in the hot
+        // loops): blo | bhi << 8 | lo << 16 | slot << 24 (all < 256), and
+        // woff | wd << 16 (woff <= 32 * 128, wd <= 128)
+        const int pk1 = (blo & 0xff) | ((bhi & 0xff) << 8) | ((lo & 0xff) << 16) | (slot << 24);
+        const int pk2 = woff | (wd << 16);
         const int sumwd = rl32(woff, 63) + rl32(wd, 63);
         const int maxw = wave_max32(wd);
 
@@ -541,7 +546,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                 const int64_t *CM = mixed_s ? time + ((int64_t)(mask_s - 1) * 3 + 2) * np : nullptr;
                 const int64_t hc_b = bdiff_s ? p2p_s : 0;
                 const int total = nact * wd_s;
-                const float inv_wd = 1.0f / (float)wd_s;
+                const float inv_wd = __builtin_amdgcn_rcpf((float)wd_s);   // split_entry corrects
                 for (int e0 = 0; e0 < total; e0 += 64) {   // wave-uniform
                     const int e = e0 + lane;
                     const bool act = e < total;
@@ -627,9 +632,10 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                 }
                 wave_sync();
                 for (int s = 0; s < PP; ++s) {
-                    const int slot_s = rl32(slot, s), lo_s = rl32(lo, s);
-                    const int blo_s = rl32(blo, s), wd_s = rl32(wd, s), off_s = rl32(woff, s);
-                    const int plo = s ? rl32(blo, s - 1) : 0, phi = s ? rl32(bhi, s - 1) : 0;
+                    const int p1 = rl32(pk1, s), p2 = rl32(pk2, s), q1 = s ? rl32(pk1, s - 1) : 0;
+                    const int blo_s = p1 & 0xff, lo_s = (p1 >> 16) & 0xff, slot_s = (p1 >> 24) & 0xff;
+                    const int off_s = p2 & 0xffff, wd_s = p2 >> 16;
+                    const int plo = q1 & 0xff, phi = (q1 >> 8) & 0xff;
                     const int64_t p2p_s = rl64(p2p, s);
                     const I64x2 *T = TM + slot_s * NP;
                     const int poff = (s & 1) ? 0 : row_bytes / 2, coff = row_bytes / 2 - poff;
@@ -637,7 +643,8 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                     // stage, and a wave-uniform split-point loop: a lane with less to
                     // do runs masked (clamped, in-range loads; predicated stores only)
                     const int total = nq * wd_s;
-                    const float inv_wd = 1.0f / (float)wd_s;
+                    // approximate reciprocal: split_entry corrects the quotient
+                    const float inv_wd = nq > 1 ? __builtin_amdgcn_rcpf((float)wd_s) : 0.0f;
                     for (int e0 = 0; e0 < total; e0 += 64) {
                         const int e = e0 + lane;
                         const bool act = e < total;
@@ -731,8 +738,9 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                     // one LDS round trip a stage
                     int b = N;
                     bool ok = fin < kBig;
-                    int k = b - rl32(blo, PP - 1);
-                    int a = ARG[rl32(woff, PP - 1) + k], a0 = A0B[rl32(woff, PP - 1) + k];
+                    const int pl = rl32(pk2, PP - 1) & 0xffff;
+                    int k = b - (rl32(pk1, PP - 1) & 0xff);
+                    int a = ARG[pl + k], a0 = A0B[pl + k];
                     for (int s = PP - 1; s >= 0 && ok; --s) {
                         if (a >= b) {
                             ok = false;
@@ -740,11 +748,11 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                         }
                         int an = 0, a0n = 0;
                         if (s > 0) {
-                            const int kn = a - rl32(blo, s - 1), offn = rl32(woff, s - 1);
+                            const int kn = a - (rl32(pk1, s - 1) & 0xff), offn = rl32(pk2, s - 1) & 0xffff;
                             an = ARG[offn + kn];
                             a0n = A0B[offn + kn];
                         }
-                        const I64x2 *T = TM + rl32(slot, s) * NP;
+                        const I64x2 *T = TM + ((rl32(pk1, s) >> 24) & 0xff) * NP;
                         const I64x2 ta = T[a], tb = T[b];   // negated prefix sums
                         const bool r1 = a < a0;
                         const int64_t c = (r1 ? ta.y - tb.y : ta.x - tb.x) + rl64(p2p, s);
