@@ -727,47 +727,57 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                 }
                 const bool odd = ((PP - 1) & 1) != 0;
                 const int64_t fin = fused ? (odd ? FG1[0].x : FG0[0].x) : (odd ? FM1[0] : FM0[0]);
-                if (on && ll == 0) {
+                const bool tracer = on && ll == 0;
+                if (tracer) {
                     CTL[sg].F = fin;
                     if (fused) CTL[sg].G = odd ? FG1[0].y : FG0[0].y;
-                    uint32_t words[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+                    for (int w = 0; w < 8; ++w) CTL[sg].bt[w] = 0;
+                }
+                // Back-trace of every running segment by its lane 0.  The loop over
+                // the stages is wave-uniform; the other lanes follow on clamped,
+                // in-range indices and drop what they compute.  The next stage's
+                // pointer and recomputation bound go out with this stage's prefix
+                // sums: one LDS round trip a stage.
+                {
+                    uint8_t *const btb = reinterpret_cast<uint8_t *>(CTL[segi].bt);
                     uint32_t rmask = 0;
                     int64_t m = 0;
-                    // the reads of the next stage (pointer and recomputation bound at
-                    // the split point just found) go out with this stage's prefix sums:
-                    // one LDS round trip a stage
                     int b = N;
-                    bool ok = fin < kBig;
-                    const int pl = rl32(pk2, PP - 1) & 0xffff;
-                    int k = b - (rl32(pk1, PP - 1) & 0xff);
-                    int a = ARG[pl + k], a0 = A0B[pl + k];
-                    for (int s = PP - 1; s >= 0 && ok; --s) {
-                        if (a >= b) {
-                            ok = false;
-                            break;
-                        }
+                    bool ok = tracer && fin < kBig;
+                    const int pl = rl32(pk2, PP - 1) & 0xffff, kl = N - (rl32(pk1, PP - 1) & 0xff);
+                    int a = ARG[pl + kl], a0 = A0B[pl + kl];
+                    for (int s = PP - 1; s >= 0; --s) {
+                        ok = ok && a < b;
                         int an = 0, a0n = 0;
-                        if (s > 0) {
-                            const int kn = a - (rl32(pk1, s - 1) & 0xff), offn = rl32(pk2, s - 1) & 0xffff;
-                            an = ARG[offn + kn];
-                            a0n = A0B[offn + kn];
+                        if (s > 0) {   // wave-uniform
+                            const int q1 = rl32(pk1, s - 1), q2 = rl32(pk2, s - 1);
+                            const int wdn = q2 >> 16;
+                            int kn = (ok ? a : 0) - (q1 & 0xff);
+                            kn = kn < 0 ? 0 : (kn >= wdn ? wdn - 1 : kn);
+                            an = ARG[(q2 & 0xffff) + kn];
+                            a0n = A0B[(q2 & 0xffff) + kn];
                         }
+                        const int ai = ok ? a : 0;
                         const I64x2 *T = TM + ((rl32(pk1, s) >> 24) & 0xff) * NP;
-                        const I64x2 ta = T[a], tb = T[b];   // negated prefix sums
-                        const bool r1 = a < a0;
+                        const I64x2 ta = T[ai], tb = T[b];   // negated prefix sums
+                        const bool r1 = ai < a0;
                         const int64_t c = (r1 ? ta.y - tb.y : ta.x - tb.x) + rl64(p2p, s);
-                        m = c > m ? c : m;
-                        words[s >> 2] |= (uint32_t)(b - a) << (8 * (s & 3));
-                        if (r1) rmask |= 1u << s;
-                        b = a;
+                        if (ok) {
+                            m = c > m ? c : m;
+                            btb[s] = (uint8_t)(b - a);
+                            if (r1) rmask |= 1u << s;
+                            b = a;
+                        }
                         a = an;
                         a0 = a0n;
                     }
-                    ok = ok && b == 0;
-                    CTL[sg].M = m;
-                    for (int w = 0; w < 8; ++w) CTL[sg].bt[w] = words[w];
-                    CTL[sg].rmask = rmask;
-                    CTL[sg].ok = ok ? 1u : 0u;
+                    if (tracer) {
+                        ok = ok && b == 0;
+                        CTL[sg].M = m;
+                        CTL[sg].rmask = rmask;
+                        CTL[sg].ok = ok ? 1u : 0u;
+                    }
                 }
                 wave_sync();
             };
