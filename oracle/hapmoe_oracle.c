@@ -651,7 +651,192 @@ int32_t orc_brute(int32_t pp, int32_t n, int64_t micro, const int64_t *cost, orc
     return 0;
 }
 
-static int32_t solve_with(const orc_problem *p, int64_t idx, orc_result *r, int brute)
+/* ------------------------------------------------------------------------
+ * 1F1B re-scoring (Eq. 4 with the appendix's steady-state term).  The
+ * appendix gives, for stage forward / backward times t_f,i and t_b,i and the
+ * bottleneck stage s (largest t_f + t_b), the iteration latency
+ *   sum_i (t_f,i + t_b,i) + sum_{i <= s} t_f,i + (M - s - 1) max_i (t_f,i + t_b,i)
+ * with M micro-batches.  Readings: a stage cost c splits as t_f = ceil(c/3),
+ * t_b = c - t_f (backward twice the forward); s is the first (1-based) stage
+ * of largest cost; the count M - s - 1 is taken as max(0, M - s - 1), as the
+ * steady state has no full cycle when B <= s.
+ * ---------------------------------------------------------------------- */
+int64_t orc_latency_1f1b(int32_t pp, const int64_t *c, int64_t micro)
+{
+    int64_t sum = 0, mx = -1;
+    int s = 0;
+    for (int i = 0; i < pp; i++) {
+        sum += c[i];
+        if (c[i] > mx) {
+            mx = c[i];
+            s = i + 1;
+        }
+    }
+    int64_t fwd = 0;
+    for (int i = 0; i < s; i++) fwd += (c[i] + 2) / 3;
+    int64_t steady = micro - s - 1;
+    if (steady < 0) steady = 0;
+    return sum + fwd + steady * mx;
+}
+
+/* The candidates are the (max, sum) Pareto frontier: the thresholds t at which
+ * F_t drops (F_t < F_t' for every t' < t), each with the canonical partition of
+ * the threshold DP at t, whose largest stage is then t.  The least latency
+ * wins; ties go to the lower max (the earlier frontier point, ascending). */
+int32_t orc_dp_exact(int32_t pp, int32_t n, int64_t micro, const int64_t *cost, orc_result *r)
+{
+    int W = n + 1;
+    int64_t ncost = (int64_t)pp * W * W;
+    memset(r, 0, sizeof(*r));
+    r->pp = pp;
+    int64_t *theta = malloc(sizeof(int64_t) * (size_t)(ncost + 1));
+    int64_t nt = 0;
+    for (int64_t i = 0; i < ncost; i++)
+        if (cost[i] != ORC_INF) theta[nt++] = cost[i];
+    qsort(theta, (size_t)nt, sizeof(int64_t), cmp_i64);
+    int64_t u = 0;
+    for (int64_t i = 0; i < nt; i++)
+        if (u == 0 || theta[i] != theta[u - 1]) theta[u++] = theta[i];
+    int64_t *F = malloc(sizeof(int64_t) * (size_t)(pp + 1) * W);
+    int16_t *arg = malloc(sizeof(int16_t) * (size_t)(pp + 1) * W);
+    int64_t best = ORC_INF, prev = ORC_INF, points = 0;
+    for (int64_t k = 0; k < u; k++) {
+        int64_t t = theta[k];
+        int64_t f = dp_pass(pp, n, cost, t, F, arg);
+        if (f == ORC_INF || f >= prev) continue;   /* not a frontier point */
+        prev = f;
+        points++;
+        int64_t c[ORC_MAX_STAGES];
+        uint8_t len[ORC_MAX_STAGES];
+        int b = n;
+        int64_t mx = 0;
+        for (int i = pp; i >= 1; i--) {
+            int a = arg[(int64_t)i * W + b];
+            c[i - 1] = cost[((int64_t)(i - 1) * W + a) * W + b];
+            len[i - 1] = (uint8_t)(b - a);
+            if (c[i - 1] > mx) mx = c[i - 1];
+            b = a;
+        }
+        int64_t lat = orc_latency_1f1b(pp, c, micro);
+        if (lat < best) {
+            best = lat;
+            r->sum = f;
+            r->tmax = mx;
+            memcpy(r->layers, len, (size_t)pp);
+        }
+    }
+    r->thresholds = points;
+    if (best == ORC_INF) {
+        r->status = 1;
+        r->opt = r->sum = r->tmax = ORC_INF;
+    } else {
+        r->opt = best;
+    }
+    free(theta);
+    free(F);
+    free(arg);
+    return 0;
+}
+
+/* Brute force for the same objective: every composition, the Pareto-optimal
+ * (max, sum) pairs, per pair the partition with the smallest
+ * (b_{pp-1}, b_{pp-2}, ..., b_1), then the least latency, ties to the lower max. */
+typedef struct part_rec {
+    int64_t mx, sum;
+    int b[ORC_MAX_STAGES + 1];
+} part_rec;
+
+typedef struct part_list {
+    int pp, n, W;
+    const int64_t *cost;
+    int b[ORC_MAX_STAGES + 1];
+    part_rec *v;
+    int64_t len, cap;
+} part_list;
+
+static void collect(part_list *L, int i)
+{
+    if (i == L->pp) {
+        part_rec rec;
+        rec.mx = 0;
+        rec.sum = 0;
+        for (int k = 0; k < L->pp; k++) {
+            int64_t c = L->cost[((int64_t)k * L->W + L->b[k]) * L->W + L->b[k + 1]];
+            if (c == ORC_INF) return;
+            rec.sum += c;
+            if (c > rec.mx) rec.mx = c;
+        }
+        memcpy(rec.b, L->b, sizeof(rec.b));
+        if (L->len == L->cap) {
+            L->cap = L->cap ? 2 * L->cap : 64;
+            L->v = realloc(L->v, sizeof(part_rec) * (size_t)L->cap);
+        }
+        L->v[L->len++] = rec;
+        return;
+    }
+    if (i == L->pp - 1) {
+        L->b[i + 1] = L->n;
+        if (L->b[i] < L->n) collect(L, i + 1);
+        return;
+    }
+    for (int e = L->b[i] + 1; e <= L->n - (L->pp - 1 - i); e++) {
+        L->b[i + 1] = e;
+        collect(L, i + 1);
+    }
+}
+
+static int lex_smaller(int pp, const int *x, const int *y)   /* (b_{pp-1}, ..., b_1) */
+{
+    for (int i = pp - 1; i >= 1; i--)
+        if (x[i] != y[i]) return x[i] < y[i];
+    return 0;
+}
+
+int32_t orc_brute_exact(int32_t pp, int32_t n, int64_t micro, const int64_t *cost, orc_result *r)
+{
+    memset(r, 0, sizeof(*r));
+    r->pp = pp;
+    part_list L;
+    memset(&L, 0, sizeof(L));
+    L.pp = pp;
+    L.n = n;
+    L.W = n + 1;
+    L.cost = cost;
+    if (pp <= n) collect(&L, 0);
+    int64_t best = ORC_INF, best_mx = ORC_INF, points = 0;
+    for (int64_t i = 0; i < L.len; i++) {
+        const part_rec *x = &L.v[i];
+        int keep = 1;
+        for (int64_t j = 0; j < L.len && keep; j++) {
+            const part_rec *y = &L.v[j];
+            if (y->mx <= x->mx && y->sum <= x->sum && (y->mx < x->mx || y->sum < x->sum)) keep = 0;   /* dominated */
+            else if (y->mx == x->mx && y->sum == x->sum && lex_smaller(pp, y->b, x->b)) keep = 0;    /* not canonical */
+        }
+        if (!keep) continue;
+        points++;
+        int64_t c[ORC_MAX_STAGES];
+        for (int k = 0; k < pp; k++) c[k] = cost[((int64_t)k * L.W + x->b[k]) * L.W + x->b[k + 1]];
+        int64_t lat = orc_latency_1f1b(pp, c, micro);
+        if (lat < best || (lat == best && x->mx < best_mx)) {
+            best = lat;
+            best_mx = x->mx;
+            r->sum = x->sum;
+            r->tmax = x->mx;
+            for (int k = 0; k < pp; k++) r->layers[k] = (uint8_t)(x->b[k + 1] - x->b[k]);
+        }
+    }
+    r->thresholds = points;
+    if (best == ORC_INF) {
+        r->status = 1;
+        r->opt = r->sum = r->tmax = ORC_INF;
+    } else {
+        r->opt = best;
+    }
+    free(L.v);
+    return 0;
+}
+
+static int32_t solve_with(const orc_problem *p, int64_t idx, orc_result *r, int mode)
 {
     orc_config c;
     int32_t order, micro;
@@ -660,10 +845,14 @@ static int32_t solve_with(const orc_problem *p, int64_t idx, orc_result *r, int 
     int64_t *cost = malloc(sizeof(int64_t) * (size_t)c.pp * W * W);
     uint8_t *rf = malloc((size_t)c.pp * W * W);
     orc_segment_costs(p, idx, cost, rf);
-    if (brute)
-        orc_brute(c.pp, p->n_layers, micro, cost, r);
-    else
+    if (mode == 0)
         orc_dp(c.pp, p->n_layers, micro, cost, r);
+    else if (mode == 1)
+        orc_brute(c.pp, p->n_layers, micro, cost, r);
+    else if (mode == 2)
+        orc_dp_exact(c.pp, p->n_layers, micro, cost, r);
+    else
+        orc_brute_exact(c.pp, p->n_layers, micro, cost, r);
     orc_stage st[ORC_MAX_STAGES];
     orc_stages(p, &c, order, micro, st);
     for (int i = 0; i < c.pp; i++) r->stage_mask[i] = (uint8_t)st[i].mask;
@@ -689,5 +878,15 @@ int32_t orc_solve_many(const orc_problem *p, const int64_t *idx, int64_t n, orc_
 {
     for (int64_t i = 0; i < n; i++)
         if (orc_solve(p, idx[i], &r[i])) return -1;
+    return 0;
+}
+
+int32_t orc_solve_exact(const orc_problem *p, int64_t idx, orc_result *r) { return solve_with(p, idx, r, 2); }
+int32_t orc_solve_exact_brute(const orc_problem *p, int64_t idx, orc_result *r) { return solve_with(p, idx, r, 3); }
+
+int32_t orc_solve_exact_many(const orc_problem *p, const int64_t *idx, int64_t n, orc_result *r)
+{
+    for (int64_t i = 0; i < n; i++)
+        if (orc_solve_exact(p, idx[i], &r[i])) return -1;
     return 0;
 }

@@ -10,6 +10,11 @@
  *     minimise  sum_i c_i + (B-1) * max_i c_i  over layer partitions,
  * solved by sweeping every distinct stage cost ascending as the threshold.
  *
+ * A second objective re-scores the partitions of the (max, sum) Pareto frontier
+ * with the 1F1B iteration latency of the appendix (the steady-state term with
+ * the bottleneck stage's position, Eq. 4 and its appendix expansion); see
+ * orc_dp_exact for the readings it takes.
+ *
  * Only the test-suite, the smoke check and the CPU-baseline leg of the bench
  * may load this code.  It shares no code, header or table with the HIP library
  * and reads its own flat problem struct.  Everything is fp64 with IEEE
@@ -133,5 +138,19 @@ int32_t orc_brute(int32_t pp, int32_t n, int64_t micro, const int64_t *cost, orc
 int32_t orc_solve(const orc_problem *p, int64_t idx, orc_result *r);
 int32_t orc_solve_many(const orc_problem *p, const int64_t *idx, int64_t n, orc_result *r);
 int32_t orc_solve_brute(const orc_problem *p, int64_t idx, orc_result *r);
+
+/* 1F1B iteration latency of a partition given its stage costs c[0..pp): with
+ * t_f = ceil(c/3), t_b = c - t_f and s the first (1-based) stage of largest c,
+ *   T = sum c + sum_{i <= s} t_f,i + max(0, B - s - 1) * max c. */
+int64_t orc_latency_1f1b(int32_t pp, const int64_t *c, int64_t micro);
+/* Exact re-scoring over the (max, sum) Pareto frontier: r->opt = least T, ties
+ * to the lower max; r->sum / r->tmax / layers describe the chosen point's
+ * canonical partition (the threshold DP's back-trace at t = its max);
+ * r->thresholds = frontier points scored. */
+int32_t orc_dp_exact(int32_t pp, int32_t n, int64_t micro, const int64_t *cost, orc_result *r);
+int32_t orc_brute_exact(int32_t pp, int32_t n, int64_t micro, const int64_t *cost, orc_result *r);
+int32_t orc_solve_exact(const orc_problem *p, int64_t idx, orc_result *r);
+int32_t orc_solve_exact_many(const orc_problem *p, const int64_t *idx, int64_t n, orc_result *r);
+int32_t orc_solve_exact_brute(const orc_problem *p, int64_t idx, orc_result *r);
 
 #endif

@@ -121,6 +121,13 @@ def lib():
         L.orc_solve.argtypes = [P(OrcProblem), C.c_int64, P(OrcResult)]
         L.orc_solve_brute.argtypes = [P(OrcProblem), C.c_int64, P(OrcResult)]
         L.orc_solve_many.argtypes = [P(OrcProblem), C.c_void_p, C.c_int64, P(OrcResult)]
+        L.orc_latency_1f1b.argtypes = [C.c_int32, C.c_void_p, C.c_int64]
+        L.orc_latency_1f1b.restype = C.c_int64
+        L.orc_dp_exact.argtypes = [C.c_int32, C.c_int32, C.c_int64, C.c_void_p, P(OrcResult)]
+        L.orc_brute_exact.argtypes = [C.c_int32, C.c_int32, C.c_int64, C.c_void_p, P(OrcResult)]
+        L.orc_solve_exact.argtypes = [P(OrcProblem), C.c_int64, P(OrcResult)]
+        L.orc_solve_exact_brute.argtypes = [P(OrcProblem), C.c_int64, P(OrcResult)]
+        L.orc_solve_exact_many.argtypes = [P(OrcProblem), C.c_void_p, C.c_int64, P(OrcResult)]
         _LIB = L
     return _LIB
 
@@ -272,6 +279,26 @@ class Oracle:
             raise IndexError("instance out of range")
         return [result_dict(r) for r in res[: len(idx)]]
 
+    # ---- 1F1B re-scoring of the (max, sum) Pareto frontier ----------------------
+    def solve_exact(self, idx):
+        r = OrcResult()
+        if self.L.orc_solve_exact(C.byref(self.P), int(idx), C.byref(r)) != 0:
+            raise IndexError(idx)
+        return result_dict(r)
+
+    def solve_exact_brute(self, idx):
+        r = OrcResult()
+        if self.L.orc_solve_exact_brute(C.byref(self.P), int(idx), C.byref(r)) != 0:
+            raise IndexError(idx)
+        return result_dict(r)
+
+    def solve_exact_many(self, idx):
+        idx = np.ascontiguousarray(idx, dtype=np.int64)
+        res = (OrcResult * max(len(idx), 1))()
+        if self.L.orc_solve_exact_many(C.byref(self.P), _ptr(idx), len(idx), res) != 0:
+            raise IndexError("instance out of range")
+        return [result_dict(r) for r in res[: len(idx)]]
+
     def best(self):
         """Global arg-min over all instances of (objective, instance index)."""
         best = None
@@ -300,10 +327,37 @@ def brute(pp, n, micro, cost):
     return result_dict(r)
 
 
+def latency_1f1b(costs, micro):
+    """1F1B iteration latency of a partition from its stage costs (see the C side)."""
+    c = np.ascontiguousarray(costs, dtype=np.int64)
+    return int(lib().orc_latency_1f1b(len(c), _ptr(c), int(micro)))
+
+
+def dp_exact(pp, n, micro, cost):
+    """1F1B re-scoring of the Pareto frontier on an explicit cost tensor."""
+    cost = np.ascontiguousarray(cost, dtype=np.int64)
+    assert cost.shape == (pp, n + 1, n + 1)
+    r = OrcResult()
+    lib().orc_dp_exact(pp, n, micro, _ptr(cost), C.byref(r))
+    return result_dict(r)
+
+
+def brute_exact(pp, n, micro, cost):
+    """Brute force of the same objective over all compositions."""
+    cost = np.ascontiguousarray(cost, dtype=np.int64)
+    assert cost.shape == (pp, n + 1, n + 1)
+    r = OrcResult()
+    lib().orc_brute_exact(pp, n, micro, _ptr(cost), C.byref(r))
+    return result_dict(r)
+
+
 def solve_worker(args):
-    """multiprocessing helper: (problem, instance indices) -> results."""
-    problem, idx = args
+    """multiprocessing helper: (problem, instance indices[, "exact"]) -> results."""
+    problem, idx = args[0], args[1]
+    if len(args) > 2 and args[2] == "exact":
+        return Oracle(problem).solve_exact_many(idx)
     return Oracle(problem).solve_many(idx)
 
 
-__all__ = ["Oracle", "dp", "brute", "INF", "lib", "solve_worker"]
+__all__ = ["Oracle", "dp", "brute", "dp_exact", "brute_exact", "latency_1f1b", "INF", "lib",
+           "solve_worker"]
