@@ -83,6 +83,38 @@ def copy_calibration(torch, dev, nbytes=1 << 30, reps=3):
     return nbytes
 
 
+def leg_1f1b(torch, pl, stream, steps, warmup):
+    """The same step with the stage DP re-scoring the (max, sum) frontier by the
+    appendix's 1F1B latency (hapmoe_stage_dp_1f1b), timed after the main metric."""
+    import numpy as np
+    pl.eval_cost_tables()
+    pl.stage_dp(stats=True, objective="1f1b")
+    st = pl.stats()
+    relax = int(st[:, 1].astype(np.int64).sum())
+    for _ in range(warmup):
+        pl.run(objective="1f1b")
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    t0 = time.perf_counter()
+    plan = None
+    for k in range(steps):
+        pl.eval_cost_tables()
+        ev[k][0].record(stream)
+        pl.stage_dp(objective="1f1b")
+        ev[k][1].record(stream)
+        plan = pl.best_plan()
+        ev[k][2].record(stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    dp_ms = float(np.mean([ev[k][0].elapsed_time(ev[k][1]) for k in range(steps)]))
+    return {"value": pl.n * steps / elapsed, "unit": "candidates/s", "ms_per_step": elapsed * 1e3 / steps,
+            "stage_dp_ms": dp_ms, "relaxations_per_launch": relax,
+            "dp_passes_per_candidate": {"mean": float(st[:, 0].mean()), "max": int(st[:, 0].max())},
+            "best_plan": {"instance": plan["instance"], "objective_ns": plan["objective"],
+                          "config": plan["config"], "order": plan["order"], "B": plan["n_micro"],
+                          "layers": plan["layers"]}}
+
+
 def cpu_baseline(problem, n_total, n_sample):
     """The oracle as it stands, single thread, on a fixed stride sample."""
     from oracle.oracle import Oracle
@@ -105,6 +137,7 @@ def main():
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--cpu-sample", type=int, default=200)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-1f1b", action="store_true", help="skip the 1F1B re-scoring leg")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (counter scaling for HBM traffic)")
     args = ap.parse_args()
@@ -191,6 +224,8 @@ def main():
                       "config": plan["config"], "order": plan["order"], "B": plan["n_micro"],
                       "layers": plan["layers"], "recompute": plan["recompute"]},
     }
+    if not args.no_1f1b:
+        out["objective_1f1b"] = leg_1f1b(torch, pl, stream, args.steps, args.warmup)
     if calib is not None:
         out["copy_calibration_bytes"] = calib
     if not args.no_cpu_baseline:

@@ -241,6 +241,26 @@ int32_t hapmoe_stage_dp(const hapmoe_problem *p, const void *d_image,
                         hapmoe_dp_result *d_res, int32_t *d_stats,
                         void *d_ws, int64_t ws_bytes, void *stream);
 
+/* Stage DP with the 1F1B iteration latency of the appendix as the objective
+ * (Eq. 4 with its steady-state term, a re-scoring of the threshold DP's
+ * frontier).  Same arguments, ranges, workspace and errors as hapmoe_stage_dp.
+ * For each candidate the (max, sum) Pareto frontier of its feasible partitions
+ * is walked -- the thresholds at which the least stage sum drops, each with the
+ * canonical partition of the threshold DP there -- and every frontier point is
+ * scored with
+ *   T = sum_i c_i + sum_{i <= s} ceil(c_i / 3) + max(0, B - s - 1) * max_i c_i,
+ * s the first (1-based) stage of largest cost (a stage's forward part is
+ * ceil(c / 3), its backward part the rest).  The result keeps the least T,
+ * ties to the lower largest stage: objective = T + C, stage_sum and t_max of the
+ * chosen partition, its recomputation mask and stage lengths.  d_stats as for
+ * hapmoe_stage_dp (passes = DP passes of the frontier walk).  Asynchronous. */
+int32_t hapmoe_stage_dp_1f1b(const hapmoe_problem *p, const void *d_image,
+                             const hapmoe_candidate *d_cand, int64_t n_cand,
+                             const void *d_tables, int64_t tables_bytes,
+                             int64_t first, int64_t count,
+                             hapmoe_dp_result *d_res, int32_t *d_stats,
+                             void *d_ws, int64_t ws_bytes, void *stream);
+
 /* Workspace of hapmoe_best_plan for n results. */
 int32_t hapmoe_best_plan_ws_bytes(const hapmoe_problem *p, int64_t n, int64_t *bytes);
 

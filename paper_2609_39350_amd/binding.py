@@ -97,13 +97,14 @@ def lib():
         L.hapmoe_debug_bytes.argtypes = [P(Problem), P(i64)]
         L.hapmoe_eval_cost_tables.argtypes = [P(Problem), vp, vp, i64, vp, i64, vp, i64, vp]
         L.hapmoe_stage_dp.argtypes = [P(Problem), vp, vp, i64, vp, i64, i64, i64, vp, vp, vp, i64, vp]
+        L.hapmoe_stage_dp_1f1b.argtypes = [P(Problem), vp, vp, i64, vp, i64, i64, i64, vp, vp, vp, i64, vp]
         L.hapmoe_stage_dp_ws_bytes.argtypes = [P(Problem), P(i64)]
         L.hapmoe_tables_layout.argtypes = [P(Problem), P(i64)]
         L.hapmoe_debug_layout.argtypes = [P(Problem), P(i64)]
         L.hapmoe_best_plan_ws_bytes.argtypes = [P(Problem), i64, P(i64)]
         L.hapmoe_best_plan.argtypes = [P(Problem), vp, vp, i64, vp, i64, vp, vp, i64, P(Plan), vp]
         for f in ("hapmoe_validate", "hapmoe_enumerate_candidates", "hapmoe_image_bytes", "hapmoe_pack_image",
-                  "hapmoe_tables_bytes", "hapmoe_debug_bytes", "hapmoe_tables_layout", "hapmoe_debug_layout", "hapmoe_eval_cost_tables", "hapmoe_stage_dp", "hapmoe_stage_dp_ws_bytes",
+                  "hapmoe_tables_bytes", "hapmoe_debug_bytes", "hapmoe_tables_layout", "hapmoe_debug_layout", "hapmoe_eval_cost_tables", "hapmoe_stage_dp", "hapmoe_stage_dp_1f1b", "hapmoe_stage_dp_ws_bytes",
                   "hapmoe_best_plan_ws_bytes", "hapmoe_best_plan"):
             getattr(L, f).restype = C.c_int32
         _LIB = L
@@ -289,6 +290,14 @@ def stage_dp(problem, d_image, d_cand, n_cand, d_tables, first, count, d_res, d_
                                  _dptr(d_ws), _nbytes(d_ws), _stream(stream)), "hapmoe_stage_dp")
 
 
+def stage_dp_1f1b(problem, d_image, d_cand, n_cand, d_tables, first, count, d_res, d_ws, d_stats=None,
+                  stream=None):
+    _check(lib().hapmoe_stage_dp_1f1b(_hp(problem).ref, _dptr(d_image), _dptr(d_cand), int(n_cand),
+                                      _dptr(d_tables), _nbytes(d_tables), int(first), int(count), _dptr(d_res),
+                                      _dptr(d_stats), _dptr(d_ws), _nbytes(d_ws), _stream(stream)),
+           "hapmoe_stage_dp_1f1b")
+
+
 def best_plan(problem, d_cand, d_tables, d_res, n, d_ws, d_config_best=None, stream=None) -> dict:
     plan = Plan()
     _check(lib().hapmoe_best_plan(_hp(problem).ref, _dptr(d_cand), _dptr(d_tables), _nbytes(d_tables),
@@ -335,7 +344,11 @@ class Planner:
     def eval_cost_tables(self, stream=None):
         eval_cost_tables(self.hp, self.d_image, self.d_cand, self.n, self.d_tables, self.d_debug, stream)
 
-    def stage_dp(self, first=0, count=None, stats=False, stream=None):
+    def stage_dp(self, first=0, count=None, stats=False, stream=None, objective="threshold"):
+        """objective "threshold": sum + (B-1) max (hapmoe_stage_dp); "1f1b": the
+        appendix's 1F1B latency over the Pareto frontier (hapmoe_stage_dp_1f1b)."""
+        if objective not in ("threshold", "1f1b"):
+            raise ValueError(objective)
         count = self.n - first if count is None else count
         d_stats = None
         if stats:
@@ -343,16 +356,16 @@ class Planner:
             self.d_stats = d_stats
         res = self.d_res[first * RESULT_DTYPE.itemsize:]
         st = None if d_stats is None else d_stats[4 * first:]
-        stage_dp(self.hp, self.d_image, self.d_cand, self.n, self.d_tables, first, count, res, self.d_dp_ws, st,
-                 stream)
+        call = stage_dp if objective == "threshold" else stage_dp_1f1b
+        call(self.hp, self.d_image, self.d_cand, self.n, self.d_tables, first, count, res, self.d_dp_ws, st, stream)
 
     def best_plan(self, stream=None):
         return best_plan(self.hp, self.d_cand, self.d_tables, self.d_res, self.n, self.d_ws, self.d_config_best,
                          stream)
 
-    def run(self, stats=False, stream=None):
+    def run(self, stats=False, stream=None, objective="threshold"):
         self.eval_cost_tables(stream)
-        self.stage_dp(stats=stats, stream=stream)
+        self.stage_dp(stats=stats, stream=stream, objective=objective)
         return self.best_plan(stream)
 
     # ---- host copies for checks ----

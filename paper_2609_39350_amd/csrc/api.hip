@@ -389,9 +389,12 @@ int32_t hapmoe_stage_dp_ws_bytes(const hapmoe_problem *p, int64_t *bytes)
     return HAPMOE_OK;
 }
 
-int32_t hapmoe_stage_dp(const hapmoe_problem *p, const void *d_image, const hapmoe_candidate *d_cand,
-                        int64_t n_cand, const void *d_tables, int64_t tables_bytes, int64_t first, int64_t count,
-                        hapmoe_dp_result *d_res, int32_t *d_stats, void *d_ws, int64_t ws_bytes, void *stream)
+namespace {
+
+int32_t stage_dp_any(const hapmoe_problem *p, const void *d_image, const hapmoe_candidate *d_cand, int64_t n_cand,
+                     const void *d_tables, int64_t tables_bytes, int64_t first, int64_t count,
+                     hapmoe_dp_result *d_res, int32_t *d_stats, void *d_ws, int64_t ws_bytes, void *stream,
+                     bool exact)
 {
     if (const int32_t e = check_problem(p)) return e;
     if (!d_image || !d_cand || !d_tables || !d_res || !d_ws) return HAPMOE_E_INVAL;
@@ -407,10 +410,29 @@ int32_t hapmoe_stage_dp(const hapmoe_problem *p, const void *d_image, const hapm
     std::vector<int32_t> cfg_pp(S.cfg.size());
     for (size_t i = 0; i < S.cfg.size(); ++i) cfg_pp[i] = S.cfg[i][0];
     if (launch_stage_dp(d_image, d_cand, p->model.n_layers, p->space.n_micro, cfg_pp, (int)S.perm.size(), L,
-                        d_tables, first, count, S.kmax, S.ppmax, d_res, d_stats, d_ws, p->space.micro,
+                        d_tables, first, count, S.kmax, S.ppmax, d_res, d_stats, d_ws, p->space.micro, exact,
                         (hipStream_t)stream) != hipSuccess)
         return HAPMOE_E_HIP;
     return HAPMOE_OK;
+}
+
+}  // namespace
+
+int32_t hapmoe_stage_dp(const hapmoe_problem *p, const void *d_image, const hapmoe_candidate *d_cand,
+                        int64_t n_cand, const void *d_tables, int64_t tables_bytes, int64_t first, int64_t count,
+                        hapmoe_dp_result *d_res, int32_t *d_stats, void *d_ws, int64_t ws_bytes, void *stream)
+{
+    return stage_dp_any(p, d_image, d_cand, n_cand, d_tables, tables_bytes, first, count, d_res, d_stats, d_ws,
+                        ws_bytes, stream, false);
+}
+
+int32_t hapmoe_stage_dp_1f1b(const hapmoe_problem *p, const void *d_image, const hapmoe_candidate *d_cand,
+                             int64_t n_cand, const void *d_tables, int64_t tables_bytes, int64_t first,
+                             int64_t count, hapmoe_dp_result *d_res, int32_t *d_stats, void *d_ws,
+                             int64_t ws_bytes, void *stream)
+{
+    return stage_dp_any(p, d_image, d_cand, n_cand, d_tables, tables_bytes, first, count, d_res, d_stats, d_ws,
+                        ws_bytes, stream, true);
 }
 
 int32_t hapmoe_best_plan_ws_bytes(const hapmoe_problem *p, int64_t n, int64_t *bytes)

@@ -116,7 +116,7 @@ hipError_t launch_stage_dp(const void *d_image, const hapmoe_candidate *d_cand, 
                            const std::vector<int32_t> &config_pp, int n_orders, const TablesLayout &L,
                            const void *d_tables, int64_t first, int64_t count, int kmax, int ppmax,
                            hapmoe_dp_result *d_res, int32_t *d_stats, void *d_ws, const int32_t *micro,
-                           hipStream_t s);
+                           bool exact, hipStream_t s);
 int64_t stage_dp_ws_bytes();
 hipError_t launch_best_plan(const hapmoe_dp_result *d_res, int64_t n, int64_t per_config,
                             int64_t n_configs, int64_t *d_config_best, void *d_ws, hipStream_t s);

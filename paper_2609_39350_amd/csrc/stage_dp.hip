@@ -72,6 +72,14 @@ struct SegCtl {
     int32_t pad;
     uint32_t bt[8];   // back-trace: n_i bytes
     uint32_t rmask, ok;
+    // 1F1B re-scoring: the traced partition's first largest stage s0 (0-based)
+    // and the forward time sum_{i <= s0} ceil(c_i / 3); the pending frontier
+    // candidate (the last point, confirmed once a lower threshold raises the sum)
+    int64_t fwd;
+    int32_t s0, pend;
+    int64_t pF, pM, pfwd;
+    int32_t ps0, prmask, pok, pad2;
+    uint32_t pbt[8];
 };
 
 
@@ -293,7 +301,7 @@ __device__ inline void write_result(hapmoe_dp_result *out, int status, int64_t o
 
 __global__ void k_reset_queue(uint32_t *q) { q[0] = 0; }
 
-template <bool STATS>
+template <bool STATS, bool EXACT>
 __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict__ img,
                                                  const hapmoe_candidate *__restrict__ cand, TablesLayout L,
                                                  const unsigned char *__restrict__ tab, int64_t first,
@@ -742,7 +750,8 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                 {
                     uint8_t *const btb = reinterpret_cast<uint8_t *>(CTL[segi].bt);
                     uint32_t rmask = 0;
-                    int64_t m = 0;
+                    int64_t m = 0, tf = 0, tf_after = 0;   // forward times (1F1B re-scoring)
+                    int s0 = 0;
                     int b = N;
                     bool ok = tracer && fin < kBig;
                     const int pl = rl32(pk2, PP - 1) & 0xffff, kl = N - (rl32(pk1, PP - 1) & 0xff);
@@ -764,6 +773,13 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                         const bool r1 = ai < a0;
                         const int64_t c = (r1 ? ta.y - tb.y : ta.x - tb.x) + rl64(p2p, s);
                         if (ok) {
+                            if (EXACT) {   // walking down, ">=" keeps the first stage of largest cost
+                                if (c >= m) {
+                                    s0 = s;
+                                    tf_after = tf;
+                                }
+                                tf += (c + 2) / 3;
+                            }
                             m = c > m ? c : m;
                             btb[s] = (uint8_t)(b - a);
                             if (r1) rmask |= 1u << s;
@@ -775,6 +791,10 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                     if (tracer) {
                         ok = ok && b == 0;
                         CTL[sg].M = m;
+                        if (EXACT) {
+                            CTL[sg].s0 = s0;
+                            CTL[sg].fwd = tf - tf_after;
+                        }
                         CTL[sg].rmask = rmask;
                         CTL[sg].ok = ok ? 1u : 0u;
                     }
@@ -791,7 +811,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
             };
 
             // this lane's incumbent and its partition
-            int64_t bs = 0, bmx = 0;
+            int64_t bs = 0, bmx = 0, bsum = 0;
             uint32_t pw[8] = {0, 0, 0, 0, 0, 0, 0, 0};
             uint32_t prm = 0, pok = 0;
             const int64_t Bm = (int64_t)Bj - 1;
@@ -829,8 +849,91 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                 segF[q] = CTL[q].G;
                 segok[q] = segF[q] < kBig;
             }
+            const int sjc = sj >= 0 ? sj : 0;   // a candidate's segment, clamped for lanes outside the batch
+            if (EXACT) {
+                // ---- 1F1B re-scoring: walk the whole (max, sum) frontier ----
+                // The last point of a segment is pending until a pass at its max - 1
+                // shows a higher sum (then it is a frontier point and is scored) or
+                // the same sum (then a lower max reaches it and it is dropped); a
+                // point at t_bot is the segment's last frontier point.
+                auto keep_pending = [&]() {   // lane 0 of a segment: the last pass's point
+                    CTL[sg].pend = CTL[sg].F < kBig ? 1 : 0;
+                    CTL[sg].pF = CTL[sg].F;
+                    CTL[sg].pM = CTL[sg].M;
+                    CTL[sg].pfwd = CTL[sg].fwd;
+                    CTL[sg].ps0 = CTL[sg].s0;
+                    CTL[sg].prmask = (int32_t)CTL[sg].rmask;
+                    CTL[sg].pok = (int32_t)CTL[sg].ok;
+                    for (int w = 0; w < 8; ++w) CTL[sg].pbt[w] = CTL[sg].bt[w];
+                };
+                auto score = [&]() {   // a candidate lane offers its segment's pending point
+                    const SegCtl &P = CTL[sjc];
+                    int64_t steady = (int64_t)Bj - P.ps0 - 2;   // B - s - 1 with s = s0 + 1
+                    steady = steady > 0 ? steady : 0;
+                    const int64_t lat = P.pF + P.pfwd + steady * P.pM;
+                    if (lat < bs || (lat == bs && P.pM < bmx)) {
+                        bs = lat;
+                        bmx = P.pM;
+                        bsum = P.pF;
+                        for (int w = 0; w < 8; ++w) pw[w] = P.pbt[w];
+                        prm = (uint32_t)P.prmask;
+                        pok = (uint32_t)P.pok;
+                    }
+                };
+                // A candidate needs no more of the walk once its incumbent is strictly
+                // below the pending point's latency and below a bound for every point
+                // further down: sum >= the pending sum, forward part >= ceil(t_bot/3)
+                // (the largest stage's own), steady part >= max(0, B - PP - 1) t_bot.
+                // Strict, so that a tie, which the lower max would win, still runs.
+                auto needs_more = [&]() {
+                    const SegCtl &P = CTL[sjc];
+                    if (!member || P.pend == 0) return false;
+                    int64_t steady = (int64_t)Bj - P.ps0 - 2;
+                    steady = steady > 0 ? steady : 0;
+                    const int64_t lat = P.pF + P.pfwd + steady * P.pM;
+                    int64_t slb = (int64_t)Bj - PP - 1;
+                    slb = slb > 0 ? slb : 0;
+                    const int64_t lb = P.pF + (P.G + 2) / 3 + slb * P.G;
+                    return !(bs < lat && bs < lb);
+                };
+                uint64_t seg_cands[kMaxSeg];
+#pragma unroll
+                for (int q = 0; q < kMaxSeg; ++q) seg_cands[q] = __builtin_amdgcn_ballot_w64(sj == q);
+                if (seg_live && ll == 0) {
+                    if (CTL[sg].on)
+                        keep_pending();
+                    else
+                        CTL[sg].pend = 0;
+                }
+                if (member) bs = kInf;
+                wave_sync();
+                for (;;) {
+                    bool any = false;
+                    const uint64_t need = __builtin_amdgcn_ballot_w64(needs_more());
+#pragma unroll
+                    for (int q = 0; q < kMaxSeg; ++q) {
+                        if (q >= nseg) continue;
+                        const bool pend = q < nact && CTL[q].pend != 0;
+                        const bool run = pend && CTL[q].pM > CTL[q].G && (need & seg_cands[q]) != 0;
+                        set_ctl(q, run, pend ? CTL[q].pM - 1 : 0);
+                        any |= run;
+                    }
+                    // a pending point at t_bot is the last frontier point
+                    const bool at_bot = member && CTL[sjc].pend != 0 && CTL[sjc].pM <= CTL[sjc].G;
+                    if (at_bot) score();
+                    wave_sync();
+                    if (seg_live && ll == 0 && CTL[sg].pend != 0 && CTL[sg].pM <= CTL[sg].G) CTL[sg].pend = 0;
+                    wave_sync();
+                    if (!any) break;
+                    pass(false);
+                    if (member && CTL[sjc].on && CTL[sjc].F > CTL[sjc].pF) score();   // confirmed
+                    wave_sync();
+                    if (seg_live && ll == 0 && CTL[sg].on) keep_pending();
+                    wave_sync();
+                }
+            }
             int64_t F1 = 0, M1 = 0;
-            if (member) {
+            if (!EXACT && member) {
                 F1 = CTL[sj].F;
                 M1 = CTL[sj].M;
                 bs = kInf;
@@ -840,7 +943,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
             wave_sync();
 
             // ---- 3) the bottleneck threshold itself ----
-            {
+            if (!EXACT) {
                 bool any = false;
 #pragma unroll
                 for (int q = 0; q < kMaxSeg; ++q) {
@@ -857,10 +960,10 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                 wave_sync();
             }
             // lanes of segments where t_bot >= M1 are already final
-            const bool sweeping = member && tbot < M1;
+            const bool sweeping = !EXACT && member && tbot < M1;
 
             // ---- 4) descending Pareto sweep ----
-            for (;;) {
+            while (!EXACT) {
                 const bool done = bmx == tbot && bs == F1 + Bm * tbot;   // reached the lower bound
                 const bool act = sweeping && !done && F + Bm * tbot <= bs;
                 const int64_t lim = act ? (Bm > 0 ? (bs - F) / Bm : kBig) : -1;
@@ -890,7 +993,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
             // ---- 5) results ----
             if (member) {
                 if (pok)
-                    write_result(out, HAPMOE_STATUS_OK, bs + ki->dp_const, bs - Bm * bmx, bmx, prm, pw);
+                    write_result(out, HAPMOE_STATUS_OK, bs + ki->dp_const, EXACT ? bsum : bs - Bm * bmx, bmx, prm, pw);
                 else
                     write_result(out, HAPMOE_STATUS_OVERFLOW, kInf, kInf, kInf, 0, zero_words);
             }
@@ -936,7 +1039,7 @@ hipError_t launch_stage_dp(const void *d_image, const hapmoe_candidate *d_cand, 
                            const std::vector<int32_t> &config_pp, int n_orders, const TablesLayout &L,
                            const void *d_tables, int64_t first, int64_t count, int kmax, int ppmax,
                            hapmoe_dp_result *d_res, int32_t *d_stats, void *d_ws, const int32_t *micro,
-                           hipStream_t s)
+                           bool exact, hipStream_t s)
 {
     (void)config_pp;
     (void)micro;
@@ -962,7 +1065,8 @@ hipError_t launch_stage_dp(const void *d_image, const hapmoe_candidate *d_cand, 
                            key_lo, n_keys, S, d_res, d_stats, queue);
         return hipGetLastError();
     };
-    return d_stats ? go(k_stage_dp<true>) : go(k_stage_dp<false>);
+    if (exact) return d_stats ? go(k_stage_dp<true, true>) : go(k_stage_dp<false, true>);
+    return d_stats ? go(k_stage_dp<true, false>) : go(k_stage_dp<false, false>);
 }
 
 }  // namespace hapmoe

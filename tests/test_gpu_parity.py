@@ -29,13 +29,15 @@ def _pool():
     return _POOL
 
 
-def oracle_many(problem, idx):
+def oracle_many(problem, idx, objective="threshold"):
     idx = [int(i) for i in idx]
     if len(idx) < 64:
-        return orc.Oracle(problem).solve_many(idx)
+        o = orc.Oracle(problem)
+        return o.solve_many(idx) if objective == "threshold" else o.solve_exact_many(idx)
     n = _pool()._processes
     parts = [idx[k::n] for k in range(n)]
-    outs = _pool().map(orc.solve_worker, [(problem, part) for part in parts])
+    mode = "main" if objective == "threshold" else "exact"
+    outs = _pool().map(orc.solve_worker, [(problem, part, mode) for part in parts])
     res = [None] * len(idx)
     for k, out in enumerate(outs):
         for j, r in enumerate(out):
@@ -51,10 +53,10 @@ def torch():
     return t
 
 
-def compare(problem, planner, idx, res=None):
+def compare(problem, planner, idx, res=None, objective="threshold"):
     """Element-by-element parity of the DP results at candidate indices idx."""
     res = planner.results() if res is None else res
-    ref = oracle_many(problem, idx)
+    ref = oracle_many(problem, idx, objective)
     bad = []
     for i, r in zip(idx, ref):
         g = res[i]
@@ -330,3 +332,50 @@ def test_config4_full_launch_sampled(torch):
     assert plan["instance"] == int(np.argmin(obj))
     idx = list(range(11, pl.n, 25013)) + [plan["instance"]]
     compare(p, pl, sorted(set(idx)), res)
+
+
+# ------------------------------------------------- 1F1B re-scoring objective
+@pytest.mark.parametrize("n", [1, 2])
+def test_1f1b_small_configs_every_candidate(torch, n):
+    p = workloads.config(n)
+    print(f"1f1b config {n}: all candidates", flush=True)
+    pl = binding.Planner(p, "cuda:0")
+    plan = pl.run(objective="1f1b")
+    assert compare(p, pl, range(pl.n), objective="1f1b") > 0
+    res = pl.results()
+    obj = np.where(res["status"] == 0, res["objective"], np.iinfo(np.int64).max)
+    assert plan["instance"] == int(np.argmin(obj)) and plan["objective"] == int(obj.min())
+
+
+def test_1f1b_random_and_tied_every_candidate(torch):
+    probs = [workloads.random_tiny(s) for s in range(20)]
+    probs += [_uniform_layers(workloads.config(1))]
+    q = _uniform_layers(workloads.config(2))
+    q["space"]["micro"] = np.arange(1, 17, dtype=np.int32)
+    probs.append(q)
+    total = 0
+    for p in probs:
+        print(f"1f1b {p.get('name', '')}", flush=True)
+        pl = binding.Planner(p, "cuda:0")
+        pl.eval_cost_tables()
+        pl.stage_dp(objective="1f1b")
+        total += compare(p, pl, range(pl.n), objective="1f1b")
+    assert total > 100
+
+
+@pytest.mark.parametrize("n,stride", [(3, 211), (5, 211), (4, 40009)])
+def test_1f1b_large_configs_sampled(torch, n, stride):
+    p = workloads.config(n)
+    print(f"1f1b config {n}: stride-{stride} sample", flush=True)
+    pl = binding.Planner(p, "cuda:0")
+    plan = pl.run(objective="1f1b")
+    idx = list(range(7, pl.n, stride)) + [pl.n - 1]
+    if plan["instance"] >= 0:
+        idx.append(plan["instance"])
+    compare(p, pl, sorted(set(idx)), objective="1f1b")
+    res = pl.results()
+    obj = np.where(res["status"] == 0, res["objective"], np.iinfo(np.int64).max)
+    assert plan["instance"] == int(np.argmin(obj))
+    # the same candidates are feasible under both objectives
+    pl.stage_dp()
+    assert np.array_equal(pl.results()["status"], res["status"])
