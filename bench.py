@@ -115,14 +115,18 @@ def leg_1f1b(torch, pl, stream, steps, warmup):
                           "layers": plan["layers"]}}
 
 
-def cpu_baseline(problem, n_total, n_sample):
-    """The oracle as it stands, single thread, on a fixed stride sample."""
+def cpu_baseline(problem, n_total, n_sample, exact=False):
+    """The oracle as it stands, single thread, on a fixed stride sample (exact:
+    its 1F1B re-scoring of the frontier)."""
     from oracle.oracle import Oracle
     o = Oracle(problem)
     stride = max(1, n_total // n_sample)
     idx = list(range(stride // 2, n_total, stride))[:n_sample]
     t0 = time.perf_counter()
-    o.solve_many(idx)
+    if exact:
+        o.solve_exact_many(idx)
+    else:
+        o.solve_many(idx)
     dt = time.perf_counter() - t0
     return {"value": len(idx) / dt, "unit": "candidates/s", "cores": 1, "kind": "oracle",
             "sample": f"{len(idx)} candidates at stride {stride} of {n_total} (every {stride}th), "
@@ -135,7 +139,8 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", type=int, default=4)
-    ap.add_argument("--cpu-sample", type=int, default=200)
+    ap.add_argument("--cpu-sample", type=int, default=400)
+    ap.add_argument("--cpu-sample-1f1b", type=int, default=200)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-1f1b", action="store_true", help="skip the 1F1B re-scoring leg")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -226,6 +231,8 @@ def main():
     }
     if not args.no_1f1b:
         out["objective_1f1b"] = leg_1f1b(torch, pl, stream, args.steps, args.warmup)
+        if not args.no_cpu_baseline:
+            out["objective_1f1b"]["cpu_baseline"] = cpu_baseline(problem, n, args.cpu_sample_1f1b, exact=True)
     if calib is not None:
         out["copy_calibration_bytes"] = calib
     if not args.no_cpu_baseline:
