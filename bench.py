@@ -83,6 +83,32 @@ def copy_calibration(torch, dev, nbytes=1 << 30, reps=3):
     return nbytes
 
 
+def leg_uniform(binding, problem, pl, dev):
+    """Ablation analogue (non-uniform layer assignment disabled): the same
+    candidates with every stage holding floor/ceil(N/PP) layers; best objective
+    of each, globally and at the largest micro-batch count."""
+    import copy
+    import numpy as np
+    pu_problem = copy.deepcopy(problem)
+    pu_problem["params"]["prune_window"] = 2
+    pu = binding.Planner(pu_problem, dev)
+    pu.run()
+    out = {}
+    micro = np.asarray(problem["space"]["micro"])
+    bmax = int(micro.max())
+    for name, planner in (("non_uniform", pl), ("uniform", pu)):
+        planner.run()
+        res = planner.results()
+        obj = np.where(res["status"] == 0, res["objective"], np.iinfo(np.int64).max)
+        at_bmax = obj[planner.cand_host["n_micro"] == bmax]
+        out[name] = {"best_ns": int(obj.min()), f"best_at_B{bmax}_ns": int(at_bmax.min()),
+                     "feasible": int((res["status"] == 0).sum())}
+    nu, un = out["non_uniform"], out["uniform"]
+    out["latency_increase"] = un["best_ns"] / nu["best_ns"] - 1.0
+    out[f"latency_increase_at_B{bmax}"] = un[f"best_at_B{bmax}_ns"] / nu[f"best_at_B{bmax}_ns"] - 1.0
+    return out
+
+
 def leg_1f1b(torch, pl, stream, steps, warmup):
     """The same step with the stage DP re-scoring the (max, sum) frontier by the
     appendix's 1F1B latency (hapmoe_stage_dp_1f1b), timed after the main metric."""
@@ -229,6 +255,7 @@ def main():
                       "config": plan["config"], "order": plan["order"], "B": plan["n_micro"],
                       "layers": plan["layers"], "recompute": plan["recompute"]},
     }
+    out["ablation_uniform_layers"] = leg_uniform(binding, problem, pl, dev)
     if not args.no_1f1b:
         out["objective_1f1b"] = leg_1f1b(torch, pl, stream, args.steps, args.warmup)
         if not args.no_cpu_baseline:

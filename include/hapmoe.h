@@ -102,7 +102,9 @@ typedef struct hapmoe_params {
     int32_t delta_num;       /* pruning-1 tolerance delta = delta_num / delta_den */
     int32_t delta_den;
     int32_t eta_prune;       /* pruning-3 factor eta */
-    int32_t prune_window;    /* pruning 1 on/off */
+    int32_t prune_window;    /* layer windows: 0 none, 1 pruning 1 (Section 3.4), 2 uniform:
+                                every stage holds floor(N/PP)..ceil(N/PP) layers (non-uniform
+                                assignment disabled, the ablation of the evaluation) */
     int32_t prune_hetero;    /* pruning 3 on/off */
     int32_t allow_recompute; /* r in {0, 1} (1) or r = 0 only (0) */
 } hapmoe_params;

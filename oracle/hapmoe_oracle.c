@@ -38,6 +38,7 @@ int32_t orc_validate(const orc_problem *p)
     if (!(p->rc_time >= 1.0) || !(p->rc_act >= 0.0 && p->rc_act <= 1.0)) return -1;
     if (!(p->gamma >= 0.0 && p->gamma <= 1.0) || !(p->opt_coef >= 0.0) || !(p->moe_ffn_mult >= 0.0)) return -1;
     if (p->delta_den < 1 || p->delta_num < 0 || p->delta_num >= p->delta_den || p->eta_prune < 0) return -1;
+    if (p->prune_window < 0 || p->prune_window > 2) return -1;
     if (p->n_micro < 1 || p->n_micro > ORC_MAX_MICRO) return -1;
     if (p->pp_max < 1 || p->pp_max > ORC_MAX_STAGES || p->mode < 0 || p->mode > 1) return -1;
     for (int i = 0; i < p->n_micro; i++)
@@ -379,6 +380,11 @@ int32_t orc_stages(const orc_problem *p, const orc_config *c, int32_t order, int
         if (!p->prune_window) {
             st[s].lo = 1;
             st[s].hi = (int32_t)N;
+            continue;
+        }
+        if (p->prune_window == 2) {   /* uniform assignment (the ablation): floor / ceil of N / PP */
+            st[s].lo = (int32_t)(N / PP);
+            st[s].hi = (int32_t)((N + PP - 1) / PP);
             continue;
         }
         int64_t den = dd * sum_speed;

@@ -58,7 +58,8 @@ typedef struct orc_problem {
     /* method parameters */
     double gamma, rc_time, rc_act, opt_coef;
     int32_t delta_num, delta_den, eta_prune;
-    int32_t prune_window, prune_hetero, allow_recompute;
+    int32_t prune_window;          /* 0 none, 1 pruning-1 windows, 2 uniform floor/ceil(N/PP) */
+    int32_t prune_hetero, allow_recompute;
     /* search space */
     int32_t pp_max, tp_mask, cp_mask, ep_max, tpe_mask, mode;
     int32_t n_micro;

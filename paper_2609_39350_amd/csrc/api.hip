@@ -61,6 +61,7 @@ int32_t check_problem(const hapmoe_problem *p)
     if (q.delta_den < 1 || q.delta_den > 1000000 || q.delta_num < 0 || q.delta_num >= q.delta_den)
         return HAPMOE_E_INVAL;
     if (q.eta_prune < 0 || q.eta_prune > 1000000) return HAPMOE_E_INVAL;
+    if (q.prune_window < 0 || q.prune_window > 2) return HAPMOE_E_INVAL;
     if (s.pp_max < 1 || s.pp_max > kMaxStages || s.mode < 0 || s.mode > 1 || s.ep_max < 1) return HAPMOE_E_INVAL;
     if (s.tp_mask < 0 || s.tp_mask > 15 || s.cp_mask < 0 || s.cp_mask > 15 || s.tpe_mask < 0 || s.tpe_mask > 15)
         return HAPMOE_E_INVAL;
@@ -286,7 +287,7 @@ int32_t hapmoe_pack_image(const hapmoe_problem *p, void *h_image, int64_t bytes)
     H.delta_num = q.delta_num;
     H.delta_den = q.delta_den;
     H.eta_prune = q.eta_prune;
-    H.prune_window = q.prune_window ? 1 : 0;
+    H.prune_window = q.prune_window;   // 0, 1 or 2 (checked)
     H.prune_hetero = q.prune_hetero ? 1 : 0;
     H.allow_recompute = q.allow_recompute ? 1 : 0;
     H.n_orders = (int32_t)S.perm.size();

@@ -170,7 +170,10 @@ __global__ __launch_bounds__(kThreads) void k_cost_tables(const unsigned char *_
         const int64_t den = dd * sum_speed;
         for (int s = 0; s < c.pp; ++s) {
             int64_t lo = 1, hi = N;
-            if (H.prune_window) {
+            if (H.prune_window == 2) {   // uniform: floor(N / PP) .. ceil(N / PP) layers per stage
+                lo = N / c.pp;
+                hi = (N + c.pp - 1) / c.pp;
+            } else if (H.prune_window) {
                 lo = ((dd - dn) * spd[s] * (int64_t)N) / den;
                 hi = ((dd + dn) * spd[s] * (int64_t)N + den - 1) / den;
                 lo = lo < 1 ? 1 : lo;

@@ -71,12 +71,15 @@ def test_validation_rejects_bad_input():
         {"space.micro": [2000]},
         {"cluster.bw": np.zeros((2, 2))},
         {"model.is_moe": np.array([2, 1], dtype=np.uint8)},
+        {"params.prune_window": 3},
+        {"params.prune_window": -1},
     ]
     for ch in bad:
         with pytest.raises(binding.HapmoeError) as e:
             binding.validate(variant(base, **ch))
         assert e.value.code == -1, ch
     binding.validate(base)
+    binding.validate(variant(base, **{"params.prune_window": 2}))
 
 
 def test_capacity_and_sizes():

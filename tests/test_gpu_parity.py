@@ -379,3 +379,26 @@ def test_1f1b_large_configs_sampled(torch, n, stride):
     # the same candidates are feasible under both objectives
     pl.stage_dp()
     assert np.array_equal(pl.results()["status"], res["status"])
+
+
+# ------------------------------------------ uniform layers (ablation windows)
+@pytest.mark.parametrize("n,stride", [(2, 1), (3, 53)])
+def test_uniform_layers(torch, n, stride):
+    p = variant(workloads.config(n), **{"params.prune_window": 2})
+    print(f"uniform layers config {n}: stride {stride}", flush=True)
+    pl = binding.Planner(p, "cuda:0")
+    plan = pl.run()
+    idx = list(range(0, pl.n, stride)) + [pl.n - 1, plan["instance"]]
+    assert compare(p, pl, sorted(set(idx))) > 0
+    pl.stage_dp(objective="1f1b")
+    compare(p, pl, sorted(set(idx))[::7], objective="1f1b")
+
+
+def test_best_plan_launcher_text(torch):
+    from paper_2609_39350_amd import launcher
+    p = workloads.config(1)
+    pl = binding.Planner(p, "cuda:0")
+    plan = pl.run()
+    text = launcher.plan_to_launcher(p, plan)
+    assert f"--pipeline-model-parallel-size {plan['config'][0]}" in text
+    assert 'PIPELINE_STAGE_LAYERS="' + ",".join(str(n) for n in plan["layers"]) + '"' in text
