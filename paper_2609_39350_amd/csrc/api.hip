@@ -103,6 +103,7 @@ void build_space(const hapmoe_problem *p, Space &S)
             if (m.n_experts % e == 0) eps.push_back(e);
     }
     S.cfg.clear();
+    S.cfg.reserve(4096);
     S.kmax = 1;
     S.ppmax = 1;
     for (int PP = 1; PP <= std::min(G, std::min(sp.pp_max, m.n_layers)); ++PP) {
@@ -461,25 +462,28 @@ int32_t hapmoe_best_plan(const hapmoe_problem *p, const hapmoe_candidate *d_cand
     if (ws_bytes < best_plan_ws_bytes(n, per, ncfg)) return HAPMOE_E_WORKSPACE;
     if (const int e = check_arch()) return e;
     hipStream_t s = (hipStream_t)stream;
-    if (launch_best_plan(d_res, n, per, ncfg, d_config_best, d_ws, s) != hipSuccess) return HAPMOE_E_HIP;
-    int64_t best[2];
-    if (hipMemcpyAsync(best, d_ws, sizeof(best), hipMemcpyDeviceToHost, s) != hipSuccess) return HAPMOE_E_HIP;
+    const auto *tab = static_cast<const unsigned char *>(d_tables);
+    if (launch_best_plan(d_res, d_cand, tab + L.off_key, p->space.n_micro, n, per, ncfg, d_config_best, d_ws, s) !=
+        hipSuccess)
+        return HAPMOE_E_HIP;
+    // one copy: the global (objective, index) pair and the winner's records
+    struct {
+        int64_t best[2];
+        hapmoe_dp_result r;
+        hapmoe_candidate cd;
+        KeyInfo ki;
+        unsigned char pad[kWinnerBytes - sizeof(hapmoe_dp_result) - sizeof(hapmoe_candidate) - sizeof(KeyInfo)];
+    } h;
+    static_assert(sizeof(h) == 16 + kWinnerBytes, "winner layout");
+    if (hipMemcpyAsync(&h, d_ws, sizeof(h), hipMemcpyDeviceToHost, s) != hipSuccess) return HAPMOE_E_HIP;
     if (hipStreamSynchronize(s) != hipSuccess) return HAPMOE_E_HIP;
     std::memset(h_plan, 0, sizeof(*h_plan));
     h_plan->instance = -1;
-    if (best[0] == kInf) return HAPMOE_E_INFEASIBLE;
-    const int64_t idx = best[1];
-    hapmoe_dp_result r;
-    hapmoe_candidate cd;
-    KeyInfo ki;
-    const int64_t key = idx / p->space.n_micro;
-    const auto *tab = static_cast<const unsigned char *>(d_tables);
-    if (hipMemcpyAsync(&r, d_res + idx, sizeof(r), hipMemcpyDeviceToHost, s) != hipSuccess ||
-        hipMemcpyAsync(&cd, d_cand + idx, sizeof(cd), hipMemcpyDeviceToHost, s) != hipSuccess ||
-        hipMemcpyAsync(&ki, tab + L.off_key + key * (int64_t)sizeof(KeyInfo), sizeof(ki), hipMemcpyDeviceToHost,
-                       s) != hipSuccess ||
-        hipStreamSynchronize(s) != hipSuccess)
-        return HAPMOE_E_HIP;
+    if (h.best[0] == kInf) return HAPMOE_E_INFEASIBLE;
+    const int64_t idx = h.best[1];
+    const hapmoe_dp_result &r = h.r;
+    const hapmoe_candidate &cd = h.cd;
+    const KeyInfo &ki = h.ki;
     h_plan->instance = idx;
     h_plan->objective = r.objective;
     h_plan->stage_sum = r.stage_sum;

@@ -99,28 +99,50 @@ __global__ __launch_bounds__(1024) void k_global(const Best *__restrict__ cfg_be
 
 int64_t chunks_per_config(int64_t per) { return (per + kChunk - 1) / kChunk; }
 
+// The winner's result, candidate and stage layout, copied next to the global
+// best so that the host reads everything with one copy.
+__global__ __launch_bounds__(64) void k_gather(const Best *__restrict__ glob, const hapmoe_dp_result *__restrict__ res,
+                                               const hapmoe_candidate *__restrict__ cand,
+                                               const unsigned char *__restrict__ key_info, int64_t n_micro,
+                                               uint32_t *__restrict__ out)
+{
+    const Best b = *glob;
+    if (b.obj == kInf) return;
+    const int w = threadIdx.x;
+    constexpr int kRes = (int)sizeof(hapmoe_dp_result) / 4, kCand = (int)sizeof(hapmoe_candidate) / 4;
+    constexpr int kKey = (int)sizeof(KeyInfo) / 4;
+    if (w < kRes) out[w] = reinterpret_cast<const uint32_t *>(res + b.idx)[w];
+    if (w < kCand) out[kRes + w] = reinterpret_cast<const uint32_t *>(cand + b.idx)[w];
+    const auto *ki = reinterpret_cast<const uint32_t *>(key_info + (b.idx / n_micro) * (int64_t)sizeof(KeyInfo));
+    for (int i = w; i < kKey; i += 64) out[kRes + kCand + i] = ki[i];
+}
+
 }  // namespace
 
-// workspace: [global Best][cfg_best n_configs][partial n_configs * chunks]
+// workspace: [global Best][winner: result | candidate | stage layout][cfg_best
+// n_configs][partial n_configs * chunks]
 int64_t best_plan_ws_bytes(int64_t n, int64_t per_config, int64_t n_configs)
 {
     (void)n;
     const int64_t chunks = chunks_per_config(per_config);
-    return (int64_t)sizeof(Best) * (1 + n_configs + n_configs * chunks);
+    return (int64_t)sizeof(Best) * (1 + n_configs + n_configs * chunks) + kWinnerBytes;
 }
 
-hipError_t launch_best_plan(const hapmoe_dp_result *d_res, int64_t n, int64_t per_config, int64_t n_configs,
-                            int64_t *d_config_best, void *d_ws, hipStream_t s)
+hipError_t launch_best_plan(const hapmoe_dp_result *d_res, const hapmoe_candidate *d_cand,
+                            const unsigned char *d_key_info, int64_t n_micro, int64_t n, int64_t per_config,
+                            int64_t n_configs, int64_t *d_config_best, void *d_ws, hipStream_t s)
 {
     const int64_t chunks = chunks_per_config(per_config);
     Best *glob = static_cast<Best *>(d_ws);
-    Best *cfg_best = glob + 1;
+    auto *winner = reinterpret_cast<uint32_t *>(static_cast<unsigned char *>(d_ws) + sizeof(Best));
+    Best *cfg_best = reinterpret_cast<Best *>(static_cast<unsigned char *>(d_ws) + sizeof(Best) + kWinnerBytes);
     Best *partial = cfg_best + n_configs;
     hipLaunchKernelGGL(k_seg_partial, dim3((unsigned)n_configs, (unsigned)chunks), dim3(kThreads), 0, s, d_res, n,
                        per_config, chunks, partial);
     hipLaunchKernelGGL(k_seg_final, dim3((unsigned)((n_configs + kThreads - 1) / kThreads)), dim3(kThreads), 0, s,
                        partial, n_configs, chunks, cfg_best, d_config_best);
     hipLaunchKernelGGL(k_global, dim3(1), dim3(1024), 0, s, cfg_best, n_configs, glob);
+    hipLaunchKernelGGL(k_gather, dim3(1), dim3(64), 0, s, glob, d_res, d_cand, d_key_info, n_micro, winner);
     return hipGetLastError();
 }
 

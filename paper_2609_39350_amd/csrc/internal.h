@@ -118,7 +118,13 @@ hipError_t launch_stage_dp(const void *d_image, const hapmoe_candidate *d_cand, 
                            hapmoe_dp_result *d_res, int32_t *d_stats, void *d_ws, const int32_t *micro,
                            bool exact, hipStream_t s);
 int64_t stage_dp_ws_bytes();
-hipError_t launch_best_plan(const hapmoe_dp_result *d_res, int64_t n, int64_t per_config,
+// bytes of the winner record in the best-plan workspace (result, candidate, stage layout)
+constexpr int64_t kWinnerBytes = 256;
+static_assert(sizeof(hapmoe_dp_result) + sizeof(hapmoe_candidate) + sizeof(KeyInfo) <= kWinnerBytes, "winner");
+static_assert(sizeof(hapmoe_dp_result) % 4 == 0 && sizeof(hapmoe_candidate) % 4 == 0 && sizeof(KeyInfo) % 4 == 0,
+              "word copies");
+hipError_t launch_best_plan(const hapmoe_dp_result *d_res, const hapmoe_candidate *d_cand,
+                            const unsigned char *d_key_info, int64_t n_micro, int64_t n, int64_t per_config,
                             int64_t n_configs, int64_t *d_config_best, void *d_ws, hipStream_t s);
 int64_t best_plan_ws_bytes(int64_t n, int64_t per_config, int64_t n_configs);
 
