@@ -173,8 +173,8 @@ def main():
                     help="also run a 1 GiB device copy (counter scaling for HBM traffic)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: the planner's candidates are independent and this build "
-              "has no multi-GPU path (see DESIGN.md for how it would shard). Run with --gpus 1.",
+        print("bench.py measures one GPU only: the planner's candidates are independent and are evaluated "
+              "on a single device here (there is no multi-GPU path). Run with --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
 

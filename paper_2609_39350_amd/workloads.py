@@ -301,12 +301,12 @@ def config5(seed=5, mem_scale=None):
             "params": _default_params(), "space": _space(16, 64, [16, 32, 64])}
 
 
-CONFIGS = {1: config1, 2: config2, 3: config3, 4: config4, 5: config5}
+_WORKLOADS = {1: config1, 2: config2, 3: config3, 4: config4, 5: config5}
 
 
 def config(n, **kw):
     """Synthetic problem of config ``n`` (1..5)."""
-    return _check_problem(CONFIGS[n](**kw))
+    return _check_problem(_WORKLOADS[n](**kw))
 
 
 def random_tiny(seed, n_layers=None, n_types=None, max_pp=4, micro=None, flags=None):
