@@ -92,20 +92,22 @@ def leg_uniform(binding, problem, pl, dev):
     pu_problem = copy.deepcopy(problem)
     pu_problem["params"]["prune_window"] = 2
     pu = binding.Planner(pu_problem, dev)
-    pu.run()
     out = {}
     micro = np.asarray(problem["space"]["micro"])
     bmax = int(micro.max())
+    big = np.iinfo(np.int64).max
     for name, planner in (("non_uniform", pl), ("uniform", pu)):
-        planner.run()
+        planner.eval_cost_tables()
+        planner.stage_dp()
         res = planner.results()
-        obj = np.where(res["status"] == 0, res["objective"], np.iinfo(np.int64).max)
+        obj = np.where(res["status"] == 0, res["objective"], big)
         at_bmax = obj[planner.cand_host["n_micro"] == bmax]
-        out[name] = {"best_ns": int(obj.min()), f"best_at_B{bmax}_ns": int(at_bmax.min()),
+        out[name] = {"best_ns": int(obj.min()) if obj.min() < big else None,
+                     f"best_at_B{bmax}_ns": int(at_bmax.min()) if at_bmax.min() < big else None,
                      "feasible": int((res["status"] == 0).sum())}
     nu, un = out["non_uniform"], out["uniform"]
-    out["latency_increase"] = un["best_ns"] / nu["best_ns"] - 1.0
-    out[f"latency_increase_at_B{bmax}"] = un[f"best_at_B{bmax}_ns"] / nu[f"best_at_B{bmax}_ns"] - 1.0
+    for key, name in (("best_ns", "latency_increase"), (f"best_at_B{bmax}_ns", f"latency_increase_at_B{bmax}")):
+        out[name] = un[key] / nu[key] - 1.0 if un[key] and nu[key] else None
     return out
 
 
