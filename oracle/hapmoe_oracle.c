@@ -41,6 +41,7 @@ int32_t orc_validate(const orc_problem *p)
     if (p->prune_window < 0 || p->prune_window > 2) return -1;
     if (p->n_micro < 1 || p->n_micro > ORC_MAX_MICRO) return -1;
     if (p->pp_max < 1 || p->pp_max > ORC_MAX_STAGES || p->mode < 0 || p->mode > 1) return -1;
+    if (p->stage_types < 0 || p->stage_types > 1) return -1;
     for (int i = 0; i < p->n_micro; i++)
         if (p->micro[i] < 1 || p->micro[i] > (1 << 20)) return -1;
     return 0;
@@ -65,6 +66,11 @@ int64_t orc_enumerate(const orc_problem *p, orc_config *out, int64_t cap)
     for (int PP = 1; PP <= G; PP++) {
         if (G % PP != 0 || PP > p->pp_max || PP > p->n_layers) continue;
         int g = G / PP;
+        if (p->stage_types) {   /* free per-stage type: every stage is one type's group */
+            int whole = 1;
+            for (int h = 0; h < p->n_types; h++) whole &= p->count[h] % g == 0;
+            if (!whole) continue;
+        }
         for (int i = 0; i < 4; i++) {
             int TP = 1 << i;
             if (!((p->tp_mask >> i) & 1) || g % TP != 0 || p->hidden % TP != 0) continue;
@@ -98,12 +104,74 @@ int64_t orc_enumerate(const orc_problem *p, orc_config *out, int64_t cap)
     return n;
 }
 
-/* Device-type orderings: all permutations of the type indices, lexicographic. */
+/* number of distinct stage-type sequences of a pp-stage pipeline: the
+ * multinomial pp! / prod_h k_h! with k_h = m_h / g, built one stage at a time
+ * (each step multiplies by r / i >= 1, so it never falls); capped at INT32_MAX */
+static int64_t n_sequences(const orc_problem *p, int pp)
+{
+    int G = 0;
+    for (int h = 0; h < p->n_types; h++) G += p->count[h];
+    int g = G / pp, r = 0;
+    int64_t n = 1;
+    for (int h = 0; h < p->n_types; h++)
+        for (int i = 1; i <= p->count[h] / g; i++) {
+            r++;
+            n = n * r / i;
+            if (n > INT32_MAX) return INT32_MAX;
+        }
+    return n;
+}
+
+/* Device-type orderings: all permutations of the type indices, lexicographic;
+ * with free per-stage types, the largest number of stage-type sequences over
+ * the configurations (a configuration with fewer has empty slots). */
 int32_t orc_n_orders(const orc_problem *p)
 {
+    if (p->stage_types) {
+        int64_t ncfg = orc_enumerate(p, NULL, 0), best = 1;
+        orc_config *all = (orc_config *)malloc(sizeof(orc_config) * (size_t)(ncfg > 0 ? ncfg : 1));
+        orc_enumerate(p, all, ncfg);
+        for (int64_t i = 0; i < ncfg; i++) {
+            int64_t n = n_sequences(p, all[i].pp);
+            if (n > best) best = n;
+        }
+        free(all);
+        return (int32_t)best;
+    }
     int f = 1;
     for (int i = 2; i <= p->n_types; i++) f *= i;
     return f;
+}
+
+/* next arrangement of a multiset in lexicographic order; 0 after the last */
+static int next_arrangement(int32_t *v, int n)
+{
+    int i = n - 2;
+    while (i >= 0 && v[i] >= v[i + 1]) i--;
+    if (i < 0) return 0;
+    int j = n - 1;
+    while (v[j] <= v[i]) j--;
+    int32_t t = v[i];
+    v[i] = v[j];
+    v[j] = t;
+    for (int a = i + 1, b = n - 1; a < b; a++, b--) {
+        t = v[a];
+        v[a] = v[b];
+        v[b] = t;
+    }
+    return 1;
+}
+
+int32_t orc_sequence(const orc_problem *p, int32_t pp, int32_t o, int32_t *seq)
+{
+    int G = 0;
+    for (int h = 0; h < p->n_types; h++) G += p->count[h];
+    int g = G / pp, k = 0;
+    for (int h = 0; h < p->n_types; h++)
+        for (int i = 0; i < p->count[h] / g; i++) seq[k++] = h;
+    for (int32_t i = 0; i < o; i++)
+        if (!next_arrangement(seq, pp)) return -1;
+    return 0;
 }
 
 void orc_order(const orc_problem *p, int32_t o, int32_t *perm)
@@ -340,7 +408,12 @@ static int dev_type(const orc_problem *p, const int *perm, int d)
 int32_t orc_stages(const orc_problem *p, const orc_config *c, int32_t order, int32_t micro, orc_stage *st)
 {
     int perm[ORC_MAX_TYPES];
-    orc_order(p, order, perm);
+    int32_t seq[ORC_MAX_STAGES];
+    if (p->stage_types) {   /* free per-stage type: stage s is one group of type seq[s] */
+        if (orc_sequence(p, c->pp, order, seq)) return -1;
+    } else {
+        orc_order(p, order, perm);
+    }
     int G = 0;
     for (int h = 0; h < p->n_types; h++) G += p->count[h];
     int PP = c->pp, g = G / PP;
@@ -349,9 +422,14 @@ int32_t orc_stages(const orc_problem *p, const orc_config *c, int32_t order, int
         orc_stage *x = &st[s];
         int lo = s * g, hi = lo + g;
         x->mask = 0;
-        for (int d = lo; d < hi; d++) x->mask |= 1 << dev_type(p, perm, d);
-        x->first_type = dev_type(p, perm, lo);
-        x->last_type = dev_type(p, perm, hi - 1);
+        if (p->stage_types) {
+            x->mask = 1 << seq[s];
+            x->first_type = x->last_type = seq[s];
+        } else {
+            for (int d = lo; d < hi; d++) x->mask |= 1 << dev_type(p, perm, d);
+            x->first_type = dev_type(p, perm, lo);
+            x->last_type = dev_type(p, perm, hi - 1);
+        }
         x->cap = -1;
         x->speed = 0;
         for (int h = 0; h < p->n_types; h++) {
@@ -362,7 +440,7 @@ int32_t orc_stages(const orc_problem *p, const orc_config *c, int32_t order, int
         mask_link(p, x->mask, &x->alpha, &x->bw);
         x->mixed = popc(x->mask) > 1;
         if (s < PP - 1) {
-            int nt = dev_type(p, perm, hi);
+            int nt = p->stage_types ? seq[s + 1] : dev_type(p, perm, hi);
             x->bdiff = nt != x->last_type;
             x->p2p = orc_p2p(p, c, x->last_type, nt);
         } else {
@@ -402,7 +480,7 @@ int32_t orc_stages(const orc_problem *p, const orc_config *c, int32_t order, int
 int64_t orc_dp_const(const orc_problem *p, const orc_config *c, int32_t order)
 {
     orc_stage st[ORC_MAX_STAGES];
-    orc_stages(p, c, order, 1, st);
+    if (orc_stages(p, c, order, 1, st)) return 0;   /* an empty slot of the free stage types */
     double al = 0.0, bw = 0.0;
     for (int s = 0; s < c->pp; s++) {
         if (s == 0 || st[s].alpha > al) al = st[s].alpha;
@@ -426,7 +504,13 @@ int32_t orc_segment_costs(const orc_problem *p, int64_t idx, int64_t *cost, uint
     if (orc_instance(p, idx, &c, &order, &micro)) return -1;
     int N = p->n_layers, PP = c.pp, W = N + 1;
     orc_stage st[ORC_MAX_STAGES];
-    orc_stages(p, &c, order, micro, st);
+    if (orc_stages(p, &c, order, micro, st)) {   /* an empty slot: no partition */
+        for (int64_t i = 0; i < (int64_t)PP * W * W; i++) {
+            cost[i] = ORC_INF;
+            rflag[i] = 0;
+        }
+        return 0;
+    }
     orc_pi_terms pt;
     orc_pi_terms_eval(p, &c, &pt);
 
@@ -860,8 +944,8 @@ static int32_t solve_with(const orc_problem *p, int64_t idx, orc_result *r, int 
     else
         orc_brute_exact(c.pp, p->n_layers, micro, cost, r);
     orc_stage st[ORC_MAX_STAGES];
-    orc_stages(p, &c, order, micro, st);
-    for (int i = 0; i < c.pp; i++) r->stage_mask[i] = (uint8_t)st[i].mask;
+    const int laid = orc_stages(p, &c, order, micro, st) == 0;
+    for (int i = 0; i < c.pp; i++) r->stage_mask[i] = laid ? (uint8_t)st[i].mask : 0;
     r->dp_const = orc_dp_const(p, &c, order);
     if (r->status == 0) {
         r->opt += r->dp_const;

@@ -62,6 +62,7 @@ typedef struct orc_problem {
     int32_t prune_hetero, allow_recompute;
     /* search space */
     int32_t pp_max, tp_mask, cp_mask, ep_max, tpe_mask, mode;
+    int32_t stage_types;           /* 0: block orderings of the types; 1: free per-stage type */
     int32_t n_micro;
     int32_t micro[ORC_MAX_MICRO];
 } orc_problem;
@@ -117,6 +118,10 @@ typedef struct orc_result {
 int32_t orc_validate(const orc_problem *p);
 int64_t orc_enumerate(const orc_problem *p, orc_config *out, int64_t cap);
 int32_t orc_n_orders(const orc_problem *p);
+/* Free per-stage types: the o-th stage-type sequence of a pipeline of pp
+ * stages (lexicographic over the distinct arrangements of the multiset with
+ * m_h / (G / pp) stages of type h); -1 if o is past the last one. */
+int32_t orc_sequence(const orc_problem *p, int32_t pp, int32_t o, int32_t *seq);
 void orc_order(const orc_problem *p, int32_t o, int32_t *perm);
 int64_t orc_n_instances(const orc_problem *p);
 int32_t orc_instance(const orc_problem *p, int64_t idx, orc_config *cfg, int32_t *order, int32_t *micro);

@@ -38,7 +38,7 @@ class OrcProblem(C.Structure):
         ("delta_num", C.c_int32), ("delta_den", C.c_int32), ("eta_prune", C.c_int32),
         ("prune_window", C.c_int32), ("prune_hetero", C.c_int32), ("allow_recompute", C.c_int32),
         ("pp_max", C.c_int32), ("tp_mask", C.c_int32), ("cp_mask", C.c_int32), ("ep_max", C.c_int32),
-        ("tpe_mask", C.c_int32), ("mode", C.c_int32),
+        ("tpe_mask", C.c_int32), ("mode", C.c_int32), ("stage_types", C.c_int32),
         ("n_micro", C.c_int32), ("micro", C.c_int32 * MAX_MICRO),
     ]
 
@@ -98,6 +98,7 @@ def lib():
         L.orc_n_orders.argtypes = [P(OrcProblem)]
         L.orc_order.argtypes = [P(OrcProblem), C.c_int32, P(C.c_int32)]
         L.orc_order.restype = None
+        L.orc_sequence.argtypes = [P(OrcProblem), C.c_int32, C.c_int32, P(C.c_int32)]
         L.orc_n_instances.argtypes = [P(OrcProblem)]
         L.orc_n_instances.restype = C.c_int64
         for name, T in (("orc_mask_terms_eval", OrcMaskTerms),):
@@ -184,6 +185,7 @@ class Oracle:
             setattr(P, name, int(pa[name]))
         for name in ("pp_max", "tp_mask", "cp_mask", "ep_max", "tpe_mask", "mode"):
             setattr(P, name, int(sp[name]))
+        P.stage_types = int(sp.get("stage_types", 0))
         micro = list(sp["micro"])
         P.n_micro = len(micro)
         for i, b in enumerate(micro):
@@ -208,6 +210,13 @@ class Oracle:
         perm = (C.c_int32 * MAX_TYPES)()
         self.L.orc_order(C.byref(self.P), o, perm)
         return list(perm[: self.P.n_types])
+
+    def sequence(self, pp, o):
+        """Free per-stage types: the o-th stage-type sequence of a pp-stage pipeline (None past the last)."""
+        seq = (C.c_int32 * MAX_STAGES)()
+        if self.L.orc_sequence(C.byref(self.P), int(pp), int(o), seq) != 0:
+            return None
+        return list(seq[: int(pp)])
 
     def n_instances(self):
         return self.L.orc_n_instances(C.byref(self.P))
