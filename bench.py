@@ -143,6 +143,43 @@ def leg_1f1b(torch, pl, stream, steps, warmup):
                           "layers": plan["layers"]}}
 
 
+def leg_free_types(torch, binding, workloads, n_config, dev, stream, steps, warmup):
+    """Free per-stage device types on a workload small enough to enumerate every
+    stage-type sequence: the whole step timed, and its best objective beside the
+    best over the block orderings of the same workload."""
+    import copy
+    import numpy as np
+    base = workloads.config(n_config)
+    free = copy.deepcopy(base)
+    free["space"]["stage_types"] = 1
+    pb, pf = binding.Planner(base, dev), binding.Planner(free, dev)
+    block_best = pb.run()["objective"]
+    for _ in range(warmup):
+        pf.run()
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
+    t0 = time.perf_counter()
+    plan = None
+    for k in range(steps):
+        pf.eval_cost_tables()
+        ev[k][0].record(stream)
+        pf.stage_dp()
+        ev[k][1].record(stream)
+        plan = pf.best_plan()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    res = pf.results()
+    return {"workload": f"config {n_config}: {WORKLOADS[n_config]}, every stage one device type",
+            "value": pf.n * steps / elapsed, "unit": "candidates/s", "ms_per_step": elapsed * 1e3 / steps,
+            "stage_dp_ms": float(np.mean([ev[k][0].elapsed_time(ev[k][1]) for k in range(steps)])),
+            "candidates": pf.n, "sequences_per_config": int(binding.tables_layout(free)["n_orders"]),
+            "feasible_candidates": int((res["status"] == 0).sum()),
+            "best_objective_ns": plan["objective"], "block_orderings_best_ns": block_best,
+            "gain_over_block_orderings": 1.0 - plan["objective"] / block_best,
+            "best_plan": {"config": plan["config"], "order": plan["order"], "B": plan["n_micro"],
+                          "stage_types": plan["stage_types"], "layers": plan["layers"]}}
+
+
 def cpu_baseline(problem, n_total, n_sample, exact=False):
     """The oracle as it stands, single thread, on a fixed stride sample (exact:
     its 1F1B re-scoring of the frontier)."""
@@ -174,6 +211,8 @@ def main():
     ap.add_argument("--cpu-sample-1f1b", type=int, default=200)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-1f1b", action="store_true", help="skip the 1F1B re-scoring leg")
+    ap.add_argument("--free-types-config", type=int, default=2,
+                    help="workload of the free per-stage device-type leg (0: skip it)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (counter scaling for HBM traffic)")
     args = ap.parse_args()
@@ -265,6 +304,9 @@ def main():
         out["objective_1f1b"] = leg_1f1b(torch, pl, stream, args.steps, args.warmup)
         if not args.no_cpu_baseline:
             out["objective_1f1b"]["cpu_baseline"], _ = cpu_baseline(problem, n, args.cpu_sample_1f1b, exact=True)
+    if args.free_types_config:
+        out["free_stage_types"] = leg_free_types(torch, binding, workloads, args.free_types_config, dev, stream,
+                                                 args.steps, args.warmup)
     if calib is not None:
         out["copy_calibration_bytes"] = calib
     if not args.no_cpu_baseline:

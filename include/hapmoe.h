@@ -118,6 +118,17 @@ typedef struct hapmoe_space {
     int32_t tpe_mask;    /* bit i: TPE = 2^i allowed */
     int32_t mode;        /* 0: EP*TPE folds inside the stage group (DP = group/(TP*CP));
                             1: literal product PP*DP*TP*CP*EP*TPE = sum_h m_h */
+    int32_t stage_types; /* 0: device-type orderings -- the devices listed type by type in each
+                            of the |H|! orders, stage i takes the i-th group of G/PP (a group
+                            may straddle two types);
+                            1: free per-stage type (the DP state m of Section 3.4): every stage
+                            is one group of a single type h, configurations whose m_h are not
+                            all multiples of G/PP are left out, and "order" o is the o-th
+                            distinct stage-type sequence (lexicographic over the arrangements
+                            of m_h / (G/PP) stages of each type h); n_orders is the most such
+                            sequences over the configurations, at most 2^20, and a slot past a
+                            configuration's own count is an infeasible candidate; a space
+                            that leaves no configuration is HAPMOE_E_INVAL */
     int32_t n_micro;     /* entries of micro[] */
     int32_t micro[HAPMOE_MAX_MICRO]; /* microbatch counts B, 1..1024 */
 } hapmoe_space;

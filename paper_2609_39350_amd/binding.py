@@ -56,7 +56,7 @@ class Params(C.Structure):
 
 class Space(C.Structure):
     _fields_ = [("pp_max", C.c_int32), ("tp_mask", C.c_int32), ("cp_mask", C.c_int32), ("ep_max", C.c_int32),
-                ("tpe_mask", C.c_int32), ("mode", C.c_int32), ("n_micro", C.c_int32),
+                ("tpe_mask", C.c_int32), ("mode", C.c_int32), ("stage_types", C.c_int32), ("n_micro", C.c_int32),
                 ("micro", C.c_int32 * MAX_MICRO)]
 
 
@@ -164,6 +164,7 @@ class HostProblem:
             setattr(p.params, f, int(pa[f]))
         for f in ("pp_max", "tp_mask", "cp_mask", "ep_max", "tpe_mask", "mode"):
             setattr(p.space, f, int(sp[f]))
+        p.space.stage_types = int(sp.get("stage_types", 0))
         micro = list(sp["micro"])
         p.space.n_micro = len(micro)
         for i, b in enumerate(micro[:MAX_MICRO]):

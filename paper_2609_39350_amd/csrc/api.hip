@@ -15,7 +15,7 @@ namespace {
 
 bool finite_nonneg(double x) { return std::isfinite(x) && x >= 0.0; }
 
-int32_t check_problem(const hapmoe_problem *p)
+int32_t check_fields(const hapmoe_problem *p)
 {
     if (!p) return HAPMOE_E_INVAL;
     const hapmoe_model &m = p->model;
@@ -68,16 +68,37 @@ int32_t check_problem(const hapmoe_problem *p)
     if (s.n_micro < 1 || s.n_micro > HAPMOE_MAX_MICRO) return HAPMOE_E_INVAL;
     for (int i = 0; i < s.n_micro; ++i)
         if (s.micro[i] < 1 || s.micro[i] > kMaxMicroValue) return HAPMOE_E_INVAL;
+    if (s.stage_types < 0 || s.stage_types > 1) return HAPMOE_E_INVAL;
     return HAPMOE_OK;
 }
 
 // The configuration set, the type orderings and the LDS bounds of the DP kernel.
 struct Space {
     std::vector<std::array<int32_t, 6>> cfg;   // pp, tp, cp, dp, ep, tpe
-    std::vector<std::array<int8_t, kMaxTypes>> perm;
+    std::vector<std::array<int8_t, kMaxTypes>> perm;   // block orderings (stage_types = 0)
+    int64_t n_orders = 1;   // orderings, or the most stage-type sequences (stage_types = 1)
     int kmax = 1;    // distinct device-type sets over the stages of any candidate
     int ppmax = 1;
 };
+
+constexpr int64_t kMaxFreeOrders = int64_t(1) << 20;
+constexpr int64_t kMaxKeys = int64_t(1) << 31;   // (configuration, order) keys: a 32-bit work queue
+
+// distinct arrangements of k_h = m_h / g stages of each type h, pp! / prod k_h!,
+// built one stage at a time: the running multinomial never falls, so it can
+// stop at a cap above every accepted count and stay exact below it
+int64_t arrangements(const hapmoe_cluster &c, int g)
+{
+    constexpr int64_t cap = int64_t(1) << 40;
+    int64_t n = 1;
+    int r = 0;
+    for (int h = 0; h < c.n_types; ++h)
+        for (int i = 1; i <= c.count[h] / g; ++i) {
+            n = n * ++r / i;
+            if (n > cap) return cap;
+        }
+    return n;
+}
 
 void build_space(const hapmoe_problem *p, Space &S)
 {
@@ -106,9 +127,16 @@ void build_space(const hapmoe_problem *p, Space &S)
     S.cfg.reserve(4096);
     S.kmax = 1;
     S.ppmax = 1;
+    const bool free_types = sp.stage_types != 0;
+    S.n_orders = 1;
     for (int PP = 1; PP <= std::min(G, std::min(sp.pp_max, m.n_layers)); ++PP) {
         if (G % PP) continue;
         const int g = G / PP;
+        if (free_types) {   // every stage one group of a single type
+            bool whole = true;
+            for (int h = 0; h < T; ++h) whole &= c.count[h] % g == 0;
+            if (!whole) continue;
+        }
         bool any = false;
         for (int TP : tps) {
             if (g % TP || m.hidden % TP) continue;
@@ -137,14 +165,29 @@ void build_space(const hapmoe_problem *p, Space &S)
             for (int h = 0; h < T; ++h) straddle |= (c.count[h] % g) != 0;
             S.kmax = std::max(S.kmax, std::min(PP, T + (straddle ? T - 1 : 0)));
             S.ppmax = std::max(S.ppmax, PP);
+            if (free_types) S.n_orders = std::max(S.n_orders, arrangements(c, g));
         }
     }
     std::array<int8_t, kMaxTypes> cur{};
     for (int h = 0; h < T; ++h) cur[h] = (int8_t)h;
     S.perm.clear();
+    if (free_types) return;
     do {
         S.perm.push_back(cur);
     } while (std::next_permutation(cur.begin(), cur.begin() + T));
+    S.n_orders = (int64_t)S.perm.size();
+}
+
+int32_t check_problem(const hapmoe_problem *p)
+{
+    if (const int32_t e = check_fields(p)) return e;
+    if (p->space.stage_types) {   // the sequence count and the key queue stay in range
+        Space S;
+        build_space(p, S);
+        if (S.cfg.empty() || S.n_orders > kMaxFreeOrders || (int64_t)S.cfg.size() * S.n_orders > kMaxKeys)
+            return HAPMOE_E_INVAL;
+    }
+    return HAPMOE_OK;
 }
 
 int check_arch()
@@ -181,7 +224,7 @@ ImageLayout image_layout(const hapmoe_problem *p)
 
 int64_t per_config(const hapmoe_problem *p, const Space &S)
 {
-    return (int64_t)S.perm.size() * p->space.n_micro;
+    return S.n_orders * p->space.n_micro;
 }
 
 }  // namespace
@@ -218,7 +261,7 @@ int32_t hapmoe_enumerate_candidates(const hapmoe_problem *p, hapmoe_candidate *o
     if (out) {
         int64_t k = 0;
         for (const auto &cf : S.cfg)
-            for (int o = 0; o < (int)S.perm.size(); ++o)
+            for (int o = 0; o < (int)S.n_orders; ++o)
                 for (int b = 0; b < p->space.n_micro; ++b) {
                     if (k >= capacity) break;
                     hapmoe_candidate &x = out[k++];
@@ -291,7 +334,8 @@ int32_t hapmoe_pack_image(const hapmoe_problem *p, void *h_image, int64_t bytes)
     H.prune_window = q.prune_window;   // 0, 1 or 2 (checked)
     H.prune_hetero = q.prune_hetero ? 1 : 0;
     H.allow_recompute = q.allow_recompute ? 1 : 0;
-    H.n_orders = (int32_t)S.perm.size();
+    H.n_orders = (int32_t)S.n_orders;
+    H.stage_types = p->space.stage_types;
     H.n_micro = p->space.n_micro;
     H.n_configs = (int32_t)S.cfg.size();
     for (size_t o = 0; o < S.perm.size(); ++o)
@@ -322,7 +366,7 @@ int32_t hapmoe_tables_bytes(const hapmoe_problem *p, int64_t *bytes)
     if (!bytes) return HAPMOE_E_INVAL;
     Space S;
     build_space(p, S);
-    *bytes = tables_layout((int64_t)S.cfg.size(), (int)S.perm.size(), p->cluster.n_types, p->model.n_layers).total;
+    *bytes = tables_layout((int64_t)S.cfg.size(), (int)S.n_orders, p->cluster.n_types, p->model.n_layers).total;
     return HAPMOE_OK;
 }
 
@@ -332,7 +376,7 @@ int32_t hapmoe_tables_layout(const hapmoe_problem *p, int64_t out[9])
     if (!out) return HAPMOE_E_INVAL;
     Space S;
     build_space(p, S);
-    const TablesLayout L = tables_layout((int64_t)S.cfg.size(), (int)S.perm.size(), p->cluster.n_types,
+    const TablesLayout L = tables_layout((int64_t)S.cfg.size(), (int)S.n_orders, p->cluster.n_types,
                                          p->model.n_layers);
     const int64_t v[9] = {L.n_configs, L.n_orders, L.n_masks, L.np, L.off_pi, L.off_key, L.off_mem, L.off_time,
                           L.total};
@@ -372,7 +416,7 @@ int32_t hapmoe_eval_cost_tables(const hapmoe_problem *p, const void *d_image, co
     build_space(p, S);
     const int64_t per = per_config(p, S);
     if (n_cand != (int64_t)S.cfg.size() * per) return HAPMOE_E_INVAL;
-    const TablesLayout L = tables_layout((int64_t)S.cfg.size(), (int)S.perm.size(), p->cluster.n_types,
+    const TablesLayout L = tables_layout((int64_t)S.cfg.size(), (int)S.n_orders, p->cluster.n_types,
                                          p->model.n_layers);
     if (tables_bytes < L.total) return HAPMOE_E_WORKSPACE;
     const DebugLayout D = debug_layout(p->cluster.n_types, p->model.n_layers);
@@ -405,13 +449,13 @@ int32_t stage_dp_any(const hapmoe_problem *p, const void *d_image, const hapmoe_
     const int64_t per = per_config(p, S);
     if (n_cand != (int64_t)S.cfg.size() * per) return HAPMOE_E_INVAL;
     if (first < 0 || count < 0 || first + count > n_cand || count > INT32_MAX) return HAPMOE_E_RANGE;
-    const TablesLayout L = tables_layout((int64_t)S.cfg.size(), (int)S.perm.size(), p->cluster.n_types,
+    const TablesLayout L = tables_layout((int64_t)S.cfg.size(), (int)S.n_orders, p->cluster.n_types,
                                          p->model.n_layers);
     if (tables_bytes < L.total || ws_bytes < stage_dp_ws_bytes()) return HAPMOE_E_WORKSPACE;
     if (const int e = check_arch()) return e;
     std::vector<int32_t> cfg_pp(S.cfg.size());
     for (size_t i = 0; i < S.cfg.size(); ++i) cfg_pp[i] = S.cfg[i][0];
-    if (launch_stage_dp(d_image, d_cand, p->model.n_layers, p->space.n_micro, cfg_pp, (int)S.perm.size(), L,
+    if (launch_stage_dp(d_image, d_cand, p->model.n_layers, p->space.n_micro, cfg_pp, (int)S.n_orders, L,
                         d_tables, first, count, S.kmax, S.ppmax, d_res, d_stats, d_ws, p->space.micro, exact,
                         (hipStream_t)stream) != hipSuccess)
         return HAPMOE_E_HIP;
@@ -457,7 +501,7 @@ int32_t hapmoe_best_plan(const hapmoe_problem *p, const hapmoe_candidate *d_cand
     build_space(p, S);
     const int64_t per = per_config(p, S), ncfg = (int64_t)S.cfg.size();
     if (n < 1 || n > ncfg * per) return HAPMOE_E_RANGE;
-    const TablesLayout L = tables_layout(ncfg, (int)S.perm.size(), p->cluster.n_types, p->model.n_layers);
+    const TablesLayout L = tables_layout(ncfg, (int)S.n_orders, p->cluster.n_types, p->model.n_layers);
     if (tables_bytes < L.total) return HAPMOE_E_WORKSPACE;
     if (ws_bytes < best_plan_ws_bytes(n, per, ncfg)) return HAPMOE_E_WORKSPACE;
     if (const int e = check_arch()) return e;

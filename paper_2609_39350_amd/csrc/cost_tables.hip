@@ -124,12 +124,49 @@ __global__ __launch_bounds__(kThreads) void k_cost_tables(const unsigned char *_
     __syncthreads();
 
     // ---- stage layout of every device-type ordering (one thread each) ----
-    if (tid < H.n_orders) {
-        const int o = tid;
+    for (int o = tid; o < H.n_orders; o += kThreads) {
+        const int g = H.total_devices / c.pp;
+        KeyInfo *K = reinterpret_cast<KeyInfo *>(tab + L.off_key) + (cfg * L.n_orders + o);
+        int seq[kMaxStages];   // free stage types: the type of each stage
+        if (H.stage_types) {
+            // the o-th distinct arrangement of k_h = m_h / g stages of type h, in
+            // lexicographic order: at each position take the smallest type whose
+            // block of arrangements (the multinomial of what remains) holds o
+            int k[kMaxTypes];
+            int64_t M = 1;   // multinomial of the counts so far; it never falls, and stays <= 2^20
+            int r = 0;
+            for (int h = 0; h < kMaxTypes; ++h) {
+                k[h] = h < T ? H.count[h] / g : 0;
+                for (int i = 1; i <= k[h]; ++i) M = M * ++r / i;
+            }
+            if (o >= M) {   // past this pipeline's sequences: no partition is feasible
+                K->dp_const = 0;
+                for (int s = 0; s < kMaxStages; ++s) {
+                    K->mask[s] = 1;
+                    K->lo[s] = K->hi[s] = K->bpair[s] = 0;
+                }
+                continue;
+            }
+            int64_t rest = o;
+            for (int s = 0; s < c.pp; ++s) {
+                const int left = c.pp - s;
+                for (int h = 0; h < T; ++h) {
+                    if (k[h] == 0) continue;
+                    const int64_t block = M * k[h] / left;   // arrangements that put h here
+                    if (rest < block) {
+                        seq[s] = h;
+                        M = block;
+                        --k[h];
+                        break;
+                    }
+                    rest -= block;
+                }
+            }
+        }
         int pos_type[kMaxTypes], pos_start[kMaxTypes], pos_end[kMaxTypes];
         int acc = 0;
         for (int j = 0; j < T; ++j) {
-            pos_type[j] = H.perm[o][j];
+            pos_type[j] = H.stage_types ? j : H.perm[o][j];   // perm holds |H|! <= 24 rows
             pos_start[j] = acc;
             acc += H.count[pos_type[j]];
             pos_end[j] = acc;
@@ -140,18 +177,20 @@ __global__ __launch_bounds__(kThreads) void k_cost_tables(const unsigned char *_
                 if (d < pos_end[j]) t = pos_type[j];
             return t;
         };
-        const int g = H.total_devices / c.pp;
-        KeyInfo *K = reinterpret_cast<KeyInfo *>(tab + L.off_key) + (cfg * L.n_orders + o);
         int spd[kMaxStages];
         int64_t sum_speed = 0;
         double al_k = 0.0, bw_k = 0.0;
         for (int s = 0; s < c.pp; ++s) {
             const int d0 = s * g, d1 = d0 + g;
-            int mask = 0;
-            for (int j = 0; j < T; ++j)
-                if (pos_start[j] < d1 && pos_end[j] > d0) mask |= 1 << pos_type[j];
-            int bpair = 0;
-            if (s < c.pp - 1) bpair = (type_of(d1 - 1) << 2) | type_of(d1);
+            int mask = 0, bpair = 0;
+            if (H.stage_types) {
+                mask = 1 << seq[s];
+                if (s < c.pp - 1) bpair = (seq[s] << 2) | seq[s + 1];
+            } else {
+                for (int j = 0; j < T; ++j)
+                    if (pos_start[j] < d1 && pos_end[j] > d0) mask |= 1 << pos_type[j];
+                if (s < c.pp - 1) bpair = (type_of(d1 - 1) << 2) | type_of(d1);
+            }
             int sp = 0;
             for (int h = 0; h < T; ++h)
                 if ((mask >> h) & 1) sp = (sp == 0 || H.speed[h] < sp) ? H.speed[h] : sp;

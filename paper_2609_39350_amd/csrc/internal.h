@@ -36,6 +36,7 @@ struct ImageHeader {
     double moe_ffn_mult, gamma, rc_time, rc_act, opt_coef;
     int32_t delta_num, delta_den, eta_prune, prune_window, prune_hetero, allow_recompute;
     int32_t n_orders, n_micro, n_configs, total_devices;
+    int32_t stage_types, pad_st;          // 1: free per-stage type sequences (perm unused)
     int8_t perm[kMaxOrders][kMaxTypes];   // orderings, lexicographic
     int32_t micro[HAPMOE_MAX_MICRO];
     int64_t off_is_moe, off_tokens, off_pdense, off_pexp, off_act, off_tdense, off_tffn;

@@ -109,3 +109,32 @@ def test_device_calls_refuse_bad_sizes_before_touching_the_gpu():
     assert f(hp.ref, 1, 1, 90, 1, 10, 0, 1, 1, None, 1, 256, None) == -3
     assert f(hp.ref, 1, 1, 90, 1, 10**9, 0, 1, 1, None, 1, 8, None) == -3
     assert f(hp.ref, 1, 1, 90, 1, 10**9, 0, 1, 1, None, None, 256, None) == -1
+
+
+def test_free_stage_types_enumeration_and_limits():
+    # free per-stage types: the same candidate set as the oracle, and sequence
+    # counts past the library's limit refused up front
+    for p in (workloads.config(1), workloads.config(2), workloads.random_tiny(5, n_types=3)):
+        q = variant(p, **{"space.stage_types": 1})
+        o = orc.Oracle(q)
+        cand = binding.enumerate_candidates(q)
+        assert len(cand) == o.n_instances()
+        per = o.n_orders() * len(q["space"]["micro"])
+        got = np.stack([cand[f] for f in ("pp", "tp", "cp", "dp", "ep", "tpe")], axis=1)[::per]
+        assert [tuple(int(v) for v in r) for r in got] == o.configs()
+        assert binding.tables_layout(q)["n_orders"] == o.n_orders()
+    q = variant(workloads.config(2), **{"space.stage_types": 1})
+    assert binding.tables_layout(q)["n_orders"] == 420   # 8! / (4! 2! 2!)
+    for bad in (2, -1):
+        with pytest.raises(binding.HapmoeError):
+            binding.validate(variant(q, **{"space.stage_types": bad}))
+    # 4 types x 64 devices at PP = 16: 16! / (4!)^4 sequences
+    huge = variant(workloads.config(3), **{"space.stage_types": 1})
+    with pytest.raises(binding.HapmoeError):
+        binding.validate(huge)
+    binding.validate(variant(huge, **{"space.pp_max": 8}))
+    # no configuration left: 5 + 3 devices never fill whole groups of 2, 4 or 8
+    empty = variant(workloads.random_tiny(900, n_types=2), **{"space.stage_types": 1})
+    assert list(empty["cluster"]["count"]) == [5, 3] and orc.Oracle(empty).n_instances() == 0
+    with pytest.raises(binding.HapmoeError):
+        binding.validate(empty)

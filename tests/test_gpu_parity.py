@@ -121,12 +121,18 @@ def _check_tables(problem, planner, cfg_sample):
                 for j, f in enumerate(("a2a", "tp", "cp")):
                     v = d[DL["off_mask"] + ((m - 1) * N + layer) * 3 + j]
                     assert abs(v - mt[f]) <= 1e-12 * abs(mt[f]), (k, m, layer, f)
+        free = problem["space"].get("stage_types", 0)
         for oi in range(o.n_orders()):
             key = t["key"][k, oi]
+            if free and o.sequence(cfg[0], oi) is None:   # an empty slot: nothing can fit
+                assert int(key["dp_const"]) == 0 and not key["hi"][:cfg[0]].any()
+                continue
             st = o.stages(cfg, oi, micro0)
             assert int(key["dp_const"]) == o.dp_const(cfg, oi)
             for s, x in enumerate(st):
                 assert (int(key["mask"][s]), int(key["lo"][s]), int(key["hi"][s])) == (x["mask"], x["lo"], x["hi"])
+                if s + 1 < len(st):
+                    assert int(key["bpair"][s]) == (x["last_type"] << 2) | st[s + 1]["first_type"]
                 assert (used >> (x["mask"] - 1)) & 1
 
 
