@@ -127,8 +127,14 @@ typedef struct hapmoe_space {
                             distinct stage-type sequence (lexicographic over the arrangements
                             of m_h / (G/PP) stages of each type h); n_orders is the most such
                             sequences over the configurations, at most 2^20, and a slot past a
-                            configuration's own count is an infeasible candidate; a space
-                            that leaves no configuration is HAPMOE_E_INVAL */
+                            configuration's own count is an infeasible candidate;
+                            2: free per-stage type chosen by the DP over device counts (the
+                            state m of Section 3.4): the same configurations as 1, one order
+                            slot each (order 0 lays out the first sequence), solved by
+                            hapmoe_stage_dp_types; at most 8192 count states prod_h (k_h + 1)
+                            per pipeline, k_h = m_h / (G/PP).
+                            With 1 or 2, a space that leaves no configuration is
+                            HAPMOE_E_INVAL */
     int32_t n_micro;     /* entries of micro[] */
     int32_t micro[HAPMOE_MAX_MICRO]; /* microbatch counts B, 1..1024 */
 } hapmoe_space;
@@ -246,6 +252,7 @@ int32_t hapmoe_stage_dp_ws_bytes(const hapmoe_problem *p, int64_t *bytes);
  * and slots are counted once, on the first of them.  d_ws
  * (hapmoe_stage_dp_ws_bytes)
  * holds the kernel's work queue: calls that may overlap need their own d_ws.
+ * Problems with stage_types = 2 are HAPMOE_E_INVAL here (hapmoe_stage_dp_types).
  * Asynchronous. */
 int32_t hapmoe_stage_dp(const hapmoe_problem *p, const void *d_image,
                         const hapmoe_candidate *d_cand, int64_t n_cand,
@@ -266,7 +273,8 @@ int32_t hapmoe_stage_dp(const hapmoe_problem *p, const void *d_image,
  * ceil(c / 3), its backward part the rest).  The result keeps the least T,
  * ties to the lower largest stage: objective = T + C, stage_sum and t_max of the
  * chosen partition, its recomputation mask and stage lengths.  d_stats as for
- * hapmoe_stage_dp (passes = DP passes of the frontier walk).  Asynchronous. */
+ * hapmoe_stage_dp (passes = DP passes of the frontier walk).  Not for
+ * stage_types = 2 (HAPMOE_E_INVAL).  Asynchronous. */
 int32_t hapmoe_stage_dp_1f1b(const hapmoe_problem *p, const void *d_image,
                              const hapmoe_candidate *d_cand, int64_t n_cand,
                              const void *d_tables, int64_t tables_bytes,
@@ -274,17 +282,47 @@ int32_t hapmoe_stage_dp_1f1b(const hapmoe_problem *p, const void *d_image,
                              hapmoe_dp_result *d_res, int32_t *d_stats,
                              void *d_ws, int64_t ws_bytes, void *stream);
 
+/* Workspace of hapmoe_stage_dp_types: the work-queue counter and one slice of
+ * DP states per workgroup (F as int64 and the back-trace pointer as int16 per
+ * state (u, b, h')); HAPMOE_E_INVAL unless stage_types = 2. */
+int32_t hapmoe_stage_dp_types_ws_bytes(const hapmoe_problem *p, int64_t *bytes);
+
+/* Stage DP over device counts for free per-stage device types (stage_types =
+ * 2; Section 3.4 with the DP state m of remaining devices per type, the
+ * transitions of Algorithm 1 choosing each stage's type h and its layers,
+ * prunings 1-3).  A pipeline of PP stages holds k_h = m_h / (G/PP) stages of
+ * type h; a stage of type h is a pure group of that type (window, capacity and
+ * speed of h, memory with min(PP - i + 1, B) stored micro-batches), and the
+ * transfer to the next stage depends on both types.  For each candidate of
+ * [first, first + count) it minimises sum_i c_i + (B-1) max_i c_i over every
+ * stage-type sequence and partition.  Ties: lowest threshold t*, then at each
+ * back-trace step from the last stage the smallest split point, then the
+ * smallest type.  Writes d_res[0 .. count) like hapmoe_stage_dp and
+ * d_types[32 * (0 .. count)], the type mask (1 << h_i) of each stage (0 past
+ * PP and for infeasible candidates).  d_stats (may be NULL): passes of the
+ * candidate's sweep and the relaxations of the sweep on the first candidate
+ * that shares it (columns 2, 3 zero).  d_ws (hapmoe_stage_dp_types_ws_bytes)
+ * is the kernel's: calls that may overlap need their own.  Asynchronous. */
+int32_t hapmoe_stage_dp_types(const hapmoe_problem *p, const void *d_image,
+                              const hapmoe_candidate *d_cand, int64_t n_cand,
+                              const void *d_tables, int64_t tables_bytes,
+                              int64_t first, int64_t count,
+                              hapmoe_dp_result *d_res, uint8_t *d_types, int32_t *d_stats,
+                              void *d_ws, int64_t ws_bytes, void *stream);
+
 /* Workspace of hapmoe_best_plan for n results. */
 int32_t hapmoe_best_plan_ws_bytes(const hapmoe_problem *p, int64_t n, int64_t *bytes);
 
 /* Segmented arg-min (Eq. 1 objective): per configuration pi the best of its
  * candidates (d_config_best, n_configs int64 entries: candidate index or -1;
  * may be NULL), then the global best by (objective, candidate index).  d_res
- * holds the results of candidates [0, n).  Waits for `stream`, fills *h_plan.
- * Returns HAPMOE_E_INFEASIBLE if no candidate is feasible. */
+ * holds the results of candidates [0, n); with stage_types = 2, d_types holds
+ * their stage types (hapmoe_stage_dp_types), otherwise it must be NULL.
+ * Waits for `stream`, fills *h_plan.  Returns HAPMOE_E_INFEASIBLE if no
+ * candidate is feasible. */
 int32_t hapmoe_best_plan(const hapmoe_problem *p, const hapmoe_candidate *d_cand,
                          const void *d_tables, int64_t tables_bytes,
-                         const hapmoe_dp_result *d_res, int64_t n,
+                         const hapmoe_dp_result *d_res, const uint8_t *d_types, int64_t n,
                          int64_t *d_config_best, void *d_ws, int64_t ws_bytes,
                          hapmoe_plan *h_plan, void *stream);
 

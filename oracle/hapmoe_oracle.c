@@ -41,7 +41,7 @@ int32_t orc_validate(const orc_problem *p)
     if (p->prune_window < 0 || p->prune_window > 2) return -1;
     if (p->n_micro < 1 || p->n_micro > ORC_MAX_MICRO) return -1;
     if (p->pp_max < 1 || p->pp_max > ORC_MAX_STAGES || p->mode < 0 || p->mode > 1) return -1;
-    if (p->stage_types < 0 || p->stage_types > 1) return -1;
+    if (p->stage_types < 0 || p->stage_types > 2) return -1;
     for (int i = 0; i < p->n_micro; i++)
         if (p->micro[i] < 1 || p->micro[i] > (1 << 20)) return -1;
     return 0;
@@ -127,6 +127,7 @@ static int64_t n_sequences(const orc_problem *p, int pp)
  * the configurations (a configuration with fewer has empty slots). */
 int32_t orc_n_orders(const orc_problem *p)
 {
+    if (p->stage_types == 2) return 1;   /* the DP over device counts picks the sequence */
     if (p->stage_types) {
         int64_t ncfg = orc_enumerate(p, NULL, 0), best = 1;
         orc_config *all = (orc_config *)malloc(sizeof(orc_config) * (size_t)(ncfg > 0 ? ncfg : 1));
@@ -497,6 +498,80 @@ int64_t orc_dp_const(const orc_problem *p, const orc_config *c, int32_t order)
  * stage's memory (pruning 2); pruning 3 on cross-type communication; then
  * T_stage + T_comm.
  * ---------------------------------------------------------------------- */
+/* layer prefix sums of one configuration: memory terms, and the stage-time
+ * terms of one device-type set */
+typedef struct prefixes {
+    int n;
+    int64_t *w, *a0, *a1, *moe, *t0, *t1, *comm;
+} prefixes;
+
+static void prefixes_init(const orc_problem *p, const orc_config *c, prefixes *P)
+{
+    int N = p->n_layers, W = N + 1;
+    P->n = N;
+    P->w = calloc((size_t)W, 8);
+    P->a0 = calloc((size_t)W, 8);
+    P->a1 = calloc((size_t)W, 8);
+    P->moe = calloc((size_t)W, 8);
+    P->t0 = calloc((size_t)W, 8);
+    P->t1 = calloc((size_t)W, 8);
+    P->comm = calloc((size_t)W, 8);
+    for (int l = 0; l < N; l++) {
+        orc_mem_terms m;
+        orc_mem_terms_eval(p, c, l, &m);
+        P->w[l + 1] = P->w[l] + m.q_w;
+        P->a0[l + 1] = P->a0[l] + m.q_a0;
+        P->a1[l + 1] = P->a1[l] + m.q_a1;
+        P->moe[l + 1] = P->moe[l] + (p->is_moe[l] ? 1 : 0);
+    }
+}
+
+static void prefixes_time(const orc_problem *p, const orc_config *c, int mask, prefixes *P)
+{
+    for (int l = 0; l < P->n; l++) {
+        orc_mask_terms m;
+        orc_mask_terms_eval(p, c, l, mask, &m);
+        P->t0[l + 1] = P->t0[l] + m.t_r0;
+        P->t1[l + 1] = P->t1[l] + m.t_r1;
+        P->comm[l + 1] = P->comm[l] + m.comm;
+    }
+}
+
+static void prefixes_free(prefixes *P)
+{
+    free(P->w); free(P->a0); free(P->a1); free(P->moe); free(P->t0); free(P->t1); free(P->comm);
+}
+
+/* c_i(a, b) of one stage (ORC_INF if pruned), *r = the recomputation choice */
+static int64_t segment_cost(const orc_problem *p, const orc_pi_terms *pt, const orc_stage *st,
+                            const prefixes *P, int a, int b, uint8_t *r)
+{
+    *r = 0;
+    if (b <= a) return ORC_INF;
+    int n = b - a;
+    if (n < st->lo || n > st->hi) return ORC_INF;                              /* pruning 1 */
+    int64_t extra = (P->moe[b] - P->moe[a]) > 0 ? pt->x_bytes : 0;
+    int64_t m0 = (P->w[b] - P->w[a]) + st->m_store * (P->a0[b] - P->a0[a]) + extra;
+    int64_t m1 = (P->w[b] - P->w[a]) + st->m_store * (P->a1[b] - P->a1[a]) + extra;
+    int64_t t;
+    if (m0 <= st->cap) {
+        t = P->t0[b] - P->t0[a];
+    } else if (p->allow_recompute && m1 <= st->cap) {
+        t = P->t1[b] - P->t1[a];
+        *r = 1;
+    } else {
+        return ORC_INF;                                                          /* pruning 2 */
+    }
+    if (p->prune_hetero) {
+        int64_t hc = (st->mixed ? P->comm[b] - P->comm[a] : 0) + (st->bdiff ? st->p2p : 0);
+        if (hc > (int64_t)p->eta_prune * pt->tbar) {                             /* pruning 3 */
+            *r = 0;
+            return ORC_INF;
+        }
+    }
+    return t + st->p2p;
+}
+
 int32_t orc_segment_costs(const orc_problem *p, int64_t idx, int64_t *cost, uint8_t *rflag)
 {
     orc_config c;
@@ -513,58 +588,17 @@ int32_t orc_segment_costs(const orc_problem *p, int64_t idx, int64_t *cost, uint
     }
     orc_pi_terms pt;
     orc_pi_terms_eval(p, &c, &pt);
-
-    int64_t *Wp = calloc((size_t)W, 8), *A0 = calloc((size_t)W, 8), *A1 = calloc((size_t)W, 8);
-    int64_t *MO = calloc((size_t)W, 8), *T0 = calloc((size_t)W, 8), *T1 = calloc((size_t)W, 8);
-    int64_t *CM = calloc((size_t)W, 8);
-    for (int l = 0; l < N; l++) {
-        orc_mem_terms m;
-        orc_mem_terms_eval(p, &c, l, &m);
-        Wp[l + 1] = Wp[l] + m.q_w;
-        A0[l + 1] = A0[l] + m.q_a0;
-        A1[l + 1] = A1[l] + m.q_a1;
-        MO[l + 1] = MO[l] + (p->is_moe[l] ? 1 : 0);
-    }
+    prefixes P;
+    prefixes_init(p, &c, &P);
     for (int i = 0; i < PP; i++) {
-        for (int l = 0; l < N; l++) {
-            orc_mask_terms m;
-            orc_mask_terms_eval(p, &c, l, st[i].mask, &m);
-            T0[l + 1] = T0[l] + m.t_r0;
-            T1[l + 1] = T1[l] + m.t_r1;
-            CM[l + 1] = CM[l] + m.comm;
-        }
-        for (int a = 0; a < W; a++) {
+        prefixes_time(p, &c, st[i].mask, &P);
+        for (int a = 0; a < W; a++)
             for (int b = 0; b < W; b++) {
                 int64_t at = ((int64_t)i * W + a) * W + b;
-                cost[at] = ORC_INF;
-                rflag[at] = 0;
-                if (b <= a) continue;
-                int n = b - a;
-                if (n < st[i].lo || n > st[i].hi) continue;                        /* pruning 1 */
-                int64_t extra = (MO[b] - MO[a]) > 0 ? pt.x_bytes : 0;
-                int64_t m0 = (Wp[b] - Wp[a]) + st[i].m_store * (A0[b] - A0[a]) + extra;
-                int64_t m1 = (Wp[b] - Wp[a]) + st[i].m_store * (A1[b] - A1[a]) + extra;
-                int64_t t;
-                int r;
-                if (m0 <= st[i].cap) {
-                    t = T0[b] - T0[a];
-                    r = 0;
-                } else if (p->allow_recompute && m1 <= st[i].cap) {
-                    t = T1[b] - T1[a];
-                    r = 1;
-                } else {
-                    continue;                                                     /* pruning 2 */
-                }
-                if (p->prune_hetero) {
-                    int64_t hc = (st[i].mixed ? CM[b] - CM[a] : 0) + (st[i].bdiff ? st[i].p2p : 0);
-                    if (hc > (int64_t)p->eta_prune * pt.tbar) continue;            /* pruning 3 */
-                }
-                cost[at] = t + st[i].p2p;
-                rflag[at] = (uint8_t)r;
+                cost[at] = segment_cost(p, &pt, &st[i], &P, a, b, &rflag[at]);
             }
-        }
     }
-    free(Wp); free(A0); free(A1); free(MO); free(T0); free(T1); free(CM);
+    prefixes_free(&P);
     return 0;
 }
 
@@ -926,8 +960,350 @@ int32_t orc_brute_exact(int32_t pp, int32_t n, int64_t micro, const int64_t *cos
     return 0;
 }
 
+/* ------------------------------------------------------------------------
+ * Free per-stage device types by the DP over device counts (Section 3.4: the
+ * DP state carries the remaining devices of each type, and every transition
+ * picks the type h and the layers of one more stage; Algorithm 1).
+ *
+ * A pipeline of pp stages with g = G / pp devices a stage holds k_h = m_h / g
+ * stages of type h.  State (u, b, h): u_h stages of type h placed so far
+ * (s = sum u of them), layers [0, b) covered, and the next stage -- number s --
+ * of type h.  A type-h stage on [a, b) followed by a type-h' stage costs
+ * c[s][h][h'](a, b) (h' = T: it is the last stage), the segment cost of a pure
+ * stage at position s; the transfer to the next stage, and pruning 3 on it,
+ * depend on h'.  Threshold form as in orc_dp:
+ *     F_t(u + e_h, b, h') = min over (a, h) of F_t(u, a, h) + c[s][h][h'](a, b)
+ * over costs <= t, starting from F(0, 0, h) = 0 for every type with k_h > 0.
+ * Ties keep the smallest a, then the smallest h.  OPT = min_t F_t + (B-1) t,
+ * t* the smallest threshold reaching it, and the back-trace at t* gives the
+ * lexicographically smallest (b_{pp-1}, h_{pp-1}, ..., b_1, h_1, h_0) among
+ * the optima (b_i = first layer of stage i, h_i = its type).
+ * ---------------------------------------------------------------------- */
+typedef struct type_space {
+    int pp, T, n, W, U;
+    int k[ORC_MAX_TYPES], rad[ORC_MAX_TYPES];
+} type_space;
+
+static void type_space_init(type_space *S, int pp, int T, const int32_t *k, int n)
+{
+    S->pp = pp;
+    S->T = T;
+    S->n = n;
+    S->W = n + 1;
+    S->U = 1;
+    for (int h = 0; h < T; h++) {
+        S->k[h] = k[h];
+        S->rad[h] = S->U;
+        S->U *= k[h] + 1;
+    }
+}
+
+static int digit(const type_space *S, int u, int h) { return (u / S->rad[h]) % (S->k[h] + 1); }
+
+static int64_t cost_at(const type_space *S, const int64_t *cost, int s, int h, int hn, int a, int b)
+{
+    return cost[((((int64_t)s * S->T + h) * (S->T + 1) + hn) * S->W + a) * S->W + b];
+}
+
+/* one pass at threshold t: F and arg over [U][W][T + 1]; returns F at the end state */
+static int64_t type_pass(const type_space *S, const int64_t *cost, int64_t t, int64_t *F, int32_t *arg)
+{
+    int W = S->W, T1 = S->T + 1;
+    for (int64_t i = 0; i < (int64_t)S->U * W * T1; i++) {
+        F[i] = ORC_INF;
+        arg[i] = -1;
+    }
+    for (int h = 0; h < S->T; h++)
+        if (S->k[h] > 0) F[h] = 0;   /* u = 0, b = 0 */
+    for (int u = 1; u < S->U; u++) {   /* u - e_h < u: increasing index is a topological order */
+        int done = 0;
+        for (int h = 0; h < S->T; h++) done += digit(S, u, h);
+        int s = done - 1;   /* the stage that ends at b */
+        for (int b = 0; b < W; b++)
+            for (int hn = 0; hn < T1; hn++) {
+                if (done == S->pp ? hn != S->T : (hn == S->T || digit(S, u, hn) >= S->k[hn])) continue;
+                int64_t best = ORC_INF;
+                int32_t ba = -1;
+                for (int a = 0; a < b; a++)
+                    for (int h = 0; h < S->T; h++) {
+                        if (digit(S, u, h) == 0) continue;
+                        int64_t prev = F[((int64_t)(u - S->rad[h]) * W + a) * T1 + h];
+                        int64_t c = cost_at(S, cost, s, h, hn, a, b);
+                        if (prev == ORC_INF || c == ORC_INF || c > t) continue;
+                        if (prev + c < best) {
+                            best = prev + c;
+                            ba = a * 8 + h;
+                        }
+                    }
+                F[((int64_t)u * W + b) * T1 + hn] = best;
+                arg[((int64_t)u * W + b) * T1 + hn] = ba;
+            }
+    }
+    return F[((int64_t)(S->U - 1) * W + S->n) * T1 + S->T];
+}
+
+int32_t orc_dp_types(int32_t pp, int32_t T, const int32_t *k, int32_t n, int64_t micro, const int64_t *cost,
+                     orc_result *r)
+{
+    type_space S;
+    type_space_init(&S, pp, T, k, n);
+    int W = S.W, T1 = T + 1;
+    int64_t ncost = (int64_t)pp * T * T1 * W * W;
+    memset(r, 0, sizeof(*r));
+    r->pp = pp;
+    int64_t *theta = malloc(sizeof(int64_t) * (size_t)(ncost + 1));
+    int64_t nt = 0;
+    for (int64_t i = 0; i < ncost; i++)
+        if (cost[i] != ORC_INF) theta[nt++] = cost[i];
+    qsort(theta, (size_t)nt, sizeof(int64_t), cmp_i64);
+    int64_t nu = 0;
+    for (int64_t i = 0; i < nt; i++)
+        if (nu == 0 || theta[i] != theta[nu - 1]) theta[nu++] = theta[i];
+    int64_t *F = malloc(sizeof(int64_t) * (size_t)S.U * W * T1);
+    int32_t *arg = malloc(sizeof(int32_t) * (size_t)S.U * W * T1);
+
+    int64_t finf = type_pass(&S, cost, ORC_INF, F, arg);
+    int64_t best = ORC_INF, tstar = -1, swept = 0;
+    if (finf != ORC_INF) {
+        for (int64_t i = 0; i < nu; i++) {
+            int64_t t = theta[i];
+            if (finf + (micro - 1) * t >= best) break;
+            int64_t f = type_pass(&S, cost, t, F, arg);
+            swept++;
+            if (f == ORC_INF) continue;
+            if (f + (micro - 1) * t < best) {
+                best = f + (micro - 1) * t;
+                tstar = t;
+            }
+        }
+    }
+    r->thresholds = swept;
+    if (tstar < 0) {
+        r->status = 1;
+        r->opt = r->sum = r->tmax = ORC_INF;
+    } else {
+        r->sum = type_pass(&S, cost, tstar, F, arg);
+        r->tmax = tstar;
+        r->opt = best;
+        int u = S.U - 1, b = n, hn = T;
+        for (int i = pp - 1; i >= 0; i--) {
+            int32_t x = arg[((int64_t)u * W + b) * T1 + hn];
+            int a = x / 8, h = x % 8;
+            r->layers[i] = (uint8_t)(b - a);
+            r->stage_mask[i] = (uint8_t)(1 << h);
+            u -= S.rad[h];
+            b = a;
+            hn = h;
+        }
+    }
+    free(theta);
+    free(F);
+    free(arg);
+    return 0;
+}
+
+/* Brute force: every stage-type sequence (arrangement of the multiset) and
+ * every composition, ordered by (objective, largest stage, b_{pp-1}, h_{pp-1},
+ * ..., b_1, h_1, h_0) -- the canonical choice of orc_dp_types. */
+typedef struct type_brute {
+    const type_space *S;
+    const int64_t *cost;
+    int64_t micro;
+    int seq[ORC_MAX_STAGES], b[ORC_MAX_STAGES + 1];
+    int best_seq[ORC_MAX_STAGES], best_b[ORC_MAX_STAGES + 1];
+    int64_t best_obj, best_max, best_sum;
+    int found;
+} type_brute;
+
+static int type_brute_better(const type_brute *x, int64_t obj, int64_t mx)
+{
+    if (!x->found) return 1;
+    if (obj != x->best_obj) return obj < x->best_obj;
+    if (mx != x->best_max) return mx < x->best_max;
+    for (int i = x->S->pp - 1; i >= 1; i--) {
+        if (x->b[i] != x->best_b[i]) return x->b[i] < x->best_b[i];
+        if (x->seq[i] != x->best_seq[i]) return x->seq[i] < x->best_seq[i];
+    }
+    return x->seq[0] < x->best_seq[0];
+}
+
+static void type_brute_parts(type_brute *x, int i)
+{
+    const type_space *S = x->S;
+    if (i == S->pp) {
+        int64_t sum = 0, mx = 0;
+        for (int j = 0; j < S->pp; j++) {
+            int hn = j + 1 < S->pp ? x->seq[j + 1] : S->T;
+            int64_t c = cost_at(S, x->cost, j, x->seq[j], hn, x->b[j], x->b[j + 1]);
+            if (c == ORC_INF) return;
+            sum += c;
+            if (c > mx) mx = c;
+        }
+        int64_t obj = sum + (x->micro - 1) * mx;
+        if (type_brute_better(x, obj, mx)) {
+            x->found = 1;
+            x->best_obj = obj;
+            x->best_max = mx;
+            x->best_sum = sum;
+            memcpy(x->best_seq, x->seq, sizeof(x->seq));
+            memcpy(x->best_b, x->b, sizeof(x->b));
+        }
+        return;
+    }
+    if (i == S->pp - 1) {
+        x->b[S->pp] = S->n;
+        if (x->b[i] < S->n) type_brute_parts(x, S->pp);
+        return;
+    }
+    for (int e = x->b[i] + 1; e <= S->n - (S->pp - 1 - i); e++) {
+        x->b[i + 1] = e;
+        type_brute_parts(x, i + 1);
+    }
+}
+
+static void type_brute_seq(type_brute *x, int i, int *left)
+{
+    if (i == x->S->pp) {
+        x->b[0] = 0;
+        type_brute_parts(x, 0);
+        return;
+    }
+    for (int h = 0; h < x->S->T; h++) {
+        if (left[h] == 0) continue;
+        left[h]--;
+        x->seq[i] = h;
+        type_brute_seq(x, i + 1, left);
+        left[h]++;
+    }
+}
+
+int32_t orc_brute_types(int32_t pp, int32_t T, const int32_t *k, int32_t n, int64_t micro, const int64_t *cost,
+                        orc_result *r)
+{
+    type_space S;
+    type_space_init(&S, pp, T, k, n);
+    type_brute x;
+    memset(&x, 0, sizeof(x));
+    x.S = &S;
+    x.cost = cost;
+    x.micro = micro;
+    int left[ORC_MAX_TYPES];
+    for (int h = 0; h < T; h++) left[h] = k[h];
+    type_brute_seq(&x, 0, left);
+    memset(r, 0, sizeof(*r));
+    r->pp = pp;
+    if (!x.found) {
+        r->status = 1;
+        r->opt = r->sum = r->tmax = ORC_INF;
+        return 0;
+    }
+    r->opt = x.best_obj;
+    r->sum = x.best_sum;
+    r->tmax = x.best_max;
+    for (int i = 0; i < pp; i++) {
+        r->layers[i] = (uint8_t)(x.best_b[i + 1] - x.best_b[i]);
+        r->stage_mask[i] = (uint8_t)(1 << x.best_seq[i]);
+    }
+    return 0;
+}
+
+/* stage counts k_h of a configuration under free per-stage types */
+static void type_counts(const orc_problem *p, const orc_config *c, int32_t *k)
+{
+    int G = 0;
+    for (int h = 0; h < p->n_types; h++) G += p->count[h];
+    int g = G / c->pp;
+    for (int h = 0; h < p->n_types; h++) k[h] = p->count[h] / g;
+}
+
+int32_t orc_type_costs(const orc_problem *p, int64_t idx, int64_t *cost, uint8_t *rflag)
+{
+    orc_config c;
+    int32_t order, micro;
+    if (p->stage_types != 2 || orc_instance(p, idx, &c, &order, &micro)) return -1;
+    int N = p->n_layers, PP = c.pp, W = N + 1, T = p->n_types;
+    int32_t k[ORC_MAX_TYPES];
+    type_counts(p, &c, k);
+    /* the first sequence's stages give every type's stage description
+     * (cap, speed, links, pruning-1 window); position and neighbour set the rest */
+    orc_stage st0[ORC_MAX_STAGES], of_type[ORC_MAX_TYPES];
+    int32_t seq[ORC_MAX_STAGES];
+    orc_stages(p, &c, 0, micro, st0);
+    orc_sequence(p, PP, 0, seq);
+    for (int s = 0; s < PP; s++) of_type[seq[s]] = st0[s];
+    orc_pi_terms pt;
+    orc_pi_terms_eval(p, &c, &pt);
+    prefixes P;
+    prefixes_init(p, &c, &P);
+    for (int h = 0; h < T; h++) {
+        if (k[h] > 0) prefixes_time(p, &c, 1 << h, &P);
+        for (int s = 0; s < PP; s++)
+            for (int hn = 0; hn <= T; hn++) {
+                int64_t base = (((int64_t)s * T + h) * (T + 1) + hn) * W * W;
+                int ok = k[h] > 0 && (s == PP - 1 ? hn == T : hn < T && k[hn] > 0);
+                orc_stage x;
+                if (ok) {
+                    x = of_type[h];
+                    x.m_store = min64(PP - s, micro);
+                    x.bdiff = hn < T && hn != h;
+                    x.p2p = hn < T ? orc_p2p(p, &c, h, hn) : 0;
+                }
+                for (int a = 0; a < W; a++)
+                    for (int b = 0; b < W; b++) {
+                        if (!ok) {
+                            cost[base + (int64_t)a * W + b] = ORC_INF;
+                            rflag[base + (int64_t)a * W + b] = 0;
+                            continue;
+                        }
+                        cost[base + (int64_t)a * W + b] = segment_cost(p, &pt, &x, &P, a, b,
+                                                                       &rflag[base + (int64_t)a * W + b]);
+                    }
+            }
+    }
+    prefixes_free(&P);
+    return 0;
+}
+
+static int32_t solve_types(const orc_problem *p, int64_t idx, orc_result *r, int brute)
+{
+    orc_config c;
+    int32_t order, micro;
+    if (orc_instance(p, idx, &c, &order, &micro)) return -1;
+    int T = p->n_types, W = p->n_layers + 1;
+    int32_t k[ORC_MAX_TYPES];
+    type_counts(p, &c, k);
+    int64_t ncost = (int64_t)c.pp * T * (T + 1) * W * W;
+    int64_t *cost = malloc(sizeof(int64_t) * (size_t)ncost);
+    uint8_t *rf = malloc((size_t)ncost);
+    orc_type_costs(p, idx, cost, rf);
+    if (brute)
+        orc_brute_types(c.pp, T, k, p->n_layers, micro, cost, r);
+    else
+        orc_dp_types(c.pp, T, k, p->n_layers, micro, cost, r);
+    r->dp_const = orc_dp_const(p, &c, 0);
+    if (r->status == 0) {
+        r->opt += r->dp_const;
+        int a = 0;
+        for (int i = 0; i < c.pp; i++) {
+            int b = a + r->layers[i], h = 0, hn = T;
+            while (!((r->stage_mask[i] >> h) & 1)) h++;
+            if (i + 1 < c.pp)
+                for (hn = 0; !((r->stage_mask[i + 1] >> hn) & 1); hn++) {}
+            r->recompute[i] = rf[((((int64_t)i * T + h) * (T + 1) + hn) * W + a) * W + b];
+            a = b;
+        }
+    }
+    free(cost);
+    free(rf);
+    return 0;
+}
+
 static int32_t solve_with(const orc_problem *p, int64_t idx, orc_result *r, int mode)
 {
+    if (p->stage_types == 2) {   /* the device-count DP (threshold objective only) */
+        if (mode > 1) return -1;
+        return solve_types(p, idx, r, mode == 1);
+    }
     orc_config c;
     int32_t order, micro;
     if (orc_instance(p, idx, &c, &order, &micro)) return -1;

@@ -62,7 +62,9 @@ typedef struct orc_problem {
     int32_t prune_hetero, allow_recompute;
     /* search space */
     int32_t pp_max, tp_mask, cp_mask, ep_max, tpe_mask, mode;
-    int32_t stage_types;           /* 0: block orderings of the types; 1: free per-stage type */
+    int32_t stage_types;           /* 0: block orderings of the types; 1: free per-stage type, one
+                                      candidate per stage-type sequence; 2: free per-stage type
+                                      chosen by the DP over device counts (one order slot) */
     int32_t n_micro;
     int32_t micro[ORC_MAX_MICRO];
 } orc_problem;
@@ -158,5 +160,15 @@ int32_t orc_brute_exact(int32_t pp, int32_t n, int64_t micro, const int64_t *cos
 int32_t orc_solve_exact(const orc_problem *p, int64_t idx, orc_result *r);
 int32_t orc_solve_exact_many(const orc_problem *p, const int64_t *idx, int64_t n, orc_result *r);
 int32_t orc_solve_exact_brute(const orc_problem *p, int64_t idx, orc_result *r);
+
+/* Free per-stage device types by the DP over device counts (stage_types = 2):
+ * cost tensor [pp][T][T + 1][n + 1][n + 1], entry (s, h, h', a, b) = the cost
+ * of a type-h stage s on layers [a, b) followed by a type-h' stage (h' = T:
+ * the last stage); k[h] = stages of type h.  r->stage_mask gets 1 << h_i. */
+int32_t orc_type_costs(const orc_problem *p, int64_t idx, int64_t *cost, uint8_t *rflag);
+int32_t orc_dp_types(int32_t pp, int32_t T, const int32_t *k, int32_t n, int64_t micro, const int64_t *cost,
+                     orc_result *r);
+int32_t orc_brute_types(int32_t pp, int32_t T, const int32_t *k, int32_t n, int64_t micro, const int64_t *cost,
+                        orc_result *r);
 
 #endif

@@ -129,6 +129,10 @@ def lib():
         L.orc_solve_exact.argtypes = [P(OrcProblem), C.c_int64, P(OrcResult)]
         L.orc_solve_exact_brute.argtypes = [P(OrcProblem), C.c_int64, P(OrcResult)]
         L.orc_solve_exact_many.argtypes = [P(OrcProblem), C.c_void_p, C.c_int64, P(OrcResult)]
+        L.orc_type_costs.argtypes = [P(OrcProblem), C.c_int64, C.c_void_p, C.c_void_p]
+        for name in ("orc_dp_types", "orc_brute_types"):
+            getattr(L, name).argtypes = [C.c_int32, C.c_int32, C.c_void_p, C.c_int32, C.c_int64, C.c_void_p,
+                                         P(OrcResult)]
         _LIB = L
     return _LIB
 
@@ -257,6 +261,17 @@ class Oracle:
         self.L.orc_stages(C.byref(self.P), C.byref(self._cfg(cfg)), order, micro, st)
         return [{k: getattr(s, k) for k, _ in s._fields_} for s in st[: int(cfg[0])]]
 
+    def type_costs(self, idx):
+        """Device-count DP (stage_types = 2): cost[s][h][h'][a][b] and the recomputation flags."""
+        cfgs = self.configs()
+        pp = cfgs[idx // (self.n_orders() * self.P.n_micro)][0]
+        T, W = self.P.n_types, self.P.n_layers + 1
+        cost = np.zeros((pp, T, T + 1, W, W), dtype=np.int64)
+        rflag = np.zeros((pp, T, T + 1, W, W), dtype=np.uint8)
+        if self.L.orc_type_costs(C.byref(self.P), idx, _ptr(cost), _ptr(rflag)) != 0:
+            raise IndexError(idx)
+        return cost, rflag
+
     def segment_costs(self, idx):
         cfgs = self.configs()
         per = self.n_orders() * self.P.n_micro
@@ -360,6 +375,28 @@ def brute_exact(pp, n, micro, cost):
     return result_dict(r)
 
 
+def _types_call(name, k, n, micro, cost):
+    cost = np.ascontiguousarray(cost, dtype=np.int64)
+    pp, T = cost.shape[0], cost.shape[1]
+    assert cost.shape == (pp, T, T + 1, n + 1, n + 1) and len(k) == T and sum(k) == pp
+    kk = np.ascontiguousarray(k, dtype=np.int32)
+    r = OrcResult()
+    getattr(lib(), name)(pp, T, _ptr(kk), n, micro, _ptr(cost), C.byref(r))
+    d = result_dict(r)
+    d["types"] = [m.bit_length() - 1 for m in d["stage_mask"]] if d["status"] == 0 else []
+    return d
+
+
+def dp_types(k, n, micro, cost):
+    """Device-count DP on an explicit tensor [pp][T][T+1][n+1][n+1] (k[h] stages of type h)."""
+    return _types_call("orc_dp_types", k, n, micro, cost)
+
+
+def brute_types(k, n, micro, cost):
+    """Brute force over every stage-type sequence and composition on the same tensor."""
+    return _types_call("orc_brute_types", k, n, micro, cost)
+
+
 def solve_worker(args):
     """multiprocessing helper: (problem, instance indices[, "exact"]) -> results."""
     problem, idx = args[0], args[1]
@@ -368,5 +405,5 @@ def solve_worker(args):
     return Oracle(problem).solve_many(idx)
 
 
-__all__ = ["Oracle", "dp", "brute", "dp_exact", "brute_exact", "latency_1f1b", "INF", "lib",
-           "solve_worker"]
+__all__ = ["Oracle", "dp", "brute", "dp_exact", "brute_exact", "dp_types", "brute_types", "latency_1f1b",
+           "INF", "lib", "solve_worker"]

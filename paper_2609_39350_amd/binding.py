@@ -102,10 +102,13 @@ def lib():
         L.hapmoe_tables_layout.argtypes = [P(Problem), P(i64)]
         L.hapmoe_debug_layout.argtypes = [P(Problem), P(i64)]
         L.hapmoe_best_plan_ws_bytes.argtypes = [P(Problem), i64, P(i64)]
-        L.hapmoe_best_plan.argtypes = [P(Problem), vp, vp, i64, vp, i64, vp, vp, i64, P(Plan), vp]
+        L.hapmoe_best_plan.argtypes = [P(Problem), vp, vp, i64, vp, vp, i64, vp, vp, i64, P(Plan), vp]
+        L.hapmoe_stage_dp_types.argtypes = [P(Problem), vp, vp, i64, vp, i64, i64, i64, vp, vp, vp, vp, i64, vp]
+        L.hapmoe_stage_dp_types_ws_bytes.argtypes = [P(Problem), P(i64)]
         for f in ("hapmoe_validate", "hapmoe_enumerate_candidates", "hapmoe_image_bytes", "hapmoe_pack_image",
                   "hapmoe_tables_bytes", "hapmoe_debug_bytes", "hapmoe_tables_layout", "hapmoe_debug_layout", "hapmoe_eval_cost_tables", "hapmoe_stage_dp", "hapmoe_stage_dp_1f1b", "hapmoe_stage_dp_ws_bytes",
-                  "hapmoe_best_plan_ws_bytes", "hapmoe_best_plan"):
+                  "hapmoe_best_plan_ws_bytes", "hapmoe_best_plan", "hapmoe_stage_dp_types",
+                  "hapmoe_stage_dp_types_ws_bytes"):
             getattr(L, f).restype = C.c_int32
         _LIB = L
     return _LIB
@@ -299,10 +302,24 @@ def stage_dp_1f1b(problem, d_image, d_cand, n_cand, d_tables, first, count, d_re
            "hapmoe_stage_dp_1f1b")
 
 
-def best_plan(problem, d_cand, d_tables, d_res, n, d_ws, d_config_best=None, stream=None) -> dict:
+def stage_dp_types_ws_bytes(problem) -> int:
+    n = C.c_int64(0)
+    _check(lib().hapmoe_stage_dp_types_ws_bytes(_hp(problem).ref, C.byref(n)), "hapmoe_stage_dp_types_ws_bytes")
+    return n.value
+
+
+def stage_dp_types(problem, d_image, d_cand, n_cand, d_tables, first, count, d_res, d_types, d_ws, d_stats=None,
+                   stream=None):
+    _check(lib().hapmoe_stage_dp_types(_hp(problem).ref, _dptr(d_image), _dptr(d_cand), int(n_cand),
+                                       _dptr(d_tables), _nbytes(d_tables), int(first), int(count), _dptr(d_res),
+                                       _dptr(d_types), _dptr(d_stats), _dptr(d_ws), _nbytes(d_ws), _stream(stream)),
+           "hapmoe_stage_dp_types")
+
+
+def best_plan(problem, d_cand, d_tables, d_res, n, d_ws, d_config_best=None, stream=None, d_types=None) -> dict:
     plan = Plan()
     _check(lib().hapmoe_best_plan(_hp(problem).ref, _dptr(d_cand), _dptr(d_tables), _nbytes(d_tables),
-                                  _dptr(d_res), int(n), _dptr(d_config_best), _dptr(d_ws), _nbytes(d_ws),
+                                  _dptr(d_res), _dptr(d_types), int(n), _dptr(d_config_best), _dptr(d_ws), _nbytes(d_ws),
                                   C.byref(plan), _stream(stream)), "hapmoe_best_plan")
     pp = plan.n_stages
     return {"instance": plan.instance, "objective": plan.objective, "stage_sum": plan.stage_sum,
@@ -337,7 +354,14 @@ class Planner:
         self.d_res = torch.empty(max(self.n, 1) * RESULT_DTYPE.itemsize, **u8)
         self.d_stats = None
         self.d_ws = torch.empty(best_plan_ws_bytes(self.hp, max(self.n, 1)), **u8)
-        self.d_dp_ws = torch.empty(stage_dp_ws_bytes(self.hp), **u8)
+        # stage_types = 2: the device-count DP, which also returns each candidate's stage types
+        self.device_count_dp = int(problem["space"].get("stage_types", 0)) == 2
+        if self.device_count_dp:
+            self.d_dp_ws = torch.empty(stage_dp_types_ws_bytes(self.hp), **u8)
+            self.d_types = torch.zeros(max(self.n, 1) * MAX_STAGES, **u8)
+        else:
+            self.d_dp_ws = torch.empty(stage_dp_ws_bytes(self.hp), **u8)
+            self.d_types = None
         n_cfg = tables_layout(self.hp)["n_configs"]
         self.n_configs = n_cfg
         self.d_config_best = torch.empty(max(n_cfg, 1), dtype=torch.int64, device=self.device)
@@ -357,12 +381,18 @@ class Planner:
             self.d_stats = d_stats
         res = self.d_res[first * RESULT_DTYPE.itemsize:]
         st = None if d_stats is None else d_stats[4 * first:]
+        if self.device_count_dp:
+            if objective != "threshold":
+                raise ValueError("the device-count DP has the threshold objective only")
+            stage_dp_types(self.hp, self.d_image, self.d_cand, self.n, self.d_tables, first, count, res,
+                           self.d_types[first * MAX_STAGES:], self.d_dp_ws, st, stream)
+            return
         call = stage_dp if objective == "threshold" else stage_dp_1f1b
         call(self.hp, self.d_image, self.d_cand, self.n, self.d_tables, first, count, res, self.d_dp_ws, st, stream)
 
     def best_plan(self, stream=None):
         return best_plan(self.hp, self.d_cand, self.d_tables, self.d_res, self.n, self.d_ws, self.d_config_best,
-                         stream)
+                         stream, self.d_types)
 
     def run(self, stats=False, stream=None, objective="threshold"):
         self.eval_cost_tables(stream)
@@ -373,6 +403,11 @@ class Planner:
     def results(self) -> np.ndarray:
         self.torch.cuda.synchronize(self.device)
         return self.d_res.cpu().numpy()[: self.n * RESULT_DTYPE.itemsize].view(RESULT_DTYPE)
+
+    def stage_types(self) -> np.ndarray:
+        """Device-count DP: the stage type masks of every candidate, [n][32]."""
+        self.torch.cuda.synchronize(self.device)
+        return self.d_types.cpu().numpy()[: self.n * MAX_STAGES].reshape(-1, MAX_STAGES)
 
     def stats(self) -> np.ndarray:
         self.torch.cuda.synchronize(self.device)

@@ -68,7 +68,7 @@ int32_t check_fields(const hapmoe_problem *p)
     if (s.n_micro < 1 || s.n_micro > HAPMOE_MAX_MICRO) return HAPMOE_E_INVAL;
     for (int i = 0; i < s.n_micro; ++i)
         if (s.micro[i] < 1 || s.micro[i] > kMaxMicroValue) return HAPMOE_E_INVAL;
-    if (s.stage_types < 0 || s.stage_types > 1) return HAPMOE_E_INVAL;
+    if (s.stage_types < 0 || s.stage_types > 2) return HAPMOE_E_INVAL;
     return HAPMOE_OK;
 }
 
@@ -79,6 +79,7 @@ struct Space {
     int64_t n_orders = 1;   // orderings, or the most stage-type sequences (stage_types = 1)
     int kmax = 1;    // distinct device-type sets over the stages of any candidate
     int ppmax = 1;
+    int umax = 1;    // device-count DP: most states u = prod_h (k_h + 1) of a pipeline
 };
 
 constexpr int64_t kMaxFreeOrders = int64_t(1) << 20;
@@ -127,6 +128,7 @@ void build_space(const hapmoe_problem *p, Space &S)
     S.cfg.reserve(4096);
     S.kmax = 1;
     S.ppmax = 1;
+    S.umax = 1;
     const bool free_types = sp.stage_types != 0;
     S.n_orders = 1;
     for (int PP = 1; PP <= std::min(G, std::min(sp.pp_max, m.n_layers)); ++PP) {
@@ -165,7 +167,12 @@ void build_space(const hapmoe_problem *p, Space &S)
             for (int h = 0; h < T; ++h) straddle |= (c.count[h] % g) != 0;
             S.kmax = std::max(S.kmax, std::min(PP, T + (straddle ? T - 1 : 0)));
             S.ppmax = std::max(S.ppmax, PP);
-            if (free_types) S.n_orders = std::max(S.n_orders, arrangements(c, g));
+            if (sp.stage_types == 1) S.n_orders = std::max(S.n_orders, arrangements(c, g));
+            if (sp.stage_types == 2) {
+                int64_t U = 1;
+                for (int h = 0; h < T; ++h) U *= c.count[h] / g + 1;
+                S.umax = (int)std::min<int64_t>(std::max<int64_t>(S.umax, U), int64_t(1) << 30);
+            }
         }
     }
     std::array<int8_t, kMaxTypes> cur{};
@@ -181,10 +188,14 @@ void build_space(const hapmoe_problem *p, Space &S)
 int32_t check_problem(const hapmoe_problem *p)
 {
     if (const int32_t e = check_fields(p)) return e;
-    if (p->space.stage_types) {   // the sequence count and the key queue stay in range
+    if (p->space.stage_types) {   // the sequence count, the key queue and the DP states stay in range
         Space S;
         build_space(p, S);
         if (S.cfg.empty() || S.n_orders > kMaxFreeOrders || (int64_t)S.cfg.size() * S.n_orders > kMaxKeys)
+            return HAPMOE_E_INVAL;
+        if (p->space.stage_types == 2 &&
+            (S.umax > kMaxTypeStates ||
+             type_dp_lds(p->model.n_layers, p->cluster.n_types, p->space.n_micro, S.umax).bytes > kTypeDpMaxLds))
             return HAPMOE_E_INVAL;
     }
     return HAPMOE_OK;
@@ -444,6 +455,7 @@ int32_t stage_dp_any(const hapmoe_problem *p, const void *d_image, const hapmoe_
 {
     if (const int32_t e = check_problem(p)) return e;
     if (!d_image || !d_cand || !d_tables || !d_res || !d_ws) return HAPMOE_E_INVAL;
+    if (p->space.stage_types == 2) return HAPMOE_E_INVAL;   // hapmoe_stage_dp_types
     Space S;
     build_space(p, S);
     const int64_t per = per_config(p, S);
@@ -481,6 +493,41 @@ int32_t hapmoe_stage_dp_1f1b(const hapmoe_problem *p, const void *d_image, const
                         ws_bytes, stream, true);
 }
 
+int32_t hapmoe_stage_dp_types_ws_bytes(const hapmoe_problem *p, int64_t *bytes)
+{
+    if (const int32_t e = check_problem(p)) return e;
+    if (!bytes || p->space.stage_types != 2) return HAPMOE_E_INVAL;
+    Space S;
+    build_space(p, S);
+    *bytes = type_dp_ws_bytes(p->model.n_layers, p->cluster.n_types, S.umax, (int64_t)S.cfg.size());
+    return HAPMOE_OK;
+}
+
+int32_t hapmoe_stage_dp_types(const hapmoe_problem *p, const void *d_image, const hapmoe_candidate *d_cand,
+                              int64_t n_cand, const void *d_tables, int64_t tables_bytes, int64_t first,
+                              int64_t count, hapmoe_dp_result *d_res, uint8_t *d_types, int32_t *d_stats,
+                              void *d_ws, int64_t ws_bytes, void *stream)
+{
+    if (const int32_t e = check_problem(p)) return e;
+    if (p->space.stage_types != 2 || !d_image || !d_cand || !d_tables || !d_res || !d_types || !d_ws)
+        return HAPMOE_E_INVAL;
+    Space S;
+    build_space(p, S);
+    const int64_t ncfg = (int64_t)S.cfg.size(), per = per_config(p, S);
+    if (n_cand != ncfg * per) return HAPMOE_E_INVAL;
+    if (first < 0 || count < 0 || first + count > n_cand || count > INT32_MAX) return HAPMOE_E_RANGE;
+    const TablesLayout L = tables_layout(ncfg, (int)S.n_orders, p->cluster.n_types, p->model.n_layers);
+    if (tables_bytes < L.total ||
+        ws_bytes < type_dp_ws_bytes(p->model.n_layers, p->cluster.n_types, S.umax, ncfg))
+        return HAPMOE_E_WORKSPACE;
+    if (const int e = check_arch()) return e;
+    if (count == 0) return HAPMOE_OK;
+    if (launch_type_dp(d_image, d_cand, p->model.n_layers, p->cluster.n_types, p->space.n_micro, S.umax, L,
+                       d_tables, first, count, d_res, d_types, d_stats, d_ws, (hipStream_t)stream) != hipSuccess)
+        return HAPMOE_E_HIP;
+    return HAPMOE_OK;
+}
+
 int32_t hapmoe_best_plan_ws_bytes(const hapmoe_problem *p, int64_t n, int64_t *bytes)
 {
     if (const int32_t e = check_problem(p)) return e;
@@ -492,11 +539,12 @@ int32_t hapmoe_best_plan_ws_bytes(const hapmoe_problem *p, int64_t n, int64_t *b
 }
 
 int32_t hapmoe_best_plan(const hapmoe_problem *p, const hapmoe_candidate *d_cand, const void *d_tables,
-                         int64_t tables_bytes, const hapmoe_dp_result *d_res, int64_t n, int64_t *d_config_best,
-                         void *d_ws, int64_t ws_bytes, hapmoe_plan *h_plan, void *stream)
+                         int64_t tables_bytes, const hapmoe_dp_result *d_res, const uint8_t *d_types, int64_t n,
+                         int64_t *d_config_best, void *d_ws, int64_t ws_bytes, hapmoe_plan *h_plan, void *stream)
 {
     if (const int32_t e = check_problem(p)) return e;
     if (!d_cand || !d_tables || !d_res || !d_ws || !h_plan) return HAPMOE_E_INVAL;
+    if (p->space.stage_types == 2 ? !d_types : d_types != nullptr) return HAPMOE_E_INVAL;
     Space S;
     build_space(p, S);
     const int64_t per = per_config(p, S), ncfg = (int64_t)S.cfg.size();
@@ -507,8 +555,8 @@ int32_t hapmoe_best_plan(const hapmoe_problem *p, const hapmoe_candidate *d_cand
     if (const int e = check_arch()) return e;
     hipStream_t s = (hipStream_t)stream;
     const auto *tab = static_cast<const unsigned char *>(d_tables);
-    if (launch_best_plan(d_res, d_cand, tab + L.off_key, p->space.n_micro, n, per, ncfg, d_config_best, d_ws, s) !=
-        hipSuccess)
+    if (launch_best_plan(d_res, d_cand, tab + L.off_key, d_types, p->space.n_micro, n, per, ncfg, d_config_best,
+                         d_ws, s) != hipSuccess)
         return HAPMOE_E_HIP;
     // one copy: the global (objective, index) pair and the winner's records
     struct {

@@ -103,7 +103,8 @@ int64_t chunks_per_config(int64_t per) { return (per + kChunk - 1) / kChunk; }
 // best so that the host reads everything with one copy.
 __global__ __launch_bounds__(64) void k_gather(const Best *__restrict__ glob, const hapmoe_dp_result *__restrict__ res,
                                                const hapmoe_candidate *__restrict__ cand,
-                                               const unsigned char *__restrict__ key_info, int64_t n_micro,
+                                               const unsigned char *__restrict__ key_info,
+                                               const uint8_t *__restrict__ types, int64_t n_micro,
                                                uint32_t *__restrict__ out)
 {
     const Best b = *glob;
@@ -114,7 +115,10 @@ __global__ __launch_bounds__(64) void k_gather(const Best *__restrict__ glob, co
     if (w < kRes) out[w] = reinterpret_cast<const uint32_t *>(res + b.idx)[w];
     if (w < kCand) out[kRes + w] = reinterpret_cast<const uint32_t *>(cand + b.idx)[w];
     const auto *ki = reinterpret_cast<const uint32_t *>(key_info + (b.idx / n_micro) * (int64_t)sizeof(KeyInfo));
-    for (int i = w; i < kKey; i += 64) out[kRes + kCand + i] = ki[i];
+    // the device-count DP chooses each candidate's stage types: they replace the
+    // layout's type masks (KeyInfo words 2..9)
+    const auto *ty = types ? reinterpret_cast<const uint32_t *>(types + b.idx * kMaxStages) : nullptr;
+    for (int i = w; i < kKey; i += 64) out[kRes + kCand + i] = (ty && i >= 2 && i < 2 + kMaxStages / 4) ? ty[i - 2] : ki[i];
 }
 
 }  // namespace
@@ -129,8 +133,9 @@ int64_t best_plan_ws_bytes(int64_t n, int64_t per_config, int64_t n_configs)
 }
 
 hipError_t launch_best_plan(const hapmoe_dp_result *d_res, const hapmoe_candidate *d_cand,
-                            const unsigned char *d_key_info, int64_t n_micro, int64_t n, int64_t per_config,
-                            int64_t n_configs, int64_t *d_config_best, void *d_ws, hipStream_t s)
+                            const unsigned char *d_key_info, const uint8_t *d_types, int64_t n_micro, int64_t n,
+                            int64_t per_config, int64_t n_configs, int64_t *d_config_best, void *d_ws,
+                            hipStream_t s)
 {
     const int64_t chunks = chunks_per_config(per_config);
     Best *glob = static_cast<Best *>(d_ws);
@@ -142,7 +147,7 @@ hipError_t launch_best_plan(const hapmoe_dp_result *d_res, const hapmoe_candidat
     hipLaunchKernelGGL(k_seg_final, dim3((unsigned)((n_configs + kThreads - 1) / kThreads)), dim3(kThreads), 0, s,
                        partial, n_configs, chunks, cfg_best, d_config_best);
     hipLaunchKernelGGL(k_global, dim3(1), dim3(1024), 0, s, cfg_best, n_configs, glob);
-    hipLaunchKernelGGL(k_gather, dim3(1), dim3(64), 0, s, glob, d_res, d_cand, d_key_info, n_micro, winner);
+    hipLaunchKernelGGL(k_gather, dim3(1), dim3(64), 0, s, glob, d_res, d_cand, d_key_info, d_types, n_micro, winner);
     return hipGetLastError();
 }
 

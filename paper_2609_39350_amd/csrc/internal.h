@@ -3,6 +3,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
 
 #include <vector>
@@ -79,6 +80,7 @@ struct DebugLayout {
 
 static_assert(sizeof(PiInfo) == 152, "PiInfo layout is part of the documented table format");
 static_assert(sizeof(KeyInfo) == 136, "KeyInfo layout is part of the documented table format");
+static_assert(offsetof(KeyInfo, mask) == 8, "stage type masks at words 2..9");
 static_assert(sizeof(hapmoe_candidate) == 32 && sizeof(hapmoe_dp_result) == 64, "ABI record sizes");
 
 inline int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
@@ -119,14 +121,33 @@ hipError_t launch_stage_dp(const void *d_image, const hapmoe_candidate *d_cand, 
                            hapmoe_dp_result *d_res, int32_t *d_stats, void *d_ws, const int32_t *micro,
                            bool exact, hipStream_t s);
 int64_t stage_dp_ws_bytes();
+
+// Device-count DP (free per-stage device types by the DP state of device counts).
+constexpr int kMaxTypeStates = 8192;                        // states u = prod_h (k_h + 1) per pipeline
+constexpr int64_t kTypeDpMaxSlots = 512;                    // workgroups with a state slice each
+constexpr int64_t kTypeDpMaxSlotBytes = int64_t(8) << 30;   // all slices together
+constexpr int kTypeDpMaxLds = 64 * 1024;
+struct TypeLds {
+    int umax;
+    int off_t0, off_t1, off_mw, off_moe, off_inc, off_path, off_ctl, off_ulist, bytes;
+};
+TypeLds type_dp_lds(int n_layers, int n_types, int n_micro, int umax);
+int64_t type_dp_slot_bytes(int n_layers, int n_types, int umax);
+int64_t type_dp_slots(int64_t n_keys, int64_t slot_bytes);
+int64_t type_dp_ws_bytes(int n_layers, int n_types, int umax, int64_t n_configs);
+hipError_t launch_type_dp(const void *d_image, const hapmoe_candidate *d_cand, int n_layers, int n_types,
+                          int n_micro, int umax, const TablesLayout &L, const void *d_tables, int64_t first,
+                          int64_t count, hapmoe_dp_result *d_res, uint8_t *d_types, int32_t *d_stats, void *d_ws,
+                          hipStream_t s);
 // bytes of the winner record in the best-plan workspace (result, candidate, stage layout)
 constexpr int64_t kWinnerBytes = 256;
 static_assert(sizeof(hapmoe_dp_result) + sizeof(hapmoe_candidate) + sizeof(KeyInfo) <= kWinnerBytes, "winner");
 static_assert(sizeof(hapmoe_dp_result) % 4 == 0 && sizeof(hapmoe_candidate) % 4 == 0 && sizeof(KeyInfo) % 4 == 0,
               "word copies");
 hipError_t launch_best_plan(const hapmoe_dp_result *d_res, const hapmoe_candidate *d_cand,
-                            const unsigned char *d_key_info, int64_t n_micro, int64_t n, int64_t per_config,
-                            int64_t n_configs, int64_t *d_config_best, void *d_ws, hipStream_t s);
+                            const unsigned char *d_key_info, const uint8_t *d_types, int64_t n_micro, int64_t n,
+                            int64_t per_config, int64_t n_configs, int64_t *d_config_best, void *d_ws,
+                            hipStream_t s);
 int64_t best_plan_ws_bytes(int64_t n, int64_t per_config, int64_t n_configs);
 
 }  // namespace hapmoe

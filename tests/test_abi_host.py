@@ -125,7 +125,7 @@ def test_free_stage_types_enumeration_and_limits():
         assert binding.tables_layout(q)["n_orders"] == o.n_orders()
     q = variant(workloads.config(2), **{"space.stage_types": 1})
     assert binding.tables_layout(q)["n_orders"] == 420   # 8! / (4! 2! 2!)
-    for bad in (2, -1):
+    for bad in (3, -1):
         with pytest.raises(binding.HapmoeError):
             binding.validate(variant(q, **{"space.stage_types": bad}))
     # 4 types x 64 devices at PP = 16: 16! / (4!)^4 sequences
@@ -138,3 +138,30 @@ def test_free_stage_types_enumeration_and_limits():
     assert list(empty["cluster"]["count"]) == [5, 3] and orc.Oracle(empty).n_instances() == 0
     with pytest.raises(binding.HapmoeError):
         binding.validate(empty)
+
+
+def test_device_count_dp_space_and_limits():
+    # stage_types = 2: one order slot per configuration, the same configurations
+    # as the sequence mode, its own workspace query, and the state limit
+    import ctypes as C
+    for p in (workloads.config(2), workloads.random_tiny(901, n_types=3)):
+        q = variant(p, **{"space.stage_types": 2})
+        o = orc.Oracle(q)
+        cand = binding.enumerate_candidates(q)
+        assert len(cand) == o.n_instances() == len(o.configs()) * len(q["space"]["micro"])
+        assert (cand["order"] == 0).all()
+        assert binding.tables_layout(q)["n_orders"] == 1
+        assert binding.stage_dp_types_ws_bytes(q) > 256
+        with pytest.raises(binding.HapmoeError):
+            binding.stage_dp_types_ws_bytes(variant(q, **{"space.stage_types": 1}))
+        hp = binding.HostProblem(q)
+        n = C.c_int64(0)
+        # the fixed-type stage DP refuses the mode (before any device work)
+        assert binding.lib().hapmoe_stage_dp(hp.ref, None, None, 0, None, 0, 0, 0, None, None, None, 0,
+                                             None) == -1
+    # 4 types x 64 devices at PP = 16: 5^4 count states, fine; a 4 x 256-device
+    # cluster at PP = 32 has 9^4 = 6561, also within 8192
+    binding.validate(variant(workloads.config(3), **{"space.stage_types": 2}))
+    binding.validate(variant(workloads.config(4), **{"space.stage_types": 2}))
+    with pytest.raises(binding.HapmoeError):
+        binding.validate(variant(workloads.config(3), **{"space.stage_types": 3}))

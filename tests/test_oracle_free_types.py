@@ -163,4 +163,98 @@ def test_empty_slots_are_infeasible():
 
 def test_stage_types_field_is_checked():
     with pytest.raises(ValueError):
-        orc.Oracle(variant(workloads.config(1), **{"space.stage_types": 2}))
+        orc.Oracle(variant(workloads.config(1), **{"space.stage_types": 3}))
+
+
+# ---------------------------------------------------------------------------
+# stage_types = 2: the DP over device counts (Section 3.4's state m) picks the
+# stage types itself; one order slot per configuration.
+def count_dp(p):
+    return variant(p, **{"space.stage_types": 2})
+
+
+def _key(r):
+    return (r["status"], r["opt"], r["sum"], r["tmax"], r["layers"], r["types"])
+
+
+def test_count_dp_core_matches_brute_force():
+    # explicit cost tensors with many ties and holes: the DP and the enumeration of
+    # every (sequence, composition) agree on the value and on the canonical choice
+    rng = np.random.default_rng(11)
+    INF = np.iinfo(np.int64).max
+    checked = feasible = 0
+    while checked < 250:
+        T = int(rng.integers(1, 4))
+        k = [int(x) for x in rng.integers(0, 3, size=T)]
+        if sum(k) == 0:
+            k[int(rng.integers(0, T))] = 1
+        pp = sum(k)
+        if pp > 5:
+            continue
+        n = int(rng.integers(pp, pp + 4))
+        cost = rng.integers(1, int(rng.choice([4, 30, 1000])), size=(pp, T, T + 1, n + 1, n + 1)).astype(np.int64)
+        cost[rng.random(cost.shape) < rng.uniform(0.0, 0.5)] = INF
+        B = int(rng.integers(1, 6))
+        a, b = orc.dp_types(k, n, B, cost), orc.brute_types(k, n, B, cost)
+        assert _key(a) == _key(b), (k, n, B, a, b)
+        checked += 1
+        feasible += a["status"] == 0
+    assert feasible > 100
+
+
+def test_count_dp_is_the_best_stage_type_sequence():
+    # on whole problems: the least objective over every sequence of the
+    # sequence-enumeration mode, its smallest threshold, and a chosen sequence
+    # whose own optimum is that value; brute force agrees in every field
+    done = 0
+    for seed in range(900, 940):
+        base = workloads.random_tiny(seed, n_types=2 + seed % 2)
+        o1, o2 = orc.Oracle(free(base)), orc.Oracle(count_dp(base))
+        if o1.n_instances() == 0:
+            continue
+        nB, no = len(base["space"]["micro"]), o1.n_orders()
+        assert o2.n_orders() == 1 and o2.configs() == o1.configs()
+        assert o2.n_instances() == len(o1.configs()) * nB
+        for ci, cfg in enumerate(o1.configs()):
+            for j in range(nB):
+                rs = o1.solve_many([(ci * no + o) * nB + j for o in range(no)])
+                r2, rb = o2.solve(ci * nB + j), o2.solve_brute(ci * nB + j)
+                assert {k: r2[k] for k in r2 if k != "thresholds"} == {k: rb[k] for k in rb if k != "thresholds"}
+                feas = [r for r in rs if r["status"] == 0]
+                if not feas:
+                    assert r2["status"] == 1
+                    continue
+                assert (r2["opt"], r2["tmax"]) == min((r["opt"], r["tmax"]) for r in feas)
+                seq = [m.bit_length() - 1 for m in r2["stage_mask"]]
+                own = rs[_find_sequence(o1, cfg[0], seq)]
+                assert (own["opt"], own["tmax"], own["sum"]) == (r2["opt"], r2["tmax"], r2["sum"])
+                assert r2["dp_const"] == o1.dp_const(cfg, 0)
+                done += 1
+    assert done > 60
+
+
+def test_count_dp_one_type_is_block_mode():
+    for s in range(4):
+        p = workloads.random_tiny(300 + s, n_types=1)
+        ob, oc = orc.Oracle(p), orc.Oracle(count_dp(p))
+        n = ob.n_instances()
+        assert oc.n_instances() == n
+        for a, b in zip(ob.solve_many(range(n)), oc.solve_many(range(n))):
+            skip = ("thresholds",) if a["status"] == 0 else ("thresholds", "stage_mask")   # no chosen types
+            assert {k: a[k] for k in a if k not in skip} == {k: b[k] for k in b if k not in skip}
+
+
+def test_count_dp_config2_against_sequences():
+    # 3 device types, pipelines of 4 and 8 stages: a stride sample
+    p = workloads.config(2)
+    o1, o2 = orc.Oracle(free(p)), orc.Oracle(count_dp(p))
+    nB, no = len(p["space"]["micro"]), o1.n_orders()
+    cfgs = o1.configs()
+    for ci in range(0, len(cfgs), 47):
+        for j in range(nB):
+            r2 = o2.solve(ci * nB + j)
+            rs = [r for r in o1.solve_many([(ci * no + o) * nB + j for o in range(no)]) if r["status"] == 0]
+            if not rs:
+                assert r2["status"] == 1
+                continue
+            assert (r2["opt"], r2["tmax"]) == min((r["opt"], r["tmax"]) for r in rs), (ci, j)
