@@ -143,41 +143,60 @@ def leg_1f1b(torch, pl, stream, steps, warmup):
                           "layers": plan["layers"]}}
 
 
-def leg_free_types(torch, binding, workloads, n_config, dev, stream, steps, warmup):
-    """Free per-stage device types on a workload small enough to enumerate every
-    stage-type sequence: the whole step timed, and its best objective beside the
-    best over the block orderings of the same workload."""
-    import copy
+def _timed_steps(torch, pl, stream, steps, warmup):
+    """Whole steps (tables, stage DP, arg-min) and the stage-DP events of each."""
     import numpy as np
-    base = workloads.config(n_config)
-    free = copy.deepcopy(base)
-    free["space"]["stage_types"] = 1
-    pb, pf = binding.Planner(base, dev), binding.Planner(free, dev)
-    block_best = pb.run()["objective"]
     for _ in range(warmup):
-        pf.run()
+        pl.run()
     torch.cuda.synchronize()
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
     t0 = time.perf_counter()
     plan = None
     for k in range(steps):
-        pf.eval_cost_tables()
+        pl.eval_cost_tables()
         ev[k][0].record(stream)
-        pf.stage_dp()
+        pl.stage_dp()
         ev[k][1].record(stream)
-        plan = pf.best_plan()
+        plan = pl.best_plan()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    res = pf.results()
-    return {"workload": f"config {n_config}: {WORKLOADS[n_config]}, every stage one device type",
-            "value": pf.n * steps / elapsed, "unit": "candidates/s", "ms_per_step": elapsed * 1e3 / steps,
-            "stage_dp_ms": float(np.mean([ev[k][0].elapsed_time(ev[k][1]) for k in range(steps)])),
-            "candidates": pf.n, "sequences_per_config": int(binding.tables_layout(free)["n_orders"]),
-            "feasible_candidates": int((res["status"] == 0).sum()),
-            "best_objective_ns": plan["objective"], "block_orderings_best_ns": block_best,
-            "gain_over_block_orderings": 1.0 - plan["objective"] / block_best,
-            "best_plan": {"config": plan["config"], "order": plan["order"], "B": plan["n_micro"],
-                          "stage_types": plan["stage_types"], "layers": plan["layers"]}}
+    return plan, elapsed, float(np.mean([ev[k][0].elapsed_time(ev[k][1]) for k in range(steps)]))
+
+
+def leg_free_types(torch, binding, workloads, dev, stream, steps, warmup, cpu_sample):
+    """Free per-stage device types: every stage-type sequence as its own candidate
+    (config 2), and the DP over device counts (configs 2 and 3, pipelines up to
+    16 stages); each with the best objective of the block orderings beside it."""
+    import copy
+    import numpy as np
+    out = {}
+    for name, n_config, mode in (("sequences", 2, 1), ("device_count_dp", 2, 2), ("device_count_dp", 3, 2)):
+        base = workloads.config(n_config)
+        free = copy.deepcopy(base)
+        free["space"]["stage_types"] = mode
+        block_best = binding.Planner(base, dev).run()["objective"]
+        pf = binding.Planner(free, dev)
+        pf.eval_cost_tables()
+        pf.stage_dp(stats=True)
+        st = pf.stats()
+        plan, elapsed, dp_ms = _timed_steps(torch, pf, stream, steps, warmup)
+        res = pf.results()
+        rec = {"workload": f"config {n_config}: {WORKLOADS[n_config]}, every stage one device type",
+               "value": pf.n * steps / elapsed, "unit": "candidates/s", "ms_per_step": elapsed * 1e3 / steps,
+               "stage_dp_ms": dp_ms, "candidates": pf.n,
+               "feasible_candidates": int((res["status"] == 0).sum()),
+               "dp_passes_per_candidate": {"mean": float(st[:, 0].mean()), "max": int(st[:, 0].max())},
+               "relaxations_per_launch": int(st[:, 1].astype(np.int64).sum()),
+               "best_objective_ns": plan["objective"], "block_orderings_best_ns": block_best,
+               "gain_over_block_orderings": 1.0 - plan["objective"] / block_best,
+               "best_plan": {"config": plan["config"], "order": plan["order"], "B": plan["n_micro"],
+                             "stage_types": plan["stage_types"], "layers": plan["layers"]}}
+        if mode == 1:
+            rec["sequences_per_config"] = int(binding.tables_layout(free)["n_orders"])
+        if mode == 2 and n_config == 2 and cpu_sample:
+            rec["cpu_baseline"], _ = cpu_baseline(free, pf.n, cpu_sample)
+        out[f"{name}_config{n_config}"] = rec
+    return out
 
 
 def cpu_baseline(problem, n_total, n_sample, exact=False):
@@ -211,8 +230,8 @@ def main():
     ap.add_argument("--cpu-sample-1f1b", type=int, default=200)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-1f1b", action="store_true", help="skip the 1F1B re-scoring leg")
-    ap.add_argument("--free-types-config", type=int, default=2,
-                    help="workload of the free per-stage device-type leg (0: skip it)")
+    ap.add_argument("--no-free-types", action="store_true", help="skip the free per-stage device-type legs")
+    ap.add_argument("--cpu-sample-free", type=int, default=40)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (counter scaling for HBM traffic)")
     args = ap.parse_args()
@@ -304,9 +323,9 @@ def main():
         out["objective_1f1b"] = leg_1f1b(torch, pl, stream, args.steps, args.warmup)
         if not args.no_cpu_baseline:
             out["objective_1f1b"]["cpu_baseline"], _ = cpu_baseline(problem, n, args.cpu_sample_1f1b, exact=True)
-    if args.free_types_config:
-        out["free_stage_types"] = leg_free_types(torch, binding, workloads, args.free_types_config, dev, stream,
-                                                 args.steps, args.warmup)
+    if not args.no_free_types:
+        out["free_stage_types"] = leg_free_types(torch, binding, workloads, dev, stream, args.steps, args.warmup,
+                                                 0 if args.no_cpu_baseline else args.cpu_sample_free)
     if calib is not None:
         out["copy_calibration_bytes"] = calib
     if not args.no_cpu_baseline:

@@ -160,8 +160,10 @@ def test_device_count_dp_space_and_limits():
         assert binding.lib().hapmoe_stage_dp(hp.ref, None, None, 0, None, 0, 0, 0, None, None, None, 0,
                                              None) == -1
     # 4 types x 64 devices at PP = 16: 5^4 count states, fine; a 4 x 256-device
-    # cluster at PP = 32 has 9^4 = 6561, also within 8192
+    # cluster at PP = 32 has 9^4 = 6561, past the 4096 limit (PP <= 16 is fine)
     binding.validate(variant(workloads.config(3), **{"space.stage_types": 2}))
-    binding.validate(variant(workloads.config(4), **{"space.stage_types": 2}))
+    with pytest.raises(binding.HapmoeError):
+        binding.validate(variant(workloads.config(4), **{"space.stage_types": 2}))
+    binding.validate(variant(workloads.config(4), **{"space.stage_types": 2, "space.pp_max": 16}))
     with pytest.raises(binding.HapmoeError):
         binding.validate(variant(workloads.config(3), **{"space.stage_types": 3}))

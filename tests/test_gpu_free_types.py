@@ -88,12 +88,14 @@ def count_dp(p):
     return variant(p, **{"space.stage_types": 2})
 
 
-def compare_types(problem, pl, idx):
-    """Every field of compare() plus the stage types the DP chose."""
+def compare_types(problem, pl, idx, slow=False):
+    """Every field of compare() plus the stage types the DP chose (slow: the
+    oracle takes seconds per candidate, so it runs in worker processes)."""
     from tests.test_gpu_parity import oracle_many
-    compare(problem, pl, idx)
+    ref = oracle_many(problem, idx, pool=True if slow else None)
+    compare(problem, pl, idx, ref=ref)
     ty = pl.stage_types()
-    for i, r in zip(idx, oracle_many(problem, idx)):
+    for i, r in zip(idx, ref):
         got = [int(x) for x in ty[i]]
         if r["status"] == 0:
             assert got[:r["pp"]] == r["stage_mask"] and not any(got[r["pp"]:]), (i, got, r)
@@ -135,7 +137,7 @@ def test_count_dp_config3_sampled(torch):
     pl = binding.Planner(p, "cuda:0")
     plan = pl.run()
     idx = sorted(set(list(range(pl.n - 1, 0, -(pl.n // 12))) + [plan["instance"]]))
-    compare_types(p, pl, idx)
+    compare_types(p, pl, idx, slow=True)
 
 
 @pytest.mark.parametrize("n", [3, 5])

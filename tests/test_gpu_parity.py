@@ -29,9 +29,11 @@ def _pool():
     return _POOL
 
 
-def oracle_many(problem, idx, objective="threshold"):
+def oracle_many(problem, idx, objective="threshold", pool=None):
+    """The oracle on candidates idx: in worker processes for long lists (or when
+    pool is True: few candidates that take seconds each)."""
     idx = [int(i) for i in idx]
-    if len(idx) < 64:
+    if not pool and len(idx) < 64:
         o = orc.Oracle(problem)
         return o.solve_many(idx) if objective == "threshold" else o.solve_exact_many(idx)
     n = _pool()._processes
@@ -53,10 +55,11 @@ def torch():
     return t
 
 
-def compare(problem, planner, idx, res=None, objective="threshold"):
-    """Element-by-element parity of the DP results at candidate indices idx."""
+def compare(problem, planner, idx, res=None, objective="threshold", ref=None):
+    """Element-by-element parity of the DP results at candidate indices idx
+    (ref: the oracle's results there, if already computed)."""
     res = planner.results() if res is None else res
-    ref = oracle_many(problem, idx, objective)
+    ref = oracle_many(problem, idx, objective) if ref is None else ref
     bad = []
     for i, r in zip(idx, ref):
         g = res[i]
