@@ -123,7 +123,7 @@ hipError_t launch_stage_dp(const void *d_image, const hapmoe_candidate *d_cand, 
 int64_t stage_dp_ws_bytes();
 
 // Device-count DP (free per-stage device types by the DP state of device counts).
-constexpr int kMaxTypeStates = 8192;                        // states u = prod_h (k_h + 1) per pipeline
+constexpr int kMaxTypeStates = 4096;                        // states u = prod_h (k_h + 1) per pipeline
 constexpr int64_t kTypeDpMaxSlots = 512;                    // workgroups with a state slice each
 constexpr int64_t kTypeDpMaxSlotBytes = int64_t(8) << 30;   // all slices together
 constexpr int kTypeDpMaxLds = 64 * 1024;

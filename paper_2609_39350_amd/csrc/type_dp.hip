@@ -37,7 +37,7 @@
 namespace hapmoe {
 namespace {
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 1024;
 constexpr int64_t kNone = INT64_MAX;   // no path
 
 struct TypePath {   // result of one pass, filled by thread 0
@@ -62,8 +62,32 @@ struct TypeCtl {   // workgroup-uniform scalars set by thread 0
     int64_t t, finf, lastF;
     int32_t cnt[kMaxStages + 2];   // states per level
     int32_t start[kMaxStages + 2];
+    int32_t wmax[kMaxStages + 2];  // widest end-layer band of a level
     uint32_t relax;
 };
+
+// one state vector u of a level: u | 6-bit digits u_h | band start | band width
+__device__ inline uint64_t pack_u(int u, const int *d, int blo, int wd)
+{
+    uint64_t x = (uint64_t)u | ((uint64_t)blo << 37) | ((uint64_t)wd << 45);
+#pragma unroll
+    for (int h = 0; h < kMaxTypes; ++h) x |= (uint64_t)d[h] << (13 + 6 * h);
+    return x;
+}
+
+// exact q = floor(i / d), r = i - q d for 0 <= i < 2^24, d >= 1, inv = 1/d in fp32
+__device__ inline void div_small(int i, int d, float inv, int &q, int &r)
+{
+    q = (int)((float)i * inv);
+    r = i - q * d;
+    if (r < 0) {
+        --q;
+        r += d;
+    } else if (r >= d) {
+        ++q;
+        r -= d;
+    }
+}
 
 // the pure type-h stage s on [a, b) followed by hn (kMaxTypes: none); returns
 // kNone if its memory does not fit, else the cost and *r
@@ -112,7 +136,7 @@ __global__ __launch_bounds__(kThreads) void k_type_dp(const unsigned char *__res
     int64_t *sMW = reinterpret_cast<int64_t *>(smem + S.off_mw);
     int64_t *sMA0 = sMW + W, *sMA1 = sMA0 + W;
     int32_t *sMOE = reinterpret_cast<int32_t *>(smem + S.off_moe);
-    uint16_t *ulist = reinterpret_cast<uint16_t *>(smem + S.off_ulist);
+    uint64_t *ulist = reinterpret_cast<uint64_t *>(smem + S.off_ulist);
     TypeInc *inc = reinterpret_cast<TypeInc *>(smem + S.off_inc);
     TypePath &P = *reinterpret_cast<TypePath *>(smem + S.off_path);
     TypeCtl &C = *reinterpret_cast<TypeCtl *>(smem + S.off_ctl);
@@ -155,7 +179,10 @@ __global__ __launch_bounds__(kThreads) void k_type_dp(const unsigned char *__res
         const bool shape_ok = pi->status == HAPMOE_STATUS_OK && sum_lo <= N && sum_hi >= N && U <= S.umax;
 
         // ---- levels: the u of each sum, then prefix sums to LDS ----
-        if (tid < kMaxStages + 2) C.cnt[tid] = 0;
+        if (tid < kMaxStages + 2) {
+            C.cnt[tid] = 0;
+            C.wmax[tid] = 0;
+        }
         __syncthreads();
         auto level_of = [&](int u) {
             int l = 0;
@@ -177,7 +204,22 @@ __global__ __launch_bounds__(kThreads) void k_type_dp(const unsigned char *__res
         }
         __syncthreads();
         if (shape_ok)
-            for (int u = tid; u < U; u += kThreads) ulist[atomicAdd(&C.cnt[level_of(u)], 1)] = (uint16_t)u;
+            for (int u = tid; u < U; u += kThreads) {   // digits and the band of end layers the windows leave
+                int d[kMaxTypes], l = 0, ulo = 0, uhi = 0, rlo = 0, rhi = 0;
+#pragma unroll
+                for (int h = 0; h < kMaxTypes; ++h) {
+                    d[h] = (u / rad[h]) % (k[h] + 1);
+                    l += d[h];
+                    ulo += d[h] * lo[h];
+                    uhi += d[h] * hi[h];
+                    rlo += (k[h] - d[h]) * lo[h];
+                    rhi += (k[h] - d[h]) * hi[h];
+                }
+                const int blo = ulo > N - rhi ? ulo : N - rhi, bhi = uhi < N - rlo ? uhi : N - rlo;
+                const int wd = bhi >= blo ? bhi - blo + 1 : 0;
+                ulist[atomicAdd(&C.cnt[l], 1)] = pack_u(u, d, wd ? blo : 0, wd);
+                atomicMax(&C.wmax[l], wd);
+            }
         const int64_t *mem = reinterpret_cast<const int64_t *>(tab + L.off_mem) + key * 4 * np;
         const int64_t *time = reinterpret_cast<const int64_t *>(tab + L.off_time) + key * L.n_masks * 3 * np;
         for (int b = tid; b < W; b += kThreads) {
@@ -206,15 +248,21 @@ __global__ __launch_bounds__(kThreads) void k_type_dp(const unsigned char *__res
             for (int l = 1; l <= PP; ++l) {
                 const int s = l - 1;   // the stage that ends at b
                 const int64_t ms = (PP - s) < v ? (PP - s) : v;
-                const int n_items = (C.start[l + 1] - C.start[l]) * W * T1;
+                const int wm = C.wmax[l], row = wm * T1;
+                const int n_items = (C.start[l + 1] - C.start[l]) * row;
+                const float inv_row = row ? 1.0f / (float)row : 0.0f, inv_t1 = 1.0f / (float)T1;
                 for (int i = tid; i < n_items; i += kThreads) {
-                    const int u = ulist[C.start[l] + i / (W * T1)];
-                    const int rem = i % (W * T1), b = rem / T1, hn = rem % T1;
-                    // digits of u, and the band of end layers the windows leave for it
+                    int pos, rem, j, hn;
+                    div_small(i, row, inv_row, pos, rem);
+                    div_small(rem, T1, inv_t1, j, hn);
+                    const uint64_t x = ulist[C.start[l] + pos];
+                    const int wd = (int)(x >> 45) & 0x1ff;
+                    if (j >= wd) continue;
+                    const int u = (int)(x & 0x1fff), b = ((int)(x >> 37) & 0xff) + j;
                     int d[kMaxTypes], ulo = 0, uhi = 0, rlo = 0, rhi = 0, dn = 0, kn = 0;
 #pragma unroll
                     for (int h = 0; h < kMaxTypes; ++h) {
-                        d[h] = (u / rad[h]) % (k[h] + 1);
+                        d[h] = (int)(x >> (13 + 6 * h)) & 63;
                         ulo += d[h] * lo[h];
                         uhi += d[h] * hi[h];
                         rlo += (k[h] - d[h]) * lo[h];
@@ -225,8 +273,6 @@ __global__ __launch_bounds__(kThreads) void k_type_dp(const unsigned char *__res
                         }
                     }
                     if (l == PP ? hn != T : (hn == T || dn >= kn)) continue;
-                    const int blo = ulo > N - rhi ? ulo : N - rhi, bhi = uhi < N - rlo ? uhi : N - rlo;
-                    if (b < blo || b > bhi) continue;
                     int64_t best = kNone;
                     int bk = 0x7fff;
 #pragma unroll
@@ -241,18 +287,26 @@ __global__ __launch_bounds__(kThreads) void k_type_dp(const unsigned char *__res
                         const int a0 = (b - hi[h]) > plo ? (b - hi[h]) : plo;
                         const int a1 = (b - lo[h]) < phi ? (b - lo[h]) : phi;
                         const int64_t cap = H.mem_bytes[h];
-                        for (int a = a0; a <= a1; ++a) {
-                            const int64_t prev = F[((int64_t)up * W + a) * T1 + h];
-                            if (STATS) ++relax;
-                            if (prev == kNone) continue;
-                            int r;
-                            const int64_t c = stage_cost(D, h, a, b, ms, cap, X, recomp, pc, &r);
-                            if (c == kNone || c > t) continue;
-                            const int64_t val = prev + c;
-                            const int key2 = a * 8 + h;
-                            if (val < best || (val == best && key2 < bk)) {
-                                best = val;
-                                bk = key2;
+                        const int64_t *Fp = F + (int64_t)up * W * T1 + h;
+                        for (int a = a0; a <= a1; a += 2) {   // two split points a trip: both loads in flight
+                            const bool two = a + 1 <= a1;
+                            const int64_t prev0 = Fp[(int64_t)a * T1];
+                            const int64_t prev1 = two ? Fp[(int64_t)(a + 1) * T1] : kNone;
+                            if (STATS) relax += two ? 2 : 1;
+#pragma unroll
+                            for (int e = 0; e < 2; ++e) {
+                                const int64_t prev = e ? prev1 : prev0;
+                                if (prev == kNone) continue;
+                                const int ae = a + e;
+                                int r;
+                                const int64_t c = stage_cost(D, h, ae, b, ms, cap, X, recomp, pc, &r);
+                                if (c == kNone || c > t) continue;
+                                const int64_t val = prev + c;
+                                const int key2 = ae * 8 + h;
+                                if (val < best || (val == best && key2 < bk)) {
+                                    best = val;
+                                    bk = key2;
+                                }
                             }
                         }
                     }
@@ -422,7 +476,7 @@ TypeLds type_dp_lds(int n_layers, int n_types, int n_micro, int umax)
     S.off_inc = take((int64_t)n_micro * sizeof(TypeInc));
     S.off_path = take(sizeof(TypePath));
     S.off_ctl = take(sizeof(TypeCtl));
-    S.off_ulist = take((int64_t)umax * 2);
+    S.off_ulist = take((int64_t)umax * 8);
     S.bytes = (int)off;
     return S;
 }
