@@ -1207,6 +1207,199 @@ int32_t orc_brute_types(int32_t pp, int32_t T, const int32_t *k, int32_t n, int6
     return 0;
 }
 
+/* 1F1B re-scoring over the device-count DP (stage_types = 2): the frontier
+ * points are the thresholds at which F_t drops, each with the canonical path
+ * at t (whose largest stage is then t); each is scored with
+ * orc_latency_1f1b of its stage costs in pipeline order.  Least latency, ties
+ * to the lower largest stage. */
+int32_t orc_dp_types_exact(int32_t pp, int32_t T, const int32_t *k, int32_t n, int64_t micro, const int64_t *cost,
+                           orc_result *r)
+{
+    type_space S;
+    type_space_init(&S, pp, T, k, n);
+    int W = S.W, T1 = T + 1;
+    int64_t ncost = (int64_t)pp * T * T1 * W * W;
+    memset(r, 0, sizeof(*r));
+    r->pp = pp;
+    int64_t *theta = malloc(sizeof(int64_t) * (size_t)(ncost + 1));
+    int64_t nt = 0;
+    for (int64_t i = 0; i < ncost; i++)
+        if (cost[i] != ORC_INF) theta[nt++] = cost[i];
+    qsort(theta, (size_t)nt, sizeof(int64_t), cmp_i64);
+    int64_t nu = 0;
+    for (int64_t i = 0; i < nt; i++)
+        if (nu == 0 || theta[i] != theta[nu - 1]) theta[nu++] = theta[i];
+    int64_t *F = malloc(sizeof(int64_t) * (size_t)S.U * W * T1);
+    int32_t *arg = malloc(sizeof(int32_t) * (size_t)S.U * W * T1);
+    int64_t best = ORC_INF, prev = ORC_INF, points = 0;
+    for (int64_t i = 0; i < nu; i++) {
+        int64_t t = theta[i];
+        int64_t f = type_pass(&S, cost, t, F, arg);
+        if (f == ORC_INF || f >= prev) continue;   /* not a frontier point */
+        prev = f;
+        points++;
+        int64_t c[ORC_MAX_STAGES], mx = 0;
+        uint8_t len[ORC_MAX_STAGES], mask[ORC_MAX_STAGES];
+        int u = S.U - 1, b = n, hn = T;
+        for (int j = pp - 1; j >= 0; j--) {
+            int32_t x = arg[((int64_t)u * W + b) * T1 + hn];
+            int a = x / 8, h = x % 8;
+            c[j] = cost_at(&S, cost, j, h, hn, a, b);
+            len[j] = (uint8_t)(b - a);
+            mask[j] = (uint8_t)(1 << h);
+            if (c[j] > mx) mx = c[j];
+            u -= S.rad[h];
+            b = a;
+            hn = h;
+        }
+        int64_t lat = orc_latency_1f1b(pp, c, micro);
+        if (lat < best) {
+            best = lat;
+            r->sum = f;
+            r->tmax = mx;
+            memcpy(r->layers, len, (size_t)pp);
+            memcpy(r->stage_mask, mask, (size_t)pp);
+        }
+    }
+    r->thresholds = points;
+    if (best == ORC_INF) {
+        r->status = 1;
+        r->opt = r->sum = r->tmax = ORC_INF;
+        memset(r->stage_mask, 0, sizeof(r->stage_mask));
+    } else {
+        r->opt = best;
+    }
+    free(theta);
+    free(F);
+    free(arg);
+    return 0;
+}
+
+/* Brute force of the same: every (sequence, composition), the Pareto-optimal
+ * (max, sum) pairs, per pair the smallest (b_{pp-1}, h_{pp-1}, ..., b_1, h_1,
+ * h_0), then the least latency, ties to the lower max. */
+typedef struct type_rec {
+    int64_t mx, sum, c[ORC_MAX_STAGES];
+    int seq[ORC_MAX_STAGES], b[ORC_MAX_STAGES + 1];
+} type_rec;
+
+typedef struct type_recs {
+    const type_space *S;
+    const int64_t *cost;
+    int seq[ORC_MAX_STAGES], b[ORC_MAX_STAGES + 1];
+    type_rec *v;
+    int64_t len, cap;
+} type_recs;
+
+static void recs_parts(type_recs *x, int i)
+{
+    const type_space *S = x->S;
+    if (i == S->pp) {
+        type_rec r;
+        r.mx = 0;
+        r.sum = 0;
+        for (int j = 0; j < S->pp; j++) {
+            int hn = j + 1 < S->pp ? x->seq[j + 1] : S->T;
+            int64_t c = cost_at(S, x->cost, j, x->seq[j], hn, x->b[j], x->b[j + 1]);
+            if (c == ORC_INF) return;
+            r.c[j] = c;
+            r.sum += c;
+            if (c > r.mx) r.mx = c;
+        }
+        memcpy(r.seq, x->seq, sizeof(r.seq));
+        memcpy(r.b, x->b, sizeof(r.b));
+        if (x->len == x->cap) {
+            x->cap = x->cap ? 2 * x->cap : 256;
+            x->v = realloc(x->v, sizeof(type_rec) * (size_t)x->cap);
+        }
+        x->v[x->len++] = r;
+        return;
+    }
+    if (i == S->pp - 1) {
+        x->b[S->pp] = S->n;
+        if (x->b[i] < S->n) recs_parts(x, S->pp);
+        return;
+    }
+    for (int e = x->b[i] + 1; e <= S->n - (S->pp - 1 - i); e++) {
+        x->b[i + 1] = e;
+        recs_parts(x, i + 1);
+    }
+}
+
+static void recs_seq(type_recs *x, int i, int *left)
+{
+    if (i == x->S->pp) {
+        x->b[0] = 0;
+        recs_parts(x, 0);
+        return;
+    }
+    for (int h = 0; h < x->S->T; h++) {
+        if (left[h] == 0) continue;
+        left[h]--;
+        x->seq[i] = h;
+        recs_seq(x, i + 1, left);
+        left[h]++;
+    }
+}
+
+static int rec_key_less(const type_rec *p, const type_rec *q, int pp)
+{
+    for (int i = pp - 1; i >= 1; i--) {
+        if (p->b[i] != q->b[i]) return p->b[i] < q->b[i];
+        if (p->seq[i] != q->seq[i]) return p->seq[i] < q->seq[i];
+    }
+    return p->seq[0] < q->seq[0];
+}
+
+int32_t orc_brute_types_exact(int32_t pp, int32_t T, const int32_t *k, int32_t n, int64_t micro,
+                              const int64_t *cost, orc_result *r)
+{
+    type_space S;
+    type_space_init(&S, pp, T, k, n);
+    type_recs x;
+    memset(&x, 0, sizeof(x));
+    x.S = &S;
+    x.cost = cost;
+    int left[ORC_MAX_TYPES];
+    for (int h = 0; h < T; h++) left[h] = k[h];
+    recs_seq(&x, 0, left);
+    memset(r, 0, sizeof(*r));
+    r->pp = pp;
+    int64_t best = ORC_INF, best_mx = ORC_INF;
+    const type_rec *win = NULL;
+    for (int64_t i = 0; i < x.len; i++) {
+        const type_rec *a = &x.v[i];
+        int pareto = 1, first = 1;   /* first: the smallest key of its (max, sum) pair */
+        for (int64_t j = 0; j < x.len && pareto; j++) {
+            const type_rec *o = &x.v[j];
+            if (o->mx <= a->mx && o->sum <= a->sum && (o->mx < a->mx || o->sum < a->sum)) pareto = 0;
+            if (o->mx == a->mx && o->sum == a->sum && rec_key_less(o, a, pp)) first = 0;
+        }
+        if (!pareto || !first) continue;
+        r->thresholds++;
+        int64_t lat = orc_latency_1f1b(pp, a->c, micro);
+        if (lat < best || (lat == best && a->mx < best_mx)) {
+            best = lat;
+            best_mx = a->mx;
+            win = a;
+        }
+    }
+    if (!win) {
+        r->status = 1;
+        r->opt = r->sum = r->tmax = ORC_INF;
+    } else {
+        r->opt = best;
+        r->sum = win->sum;
+        r->tmax = win->mx;
+        for (int i = 0; i < pp; i++) {
+            r->layers[i] = (uint8_t)(win->b[i + 1] - win->b[i]);
+            r->stage_mask[i] = (uint8_t)(1 << win->seq[i]);
+        }
+    }
+    free(x.v);
+    return 0;
+}
+
 /* stage counts k_h of a configuration under free per-stage types */
 static void type_counts(const orc_problem *p, const orc_config *c, int32_t *k)
 {
@@ -1264,7 +1457,8 @@ int32_t orc_type_costs(const orc_problem *p, int64_t idx, int64_t *cost, uint8_t
     return 0;
 }
 
-static int32_t solve_types(const orc_problem *p, int64_t idx, orc_result *r, int brute)
+/* mode: 0 threshold DP, 1 its brute force, 2 1F1B re-scoring, 3 its brute force */
+static int32_t solve_types(const orc_problem *p, int64_t idx, orc_result *r, int mode)
 {
     orc_config c;
     int32_t order, micro;
@@ -1276,10 +1470,14 @@ static int32_t solve_types(const orc_problem *p, int64_t idx, orc_result *r, int
     int64_t *cost = malloc(sizeof(int64_t) * (size_t)ncost);
     uint8_t *rf = malloc((size_t)ncost);
     orc_type_costs(p, idx, cost, rf);
-    if (brute)
-        orc_brute_types(c.pp, T, k, p->n_layers, micro, cost, r);
-    else
+    if (mode == 0)
         orc_dp_types(c.pp, T, k, p->n_layers, micro, cost, r);
+    else if (mode == 1)
+        orc_brute_types(c.pp, T, k, p->n_layers, micro, cost, r);
+    else if (mode == 2)
+        orc_dp_types_exact(c.pp, T, k, p->n_layers, micro, cost, r);
+    else
+        orc_brute_types_exact(c.pp, T, k, p->n_layers, micro, cost, r);
     r->dp_const = orc_dp_const(p, &c, 0);
     if (r->status == 0) {
         r->opt += r->dp_const;
@@ -1300,10 +1498,7 @@ static int32_t solve_types(const orc_problem *p, int64_t idx, orc_result *r, int
 
 static int32_t solve_with(const orc_problem *p, int64_t idx, orc_result *r, int mode)
 {
-    if (p->stage_types == 2) {   /* the device-count DP (threshold objective only) */
-        if (mode > 1) return -1;
-        return solve_types(p, idx, r, mode == 1);
-    }
+    if (p->stage_types == 2) return solve_types(p, idx, r, mode);   /* the device-count DP */
     orc_config c;
     int32_t order, micro;
     if (orc_instance(p, idx, &c, &order, &micro)) return -1;

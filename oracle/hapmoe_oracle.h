@@ -170,5 +170,10 @@ int32_t orc_dp_types(int32_t pp, int32_t T, const int32_t *k, int32_t n, int64_t
                      orc_result *r);
 int32_t orc_brute_types(int32_t pp, int32_t T, const int32_t *k, int32_t n, int64_t micro, const int64_t *cost,
                         orc_result *r);
+/* ... and its 1F1B re-scoring of the (max, sum) frontier (as orc_dp_exact) */
+int32_t orc_dp_types_exact(int32_t pp, int32_t T, const int32_t *k, int32_t n, int64_t micro, const int64_t *cost,
+                           orc_result *r);
+int32_t orc_brute_types_exact(int32_t pp, int32_t T, const int32_t *k, int32_t n, int64_t micro,
+                              const int64_t *cost, orc_result *r);
 
 #endif

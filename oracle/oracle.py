@@ -130,7 +130,7 @@ def lib():
         L.orc_solve_exact_brute.argtypes = [P(OrcProblem), C.c_int64, P(OrcResult)]
         L.orc_solve_exact_many.argtypes = [P(OrcProblem), C.c_void_p, C.c_int64, P(OrcResult)]
         L.orc_type_costs.argtypes = [P(OrcProblem), C.c_int64, C.c_void_p, C.c_void_p]
-        for name in ("orc_dp_types", "orc_brute_types"):
+        for name in ("orc_dp_types", "orc_brute_types", "orc_dp_types_exact", "orc_brute_types_exact"):
             getattr(L, name).argtypes = [C.c_int32, C.c_int32, C.c_void_p, C.c_int32, C.c_int64, C.c_void_p,
                                          P(OrcResult)]
         _LIB = L
@@ -397,6 +397,16 @@ def brute_types(k, n, micro, cost):
     return _types_call("orc_brute_types", k, n, micro, cost)
 
 
+def dp_types_exact(k, n, micro, cost):
+    """1F1B re-scoring of the device-count DP's frontier on an explicit tensor."""
+    return _types_call("orc_dp_types_exact", k, n, micro, cost)
+
+
+def brute_types_exact(k, n, micro, cost):
+    """Brute force of the same objective over every sequence and composition."""
+    return _types_call("orc_brute_types_exact", k, n, micro, cost)
+
+
 def solve_worker(args):
     """multiprocessing helper: (problem, instance indices[, "exact"]) -> results."""
     problem, idx = args[0], args[1]
@@ -405,5 +415,6 @@ def solve_worker(args):
     return Oracle(problem).solve_many(idx)
 
 
-__all__ = ["Oracle", "dp", "brute", "dp_exact", "brute_exact", "dp_types", "brute_types", "latency_1f1b",
+__all__ = ["Oracle", "dp", "brute", "dp_exact", "brute_exact", "dp_types", "brute_types", "dp_types_exact",
+           "brute_types_exact", "latency_1f1b",
            "INF", "lib", "solve_worker"]

@@ -258,3 +258,63 @@ def test_count_dp_config2_against_sequences():
                 assert r2["status"] == 1
                 continue
             assert (r2["opt"], r2["tmax"]) == min((r["opt"], r["tmax"]) for r in rs), (ci, j)
+
+
+def test_count_dp_1f1b_core_matches_brute_force():
+    # the 1F1B re-scoring over the device-count frontier: the DP's frontier walk
+    # against every (sequence, composition), Pareto filter and canonical choice
+    rng = np.random.default_rng(5)
+    INF = np.iinfo(np.int64).max
+    checked = feasible = 0
+    while checked < 250:
+        T = int(rng.integers(1, 4))
+        k = [int(x) for x in rng.integers(0, 3, size=T)]
+        if sum(k) == 0:
+            k[0] = 1
+        pp = sum(k)
+        if pp > 5:
+            continue
+        n = int(rng.integers(pp, pp + 4))
+        cost = rng.integers(1, int(rng.choice([4, 30, 1000])), size=(pp, T, T + 1, n + 1, n + 1)).astype(np.int64)
+        cost[rng.random(cost.shape) < rng.uniform(0.0, 0.5)] = INF
+        B = int(rng.integers(1, 8))
+        a, b = orc.dp_types_exact(k, n, B, cost), orc.brute_types_exact(k, n, B, cost)
+        assert _key(a) + (a["thresholds"],) == _key(b) + (b["thresholds"],), (k, n, B, a, b)
+        checked += 1
+        feasible += a["status"] == 0
+    assert feasible > 100
+
+
+def test_count_dp_1f1b_problems():
+    # whole problems: brute force agrees in every field; the chosen plan's latency
+    # recomputed from the oracle's cost tensor; one device type is block mode
+    done = 0
+    for seed in range(900, 930):
+        p = count_dp(workloads.random_tiny(seed, n_types=2 + seed % 2))
+        o = orc.Oracle(p)
+        for i in range(o.n_instances()):
+            e, f = o.solve_exact(i), o.solve_exact_brute(i)
+            assert {x: e[x] for x in e if x != "thresholds"} == {x: f[x] for x in f if x != "thresholds"}
+            if e["status"] != 0:
+                continue
+            cost, _ = o.type_costs(i)
+            types = [m.bit_length() - 1 for m in e["stage_mask"]]
+            a, cs = 0, []
+            for s, n_i in enumerate(e["layers"]):
+                hn = types[s + 1] if s + 1 < len(types) else p["cluster"]["n_types"]
+                cs.append(int(cost[s, types[s], hn, a, a + n_i]))
+                a += n_i
+            B = p["space"]["micro"][i % len(p["space"]["micro"])]
+            assert e["opt"] == orc.latency_1f1b(cs, B) + e["dp_const"]
+            assert (e["sum"], e["tmax"]) == (sum(cs), max(cs))
+            done += 1
+    assert done > 30
+    for s in range(3):
+        p = workloads.random_tiny(300 + s, n_types=1)
+        ob, oc = orc.Oracle(p), orc.Oracle(count_dp(p))
+        for i in range(ob.n_instances()):
+            a, b = ob.solve_exact(i), oc.solve_exact(i)
+            if a["status"] == 0:
+                assert {x: a[x] for x in a if x != "thresholds"} == {x: b[x] for x in b if x != "thresholds"}
+            else:
+                assert b["status"] == 1
