@@ -193,6 +193,18 @@ def leg_free_types(torch, binding, workloads, dev, stream, steps, warmup, cpu_sa
                              "stage_types": plan["stage_types"], "layers": plan["layers"]}}
         if mode == 1:
             rec["sequences_per_config"] = int(binding.tables_layout(free)["n_orders"])
+        if mode == 2:   # the 1F1B re-scoring of the same DP (hapmoe_stage_dp_types_1f1b)
+            pf.stage_dp(objective="1f1b")
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(steps):
+                pf.stage_dp(objective="1f1b")
+            e1.record(stream)
+            plan_1f1b = pf.best_plan()
+            rec["objective_1f1b"] = {"stage_dp_ms": e0.elapsed_time(e1) / steps,
+                                     "best_objective_ns": plan_1f1b["objective"],
+                                     "stage_types": plan_1f1b["stage_types"], "layers": plan_1f1b["layers"]}
         if mode == 2 and n_config == 2 and cpu_sample:
             rec["cpu_baseline"], _ = cpu_baseline(free, pf.n, cpu_sample)
         out[f"{name}_config{n_config}"] = rec

@@ -310,6 +310,21 @@ int32_t hapmoe_stage_dp_types(const hapmoe_problem *p, const void *d_image,
                               hapmoe_dp_result *d_res, uint8_t *d_types, int32_t *d_stats,
                               void *d_ws, int64_t ws_bytes, void *stream);
 
+/* The device-count DP with the 1F1B latency of hapmoe_stage_dp_1f1b as the
+ * objective: the (max, sum) frontier of each candidate over every stage-type
+ * sequence and partition is walked (a threshold at which the least sum drops,
+ * with the canonical path there), each point is scored with
+ *   T = sum_i c_i + sum_{i <= s} ceil(c_i / 3) + max(0, B - s - 1) * max_i c_i,
+ * and the least T wins, ties to the lower largest stage.  Same arguments,
+ * outputs, workspace and errors as hapmoe_stage_dp_types (d_stats: passes of
+ * the walk).  Asynchronous. */
+int32_t hapmoe_stage_dp_types_1f1b(const hapmoe_problem *p, const void *d_image,
+                                   const hapmoe_candidate *d_cand, int64_t n_cand,
+                                   const void *d_tables, int64_t tables_bytes,
+                                   int64_t first, int64_t count,
+                                   hapmoe_dp_result *d_res, uint8_t *d_types, int32_t *d_stats,
+                                   void *d_ws, int64_t ws_bytes, void *stream);
+
 /* Workspace of hapmoe_best_plan for n results. */
 int32_t hapmoe_best_plan_ws_bytes(const hapmoe_problem *p, int64_t n, int64_t *bytes);
 

@@ -105,10 +105,11 @@ def lib():
         L.hapmoe_best_plan.argtypes = [P(Problem), vp, vp, i64, vp, vp, i64, vp, vp, i64, P(Plan), vp]
         L.hapmoe_stage_dp_types.argtypes = [P(Problem), vp, vp, i64, vp, i64, i64, i64, vp, vp, vp, vp, i64, vp]
         L.hapmoe_stage_dp_types_ws_bytes.argtypes = [P(Problem), P(i64)]
+        L.hapmoe_stage_dp_types_1f1b.argtypes = L.hapmoe_stage_dp_types.argtypes
         for f in ("hapmoe_validate", "hapmoe_enumerate_candidates", "hapmoe_image_bytes", "hapmoe_pack_image",
                   "hapmoe_tables_bytes", "hapmoe_debug_bytes", "hapmoe_tables_layout", "hapmoe_debug_layout", "hapmoe_eval_cost_tables", "hapmoe_stage_dp", "hapmoe_stage_dp_1f1b", "hapmoe_stage_dp_ws_bytes",
                   "hapmoe_best_plan_ws_bytes", "hapmoe_best_plan", "hapmoe_stage_dp_types",
-                  "hapmoe_stage_dp_types_ws_bytes"):
+                  "hapmoe_stage_dp_types_ws_bytes", "hapmoe_stage_dp_types_1f1b"):
             getattr(L, f).restype = C.c_int32
         _LIB = L
     return _LIB
@@ -316,6 +317,14 @@ def stage_dp_types(problem, d_image, d_cand, n_cand, d_tables, first, count, d_r
            "hapmoe_stage_dp_types")
 
 
+def stage_dp_types_1f1b(problem, d_image, d_cand, n_cand, d_tables, first, count, d_res, d_types, d_ws,
+                        d_stats=None, stream=None):
+    _check(lib().hapmoe_stage_dp_types_1f1b(_hp(problem).ref, _dptr(d_image), _dptr(d_cand), int(n_cand),
+                                            _dptr(d_tables), _nbytes(d_tables), int(first), int(count),
+                                            _dptr(d_res), _dptr(d_types), _dptr(d_stats), _dptr(d_ws),
+                                            _nbytes(d_ws), _stream(stream)), "hapmoe_stage_dp_types_1f1b")
+
+
 def best_plan(problem, d_cand, d_tables, d_res, n, d_ws, d_config_best=None, stream=None, d_types=None) -> dict:
     plan = Plan()
     _check(lib().hapmoe_best_plan(_hp(problem).ref, _dptr(d_cand), _dptr(d_tables), _nbytes(d_tables),
@@ -382,10 +391,9 @@ class Planner:
         res = self.d_res[first * RESULT_DTYPE.itemsize:]
         st = None if d_stats is None else d_stats[4 * first:]
         if self.device_count_dp:
-            if objective != "threshold":
-                raise ValueError("the device-count DP has the threshold objective only")
-            stage_dp_types(self.hp, self.d_image, self.d_cand, self.n, self.d_tables, first, count, res,
-                           self.d_types[first * MAX_STAGES:], self.d_dp_ws, st, stream)
+            call = stage_dp_types if objective == "threshold" else stage_dp_types_1f1b
+            call(self.hp, self.d_image, self.d_cand, self.n, self.d_tables, first, count, res,
+                 self.d_types[first * MAX_STAGES:], self.d_dp_ws, st, stream)
             return
         call = stage_dp if objective == "threshold" else stage_dp_1f1b
         call(self.hp, self.d_image, self.d_cand, self.n, self.d_tables, first, count, res, self.d_dp_ws, st, stream)

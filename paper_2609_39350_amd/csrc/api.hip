@@ -503,10 +503,12 @@ int32_t hapmoe_stage_dp_types_ws_bytes(const hapmoe_problem *p, int64_t *bytes)
     return HAPMOE_OK;
 }
 
-int32_t hapmoe_stage_dp_types(const hapmoe_problem *p, const void *d_image, const hapmoe_candidate *d_cand,
-                              int64_t n_cand, const void *d_tables, int64_t tables_bytes, int64_t first,
-                              int64_t count, hapmoe_dp_result *d_res, uint8_t *d_types, int32_t *d_stats,
-                              void *d_ws, int64_t ws_bytes, void *stream)
+namespace {
+
+int32_t stage_dp_types_any(const hapmoe_problem *p, const void *d_image, const hapmoe_candidate *d_cand,
+                           int64_t n_cand, const void *d_tables, int64_t tables_bytes, int64_t first, int64_t count,
+                           hapmoe_dp_result *d_res, uint8_t *d_types, int32_t *d_stats, void *d_ws,
+                           int64_t ws_bytes, void *stream, bool exact)
 {
     if (const int32_t e = check_problem(p)) return e;
     if (p->space.stage_types != 2 || !d_image || !d_cand || !d_tables || !d_res || !d_types || !d_ws)
@@ -523,9 +525,30 @@ int32_t hapmoe_stage_dp_types(const hapmoe_problem *p, const void *d_image, cons
     if (const int e = check_arch()) return e;
     if (count == 0) return HAPMOE_OK;
     if (launch_type_dp(d_image, d_cand, p->model.n_layers, p->cluster.n_types, p->space.n_micro, S.umax, L,
-                       d_tables, first, count, d_res, d_types, d_stats, d_ws, (hipStream_t)stream) != hipSuccess)
+                       d_tables, first, count, d_res, d_types, d_stats, d_ws, exact,
+                       (hipStream_t)stream) != hipSuccess)
         return HAPMOE_E_HIP;
     return HAPMOE_OK;
+}
+
+}  // namespace
+
+int32_t hapmoe_stage_dp_types(const hapmoe_problem *p, const void *d_image, const hapmoe_candidate *d_cand,
+                              int64_t n_cand, const void *d_tables, int64_t tables_bytes, int64_t first,
+                              int64_t count, hapmoe_dp_result *d_res, uint8_t *d_types, int32_t *d_stats,
+                              void *d_ws, int64_t ws_bytes, void *stream)
+{
+    return stage_dp_types_any(p, d_image, d_cand, n_cand, d_tables, tables_bytes, first, count, d_res, d_types,
+                              d_stats, d_ws, ws_bytes, stream, false);
+}
+
+int32_t hapmoe_stage_dp_types_1f1b(const hapmoe_problem *p, const void *d_image, const hapmoe_candidate *d_cand,
+                                   int64_t n_cand, const void *d_tables, int64_t tables_bytes, int64_t first,
+                                   int64_t count, hapmoe_dp_result *d_res, uint8_t *d_types, int32_t *d_stats,
+                                   void *d_ws, int64_t ws_bytes, void *stream)
+{
+    return stage_dp_types_any(p, d_image, d_cand, n_cand, d_tables, tables_bytes, first, count, d_res, d_types,
+                              d_stats, d_ws, ws_bytes, stream, true);
 }
 
 int32_t hapmoe_best_plan_ws_bytes(const hapmoe_problem *p, int64_t n, int64_t *bytes)

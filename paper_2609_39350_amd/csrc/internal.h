@@ -138,7 +138,7 @@ int64_t type_dp_ws_bytes(int n_layers, int n_types, int umax, int64_t n_configs)
 hipError_t launch_type_dp(const void *d_image, const hapmoe_candidate *d_cand, int n_layers, int n_types,
                           int n_micro, int umax, const TablesLayout &L, const void *d_tables, int64_t first,
                           int64_t count, hapmoe_dp_result *d_res, uint8_t *d_types, int32_t *d_stats, void *d_ws,
-                          hipStream_t s);
+                          bool exact, hipStream_t s);
 // bytes of the winner record in the best-plan workspace (result, candidate, stage layout)
 constexpr int64_t kWinnerBytes = 256;
 static_assert(sizeof(hapmoe_dp_result) + sizeof(hapmoe_candidate) + sizeof(KeyInfo) <= kWinnerBytes, "winner");

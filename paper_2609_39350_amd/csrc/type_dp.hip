@@ -42,8 +42,9 @@ constexpr int64_t kNone = INT64_MAX;   // no path
 
 struct TypePath {   // result of one pass, filled by thread 0
     int64_t F, M;
+    int64_t fwd;        // forward time (ceil(c/3)) of the stages up to the first largest one
+    int32_t s1;         // that stage, 1-based
     uint32_t rmask;
-    int32_t pad;
     uint8_t layers[kMaxStages];
     uint8_t types[kMaxStages];
 };
@@ -114,7 +115,7 @@ __device__ inline int64_t stage_cost(const StageData &D, int h, int a, int b, in
     return kNone;
 }
 
-template <bool STATS>
+template <bool STATS, bool EXACT>
 __global__ __launch_bounds__(kThreads) void k_type_dp(const unsigned char *__restrict__ img,
                                                       const hapmoe_candidate *__restrict__ cand, TablesLayout L,
                                                       const unsigned char *__restrict__ tab, int64_t first,
@@ -139,6 +140,7 @@ __global__ __launch_bounds__(kThreads) void k_type_dp(const unsigned char *__res
     uint64_t *ulist = reinterpret_cast<uint64_t *>(smem + S.off_ulist);
     TypeInc *inc = reinterpret_cast<TypeInc *>(smem + S.off_inc);
     TypePath &P = *reinterpret_cast<TypePath *>(smem + S.off_path);
+    TypePath &Q = *(reinterpret_cast<TypePath *>(smem + S.off_path) + 1);   // 1F1B: the pending frontier point
     TypeCtl &C = *reinterpret_cast<TypeCtl *>(smem + S.off_ctl);
     const StageData D{sT0, sT1, sMW, sMA0, sMA1, sMOE, W};
 
@@ -322,8 +324,11 @@ __global__ __launch_bounds__(kThreads) void k_type_dp(const unsigned char *__res
                 P.F = fe;
                 P.M = 0;
                 P.rmask = 0;
+                P.fwd = 0;
+                P.s1 = 0;
                 if (fe != kNone) {
                     int u = U - 1, b = N, hn = T;
+                    int64_t fsum = 0, fafter = 0;   // forward times: all stages, those after the first largest
                     for (int i = PP - 1; i >= 0; --i) {
                         const int x = ARG[((int64_t)u * W + b) * T1 + hn];
                         const int a = x >> 3, h = x & 7;
@@ -331,7 +336,12 @@ __global__ __launch_bounds__(kThreads) void k_type_dp(const unsigned char *__res
                         const int64_t pc = hn < T ? pi->p2p[h * kMaxTypes + hn] : 0;
                         int r = 0;
                         const int64_t c = stage_cost(D, h, a, b, msi, H.mem_bytes[h], X, recomp, pc, &r);
-                        P.M = c > P.M ? c : P.M;
+                        if (c >= P.M) {   // ">=": going down, the smaller stage index wins ties
+                            P.M = c;
+                            P.s1 = i + 1;
+                            fafter = fsum;
+                        }
+                        fsum += (c + 2) / 3;
                         P.layers[i] = (uint8_t)(b - a);
                         P.types[i] = (uint8_t)h;
                         P.rmask |= (uint32_t)r << i;
@@ -339,6 +349,7 @@ __global__ __launch_bounds__(kThreads) void k_type_dp(const unsigned char *__res
                         b = a;
                         hn = h;
                     }
+                    P.fwd = fsum - fafter;
                 }
             }
             __syncthreads();
@@ -356,6 +367,25 @@ __global__ __launch_bounds__(kThreads) void k_type_dp(const unsigned char *__res
                 for (int i = 0; i < kMaxStages; ++i) {
                     I.layers[i] = i < PP ? P.layers[i] : 0;
                     I.types[i] = i < PP ? P.types[i] : 0;
+                }
+            }
+        };
+
+        // 1F1B: thread j scores a frontier point for microbatch count j (least
+        // latency, ties to the lower largest stage)
+        auto take_exact = [&](int j, const TypePath &R) {
+            const int64_t B = H.micro[j];
+            const int64_t steady = B - R.s1 - 1 > 0 ? B - R.s1 - 1 : 0;
+            const int64_t obj = R.F + R.fwd + steady * R.M;
+            TypeInc &I = inc[j];
+            if (obj < I.obj || (obj == I.obj && R.M < I.M)) {
+                I.obj = obj;
+                I.M = R.M;
+                I.F = R.F;
+                I.rmask = R.rmask;
+                for (int i = 0; i < kMaxStages; ++i) {
+                    I.layers[i] = i < PP ? R.layers[i] : 0;
+                    I.types[i] = i < PP ? R.types[i] : 0;
                 }
             }
         };
@@ -378,7 +408,7 @@ __global__ __launch_bounds__(kThreads) void k_type_dp(const unsigned char *__res
             if (tid == 0) C.relax = 0;
             __syncthreads();
             int passes = 0;
-            if (shape_ok) {
+            if (shape_ok && !EXACT) {
                 pass(kNone, v);
                 ++passes;
                 if (P.F != kNone) {
@@ -415,6 +445,43 @@ __global__ __launch_bounds__(kThreads) void k_type_dp(const unsigned char *__res
                         }
                         __syncthreads();
                     }
+                }
+            }
+            if (shape_ok && EXACT) {
+                // walk the (max, sum) frontier downwards: the pending point Q is a
+                // frontier point once a pass at its max - 1 has a larger sum, and is
+                // dropped if the sum is the same (a lower max reaches it)
+                pass(kNone, v);
+                ++passes;
+                if (P.F != kNone) {
+                    if (tid == 0) {
+                        Q = P;
+                        C.t = P.M - 1;
+                    }
+                    __syncthreads();
+                    for (;;) {
+                        if (tid == 0) {
+                            // every later point has latency >= its sum >= Q.F: stop once no
+                            // incumbent can be reached (Q itself included)
+                            bool need = false;
+                            for (int j = 0; j < nB; ++j)
+                                if (member(j)) need = need || !(inc[j].obj < Q.F);
+                            C.go = C.t >= 0 && need;
+                        }
+                        __syncthreads();
+                        if (!C.go) break;
+                        pass(C.t, v);
+                        ++passes;
+                        if (P.F == kNone) break;
+                        if (P.F > Q.F && tid < nB && member(tid)) take_exact(tid, Q);
+                        __syncthreads();
+                        if (tid == 0) {
+                            Q = P;
+                            C.t = P.M - 1;
+                        }
+                        __syncthreads();
+                    }
+                    if (tid < nB && member(tid)) take_exact(tid, Q);   // the last point
                 }
             }
             __syncthreads();
@@ -474,7 +541,7 @@ TypeLds type_dp_lds(int n_layers, int n_types, int n_micro, int umax)
     S.off_mw = take((int64_t)3 * W * 8);
     S.off_moe = take((int64_t)W * 4);
     S.off_inc = take((int64_t)n_micro * sizeof(TypeInc));
-    S.off_path = take(sizeof(TypePath));
+    S.off_path = take(2 * sizeof(TypePath));
     S.off_ctl = take(sizeof(TypeCtl));
     S.off_ulist = take((int64_t)umax * 8);
     S.bytes = (int)off;
@@ -498,7 +565,7 @@ int64_t type_dp_slots(int64_t n_keys, int64_t slot_bytes)
 hipError_t launch_type_dp(const void *d_image, const hapmoe_candidate *d_cand, int n_layers, int n_types,
                           int n_micro, int umax, const TablesLayout &L, const void *d_tables, int64_t first,
                           int64_t count, hapmoe_dp_result *d_res, uint8_t *d_types, int32_t *d_stats, void *d_ws,
-                          hipStream_t s)
+                          bool exact, hipStream_t s)
 {
     const int64_t key_lo = first / n_micro, key_hi = (first + count - 1) / n_micro;
     const int64_t n_keys = key_hi - key_lo + 1;
@@ -511,12 +578,19 @@ hipError_t launch_type_dp(const void *d_image, const hapmoe_candidate *d_cand, i
     hipLaunchKernelGGL(k_reset_type_queue, dim3(1), dim3(1), 0, s, queue);
     const auto *img = static_cast<const unsigned char *>(d_image);
     const auto *tab = static_cast<const unsigned char *>(d_tables);
-    if (d_stats)
-        hipLaunchKernelGGL(k_type_dp<true>, dim3((unsigned)grid), dim3(kThreads), S.bytes, s, img, d_cand, L, tab,
-                           first, count, key_lo, n_keys, S, slot_base, slot_bytes, d_res, d_types, d_stats, queue);
+    const dim3 grid3((unsigned)grid), block(kThreads);
+#define HAPMOE_TYPE_DP(ST, EX)                                                                                 \
+    hipLaunchKernelGGL((k_type_dp<ST, EX>), grid3, block, S.bytes, s, img, d_cand, L, tab, first, count, key_lo, \
+                       n_keys, S, slot_base, slot_bytes, d_res, d_types, d_stats, queue)
+    if (d_stats && exact)
+        HAPMOE_TYPE_DP(true, true);
+    else if (d_stats)
+        HAPMOE_TYPE_DP(true, false);
+    else if (exact)
+        HAPMOE_TYPE_DP(false, true);
     else
-        hipLaunchKernelGGL(k_type_dp<false>, dim3((unsigned)grid), dim3(kThreads), S.bytes, s, img, d_cand, L, tab,
-                           first, count, key_lo, n_keys, S, slot_base, slot_bytes, d_res, d_types, d_stats, queue);
+        HAPMOE_TYPE_DP(false, false);
+#undef HAPMOE_TYPE_DP
     return hipGetLastError();
 }
 

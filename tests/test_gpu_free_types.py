@@ -88,12 +88,12 @@ def count_dp(p):
     return variant(p, **{"space.stage_types": 2})
 
 
-def compare_types(problem, pl, idx, slow=False):
+def compare_types(problem, pl, idx, slow=False, objective="threshold"):
     """Every field of compare() plus the stage types the DP chose (slow: the
     oracle takes seconds per candidate, so it runs in worker processes)."""
     from tests.test_gpu_parity import oracle_many
-    ref = oracle_many(problem, idx, pool=True if slow else None)
-    compare(problem, pl, idx, ref=ref)
+    ref = oracle_many(problem, idx, objective, pool=True if slow else None)
+    compare(problem, pl, idx, ref=ref, objective=objective)
     ty = pl.stage_types()
     for i, r in zip(idx, ref):
         got = [int(x) for x in ty[i]]
@@ -208,3 +208,30 @@ def test_count_dp_subranges_match(torch):
     pl.stage_dp(stats=True)
     st = pl.stats()
     assert (st[:, 0] >= 1).all() and st[:, 1].sum() > 0
+
+
+@pytest.mark.parametrize("n,stride", [(1, 1), (2, 5)])
+def test_count_dp_1f1b(torch, n, stride):
+    p = count_dp(workloads.config(n))
+    print(f"device-count DP, 1F1B, config {n}: stride {stride}", flush=True)
+    pl = binding.Planner(p, "cuda:0")
+    plan = pl.run(objective="1f1b")
+    idx = sorted(set(list(range(0, pl.n, stride)) + [pl.n - 1, plan["instance"]]))
+    compare_types(p, pl, idx, slow=True, objective="1f1b")
+    res = pl.results()
+    obj = np.where(res["status"] == 0, res["objective"], np.iinfo(np.int64).max)
+    assert plan["instance"] == int(np.argmin(obj))
+
+
+def test_count_dp_1f1b_random_tiny(torch):
+    done = 0
+    for s in range(40):
+        p = count_dp(workloads.random_tiny(900 + s, n_types=2 + s % 2))
+        if orc.Oracle(p).n_instances() == 0:
+            continue
+        done += 1
+        pl = binding.Planner(p, "cuda:0")
+        pl.eval_cost_tables()
+        pl.stage_dp(objective="1f1b")
+        compare_types(p, pl, range(pl.n), objective="1f1b")
+    assert done >= 10
