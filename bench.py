@@ -243,6 +243,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-1f1b", action="store_true", help="skip the 1F1B re-scoring leg")
     ap.add_argument("--no-free-types", action="store_true", help="skip the free per-stage device-type legs")
+    ap.add_argument("--section-clocks", action="store_true",
+                    help="diagnostic build: report where the stage-DP kernel's cycles go (slightly slower kernel)")
     ap.add_argument("--cpu-sample-free", type=int, default=40)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (counter scaling for HBM traffic)")
@@ -258,6 +260,8 @@ def main():
 
     from paper_2609_39350_amd import binding, workloads
 
+    if args.section_clocks:
+        binding.use_section_clocks()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     problem = workloads.config(args.config)
@@ -280,6 +284,8 @@ def main():
     for _ in range(args.warmup):
         pl.run()
     torch.cuda.synchronize()
+    if args.section_clocks:
+        binding.section_clocks(clear=True)
 
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     t0 = time.perf_counter()
@@ -299,6 +305,7 @@ def main():
     ms = {name: float(np.mean([ev[k][j].elapsed_time(ev[k][j + 1]) for k in range(args.steps)]))
           for j, name in enumerate(("cost_tables", "stage_dp", "best_plan"))}
 
+    clocks = binding.section_clocks(clear=True) if args.section_clocks else None
     dp_s = ms["stage_dp"] / 1e3
     achieved = (relax * OPS_PER_RELAXATION + evals * OPS_PER_EVALUATION) / dp_s
     out = {
@@ -330,6 +337,9 @@ def main():
                       "config": plan["config"], "order": plan["order"], "B": plan["n_micro"],
                       "layers": plan["layers"], "recompute": plan["recompute"]},
     }
+    if clocks is not None:
+        clocks["steps"] = args.steps
+        out["stage_dp_section_clocks"] = clocks
     out["ablation_uniform_layers"] = leg_uniform(binding, problem, pl, dev)
     if not args.no_1f1b:
         out["objective_1f1b"] = leg_1f1b(torch, pl, stream, args.steps, args.warmup)

@@ -175,6 +175,15 @@ typedef struct hapmoe_plan {
     uint8_t stage_types[HAPMOE_MAX_STAGES]; /* bit h set = stage uses device type h */
 } hapmoe_plan;
 
+/* Diagnostics: where the stage-DP kernel's time goes.  Only a library built
+ * with HAPMOE_SECTION_CLOCKS defined records it (HAPMOE_E_INVAL otherwise).
+ * out[0..4] = shader-clock cycles summed over all waves of the launches since
+ * the last clear, spent in key set-up and classification, feasibility scans,
+ * the relaxation rounds of the passes, the back-traces, and the sweep control;
+ * out[5] = the waves' total cycles; out[6..8] = keys, segment batches and
+ * passes.  clear != 0 zeroes the table after reading. */
+int32_t hapmoe_section_clocks(uint64_t out[16], int32_t clear);
+
 /* Name of a status code (static string). */
 const char *hapmoe_strerror(int32_t code);
 

@@ -106,6 +106,8 @@ def lib():
         L.hapmoe_stage_dp_types.argtypes = [P(Problem), vp, vp, i64, vp, i64, i64, i64, vp, vp, vp, vp, i64, vp]
         L.hapmoe_stage_dp_types_ws_bytes.argtypes = [P(Problem), P(i64)]
         L.hapmoe_stage_dp_types_1f1b.argtypes = L.hapmoe_stage_dp_types.argtypes
+        L.hapmoe_section_clocks.argtypes = [P(C.c_uint64), C.c_int32]
+        L.hapmoe_section_clocks.restype = C.c_int32
         for f in ("hapmoe_validate", "hapmoe_enumerate_candidates", "hapmoe_image_bytes", "hapmoe_pack_image",
                   "hapmoe_tables_bytes", "hapmoe_debug_bytes", "hapmoe_tables_layout", "hapmoe_debug_layout", "hapmoe_eval_cost_tables", "hapmoe_stage_dp", "hapmoe_stage_dp_1f1b", "hapmoe_stage_dp_ws_bytes",
                   "hapmoe_best_plan_ws_bytes", "hapmoe_best_plan", "hapmoe_stage_dp_types",
@@ -175,6 +177,28 @@ class HostProblem:
             p.space.micro[i] = int(b)
         self.c = p
         self.ref = C.byref(p)
+
+
+def use_section_clocks():
+    """Load the diagnostic build (libhapmoe_clocks.so) instead of the library;
+    call before anything else touches the binding."""
+    global LIB_PATH
+    if _LIB is not None:
+        raise RuntimeError("the library is already loaded")
+    LIB_PATH = os.path.join(os.path.dirname(LIB_PATH), "libhapmoe_clocks.so")
+
+
+SECTION_NAMES = ("setup", "scan", "relax", "trace", "control")
+
+
+def section_clocks(clear=True) -> dict:
+    """Stage-DP section clocks since the last clear (diagnostic build only)."""
+    out = (C.c_uint64 * 16)()
+    _check(lib().hapmoe_section_clocks(out, 1 if clear else 0), "hapmoe_section_clocks")
+    v = list(out)
+    total = max(v[5], 1)
+    return {"share": {n: v[i] / total for i, n in enumerate(SECTION_NAMES)}, "wave_cycles": v[5],
+            "keys": v[6], "segment_batches": v[7], "passes": v[8]}
 
 
 def _hp(problem):

@@ -15,20 +15,28 @@ FLAGS = [
 ]
 
 
-def build(force=True, verbose=False):
-    """Compile every HIP source of the library; returns the .so path."""
-    if not force and os.path.exists(LIB):
-        return LIB
+CLOCKS_LIB = os.path.join(PKG, "libhapmoe_clocks.so")
+
+
+def build(force=True, verbose=False, section_clocks=False):
+    """Compile every HIP source of the library; returns the .so path.
+    section_clocks: the diagnostic variant (libhapmoe_clocks.so) whose stage-DP
+    kernel records where its time goes (hapmoe_section_clocks)."""
+    lib = CLOCKS_LIB if section_clocks else LIB
+    if not force and os.path.exists(lib):
+        return lib
     srcs = [os.path.join(PKG, "csrc", s) for s in SOURCES]
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, *FLAGS, "-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG, "csrc"),
+    tmp = lib + ".tmp"
+    extra = ["-DHAPMOE_SECTION_CLOCKS"] if section_clocks else []
+    cmd = [HIPCC, *FLAGS, *extra, "-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG, "csrc"),
            "-o", tmp, *srcs]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":
-    print(build(verbose=True))
+    import sys
+    print(build(verbose=True, section_clocks="--section-clocks" in sys.argv))

@@ -242,6 +242,14 @@ int64_t per_config(const hapmoe_problem *p, const Space &S)
 
 extern "C" {
 
+int32_t hapmoe_section_clocks(uint64_t out[16], int32_t clear)
+{
+    if (!out) return HAPMOE_E_INVAL;
+    for (int i = 0; i < 16; ++i) out[i] = 0;
+    static_assert(kSectionClocks <= 16, "section table");
+    return stage_dp_section_clocks(out, clear != 0);
+}
+
 const char *hapmoe_strerror(int32_t code)
 {
     switch (code) {

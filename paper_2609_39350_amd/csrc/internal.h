@@ -121,6 +121,12 @@ hipError_t launch_stage_dp(const void *d_image, const hapmoe_candidate *d_cand, 
                            hapmoe_dp_result *d_res, int32_t *d_stats, void *d_ws, const int32_t *micro,
                            bool exact, hipStream_t s);
 int64_t stage_dp_ws_bytes();
+// section clocks of the stage-DP kernel (libraries built with HAPMOE_SECTION_CLOCKS)
+enum {
+    kClockSetup, kClockScan, kClockRelax, kClockTrace, kClockControl, kClockTotal,
+    kCountKeys, kCountBatches, kCountPasses, kSectionClocks
+};
+int32_t stage_dp_section_clocks(uint64_t *out, bool clear);
 
 // Device-count DP (free per-stage device types by the DP state of device counts).
 constexpr int kMaxTypeStates = 4096;                        // states u = prod_h (k_h + 1) per pipeline

@@ -53,6 +53,39 @@ constexpr int64_t kNegInf = INT64_MIN;        // a threshold no stage cost meets
 constexpr int kRelaxUnroll = 2;   // split points per relaxation-loop trip
 constexpr int kMaxSeg = 4;
 
+// Optional section clocks (built with -DHAPMOE_SECTION_CLOCKS into a separate
+// library): every wave accumulates the shader-clock cycles it spends in each
+// part of the kernel and adds them to a device-wide table when it exits.
+// Sections: key set-up and classification, feasibility scan, the relaxation
+// rounds of the passes, the back-traces, and the sweep control in between.
+#ifdef HAPMOE_SECTION_CLOCKS
+__device__ unsigned long long g_section_clocks[kSectionClocks];
+#define HAPMOE_CLOCK_VARS                                                           \
+    unsigned long long clk_acc[kSectionClocks] = {};                                \
+    const unsigned long long clk_start = clock64();                                 \
+    unsigned long long clk_last = clk_start
+#define HAPMOE_CLOCK(sec)                                                           \
+    do {                                                                            \
+        const unsigned long long clk_now = clock64();                               \
+        clk_acc[sec] += clk_now - clk_last;                                         \
+        clk_last = clk_now;                                                         \
+    } while (0)
+#define HAPMOE_CLOCK_RESTART() (clk_last = clock64())
+#define HAPMOE_COUNT(sec) (++clk_acc[sec])
+#define HAPMOE_CLOCK_FLUSH(lane)                                                    \
+    do {                                                                            \
+        clk_acc[kClockTotal] = clock64() - clk_start;                               \
+        if ((lane) == 0)                                                            \
+            for (int i_ = 0; i_ < kSectionClocks; ++i_) atomicAdd(&g_section_clocks[i_], clk_acc[i_]); \
+    } while (0)
+#else
+#define HAPMOE_CLOCK_VARS
+#define HAPMOE_CLOCK(sec)
+#define HAPMOE_CLOCK_RESTART()
+#define HAPMOE_COUNT(sec)
+#define HAPMOE_CLOCK_FLUSH(lane)
+#endif
+
 // LDS of one wave: TM [kmax][np] {T0, T1} | memory prefixes | per-segment
 // region | control.  The per-segment region holds, for each active segment:
 // AMIN, A0B, ARG [sum of band widths] bytes and two DP rows [max band width].
@@ -322,7 +355,9 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
     unsigned char *REG = smem + S.off_region;
     SegCtl *CTL = reinterpret_cast<SegCtl *>(smem + S.off_ctl);
 
+    HAPMOE_CLOCK_VARS;
     for (;;) {
+        HAPMOE_CLOCK_RESTART();
         uint32_t qi = 0;
         if (lane == 0) qi = atomicAdd(queue, 1u);
         qi = __shfl(qi, 0, 64);
@@ -498,7 +533,10 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
         const int ng = __popcll(bnd);   // classes
         const int gj = __popcll(bnd & ((uint64_t(2) << vj) - 1)) - 1;   // this lane's class
 
+        HAPMOE_CLOCK(kClockSetup);
+        HAPMOE_COUNT(kCountKeys);
         for (int g0 = 0; g0 < ng; g0 += smax) {
+            HAPMOE_COUNT(kCountBatches);
             const int nact = (ng - g0) < smax ? (ng - g0) : smax;
             const int nseg = nact <= 1 ? 1 : (nact <= 2 ? 2 : 4);
             const int W = 64 / nseg;
@@ -611,6 +649,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
             }
             wave_sync();
 
+            HAPMOE_CLOCK(kClockScan);
             int passes = 0;
             int relq[kMaxSeg] = {0, 0, 0, 0}, slq[kMaxSeg] = {0, 0, 0, 0};   // per segment (stats)
 
@@ -620,6 +659,8 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
             // stage M into the segment's control block.  The fused pass (t = inf)
             // also carries the min-max row: G = least possible largest stage.
             auto pass = [&](bool fused) {
+                HAPMOE_CLOCK(kClockControl);
+                HAPMOE_COUNT(kCountPasses);
                 const bool on = seg_live && CTL[sg].on != 0;
                 if (on) ++passes;
                 if (on && ll == 0) {   // stage -1: layer 0 reached at cost 0
@@ -733,6 +774,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                     }
                     wave_sync();
                 }
+                HAPMOE_CLOCK(kClockRelax);
                 const bool odd = ((PP - 1) & 1) != 0;
                 const int64_t fin = fused ? (odd ? FG1[0].x : FG0[0].x) : (odd ? FM1[0] : FM0[0]);
                 const bool tracer = on && ll == 0;
@@ -800,6 +842,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                     }
                 }
                 wave_sync();
+                HAPMOE_CLOCK(kClockTrace);
             };
 
             // per-segment control, written by lane 0 from wave-uniform values
@@ -1029,9 +1072,28 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
             wave_sync();
         }
     }
+    HAPMOE_CLOCK(kClockControl);
+    HAPMOE_CLOCK_FLUSH(lane);
 }
 
 }  // namespace
+
+int32_t stage_dp_section_clocks(uint64_t *out, bool clear)
+{
+#ifdef HAPMOE_SECTION_CLOCKS
+    if (hipMemcpyFromSymbol(out, HIP_SYMBOL(g_section_clocks), sizeof(uint64_t) * kSectionClocks) != hipSuccess)
+        return HAPMOE_E_HIP;
+    if (clear) {
+        const uint64_t z[kSectionClocks] = {};
+        if (hipMemcpyToSymbol(HIP_SYMBOL(g_section_clocks), z, sizeof(z)) != hipSuccess) return HAPMOE_E_HIP;
+    }
+    return HAPMOE_OK;
+#else
+    (void)out;
+    (void)clear;
+    return HAPMOE_E_INVAL;   // built without the section clocks
+#endif
+}
 
 int64_t stage_dp_ws_bytes() { return 256; }
 
