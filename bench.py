@@ -137,10 +137,20 @@ def leg_1f1b(torch, pl, stream, steps, warmup):
     dp_ms = float(np.mean([ev[k][0].elapsed_time(ev[k][1]) for k in range(steps)]))
     return {"value": pl.n * steps / elapsed, "unit": "candidates/s", "ms_per_step": elapsed * 1e3 / steps,
             "stage_dp_ms": dp_ms, "relaxations_per_launch": relax,
+            "roofline": alu_roofline(relax, int(st[:, 2].astype(np.int64).sum()), dp_ms, "stage_dp (1F1B)"),
             "dp_passes_per_candidate": {"mean": float(st[:, 0].mean()), "max": int(st[:, 0].max())},
             "best_plan": {"instance": plan["instance"], "objective_ns": plan["objective"],
                           "config": plan["config"], "order": plan["order"], "B": plan["n_micro"],
                           "layers": plan["layers"]}}
+
+
+def alu_roofline(relaxations, evaluations, ms, kernel):
+    """VALU roofline of one stage-DP launch from its algorithmic operation count."""
+    ops = relaxations * OPS_PER_RELAXATION + evaluations * OPS_PER_EVALUATION
+    achieved = ops / (ms / 1e3) if ms > 0 else 0.0
+    return {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK_OPS / 1e12, "unit": "TOP/s",
+            "frac": achieved / VALU_PEAK_OPS, "kernel": kernel, "relaxations_per_launch": relaxations,
+            "evaluations_per_launch": evaluations}
 
 
 def _timed_steps(torch, pl, stream, steps, warmup):
@@ -187,6 +197,8 @@ def leg_free_types(torch, binding, workloads, dev, stream, steps, warmup, cpu_sa
                "feasible_candidates": int((res["status"] == 0).sum()),
                "dp_passes_per_candidate": {"mean": float(st[:, 0].mean()), "max": int(st[:, 0].max())},
                "relaxations_per_launch": int(st[:, 1].astype(np.int64).sum()),
+               "roofline": alu_roofline(int(st[:, 1].astype(np.int64).sum()), int(st[:, 2].astype(np.int64).sum()),
+                                        dp_ms, "stage_dp" if mode == 1 else "type_dp"),
                "best_objective_ns": plan["objective"], "block_orderings_best_ns": block_best,
                "gain_over_block_orderings": 1.0 - plan["objective"] / block_best,
                "best_plan": {"config": plan["config"], "order": plan["order"], "B": plan["n_micro"],
