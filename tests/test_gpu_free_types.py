@@ -235,3 +235,19 @@ def test_count_dp_1f1b_random_tiny(torch):
         pl.stage_dp(objective="1f1b")
         compare_types(p, pl, range(pl.n), objective="1f1b")
     assert done >= 10
+
+
+@pytest.mark.parametrize("flags", [{"params.prune_window": 0}, {"params.prune_window": 2},
+                                   {"params.allow_recompute": 0, "params.prune_hetero": 0},
+                                   {"space.micro": [1, 2, 3, 5, 8, 13]}])
+def test_count_dp_flag_variants(torch, flags):
+    # no windows (every end layer in the band), uniform windows, no recomputation
+    # and no pruning 3, and B below PP (several groups of min(B, PP)): a stride
+    # sample of configuration 2 against the oracle
+    p = variant(count_dp(workloads.config(2)), **flags)
+    print(f"device-count DP, config 2, {flags}", flush=True)
+    pl = binding.Planner(p, "cuda:0")
+    pl.eval_cost_tables()
+    pl.stage_dp()
+    idx = sorted(set(list(range(0, pl.n, 13)) + [pl.n - 1]))
+    compare_types(p, pl, idx, slow=True)
