@@ -339,8 +339,20 @@ def test_config4_full_launch_sampled(torch):
     assert all((res["layers"][ok][:, :] > 0).sum(axis=1) == pp[ok])
     obj = np.where(ok, res["objective"], np.iinfo(np.int64).max)
     assert plan["instance"] == int(np.argmin(obj))
-    idx = list(range(11, pl.n, 25013)) + [plan["instance"]]
+    # a stride sample (every pipeline depth, ordering and B) plus the first and
+    # last candidate of each depth and the winner
+    idx = list(range(11, pl.n, 397)) + [plan["instance"]]
+    for d in np.unique(pp):
+        at = np.nonzero(pp == d)[0]
+        idx += [int(at[0]), int(at[-1])]
     compare(p, pl, sorted(set(idx)), res)
+    # the per-configuration minima agree with the results
+    per = pl.n // pl.n_configs
+    cb = pl.config_best()
+    seg = obj.reshape(pl.n_configs, per)
+    exp = np.where(seg.min(axis=1) == np.iinfo(np.int64).max, -1,
+                   np.arange(pl.n_configs) * per + seg.argmin(axis=1))
+    assert (cb == exp).all()
 
 
 # ------------------------------------------------- 1F1B re-scoring objective
