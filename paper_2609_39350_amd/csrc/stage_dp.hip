@@ -52,6 +52,7 @@ constexpr int64_t kBig = int64_t(1) << 62;   // "no partition" inside the DP (su
 constexpr int64_t kNegInf = INT64_MIN;        // a threshold no stage cost meets
 constexpr int kRelaxUnroll = 2;   // split points per relaxation-loop trip
 constexpr int kMaxSeg = 4;
+constexpr int kParallelTrace = 4;    // pipelines at least this deep back-trace in two phases
 
 // Optional section clocks (built with -DHAPMOE_SECTION_CLOCKS into a separate
 // library): every wave accumulates the shader-clock cycles it spends in each
@@ -104,6 +105,7 @@ struct SegCtl {
     int32_t on;       // the segment takes part in the next pass
     int32_t pad;
     uint32_t bt[8];   // back-trace: n_i bytes
+    uint32_t sb[8];   // back-trace of deep pipelines: first layer of each stage
     uint32_t rmask, ok;
     // 1F1B re-scoring: the traced partition's first largest stage s0 (0-based)
     // and the forward time sum_{i <= s0} ceil(c_i / 3); the pending frontier
@@ -784,61 +786,144 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
 #pragma unroll
                     for (int w = 0; w < 8; ++w) CTL[sg].bt[w] = 0;
                 }
-                // Back-trace of every running segment by its lane 0.  The loop over
-                // the stages is wave-uniform; the other lanes follow on clamped,
-                // in-range indices and drop what they compute.  The next stage's
-                // pointer and recomputation bound go out with this stage's prefix
-                // sums: one LDS round trip a stage.
-                {
-                    uint8_t *const btb = reinterpret_cast<uint8_t *>(CTL[segi].bt);
-                    uint32_t rmask = 0;
-                    int64_t m = 0, tf = 0, tf_after = 0;   // forward times (1F1B re-scoring)
-                    int s0 = 0;
-                    int b = N;
-                    bool ok = tracer && fin < kBig;
-                    const int pl = rl32(pk2, PP - 1) & 0xffff, kl = N - (rl32(pk1, PP - 1) & 0xff);
-                    int a = ARG[pl + kl], a0 = A0B[pl + kl];
-                    for (int s = PP - 1; s >= 0; --s) {
-                        ok = ok && a < b;
-                        int an = 0, a0n = 0;
-                        if (s > 0) {   // wave-uniform
-                            const int q1 = rl32(pk1, s - 1), q2 = rl32(pk2, s - 1);
+                if (PP >= kParallelTrace) {
+                    // Deep pipelines: lane 0 of each segment only follows the chain of
+                    // split points (one byte load a stage) into CTL.sb; then every
+                    // (segment, stage) entry recomputes its stage cost on its own lane
+                    // and the segment's largest stage, recomputation mask and layer
+                    // counts are combined with LDS atomics.  Same results as the
+                    // stage-by-stage trace below.
+                    {
+                        uint8_t *const sbb = reinterpret_cast<uint8_t *>(CTL[segi].sb);
+                        bool ok = tracer && fin < kBig;
+                        int b = N;
+                        for (int s = PP - 1; s >= 0; --s) {   // wave-uniform; clamped, in-range indices
+                            const int q1 = rl32(pk1, s), q2 = rl32(pk2, s);
                             const int wdn = q2 >> 16;
-                            int kn = (ok ? a : 0) - (q1 & 0xff);
-                            kn = kn < 0 ? 0 : (kn >= wdn ? wdn - 1 : kn);
-                            an = ARG[(q2 & 0xffff) + kn];
-                            a0n = A0B[(q2 & 0xffff) + kn];
+                            int k = b - (q1 & 0xff);
+                            k = k < 0 ? 0 : (k >= wdn ? wdn - 1 : k);
+                            const int a = ARG[(q2 & 0xffff) + k];
+                            ok = ok && a < b;
+                            if (tracer) sbb[s] = (uint8_t)a;
+                            b = ok ? a : b;
                         }
-                        const int ai = ok ? a : 0;
-                        const I64x2 *T = TM + ((rl32(pk1, s) >> 24) & 0xff) * NP;
-                        const I64x2 ta = T[ai], tb = T[b];   // negated prefix sums
-                        const bool r1 = ai < a0;
-                        const int64_t c = (r1 ? ta.y - tb.y : ta.x - tb.x) + rl64(p2p, s);
-                        if (ok) {
-                            if (EXACT) {   // walking down, ">=" keeps the first stage of largest cost
-                                if (c >= m) {
-                                    s0 = s;
-                                    tf_after = tf;
-                                }
-                                tf += (c + 2) / 3;
-                            }
-                            m = c > m ? c : m;
-                            btb[s] = (uint8_t)(b - a);
-                            if (r1) rmask |= 1u << s;
-                            b = a;
-                        }
-                        a = an;
-                        a0 = a0n;
-                    }
-                    if (tracer) {
                         ok = ok && b == 0;
-                        CTL[sg].M = m;
-                        if (EXACT) {
-                            CTL[sg].s0 = s0;
-                            CTL[sg].fwd = tf - tf_after;
+                        if (tracer) {
+                            CTL[sg].ok = ok ? 1u : 0u;
+                            CTL[sg].M = 0;
+                            CTL[sg].rmask = 0;
+                            if (EXACT) {
+                                CTL[sg].s0 = ok ? PP : 0;
+                                CTL[sg].fwd = 0;
+                            }
                         }
-                        CTL[sg].rmask = rmask;
-                        CTL[sg].ok = ok ? 1u : 0u;
+                    }
+                    wave_sync();
+                    const int nent = nseg * PP;   // <= 4 * 32: two rounds at most
+                    int64_t ce[2] = {0, 0};
+                    int qe[2] = {0, 0}, se[2] = {0, 0};
+                    bool ve[2] = {false, false};
+#pragma unroll
+                    for (int r = 0; r < 2; ++r) {
+                        const int e = r * 64 + lane;
+                        const bool act = e < nent;
+                        const int q = act ? e / PP : 0, s = act ? e % PP : 0;
+                        // only segments that ran this pass (the others keep their last trace)
+                        const bool valid = act && q < nact && CTL[q].on != 0 && CTL[q].ok != 0;
+                        const int p1 = __shfl(pk1, s, 64), p2 = __shfl(pk2, s, 64);
+                        const int plo = __shfl((int)(uint32_t)(uint64_t)p2p, s, 64);
+                        const int phi = __shfl((int)(uint32_t)((uint64_t)p2p >> 32), s, 64);
+                        const int64_t pc = (int64_t)(((uint64_t)(uint32_t)phi << 32) | (uint32_t)plo);
+                        const uint8_t *sbq = reinterpret_cast<const uint8_t *>(CTL[q].sb);
+                        const int a = valid ? sbq[s] : 0;
+                        const int b = valid ? (s + 1 < PP ? sbq[s + 1] : N) : 0;
+                        const int wdn = p2 >> 16;
+                        int k = b - (p1 & 0xff);
+                        k = k < 0 ? 0 : (k >= wdn ? wdn - 1 : k);
+                        const int a0 = (REG + q * arr_bytes + sumwd)[(p2 & 0xffff) + k];
+                        const I64x2 *T = TM + ((p1 >> 24) & 0xff) * NP;
+                        const I64x2 ta = T[a], tb = T[b];   // negated prefix sums
+                        const bool r1 = a < a0;
+                        const int64_t c = (r1 ? ta.y - tb.y : ta.x - tb.x) + pc;
+                        if (valid) {
+                            atomicMax(reinterpret_cast<unsigned long long *>(&CTL[q].M), (unsigned long long)c);
+                            if (r1) atomicOr(&CTL[q].rmask, 1u << s);
+                            reinterpret_cast<uint8_t *>(CTL[q].bt)[s] = (uint8_t)(b - a);
+                        }
+                        ce[r] = c;
+                        qe[r] = q;
+                        se[r] = s;
+                        ve[r] = valid;
+                    }
+                    if (EXACT) {   // the first stage of largest cost, then the forward time up to it
+                        wave_sync();
+#pragma unroll
+                        for (int r = 0; r < 2; ++r)
+                            if (ve[r] && ce[r] == CTL[qe[r]].M) atomicMin(&CTL[qe[r]].s0, se[r]);
+                        wave_sync();
+#pragma unroll
+                        for (int r = 0; r < 2; ++r)
+                            if (ve[r] && se[r] <= CTL[qe[r]].s0)
+                                atomicAdd(reinterpret_cast<unsigned long long *>(&CTL[qe[r]].fwd),
+                                          (unsigned long long)((ce[r] + 2) / 3));
+                    }
+                } else {
+                    // Back-trace of every running segment by its lane 0.  The loop over
+                    // the stages is wave-uniform; the other lanes follow on clamped,
+                    // in-range indices and drop what they compute.  The next stage's
+                    // pointer and recomputation bound go out with this stage's prefix
+                    // sums: one LDS round trip a stage.
+                    {
+                        uint8_t *const btb = reinterpret_cast<uint8_t *>(CTL[segi].bt);
+                        uint32_t rmask = 0;
+                        int64_t m = 0, tf = 0, tf_after = 0;   // forward times (1F1B re-scoring)
+                        int s0 = 0;
+                        int b = N;
+                        bool ok = tracer && fin < kBig;
+                        const int pl = rl32(pk2, PP - 1) & 0xffff, kl = N - (rl32(pk1, PP - 1) & 0xff);
+                        int a = ARG[pl + kl], a0 = A0B[pl + kl];
+                        for (int s = PP - 1; s >= 0; --s) {
+                            ok = ok && a < b;
+                            int an = 0, a0n = 0;
+                            if (s > 0) {   // wave-uniform
+                                const int q1 = rl32(pk1, s - 1), q2 = rl32(pk2, s - 1);
+                                const int wdn = q2 >> 16;
+                                int kn = (ok ? a : 0) - (q1 & 0xff);
+                                kn = kn < 0 ? 0 : (kn >= wdn ? wdn - 1 : kn);
+                                an = ARG[(q2 & 0xffff) + kn];
+                                a0n = A0B[(q2 & 0xffff) + kn];
+                            }
+                            const int ai = ok ? a : 0;
+                            const I64x2 *T = TM + ((rl32(pk1, s) >> 24) & 0xff) * NP;
+                            const I64x2 ta = T[ai], tb = T[b];   // negated prefix sums
+                            const bool r1 = ai < a0;
+                            const int64_t c = (r1 ? ta.y - tb.y : ta.x - tb.x) + rl64(p2p, s);
+                            if (ok) {
+                                if (EXACT) {   // walking down, ">=" keeps the first stage of largest cost
+                                    if (c >= m) {
+                                        s0 = s;
+                                        tf_after = tf;
+                                    }
+                                    tf += (c + 2) / 3;
+                                }
+                                m = c > m ? c : m;
+                                btb[s] = (uint8_t)(b - a);
+                                if (r1) rmask |= 1u << s;
+                                b = a;
+                            }
+                            a = an;
+                            a0 = a0n;
+                        }
+                        if (tracer) {
+                            ok = ok && b == 0;
+                            CTL[sg].M = m;
+                            if (EXACT) {
+                                CTL[sg].s0 = s0;
+                                CTL[sg].fwd = tf - tf_after;
+                            }
+                            CTL[sg].rmask = rmask;
+                            CTL[sg].ok = ok ? 1u : 0u;
+                        }
                     }
                 }
                 wave_sync();
