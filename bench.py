@@ -144,6 +144,38 @@ def leg_1f1b(torch, pl, stream, steps, warmup):
                           "layers": plan["layers"]}}
 
 
+FP64_PEAK_FLOPS = 78.6e12            # MI355X vector fp64
+HBM_PEAK_BYTES = 8.0e12
+COST_FLOPS_PER_ENTRY = 40            # fp64 operations per (configuration, type set, layer) entry
+ARGMIN_BYTES_PER_CANDIDATE = 16      # objective + status read per candidate
+
+
+def side_rooflines(binding, pl, ms):
+    """Kernel 1 (cost tables): bytes written against HBM and fp64 work against
+    the fp64 peak; kernel 3 (arg-min): bytes read against HBM (its time is the
+    whole hapmoe_best_plan call, plan read-back included)."""
+    import numpy as np
+    t = binding.decode_tables(pl.problem, pl.tables())
+    L = t["layout"]
+    used = np.array([bin(int(u)).count("1") for u in t["pi"]["used_masks"]], dtype=np.int64)
+    N = pl.problem["model"]["n_layers"]
+    entries = int(used.sum()) * N
+    written = (L["n_configs"] * 152 + L["n_configs"] * L["n_orders"] * 136 + L["n_configs"] * 4 * (N + 1) * 8
+               + int(used.sum()) * 3 * (N + 1) * 8)
+    ct_s, bp_s = ms["cost_tables"] / 1e3, ms["best_plan"] / 1e3
+    return {
+        "cost_tables": {"bound": "hbm", "achieved": written / ct_s / 1e9, "peak": HBM_PEAK_BYTES / 1e9,
+                        "unit": "GB/s", "frac": written / ct_s / HBM_PEAK_BYTES, "bytes_written": written,
+                        "fp64_achieved_tflops": entries * COST_FLOPS_PER_ENTRY / ct_s / 1e12,
+                        "fp64_frac": entries * COST_FLOPS_PER_ENTRY / ct_s / FP64_PEAK_FLOPS,
+                        "entries": entries, "flops_per_entry": COST_FLOPS_PER_ENTRY},
+        "best_plan": {"bound": "hbm", "achieved": pl.n * ARGMIN_BYTES_PER_CANDIDATE / bp_s / 1e9,
+                      "peak": HBM_PEAK_BYTES / 1e9, "unit": "GB/s",
+                      "frac": pl.n * ARGMIN_BYTES_PER_CANDIDATE / bp_s / HBM_PEAK_BYTES,
+                      "bytes_per_candidate": ARGMIN_BYTES_PER_CANDIDATE},
+    }
+
+
 def alu_roofline(relaxations, evaluations, ms, kernel):
     """VALU roofline of one stage-DP launch from its algorithmic operation count."""
     ops = relaxations * OPS_PER_RELAXATION + evaluations * OPS_PER_EVALUATION
@@ -349,6 +381,7 @@ def main():
                       "config": plan["config"], "order": plan["order"], "B": plan["n_micro"],
                       "layers": plan["layers"], "recompute": plan["recompute"]},
     }
+    out["side_rooflines"] = side_rooflines(binding, pl, ms)
     if clocks is not None:
         clocks["steps"] = args.steps
         out["stage_dp_section_clocks"] = clocks

@@ -76,6 +76,16 @@ __device__ inline int64_t wave_sum(int64_t x)
     return x;
 }
 
+__device__ inline int64_t wave_max(int64_t x)
+{
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) {
+        const int64_t y = __shfl_xor(x, d, 64);
+        x = y > x ? y : x;
+    }
+    return x;
+}
+
 __global__ __launch_bounds__(kThreads) void k_cost_tables(const unsigned char *__restrict__ img,
                                                           const hapmoe_candidate *__restrict__ cand,
                                                           int64_t per_config, TablesLayout L,
@@ -104,6 +114,9 @@ __global__ __launch_bounds__(kThreads) void k_cost_tables(const unsigned char *_
     __shared__ double s_pavg;
     __shared__ unsigned s_used, s_flag;
     __shared__ int64_t s_tbar;
+    __shared__ int32_t s_ospd[kMaxOrders][kMaxStages];   // block orderings: speed of each stage
+    __shared__ uint8_t s_omask[kMaxOrders][kMaxStages];  //   and its device-type set
+    __shared__ int64_t s_osum[kMaxOrders];               //   summed stage speeds
 
     // tokens of one micro-batch per rank, activation tensor bytes, D_moe (Eq. 3)
     const double tok = (double)((int64_t)H.seq_len * H.mbs / c.cp);
@@ -113,18 +126,111 @@ __global__ __launch_bounds__(kThreads) void k_cost_tables(const unsigned char *_
     if (tid == 0) {
         s_used = 0;
         s_flag = 0;
+    }
+    if (wave == 0) {   // parameters per device, averaged over the stages (exact int64 sums)
         int64_t pd = 0, pe = 0;
-        for (int l = 0; l < N; ++l) {
+        for (int l = lane; l < N; l += 64) {
             pd += pdense[l];
             pe += pexp[l];
         }
-        // parameters per device, averaged over the stages
-        s_pavg = ((double)pd / (double)c.tp + (double)pe / (double)(c.ep * c.tpe)) / (double)c.pp;
+        pd = wave_sum(pd);
+        pe = wave_sum(pe);
+        if (lane == 0) s_pavg = ((double)pd / (double)c.tp + (double)pe / (double)(c.ep * c.tpe)) / (double)c.pp;
+    }
+    // load-imbalance factor 1 + gamma (rho - 1), rho = max / mean tokens over the
+    // experts of a MoE layer: each wave takes every fourth layer, lanes over experts
+    for (int l = wave; l < N; l += kThreads / 64) {
+        double sk = 1.0;
+        if (is_moe[l]) {   // wave-uniform
+            int64_t sum = 0, mx = 0;
+            for (int e = lane; e < E; e += 64) {
+                const int64_t v = tokens[(int64_t)l * E + e];
+                sum += v;
+                mx = v > mx ? v : mx;
+            }
+            sum = wave_sum(sum);
+            mx = wave_max(mx);
+            const double rho = sum > 0 ? (double)(mx * E) / (double)sum : 1.0;
+            sk = 1.0 + H.gamma * (rho - 1.0);
+        }
+        if (lane == 0) s_skew[l] = sk;
     }
     __syncthreads();
 
-    // ---- stage layout of every device-type ordering (one thread each) ----
-    for (int o = tid; o < H.n_orders; o += kThreads) {
+    // ---- stage layout of the block orderings: (ordering, stage) pairs over the threads ----
+    if (H.stage_types == 0) {
+        const int nord = H.n_orders, PP = c.pp, g = H.total_devices / PP, npair = nord * PP;
+        for (int i = tid; i < npair; i += kThreads) {
+            const int o = i / PP, s = i - o * PP;
+            int pos_type[kMaxTypes], pos_end[kMaxTypes];
+            int acc = 0;
+            for (int j = 0; j < T; ++j) {
+                pos_type[j] = H.perm[o][j];
+                acc += H.count[pos_type[j]];
+                pos_end[j] = acc;
+            }
+            auto type_of = [&](int d) {
+                int t = pos_type[T - 1];
+                for (int j = T - 1; j >= 0; --j)
+                    if (d < pos_end[j]) t = pos_type[j];
+                return t;
+            };
+            const int d0 = s * g, d1 = d0 + g;
+            int mask = 0;
+            for (int j = 0; j < T; ++j)
+                if (pos_end[j] - H.count[pos_type[j]] < d1 && pos_end[j] > d0) mask |= 1 << pos_type[j];
+            const int bpair = s < PP - 1 ? (type_of(d1 - 1) << 2) | type_of(d1) : 0;
+            int sp = 0;
+            for (int h = 0; h < T; ++h)
+                if ((mask >> h) & 1) sp = (sp == 0 || H.speed[h] < sp) ? H.speed[h] : sp;
+            KeyInfo *K = reinterpret_cast<KeyInfo *>(tab + L.off_key) + (cfg * L.n_orders + o);
+            K->mask[s] = (uint8_t)mask;
+            K->bpair[s] = (uint8_t)bpair;
+            atomicOr(&s_used, 1u << (mask - 1));
+            s_ospd[o][s] = sp;
+            s_omask[o][s] = (uint8_t)mask;
+        }
+        __syncthreads();
+        // per ordering: summed speed, slowest link over the stages, T_dp-sync + T_opt
+        for (int o = tid; o < nord; o += kThreads) {
+            int64_t sum_speed = 0;
+            double al_k = 0.0, bw_k = 0.0;
+            for (int s = 0; s < PP; ++s) {
+                sum_speed += s_ospd[o][s];
+                double a, b;
+                set_link(H, s_omask[o][s], a, b);
+                if (s == 0 || a > al_k) al_k = a;
+                if (s == 0 || b < bw_k) bw_k = b;
+            }
+            s_osum[o] = sum_speed;
+            KeyInfo *K = reinterpret_cast<KeyInfo *>(tab + L.off_key) + (cfg * L.n_orders + o);
+            const double pavg = s_pavg;
+            K->dp_const = qterm(ring_ar(4.0 * pavg, c.dp, al_k, bw_k) + (H.opt_coef * pavg) / (double)c.dp, &s_flag);
+        }
+        __syncthreads();
+        // pruning-1 window: n_s in [(1-delta) w_s N, (1+delta) w_s N], w_s = P_s / sum P
+        const int64_t dn = H.delta_num, dd = H.delta_den;
+        for (int i = tid; i < npair; i += kThreads) {
+            const int o = i / PP, s = i - o * PP;
+            int64_t lo = 1, hi = N;
+            if (H.prune_window == 2) {   // uniform: floor(N / PP) .. ceil(N / PP) layers per stage
+                lo = N / PP;
+                hi = (N + PP - 1) / PP;
+            } else if (H.prune_window) {
+                const int64_t den = dd * s_osum[o];
+                lo = ((dd - dn) * s_ospd[o][s] * (int64_t)N) / den;
+                hi = ((dd + dn) * s_ospd[o][s] * (int64_t)N + den - 1) / den;
+                lo = lo < 1 ? 1 : lo;
+                hi = hi > N ? N : hi;
+            }
+            KeyInfo *K = reinterpret_cast<KeyInfo *>(tab + L.off_key) + (cfg * L.n_orders + o);
+            K->lo[s] = (uint8_t)lo;
+            K->hi[s] = (uint8_t)hi;
+        }
+    }
+
+    // ---- free stage types: the layout of every stage-type sequence (one thread each) ----
+    for (int o = tid; H.stage_types != 0 && o < H.n_orders; o += kThreads) {
         const int g = H.total_devices / c.pp;
         KeyInfo *K = reinterpret_cast<KeyInfo *>(tab + L.off_key) + (cfg * L.n_orders + o);
         int seq[kMaxStages];   // free stage types: the type of each stage
@@ -228,18 +334,7 @@ __global__ __launch_bounds__(kThreads) void k_cost_tables(const unsigned char *_
     // ---- per-layer terms: Eq. 2 per device type, load imbalance, memory ----
     for (int l = tid; l < N; l += kThreads) {
         const bool moe = is_moe[l] != 0;
-        double sk = 1.0;
-        if (moe) {
-            int64_t sum = 0, mx = 0;
-            for (int e = 0; e < E; ++e) {
-                const int64_t v = tokens[(int64_t)l * E + e];
-                sum += v;
-                mx = v > mx ? v : mx;
-            }
-            const double rho = sum > 0 ? (double)(mx * E) / (double)sum : 1.0;
-            sk = 1.0 + H.gamma * (rho - 1.0);
-        }
-        s_skew[l] = sk;
+        const double sk = s_skew[l];
         int64_t mce = 0;
         for (int h = 0; h < T; ++h) {
             const int64_t off = (((int64_t)h * 4 + lg2i(c.tp)) * 4 + lg2i(c.cp)) * N + l;
