@@ -90,8 +90,8 @@ __device__ inline void div_small(int i, int d, float inv, int &q, int &r)
     }
 }
 
-// the pure type-h stage s on [a, b) followed by hn (kMaxTypes: none); returns
-// kNone if its memory does not fit, else the cost and *r
+// Layer prefix sums of one configuration in LDS: stage times of each pure type
+// set without / with recomputation, weights, activations, MoE-layer count.
 struct StageData {
     const int64_t *T0, *T1;        // [T][W]
     const int64_t *MW, *MA0, *MA1;
@@ -99,6 +99,10 @@ struct StageData {
     int W;
 };
 
+// Cost of a pure type-h stage on layers [a, b) holding ms micro-batches of
+// activations in capacity cap, plus its outgoing transfer pc: kNone if it does
+// not fit even with recomputation, else the cost, *r = 1 if recomputation was
+// needed.
 __device__ inline int64_t stage_cost(const StageData &D, int h, int a, int b, int64_t ms, int64_t cap, int64_t X,
                                      bool recomp, int64_t pc, int *r)
 {
