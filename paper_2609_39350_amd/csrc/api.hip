@@ -195,7 +195,8 @@ int32_t check_problem(const hapmoe_problem *p)
             return HAPMOE_E_INVAL;
         if (p->space.stage_types == 2 &&
             (S.umax > kMaxTypeStates ||
-             type_dp_lds(p->model.n_layers, p->cluster.n_types, p->space.n_micro, S.umax).bytes > kTypeDpMaxLds))
+             type_dp_lds(p->model.n_layers, p->cluster.n_types, p->space.n_micro, S.umax, S.ppmax).bytes >
+                 kTypeDpMaxLds))
             return HAPMOE_E_INVAL;
     }
     return HAPMOE_OK;
@@ -532,7 +533,7 @@ int32_t stage_dp_types_any(const hapmoe_problem *p, const void *d_image, const h
         return HAPMOE_E_WORKSPACE;
     if (const int e = check_arch()) return e;
     if (count == 0) return HAPMOE_OK;
-    if (launch_type_dp(d_image, d_cand, p->model.n_layers, p->cluster.n_types, p->space.n_micro, S.umax, L,
+    if (launch_type_dp(d_image, d_cand, p->model.n_layers, p->cluster.n_types, p->space.n_micro, S.umax, S.ppmax, L,
                        d_tables, first, count, d_res, d_types, d_stats, d_ws, exact,
                        (hipStream_t)stream) != hipSuccess)
         return HAPMOE_E_HIP;

@@ -135,14 +135,14 @@ constexpr int64_t kTypeDpMaxSlotBytes = int64_t(8) << 30;   // all slices togeth
 constexpr int kTypeDpMaxLds = 64 * 1024;
 struct TypeLds {
     int umax;
-    int off_t0, off_t1, off_mw, off_moe, off_inc, off_path, off_ctl, off_ulist, bytes;
+    int off_t0, off_t1, off_mw, off_moe, off_inc, off_path, off_ctl, off_ulist, off_bounds, bytes;
 };
-TypeLds type_dp_lds(int n_layers, int n_types, int n_micro, int umax);
+TypeLds type_dp_lds(int n_layers, int n_types, int n_micro, int umax, int ppmax);
 int64_t type_dp_slot_bytes(int n_layers, int n_types, int umax);
 int64_t type_dp_slots(int64_t n_keys, int64_t slot_bytes);
 int64_t type_dp_ws_bytes(int n_layers, int n_types, int umax, int64_t n_configs);
 hipError_t launch_type_dp(const void *d_image, const hapmoe_candidate *d_cand, int n_layers, int n_types,
-                          int n_micro, int umax, const TablesLayout &L, const void *d_tables, int64_t first,
+                          int n_micro, int umax, int ppmax, const TablesLayout &L, const void *d_tables, int64_t first,
                           int64_t count, hapmoe_dp_result *d_res, uint8_t *d_types, int32_t *d_stats, void *d_ws,
                           bool exact, hipStream_t s);
 // bytes of the winner record in the best-plan workspace (result, candidate, stage layout)

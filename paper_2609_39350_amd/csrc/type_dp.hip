@@ -39,6 +39,7 @@ namespace {
 
 constexpr int kThreads = 1024;
 constexpr int64_t kNone = INT64_MAX;   // no path
+constexpr int kTypeWin = 4;            // split points a predecessor type loads at once
 
 struct TypePath {   // result of one pass, filled by thread 0
     int64_t F, M;
@@ -142,6 +143,10 @@ __global__ __launch_bounds__(kThreads) void k_type_dp(const unsigned char *__res
     int64_t *sMA0 = sMW + W, *sMA1 = sMA0 + W;
     int32_t *sMOE = reinterpret_cast<int32_t *>(smem + S.off_moe);
     uint64_t *ulist = reinterpret_cast<uint64_t *>(smem + S.off_ulist);
+    // per (stage, type, end layer b) of the current B group: the least split
+    // point that fits at all (low byte) and the least that fits without
+    // recomputation (high byte); b itself means none
+    uint16_t *bounds = reinterpret_cast<uint16_t *>(smem + S.off_bounds);
     TypeInc *inc = reinterpret_cast<TypeInc *>(smem + S.off_inc);
     TypePath &P = *reinterpret_cast<TypePath *>(smem + S.off_path);
     TypePath &Q = *(reinterpret_cast<TypePath *>(smem + S.off_path) + 1);   // 1F1B: the pending frontier point
@@ -253,7 +258,6 @@ __global__ __launch_bounds__(kThreads) void k_type_dp(const unsigned char *__res
             __syncthreads();
             for (int l = 1; l <= PP; ++l) {
                 const int s = l - 1;   // the stage that ends at b
-                const int64_t ms = (PP - s) < v ? (PP - s) : v;
                 const int wm = C.wmax[l], row = wm * T1;
                 const int n_items = (C.start[l + 1] - C.start[l]) * row;
                 const float inv_row = row ? 1.0f / (float)row : 0.0f, inv_t1 = 1.0f / (float)T1;
@@ -281,40 +285,59 @@ __global__ __launch_bounds__(kThreads) void k_type_dp(const unsigned char *__res
                     if (l == PP ? hn != T : (hn == T || dn >= kn)) continue;
                     int64_t best = kNone;
                     int bk = 0x7fff;
+                    auto relax1 = [&](int h, int a, int64_t prev, int amin, int a0, int64_t tb0, int64_t tb1,
+                                      int64_t pc) {
+                        if (prev == kNone || a < amin) return;
+                        const int64_t c = (a < a0 ? tb1 - sT1[h * W + a] : tb0 - sT0[h * W + a]) + pc;
+                        if (c > t) return;
+                        const int64_t val = prev + c;
+                        const int key2 = a * 8 + h;
+                        if (val < best || (val == best && key2 < bk)) {
+                            best = val;
+                            bk = key2;
+                        }
+                    };
+                    // the first kTypeWin split points of every predecessor type are
+                    // loaded together (up to 16 loads in flight), then relaxed; longer
+                    // windows (no pruning-1 windows) finish in a second loop
+                    int wa0[kMaxTypes], wa1[kMaxTypes];
+                    int64_t wpc[kMaxTypes], pv[kMaxTypes][kTypeWin];
 #pragma unroll
                     for (int h = 0; h < kMaxTypes; ++h) {
-                        if (h >= T || d[h] == 0) continue;
-                        const int64_t pc = hn < T ? pi->p2p[h * kMaxTypes + hn] : 0;
-                        if (prune_het && hn < T && hn != h && pc > eta_tbar) continue;   // pruning 3
-                        const int up = u - rad[h];
-                        // the predecessor's band: one stage of type h fewer
-                        const int plo = (ulo - lo[h]) > N - (rhi + hi[h]) ? (ulo - lo[h]) : N - (rhi + hi[h]);
-                        const int phi = (uhi - hi[h]) < N - (rlo + lo[h]) ? (uhi - hi[h]) : N - (rlo + lo[h]);
-                        const int a0 = (b - hi[h]) > plo ? (b - hi[h]) : plo;
-                        const int a1 = (b - lo[h]) < phi ? (b - lo[h]) : phi;
-                        const int64_t cap = H.mem_bytes[h];
-                        const int64_t *Fp = F + (int64_t)up * W * T1 + h;
-                        for (int a = a0; a <= a1; a += 2) {   // two split points a trip: both loads in flight
-                            const bool two = a + 1 <= a1;
-                            const int64_t prev0 = Fp[(int64_t)a * T1];
-                            const int64_t prev1 = two ? Fp[(int64_t)(a + 1) * T1] : kNone;
-                            if (STATS) relax += two ? 2 : 1;
-#pragma unroll
-                            for (int e = 0; e < 2; ++e) {
-                                const int64_t prev = e ? prev1 : prev0;
-                                if (prev == kNone) continue;
-                                const int ae = a + e;
-                                int r;
-                                const int64_t c = stage_cost(D, h, ae, b, ms, cap, X, recomp, pc, &r);
-                                if (c == kNone || c > t) continue;
-                                const int64_t val = prev + c;
-                                const int key2 = ae * 8 + h;
-                                if (val < best || (val == best && key2 < bk)) {
-                                    best = val;
-                                    bk = key2;
-                                }
+                        wa0[h] = 1;
+                        wa1[h] = 0;   // empty
+                        wpc[h] = 0;
+                        if (h < T && d[h] > 0) {
+                            const int64_t pc = hn < T ? pi->p2p[h * kMaxTypes + hn] : 0;
+                            if (!(prune_het && hn < T && hn != h && pc > eta_tbar)) {   // pruning 3
+                                // the predecessor's band: one stage of type h fewer
+                                const int plo = (ulo - lo[h]) > N - (rhi + hi[h]) ? (ulo - lo[h]) : N - (rhi + hi[h]);
+                                const int phi = (uhi - hi[h]) < N - (rlo + lo[h]) ? (uhi - hi[h]) : N - (rlo + lo[h]);
+                                wa0[h] = (b - hi[h]) > plo ? (b - hi[h]) : plo;
+                                wa1[h] = (b - lo[h]) < phi ? (b - lo[h]) : phi;
+                                wpc[h] = pc;
                             }
                         }
+                        const int64_t *Fp = F + (int64_t)(u - rad[h]) * W * T1 + h;
+#pragma unroll
+                        for (int j = 0; j < kTypeWin; ++j) {
+                            const int a = wa0[h] + j;
+                            pv[h][j] = a <= wa1[h] ? Fp[(int64_t)a * T1] : kNone;
+                        }
+                    }
+#pragma unroll
+                    for (int h = 0; h < kMaxTypes; ++h) {
+                        if (wa0[h] > wa1[h]) continue;
+                        if (STATS) relax += (uint32_t)(wa1[h] - wa0[h] + 1);
+                        const int bd = bounds[(s * T + h) * W + b];
+                        const int amin = bd & 0xff, a0 = bd >> 8;
+                        const int64_t tb0 = sT0[h * W + b], tb1 = sT1[h * W + b];
+#pragma unroll
+                        for (int j = 0; j < kTypeWin; ++j)
+                            if (wa0[h] + j <= wa1[h]) relax1(h, wa0[h] + j, pv[h][j], amin, a0, tb0, tb1, wpc[h]);
+                        const int64_t *Fp = F + (int64_t)(u - rad[h]) * W * T1 + h;
+                        for (int a = wa0[h] + kTypeWin; a <= wa1[h]; ++a)
+                            relax1(h, a, Fp[(int64_t)a * T1], amin, a0, tb0, tb1, wpc[h]);
                     }
                     const int64_t at = ((int64_t)u * W + b) * T1 + hn;
                     F[at] = best;
@@ -410,6 +433,28 @@ __global__ __launch_bounds__(kThreads) void k_type_dp(const unsigned char *__res
                 inc[tid].passes = 0;
             }
             if (tid == 0) C.relax = 0;
+            // feasible split points of every (stage, type, end layer) for this group:
+            // memory only falls as the split point a rises, so they form a suffix of
+            // the pruning-1 window; scan it downwards
+            if (shape_ok)
+                for (int i = tid; i < PP * T * W; i += kThreads) {
+                    const int b = i % W, sh = i / W, h = sh % T, st = sh / T;
+                    const int64_t ms = (PP - st) < v ? (PP - st) : v;
+                    const int64_t cap = H.mem_bytes[h];
+                    int amin = b, a0 = b;
+                    const int top = b - (h == 0 ? lo[0] : h == 1 ? lo[1] : h == 2 ? lo[2] : lo[3]);
+                    const int bot = b - (h == 0 ? hi[0] : h == 1 ? hi[1] : h == 2 ? hi[2] : hi[3]);
+                    for (int a = top; a >= 0 && a >= bot; --a) {
+                        const int64_t dw = sMW[b] - sMW[a];
+                        const int64_t ex = (sMOE[b] - sMOE[a]) > 0 ? X : 0;
+                        const bool fit0 = dw + ms * (sMA0[b] - sMA0[a]) + ex <= cap;
+                        const bool fit1 = recomp && dw + ms * (sMA1[b] - sMA1[a]) + ex <= cap;
+                        if (!(fit0 || fit1)) break;
+                        amin = a;
+                        if (fit0) a0 = a;
+                    }
+                    bounds[i] = (uint16_t)(amin | (a0 << 8));
+                }
             __syncthreads();
             int passes = 0;
             if (shape_ok && !EXACT) {
@@ -529,7 +574,7 @@ __global__ void k_reset_type_queue(uint32_t *q) { q[0] = 0; }
 
 }  // namespace
 
-TypeLds type_dp_lds(int n_layers, int n_types, int n_micro, int umax)
+TypeLds type_dp_lds(int n_layers, int n_types, int n_micro, int umax, int ppmax)
 {
     const int W = n_layers + 1;
     TypeLds S;
@@ -548,6 +593,7 @@ TypeLds type_dp_lds(int n_layers, int n_types, int n_micro, int umax)
     S.off_path = take(2 * sizeof(TypePath));
     S.off_ctl = take(sizeof(TypeCtl));
     S.off_ulist = take((int64_t)umax * 8);
+    S.off_bounds = take((int64_t)ppmax * n_types * W * 2);
     S.bytes = (int)off;
     return S;
 }
@@ -567,13 +613,13 @@ int64_t type_dp_slots(int64_t n_keys, int64_t slot_bytes)
 }
 
 hipError_t launch_type_dp(const void *d_image, const hapmoe_candidate *d_cand, int n_layers, int n_types,
-                          int n_micro, int umax, const TablesLayout &L, const void *d_tables, int64_t first,
+                          int n_micro, int umax, int ppmax, const TablesLayout &L, const void *d_tables, int64_t first,
                           int64_t count, hapmoe_dp_result *d_res, uint8_t *d_types, int32_t *d_stats, void *d_ws,
                           bool exact, hipStream_t s)
 {
     const int64_t key_lo = first / n_micro, key_hi = (first + count - 1) / n_micro;
     const int64_t n_keys = key_hi - key_lo + 1;
-    const TypeLds S = type_dp_lds(n_layers, n_types, n_micro, umax);
+    const TypeLds S = type_dp_lds(n_layers, n_types, n_micro, umax, ppmax);
     const int64_t slot_bytes = type_dp_slot_bytes(n_layers, n_types, umax);
     const int64_t slots = type_dp_slots(L.n_configs, slot_bytes);
     const int64_t grid = slots < n_keys ? slots : n_keys;
