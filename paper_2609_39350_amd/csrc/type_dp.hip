@@ -258,18 +258,20 @@ __global__ __launch_bounds__(kThreads) void k_type_dp(const unsigned char *__res
             __syncthreads();
             for (int l = 1; l <= PP; ++l) {
                 const int s = l - 1;   // the stage that ends at b
-                const int wm = C.wmax[l], row = wm * T1;
-                const int n_items = (C.start[l + 1] - C.start[l]) * row;
-                const float inv_row = row ? 1.0f / (float)row : 0.0f, inv_t1 = 1.0f / (float)T1;
+                // one (u, b) state vector a thread: its predecessors are loaded once and
+                // relaxed into every valid next type h' (the transfer and pruning 3
+                // depend on h', the rest does not)
+                const int wm = C.wmax[l];
+                const int n_items = (C.start[l + 1] - C.start[l]) * wm;
+                const float inv_wm = wm ? 1.0f / (float)wm : 0.0f;
                 for (int i = tid; i < n_items; i += kThreads) {
-                    int pos, rem, j, hn;
-                    div_small(i, row, inv_row, pos, rem);
-                    div_small(rem, T1, inv_t1, j, hn);
+                    int pos, j;
+                    div_small(i, wm, inv_wm, pos, j);
                     const uint64_t x = ulist[C.start[l] + pos];
                     const int wd = (int)(x >> 45) & 0x1ff;
                     if (j >= wd) continue;
                     const int u = (int)(x & 0x1fff), b = ((int)(x >> 37) & 0xff) + j;
-                    int d[kMaxTypes], ulo = 0, uhi = 0, rlo = 0, rhi = 0, dn = 0, kn = 0;
+                    int d[kMaxTypes], ulo = 0, uhi = 0, rlo = 0, rhi = 0, hnmask = 0;
 #pragma unroll
                     for (int h = 0; h < kMaxTypes; ++h) {
                         d[h] = (int)(x >> (13 + 6 * h)) & 63;
@@ -277,71 +279,86 @@ __global__ __launch_bounds__(kThreads) void k_type_dp(const unsigned char *__res
                         uhi += d[h] * hi[h];
                         rlo += (k[h] - d[h]) * lo[h];
                         rhi += (k[h] - d[h]) * hi[h];
-                        if (h == hn) {
-                            dn = d[h];
-                            kn = k[h];
-                        }
+                        if (h < T && d[h] < k[h]) hnmask |= 1 << h;   // a stage of type h can follow
                     }
-                    if (l == PP ? hn != T : (hn == T || dn >= kn)) continue;
-                    int64_t best = kNone;
-                    int bk = 0x7fff;
-                    auto relax1 = [&](int h, int a, int64_t prev, int amin, int a0, int64_t tb0, int64_t tb1,
-                                      int64_t pc) {
-                        if (prev == kNone || a < amin) return;
-                        const int64_t c = (a < a0 ? tb1 - sT1[h * W + a] : tb0 - sT0[h * W + a]) + pc;
-                        if (c > t) return;
-                        const int64_t val = prev + c;
-                        const int key2 = a * 8 + h;
-                        if (val < best || (val == best && key2 < bk)) {
-                            best = val;
-                            bk = key2;
-                        }
-                    };
+                    if (l == PP) hnmask = 1 << T;   // the last stage: no successor
+                    int64_t best[kMaxTypes + 1];
+                    int bk[kMaxTypes + 1];
+#pragma unroll
+                    for (int e = 0; e <= kMaxTypes; ++e) {
+                        best[e] = kNone;
+                        bk[e] = 0x7fff;
+                    }
                     // the first kTypeWin split points of every predecessor type are
                     // loaded together (up to 16 loads in flight), then relaxed; longer
                     // windows (no pruning-1 windows) finish in a second loop
                     int wa0[kMaxTypes], wa1[kMaxTypes];
-                    int64_t wpc[kMaxTypes], pv[kMaxTypes][kTypeWin];
+                    int64_t pv[kMaxTypes][kTypeWin];
 #pragma unroll
                     for (int h = 0; h < kMaxTypes; ++h) {
                         wa0[h] = 1;
                         wa1[h] = 0;   // empty
-                        wpc[h] = 0;
                         if (h < T && d[h] > 0) {
-                            const int64_t pc = hn < T ? pi->p2p[h * kMaxTypes + hn] : 0;
-                            if (!(prune_het && hn < T && hn != h && pc > eta_tbar)) {   // pruning 3
-                                // the predecessor's band: one stage of type h fewer
-                                const int plo = (ulo - lo[h]) > N - (rhi + hi[h]) ? (ulo - lo[h]) : N - (rhi + hi[h]);
-                                const int phi = (uhi - hi[h]) < N - (rlo + lo[h]) ? (uhi - hi[h]) : N - (rlo + lo[h]);
-                                wa0[h] = (b - hi[h]) > plo ? (b - hi[h]) : plo;
-                                wa1[h] = (b - lo[h]) < phi ? (b - lo[h]) : phi;
-                                wpc[h] = pc;
-                            }
+                            // the predecessor's band: one stage of type h fewer
+                            const int plo = (ulo - lo[h]) > N - (rhi + hi[h]) ? (ulo - lo[h]) : N - (rhi + hi[h]);
+                            const int phi = (uhi - hi[h]) < N - (rlo + lo[h]) ? (uhi - hi[h]) : N - (rlo + lo[h]);
+                            wa0[h] = (b - hi[h]) > plo ? (b - hi[h]) : plo;
+                            wa1[h] = (b - lo[h]) < phi ? (b - lo[h]) : phi;
                         }
                         const int64_t *Fp = F + (int64_t)(u - rad[h]) * W * T1 + h;
 #pragma unroll
-                        for (int j = 0; j < kTypeWin; ++j) {
-                            const int a = wa0[h] + j;
-                            pv[h][j] = a <= wa1[h] ? Fp[(int64_t)a * T1] : kNone;
+                        for (int jj = 0; jj < kTypeWin; ++jj) {
+                            const int a = wa0[h] + jj;
+                            pv[h][jj] = a <= wa1[h] ? Fp[(int64_t)a * T1] : kNone;
                         }
                     }
 #pragma unroll
                     for (int h = 0; h < kMaxTypes; ++h) {
                         if (wa0[h] > wa1[h]) continue;
-                        if (STATS) relax += (uint32_t)(wa1[h] - wa0[h] + 1);
+                        // transfer to each next type, and pruning 3 on it
+                        int64_t pc[kMaxTypes + 1];
+                        int ok = 0;
+#pragma unroll
+                        for (int e = 0; e <= kMaxTypes; ++e) {
+                            pc[e] = e < T ? pi->p2p[h * kMaxTypes + e] : 0;
+                            const bool p3 = prune_het && e < T && e != h && pc[e] > eta_tbar;
+                            if (((hnmask >> e) & 1) && !p3) ok |= 1 << e;
+                        }
+                        if (!ok) continue;
+                        if (STATS) relax += (uint32_t)((wa1[h] - wa0[h] + 1) * __popc(ok));
                         const int bd = bounds[(s * T + h) * W + b];
                         const int amin = bd & 0xff, a0 = bd >> 8;
                         const int64_t tb0 = sT0[h * W + b], tb1 = sT1[h * W + b];
-#pragma unroll
-                        for (int j = 0; j < kTypeWin; ++j)
-                            if (wa0[h] + j <= wa1[h]) relax1(h, wa0[h] + j, pv[h][j], amin, a0, tb0, tb1, wpc[h]);
                         const int64_t *Fp = F + (int64_t)(u - rad[h]) * W * T1 + h;
-                        for (int a = wa0[h] + kTypeWin; a <= wa1[h]; ++a)
-                            relax1(h, a, Fp[(int64_t)a * T1], amin, a0, tb0, tb1, wpc[h]);
+                        for (int a = wa0[h]; a <= wa1[h]; ++a) {
+                            const int jj = a - wa0[h];
+                            int64_t prev = kNone;
+#pragma unroll
+                            for (int q = 0; q < kTypeWin; ++q) prev = jj == q ? pv[h][q] : prev;
+                            if (jj >= kTypeWin) prev = Fp[(int64_t)a * T1];
+                            if (prev == kNone || a < amin) continue;
+                            const int64_t st = a < a0 ? tb1 - sT1[h * W + a] : tb0 - sT0[h * W + a];
+                            const int key2 = a * 8 + h;
+#pragma unroll
+                            for (int e = 0; e <= kMaxTypes; ++e) {
+                                if (!((ok >> e) & 1)) continue;
+                                const int64_t c = st + pc[e];
+                                if (c > t) continue;
+                                const int64_t val = prev + c;
+                                if (val < best[e] || (val == best[e] && key2 < bk[e])) {
+                                    best[e] = val;
+                                    bk[e] = key2;
+                                }
+                            }
+                        }
                     }
-                    const int64_t at = ((int64_t)u * W + b) * T1 + hn;
-                    F[at] = best;
-                    ARG[at] = (int16_t)(best == kNone ? -1 : bk);
+                    const int64_t at = ((int64_t)u * W + b) * T1;
+#pragma unroll
+                    for (int e = 0; e <= kMaxTypes; ++e) {
+                        if (!((hnmask >> e) & 1)) continue;
+                        F[at + e] = best[e];
+                        ARG[at + e] = (int16_t)(best[e] == kNone ? -1 : bk[e]);
+                    }
                 }
                 __syncthreads();
             }
