@@ -425,6 +425,49 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
         // woff | wd << 16 (woff <= 32 * 128, wd <= 128)
         const int pk1 = (blo & 0xff) | ((bhi & 0xff) << 8) | ((lo & 0xff) << 16) | (slot << 24);
         const int pk2 = woff | (wd << 16);
+        // and hi | mask << 8 | mixed << 16 | bdiff << 17, for the stage-flattened scans
+        const int pk3 = (hi & 0xff) | (mask << 8) | (mixed << 16) | (bdiff << 17);
+        // The classification and feasibility scans spread the (stage, end layer)
+        // entries of all stages over the lanes at once (the stages are independent
+        // there); each lane finds its stage by a binary search over the packed
+        // offsets and reads the stage's fields from that lane.
+        // (both read other lanes: call them with every lane of the wave active)
+        auto stage_of = [&](int e) {   // the stage whose packed band holds entry e
+            int st = 0;
+#pragma unroll
+            for (int step = 16; step >= 1; step >>= 1) {
+                const int c = st + step;
+                const int wc = __shfl(woff, c < 64 ? c : 63, 64);
+                if (c < PP && wc <= e) st = c;
+            }
+            return st;
+        };
+        struct StageP {
+            int lo, hi, blo, off, wd, mask, mixed, bdiff, plo, phi;
+            int64_t cap, p2p;
+        };
+        auto stage_p = [&](int st) {   // stage st's fields (st may differ across lanes)
+            StageP P;
+            const int q1 = __shfl(pk1, st, 64), q2 = __shfl(pk2, st, 64), q3 = __shfl(pk3, st, 64);
+            const int r1 = __shfl(pk1, st > 0 ? st - 1 : 0, 64);
+            P.blo = q1 & 0xff;
+            P.lo = (q1 >> 16) & 0xff;
+            P.off = q2 & 0xffff;
+            P.wd = q2 >> 16;
+            P.hi = q3 & 0xff;
+            P.mask = (q3 >> 8) & 0xff;
+            P.mixed = (q3 >> 16) & 1;
+            P.bdiff = (q3 >> 17) & 1;
+            P.plo = st ? (r1 & 0xff) : 0;
+            P.phi = st ? ((r1 >> 8) & 0xff) : 0;
+            const int c0 = __shfl((int)(uint32_t)(uint64_t)cap, st, 64);
+            const int c1 = __shfl((int)(uint32_t)((uint64_t)cap >> 32), st, 64);
+            const int p0 = __shfl((int)(uint32_t)(uint64_t)p2p, st, 64);
+            const int p1 = __shfl((int)(uint32_t)((uint64_t)p2p >> 32), st, 64);
+            P.cap = (int64_t)(((uint64_t)(uint32_t)c1 << 32) | (uint32_t)c0);
+            P.p2p = (int64_t)(((uint64_t)(uint32_t)p1 << 32) | (uint32_t)p0);
+            return P;
+        };
         const int sumwd = rl32(woff, 63) + rl32(wd, 63);
         const int maxw = wave_max32(wd);
 
@@ -488,36 +531,41 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
         wave_sync();
         uint64_t brk = 0;
         int cls_evals = 0;
-        for (int s = 0; s + 1 < PP; ++s) {
-            const int mtop = PP - s - 1;   // steps that matter: m in [1, mtop]
-            const int lo_s = rl32(lo, s), hi_s = rl32(hi, s), mask_s = rl32(mask, s);
-            const int blo_s = rl32(blo, s), wd_s = rl32(wd, s);
-            const int plo = s ? rl32(blo, s - 1) : 0, phi = s ? rl32(bhi, s - 1) : 0;
-            const int mixed_s = rl32(mixed, s), bdiff_s = rl32(bdiff, s);
-            const int64_t cap_s = rl64(cap, s), p2p_s = rl64(p2p, s);
-            const int64_t *CM = mixed_s ? time + ((int64_t)(mask_s - 1) * 3 + 2) * np : nullptr;
-            const int64_t hc_b = bdiff_s ? p2p_s : 0;
-            for (int k = lane; k < wd_s; k += 64) {
-                const int b = blo_s + k;
-                const int ahi = (b - lo_s) < phi ? (b - lo_s) : phi;
-                const int alo = (b - hi_s) > plo ? (b - hi_s) : plo;
-                const int64_t wb = MW[b], a0b = MA0[b], a1b = MA1[b];
-                const int mb = MOE[b];
-                const int64_t cmb = CM ? CM[b] : 0;
-                // the counts do not fall as a grows: once both exceed mtop, so do
-                // all the later ones
-                for (int a = alo; a <= ahi; ++a) {
-                    if (STATS) ++cls_evals;
-                    const int64_t xb = (mb - MOE[a]) > 0 ? X : 0;
-                    const int64_t room = cap_s - (wb - MW[a] + xb);
-                    const bool ok3 = !prune_het || (CM ? cmb - CM[a] : 0) + hc_b <= eta_tbar;
-                    if (!ok3) continue;
-                    const int m0 = cap_count(room, a0b - MA0[a]);
-                    const int m1 = recomp ? cap_count(room, a1b - MA1[a]) : 64;
-                    brk |= step_bit(m0, mtop) | (recomp ? step_bit(m1, mtop) : 0);
-                    if (m0 > mtop && m1 > mtop) break;
-                }
+        // one (stage, b) entry's window: every step m <= mtop of its fitting counts
+        auto classify = [&](int b, int lo_s, int hi_s, int plo, int phi, int mtop, int64_t cap_s,
+                            const int64_t *CM, int64_t hc_b) {
+            const int ahi = (b - lo_s) < phi ? (b - lo_s) : phi;
+            const int alo = (b - hi_s) > plo ? (b - hi_s) : plo;
+            const int64_t wb = MW[b], a0b = MA0[b], a1b = MA1[b];
+            const int mb = MOE[b];
+            const int64_t cmb = CM ? CM[b] : 0;
+            // the counts do not fall as a grows: once both exceed mtop, so do
+            // all the later ones
+            for (int a = alo; a <= ahi; ++a) {
+                if (STATS) ++cls_evals;
+                const int64_t xb = (mb - MOE[a]) > 0 ? X : 0;
+                const int64_t room = cap_s - (wb - MW[a] + xb);
+                const bool ok3 = !prune_het || (CM ? cmb - CM[a] : 0) + hc_b <= eta_tbar;
+                if (!ok3) continue;
+                const int m0 = cap_count(room, a0b - MA0[a]);
+                const int m1 = recomp ? cap_count(room, a1b - MA1[a]) : 64;
+                brk |= step_bit(m0, mtop) | (recomp ? step_bit(m1, mtop) : 0);
+                if (m0 > mtop && m1 > mtop) break;
             }
+        };
+        const int nent = rl32(woff, PP - 1);   // the entries of stages 0 .. PP - 2
+        for (int e0 = 0; e0 < nent; e0 += 64) {   // wave-uniform
+            // every lane takes part in the cross-lane reads of stage_of and
+            // stage_p (a read from an inactive lane is undefined); only the
+            // lanes holding an entry classify it
+            const int e = e0 + lane;
+            const bool act = e < nent;
+            const int st = stage_of(act ? e : 0);
+            const StageP P = stage_p(st);
+            const int64_t *CM = P.mixed ? time + ((int64_t)(P.mask - 1) * 3 + 2) * np : nullptr;
+            if (act)
+                classify(P.blo + (e - P.off), P.lo, P.hi, P.plo, P.phi, PP - st - 1, P.cap, CM,
+                         P.bdiff ? P.p2p : 0);
         }
         brk = wave_or64(brk);
         const int cls_sum = STATS ? wave_sum32(cls_evals) : 0;
@@ -584,70 +632,69 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
             int evq[kMaxSeg] = {(STATS && g0 == 0 && lane == 0) ? cls_sum : 0, 0, 0, 0};
             // ---- feasible split interval of every (stage, b in band), per segment ----
             // a in [AMIN, A0B) fits only with recomputation (r = 1), a in [A0B, b - lo] without.
-            // The (segment, b) entries of a stage are spread over all 64 lanes.
-            for (int s = 0; s < PP; ++s) {
-                const int lo_s = rl32(lo, s), hi_s = rl32(hi, s), mask_s = rl32(mask, s);
-                const int blo_s = rl32(blo, s), wd_s = rl32(wd, s), off_s = rl32(woff, s);
-                const int plo = s ? rl32(blo, s - 1) : 0, phi = s ? rl32(bhi, s - 1) : 0;
-                const int mixed_s = rl32(mixed, s), bdiff_s = rl32(bdiff, s);
-                const int64_t cap_s = rl64(cap, s), p2p_s = rl64(p2p, s);
-                const int64_t *CM = mixed_s ? time + ((int64_t)(mask_s - 1) * 3 + 2) * np : nullptr;
-                const int64_t hc_b = bdiff_s ? p2p_s : 0;
-                const int total = nact * wd_s;
-                const float inv_wd = __builtin_amdgcn_rcpf((float)wd_s);   // split_entry corrects
-                for (int e0 = 0; e0 < total; e0 += 64) {   // wave-uniform
-                    const int e = e0 + lane;
-                    const bool act = e < total;
-                    int q, k;
-                    split_entry(act ? e : 0, wd_s, inv_wd, q, k);
-                    const int vs = sel4(vq, q);
-                    const int64_t ms = (int64_t)((PP - s) < vs ? (PP - s) : vs);   // 1F1B stored micro-batches
-                    uint8_t *const AMq = REG + q * arr_bytes;
-                    const int b = blo_s + k;
-                    const int ahi = (b - lo_s) < phi ? (b - lo_s) : phi;
-                    const int alo = (b - hi_s) > plo ? (b - hi_s) : plo;
-                    const bool has = act && ahi >= alo;
-                    // the feasible split points form a suffix [amin, ahi] of the window
-                    // (memory and pruning 3 only grow with the segment), and so do those
-                    // feasible without recomputation, [a0, ahi]: scanning a upwards, the
-                    // first hit of each is its bound, and a lane is done at its first
-                    // split point that fits without recomputation
-                    int amin = has ? ahi + 1 : 255, a0 = amin;
-                    const int64_t wb = MW[b], a0b = MA0[b], a1b = MA1[b];
-                    const int mb = MOE[b];
-                    const int64_t cmb = CM ? CM[b] : 0;
-                    const int aend = has ? ahi : plo;
-                    bool open = has;
-                    // one split point's test, gated by the lane still being open
-                    auto test = [&](int a, int64_t mwa, int64_t ma0, int64_t ma1, int moea, int64_t cma) {
-                        const int64_t xb = (mb - moea) > 0 ? X : 0;
-                        const int64_t base = wb - mwa + xb;
-                        const bool ok3 = !prune_het | (cmb - cma + hc_b <= eta_tbar);
-                        const bool f0 = open & ok3 & (base + ms * (a0b - ma0) <= cap_s);
-                        const bool f1 = open & ok3 & recomp & (base + ms * (a1b - ma1) <= cap_s);
-                        if (STATS) add4(evq, q, open ? 1 : 0);
-                        amin = ((f0 | f1) & (a < amin)) ? a : amin;
-                        a0 = f0 ? a : a0;
-                        open = open & !f0 & (a < aend);
-                    };
-                    // two split points per trip, all loads issued before either test
-                    int a = has ? alo : plo;
-                    for (;;) {   // a lane closes at aend at the latest
-                        const int a2 = a < aend ? a + 1 : a;
-                        const int64_t w1 = MW[a], w2 = MW[a2], p1 = MA0[a], p2 = MA0[a2];
-                        const int64_t q1 = MA1[a], q2 = MA1[a2];
-                        const int m1 = MOE[a], m2 = MOE[a2];
-                        const int64_t c1 = CM ? CM[a] : 0, c2 = CM ? CM[a2] : 0;
-                        test(a, w1, p1, q1, m1, c1);
-                        test(a2, w2, p2, q2, m2, c2);
-                        if (__builtin_amdgcn_ballot_w64(open) == 0) break;
-                        a = a2 < aend ? a2 + 1 : a2;   // stays inside the window
-                    }
-                    if (act) {
-                        AMq[off_s + k] = (uint8_t)amin;
-                        AMq[sumwd + off_s + k] = (uint8_t)a0;
-                    }
+            // One (segment, stage, b) entry a lane, the entries of all segments and stages
+            // spread over the lanes at once.
+            auto scan_entry = [&](bool act, int q, int s, int k, int lo_s, int hi_s, int blo_s, int off_s, int plo,
+                                  int phi, int64_t cap_s, const int64_t *CM, int64_t hc_b) {
+                const int vs = sel4(vq, q);
+                const int64_t ms = (int64_t)((PP - s) < vs ? (PP - s) : vs);   // 1F1B stored micro-batches
+                uint8_t *const AMq = REG + q * arr_bytes;
+                const int b = blo_s + k;
+                const int ahi = (b - lo_s) < phi ? (b - lo_s) : phi;
+                const int alo = (b - hi_s) > plo ? (b - hi_s) : plo;
+                const bool has = act && ahi >= alo;
+                // the feasible split points form a suffix [amin, ahi] of the window
+                // (memory and pruning 3 only grow with the segment), and so do those
+                // feasible without recomputation, [a0, ahi]: scanning a upwards, the
+                // first hit of each is its bound, and a lane is done at its first
+                // split point that fits without recomputation
+                int amin = has ? ahi + 1 : 255, a0 = amin;
+                const int64_t wb = MW[b], a0b = MA0[b], a1b = MA1[b];
+                const int mb = MOE[b];
+                const int64_t cmb = CM ? CM[b] : 0;
+                const int aend = has ? ahi : plo;
+                bool open = has;
+                // one split point's test, gated by the lane still being open
+                auto test = [&](int a, int64_t mwa, int64_t ma0, int64_t ma1, int moea, int64_t cma) {
+                    const int64_t xb = (mb - moea) > 0 ? X : 0;
+                    const int64_t base = wb - mwa + xb;
+                    const bool ok3 = !prune_het | (cmb - cma + hc_b <= eta_tbar);
+                    const bool f0 = open & ok3 & (base + ms * (a0b - ma0) <= cap_s);
+                    const bool f1 = open & ok3 & recomp & (base + ms * (a1b - ma1) <= cap_s);
+                    if (STATS) add4(evq, q, open ? 1 : 0);
+                    amin = ((f0 | f1) & (a < amin)) ? a : amin;
+                    a0 = f0 ? a : a0;
+                    open = open & !f0 & (a < aend);
+                };
+                // two split points per trip, all loads issued before either test
+                int a = has ? alo : plo;
+                for (;;) {   // a lane closes at aend at the latest
+                    const int a2 = a < aend ? a + 1 : a;
+                    const int64_t w1 = MW[a], w2 = MW[a2], p1 = MA0[a], p2 = MA0[a2];
+                    const int64_t q1 = MA1[a], q2 = MA1[a2];
+                    const int m1 = MOE[a], m2 = MOE[a2];
+                    const int64_t c1 = CM ? CM[a] : 0, c2 = CM ? CM[a2] : 0;
+                    test(a, w1, p1, q1, m1, c1);
+                    test(a2, w2, p2, q2, m2, c2);
+                    if (__builtin_amdgcn_ballot_w64(open) == 0) break;
+                    a = a2 < aend ? a2 + 1 : a2;   // stays inside the window
                 }
+                if (act) {
+                    AMq[off_s + k] = (uint8_t)amin;
+                    AMq[sumwd + off_s + k] = (uint8_t)a0;
+                }
+            };
+            const int total = nact * sumwd;
+            for (int e0 = 0; e0 < total; e0 += 64) {   // wave-uniform
+                const int e = e0 + lane;
+                const bool act = e < total;
+                const int ee = act ? e : 0;
+                const int q = ee / sumwd, ke = ee - q * sumwd;
+                const int st = stage_of(ke);
+                const StageP P = stage_p(st);
+                const int64_t *CM = P.mixed ? time + ((int64_t)(P.mask - 1) * 3 + 2) * np : nullptr;
+                scan_entry(act, q, st, ke - P.off, P.lo, P.hi, P.blo, P.off, P.plo, P.phi, P.cap, CM,
+                           P.bdiff ? P.p2p : 0);
             }
             wave_sync();
 
