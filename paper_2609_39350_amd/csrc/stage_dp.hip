@@ -128,16 +128,22 @@ __host__ __device__ inline int mem_bytes(int n_layers)
 DpLds dp_lds(int n_layers, int kmax, int ppmax)
 {
     DpLds S;
-    S.np = (n_layers + 1 + 15) & ~15;
+    S.np = n_layers + 1;
     S.kmax = kmax;
     S.ppmax = ppmax;
-    const int w = n_layers + 1;
     S.off_region = kmax * S.np * 16;
-    // one segment always fits: every stage band is at most N + 1 wide; the
-    // memory prefix sums share the space of the DP rows (they are only read
-    // before the first DP pass of a batch)
-    const int rows = 2 * align16(w * 16), mb = mem_bytes(n_layers);
-    S.region = align16(3 * ppmax * w) + (rows > mb ? rows : mb) + 64;
+    // one segment of any key always fits: every stage holds at least one
+    // layer, so each of the PP stage bands of end layers is at most N - PP + 1
+    // wide; the memory prefix sums share the space of the DP rows (they are
+    // only read before the first DP pass of a batch)
+    const int mb = mem_bytes(n_layers);
+    int need = 0;
+    for (int pp = 1; pp <= ppmax && pp <= n_layers; ++pp) {
+        const int wmax = n_layers - pp + 1, rows = 2 * align16(wmax * 16);
+        const int n = align16(3 * pp * wmax) + (rows > mb ? rows : mb);
+        need = n > need ? n : need;
+    }
+    S.region = need + 64;
     S.off_ctl = S.off_region + S.region;
     S.total = S.off_ctl + kMaxSeg * (int)sizeof(SegCtl);
     return S;
