@@ -18,7 +18,12 @@
 // row (t_bot = least possible largest stage), one pass at t_bot, then the
 // descending sweep.  An incumbent is replaced by a lower objective, or by an
 // equal one with a lower largest stage, so the result does not depend on the
-// order of the passes.
+// order of the passes.  A pass at any threshold t returns a genuine Pareto
+// point (the one whose constant range holds t), so the descending sweep of a
+// class can run as two chains side by side in two slots, each covering part of
+// the threshold range: the upper chain starts at the top, the lower one at the
+// middle of what remains, and an idle chain takes over the lower half of the
+// other's range.  The passes of a sweep then run about a third fewer rounds.
 //
 // Work sharing across B: B enters a candidate only through the 1F1B count of
 // stored micro-batches min(PP - i, B) (memory) and the (B-1) weight of the
@@ -53,6 +58,12 @@ constexpr int64_t kNegInf = INT64_MIN;        // a threshold no stage cost meets
 constexpr int kRelaxUnroll = 2;   // split points per relaxation-loop trip
 constexpr int kMaxSeg = 4;
 constexpr int kParallelTrace = 4;    // pipelines at least this deep back-trace in two phases
+// Threshold sweeps give every class up to kMaxChains slots (chains) while the
+// batch has room for them and the slots' entries of the widest stage band take at
+// most kChainEntries lanes.  A third chain saves passes but costs more per pass
+// (a second round of entries and of back-trace work on deep pipelines).
+constexpr int kMaxChains = 2;
+constexpr int kChainEntries = 128;
 
 // Optional section clocks (built with -DHAPMOE_SECTION_CLOCKS into a separate
 // library): every wave accumulates the shader-clock cycles it spends in each
@@ -115,6 +126,10 @@ struct SegCtl {
     int64_t pF, pM, pfwd;
     int32_t ps0, prmask, pok, pad2;
     uint32_t pbt[8];
+    // threshold sweep: the chain of passes this slot runs -- the sum of its last
+    // pass (a lower bound for every lower threshold), the next threshold it
+    // needs, and the threshold it stops above (the next chain covers the rest)
+    int64_t cF, ct, cs;
 };
 
 
@@ -594,7 +609,20 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
         for (int g0 = 0; g0 < ng; g0 += smax) {
             HAPMOE_COUNT(kCountBatches);
             const int nact = (ng - g0) < smax ? (ng - g0) : smax;
-            const int nseg = nact <= 1 ? 1 : (nact <= 2 ? 2 : 4);
+            // threshold sweeps: with room for it, class q also runs in the slots
+            // q + nact, q + 2 nact, ..., each sweeping a part of the class's
+            // threshold range (chains, below)
+            int nchain = 1;
+            if (!EXACT)
+                while (nchain < kMaxChains && (nchain + 1) * nact <= smax && (nchain + 1) * nact <= kMaxSeg &&
+                       (nchain + 1) * nact * maxw <= kChainEntries)
+                    ++nchain;
+            const int nslot = nchain * nact;
+            // class of every slot, 2 bits a slot
+            int cmap = 0;
+#pragma unroll
+            for (int q = 0; q < kMaxSeg; ++q) cmap |= (q % (nact > 0 ? nact : 1)) << (2 * q);
+            const int nseg = nslot <= 1 ? 1 : (nslot <= 2 ? 2 : 4);
             const int W = 64 / nseg;
             const int sg = lane / W, ll = lane % W;   // DP view: segment and lane in segment
             // class value (its smallest group value) of every segment of the batch
@@ -610,11 +638,13 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                     }
                 }
             }
-            const bool seg_live = sg < nact;
+            const bool seg_live = sg < nslot;
             const int segi = seg_live ? sg : 0;
-            uint8_t *AMIN = REG + segi * arr_bytes;
+            // a slot reads the feasible intervals of its class and keeps its own
+            // back-trace pointers and DP rows
+            uint8_t *AMIN = REG + ((cmap >> (2 * segi)) & 3) * arr_bytes;
             uint8_t *A0B = AMIN + sumwd;
-            uint8_t *ARG = AMIN + 2 * sumwd;
+            uint8_t *ARG = REG + segi * arr_bytes + 2 * sumwd;
             unsigned char *RW = REG + off_rows + segi * row_bytes;
             int64_t *const FM0 = reinterpret_cast<int64_t *>(RW);
             int64_t *const FM1 = reinterpret_cast<int64_t *>(RW + row_bytes / 2);
@@ -717,7 +747,11 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                 HAPMOE_CLOCK(kClockControl);
                 HAPMOE_COUNT(kCountPasses);
                 const bool on = seg_live && CTL[sg].on != 0;
-                if (on) ++passes;
+                if (STATS && sj >= 0) {
+                    bool ran = false;
+                    for (int k = 0; k < nchain; ++k) ran |= CTL[sj + k * nact].on != 0;
+                    if (ran) ++passes;
+                }
                 if (on && ll == 0) {   // stage -1: layer 0 reached at cost 0
                     if (fused)
                         FG1[0] = I64x2{0, 0};
@@ -756,7 +790,8 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                         if (nq > 1) split_entry(k, wd_s, inv_wd, qi, k);   // wave-uniform branch
                         const int q = (qmap >> (2 * qi)) & 3;
                         const int64_t t = CTL[q].t;
-                        uint8_t *const AMq = REG + q * arr_bytes;
+                        const uint8_t *const AMq = REG + ((cmap >> (2 * q)) & 3) * arr_bytes;   // class
+                        uint8_t *const ARq = REG + q * arr_bytes + 2 * sumwd;                   // slot
                         unsigned char *const RWq = REG + off_rows + q * row_bytes;
                         const int64_t *Fp = reinterpret_cast<const int64_t *>(RWq + poff);
                         int64_t *Fc = reinterpret_cast<int64_t *>(RWq + coff);
@@ -824,7 +859,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                                 Gc[k] = I64x2{best, gbest};
                             else
                                 Fc[k] = best;
-                            AMq[2 * sumwd + off_s + k] = (uint8_t)ba;
+                            ARq[off_s + k] = (uint8_t)ba;
                         }
                     }
                     wave_sync();
@@ -882,7 +917,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                         const bool act = e < nent;
                         const int q = act ? e / PP : 0, s = act ? e % PP : 0;
                         // only segments that ran this pass (the others keep their last trace)
-                        const bool valid = act && q < nact && CTL[q].on != 0 && CTL[q].ok != 0;
+                        const bool valid = act && q < nslot && CTL[q].on != 0 && CTL[q].ok != 0;
                         const int p1 = __shfl(pk1, s, 64), p2 = __shfl(pk2, s, 64);
                         const int plo = __shfl((int)(uint32_t)(uint64_t)p2p, s, 64);
                         const int phi = __shfl((int)(uint32_t)((uint64_t)p2p >> 32), s, 64);
@@ -893,7 +928,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                         const int wdn = p2 >> 16;
                         int k = b - (p1 & 0xff);
                         k = k < 0 ? 0 : (k >= wdn ? wdn - 1 : k);
-                        const int a0 = (REG + q * arr_bytes + sumwd)[(p2 & 0xffff) + k];
+                        const int a0 = (REG + ((cmap >> (2 * q)) & 3) * arr_bytes + sumwd)[(p2 & 0xffff) + k];
                         const I64x2 *T = TM + ((p1 >> 24) & 0xff) * NP;
                         const I64x2 ta = T[a], tb = T[b];   // negated prefix sums
                         const bool r1 = a < a0;
@@ -1000,14 +1035,15 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
             // objectives the lower largest stage (the least threshold reaching the
             // optimum), whatever order the passes ran in; equal (objective, M)
             // points share the partition of threshold M
-            auto take = [&](int64_t Fx, int64_t Mx) {
+            auto take = [&](int slot) {
+                const int64_t Fx = CTL[slot].F, Mx = CTL[slot].M;
                 const int64_t sc = Fx + Bm * Mx;
                 if (sc < bs || (sc == bs && Mx < bmx)) {
                     bs = sc;
                     bmx = Mx;
-                    for (int w = 0; w < 8; ++w) pw[w] = CTL[sj].bt[w];
-                    prm = CTL[sj].rmask;
-                    pok = CTL[sj].ok;
+                    for (int w = 0; w < 8; ++w) pw[w] = CTL[slot].bt[w];
+                    prm = CTL[slot].rmask;
+                    pok = CTL[slot].ok;
                 }
             };
 
@@ -1118,57 +1154,158 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                 F1 = CTL[sj].F;
                 M1 = CTL[sj].M;
                 bs = kInf;
-                take(F1, M1);
+                take(sj);
             }
-            int64_t F = F1, tcur = M1 - 1;
+            // lanes of segments where t_bot >= M1 are already final
+            const bool sweeping = !EXACT && member && tbot < M1;
+            // Chains of the descending sweep.  A chain runs passes at the largest
+            // threshold some candidate of its class still needs, min(lim, ct): below
+            // ct = (last largest stage) - 1 the sum is at least cF, so thresholds above
+            // lim = (incumbent - cF) / (B - 1) cannot win.  It covers the thresholds
+            // above its stop cs; together the chains of a class cover (t_bot, M1 - 1].
+            // Chain k of class q runs in slot q + k nact.  The last chain starts at
+            // the top (alongside the pass at t_bot, in slot q); whenever a chain is
+            // idle and another one runs, the idle one takes the lower half of the
+            // widest running range.  Each chain visits every Pareto point of its range
+            // that can still win, and the incumbent rule does not depend on the order,
+            // so the result is that of a single chain.
+            if (!EXACT) {
+                if (lane == 0) {
+                    for (int q = 0; q < nslot; ++q) {
+                        const int c = (cmap >> (2 * q)) & 3;
+                        CTL[q].cF = CTL[c].F;
+                        CTL[q].ct = q >= nslot - nact ? CTL[c].M - 1 : -1;   // -1: idle
+                        CTL[q].cs = CTL[c].G;
+                    }
+                }
+            }
             wave_sync();
+            // this lane's threshold for the chain in a slot of its class (-1: none)
+            auto need = [&](int slot) -> int64_t {
+                const bool done = bmx == tbot && bs == F1 + Bm * tbot;   // reached the lower bound
+                const int64_t cF = CTL[slot].cF, ct = CTL[slot].ct;
+                if (!sweeping || done || cF + Bm * tbot > bs) return -1;
+                const int64_t lim = Bm > 0 ? (bs - cF) / Bm : kBig;
+                return lim < ct ? lim : ct;
+            };
+            // the chains' passes: offer them, and move the chains on
+            auto advance = [&](int from) {
+                if (sweeping)
+                    for (int k = from; k < nchain; ++k)
+                        if (CTL[sj + k * nact].on) take(sj + k * nact);
+                wave_sync();
+                if (lane == 0) {
+                    for (int q = from * nact; q < nslot; ++q) {
+                        if (!CTL[q].on) continue;
+                        CTL[q].cF = CTL[q].F;
+                        CTL[q].ct = CTL[q].M - 1;
+                    }
+                }
+                wave_sync();
+            };
 
-            // ---- 3) the bottleneck threshold itself ----
+            // ---- 3) the bottleneck threshold itself (and the top chain's first pass) ----
             if (!EXACT) {
                 bool any = false;
 #pragma unroll
                 for (int q = 0; q < kMaxSeg; ++q) {
-                    if (q >= nseg) continue;
+                    if (q >= nact) continue;
                     const bool run = segok[q] && segF[q] < CTL[q].M;   // t_bot < M1
                     set_ctl(q, run, segF[q]);
                     any |= run;
+                    if (nchain > 1) {
+                        const int top = q + (nchain - 1) * nact;
+                        const int64_t t1 = wave_max64(sj == q ? need(top) : -1);
+                        const int64_t tb = wave_max64(sj == q && sweeping ? tbot : -1);
+                        const bool run1 = t1 > tb;
+                        set_ctl(top, run1, t1);
+                        any |= run1;
+                    }
                 }
                 wave_sync();
                 if (any) {
                     pass(false);
-                    if (member && CTL[sj].on) take(CTL[sj].F, CTL[sj].M);
+                    if (member && CTL[sj].on) take(sj);   // the t_bot pass is no chain's
+                    if (nchain > 1) advance(1);
                 }
                 wave_sync();
             }
-            // lanes of segments where t_bot >= M1 are already final
-            const bool sweeping = !EXACT && member && tbot < M1;
 
             // ---- 4) descending Pareto sweep ----
             while (!EXACT) {
-                const bool done = bmx == tbot && bs == F1 + Bm * tbot;   // reached the lower bound
-                const bool act = sweeping && !done && F + Bm * tbot <= bs;
-                const int64_t lim = act ? (Bm > 0 ? (bs - F) / Bm : kBig) : -1;
-                const int64_t mine = lim < tcur ? lim : tcur;
                 bool any = false;
 #pragma unroll
                 for (int q = 0; q < kMaxSeg; ++q) {
-                    if (q >= nseg) continue;
-                    const int64_t tn = wave_max64(sj == q && act ? mine : -1);
-                    const int64_t tb = wave_max64(sj == q && act ? tbot : -1);
-                    const bool run = tn >= 0 && tn > tb;
-                    set_ctl(q, run, tn);
-                    any |= run;
+                    if (q >= nact) continue;
+                    const int64_t tb = wave_max64(sj == q && sweeping ? tbot : -1);
+                    // every chain's threshold and the bound it runs above (wave-uniform)
+                    int64_t tk[kMaxSeg], lk[kMaxSeg];
+#pragma unroll
+                    for (int k = 0; k < kMaxSeg; ++k) {
+                        tk[k] = -1;
+                        lk[k] = 0;
+                        if (k >= nchain) continue;
+                        const int slot = q + k * nact;
+                        tk[k] = wave_max64(sj == q ? need(slot) : -1);
+                        lk[k] = CTL[slot].cs > tb ? CTL[slot].cs : tb;
+                    }
+                    // idle chains take the lower half of the widest running range
+                    for (int it = 1; it < nchain; ++it) {
+                        int x = -1, y = -1;
+                        int64_t wx = 1;
+#pragma unroll
+                        for (int k = 0; k < kMaxSeg; ++k) {
+                            if (k >= nchain) continue;
+                            if (tk[k] > lk[k]) {
+                                if (tk[k] - lk[k] > wx) {
+                                    wx = tk[k] - lk[k];
+                                    x = k;
+                                }
+                            } else if (y < 0) {
+                                y = k;
+                            }
+                        }
+                        if (x < 0 || y < 0) break;   // wave-uniform
+                        int64_t tx = 0, lx = 0;
+#pragma unroll
+                        for (int k = 0; k < kMaxSeg; ++k)
+                            if (k == x) {
+                                tx = tk[k];
+                                lx = lk[k];
+                            }
+                        // the new chain starts at mid with x's sum: its lanes' thresholds
+                        // are min(theirs for x, mid), whose largest is mid
+                        const int64_t mid = lx + (tx - lx) / 2;
+                        const int sx = q + x * nact, sy = q + y * nact;
+                        const int64_t xF = CTL[sx].cF, xs = CTL[sx].cs;
+                        wave_sync();
+                        if (lane == 0) {
+                            CTL[sy].cF = xF;
+                            CTL[sy].ct = mid;
+                            CTL[sy].cs = xs;
+                            CTL[sx].cs = mid;
+                        }
+#pragma unroll
+                        for (int k = 0; k < kMaxSeg; ++k) {
+                            if (k == y) {
+                                tk[k] = mid;
+                                lk[k] = lx;
+                            }
+                            if (k == x) lk[k] = mid;
+                        }
+                    }
+#pragma unroll
+                    for (int k = 0; k < kMaxSeg; ++k) {
+                        if (k >= nchain) continue;
+                        const bool r = tk[k] > lk[k];
+                        set_ctl(q + k * nact, r, tk[k]);
+                        any |= r;
+                    }
                 }
                 wave_sync();
                 if (!any) break;
                 pass(false);
-                if (sweeping && CTL[sj].on) {
-                    const int64_t Fc = CTL[sj].F, Mc = CTL[sj].M;
-                    take(Fc, Mc);
-                    F = Fc;
-                    tcur = Mc - 1;
-                }
-                wave_sync();
+                advance(0);
             }
 
             // ---- 5) results ----
@@ -1180,10 +1317,11 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
             }
 
             if (STATS) {
-                // per segment: passes, relaxations, split-point evaluations and the
-                // lane slots the relaxation loops issued while the segment took part;
-                // the shared work is counted once, on the group's first candidate in range
-                int rq[kMaxSeg] = {0, 0, 0, 0}, eq[kMaxSeg] = {0, 0, 0, 0}, pq[kMaxSeg] = {0, 0, 0, 0};
+                // per class: the passes its candidates took part in (rounds, counted
+                // once when both of its slots ran), and the relaxations, split-point
+                // evaluations and lane slots of the relaxation loops of its slots; the
+                // shared work is counted once, on the class's first candidate in range
+                int rq[kMaxSeg] = {0, 0, 0, 0}, eq[kMaxSeg] = {0, 0, 0, 0};
                 int sq[kMaxSeg] = {0, 0, 0, 0};
                 int lead[kMaxSeg] = {-1, -1, -1, -1};
     #pragma unroll
@@ -1192,11 +1330,18 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                     rq[q] = wave_sum32(relq[q]);
                     eq[q] = wave_sum32(evq[q]);
                     sq[q] = wave_sum32(slq[q]);
-                    pq[q] = wave_max32(sg == q ? passes : 0);
                     lead[q] = __ffsll((unsigned long long)__ballot(inr && sj == q)) - 1;
                 }
+    #pragma unroll
+                for (int q = 0; q < kMaxSeg; ++q) {
+                    if (q >= nact) continue;
+                    for (int k = 1; k < nchain; ++k) {
+                        rq[q] += sel4(rq, q + k * nact);
+                        sq[q] += sel4(sq, q + k * nact);
+                    }
+                }
                 if (inr && sj >= 0) {
-                    const int p = sj == 0 ? pq[0] : sj == 1 ? pq[1] : sj == 2 ? pq[2] : pq[3];
+                    const int p = passes;
                     const int r = sj == 0 ? rq[0] : sj == 1 ? rq[1] : sj == 2 ? rq[2] : rq[3];
                     const int e = sj == 0 ? eq[0] : sj == 1 ? eq[1] : sj == 2 ? eq[2] : eq[3];
                     const int l = sj == 0 ? lead[0] : sj == 1 ? lead[1] : sj == 2 ? lead[2] : lead[3];
