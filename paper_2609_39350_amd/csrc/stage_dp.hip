@@ -301,6 +301,17 @@ __device__ inline void split_entry(int e, int wd, float inv_wd, int &q, int &k)
 
 // Per-segment values held in registers, selected / updated without dynamic
 // register indexing.
+// floor(x / d) for x >= 0, d > 0: below 2^52 through the correctly rounded
+// double quotient, whose truncation is the floor or one more than it
+__device__ inline int64_t div_nonneg(int64_t x, int64_t d)
+{
+    if (x < (int64_t(1) << 52)) {
+        const int64_t q = (int64_t)((double)x / (double)d);
+        return q * d > x ? q - 1 : q;
+    }
+    return x / d;
+}
+
 __device__ inline int sel4(const int (&v)[4], int q)
 {
     return q == 0 ? v[0] : q == 1 ? v[1] : q == 2 ? v[2] : v[3];
@@ -1185,7 +1196,8 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                 const bool done = bmx == tbot && bs == F1 + Bm * tbot;   // reached the lower bound
                 const int64_t cF = CTL[slot].cF, ct = CTL[slot].ct;
                 if (!sweeping || done || cF + Bm * tbot > bs) return -1;
-                const int64_t lim = Bm > 0 ? (bs - cF) / Bm : kBig;
+                if (Bm == 0 || cF + Bm * ct <= bs) return ct;   // ct binds: no division
+                const int64_t lim = div_nonneg(bs - cF, Bm);
                 return lim < ct ? lim : ct;
             };
             // the chains' passes: offer them, and move the chains on
@@ -1234,6 +1246,10 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
             // ---- 4) descending Pareto sweep ----
             while (!EXACT) {
                 bool any = false;
+                // this lane's thresholds for the chains of its class
+                int64_t nk[kMaxChains];
+#pragma unroll
+                for (int k = 0; k < kMaxChains; ++k) nk[k] = (sweeping && k < nchain) ? need(sj + k * nact) : -1;
 #pragma unroll
                 for (int q = 0; q < kMaxSeg; ++q) {
                     if (q >= nact) continue;
@@ -1244,9 +1260,9 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                     for (int k = 0; k < kMaxSeg; ++k) {
                         tk[k] = -1;
                         lk[k] = 0;
-                        if (k >= nchain) continue;
+                        if (k >= nchain || k >= kMaxChains) continue;
                         const int slot = q + k * nact;
-                        tk[k] = wave_max64(sj == q ? need(slot) : -1);
+                        tk[k] = wave_max64(sj == q ? nk[k] : -1);
                         lk[k] = CTL[slot].cs > tb ? CTL[slot].cs : tb;
                     }
                     // idle chains take the lower half of the widest running range
