@@ -918,12 +918,13 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                         }
                     }
                     wave_sync();
-                    const int nent = nseg * PP;   // <= 4 * 32: two rounds at most
+                    const int nent = nslot * PP;   // <= 4 * 32: two rounds at most
                     int64_t ce[2] = {0, 0};
                     int qe[2] = {0, 0}, se[2] = {0, 0};
                     bool ve[2] = {false, false};
 #pragma unroll
                     for (int r = 0; r < 2; ++r) {
+                        if (r * 64 >= nent) break;   // wave-uniform
                         const int e = r * 64 + lane;
                         const bool act = e < nent;
                         const int q = act ? e / PP : 0, s = act ? e % PP : 0;
