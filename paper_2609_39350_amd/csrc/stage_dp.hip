@@ -394,12 +394,13 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
         HAPMOE_CLOCK_RESTART();
         uint32_t qi = 0;
         if (lane == 0) qi = atomicAdd(queue, 1u);
-        qi = __shfl(qi, 0, 64);
+        // wave-uniform from here on: everything indexed by the key stays scalar
+        qi = (uint32_t)__builtin_amdgcn_readlane((int)qi, 0);
         if ((int64_t)qi >= n_keys) break;   // every wave exits once the queue is drained
         const int64_t key = key_lo + n_keys - 1 - (int64_t)qi;   // keys are PP-ascending: biggest work first
         const int64_t cfg = key / H.n_orders;
         const int64_t idx0 = key * nB;
-        const int PP = cand[idx0].pp;
+        const int PP = __builtin_amdgcn_readfirstlane(cand[idx0].pp);
         const PiInfo *pi = reinterpret_cast<const PiInfo *>(tab + L.off_pi) + cfg;
         const KeyInfo *ki = reinterpret_cast<const KeyInfo *>(tab + L.off_key) + key;
 
