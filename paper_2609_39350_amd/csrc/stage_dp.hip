@@ -390,6 +390,9 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
     SegCtl *CTL = reinterpret_cast<SegCtl *>(smem + S.off_ctl);
 
     HAPMOE_CLOCK_VARS;
+    // Keys come off the queue largest first, one at a time: fetching the next
+    // key's index early (to hide the atomic's latency) binds a wave to it too
+    // soon and costs more in balance than it saves, at every depth measured.
     for (;;) {
         HAPMOE_CLOCK_RESTART();
         uint32_t qi = 0;
@@ -662,14 +665,17 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
             int64_t *const FM1 = reinterpret_cast<int64_t *>(RW + row_bytes / 2);
             I64x2 *const FG0 = reinterpret_cast<I64x2 *>(RW);   // fused pass: {sum, min-max}
             I64x2 *const FG1 = reinterpret_cast<I64x2 *>(RW + row_bytes / 2);
-            // memory prefix sums for the feasibility scan (they share the DP-row space)
-            for (int b = lane; b <= N; b += 64) {
-                MW[b] = mem[b];
-                MA0[b] = mem[np + b];
-                MA1[b] = mem[2 * np + b];
-                MOE[b] = (int32_t)mem[3 * np + b];
+            // memory prefix sums for the feasibility scan (they share the DP-row space;
+            // the first batch finds them there from the class split)
+            if (g0 > 0) {
+                for (int b = lane; b <= N; b += 64) {
+                    MW[b] = mem[b];
+                    MA0[b] = mem[np + b];
+                    MA1[b] = mem[2 * np + b];
+                    MOE[b] = (int32_t)mem[3 * np + b];
+                }
+                wave_sync();
             }
-            wave_sync();
             // candidate view: lane j's segment in this batch (-1: not in this batch)
             const int sj = (gj >= g0 && gj < g0 + nact) ? gj - g0 : -1;
             bool member = inr && sj >= 0;

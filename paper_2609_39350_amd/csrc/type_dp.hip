@@ -159,13 +159,14 @@ __global__ __launch_bounds__(kThreads) void k_type_dp(const unsigned char *__res
     for (;;) {
         if (tid == 0) C.qi = atomicAdd(queue, 1u);
         __syncthreads();
-        const uint32_t qi = C.qi;
+        // wave-uniform: everything indexed by the key stays scalar
+        const uint32_t qi = (uint32_t)__builtin_amdgcn_readfirstlane((int)C.qi);
         __syncthreads();
         if ((int64_t)qi >= n_keys) break;   // every workgroup exits once the queue is drained
         const int64_t key = key_lo + n_keys - 1 - (int64_t)qi;   // one key per configuration, PP-ascending
         const int64_t idx0 = key * nB;
         if (idx0 + nB <= first || idx0 >= first + count) continue;
-        const int PP = cand[idx0].pp;
+        const int PP = __builtin_amdgcn_readfirstlane(cand[idx0].pp);
         const PiInfo *pi = reinterpret_cast<const PiInfo *>(tab + L.off_pi) + key;
         const KeyInfo *ki = reinterpret_cast<const KeyInfo *>(tab + L.off_key) + key;
 
