@@ -223,6 +223,9 @@ int32_t hapmoe_debug_bytes(const hapmoe_problem *p, int64_t *bytes);
  *        without / with recomputation and of its communication part, for the
  *        device-type set m at index m - 1 (only sets some stage uses are
  *        written).
+ *   then, 256-byte aligned after time, [N] double: every layer's
+ *        load-imbalance factor 1 + gamma (rho - 1) (1 for dense layers),
+ *        written once per call before the per-configuration tables.
  * Debug buffer (fp64, per configuration, out[0..3] = doubles per
  * configuration, offsets of the type, set and memory blocks):
  *   type [N][T][2] (Eq. 2 compute, expert), set [n_masks][N][3] (all-to-all,

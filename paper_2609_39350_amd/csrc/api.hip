@@ -442,7 +442,8 @@ int32_t hapmoe_eval_cost_tables(const hapmoe_problem *p, const void *d_image, co
     const DebugLayout D = debug_layout(p->cluster.n_types, p->model.n_layers);
     if (d_debug && debug_bytes < (int64_t)S.cfg.size() * D.per_cfg * 8) return HAPMOE_E_WORKSPACE;
     if (const int e = check_arch()) return e;
-    if (launch_cost_tables(d_image, d_cand, per, L, d_tables, d_debug, D, (hipStream_t)stream) != hipSuccess)
+    if (launch_cost_tables(d_image, d_cand, per, p->model.n_layers, L, d_tables, d_debug, D, (hipStream_t)stream) !=
+        hipSuccess)
         return HAPMOE_E_HIP;
     return HAPMOE_OK;
 }

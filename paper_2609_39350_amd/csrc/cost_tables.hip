@@ -86,6 +86,45 @@ __device__ inline int64_t wave_max(int64_t x)
     return x;
 }
 
+// Load-imbalance factor of every layer (Section 3.2, router skew): one block a
+// layer, rho = max / mean token count over its experts.  It depends on the
+// model only, so it is computed once per launch, not once per configuration.
+__global__ __launch_bounds__(kThreads) void k_layer_skew(const unsigned char *__restrict__ img, TablesLayout L,
+                                                         unsigned char *__restrict__ tab)
+{
+    const ImageHeader &H = *reinterpret_cast<const ImageHeader *>(img);
+    const uint8_t *is_moe = img + H.off_is_moe;
+    const int64_t *tokens = reinterpret_cast<const int64_t *>(img + H.off_tokens);
+    const int l = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int E = H.n_experts;
+    __shared__ int64_t s_sum[kThreads / 64], s_max[kThreads / 64];
+    double sk = 1.0;
+    if (is_moe[l]) {   // block-uniform
+        int64_t sum = 0, mx = 0;
+        for (int e = tid; e < E; e += kThreads) {
+            const int64_t v = tokens[(int64_t)l * E + e];
+            sum += v;
+            mx = v > mx ? v : mx;
+        }
+        sum = wave_sum(sum);
+        mx = wave_max(mx);
+        if (lane == 0) {
+            s_sum[wave] = sum;
+            s_max[wave] = mx;
+        }
+        __syncthreads();
+        if (tid == 0) {
+            for (int w = 1; w < kThreads / 64; ++w) {
+                sum += s_sum[w];
+                mx = s_max[w] > mx ? s_max[w] : mx;
+            }
+            const double rho = sum > 0 ? (double)(mx * E) / (double)sum : 1.0;
+            sk = 1.0 + H.gamma * (rho - 1.0);
+        }
+    }
+    if (tid == 0) reinterpret_cast<double *>(tab + L.off_layer)[l] = sk;
+}
+
 __global__ __launch_bounds__(kThreads) void k_cost_tables(const unsigned char *__restrict__ img,
                                                           const hapmoe_candidate *__restrict__ cand,
                                                           int64_t per_config, TablesLayout L,
@@ -94,7 +133,6 @@ __global__ __launch_bounds__(kThreads) void k_cost_tables(const unsigned char *_
 {
     const ImageHeader &H = *reinterpret_cast<const ImageHeader *>(img);
     const uint8_t *is_moe = img + H.off_is_moe;
-    const int64_t *tokens = reinterpret_cast<const int64_t *>(img + H.off_tokens);
     const int64_t *pdense = reinterpret_cast<const int64_t *>(img + H.off_pdense);
     const int64_t *pexp = reinterpret_cast<const int64_t *>(img + H.off_pexp);
     const int64_t *act = reinterpret_cast<const int64_t *>(img + H.off_act);
@@ -104,12 +142,13 @@ __global__ __launch_bounds__(kThreads) void k_cost_tables(const unsigned char *_
     const int64_t cfg = blockIdx.x;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const hapmoe_candidate c = cand[cfg * per_config];
-    const int N = H.n_layers, T = H.n_types, E = H.n_experts;
+    const int N = H.n_layers, T = H.n_types;
     double *dcfg = dbg ? dbg + cfg * D.per_cfg : nullptr;
 
     __shared__ int64_t s_qce[kMaxTypes][kLayerSlots];   // q(comp) + q(expert) per type, layer
     __shared__ int64_t s_maxce[kLayerSlots];
     __shared__ double s_skew[kLayerSlots];
+    __shared__ double s_link_a[1 << kMaxTypes], s_link_b[1 << kMaxTypes];   // per device-type set
     __shared__ int64_t s_w[kLayerSlots], s_a0[kLayerSlots], s_a1[kLayerSlots];
     __shared__ double s_pavg;
     __shared__ unsigned s_used, s_flag;
@@ -137,24 +176,10 @@ __global__ __launch_bounds__(kThreads) void k_cost_tables(const unsigned char *_
         pe = wave_sum(pe);
         if (lane == 0) s_pavg = ((double)pd / (double)c.tp + (double)pe / (double)(c.ep * c.tpe)) / (double)c.pp;
     }
-    // load-imbalance factor 1 + gamma (rho - 1), rho = max / mean tokens over the
-    // experts of a MoE layer: each wave takes every fourth layer, lanes over experts
-    for (int l = wave; l < N; l += kThreads / 64) {
-        double sk = 1.0;
-        if (is_moe[l]) {   // wave-uniform
-            int64_t sum = 0, mx = 0;
-            for (int e = lane; e < E; e += 64) {
-                const int64_t v = tokens[(int64_t)l * E + e];
-                sum += v;
-                mx = v > mx ? v : mx;
-            }
-            sum = wave_sum(sum);
-            mx = wave_max(mx);
-            const double rho = sum > 0 ? (double)(mx * E) / (double)sum : 1.0;
-            sk = 1.0 + H.gamma * (rho - 1.0);
-        }
-        if (lane == 0) s_skew[l] = sk;
-    }
+    // load-imbalance factors (k_layer_skew) and the slowest link of every
+    // device-type set
+    for (int l = tid; l < N; l += kThreads) s_skew[l] = reinterpret_cast<const double *>(tab + L.off_layer)[l];
+    if (tid >= 1 && tid < (1 << T)) set_link(H, tid, s_link_a[tid], s_link_b[tid]);
     __syncthreads();
 
     // ---- stage layout of the block orderings: (ordering, stage) pairs over the threads ----
@@ -197,8 +222,8 @@ __global__ __launch_bounds__(kThreads) void k_cost_tables(const unsigned char *_
             double al_k = 0.0, bw_k = 0.0;
             for (int s = 0; s < PP; ++s) {
                 sum_speed += s_ospd[o][s];
-                double a, b;
-                set_link(H, s_omask[o][s], a, b);
+                const int m = s_omask[o][s];
+                const double a = s_link_a[m], b = s_link_b[m];
                 if (s == 0 || a > al_k) al_k = a;
                 if (s == 0 || b < bw_k) bw_k = b;
             }
@@ -477,10 +502,12 @@ __global__ __launch_bounds__(kThreads) void k_cost_tables(const unsigned char *_
 namespace hapmoe {
 
 hipError_t launch_cost_tables(const void *d_image, const hapmoe_candidate *d_cand, int64_t per_config,
-                              const TablesLayout &L, void *d_tables, double *d_debug,
+                              int n_layers, const TablesLayout &L, void *d_tables, double *d_debug,
                               const DebugLayout &D, hipStream_t s)
 {
     if (L.n_configs == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_layer_skew, dim3((unsigned)n_layers), dim3(kThreads), 0, s,
+                       static_cast<const unsigned char *>(d_image), L, static_cast<unsigned char *>(d_tables));
     hipLaunchKernelGGL(k_cost_tables, dim3((unsigned)L.n_configs), dim3(kThreads), 0, s,
                        static_cast<const unsigned char *>(d_image), d_cand, per_config, L,
                        static_cast<unsigned char *>(d_tables), d_debug, D);

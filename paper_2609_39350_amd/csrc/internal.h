@@ -67,9 +67,10 @@ struct KeyInfo {
 //   key  [n_configs * n_orders] KeyInfo
 //   mem  [n_configs][4][np] int64   W, A0, A1 prefix sums and MoE-layer count
 //   time [n_configs][n_masks][3][np] int64   T0, T1, comm prefix sums
+//   layer [N] double   load-imbalance factor 1 + gamma (rho - 1) of every layer
 struct TablesLayout {
     int64_t n_configs, n_orders, n_masks, np;
-    int64_t off_pi, off_key, off_mem, off_time, total;
+    int64_t off_pi, off_key, off_mem, off_time, off_layer, total;
 };
 
 // fp64 debug buffer: per configuration
@@ -96,7 +97,8 @@ inline TablesLayout tables_layout(int64_t n_configs, int n_orders, int n_types, 
     L.off_key = align256(L.off_pi + n_configs * (int64_t)sizeof(PiInfo));
     L.off_mem = align256(L.off_key + n_configs * n_orders * (int64_t)sizeof(KeyInfo));
     L.off_time = align256(L.off_mem + n_configs * 4 * L.np * 8);
-    L.total = align256(L.off_time + n_configs * L.n_masks * 3 * L.np * 8);
+    L.off_layer = align256(L.off_time + n_configs * L.n_masks * 3 * L.np * 8);
+    L.total = align256(L.off_layer + (int64_t)n_layers * 8);
     return L;
 }
 
@@ -113,7 +115,7 @@ inline DebugLayout debug_layout(int n_types, int n_layers)
 
 // Kernel launchers (stream = hipStream_t).
 hipError_t launch_cost_tables(const void *d_image, const hapmoe_candidate *d_cand, int64_t per_config,
-                              const TablesLayout &L, void *d_tables, double *d_debug,
+                              int n_layers, const TablesLayout &L, void *d_tables, double *d_debug,
                               const DebugLayout &D, hipStream_t s);
 hipError_t launch_stage_dp(const void *d_image, const hapmoe_candidate *d_cand, int n_layers, int n_micro,
                            const std::vector<int32_t> &config_pp, int n_orders, const TablesLayout &L,
