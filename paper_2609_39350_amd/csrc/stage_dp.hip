@@ -58,7 +58,7 @@ constexpr int64_t kNegInf = INT64_MIN;        // a threshold no stage cost meets
 constexpr int kRelaxUnroll = 2;   // split points per relaxation-loop trip
 constexpr int kMaxSeg = 4;
 constexpr int kParallelTrace = 4;    // pipelines at least this deep back-trace in two phases
-// Threshold sweeps give every class up to kMaxChains slots (chains) while the
+// Sweeps and 1F1B walks give every class up to kMaxChains slots (chains) while the
 // batch has room for them and the slots' entries of the widest stage band take at
 // most kChainEntries lanes.  A third chain saves passes but costs more per pass
 // (a second round of entries and of back-trace work on deep pipelines).
@@ -624,14 +624,13 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
         for (int g0 = 0; g0 < ng; g0 += smax) {
             HAPMOE_COUNT(kCountBatches);
             const int nact = (ng - g0) < smax ? (ng - g0) : smax;
-            // threshold sweeps: with room for it, class q also runs in the slots
-            // q + nact, q + 2 nact, ..., each sweeping a part of the class's
-            // threshold range (chains, below)
+            // with room for it, class q also runs in the slots q + nact, ..., each
+            // covering a part of the class's threshold range (the chains of the
+            // descending sweep and of the 1F1B frontier walk, below)
             int nchain = 1;
-            if (!EXACT)
-                while (nchain < kMaxChains && (nchain + 1) * nact <= smax && (nchain + 1) * nact <= kMaxSeg &&
-                       (nchain + 1) * nact * maxw <= kChainEntries)
-                    ++nchain;
+            while (nchain < kMaxChains && (nchain + 1) * nact <= smax && (nchain + 1) * nact <= kMaxSeg &&
+                   (nchain + 1) * nact * maxw <= kChainEntries)
+                ++nchain;
             const int nslot = nchain * nact;
             // class of every slot, 2 bits a slot
             int cmap = 0;
@@ -1092,6 +1091,14 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                 // shows a higher sum (then it is a frontier point and is scored) or
                 // the same sum (then a lower max reaches it and it is dropped); a
                 // point at t_bot is the segment's last frontier point.
+                // With a second slot per class the walk runs as two chains: the upper
+                // one (slot q) walks down to a middle threshold mid, where its last
+                // pass only confirms its pending point; the lower one (slot q + nact)
+                // starts with a pass at mid (pend = 2: nothing to confirm yet) and
+                // walks on down.  A point both find is scored twice, which changes
+                // nothing.  (Splitting again whenever one chain falls idle, as the
+                // descending sweep does, measured slower here: every split adds a
+                // confirming pass.)
                 auto keep_pending = [&]() {   // lane 0 of a segment: the last pass's point
                     CTL[sg].pend = CTL[sg].F < kBig ? 1 : 0;
                     CTL[sg].pF = CTL[sg].F;
@@ -1102,11 +1109,14 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                     CTL[sg].pok = (int32_t)CTL[sg].ok;
                     for (int w = 0; w < 8; ++w) CTL[sg].pbt[w] = CTL[sg].bt[w];
                 };
-                auto score = [&]() {   // a candidate lane offers its segment's pending point
-                    const SegCtl &P = CTL[sjc];
+                auto latency = [&](const SegCtl &P) {
                     int64_t steady = (int64_t)Bj - P.ps0 - 2;   // B - s - 1 with s = s0 + 1
                     steady = steady > 0 ? steady : 0;
-                    const int64_t lat = P.pF + P.pfwd + steady * P.pM;
+                    return P.pF + P.pfwd + steady * P.pM;
+                };
+                auto score = [&](int slot) {   // a candidate lane offers a slot's pending point
+                    const SegCtl &P = CTL[slot];
+                    const int64_t lat = latency(P);
                     if (lat < bs || (lat == bs && P.pM < bmx)) {
                         bs = lat;
                         bmx = P.pM;
@@ -1116,25 +1126,20 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                         pok = (uint32_t)P.pok;
                     }
                 };
-                // A candidate needs no more of the walk once its incumbent is strictly
+                // A candidate needs no more of a chain once its incumbent is strictly
                 // below the pending point's latency and below a bound for every point
                 // further down: sum >= the pending sum, forward part >= ceil(t_bot/3)
                 // (the largest stage's own), steady part >= max(0, B - PP - 1) t_bot.
                 // Strict, so that a tie, which the lower max would win, still runs.
-                auto needs_more = [&]() {
-                    const SegCtl &P = CTL[sjc];
-                    if (!member || P.pend == 0) return false;
-                    int64_t steady = (int64_t)Bj - P.ps0 - 2;
-                    steady = steady > 0 ? steady : 0;
-                    const int64_t lat = P.pF + P.pfwd + steady * P.pM;
+                auto needs_more = [&](int slot) {
+                    const SegCtl &P = CTL[slot];
+                    if (!member || P.pend != 1) return false;
+                    const int64_t lat = latency(P);
                     int64_t slb = (int64_t)Bj - PP - 1;
                     slb = slb > 0 ? slb : 0;
                     const int64_t lb = P.pF + (P.G + 2) / 3 + slb * P.G;
                     return !(bs < lat && bs < lb);
                 };
-                uint64_t seg_cands[kMaxSeg];
-#pragma unroll
-                for (int q = 0; q < kMaxSeg; ++q) seg_cands[q] = __builtin_amdgcn_ballot_w64(sj == q);
                 if (seg_live && ll == 0) {
                     if (CTL[sg].on)
                         keep_pending();
@@ -1143,28 +1148,65 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                 }
                 if (member) bs = kInf;
                 wave_sync();
+                // the upper chains' stops and the lower chains' starts
+                if (lane == 0) {
+                    for (int q = 0; q < nact; ++q) {
+                        CTL[q].cs = -1;   // no stop: walks to t_bot
+                        if (nchain < 2) continue;
+                        const int y = q + nact;
+                        CTL[y].cs = -1;
+                        CTL[y].G = CTL[q].G;
+                        CTL[y].pend = 0;
+                        const int64_t top = CTL[q].M - 1, g = CTL[q].G;
+                        if (CTL[q].pend == 1 && top - g >= 2) {
+                            const int64_t mid = g + (top - g) / 2;
+                            CTL[q].cs = mid;
+                            CTL[y].pend = 2;
+                            CTL[y].pM = mid + 1;   // its first pass runs at mid
+                        }
+                    }
+                }
+                wave_sync();
                 for (;;) {
                     bool any = false;
-                    const uint64_t need = __builtin_amdgcn_ballot_w64(needs_more());
+                    const uint64_t need0 = __builtin_amdgcn_ballot_w64(sj >= 0 && needs_more(sjc));
+                    const uint64_t need1 =
+                        nchain > 1 ? __builtin_amdgcn_ballot_w64(sj >= 0 && needs_more(sjc + nact)) : 0;
 #pragma unroll
                     for (int q = 0; q < kMaxSeg; ++q) {
                         if (q >= nseg) continue;
-                        const bool pend = q < nact && CTL[q].pend != 0;
-                        const bool run = pend && CTL[q].pM > CTL[q].G && (need & seg_cands[q]) != 0;
+                        const int c = q < nact ? q : q - nact;
+                        const int pend = q < nslot ? CTL[q].pend : 0;
+                        // a lower chain starts where its class still needs the upper one
+                        const uint64_t need = (q < nact || pend == 2) ? need0 : need1;
+                        const bool run = pend != 0 && CTL[q].pM > CTL[q].G &&
+                                         (need & __builtin_amdgcn_ballot_w64(sj == c)) != 0;
                         set_ctl(q, run, pend ? CTL[q].pM - 1 : 0);
                         any |= run;
                     }
                     // a pending point at t_bot is the last frontier point
-                    const bool at_bot = member && CTL[sjc].pend != 0 && CTL[sjc].pM <= CTL[sjc].G;
-                    if (at_bot) score();
+                    if (member)
+                        for (int k = 0; k < nchain; ++k) {
+                            const int slot = sjc + k * nact;
+                            if (CTL[slot].pend == 1 && CTL[slot].pM <= CTL[slot].G) score(slot);
+                        }
                     wave_sync();
-                    if (seg_live && ll == 0 && CTL[sg].pend != 0 && CTL[sg].pM <= CTL[sg].G) CTL[sg].pend = 0;
+                    if (seg_live && ll == 0 && CTL[sg].pend == 1 && CTL[sg].pM <= CTL[sg].G) CTL[sg].pend = 0;
                     wave_sync();
                     if (!any) break;
                     pass(false);
-                    if (member && CTL[sjc].on && CTL[sjc].F > CTL[sjc].pF) score();   // confirmed
+                    if (member)
+                        for (int k = 0; k < nchain; ++k) {
+                            const int slot = sjc + k * nact;
+                            if (CTL[slot].on && CTL[slot].pend == 1 && CTL[slot].F > CTL[slot].pF) score(slot);   // confirmed
+                        }
                     wave_sync();
-                    if (seg_live && ll == 0 && CTL[sg].on) keep_pending();
+                    if (seg_live && ll == 0 && CTL[sg].on) {
+                        if (CTL[sg].t <= CTL[sg].cs)
+                            CTL[sg].pend = 0;   // an upper chain's last pass only confirmed its point
+                        else
+                            keep_pending();
+                    }
                     wave_sync();
                 }
             }
