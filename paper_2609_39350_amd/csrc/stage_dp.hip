@@ -58,6 +58,7 @@ constexpr int64_t kNegInf = INT64_MIN;        // a threshold no stage cost meets
 constexpr int kRelaxUnroll = 2;   // split points per relaxation-loop trip
 constexpr int kMaxSeg = 4;
 constexpr int kParallelTrace = 4;    // pipelines at least this deep back-trace in two phases
+constexpr int kEarlySlots = 4;       // slots whose time prefix sums are loaded ahead of the layout work
 // Sweeps and 1F1B walks give every class up to kMaxChains slots (chains) while the
 // batch has room for them and the slots' entries of the widest stage band take at
 // most kChainEntries lanes.  A third chain saves passes but costs more per pass
@@ -406,6 +407,24 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
         const int PP = __builtin_amdgcn_readfirstlane(cand[idx0].pp);
         const PiInfo *pi = reinterpret_cast<const PiInfo *>(tab + L.off_pi) + cfg;
         const KeyInfo *ki = reinterpret_cast<const KeyInfo *>(tab + L.off_key) + key;
+        // The configuration's memory prefix sums (stored to LDS for the class
+        // split) and, below, the slots' time prefix sums are loaded as soon as
+        // their addresses are known, so that their latency overlaps the stage
+        // layout work; lane l holds end layers l and l + 64 (N <= 127).
+        const int64_t *time = reinterpret_cast<const int64_t *>(tab + L.off_time) + cfg * L.n_masks * 3 * np;
+        const int64_t *mem = reinterpret_cast<const int64_t *>(tab + L.off_mem) + cfg * 4 * np;
+        int64_t mv[2][3] = {{0, 0, 0}, {0, 0, 0}};
+        int32_t mo[2] = {0, 0};
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+            const int b = lane + 64 * c;
+            if (b <= N) {
+                mv[c][0] = mem[b];
+                mv[c][1] = mem[np + b];
+                mv[c][2] = mem[2 * np + b];
+                mo[c] = (int32_t)mem[3 * np + b];
+            }
+        }
 
         // ---- lane j holds the key's j-th microbatch count ----
         const int64_t inst = idx0 + lane;
@@ -438,6 +457,27 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
         const uint64_t used = wave_or64(lane < PP ? (uint64_t(1) << mask) : 0);
         const int nslot = __popcll(used);
         const int slot = __popcll(used & ((uint64_t(1) << mask) - 1));
+        // time prefix sums (r = 0, 1) of the first kEarlySlots slots, in flight
+        // during the layout work below
+        int64_t tv[kEarlySlots][2][2];
+        {
+            uint64_t rs = used;
+#pragma unroll
+            for (int k = 0; k < kEarlySlots; ++k) {
+                const int m = rs ? __ffsll((unsigned long long)rs) - 1 : 0;   // bit m: set m (>= 1)
+                rs = rs ? rs & (rs - 1) : 0;
+                const int64_t *src = time + (int64_t)(m > 0 ? m - 1 : 0) * 3 * np;
+#pragma unroll
+                for (int c = 0; c < 2; ++c) {
+                    const int b = lane + 64 * c;
+                    tv[k][c][0] = tv[k][c][1] = 0;
+                    if (m > 0 && b <= N) {
+                        tv[k][c][0] = src[b];
+                        tv[k][c][1] = src[np + b];
+                    }
+                }
+            }
+        }
         int64_t cap = kInf;
         for (int h = 0; h < H.n_types; ++h)
             if ((mask >> h) & 1) cap = H.mem_bytes[h] < cap ? H.mem_bytes[h] : cap;
@@ -526,11 +566,21 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
         }
 
         // ---- the key's prefix sums in LDS ----
-        const int64_t *time = reinterpret_cast<const int64_t *>(tab + L.off_time) + cfg * L.n_masks * 3 * np;
-        const int64_t *mem = reinterpret_cast<const int64_t *>(tab + L.off_mem) + cfg * 4 * np;
         {
+            // negated, so that a stage cost T[b] - T[a] is one 64-bit add
+#pragma unroll
+            for (int k = 0; k < kEarlySlots; ++k) {
+                if (k >= nslot) continue;
+#pragma unroll
+                for (int c = 0; c < 2; ++c) {
+                    const int b = lane + 64 * c;
+                    if (b <= N) TM[k * NP + b] = I64x2{-tv[k][c][0], -tv[k][c][1]};
+                }
+            }
+            // further slots (device-type sets across the boundaries of an ordering)
             uint64_t rs = used;
-            int k = 0;
+            for (int k = 0; k < kEarlySlots && rs; ++k) rs &= rs - 1;
+            int k = kEarlySlots;
             while (rs) {
                 const int m = __ffsll((unsigned long long)rs) - 1;
                 rs &= rs - 1;
@@ -558,11 +608,15 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
         // threshold -- unless some stage steps at an m in [v, min(PP - s, v') - 1]:
         // collect every step m <= PP - s - 1 into brk, then a present group value
         // opens a new class iff brk has a bit between the previous value and it.
-        for (int b = lane; b <= N; b += 64) {
-            MW[b] = mem[b];
-            MA0[b] = mem[np + b];
-            MA1[b] = mem[2 * np + b];
-            MOE[b] = (int32_t)mem[3 * np + b];
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+            const int b = lane + 64 * c;
+            if (b <= N) {
+                MW[b] = mv[c][0];
+                MA0[b] = mv[c][1];
+                MA1[b] = mv[c][2];
+                MOE[b] = mo[c];
+            }
         }
         wave_sync();
         uint64_t brk = 0;
