@@ -5,6 +5,7 @@ recomputation choice and status for every compared candidate; fp64 terms
 before rounding within 1e-12 relative.  Small problems are compared in full;
 the large configurations on a fixed stride sample plus the chosen best plan.
 """
+import copy
 import multiprocessing as mp
 import os
 
@@ -260,6 +261,33 @@ def test_random_tiny_every_candidate(torch):
         pl.stage_dp()
         total += compare(p, pl, range(pl.n))
     assert total > 100
+
+
+def _seven_sets(seed):
+    """Four device types of 3, 4, 4 and 3 devices: the 2-device stages of the
+    7-stage pipelines straddle every type boundary, so a key uses 7 device-type
+    sets (4 single-type, 3 mixed) -- more than the kernel loads ahead."""
+    p = copy.deepcopy(workloads.random_tiny(seed, n_layers=10, n_types=4, max_pp=8))
+    p["cluster"]["count"] = np.array([3, 4, 4, 3], dtype=np.int32)
+    p["name"] = f"seven-sets-{seed}"
+    return p
+
+
+def test_seven_device_type_sets_every_candidate(torch):
+    total = 0
+    for s in range(3):
+        p = _seven_sets(s)
+        print(p["name"], flush=True)
+        o = orc.Oracle(p)
+        assert max(len({st["mask"] for st in o.stages(c, od, 1)})
+                   for c in o.configs() for od in range(o.n_orders())) == 7
+        pl = binding.Planner(p, "cuda:0")
+        pl.eval_cost_tables()
+        pl.stage_dp()
+        total += compare(p, pl, range(pl.n))
+        pl.stage_dp(objective="1f1b")
+        compare(p, pl, range(pl.n), objective="1f1b")
+    assert total > 50
 
 
 def test_subranges_and_repeat_are_identical(torch):
