@@ -1348,6 +1348,12 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
             }
 
             // ---- 4) descending Pareto sweep ----
+            // each class's t_bot as seen by its sweeping candidates (-1: none), fixed
+            // for the whole sweep
+            int64_t tbq[kMaxSeg] = {-1, -1, -1, -1};
+#pragma unroll
+            for (int q = 0; q < kMaxSeg; ++q)
+                if (!EXACT && q < nact) tbq[q] = wave_max64(sj == q && sweeping ? tbot : -1);
             while (!EXACT) {
                 bool any = false;
                 // this lane's thresholds for the chains of its class
@@ -1357,7 +1363,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
 #pragma unroll
                 for (int q = 0; q < kMaxSeg; ++q) {
                     if (q >= nact) continue;
-                    const int64_t tb = wave_max64(sj == q && sweeping ? tbot : -1);
+                    const int64_t tb = tbq[q];
                     // every chain's threshold and the bound it runs above (wave-uniform)
                     int64_t tk[kMaxSeg], lk[kMaxSeg];
 #pragma unroll
