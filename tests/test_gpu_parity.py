@@ -451,3 +451,28 @@ def test_best_plan_launcher_text(torch):
     text = launcher.plan_to_launcher(p, plan)
     assert f"--pipeline-model-parallel-size {plan['config'][0]}" in text
     assert 'PIPELINE_STAGE_LAYERS="' + ",".join(str(n) for n in plan["layers"]) + '"' in text
+
+
+# ------------------------------------- no pruning windows on the large models
+@pytest.mark.parametrize("n", [4, 5])
+def test_no_windows_large_configs_sampled(torch, n):
+    """Pruning-1 windows off: every stage may take 1 .. N - PP + 1 layers, so the
+    split ranges reach their widest (65 split points a stage on the 96-layer
+    model at PP = 32) and the sweep keeps one chain per class. Both objectives on
+    a sample of the deepest pipelines (the only feasible ones) plus a stride
+    sample of all candidates."""
+    p = variant(workloads.config(n), **{"params.prune_window": 0})
+    print(f"config {n}: no windows", flush=True)
+    pl = binding.Planner(p, "cuda:0")
+    plan = pl.run()
+    res = pl.results()
+    pp = pl.cand_host["pp"]
+    deep = np.nonzero(pp == pp.max())[0]
+    idx = sorted(set(deep[::max(1, len(deep) // 48)].tolist() + list(range(5, pl.n, pl.n // 97))
+                     + [plan["instance"]]))
+    assert compare(p, pl, idx, res, ref=oracle_many(p, idx, pool=True)) > 0
+    obj = np.where(res["status"] == 0, res["objective"], np.iinfo(np.int64).max)
+    assert plan["instance"] == int(np.argmin(obj))
+    pl.stage_dp(objective="1f1b")
+    sub = deep[::max(1, len(deep) // 24)].tolist()
+    assert compare(p, pl, sub, objective="1f1b", ref=oracle_many(p, sub, "1f1b", pool=True)) > 0
