@@ -24,7 +24,7 @@
 // back-trace there.  B enters through min(B, PP) (memory) and the objective
 // weight: the B values with one min(B, PP) share every pass.
 //
-// Mapping: one 256-thread workgroup per configuration, pulled from an atomic
+// Mapping: one 1024-thread workgroup per configuration, pulled from an atomic
 // queue (largest PP first).  States of one level (equal sum u) are
 // independent: their (u, b, h') entries are spread over the threads, and the
 // levels follow one another with a barrier.  Only end layers b inside the
