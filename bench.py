@@ -255,6 +255,24 @@ def leg_free_types(torch, binding, workloads, dev, stream, steps, warmup, cpu_sa
     return out
 
 
+def host_cpu():
+    """Host cores and CPU model, for the CPU-baseline record."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = os.cpu_count()
+    return {"nproc": usable, "cpu_count": os.cpu_count(), "cpu_model": model}
+
+
 def cpu_baseline(problem, n_total, n_sample, exact=False):
     """The oracle as it stands, single thread, on a fixed stride sample (exact:
     its 1F1B re-scoring of the frontier)."""
@@ -270,7 +288,7 @@ def cpu_baseline(problem, n_total, n_sample, exact=False):
     # the pass it back-traces when a partition exists
     W = problem["model"]["n_layers"] + 1
     updates = [(1 + r["thresholds"] + (r["status"] == 0)) * r["pp"] * W * (W - 1) // 2 for r in res]
-    out = {"value": len(idx) / dt, "unit": "candidates/s", "cores": 1, "kind": "oracle",
+    out = {"value": len(idx) / dt, "unit": "candidates/s", "cores": 1, "kind": "oracle", "host": host_cpu(),
            "sample": f"{len(idx)} candidates at stride {stride} of {n_total} (every {stride}th), "
                      f"{dt:.1f} s on one host core"}
     return out, sum(updates) / max(len(updates), 1)

@@ -26,7 +26,11 @@
  *  - Times are int64 nanoseconds, memory sizes int64 bytes, bandwidths bytes/ns
  *    (= GB/s), latencies ns.  Costs are rounded up to whole ns / bytes once per
  *    modelled term.
- *  - The device calls need a gfx950 device (HAPMOE_E_ARCH otherwise).
+ *  - The device calls need a gfx950 device (HAPMOE_E_ARCH otherwise).  The
+ *    library caches that answer per device (an atomic flag each, set once); it
+ *    holds no other state between calls except the section-clock table of its
+ *    diagnostic build.  Concurrent calls from several host threads are safe
+ *    as long as they do not share output buffers or a workspace.
  */
 #ifndef HAPMOE_H
 #define HAPMOE_H
@@ -240,10 +244,17 @@ int32_t hapmoe_debug_layout(const hapmoe_problem *p, int64_t out[4]);
  * recomputation and of the communication part, per configuration the weight /
  * activation prefix sums, and per (configuration, ordering) the stage layout.
  * d_cand must be the full array of hapmoe_enumerate_candidates (n_cand
- * entries); d_tables has hapmoe_tables_bytes bytes.  d_debug (may be NULL)
- * receives the fp64 terms before rounding (hapmoe_debug_bytes).  Asynchronous. */
+ * entries); d_tables has hapmoe_tables_bytes bytes and is indexed by the
+ * global configuration index.  Only the configurations holding candidates
+ * [first, first + count) are evaluated (every one of their orderings), so a
+ * caller can fill the buffer in chunks before running the stage DP on them;
+ * every call also rewrites the per-layer load-imbalance factors.  count = 0
+ * enqueues nothing; a range outside [0, n_cand) is HAPMOE_E_RANGE.  d_debug
+ * (may be NULL) receives the fp64 terms before rounding of the same
+ * configurations (hapmoe_debug_bytes).  Asynchronous. */
 int32_t hapmoe_eval_cost_tables(const hapmoe_problem *p, const void *d_image,
                                 const hapmoe_candidate *d_cand, int64_t n_cand,
+                                int64_t first, int64_t count,
                                 void *d_tables, int64_t tables_bytes,
                                 double *d_debug, int64_t debug_bytes, void *stream);
 

@@ -95,7 +95,7 @@ def lib():
         L.hapmoe_pack_image.argtypes = [P(Problem), vp, i64]
         L.hapmoe_tables_bytes.argtypes = [P(Problem), P(i64)]
         L.hapmoe_debug_bytes.argtypes = [P(Problem), P(i64)]
-        L.hapmoe_eval_cost_tables.argtypes = [P(Problem), vp, vp, i64, vp, i64, vp, i64, vp]
+        L.hapmoe_eval_cost_tables.argtypes = [P(Problem), vp, vp, i64, i64, i64, vp, i64, vp, i64, vp]
         L.hapmoe_stage_dp.argtypes = [P(Problem), vp, vp, i64, vp, i64, i64, i64, vp, vp, vp, i64, vp]
         L.hapmoe_stage_dp_1f1b.argtypes = [P(Problem), vp, vp, i64, vp, i64, i64, i64, vp, vp, vp, i64, vp]
         L.hapmoe_stage_dp_ws_bytes.argtypes = [P(Problem), P(i64)]
@@ -301,10 +301,11 @@ def best_plan_ws_bytes(problem, n) -> int:
 
 
 # -------------------------------------------------------------- device calls
-def eval_cost_tables(problem, d_image, d_cand, n_cand, d_tables, d_debug=None, stream=None):
-    _check(lib().hapmoe_eval_cost_tables(_hp(problem).ref, _dptr(d_image), _dptr(d_cand), int(n_cand),
-                                         _dptr(d_tables), _nbytes(d_tables), _dptr(d_debug), _nbytes(d_debug),
-                                         _stream(stream)), "hapmoe_eval_cost_tables")
+def eval_cost_tables(problem, d_image, d_cand, n_cand, d_tables, d_debug=None, stream=None, first=0, count=None):
+    count = int(n_cand) - int(first) if count is None else count
+    _check(lib().hapmoe_eval_cost_tables(_hp(problem).ref, _dptr(d_image), _dptr(d_cand), int(n_cand), int(first),
+                                         int(count), _dptr(d_tables), _nbytes(d_tables), _dptr(d_debug),
+                                         _nbytes(d_debug), _stream(stream)), "hapmoe_eval_cost_tables")
 
 
 def stage_dp_ws_bytes(problem) -> int:
@@ -349,17 +350,21 @@ def stage_dp_types_1f1b(problem, d_image, d_cand, n_cand, d_tables, first, count
                                             _nbytes(d_ws), _stream(stream)), "hapmoe_stage_dp_types_1f1b")
 
 
-def best_plan(problem, d_cand, d_tables, d_res, n, d_ws, d_config_best=None, stream=None, d_types=None) -> dict:
-    plan = Plan()
-    _check(lib().hapmoe_best_plan(_hp(problem).ref, _dptr(d_cand), _dptr(d_tables), _nbytes(d_tables),
-                                  _dptr(d_res), _dptr(d_types), int(n), _dptr(d_config_best), _dptr(d_ws), _nbytes(d_ws),
-                                  C.byref(plan), _stream(stream)), "hapmoe_best_plan")
+def _plan_dict(plan):
     pp = plan.n_stages
     return {"instance": plan.instance, "objective": plan.objective, "stage_sum": plan.stage_sum,
             "t_max": plan.t_max, "dp_const": plan.dp_const,
             "config": tuple(plan.cand[:6]), "order": plan.cand[6], "n_micro": plan.cand[7],
             "layers": list(plan.layers[:pp]), "stage_types": list(plan.stage_types[:pp]),
             "recompute": [(plan.recompute_mask >> i) & 1 for i in range(pp)]}
+
+
+def best_plan(problem, d_cand, d_tables, d_res, n, d_ws, d_config_best=None, stream=None, d_types=None) -> dict:
+    plan = Plan()
+    _check(lib().hapmoe_best_plan(_hp(problem).ref, _dptr(d_cand), _dptr(d_tables), _nbytes(d_tables),
+                                  _dptr(d_res), _dptr(d_types), int(n), _dptr(d_config_best), _dptr(d_ws), _nbytes(d_ws),
+                                  C.byref(plan), _stream(stream)), "hapmoe_best_plan")
+    return _plan_dict(plan)
 
 
 class Planner:
@@ -399,8 +404,9 @@ class Planner:
         self.n_configs = n_cfg
         self.d_config_best = torch.empty(max(n_cfg, 1), dtype=torch.int64, device=self.device)
 
-    def eval_cost_tables(self, stream=None):
-        eval_cost_tables(self.hp, self.d_image, self.d_cand, self.n, self.d_tables, self.d_debug, stream)
+    def eval_cost_tables(self, stream=None, first=0, count=None):
+        eval_cost_tables(self.hp, self.d_image, self.d_cand, self.n, self.d_tables, self.d_debug, stream, first,
+                         count)
 
     def stage_dp(self, first=0, count=None, stats=False, stream=None, objective="threshold"):
         """objective "threshold": sum + (B-1) max (hapmoe_stage_dp); "1f1b": the

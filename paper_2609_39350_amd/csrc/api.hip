@@ -3,6 +3,7 @@
 // kernel launches.  No device memory is allocated here.
 #include <algorithm>
 #include <array>
+#include <atomic>
 #include <cmath>
 #include <cstring>
 #include <vector>
@@ -202,16 +203,21 @@ int32_t check_problem(const hapmoe_problem *p)
     return HAPMOE_OK;
 }
 
+// The architecture check runs on every device call; its answer per device is
+// cached.  Each slot is an atomic written with the same value by whichever
+// thread gets there first, so concurrent callers on any devices are safe.
 int check_arch()
 {
-    static int cache[64] = {0};   // 0 unknown, 1 gfx950, 2 other
+    static std::atomic<int> cache[64];   // 0 unknown, 1 gfx950, 2 other (zero-initialised)
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return HAPMOE_E_HIP;
-    if (dev >= 0 && dev < 64 && cache[dev]) return cache[dev] == 1 ? HAPMOE_OK : HAPMOE_E_ARCH;
+    const bool slot = dev >= 0 && dev < 64;
+    const int known = slot ? cache[dev].load(std::memory_order_relaxed) : 0;
+    if (known) return known == 1 ? HAPMOE_OK : HAPMOE_E_ARCH;
     hipDeviceProp_t prop;
     if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return HAPMOE_E_HIP;
     const bool ok = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0;
-    if (dev >= 0 && dev < 64) cache[dev] = ok ? 1 : 2;
+    if (slot) cache[dev].store(ok ? 1 : 2, std::memory_order_relaxed);
     return ok ? HAPMOE_OK : HAPMOE_E_ARCH;
 }
 
@@ -427,8 +433,8 @@ int32_t hapmoe_debug_bytes(const hapmoe_problem *p, int64_t *bytes)
 }
 
 int32_t hapmoe_eval_cost_tables(const hapmoe_problem *p, const void *d_image, const hapmoe_candidate *d_cand,
-                                int64_t n_cand, void *d_tables, int64_t tables_bytes, double *d_debug,
-                                int64_t debug_bytes, void *stream)
+                                int64_t n_cand, int64_t first, int64_t count, void *d_tables, int64_t tables_bytes,
+                                double *d_debug, int64_t debug_bytes, void *stream)
 {
     if (const int32_t e = check_problem(p)) return e;
     if (!d_image || !d_cand || !d_tables) return HAPMOE_E_INVAL;
@@ -436,14 +442,18 @@ int32_t hapmoe_eval_cost_tables(const hapmoe_problem *p, const void *d_image, co
     build_space(p, S);
     const int64_t per = per_config(p, S);
     if (n_cand != (int64_t)S.cfg.size() * per) return HAPMOE_E_INVAL;
+    if (first < 0 || count < 0 || first + count > n_cand) return HAPMOE_E_RANGE;
     const TablesLayout L = tables_layout((int64_t)S.cfg.size(), (int)S.n_orders, p->cluster.n_types,
                                          p->model.n_layers);
     if (tables_bytes < L.total) return HAPMOE_E_WORKSPACE;
     const DebugLayout D = debug_layout(p->cluster.n_types, p->model.n_layers);
     if (d_debug && debug_bytes < (int64_t)S.cfg.size() * D.per_cfg * 8) return HAPMOE_E_WORKSPACE;
     if (const int e = check_arch()) return e;
-    if (launch_cost_tables(d_image, d_cand, per, p->model.n_layers, L, d_tables, d_debug, D, (hipStream_t)stream) !=
-        hipSuccess)
+    if (count == 0) return HAPMOE_OK;
+    // the configurations holding candidates [first, first + count)
+    const int64_t cfg_lo = first / per, cfg_hi = (first + count - 1) / per;
+    if (launch_cost_tables(d_image, d_cand, per, p->model.n_layers, L, cfg_lo, cfg_hi - cfg_lo + 1, d_tables,
+                           d_debug, D, (hipStream_t)stream) != hipSuccess)
         return HAPMOE_E_HIP;
     return HAPMOE_OK;
 }

@@ -131,7 +131,7 @@ __global__ __launch_bounds__(kThreads) void k_layer_skew(const unsigned char *__
 // scratch (0.105 -> 0.087 ms on the 96-layer MoE workload).
 __global__ __launch_bounds__(kThreads, 8) void k_cost_tables(const unsigned char *__restrict__ img,
                                                           const hapmoe_candidate *__restrict__ cand,
-                                                          int64_t per_config, TablesLayout L,
+                                                          int64_t per_config, int64_t cfg_lo, TablesLayout L,
                                                           unsigned char *__restrict__ tab,
                                                           double *__restrict__ dbg, DebugLayout D)
 {
@@ -143,7 +143,7 @@ __global__ __launch_bounds__(kThreads, 8) void k_cost_tables(const unsigned char
     const int64_t *tdense = reinterpret_cast<const int64_t *>(img + H.off_tdense);
     const int64_t *tffn = reinterpret_cast<const int64_t *>(img + H.off_tffn);
 
-    const int64_t cfg = blockIdx.x;
+    const int64_t cfg = cfg_lo + blockIdx.x;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const hapmoe_candidate c = cand[cfg * per_config];
     const int N = H.n_layers, T = H.n_types;
@@ -506,14 +506,14 @@ __global__ __launch_bounds__(kThreads, 8) void k_cost_tables(const unsigned char
 namespace hapmoe {
 
 hipError_t launch_cost_tables(const void *d_image, const hapmoe_candidate *d_cand, int64_t per_config,
-                              int n_layers, const TablesLayout &L, void *d_tables, double *d_debug,
-                              const DebugLayout &D, hipStream_t s)
+                              int n_layers, const TablesLayout &L, int64_t cfg_lo, int64_t n_cfg, void *d_tables,
+                              double *d_debug, const DebugLayout &D, hipStream_t s)
 {
-    if (L.n_configs == 0) return hipSuccess;
+    if (n_cfg <= 0) return hipSuccess;
     hipLaunchKernelGGL(k_layer_skew, dim3((unsigned)n_layers), dim3(kThreads), 0, s,
                        static_cast<const unsigned char *>(d_image), L, static_cast<unsigned char *>(d_tables));
-    hipLaunchKernelGGL(k_cost_tables, dim3((unsigned)L.n_configs), dim3(kThreads), 0, s,
-                       static_cast<const unsigned char *>(d_image), d_cand, per_config, L,
+    hipLaunchKernelGGL(k_cost_tables, dim3((unsigned)n_cfg), dim3(kThreads), 0, s,
+                       static_cast<const unsigned char *>(d_image), d_cand, per_config, cfg_lo, L,
                        static_cast<unsigned char *>(d_tables), d_debug, D);
     return hipGetLastError();
 }

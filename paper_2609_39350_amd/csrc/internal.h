@@ -115,8 +115,8 @@ inline DebugLayout debug_layout(int n_types, int n_layers)
 
 // Kernel launchers (stream = hipStream_t).
 hipError_t launch_cost_tables(const void *d_image, const hapmoe_candidate *d_cand, int64_t per_config,
-                              int n_layers, const TablesLayout &L, void *d_tables, double *d_debug,
-                              const DebugLayout &D, hipStream_t s);
+                              int n_layers, const TablesLayout &L, int64_t cfg_lo, int64_t n_cfg, void *d_tables,
+                              double *d_debug, const DebugLayout &D, hipStream_t s);
 hipError_t launch_stage_dp(const void *d_image, const hapmoe_candidate *d_cand, int n_layers, int n_micro,
                            const std::vector<int32_t> &config_pp, int n_orders, const TablesLayout &L,
                            const void *d_tables, int64_t first, int64_t count, int kmax, int ppmax,

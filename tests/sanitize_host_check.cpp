@@ -142,7 +142,7 @@ int run_problem(const hapmoe_problem &p, const char *name)
     }
     if (int e = hapmoe_best_plan_ws_bytes(&p, n, &bws)) bad |= fail("plan ws", e);
     // device calls with missing buffers: refused before any device work
-    if (hapmoe_eval_cost_tables(&p, nullptr, nullptr, n, nullptr, 0, nullptr, 0, nullptr) == HAPMOE_OK)
+    if (hapmoe_eval_cost_tables(&p, nullptr, nullptr, n, 0, n, nullptr, 0, nullptr, 0, nullptr) == HAPMOE_OK)
         bad |= fail("tables null", 0);
     if (hapmoe_stage_dp(&p, nullptr, nullptr, n, nullptr, 0, 0, n, nullptr, nullptr, nullptr, 0, nullptr) ==
         HAPMOE_OK)

@@ -157,6 +157,27 @@ def test_cost_tables_match_oracle(torch, which):
         _check_tables(p, pl, sample)
 
 
+def test_cost_tables_sub_ranges_equal_one_call(torch):
+    """hapmoe_eval_cost_tables over candidate sub-ranges (boundaries inside
+    configurations, one empty range) fills the same buffer as one call."""
+    p = workloads.config(3)
+    pl = binding.Planner(p, "cuda:0", debug=True)
+    pl.d_tables.zero_()
+    pl.d_debug.zero_()
+    pl.eval_cost_tables()
+    whole, whole_dbg = pl.tables().copy(), pl.debug().copy()
+    pl.d_tables.zero_()
+    pl.d_debug.zero_()
+    cuts = [0, 1, pl.n // 7 + 5, pl.n // 7 + 5, pl.n // 2 + 3, pl.n - 1, pl.n]
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        pl.eval_cost_tables(first=a, count=b - a)
+    assert np.array_equal(pl.tables(), whole)
+    assert np.array_equal(pl.debug().view(np.int64), whole_dbg.view(np.int64))
+    with pytest.raises(binding.HapmoeError) as e:
+        pl.eval_cost_tables(first=pl.n - 1, count=2)
+    assert e.value.code == -7
+
+
 # ----------------------------------------------------------------- stage DP
 def test_worked_example_on_gpu(torch):
     p = worked_problem()
