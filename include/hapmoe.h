@@ -364,6 +364,23 @@ int32_t hapmoe_best_plan(const hapmoe_problem *p, const hapmoe_candidate *d_cand
                          int64_t *d_config_best, void *d_ws, int64_t ws_bytes,
                          hapmoe_plan *h_plan, void *stream);
 
+/* hapmoe_best_plan without a caller workspace, for callers that cannot
+ * allocate device memory (code under stream capture, tight serving loops,
+ * harnesses that forbid allocation).  Same arguments, outputs and errors as
+ * hapmoe_best_plan minus d_ws / ws_bytes: the workspace is a fixed array of
+ * HAPMOE_BEST_PLAN_SCRATCH_BYTES in the library's device image, which each GPU
+ * holds until the process ends.  A problem whose hapmoe_best_plan_ws_bytes(p, n)
+ * exceeds it is HAPMOE_E_WORKSPACE (checked before any device work).  The call
+ * allocates nothing; nothing in the array has to start at zero.  Every call on
+ * one GPU shares that GPU's array, so calls that may overlap on one GPU (other
+ * host threads, other streams) race and must be serialised by the caller.
+ * Waits for `stream`, fills *h_plan. */
+#define HAPMOE_BEST_PLAN_SCRATCH_BYTES 262144
+int32_t hapmoe_best_plan_noalloc(const hapmoe_problem *p, const hapmoe_candidate *d_cand,
+                                 const void *d_tables, int64_t tables_bytes,
+                                 const hapmoe_dp_result *d_res, const uint8_t *d_types, int64_t n,
+                                 int64_t *d_config_best, hapmoe_plan *h_plan, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -103,6 +103,7 @@ def lib():
         L.hapmoe_debug_layout.argtypes = [P(Problem), P(i64)]
         L.hapmoe_best_plan_ws_bytes.argtypes = [P(Problem), i64, P(i64)]
         L.hapmoe_best_plan.argtypes = [P(Problem), vp, vp, i64, vp, vp, i64, vp, vp, i64, P(Plan), vp]
+        L.hapmoe_best_plan_noalloc.argtypes = [P(Problem), vp, vp, i64, vp, vp, i64, vp, P(Plan), vp]
         L.hapmoe_stage_dp_types.argtypes = [P(Problem), vp, vp, i64, vp, i64, i64, i64, vp, vp, vp, vp, i64, vp]
         L.hapmoe_stage_dp_types_ws_bytes.argtypes = [P(Problem), P(i64)]
         L.hapmoe_stage_dp_types_1f1b.argtypes = L.hapmoe_stage_dp_types.argtypes
@@ -110,7 +111,7 @@ def lib():
         L.hapmoe_section_clocks.restype = C.c_int32
         for f in ("hapmoe_validate", "hapmoe_enumerate_candidates", "hapmoe_image_bytes", "hapmoe_pack_image",
                   "hapmoe_tables_bytes", "hapmoe_debug_bytes", "hapmoe_tables_layout", "hapmoe_debug_layout", "hapmoe_eval_cost_tables", "hapmoe_stage_dp", "hapmoe_stage_dp_1f1b", "hapmoe_stage_dp_ws_bytes",
-                  "hapmoe_best_plan_ws_bytes", "hapmoe_best_plan", "hapmoe_stage_dp_types",
+                  "hapmoe_best_plan_ws_bytes", "hapmoe_best_plan", "hapmoe_best_plan_noalloc", "hapmoe_stage_dp_types",
                   "hapmoe_stage_dp_types_ws_bytes", "hapmoe_stage_dp_types_1f1b"):
             getattr(L, f).restype = C.c_int32
         _LIB = L
@@ -364,6 +365,18 @@ def best_plan(problem, d_cand, d_tables, d_res, n, d_ws, d_config_best=None, str
     _check(lib().hapmoe_best_plan(_hp(problem).ref, _dptr(d_cand), _dptr(d_tables), _nbytes(d_tables),
                                   _dptr(d_res), _dptr(d_types), int(n), _dptr(d_config_best), _dptr(d_ws), _nbytes(d_ws),
                                   C.byref(plan), _stream(stream)), "hapmoe_best_plan")
+    return _plan_dict(plan)
+
+
+BEST_PLAN_SCRATCH_BYTES = 262144   # HAPMOE_BEST_PLAN_SCRATCH_BYTES
+
+
+def best_plan_noalloc(problem, d_cand, d_tables, d_res, n, d_config_best=None, stream=None, d_types=None) -> dict:
+    """hapmoe_best_plan_noalloc: the same arg-min with the library's own fixed workspace."""
+    plan = Plan()
+    _check(lib().hapmoe_best_plan_noalloc(_hp(problem).ref, _dptr(d_cand), _dptr(d_tables), _nbytes(d_tables),
+                                          _dptr(d_res), _dptr(d_types), int(n), _dptr(d_config_best), C.byref(plan),
+                                          _stream(stream)), "hapmoe_best_plan_noalloc")
     return _plan_dict(plan)
 
 

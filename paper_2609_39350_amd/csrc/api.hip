@@ -581,12 +581,19 @@ int32_t hapmoe_best_plan_ws_bytes(const hapmoe_problem *p, int64_t n, int64_t *b
     return HAPMOE_OK;
 }
 
-int32_t hapmoe_best_plan(const hapmoe_problem *p, const hapmoe_candidate *d_cand, const void *d_tables,
-                         int64_t tables_bytes, const hapmoe_dp_result *d_res, const uint8_t *d_types, int64_t n,
-                         int64_t *d_config_best, void *d_ws, int64_t ws_bytes, hapmoe_plan *h_plan, void *stream)
+}  // extern "C"
+
+namespace {
+
+// hapmoe_best_plan with its workspace [d_ws, d_ws + ws_bytes); `noalloc`: the
+// workspace is the library's fixed array (its size checked before any device work)
+int32_t best_plan_any(const hapmoe_problem *p, const hapmoe_candidate *d_cand, const void *d_tables,
+                      int64_t tables_bytes, const hapmoe_dp_result *d_res, const uint8_t *d_types, int64_t n,
+                      int64_t *d_config_best, void *d_ws, int64_t ws_bytes, hapmoe_plan *h_plan, void *stream,
+                      bool noalloc)
 {
     if (const int32_t e = check_problem(p)) return e;
-    if (!d_cand || !d_tables || !d_res || !d_ws || !h_plan) return HAPMOE_E_INVAL;
+    if (!d_cand || !d_tables || !d_res || (!noalloc && !d_ws) || !h_plan) return HAPMOE_E_INVAL;
     if (p->space.stage_types == 2 ? !d_types : d_types != nullptr) return HAPMOE_E_INVAL;
     Space S;
     build_space(p, S);
@@ -594,8 +601,14 @@ int32_t hapmoe_best_plan(const hapmoe_problem *p, const hapmoe_candidate *d_cand
     if (n < 1 || n > ncfg * per) return HAPMOE_E_RANGE;
     const TablesLayout L = tables_layout(ncfg, (int)S.n_orders, p->cluster.n_types, p->model.n_layers);
     if (tables_bytes < L.total) return HAPMOE_E_WORKSPACE;
-    if (ws_bytes < best_plan_ws_bytes(n, per, ncfg)) return HAPMOE_E_WORKSPACE;
+    const int64_t need = best_plan_ws_bytes(n, per, ncfg);
+    if (noalloc ? need > HAPMOE_BEST_PLAN_SCRATCH_BYTES : ws_bytes < need) return HAPMOE_E_WORKSPACE;
     if (const int e = check_arch()) return e;
+    if (noalloc) {
+        int64_t have = 0;
+        if (best_plan_scratch(&d_ws, &have) != hipSuccess) return HAPMOE_E_HIP;
+        if (have < need) return HAPMOE_E_WORKSPACE;
+    }
     hipStream_t s = (hipStream_t)stream;
     const auto *tab = static_cast<const unsigned char *>(d_tables);
     if (launch_best_plan(d_res, d_cand, tab + L.off_key, d_types, p->space.n_micro, n, per, ncfg, d_config_best,
@@ -632,6 +645,26 @@ int32_t hapmoe_best_plan(const hapmoe_problem *p, const hapmoe_candidate *d_cand
         h_plan->stage_types[i] = i < cd.pp ? ki.mask[i] : 0;
     }
     return HAPMOE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t hapmoe_best_plan(const hapmoe_problem *p, const hapmoe_candidate *d_cand, const void *d_tables,
+                         int64_t tables_bytes, const hapmoe_dp_result *d_res, const uint8_t *d_types, int64_t n,
+                         int64_t *d_config_best, void *d_ws, int64_t ws_bytes, hapmoe_plan *h_plan, void *stream)
+{
+    return best_plan_any(p, d_cand, d_tables, tables_bytes, d_res, d_types, n, d_config_best, d_ws, ws_bytes, h_plan,
+                         stream, false);
+}
+
+int32_t hapmoe_best_plan_noalloc(const hapmoe_problem *p, const hapmoe_candidate *d_cand, const void *d_tables,
+                                 int64_t tables_bytes, const hapmoe_dp_result *d_res, const uint8_t *d_types,
+                                 int64_t n, int64_t *d_config_best, hapmoe_plan *h_plan, void *stream)
+{
+    return best_plan_any(p, d_cand, d_tables, tables_bytes, d_res, d_types, n, d_config_best, nullptr, 0, h_plan,
+                         stream, true);
 }
 
 }  // extern "C"

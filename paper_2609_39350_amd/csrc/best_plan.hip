@@ -3,10 +3,24 @@
 // candidates, then the global best.  Order: objective, then candidate index.
 // Reading the 8-byte objective of every 64-byte result record, this is a
 // streaming (HBM-bound) reduction.
+#include <mutex>
+
 #include "internal.h"
 
 namespace hapmoe {
 namespace {
+
+// Workspace of hapmoe_best_plan_noalloc: a fixed device array that every call
+// on a GPU shares (each GPU that loads the library holds its own copy until the
+// process ends).  Host code never passes `scratch` itself to a kernel -- in
+// host code it names a host-side stand-in -- but the device address that
+// hipGetSymbolAddress returns for the current device.
+constexpr int64_t kScratchBytes = HAPMOE_BEST_PLAN_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];   // per device, looked up once with that device current
 
 struct Best {
     int64_t obj;
@@ -122,6 +136,27 @@ __global__ __launch_bounds__(64) void k_gather(const Best *__restrict__ glob, co
 }
 
 }  // namespace
+
+// The device address of `scratch` on the current device: looked up with
+// hipGetSymbolAddress on the first call per device, then reused.
+hipError_t best_plan_scratch(void **ptr, int64_t *bytes)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
+    *bytes = kScratchBytes;
+    return hipSuccess;
+}
 
 // workspace: [global Best][winner: result | candidate | stage layout][cfg_best
 // n_configs][partial n_configs * chunks]

@@ -167,3 +167,26 @@ def test_device_count_dp_space_and_limits():
     binding.validate(variant(workloads.config(4), **{"space.stage_types": 2, "space.pp_max": 16}))
     with pytest.raises(binding.HapmoeError):
         binding.validate(variant(workloads.config(3), **{"space.stage_types": 3}))
+
+
+def test_noalloc_best_plan_rejects_problems_beyond_its_workspace():
+    """hapmoe_best_plan_noalloc refuses, before any device work, a problem whose
+    arg-min needs more than its fixed workspace; one that fits passes the size
+    check and stops only at the device check (no GPU here)."""
+    import copy
+    import ctypes as C
+    big = copy.deepcopy(workloads.config(4))
+    big["space"]["stage_types"] = 1   # 880 configurations x 2,520 stage-type sequences x 64 B values
+    big["space"]["pp_max"] = 8
+    small = workloads.config(2)
+    assert binding.best_plan_ws_bytes(big, 1) > binding.BEST_PLAN_SCRATCH_BYTES
+    assert binding.best_plan_ws_bytes(small, 1) <= binding.BEST_PLAN_SCRATCH_BYTES
+    fake = C.c_void_p(1 << 20)   # never dereferenced: both calls return before device work
+    codes = []
+    for p in (big, small):
+        hp = binding.HostProblem(p)
+        plan = binding.Plan()
+        codes.append(binding.lib().hapmoe_best_plan_noalloc(hp.ref, fake, fake, binding.tables_bytes(hp), fake,
+                                                            None, 1, None, C.byref(plan), None))
+    assert codes[0] == -3                 # HAPMOE_E_WORKSPACE
+    assert codes[1] in (-4, -5)           # past the size check: no usable device here
