@@ -961,6 +961,192 @@ int32_t orc_brute_exact(int32_t pp, int32_t n, int64_t micro, const int64_t *cos
 }
 
 /* ------------------------------------------------------------------------
+ * The least 1F1B latency itself (Eq. 4 with the appendix's steady-state term,
+ * orc_latency_1f1b) over every partition -- not only the partitions of the
+ * (max, sum) frontier that orc_dp_exact re-scores.  The latency of a partition
+ * depends on where its first largest stage s sits, so it is not a function of
+ * (max, sum): a partition off the frontier can have a lower latency.
+ *
+ * Exact minimisation: every partition has one largest cost t and one first
+ * stage s reaching it, and then its latency is the sum of per-stage weights
+ *   stages i < s:  c_i < t,   weight c_i + ceil(c_i / 3)   (its forward time counts)
+ *   stage s:       c_s = t,   weight t + ceil(t / 3) + max(0, B - s - 1) t
+ *   stages i > s:  c_i <= t,  weight c_i.
+ * For each threshold t (every distinct finite stage cost, ascending) a DP over
+ * (stage, end layer, z) -- z = 1 once the bottleneck stage is placed -- finds
+ * the least weight sum with the largest stage exactly t.  The sweep stops once
+ * F_inf + ceil(t/3) + max(0, B - pp - 1) t (a lower bound for every larger t)
+ * reaches the best latency.  Ties: least latency, then the lower largest
+ * stage, then the lexicographically smallest (b_{pp-1}, ..., b_1).
+ * ---------------------------------------------------------------------- */
+typedef struct lat_dp {
+    int pp, n, W;
+    int64_t micro, t;
+    const int64_t *cost;
+    int64_t *V;   /* [pp + 1][W][2] least weight sums */
+} lat_dp;
+
+static int64_t *lat_at(const lat_dp *d, int i, int b, int z) { return &d->V[((int64_t)i * d->W + b) * 2 + z]; }
+
+/* weight of stage i (1-based) on [a, b) moving from z0 to z1 (ORC_INF if not allowed) */
+static int64_t lat_weight(const lat_dp *d, int i, int a, int b, int z0, int z1)
+{
+    int64_t c = d->cost[((int64_t)(i - 1) * d->W + a) * d->W + b];
+    if (c == ORC_INF) return ORC_INF;
+    if (z0 == 0 && z1 == 0) return c < d->t ? c + (c + 2) / 3 : ORC_INF;
+    if (z0 == 0 && z1 == 1) {
+        if (c != d->t) return ORC_INF;
+        int64_t steady = d->micro - i - 1;
+        return c + (c + 2) / 3 + (steady > 0 ? steady : 0) * c;
+    }
+    if (z0 == 1 && z1 == 1) return c <= d->t ? c : ORC_INF;
+    return ORC_INF;
+}
+
+static void lat_pass(lat_dp *d)
+{
+    for (int i = 0; i <= d->pp; i++)
+        for (int b = 0; b < d->W; b++)
+            for (int z = 0; z < 2; z++) *lat_at(d, i, b, z) = (i == 0 && b == 0 && z == 0) ? 0 : ORC_INF;
+    for (int i = 1; i <= d->pp; i++)
+        for (int b = 1; b < d->W; b++)
+            for (int z = 0; z < 2; z++) {
+                int64_t best = ORC_INF;
+                for (int a = 0; a < b; a++)
+                    for (int z0 = 0; z0 <= z; z0++) {
+                        int64_t v = *lat_at(d, i - 1, a, z0), w = lat_weight(d, i, a, b, z0, z);
+                        if (v != ORC_INF && w != ORC_INF && v + w < best) best = v + w;
+                    }
+                *lat_at(d, i, b, z) = best;
+            }
+}
+
+/* The lexicographically smallest (b_{pp-1}, ..., b_1) among the optimal paths
+ * into (pp, n, z = 1): walking back from the last stage, keep the set of states
+ * (one end layer, z in {0, 1}) on some optimal path, take the smallest split
+ * point a through which one continues optimally, and move to those states. */
+static void lat_trace(const lat_dp *d, uint8_t *len)
+{
+    int b = d->n;
+    int live[2] = {0, 1};   /* live[z]: state (i, b, z) is on an optimal path */
+    for (int i = d->pp; i >= 1; i--) {
+        int na = -1, nl[2] = {0, 0};
+        for (int a = 0; a < b && na < 0; a++)
+            for (int z0 = 0; z0 < 2; z0++)
+                for (int z = z0; z < 2; z++) {
+                    if (!live[z]) continue;
+                    int64_t v = *lat_at(d, i - 1, a, z0), w = lat_weight(d, i, a, b, z0, z);
+                    if (v != ORC_INF && w != ORC_INF && v + w == *lat_at(d, i, b, z)) {
+                        na = a;
+                        nl[z0] = 1;
+                    }
+                }
+        len[i - 1] = (uint8_t)(b - na);
+        b = na;
+        live[0] = nl[0];
+        live[1] = nl[1];
+    }
+}
+
+int32_t orc_dp_latency(int32_t pp, int32_t n, int64_t micro, const int64_t *cost, orc_result *r)
+{
+    int W = n + 1;
+    int64_t ncost = (int64_t)pp * W * W;
+    memset(r, 0, sizeof(*r));
+    r->pp = pp;
+    int64_t *theta = malloc(sizeof(int64_t) * (size_t)(ncost + 1));
+    int64_t nt = 0;
+    for (int64_t i = 0; i < ncost; i++)
+        if (cost[i] != ORC_INF) theta[nt++] = cost[i];
+    qsort(theta, (size_t)nt, sizeof(int64_t), cmp_i64);
+    int64_t u = 0;
+    for (int64_t i = 0; i < nt; i++)
+        if (u == 0 || theta[i] != theta[u - 1]) theta[u++] = theta[i];
+    int64_t *F = malloc(sizeof(int64_t) * (size_t)(pp + 1) * W);
+    int16_t *arg = malloc(sizeof(int16_t) * (size_t)(pp + 1) * W);
+    lat_dp d;
+    d.pp = pp;
+    d.n = n;
+    d.W = W;
+    d.micro = micro;
+    d.cost = cost;
+    d.V = malloc(sizeof(int64_t) * (size_t)(pp + 1) * W * 2);
+    int64_t finf = pp <= n ? dp_pass(pp, n, cost, ORC_INF, F, arg) : ORC_INF;
+    int64_t best = ORC_INF, swept = 0, steady_min = micro - pp - 1;
+    if (steady_min < 0) steady_min = 0;
+    for (int64_t k = 0; k < u && finf != ORC_INF; k++) {
+        d.t = theta[k];
+        if (finf + (d.t + 2) / 3 + steady_min * d.t >= best) break;
+        lat_pass(&d);
+        swept++;
+        int64_t v = *lat_at(&d, pp, n, 1);
+        if (v < best) {
+            best = v;
+            r->tmax = d.t;
+            lat_trace(&d, r->layers);
+        }
+    }
+    r->thresholds = swept;
+    if (best == ORC_INF) {
+        r->status = 1;
+        r->opt = r->sum = r->tmax = ORC_INF;
+        memset(r->layers, 0, sizeof(r->layers));
+    } else {
+        r->opt = best;
+        r->sum = 0;
+        for (int i = 0, a = 0; i < pp; i++) {
+            r->sum += cost[((int64_t)i * W + a) * W + a + r->layers[i]];
+            a += r->layers[i];
+        }
+    }
+    free(theta);
+    free(F);
+    free(arg);
+    free(d.V);
+    return 0;
+}
+
+/* Brute force of the same minimum: every composition, key (latency, largest
+ * stage, b_{pp-1}, ..., b_1) ascending. */
+int32_t orc_brute_latency(int32_t pp, int32_t n, int64_t micro, const int64_t *cost, orc_result *r)
+{
+    memset(r, 0, sizeof(*r));
+    r->pp = pp;
+    part_list L;
+    memset(&L, 0, sizeof(L));
+    L.pp = pp;
+    L.n = n;
+    L.W = n + 1;
+    L.cost = cost;
+    if (pp <= n) collect(&L, 0);
+    int64_t best = ORC_INF, best_mx = ORC_INF;
+    const part_rec *win = NULL;
+    for (int64_t i = 0; i < L.len; i++) {
+        const part_rec *x = &L.v[i];
+        int64_t c[ORC_MAX_STAGES];
+        for (int k = 0; k < pp; k++) c[k] = cost[((int64_t)k * L.W + x->b[k]) * L.W + x->b[k + 1]];
+        int64_t lat = orc_latency_1f1b(pp, c, micro);
+        if (lat < best || (lat == best && (x->mx < best_mx || (x->mx == best_mx && lex_smaller(pp, x->b, win->b))))) {
+            best = lat;
+            best_mx = x->mx;
+            win = x;
+        }
+    }
+    r->thresholds = L.len;
+    if (!win) {
+        r->status = 1;
+        r->opt = r->sum = r->tmax = ORC_INF;
+    } else {
+        r->opt = best;
+        r->sum = win->sum;
+        r->tmax = win->mx;
+        for (int k = 0; k < pp; k++) r->layers[k] = (uint8_t)(win->b[k + 1] - win->b[k]);
+    }
+    free(L.v);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------
  * Free per-stage device types by the DP over device counts (Section 3.4: the
  * DP state carries the remaining devices of each type, and every transition
  * picks the type h and the layers of one more stage; Algorithm 1).
@@ -1496,9 +1682,14 @@ static int32_t solve_types(const orc_problem *p, int64_t idx, orc_result *r, int
     return 0;
 }
 
+/* mode: 0 threshold DP, 1 its brute force, 2 1F1B frontier re-scoring, 3 its
+ * brute force, 4 the least 1F1B latency, 5 its brute force */
 static int32_t solve_with(const orc_problem *p, int64_t idx, orc_result *r, int mode)
 {
-    if (p->stage_types == 2) return solve_types(p, idx, r, mode);   /* the device-count DP */
+    if (p->stage_types == 2) {   /* the device-count DP (no least-latency mode) */
+        if (mode > 3) return -1;
+        return solve_types(p, idx, r, mode);
+    }
     orc_config c;
     int32_t order, micro;
     if (orc_instance(p, idx, &c, &order, &micro)) return -1;
@@ -1512,8 +1703,12 @@ static int32_t solve_with(const orc_problem *p, int64_t idx, orc_result *r, int 
         orc_brute(c.pp, p->n_layers, micro, cost, r);
     else if (mode == 2)
         orc_dp_exact(c.pp, p->n_layers, micro, cost, r);
-    else
+    else if (mode == 3)
         orc_brute_exact(c.pp, p->n_layers, micro, cost, r);
+    else if (mode == 4)
+        orc_dp_latency(c.pp, p->n_layers, micro, cost, r);
+    else
+        orc_brute_latency(c.pp, p->n_layers, micro, cost, r);
     orc_stage st[ORC_MAX_STAGES];
     const int laid = orc_stages(p, &c, order, micro, st) == 0;
     for (int i = 0; i < c.pp; i++) r->stage_mask[i] = laid ? (uint8_t)st[i].mask : 0;
@@ -1549,5 +1744,15 @@ int32_t orc_solve_exact_many(const orc_problem *p, const int64_t *idx, int64_t n
 {
     for (int64_t i = 0; i < n; i++)
         if (orc_solve_exact(p, idx[i], &r[i])) return -1;
+    return 0;
+}
+
+int32_t orc_solve_latency(const orc_problem *p, int64_t idx, orc_result *r) { return solve_with(p, idx, r, 4); }
+int32_t orc_solve_latency_brute(const orc_problem *p, int64_t idx, orc_result *r) { return solve_with(p, idx, r, 5); }
+
+int32_t orc_solve_latency_many(const orc_problem *p, const int64_t *idx, int64_t n, orc_result *r)
+{
+    for (int64_t i = 0; i < n; i++)
+        if (orc_solve_latency(p, idx[i], &r[i])) return -1;
     return 0;
 }

@@ -161,6 +161,16 @@ int32_t orc_solve_exact(const orc_problem *p, int64_t idx, orc_result *r);
 int32_t orc_solve_exact_many(const orc_problem *p, const int64_t *idx, int64_t n, orc_result *r);
 int32_t orc_solve_exact_brute(const orc_problem *p, int64_t idx, orc_result *r);
 
+/* The least 1F1B latency over every partition (not only the frontier's): r->opt
+ * = least orc_latency_1f1b, ties to the lower largest stage, then the
+ * lexicographically smallest (b_{pp-1}, ..., b_1); r->thresholds = thresholds
+ * swept (orc_dp_latency) or compositions scored (orc_brute_latency). */
+int32_t orc_dp_latency(int32_t pp, int32_t n, int64_t micro, const int64_t *cost, orc_result *r);
+int32_t orc_brute_latency(int32_t pp, int32_t n, int64_t micro, const int64_t *cost, orc_result *r);
+int32_t orc_solve_latency(const orc_problem *p, int64_t idx, orc_result *r);
+int32_t orc_solve_latency_brute(const orc_problem *p, int64_t idx, orc_result *r);
+int32_t orc_solve_latency_many(const orc_problem *p, const int64_t *idx, int64_t n, orc_result *r);
+
 /* Free per-stage device types by the DP over device counts (stage_types = 2):
  * cost tensor [pp][T][T + 1][n + 1][n + 1], entry (s, h, h', a, b) = the cost
  * of a type-h stage s on layers [a, b) followed by a type-h' stage (h' = T:

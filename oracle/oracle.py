@@ -9,6 +9,7 @@ from the HIP library's package.
 from __future__ import annotations
 
 import ctypes as C
+import os
 
 import numpy as np
 
@@ -86,10 +87,12 @@ _LIB = None
 
 
 def lib():
-    """Load liboracle.so, compiling it first if it is not there."""
+    """Load liboracle.so, compiling it first if it is not there.  The
+    environment variable HAPMOE_ORACLE_LIB names another build of the same
+    source to load instead (the mutation test plants mistakes in copies)."""
     global _LIB
     if _LIB is None:
-        path = _build.build(force=False)
+        path = os.environ.get("HAPMOE_ORACLE_LIB") or _build.build(force=False)
         L = C.CDLL(path)
         P = C.POINTER
         L.orc_validate.argtypes = [P(OrcProblem)]
@@ -129,6 +132,11 @@ def lib():
         L.orc_solve_exact.argtypes = [P(OrcProblem), C.c_int64, P(OrcResult)]
         L.orc_solve_exact_brute.argtypes = [P(OrcProblem), C.c_int64, P(OrcResult)]
         L.orc_solve_exact_many.argtypes = [P(OrcProblem), C.c_void_p, C.c_int64, P(OrcResult)]
+        for name in ("orc_dp_latency", "orc_brute_latency"):
+            getattr(L, name).argtypes = [C.c_int32, C.c_int32, C.c_int64, C.c_void_p, P(OrcResult)]
+        for name in ("orc_solve_latency", "orc_solve_latency_brute"):
+            getattr(L, name).argtypes = [P(OrcProblem), C.c_int64, P(OrcResult)]
+        L.orc_solve_latency_many.argtypes = [P(OrcProblem), C.c_void_p, C.c_int64, P(OrcResult)]
         L.orc_type_costs.argtypes = [P(OrcProblem), C.c_int64, C.c_void_p, C.c_void_p]
         for name in ("orc_dp_types", "orc_brute_types", "orc_dp_types_exact", "orc_brute_types_exact"):
             getattr(L, name).argtypes = [C.c_int32, C.c_int32, C.c_void_p, C.c_int32, C.c_int64, C.c_void_p,
@@ -323,6 +331,26 @@ class Oracle:
             raise IndexError("instance out of range")
         return [result_dict(r) for r in res[: len(idx)]]
 
+    # ---- the least 1F1B latency over every partition ---------------------------
+    def solve_latency(self, idx):
+        r = OrcResult()
+        if self.L.orc_solve_latency(C.byref(self.P), int(idx), C.byref(r)) != 0:
+            raise IndexError(idx)
+        return result_dict(r)
+
+    def solve_latency_brute(self, idx):
+        r = OrcResult()
+        if self.L.orc_solve_latency_brute(C.byref(self.P), int(idx), C.byref(r)) != 0:
+            raise IndexError(idx)
+        return result_dict(r)
+
+    def solve_latency_many(self, idx):
+        idx = np.ascontiguousarray(idx, dtype=np.int64)
+        res = (OrcResult * max(len(idx), 1))()
+        if self.L.orc_solve_latency_many(C.byref(self.P), _ptr(idx), len(idx), res) != 0:
+            raise IndexError("instance out of range")
+        return [result_dict(r) for r in res[: len(idx)]]
+
     def best(self):
         """Global arg-min over all instances of (objective, instance index)."""
         best = None
@@ -375,6 +403,24 @@ def brute_exact(pp, n, micro, cost):
     return result_dict(r)
 
 
+def dp_latency(pp, n, micro, cost):
+    """The least 1F1B latency over every partition of an explicit cost tensor."""
+    cost = np.ascontiguousarray(cost, dtype=np.int64)
+    assert cost.shape == (pp, n + 1, n + 1)
+    r = OrcResult()
+    lib().orc_dp_latency(pp, n, micro, _ptr(cost), C.byref(r))
+    return result_dict(r)
+
+
+def brute_latency(pp, n, micro, cost):
+    """Brute force of the same minimum over all compositions."""
+    cost = np.ascontiguousarray(cost, dtype=np.int64)
+    assert cost.shape == (pp, n + 1, n + 1)
+    r = OrcResult()
+    lib().orc_brute_latency(pp, n, micro, _ptr(cost), C.byref(r))
+    return result_dict(r)
+
+
 def _types_call(name, k, n, micro, cost):
     cost = np.ascontiguousarray(cost, dtype=np.int64)
     pp, T = cost.shape[0], cost.shape[1]
@@ -412,9 +458,11 @@ def solve_worker(args):
     problem, idx = args[0], args[1]
     if len(args) > 2 and args[2] == "exact":
         return Oracle(problem).solve_exact_many(idx)
+    if len(args) > 2 and args[2] == "latency":
+        return Oracle(problem).solve_latency_many(idx)
     return Oracle(problem).solve_many(idx)
 
 
 __all__ = ["Oracle", "dp", "brute", "dp_exact", "brute_exact", "dp_types", "brute_types", "dp_types_exact",
-           "brute_types_exact", "latency_1f1b",
+           "brute_types_exact", "latency_1f1b", "dp_latency", "brute_latency",
            "INF", "lib", "solve_worker"]

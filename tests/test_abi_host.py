@@ -190,3 +190,12 @@ def test_noalloc_best_plan_rejects_problems_beyond_its_workspace():
                                                             None, 1, None, C.byref(plan), None))
     assert codes[0] == -3                 # HAPMOE_E_WORKSPACE
     assert codes[1] in (-4, -5)           # past the size check: no usable device here
+
+
+@pytest.mark.parametrize("n,n_candidates", [(1, 290), (2, 16272), (3, 117792), (4, 3855360), (5, 117792)])
+def test_library_enumeration_pinned_counts(n, n_candidates):
+    p = workloads.config(n)
+    assert binding.tables_layout(p)["n_configs"] * binding.tables_layout(p)["n_orders"] * \
+        len(p["space"]["micro"]) == n_candidates
+    if n_candidates <= 200000:
+        assert len(binding.enumerate_candidates(p)) == n_candidates

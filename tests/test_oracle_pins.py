@@ -409,3 +409,15 @@ def test_segment_costs_monotone_in_length():
                     assert fin == list(range(fin[0], fin[-1] + 1))
                     vals = [row[a] for a in fin]
                     assert all(x >= y for x, y in zip(vals, vals[1:]))
+
+
+@pytest.mark.parametrize("n,n_configs,n_candidates", [(1, 145, 290), (2, 904, 16272), (3, 1636, 117792),
+                                                      (4, 2510, 3855360), (5, 1636, 117792)])
+def test_enumeration_pinned_counts(n, n_configs, n_candidates):
+    """Configuration and candidate counts of the five workloads, counted
+    independently of both enumerators from the loop rules (PP | G, TP | group and
+    hidden, CP | sequence, EP | experts, EP * TPE | group) times the orderings
+    and micro-batch counts."""
+    o = orc.Oracle(workloads.config(n))
+    assert len(o.configs()) == n_configs
+    assert o.n_instances() == n_candidates
