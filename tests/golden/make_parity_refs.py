@@ -1,0 +1,94 @@
+"""Writes tests/golden/parity_refs.npz: digests of the oracle's results on the
+large workloads, for the GPU parity tests (which cannot afford to run the
+oracle over them on the GPU machine).  Calls only oracle/ and the seeded
+workload generators.  Run: python tests/golden/make_parity_refs.py [workers]
+
+Contents (each an index array and a uint32 digest array, tests/parity_digest.py):
+  cfg3_threshold, cfg3_1f1b, cfg5_threshold, cfg5_1f1b   every candidate
+  cfg4_threshold   one candidate per (configuration, ordering) key, B rotating 1..64
+  cfg4_1f1b        one candidate per configuration, ordering and B rotating
+  cfg3_types16     device-count DP, 16 candidates of 16-stage pipelines
+"""
+import copy
+import os
+import sys
+import time
+from multiprocessing import get_context
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+sys.path.insert(0, ROOT)
+
+from oracle import oracle as orc  # noqa: E402
+from paper_2609_39350_amd import workloads  # noqa: E402
+from tests import parity_digest  # noqa: E402
+
+OUT = os.path.join(os.path.dirname(os.path.abspath(__file__)), "parity_refs.npz")
+
+
+def _problem(name):
+    if name == "cfg3_types":
+        p = copy.deepcopy(workloads.config(3))
+        p["space"]["stage_types"] = 2
+        return p
+    return workloads.config(int(name[3]))
+
+
+def _work(args):
+    name, mode, idx = args
+    o = orc.Oracle(_problem(name))
+    res = {"threshold": o.solve_many, "1f1b": o.solve_exact_many}[mode](idx)
+    return parity_digest.of_oracle(res, with_types=name == "cfg3_types")
+
+
+def run(pool, name, mode, idx, chunk):
+    parts = [idx[k:k + chunk] for k in range(0, len(idx), chunk)]
+    t0 = time.time()
+    out = np.concatenate(pool.map(_work, [(name, mode, list(map(int, p))) for p in parts]))
+    print(f"{name} {mode}: {len(idx)} candidates, {time.time() - t0:.0f} s", flush=True)
+    return out
+
+
+def cfg4_samples():
+    o = orc.Oracle(workloads.config(4))
+    n_cfg, n_ord, n_b = len(o.configs()), o.n_orders(), len(workloads.config(4)["space"]["micro"])
+    keys = np.arange(n_cfg * n_ord)
+    thr = keys * n_b + keys % n_b
+    cfg = np.arange(n_cfg)
+    f1b = (cfg * n_ord + cfg % n_ord) * n_b + (cfg * 7) % n_b
+    return thr, f1b
+
+
+def types16_samples():
+    p = _problem("cfg3_types")
+    o = orc.Oracle(p)
+    per = o.n_orders() * len(p["space"]["micro"])
+    idx = [i for k, c in enumerate(o.configs()) if c[0] == 16 for i in range(k * per, (k + 1) * per)]
+    return np.array(idx[:: max(1, len(idx) // 16)][:16])
+
+
+def main():
+    workers = int(sys.argv[1]) if len(sys.argv) > 1 else (os.cpu_count() or 1)
+    out = {}
+    thr4, f1b4 = cfg4_samples()
+    with get_context("spawn").Pool(workers) as pool:
+        for n in (3, 5):
+            N = orc.Oracle(workloads.config(n)).n_instances()
+            idx = np.arange(N)
+            for mode in ("threshold", "1f1b"):
+                out[f"cfg{n}_{mode}_idx"] = idx
+                out[f"cfg{n}_{mode}"] = run(pool, f"cfg{n}", mode, idx, 500)
+        out["cfg4_threshold_idx"] = thr4
+        out["cfg4_threshold"] = run(pool, "cfg4", "threshold", thr4, 200)
+        out["cfg4_1f1b_idx"] = f1b4
+        out["cfg4_1f1b"] = run(pool, "cfg4", "1f1b", f1b4, 40)
+        t16 = types16_samples()
+        out["cfg3_types16_idx"] = t16
+        out["cfg3_types16"] = run(pool, "cfg3_types", "threshold", t16, 1)
+    np.savez_compressed(OUT, **out)
+    print("wrote", OUT, os.path.getsize(OUT), "bytes")
+
+
+if __name__ == "__main__":
+    main()
