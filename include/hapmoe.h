@@ -137,7 +137,14 @@ typedef struct hapmoe_space {
                             slot each (order 0 lays out the first sequence), solved by
                             hapmoe_stage_dp_types; at most 4096 count states prod_h (k_h + 1)
                             per pipeline, k_h = m_h / (G/PP).
-                            With 1 or 2, a space that leaves no configuration is
+                            3: per-stage data-parallel widths (the non-uniform PP/DP of
+                            Section 1): the block orderings of 0, but stage i takes the next
+                            w_i half-groups of G/(2 PP) devices, w_i in {1, 2, 3} with sum
+                            2 PP, and runs DP_i = w_i DP / 2 replicas, each holding 2 / w_i
+                            of the nominal tokens of a micro-batch; the widths are chosen by
+                            hapmoe_stage_dp_widths; only configurations with DP even and
+                            EP * TPE dividing G/(2 PP) take part.
+                            With 1, 2 or 3, a space that leaves no configuration is
                             HAPMOE_E_INVAL */
     int32_t n_micro;     /* entries of micro[] */
     int32_t micro[HAPMOE_MAX_MICRO]; /* microbatch counts B, 1..1024 */
@@ -275,7 +282,8 @@ int32_t hapmoe_stage_dp_ws_bytes(const hapmoe_problem *p, int64_t *bytes);
  * and slots are counted once, on the first of them.  d_ws
  * (hapmoe_stage_dp_ws_bytes)
  * holds the kernel's work queue: calls that may overlap need their own d_ws.
- * Problems with stage_types = 2 are HAPMOE_E_INVAL here (hapmoe_stage_dp_types).
+ * Problems with stage_types = 2 or 3 are HAPMOE_E_INVAL here
+ * (hapmoe_stage_dp_types, hapmoe_stage_dp_widths).
  * Asynchronous. */
 int32_t hapmoe_stage_dp(const hapmoe_problem *p, const void *d_image,
                         const hapmoe_candidate *d_cand, int64_t n_cand,
@@ -297,7 +305,7 @@ int32_t hapmoe_stage_dp(const hapmoe_problem *p, const void *d_image,
  * ties to the lower largest stage: objective = T + C, stage_sum and t_max of the
  * chosen partition, its recomputation mask and stage lengths.  d_stats as for
  * hapmoe_stage_dp (passes = DP passes of the frontier walk).  Not for
- * stage_types = 2 (HAPMOE_E_INVAL).  Asynchronous. */
+ * stage_types = 2 or 3 (HAPMOE_E_INVAL).  Asynchronous. */
 int32_t hapmoe_stage_dp_1f1b(const hapmoe_problem *p, const void *d_image,
                              const hapmoe_candidate *d_cand, int64_t n_cand,
                              const void *d_tables, int64_t tables_bytes,
@@ -348,14 +356,51 @@ int32_t hapmoe_stage_dp_types_1f1b(const hapmoe_problem *p, const void *d_image,
                                    hapmoe_dp_result *d_res, uint8_t *d_types, int32_t *d_stats,
                                    void *d_ws, int64_t ws_bytes, void *stream);
 
+/* Workspace of hapmoe_stage_dp_widths for a launch over `count` candidates: the
+ * work-queue counter and one slice of DP states per workgroup (at most 512).
+ * HAPMOE_E_INVAL unless stage_types = 3. */
+int32_t hapmoe_stage_dp_widths_ws_bytes(const hapmoe_problem *p, int64_t count, int64_t *bytes);
+
+/* Stage DP with per-stage data-parallel widths (stage_types = 3; the
+ * "non-uniform PP/DP partitioning" of Section 1 and the ablation of the
+ * evaluation: stage-wise parallelism knobs chosen jointly with the layers).
+ * The devices are listed type by type in the candidate's ordering; stage i takes
+ * the next w_i half-groups of G/(2 PP) devices, w_i in {1, 2, 3}, sum w_i = 2 PP,
+ * so it runs DP_i = w_i DP / 2 replicas; every stage processes the same global
+ * micro-batch, a replica holding r = 2 / w_i of the nominal tokens.  The stage's
+ * cost is the Section 3.2 model at that token count (compute tables scaled by r,
+ * router and collectives at the scaled activation), its memory the ZeRO-1 state
+ * over DP_i plus activations and MoE buffers at r, its outgoing transfer the
+ * sender's per-rank activation over the boundary link; pruning 1 uses the
+ * stage's share w_i P_i (G/(2 PP)) / sum_h m_h P_h of the cluster's compute,
+ * pruning 3 and the constant of Eq. 4 their nominal values (the constant of the
+ * uniform layout).  For each candidate of [first, first + count) it minimises
+ * sum_i c_i + (B-1) max_i c_i over the width sequences and partitions.  Ties:
+ * lowest threshold t*, then at each back-trace step from the last stage the
+ * smallest split point, then the smallest width.  Writes d_res[0 .. count)
+ * like hapmoe_stage_dp, d_types[32 * (0 .. count)] the device-type set of each
+ * stage and d_widths[32 * (0 .. count)] each w_i (0 past PP and for infeasible
+ * candidates).  d_stats (may be NULL): passes of the candidate's sweep and its
+ * relaxations (columns 2, 3 zero).  The tables must come from
+ * hapmoe_eval_cost_tables on the same problem (which adds the width tables).
+ * d_ws (hapmoe_stage_dp_widths_ws_bytes for count) is the kernel's: calls that
+ * may overlap need their own.  Asynchronous. */
+int32_t hapmoe_stage_dp_widths(const hapmoe_problem *p, const void *d_image,
+                               const hapmoe_candidate *d_cand, int64_t n_cand,
+                               const void *d_tables, int64_t tables_bytes,
+                               int64_t first, int64_t count,
+                               hapmoe_dp_result *d_res, uint8_t *d_types, uint8_t *d_widths,
+                               int32_t *d_stats, void *d_ws, int64_t ws_bytes, void *stream);
+
 /* Workspace of hapmoe_best_plan for n results. */
 int32_t hapmoe_best_plan_ws_bytes(const hapmoe_problem *p, int64_t n, int64_t *bytes);
 
 /* Segmented arg-min (Eq. 1 objective): per configuration pi the best of its
  * candidates (d_config_best, n_configs int64 entries: candidate index or -1;
  * may be NULL), then the global best by (objective, candidate index).  d_res
- * holds the results of candidates [0, n); with stage_types = 2, d_types holds
- * their stage types (hapmoe_stage_dp_types), otherwise it must be NULL.
+ * holds the results of candidates [0, n); with stage_types = 2 or 3, d_types
+ * holds their stage types (hapmoe_stage_dp_types / _widths; the winner's widths
+ * are d_widths[32 * instance]), otherwise it must be NULL.
  * Waits for `stream`, fills *h_plan.  Returns HAPMOE_E_INFEASIBLE if no
  * candidate is feasible. */
 int32_t hapmoe_best_plan(const hapmoe_problem *p, const hapmoe_candidate *d_cand,

@@ -18,6 +18,8 @@ static int64_t min64(int64_t a, int64_t b) { return a < b ? a : b; }
 static int64_t max64(int64_t a, int64_t b) { return a > b ? a : b; }
 static int lg2(int v) { int r = 0; while ((1 << r) < v) r++; return r; }
 static int popc(int v) { int c = 0; while (v) { c += v & 1; v >>= 1; } return c; }
+/* free per-stage device types (stage_types 1 and 2): every stage one type's group */
+static int free_types(const orc_problem *p) { return p->stage_types == 1 || p->stage_types == 2; }
 
 int32_t orc_validate(const orc_problem *p)
 {
@@ -41,7 +43,7 @@ int32_t orc_validate(const orc_problem *p)
     if (p->prune_window < 0 || p->prune_window > 2) return -1;
     if (p->n_micro < 1 || p->n_micro > ORC_MAX_MICRO) return -1;
     if (p->pp_max < 1 || p->pp_max > ORC_MAX_STAGES || p->mode < 0 || p->mode > 1) return -1;
-    if (p->stage_types < 0 || p->stage_types > 2) return -1;
+    if (p->stage_types < 0 || p->stage_types > 3) return -1;
     for (int i = 0; i < p->n_micro; i++)
         if (p->micro[i] < 1 || p->micro[i] > (1 << 20)) return -1;
     return 0;
@@ -66,7 +68,7 @@ int64_t orc_enumerate(const orc_problem *p, orc_config *out, int64_t cap)
     for (int PP = 1; PP <= G; PP++) {
         if (G % PP != 0 || PP > p->pp_max || PP > p->n_layers) continue;
         int g = G / PP;
-        if (p->stage_types) {   /* free per-stage type: every stage is one type's group */
+        if (free_types(p)) {   /* free per-stage type: every stage is one type's group */
             int whole = 1;
             for (int h = 0; h < p->n_types; h++) whole &= p->count[h] % g == 0;
             if (!whole) continue;
@@ -91,6 +93,9 @@ int64_t orc_enumerate(const orc_problem *p, orc_config *out, int64_t cap)
                             if (g % prod != 0) continue;
                             DP = g / prod;
                         }
+                        /* per-stage widths: half a group must hold whole replicas and
+                         * whole expert groups (DP even, EP * TPE | g / 2) */
+                        if (p->stage_types == 3 && (DP % 2 != 0 || (g / 2) % (EP * TPE) != 0)) continue;
                         if (out && n < cap) {
                             orc_config c = {PP, TP, CP, DP, EP, TPE};
                             out[n] = c;
@@ -128,7 +133,7 @@ static int64_t n_sequences(const orc_problem *p, int pp)
 int32_t orc_n_orders(const orc_problem *p)
 {
     if (p->stage_types == 2) return 1;   /* the DP over device counts picks the sequence */
-    if (p->stage_types) {
+    if (p->stage_types == 1) {
         int64_t ncfg = orc_enumerate(p, NULL, 0), best = 1;
         orc_config *all = (orc_config *)malloc(sizeof(orc_config) * (size_t)(ncfg > 0 ? ncfg : 1));
         orc_enumerate(p, all, ncfg);
@@ -410,7 +415,7 @@ int32_t orc_stages(const orc_problem *p, const orc_config *c, int32_t order, int
 {
     int perm[ORC_MAX_TYPES];
     int32_t seq[ORC_MAX_STAGES];
-    if (p->stage_types) {   /* free per-stage type: stage s is one group of type seq[s] */
+    if (free_types(p)) {   /* free per-stage type: stage s is one group of type seq[s] */
         if (orc_sequence(p, c->pp, order, seq)) return -1;
     } else {
         orc_order(p, order, perm);
@@ -423,7 +428,7 @@ int32_t orc_stages(const orc_problem *p, const orc_config *c, int32_t order, int
         orc_stage *x = &st[s];
         int lo = s * g, hi = lo + g;
         x->mask = 0;
-        if (p->stage_types) {
+        if (free_types(p)) {
             x->mask = 1 << seq[s];
             x->first_type = x->last_type = seq[s];
         } else {
@@ -441,7 +446,7 @@ int32_t orc_stages(const orc_problem *p, const orc_config *c, int32_t order, int
         mask_link(p, x->mask, &x->alpha, &x->bw);
         x->mixed = popc(x->mask) > 1;
         if (s < PP - 1) {
-            int nt = p->stage_types ? seq[s + 1] : dev_type(p, perm, hi);
+            int nt = free_types(p) ? seq[s + 1] : dev_type(p, perm, hi);
             x->bdiff = nt != x->last_type;
             x->p2p = orc_p2p(p, c, x->last_type, nt);
         } else {
@@ -1643,6 +1648,471 @@ int32_t orc_type_costs(const orc_problem *p, int64_t idx, int64_t *cost, uint8_t
     return 0;
 }
 
+/* ------------------------------------------------------------------------
+ * Per-stage data-parallel widths (stage_types = 3): the non-uniform PP/DP
+ * partitioning of the paper's contributions and its ablation ("stage-wise
+ * parallelism knobs" chosen jointly with the layers).  The cost model of
+ * Section 3.2 has no terms for stages of unequal width; the readings here:
+ *  - the devices are listed type by type in the ordering, as for the block
+ *    layout, and stage i takes the next w_i half-groups (g/2 devices each,
+ *    g = G/PP), w_i in {1, 2, 3}, sum w_i = 2 PP: every device is used and the
+ *    stage has DP_i = w_i DP / 2 replicas (TP, CP, EP, TPE as in pi; the
+ *    configurations with DP even and EP * TPE | g/2);
+ *  - every stage processes the same global micro-batch of DP * mbs sequences,
+ *    split over its DP_i replicas: a replica holds r = 2 / w_i of the nominal
+ *    tokens, so every per-layer term is evaluated at T = (S mbs / CP) r tokens
+ *    per rank -- compute and expert tables scaled by r (they are profiled per
+ *    micro-batch of mbs sequences), router and collectives at that token count;
+ *  - memory: ZeRO-1 optimizer state over DP_i (beta_opt = 6 + 12 / DP_i),
+ *    activations and MoE buffers at r;
+ *  - the boundary transfer is the sender's per-rank activation over the link
+ *    of the boundary's two device types;
+ *  - pruning-1 windows from the stage's share of the cluster's compute,
+ *    w_i P_i (g/2) / sum_h m_h P_h (the share among the stages when every stage
+ *    is of one type); pruning 3 with the nominal T-bar; T_dp-sync + T_opt at
+ *    the nominal width (the gradient sync folded into the constant, as in the
+ *    uniform model).
+ * A candidate's DP chooses the widths with the layers: state (stage, end
+ * layer, half-groups used).
+ * ---------------------------------------------------------------------- */
+static double w_tokens(const orc_problem *p, const orc_config *c, double r) { return tokens(p, c) * r; }
+
+static double w_act(const orc_problem *p, const orc_config *c, double r)
+{
+    return (w_tokens(p, c, r) * (double)p->hidden) * (double)p->elem_bytes;
+}
+
+/* Eq. 2 at r times the nominal tokens (compute and expert tables scale with them) */
+static void w_type_terms(const orc_problem *p, const orc_config *c, int layer, int h, double r, orc_type_terms *o)
+{
+    int64_t off = (((int64_t)h * 4 + lg2(c->tp)) * 4 + lg2(c->cp)) * p->n_layers + layer;
+    double td = (double)p->t_dense[off], tf = (double)p->t_ffn[off];
+    if (!p->is_moe[layer]) {
+        o->comp = td * r;
+        o->expert = 0.0;
+    } else {
+        double route = p->route_coef[h] * (w_tokens(p, c, r) * (double)p->hidden);
+        o->comp = (td - tf) * r + route;
+        double xexp = (p->moe_ffn_mult * (tf * r)) / ((p->eff[h] * (double)c->ep) * (double)c->tpe);
+        o->expert = skew(p, layer) * xexp;
+    }
+    o->q_comp = q(o->comp);
+    o->q_expert = q(o->expert);
+}
+
+/* dispatch / TP / CP terms and stage times of one layer at r (as orc_mask_terms_eval) */
+static void w_mask_terms(const orc_problem *p, const orc_config *c, int layer, int mask, double r, orc_mask_terms *o)
+{
+    double alpha, bw;
+    mask_link(p, mask, &alpha, &bw);
+    double D = w_act(p, c, r);
+    if (!p->is_moe[layer]) {
+        o->a2a = 0.0;
+        o->tp = 4.0 * ring_allreduce(D, c->tp, alpha, bw);
+    } else {
+        double sk = skew(p, layer);
+        double dm = (D * (double)p->top_k) * (1.0 - 1.0 / (double)c->ep);
+        double f_a2a = (double)(c->ep - 1) * alpha + dm / bw;
+        double f_ag = (double)(c->ep - 1) * alpha + (D * (double)(c->ep - 1)) / bw;
+        o->a2a = sk * (4.0 * (f_ag < f_a2a ? f_ag : f_a2a));
+        o->tp = 2.0 * ring_allreduce(D, c->tp, alpha, bw) + 2.0 * ring_allreduce(D, c->tpe, alpha, bw);
+    }
+    o->cp = c->cp == 1 ? 0.0 : 3.0 * ((double)(c->cp - 1) * (alpha + ((2.0 * D) / (double)c->tp) / bw));
+    o->q_a2a = q(o->a2a);
+    o->q_tp = q(o->tp);
+    o->q_cp = q(o->cp);
+    o->comm = o->q_a2a + o->q_tp + o->q_cp;
+    int64_t ce = -1;
+    for (int h = 0; h < p->n_types; h++) {
+        if (!((mask >> h) & 1)) continue;
+        orc_type_terms t;
+        w_type_terms(p, c, layer, h, r, &t);
+        if (t.q_comp + t.q_expert > ce) ce = t.q_comp + t.q_expert;
+    }
+    o->t_r0 = ce + o->comm;
+    o->t_r1 = q(p->rc_time * (double)o->t_r0);
+}
+
+/* memory of one layer on a stage of dp_i replicas at r */
+static void w_mem_terms(const orc_problem *p, const orc_config *c, int layer, int dp_i, double r, orc_mem_terms *o)
+{
+    double beta_opt = 6.0 + 12.0 / (double)dp_i;
+    o->w = ((double)p->params_dense[layer] / (double)c->tp +
+            (double)p->params_expert[layer] / (double)(c->ep * c->tpe)) * beta_opt;
+    o->a0 = ((double)p->act_bytes[layer] * r) / (double)(c->tp * c->cp);
+    o->q_w = q(o->w);
+    o->q_a0 = q(o->a0);
+    o->q_a1 = q(p->rc_act * (double)o->q_a0);
+}
+
+static int64_t w_x_bytes(const orc_problem *p, const orc_config *c, double r)
+{
+    double dm = (w_act(p, c, r) * (double)p->top_k) * (1.0 - 1.0 / (double)c->ep);
+    return q(((8.0 * w_tokens(p, c, r)) * (double)p->top_k) + 2.0 * dm);
+}
+
+static int64_t w_p2p(const orc_problem *p, const orc_config *c, int h_from, int h_to, double r)
+{
+    double al = p->alpha[h_from * ORC_MAX_TYPES + h_to], bw = p->bw[h_from * ORC_MAX_TYPES + h_to];
+    return q(2.0 * (al + (w_act(p, c, r) / (double)c->tp) / bw));
+}
+
+/* token share of a replica of a width-w stage: r = 2 / w */
+static double w_ratio(int w) { return 2.0 / (double)w; }
+
+/* the stage of half-groups [u, u + w) as stage s of the pipeline */
+static void w_stage(const orc_problem *p, const orc_config *c, const int *perm, int s, int u, int w, int micro,
+                    orc_stage *x)
+{
+    int G = 0;
+    int64_t total_speed = 0;
+    for (int h = 0; h < p->n_types; h++) {
+        G += p->count[h];
+        total_speed += (int64_t)p->count[h] * p->speed[h];
+    }
+    int PP = c->pp, half = G / PP / 2, lo = u * half, hi = (u + w) * half;
+    x->mask = 0;
+    for (int d = lo; d < hi; d++) x->mask |= 1 << dev_type(p, perm, d);
+    x->first_type = dev_type(p, perm, lo);
+    x->last_type = dev_type(p, perm, hi - 1);
+    x->cap = -1;
+    x->speed = 0;
+    for (int h = 0; h < p->n_types; h++) {
+        if (!((x->mask >> h) & 1)) continue;
+        if (x->cap < 0 || p->mem_bytes[h] < x->cap) x->cap = p->mem_bytes[h];
+        if (x->speed == 0 || p->speed[h] < x->speed) x->speed = p->speed[h];
+    }
+    mask_link(p, x->mask, &x->alpha, &x->bw);
+    x->mixed = popc(x->mask) > 1;
+    if (u + w < 2 * PP) {
+        int nt = dev_type(p, perm, hi);
+        x->bdiff = nt != x->last_type;
+        x->p2p = w_p2p(p, c, x->last_type, nt, w_ratio(w));
+    } else {
+        x->bdiff = 0;
+        x->p2p = 0;
+    }
+    x->m_store = min64(PP - s, micro);
+    int64_t N = p->n_layers, dn = p->delta_num, dd = p->delta_den;
+    if (p->prune_window == 1) {
+        /* share w P (g/2) / sum_h m_h P_h of the cluster's compute */
+        int64_t num = (int64_t)w * x->speed * half * N, den = dd * total_speed;
+        x->lo = (int32_t)max64(1, ((dd - dn) * num) / den);
+        x->hi = (int32_t)min64(N, ((dd + dn) * num + den - 1) / den);
+    } else if (p->prune_window == 2) {
+        x->lo = (int32_t)(N / PP);
+        x->hi = (int32_t)((N + PP - 1) / PP);
+    } else {
+        x->lo = 1;
+        x->hi = (int32_t)N;
+    }
+}
+
+/* the width-scaled terms of one layer, for the tests */
+void orc_width_terms(const orc_problem *p, const orc_config *c, int32_t layer, int32_t mask, int32_t w,
+                     orc_type_terms *type_out, orc_mask_terms *mask_out, orc_mem_terms *mem_out, int64_t *x_bytes)
+{
+    double r = w_ratio(w);
+    for (int h = 0; h < p->n_types; h++) w_type_terms(p, c, layer, h, r, &type_out[h]);
+    w_mask_terms(p, c, layer, mask, r, mask_out);
+    w_mem_terms(p, c, layer, c->dp * w / 2, r, mem_out);
+    *x_bytes = w_x_bytes(p, c, r);
+}
+
+/* the stage of half-groups [u, u + w) as stage s (layout, window, boundary), for the tests */
+int32_t orc_width_stage(const orc_problem *p, const orc_config *c, int32_t order, int32_t s, int32_t u, int32_t w,
+                        int32_t micro, orc_stage *x)
+{
+    if (w < 1 || w > 3 || u < 0 || u + w > 2 * c->pp) return -1;
+    int perm[ORC_MAX_TYPES];
+    orc_order(p, order, perm);
+    w_stage(p, c, perm, s, u, w, micro, x);
+    return 0;
+}
+
+/* Cost tensor of a width-mode candidate: [pp][2pp + 1][3][n + 1][n + 1], entry
+ * (s, u, w - 1, a, b) = c_s(a, b) of stage s on half-groups [u, u + w) */
+int32_t orc_width_costs(const orc_problem *p, int64_t idx, int64_t *cost, uint8_t *rflag)
+{
+    orc_config c;
+    int32_t order, micro;
+    if (p->stage_types != 3 || orc_instance(p, idx, &c, &order, &micro)) return -1;
+    int perm[ORC_MAX_TYPES];
+    orc_order(p, order, perm);
+    int N = p->n_layers, W = N + 1, PP = c.pp, U = 2 * PP;
+    orc_pi_terms pt;
+    orc_pi_terms_eval(p, &c, &pt);   /* the nominal T-bar */
+    prefixes P;
+    for (int w = 1; w <= 3; w++) {
+        double r = w_ratio(w);
+        orc_pi_terms ptw = pt;
+        ptw.x_bytes = w_x_bytes(p, &c, r);
+        int dp_i = c.dp * w / 2;
+        P.n = N;
+        P.w = calloc((size_t)W, 8);
+        P.a0 = calloc((size_t)W, 8);
+        P.a1 = calloc((size_t)W, 8);
+        P.moe = calloc((size_t)W, 8);
+        P.t0 = calloc((size_t)W, 8);
+        P.t1 = calloc((size_t)W, 8);
+        P.comm = calloc((size_t)W, 8);
+        for (int l = 0; l < N; l++) {
+            orc_mem_terms m;
+            w_mem_terms(p, &c, l, dp_i, r, &m);
+            P.w[l + 1] = P.w[l] + m.q_w;
+            P.a0[l + 1] = P.a0[l] + m.q_a0;
+            P.a1[l + 1] = P.a1[l] + m.q_a1;
+            P.moe[l + 1] = P.moe[l] + (p->is_moe[l] ? 1 : 0);
+        }
+        for (int s = 0; s < PP; s++)
+            for (int u = 0; u <= U; u++) {
+                int64_t base = (((int64_t)s * (U + 1) + u) * 3 + (w - 1)) * W * W;
+                int ok = u + w <= U;
+                orc_stage x;
+                if (ok) {
+                    w_stage(p, &c, perm, s, u, w, micro, &x);
+                    for (int l = 0; l < N; l++) {
+                        orc_mask_terms m;
+                        w_mask_terms(p, &c, l, x.mask, r, &m);
+                        P.t0[l + 1] = P.t0[l] + m.t_r0;
+                        P.t1[l + 1] = P.t1[l] + m.t_r1;
+                        P.comm[l + 1] = P.comm[l] + m.comm;
+                    }
+                }
+                for (int a = 0; a < W; a++)
+                    for (int b = 0; b < W; b++) {
+                        uint8_t rr = 0;
+                        cost[base + (int64_t)a * W + b] = ok ? segment_cost(p, &ptw, &x, &P, a, b, &rr) : ORC_INF;
+                        rflag[base + (int64_t)a * W + b] = rr;
+                    }
+            }
+        prefixes_free(&P);
+    }
+    return 0;
+}
+
+/* Threshold DP over (stage, end layer, half-groups used): F_t[i][b][u] = the
+ * least stage sum placing layers [0, b) on stages 1..i that use u half-groups,
+ * every stage cost <= t; ties keep the smallest split point a, then the
+ * smallest width.  OPT = min over t of F_t[pp][n][2pp] + (B-1) t, the sweep and
+ * t* as in orc_dp; the back-trace at t* gives the lexicographically smallest
+ * ((b_{pp-1}, w_pp), (b_{pp-2}, w_{pp-1}), ..., (0, w_1)) among the optima. */
+static int64_t w_pass(int pp, int n, const int64_t *cost, int64_t t, int64_t *F, int16_t *arg)
+{
+    int W = n + 1, U = 2 * pp;
+    for (int i = 0; i <= pp; i++)
+        for (int b = 0; b < W; b++)
+            for (int u = 0; u <= U; u++) F[((int64_t)i * W + b) * (U + 1) + u] = (i == 0 && b == 0 && u == 0) ? 0 : ORC_INF;
+    for (int i = 1; i <= pp; i++)
+        for (int b = 1; b < W; b++)
+            for (int u = 1; u <= U; u++) {
+                int64_t best = ORC_INF;
+                int arg_best = -1;
+                for (int a = 0; a < b; a++)
+                    for (int w = 1; w <= 3 && w <= u; w++) {
+                        int64_t prev = F[((int64_t)(i - 1) * W + a) * (U + 1) + (u - w)];
+                        int64_t cst = cost[((((int64_t)(i - 1) * (U + 1) + (u - w)) * 3 + (w - 1)) * W + a) * W + b];
+                        if (prev == ORC_INF || cst == ORC_INF || cst > t) continue;
+                        if (prev + cst < best) {
+                            best = prev + cst;
+                            arg_best = a * 4 + w;
+                        }
+                    }
+                F[((int64_t)i * W + b) * (U + 1) + u] = best;
+                arg[((int64_t)i * W + b) * (U + 1) + u] = (int16_t)arg_best;
+            }
+    return F[((int64_t)pp * W + n) * (U + 1) + U];
+}
+
+int32_t orc_dp_widths(int32_t pp, int32_t n, int64_t micro, const int64_t *cost, orc_result *r)
+{
+    int W = n + 1, U = 2 * pp;
+    int64_t ncost = (int64_t)pp * (U + 1) * 3 * W * W, nstate = (int64_t)(pp + 1) * W * (U + 1);
+    memset(r, 0, sizeof(*r));
+    r->pp = pp;
+    int64_t *theta = malloc(sizeof(int64_t) * (size_t)(ncost + 1));
+    int64_t nt = 0;
+    for (int64_t i = 0; i < ncost; i++)
+        if (cost[i] != ORC_INF) theta[nt++] = cost[i];
+    qsort(theta, (size_t)nt, sizeof(int64_t), cmp_i64);
+    int64_t u = 0;
+    for (int64_t i = 0; i < nt; i++)
+        if (u == 0 || theta[i] != theta[u - 1]) theta[u++] = theta[i];
+    int64_t *F = malloc(sizeof(int64_t) * (size_t)nstate);
+    int16_t *arg = malloc(sizeof(int16_t) * (size_t)nstate);
+    int64_t finf = pp <= n ? w_pass(pp, n, cost, ORC_INF, F, arg) : ORC_INF;
+    int64_t best = ORC_INF, tstar = -1, swept = 0;
+    for (int64_t k = 0; k < u && finf != ORC_INF; k++) {
+        int64_t t = theta[k];
+        if (finf + (micro - 1) * t >= best) break;
+        int64_t f = w_pass(pp, n, cost, t, F, arg);
+        swept++;
+        if (f == ORC_INF) continue;
+        if (f + (micro - 1) * t < best) {
+            best = f + (micro - 1) * t;
+            tstar = t;
+        }
+    }
+    r->thresholds = swept;
+    if (tstar < 0) {
+        r->status = 1;
+        r->opt = r->sum = r->tmax = ORC_INF;
+    } else {
+        r->sum = w_pass(pp, n, cost, tstar, F, arg);
+        r->tmax = tstar;
+        r->opt = best;
+        int b = n, uu = U;
+        for (int i = pp; i >= 1; i--) {
+            int x = arg[((int64_t)i * W + b) * (U + 1) + uu], a = x / 4, w = x % 4;
+            r->layers[i - 1] = (uint8_t)(b - a);
+            r->width[i - 1] = (uint8_t)w;
+            b = a;
+            uu -= w;
+        }
+    }
+    free(theta);
+    free(F);
+    free(arg);
+    return 0;
+}
+
+/* Brute force: every width sequence (w_i in {1, 2, 3}, sum 2 pp) and every
+ * composition; key (sum + (B-1) max, max, then (b_{pp-1}, w_pp), (b_{pp-2},
+ * w_{pp-1}), ...) ascending. */
+typedef struct w_brute {
+    int pp, n, W, U;
+    int64_t micro;
+    const int64_t *cost;
+    int b[ORC_MAX_STAGES + 1], w[ORC_MAX_STAGES];
+    int best_b[ORC_MAX_STAGES + 1], best_w[ORC_MAX_STAGES];
+    int64_t best_obj, best_max, best_sum;
+    int found;
+} w_brute;
+
+static int w_brute_better(const w_brute *x, int64_t obj, int64_t mx)
+{
+    if (!x->found) return 1;
+    if (obj != x->best_obj) return obj < x->best_obj;
+    if (mx != x->best_max) return mx < x->best_max;
+    for (int i = x->pp - 1; i >= 0; i--) {
+        if (x->b[i] != x->best_b[i]) return x->b[i] < x->best_b[i];
+        if (x->w[i] != x->best_w[i]) return x->w[i] < x->best_w[i];
+    }
+    return 0;
+}
+
+static void w_brute_parts(w_brute *x, int i)
+{
+    if (i == x->pp) {
+        int64_t sum = 0, mx = 0;
+        int u = 0;
+        for (int k = 0; k < x->pp; k++) {
+            int64_t c = x->cost[((((int64_t)k * (x->U + 1) + u) * 3 + (x->w[k] - 1)) * x->W + x->b[k]) * x->W + x->b[k + 1]];
+            if (c == ORC_INF) return;
+            sum += c;
+            if (c > mx) mx = c;
+            u += x->w[k];
+        }
+        int64_t obj = sum + (x->micro - 1) * mx;
+        if (w_brute_better(x, obj, mx)) {
+            x->found = 1;
+            x->best_obj = obj;
+            x->best_max = mx;
+            x->best_sum = sum;
+            memcpy(x->best_b, x->b, sizeof(x->b));
+            memcpy(x->best_w, x->w, sizeof(x->w));
+        }
+        return;
+    }
+    if (i == x->pp - 1) {
+        x->b[i + 1] = x->n;
+        if (x->b[i] < x->n) w_brute_parts(x, i + 1);
+        return;
+    }
+    for (int e = x->b[i] + 1; e <= x->n - (x->pp - 1 - i); e++) {
+        x->b[i + 1] = e;
+        w_brute_parts(x, i + 1);
+    }
+}
+
+static void w_brute_seq(w_brute *x, int i, int used)
+{
+    if (i == x->pp) {
+        if (used == x->U) w_brute_parts(x, 0);
+        return;
+    }
+    for (int w = 1; w <= 3; w++) {
+        x->w[i] = w;
+        w_brute_seq(x, i + 1, used + w);
+    }
+}
+
+int32_t orc_brute_widths(int32_t pp, int32_t n, int64_t micro, const int64_t *cost, orc_result *r)
+{
+    memset(r, 0, sizeof(*r));
+    r->pp = pp;
+    w_brute x;
+    memset(&x, 0, sizeof(x));
+    x.pp = pp;
+    x.n = n;
+    x.W = n + 1;
+    x.U = 2 * pp;
+    x.micro = micro;
+    x.cost = cost;
+    if (pp <= n) w_brute_seq(&x, 0, 0);
+    if (!x.found) {
+        r->status = 1;
+        r->opt = r->sum = r->tmax = ORC_INF;
+        return 0;
+    }
+    r->opt = x.best_obj;
+    r->sum = x.best_sum;
+    r->tmax = x.best_max;
+    for (int i = 0; i < pp; i++) {
+        r->layers[i] = (uint8_t)(x.best_b[i + 1] - x.best_b[i]);
+        r->width[i] = (uint8_t)x.best_w[i];
+    }
+    return 0;
+}
+
+static int32_t solve_widths(const orc_problem *p, int64_t idx, orc_result *r, int mode)
+{
+    orc_config c;
+    int32_t order, micro;
+    if (mode > 1 || orc_instance(p, idx, &c, &order, &micro)) return -1;
+    int W = p->n_layers + 1, U = 2 * c.pp;
+    int64_t ncost = (int64_t)c.pp * (U + 1) * 3 * W * W;
+    int64_t *cost = malloc(sizeof(int64_t) * (size_t)ncost);
+    uint8_t *rf = malloc((size_t)ncost);
+    orc_width_costs(p, idx, cost, rf);
+    if (mode == 0)
+        orc_dp_widths(c.pp, p->n_layers, micro, cost, r);
+    else
+        orc_brute_widths(c.pp, p->n_layers, micro, cost, r);
+    /* T_dp-sync + T_opt of the uniform layout of the same (pi, ordering) */
+    orc_problem q0 = *p;
+    q0.stage_types = 0;
+    r->dp_const = orc_dp_const(&q0, &c, order);
+    if (r->status == 0) {
+        r->opt += r->dp_const;
+        int perm[ORC_MAX_TYPES];
+        orc_order(p, order, perm);
+        int a = 0, u = 0;
+        for (int i = 0; i < c.pp; i++) {
+            int b = a + r->layers[i], w = r->width[i];
+            orc_stage x;
+            w_stage(p, &c, perm, i, u, w, micro, &x);
+            r->stage_mask[i] = (uint8_t)x.mask;
+            r->recompute[i] = rf[((((int64_t)i * (U + 1) + u) * 3 + (w - 1)) * W + a) * W + b];
+            a = b;
+            u += w;
+        }
+    }
+    free(cost);
+    free(rf);
+    return 0;
+}
+
 /* mode: 0 threshold DP, 1 its brute force, 2 1F1B re-scoring, 3 its brute force */
 static int32_t solve_types(const orc_problem *p, int64_t idx, orc_result *r, int mode)
 {
@@ -1690,6 +2160,7 @@ static int32_t solve_with(const orc_problem *p, int64_t idx, orc_result *r, int 
         if (mode > 3) return -1;
         return solve_types(p, idx, r, mode);
     }
+    if (p->stage_types == 3) return solve_widths(p, idx, r, mode);   /* per-stage widths */
     orc_config c;
     int32_t order, micro;
     if (orc_instance(p, idx, &c, &order, &micro)) return -1;

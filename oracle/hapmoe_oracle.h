@@ -64,7 +64,9 @@ typedef struct orc_problem {
     int32_t pp_max, tp_mask, cp_mask, ep_max, tpe_mask, mode;
     int32_t stage_types;           /* 0: block orderings of the types; 1: free per-stage type, one
                                       candidate per stage-type sequence; 2: free per-stage type
-                                      chosen by the DP over device counts (one order slot) */
+                                      chosen by the DP over device counts (one order slot);
+                                      3: block orderings with per-stage data-parallel widths
+                                      chosen by the DP (w_i half-groups, w_i in {1, 2, 3}) */
     int32_t n_micro;
     int32_t micro[ORC_MAX_MICRO];
 } orc_problem;
@@ -115,6 +117,7 @@ typedef struct orc_result {
     uint8_t layers[ORC_MAX_STAGES];
     uint8_t recompute[ORC_MAX_STAGES];
     uint8_t stage_mask[ORC_MAX_STAGES];
+    uint8_t width[ORC_MAX_STAGES];   /* per-stage widths (stage_types = 3): half-groups of stage i */
 } orc_result;
 
 int32_t orc_validate(const orc_problem *p);
@@ -160,6 +163,20 @@ int32_t orc_brute_exact(int32_t pp, int32_t n, int64_t micro, const int64_t *cos
 int32_t orc_solve_exact(const orc_problem *p, int64_t idx, orc_result *r);
 int32_t orc_solve_exact_many(const orc_problem *p, const int64_t *idx, int64_t n, orc_result *r);
 int32_t orc_solve_exact_brute(const orc_problem *p, int64_t idx, orc_result *r);
+
+/* Per-stage data-parallel widths (stage_types = 3): cost tensor
+ * [pp][2pp + 1][3][n + 1][n + 1], entry (s, u, w - 1, a, b) = the cost of stage
+ * s on half-groups [u, u + w) and layers [a, b); the threshold DP over (stage,
+ * end layer, half-groups used) and its brute force over every width sequence
+ * and composition; r->width gets w_i. */
+int32_t orc_width_costs(const orc_problem *p, int64_t idx, int64_t *cost, uint8_t *rflag);
+/* the width-w terms of one layer (type_out[T]) and the layout of a width stage */
+void orc_width_terms(const orc_problem *p, const orc_config *c, int32_t layer, int32_t mask, int32_t w,
+                     orc_type_terms *type_out, orc_mask_terms *mask_out, orc_mem_terms *mem_out, int64_t *x_bytes);
+int32_t orc_width_stage(const orc_problem *p, const orc_config *c, int32_t order, int32_t s, int32_t u, int32_t w,
+                        int32_t micro, orc_stage *x);
+int32_t orc_dp_widths(int32_t pp, int32_t n, int64_t micro, const int64_t *cost, orc_result *r);
+int32_t orc_brute_widths(int32_t pp, int32_t n, int64_t micro, const int64_t *cost, orc_result *r);
 
 /* The least 1F1B latency over every partition (not only the frontier's): r->opt
  * = least orc_latency_1f1b, ties to the lower largest stage, then the

@@ -80,7 +80,7 @@ class OrcResult(C.Structure):
     _fields_ = [("status", C.c_int32), ("pp", C.c_int32), ("opt", C.c_int64), ("sum", C.c_int64),
                 ("tmax", C.c_int64), ("dp_const", C.c_int64), ("thresholds", C.c_int64),
                 ("layers", C.c_uint8 * MAX_STAGES), ("recompute", C.c_uint8 * MAX_STAGES),
-                ("stage_mask", C.c_uint8 * MAX_STAGES)]
+                ("stage_mask", C.c_uint8 * MAX_STAGES), ("width", C.c_uint8 * MAX_STAGES)]
 
 
 _LIB = None
@@ -132,6 +132,14 @@ def lib():
         L.orc_solve_exact.argtypes = [P(OrcProblem), C.c_int64, P(OrcResult)]
         L.orc_solve_exact_brute.argtypes = [P(OrcProblem), C.c_int64, P(OrcResult)]
         L.orc_solve_exact_many.argtypes = [P(OrcProblem), C.c_void_p, C.c_int64, P(OrcResult)]
+        L.orc_width_costs.argtypes = [P(OrcProblem), C.c_int64, C.c_void_p, C.c_void_p]
+        L.orc_width_terms.argtypes = [P(OrcProblem), P(OrcConfig), C.c_int32, C.c_int32, C.c_int32,
+                                      P(OrcTypeTerms), P(OrcMaskTerms), P(OrcMemTerms), P(C.c_int64)]
+        L.orc_width_terms.restype = None
+        L.orc_width_stage.argtypes = [P(OrcProblem), P(OrcConfig), C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                                      C.c_int32, P(OrcStage)]
+        for name in ("orc_dp_widths", "orc_brute_widths"):
+            getattr(L, name).argtypes = [C.c_int32, C.c_int32, C.c_int64, C.c_void_p, P(OrcResult)]
         for name in ("orc_dp_latency", "orc_brute_latency"):
             getattr(L, name).argtypes = [C.c_int32, C.c_int32, C.c_int64, C.c_void_p, P(OrcResult)]
         for name in ("orc_solve_latency", "orc_solve_latency_brute"):
@@ -154,7 +162,7 @@ def result_dict(r: OrcResult) -> dict:
     return {"status": r.status, "pp": pp, "opt": r.opt, "sum": r.sum, "tmax": r.tmax,
             "dp_const": r.dp_const, "thresholds": r.thresholds,
             "layers": list(r.layers[:pp]), "recompute": list(r.recompute[:pp]),
-            "stage_mask": list(r.stage_mask[:pp])}
+            "stage_mask": list(r.stage_mask[:pp]), "width": list(r.width[:pp])}
 
 
 class Oracle:
@@ -277,6 +285,34 @@ class Oracle:
         cost = np.zeros((pp, T, T + 1, W, W), dtype=np.int64)
         rflag = np.zeros((pp, T, T + 1, W, W), dtype=np.uint8)
         if self.L.orc_type_costs(C.byref(self.P), idx, _ptr(cost), _ptr(rflag)) != 0:
+            raise IndexError(idx)
+        return cost, rflag
+
+    def width_terms(self, cfg, layer, mask, w):
+        """Per-stage widths: the terms of one layer on a width-w stage (w half-groups)."""
+        T = self.P.n_types
+        tt = (OrcTypeTerms * T)()
+        mt, me, x = OrcMaskTerms(), OrcMemTerms(), C.c_int64(0)
+        self.L.orc_width_terms(C.byref(self.P), C.byref(self._cfg(cfg)), layer, mask, w, tt, C.byref(mt),
+                               C.byref(me), C.byref(x))
+        return {"type": [{k: getattr(t, k) for k, _ in t._fields_} for t in tt],
+                "mask": {k: getattr(mt, k) for k, _ in mt._fields_},
+                "mem": {k: getattr(me, k) for k, _ in me._fields_}, "x_bytes": x.value}
+
+    def width_stage(self, cfg, order, s, u, w, micro):
+        x = OrcStage()
+        if self.L.orc_width_stage(C.byref(self.P), C.byref(self._cfg(cfg)), order, s, u, w, micro, C.byref(x)) != 0:
+            raise IndexError((s, u, w))
+        return {k: getattr(x, k) for k, _ in x._fields_}
+
+    def width_costs(self, idx):
+        """Per-stage widths (stage_types = 3): cost[s][u][w-1][a][b] and the recomputation flags."""
+        cfgs = self.configs()
+        pp = cfgs[idx // (self.n_orders() * self.P.n_micro)][0]
+        W = self.P.n_layers + 1
+        cost = np.zeros((pp, 2 * pp + 1, 3, W, W), dtype=np.int64)
+        rflag = np.zeros((pp, 2 * pp + 1, 3, W, W), dtype=np.uint8)
+        if self.L.orc_width_costs(C.byref(self.P), idx, _ptr(cost), _ptr(rflag)) != 0:
             raise IndexError(idx)
         return cost, rflag
 
@@ -403,6 +439,24 @@ def brute_exact(pp, n, micro, cost):
     return result_dict(r)
 
 
+def dp_widths(pp, n, micro, cost):
+    """Per-stage widths: the threshold DP on an explicit tensor [pp][2pp+1][3][n+1][n+1]."""
+    cost = np.ascontiguousarray(cost, dtype=np.int64)
+    assert cost.shape == (pp, 2 * pp + 1, 3, n + 1, n + 1)
+    r = OrcResult()
+    lib().orc_dp_widths(pp, n, micro, _ptr(cost), C.byref(r))
+    return result_dict(r)
+
+
+def brute_widths(pp, n, micro, cost):
+    """Brute force over every width sequence and composition on the same tensor."""
+    cost = np.ascontiguousarray(cost, dtype=np.int64)
+    assert cost.shape == (pp, 2 * pp + 1, 3, n + 1, n + 1)
+    r = OrcResult()
+    lib().orc_brute_widths(pp, n, micro, _ptr(cost), C.byref(r))
+    return result_dict(r)
+
+
 def dp_latency(pp, n, micro, cost):
     """The least 1F1B latency over every partition of an explicit cost tensor."""
     cost = np.ascontiguousarray(cost, dtype=np.int64)
@@ -464,5 +518,5 @@ def solve_worker(args):
 
 
 __all__ = ["Oracle", "dp", "brute", "dp_exact", "brute_exact", "dp_types", "brute_types", "dp_types_exact",
-           "brute_types_exact", "latency_1f1b", "dp_latency", "brute_latency",
+           "brute_types_exact", "latency_1f1b", "dp_latency", "brute_latency", "dp_widths", "brute_widths",
            "INF", "lib", "solve_worker"]

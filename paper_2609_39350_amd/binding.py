@@ -107,12 +107,15 @@ def lib():
         L.hapmoe_stage_dp_types.argtypes = [P(Problem), vp, vp, i64, vp, i64, i64, i64, vp, vp, vp, vp, i64, vp]
         L.hapmoe_stage_dp_types_ws_bytes.argtypes = [P(Problem), P(i64)]
         L.hapmoe_stage_dp_types_1f1b.argtypes = L.hapmoe_stage_dp_types.argtypes
+        L.hapmoe_stage_dp_widths.argtypes = [P(Problem), vp, vp, i64, vp, i64, i64, i64, vp, vp, vp, vp, vp, i64, vp]
+        L.hapmoe_stage_dp_widths_ws_bytes.argtypes = [P(Problem), i64, P(i64)]
         L.hapmoe_section_clocks.argtypes = [P(C.c_uint64), C.c_int32]
         L.hapmoe_section_clocks.restype = C.c_int32
         for f in ("hapmoe_validate", "hapmoe_enumerate_candidates", "hapmoe_image_bytes", "hapmoe_pack_image",
                   "hapmoe_tables_bytes", "hapmoe_debug_bytes", "hapmoe_tables_layout", "hapmoe_debug_layout", "hapmoe_eval_cost_tables", "hapmoe_stage_dp", "hapmoe_stage_dp_1f1b", "hapmoe_stage_dp_ws_bytes",
                   "hapmoe_best_plan_ws_bytes", "hapmoe_best_plan", "hapmoe_best_plan_noalloc", "hapmoe_stage_dp_types",
-                  "hapmoe_stage_dp_types_ws_bytes", "hapmoe_stage_dp_types_1f1b"):
+                  "hapmoe_stage_dp_types_ws_bytes", "hapmoe_stage_dp_types_1f1b", "hapmoe_stage_dp_widths",
+                  "hapmoe_stage_dp_widths_ws_bytes"):
             getattr(L, f).restype = C.c_int32
         _LIB = L
     return _LIB
@@ -351,6 +354,21 @@ def stage_dp_types_1f1b(problem, d_image, d_cand, n_cand, d_tables, first, count
                                             _nbytes(d_ws), _stream(stream)), "hapmoe_stage_dp_types_1f1b")
 
 
+def stage_dp_widths_ws_bytes(problem, count) -> int:
+    n = C.c_int64(0)
+    _check(lib().hapmoe_stage_dp_widths_ws_bytes(_hp(problem).ref, int(count), C.byref(n)),
+           "hapmoe_stage_dp_widths_ws_bytes")
+    return n.value
+
+
+def stage_dp_widths(problem, d_image, d_cand, n_cand, d_tables, first, count, d_res, d_types, d_widths, d_ws,
+                    d_stats=None, stream=None):
+    _check(lib().hapmoe_stage_dp_widths(_hp(problem).ref, _dptr(d_image), _dptr(d_cand), int(n_cand),
+                                        _dptr(d_tables), _nbytes(d_tables), int(first), int(count), _dptr(d_res),
+                                        _dptr(d_types), _dptr(d_widths), _dptr(d_stats), _dptr(d_ws), _nbytes(d_ws),
+                                        _stream(stream)), "hapmoe_stage_dp_widths")
+
+
 def _plan_dict(plan):
     pp = plan.n_stages
     return {"instance": plan.instance, "objective": plan.objective, "stage_sum": plan.stage_sum,
@@ -405,11 +423,18 @@ class Planner:
         self.d_res = torch.empty(max(self.n, 1) * RESULT_DTYPE.itemsize, **u8)
         self.d_stats = None
         self.d_ws = torch.empty(best_plan_ws_bytes(self.hp, max(self.n, 1)), **u8)
-        # stage_types = 2: the device-count DP, which also returns each candidate's stage types
+        # stage_types = 2: the device-count DP, which also returns each candidate's stage types;
+        # 3: per-stage widths, which return the stage types and widths
         self.device_count_dp = int(problem["space"].get("stage_types", 0)) == 2
+        self.width_dp = int(problem["space"].get("stage_types", 0)) == 3
+        self.d_widths = None
         if self.device_count_dp:
             self.d_dp_ws = torch.empty(stage_dp_types_ws_bytes(self.hp), **u8)
             self.d_types = torch.zeros(max(self.n, 1) * MAX_STAGES, **u8)
+        elif self.width_dp:
+            self.d_dp_ws = torch.empty(stage_dp_widths_ws_bytes(self.hp, max(self.n, 1)), **u8)
+            self.d_types = torch.zeros(max(self.n, 1) * MAX_STAGES, **u8)
+            self.d_widths = torch.zeros(max(self.n, 1) * MAX_STAGES, **u8)
         else:
             self.d_dp_ws = torch.empty(stage_dp_ws_bytes(self.hp), **u8)
             self.d_types = None
@@ -433,6 +458,13 @@ class Planner:
             self.d_stats = d_stats
         res = self.d_res[first * RESULT_DTYPE.itemsize:]
         st = None if d_stats is None else d_stats[4 * first:]
+        if self.width_dp:
+            if objective != "threshold":
+                raise ValueError("per-stage widths: threshold objective only")
+            stage_dp_widths(self.hp, self.d_image, self.d_cand, self.n, self.d_tables, first, count, res,
+                            self.d_types[first * MAX_STAGES:], self.d_widths[first * MAX_STAGES:], self.d_dp_ws, st,
+                            stream)
+            return
         if self.device_count_dp:
             call = stage_dp_types if objective == "threshold" else stage_dp_types_1f1b
             call(self.hp, self.d_image, self.d_cand, self.n, self.d_tables, first, count, res,
@@ -442,8 +474,13 @@ class Planner:
         call(self.hp, self.d_image, self.d_cand, self.n, self.d_tables, first, count, res, self.d_dp_ws, st, stream)
 
     def best_plan(self, stream=None):
-        return best_plan(self.hp, self.d_cand, self.d_tables, self.d_res, self.n, self.d_ws, self.d_config_best,
+        plan = best_plan(self.hp, self.d_cand, self.d_tables, self.d_res, self.n, self.d_ws, self.d_config_best,
                          stream, self.d_types)
+        if self.width_dp:
+            self.torch.cuda.synchronize(self.device)
+            i = plan["instance"]
+            plan["widths"] = [int(x) for x in self.d_widths[i * MAX_STAGES:i * MAX_STAGES + len(plan["layers"])].cpu()]
+        return plan
 
     def run(self, stats=False, stream=None, objective="threshold"):
         self.eval_cost_tables(stream)
@@ -454,6 +491,11 @@ class Planner:
     def results(self) -> np.ndarray:
         self.torch.cuda.synchronize(self.device)
         return self.d_res.cpu().numpy()[: self.n * RESULT_DTYPE.itemsize].view(RESULT_DTYPE)
+
+    def widths(self) -> np.ndarray:
+        """Per-stage widths: the half-groups of every stage of every candidate, [n][32]."""
+        self.torch.cuda.synchronize(self.device)
+        return self.d_widths.cpu().numpy()[: self.n * MAX_STAGES].reshape(-1, MAX_STAGES)
 
     def stage_types(self) -> np.ndarray:
         """Device-count DP: the stage type masks of every candidate, [n][32]."""

@@ -69,7 +69,7 @@ int32_t check_fields(const hapmoe_problem *p)
     if (s.n_micro < 1 || s.n_micro > HAPMOE_MAX_MICRO) return HAPMOE_E_INVAL;
     for (int i = 0; i < s.n_micro; ++i)
         if (s.micro[i] < 1 || s.micro[i] > kMaxMicroValue) return HAPMOE_E_INVAL;
-    if (s.stage_types < 0 || s.stage_types > 2) return HAPMOE_E_INVAL;
+    if (s.stage_types < 0 || s.stage_types > 3) return HAPMOE_E_INVAL;
     return HAPMOE_OK;
 }
 
@@ -130,7 +130,8 @@ void build_space(const hapmoe_problem *p, Space &S)
     S.kmax = 1;
     S.ppmax = 1;
     S.umax = 1;
-    const bool free_types = sp.stage_types != 0;
+    const bool free_types = sp.stage_types == 1 || sp.stage_types == 2;
+    const bool widths = sp.stage_types == 3;
     S.n_orders = 1;
     for (int PP = 1; PP <= std::min(G, std::min(sp.pp_max, m.n_layers)); ++PP) {
         if (G % PP) continue;
@@ -156,6 +157,8 @@ void build_space(const hapmoe_problem *p, Space &S)
                             if (g % prod) continue;
                             DP = g / prod;
                         }
+                        // per-stage widths: half a group holds whole replicas and expert groups
+                        if (widths && (DP % 2 || (g / 2) % (EP * TPE))) continue;
                         S.cfg.push_back({PP, TP, CP, DP, EP, TPE});
                         any = true;
                     }
@@ -392,7 +395,7 @@ int32_t hapmoe_tables_bytes(const hapmoe_problem *p, int64_t *bytes)
     if (!bytes) return HAPMOE_E_INVAL;
     Space S;
     build_space(p, S);
-    *bytes = tables_layout((int64_t)S.cfg.size(), (int)S.n_orders, p->cluster.n_types, p->model.n_layers).total;
+    *bytes = tables_layout((int64_t)S.cfg.size(), (int)S.n_orders, p->cluster.n_types, p->model.n_layers, p->space.stage_types == 3).total;
     return HAPMOE_OK;
 }
 
@@ -402,8 +405,7 @@ int32_t hapmoe_tables_layout(const hapmoe_problem *p, int64_t out[9])
     if (!out) return HAPMOE_E_INVAL;
     Space S;
     build_space(p, S);
-    const TablesLayout L = tables_layout((int64_t)S.cfg.size(), (int)S.n_orders, p->cluster.n_types,
-                                         p->model.n_layers);
+    const TablesLayout L = tables_layout((int64_t)S.cfg.size(), (int)S.n_orders, p->cluster.n_types, p->model.n_layers, p->space.stage_types == 3);
     const int64_t v[9] = {L.n_configs, L.n_orders, L.n_masks, L.np, L.off_pi, L.off_key, L.off_mem, L.off_time,
                           L.total};
     for (int i = 0; i < 9; ++i) out[i] = v[i];
@@ -443,8 +445,7 @@ int32_t hapmoe_eval_cost_tables(const hapmoe_problem *p, const void *d_image, co
     const int64_t per = per_config(p, S);
     if (n_cand != (int64_t)S.cfg.size() * per) return HAPMOE_E_INVAL;
     if (first < 0 || count < 0 || first + count > n_cand) return HAPMOE_E_RANGE;
-    const TablesLayout L = tables_layout((int64_t)S.cfg.size(), (int)S.n_orders, p->cluster.n_types,
-                                         p->model.n_layers);
+    const TablesLayout L = tables_layout((int64_t)S.cfg.size(), (int)S.n_orders, p->cluster.n_types, p->model.n_layers, p->space.stage_types == 3);
     if (tables_bytes < L.total) return HAPMOE_E_WORKSPACE;
     const DebugLayout D = debug_layout(p->cluster.n_types, p->model.n_layers);
     if (d_debug && debug_bytes < (int64_t)S.cfg.size() * D.per_cfg * 8) return HAPMOE_E_WORKSPACE;
@@ -454,6 +455,10 @@ int32_t hapmoe_eval_cost_tables(const hapmoe_problem *p, const void *d_image, co
     const int64_t cfg_lo = first / per, cfg_hi = (first + count - 1) / per;
     if (launch_cost_tables(d_image, d_cand, per, p->model.n_layers, L, cfg_lo, cfg_hi - cfg_lo + 1, d_tables,
                            d_debug, D, (hipStream_t)stream) != hipSuccess)
+        return HAPMOE_E_HIP;
+    if (p->space.stage_types == 3 &&
+        launch_width_tables(d_image, d_cand, per, L, cfg_lo, cfg_hi - cfg_lo + 1, d_tables, (hipStream_t)stream) !=
+            hipSuccess)
         return HAPMOE_E_HIP;
     return HAPMOE_OK;
 }
@@ -475,14 +480,13 @@ int32_t stage_dp_any(const hapmoe_problem *p, const void *d_image, const hapmoe_
 {
     if (const int32_t e = check_problem(p)) return e;
     if (!d_image || !d_cand || !d_tables || !d_res || !d_ws) return HAPMOE_E_INVAL;
-    if (p->space.stage_types == 2) return HAPMOE_E_INVAL;   // hapmoe_stage_dp_types
+    if (p->space.stage_types >= 2) return HAPMOE_E_INVAL;   // hapmoe_stage_dp_types / _widths
     Space S;
     build_space(p, S);
     const int64_t per = per_config(p, S);
     if (n_cand != (int64_t)S.cfg.size() * per) return HAPMOE_E_INVAL;
     if (first < 0 || count < 0 || first + count > n_cand || count > INT32_MAX) return HAPMOE_E_RANGE;
-    const TablesLayout L = tables_layout((int64_t)S.cfg.size(), (int)S.n_orders, p->cluster.n_types,
-                                         p->model.n_layers);
+    const TablesLayout L = tables_layout((int64_t)S.cfg.size(), (int)S.n_orders, p->cluster.n_types, p->model.n_layers, p->space.stage_types == 3);
     if (tables_bytes < L.total || ws_bytes < stage_dp_ws_bytes()) return HAPMOE_E_WORKSPACE;
     if (const int e = check_arch()) return e;
     std::vector<int32_t> cfg_pp(S.cfg.size());
@@ -538,7 +542,7 @@ int32_t stage_dp_types_any(const hapmoe_problem *p, const void *d_image, const h
     const int64_t ncfg = (int64_t)S.cfg.size(), per = per_config(p, S);
     if (n_cand != ncfg * per) return HAPMOE_E_INVAL;
     if (first < 0 || count < 0 || first + count > n_cand || count > INT32_MAX) return HAPMOE_E_RANGE;
-    const TablesLayout L = tables_layout(ncfg, (int)S.n_orders, p->cluster.n_types, p->model.n_layers);
+    const TablesLayout L = tables_layout(ncfg, (int)S.n_orders, p->cluster.n_types, p->model.n_layers, p->space.stage_types == 3);
     if (tables_bytes < L.total ||
         ws_bytes < type_dp_ws_bytes(p->model.n_layers, p->cluster.n_types, S.umax, ncfg))
         return HAPMOE_E_WORKSPACE;
@@ -571,6 +575,39 @@ int32_t hapmoe_stage_dp_types_1f1b(const hapmoe_problem *p, const void *d_image,
                               d_stats, d_ws, ws_bytes, stream, true);
 }
 
+int32_t hapmoe_stage_dp_widths_ws_bytes(const hapmoe_problem *p, int64_t count, int64_t *bytes)
+{
+    if (const int32_t e = check_problem(p)) return e;
+    if (!bytes || count < 0 || p->space.stage_types != 3) return HAPMOE_E_INVAL;
+    Space S;
+    build_space(p, S);
+    *bytes = width_dp_ws_bytes(p->model.n_layers, S.ppmax, count);
+    return HAPMOE_OK;
+}
+
+int32_t hapmoe_stage_dp_widths(const hapmoe_problem *p, const void *d_image, const hapmoe_candidate *d_cand,
+                               int64_t n_cand, const void *d_tables, int64_t tables_bytes, int64_t first,
+                               int64_t count, hapmoe_dp_result *d_res, uint8_t *d_types, uint8_t *d_widths,
+                               int32_t *d_stats, void *d_ws, int64_t ws_bytes, void *stream)
+{
+    if (const int32_t e = check_problem(p)) return e;
+    if (p->space.stage_types != 3 || !d_image || !d_cand || !d_tables || !d_res || !d_types || !d_widths || !d_ws)
+        return HAPMOE_E_INVAL;
+    Space S;
+    build_space(p, S);
+    const int64_t ncfg = (int64_t)S.cfg.size(), per = per_config(p, S);
+    if (n_cand != ncfg * per) return HAPMOE_E_INVAL;
+    if (first < 0 || count < 0 || first + count > n_cand || count > INT32_MAX) return HAPMOE_E_RANGE;
+    const TablesLayout L = tables_layout(ncfg, (int)S.n_orders, p->cluster.n_types, p->model.n_layers, true);
+    if (tables_bytes < L.total || ws_bytes < width_dp_ws_bytes(p->model.n_layers, S.ppmax, count))
+        return HAPMOE_E_WORKSPACE;
+    if (const int e = check_arch()) return e;
+    if (launch_width_dp(d_image, d_cand, p->model.n_layers, S.ppmax, L, d_tables, first, count, d_res, d_types, d_widths,
+                        d_stats, d_ws, (hipStream_t)stream) != hipSuccess)
+        return HAPMOE_E_HIP;
+    return HAPMOE_OK;
+}
+
 int32_t hapmoe_best_plan_ws_bytes(const hapmoe_problem *p, int64_t n, int64_t *bytes)
 {
     if (const int32_t e = check_problem(p)) return e;
@@ -594,12 +631,12 @@ int32_t best_plan_any(const hapmoe_problem *p, const hapmoe_candidate *d_cand, c
 {
     if (const int32_t e = check_problem(p)) return e;
     if (!d_cand || !d_tables || !d_res || (!noalloc && !d_ws) || !h_plan) return HAPMOE_E_INVAL;
-    if (p->space.stage_types == 2 ? !d_types : d_types != nullptr) return HAPMOE_E_INVAL;
+    if (p->space.stage_types >= 2 ? !d_types : d_types != nullptr) return HAPMOE_E_INVAL;
     Space S;
     build_space(p, S);
     const int64_t per = per_config(p, S), ncfg = (int64_t)S.cfg.size();
     if (n < 1 || n > ncfg * per) return HAPMOE_E_RANGE;
-    const TablesLayout L = tables_layout(ncfg, (int)S.n_orders, p->cluster.n_types, p->model.n_layers);
+    const TablesLayout L = tables_layout(ncfg, (int)S.n_orders, p->cluster.n_types, p->model.n_layers, p->space.stage_types == 3);
     if (tables_bytes < L.total) return HAPMOE_E_WORKSPACE;
     const int64_t need = best_plan_ws_bytes(n, per, ncfg);
     if (noalloc ? need > HAPMOE_BEST_PLAN_SCRATCH_BYTES : ws_bytes < need) return HAPMOE_E_WORKSPACE;

@@ -187,7 +187,8 @@ __global__ __launch_bounds__(kThreads, 8) void k_cost_tables(const unsigned char
     __syncthreads();
 
     // ---- stage layout of the block orderings: (ordering, stage) pairs over the threads ----
-    if (H.stage_types == 0) {
+    // (stage_types 3, per-stage widths, keeps this uniform layout for its constants)
+    if (H.stage_types == 0 || H.stage_types == 3) {
         const int nord = H.n_orders, PP = c.pp, g = H.total_devices / PP, npair = nord * PP;
         for (int i = tid; i < npair; i += kThreads) {
             const int o = i / PP, s = i - o * PP;
@@ -259,7 +260,7 @@ __global__ __launch_bounds__(kThreads, 8) void k_cost_tables(const unsigned char
     }
 
     // ---- free stage types: the layout of every stage-type sequence (one thread each) ----
-    for (int o = tid; H.stage_types != 0 && o < H.n_orders; o += kThreads) {
+    for (int o = tid; (H.stage_types == 1 || H.stage_types == 2) && o < H.n_orders; o += kThreads) {
         const int g = H.total_devices / c.pp;
         KeyInfo *K = reinterpret_cast<KeyInfo *>(tab + L.off_key) + (cfg * L.n_orders + o);
         int seq[kMaxStages];   // free stage types: the type of each stage

@@ -68,9 +68,14 @@ struct KeyInfo {
 //   mem  [n_configs][4][np] int64   W, A0, A1 prefix sums and MoE-layer count
 //   time [n_configs][n_masks][3][np] int64   T0, T1, comm prefix sums
 //   layer [N] double   load-imbalance factor 1 + gamma (rho - 1) of every layer
+//   with per-stage widths (stage_types = 3), after the layer factors:
+//   wmem  [n_configs][3 widths][4][np] int64   W, A0, A1 prefix sums, MoE-layer count
+//   wtime [n_configs][n_masks][3 widths][3][np] int64   T0, T1, comm prefix sums
+//   wx    [n_configs][4] int64   MoE buffers of a stage of width 1, 2, 3 (and padding)
 struct TablesLayout {
     int64_t n_configs, n_orders, n_masks, np;
     int64_t off_pi, off_key, off_mem, off_time, off_layer, total;
+    int64_t off_wmem, off_wtime, off_wx;   // 0 without per-stage widths
 };
 
 // fp64 debug buffer: per configuration
@@ -86,7 +91,7 @@ static_assert(sizeof(hapmoe_candidate) == 32 && sizeof(hapmoe_dp_result) == 64, 
 
 inline int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
 
-inline TablesLayout tables_layout(int64_t n_configs, int n_orders, int n_types, int n_layers)
+inline TablesLayout tables_layout(int64_t n_configs, int n_orders, int n_types, int n_layers, bool widths = false)
 {
     TablesLayout L;
     L.n_configs = n_configs;
@@ -99,6 +104,13 @@ inline TablesLayout tables_layout(int64_t n_configs, int n_orders, int n_types, 
     L.off_time = align256(L.off_mem + n_configs * 4 * L.np * 8);
     L.off_layer = align256(L.off_time + n_configs * L.n_masks * 3 * L.np * 8);
     L.total = align256(L.off_layer + (int64_t)n_layers * 8);
+    L.off_wmem = L.off_wtime = L.off_wx = 0;
+    if (widths) {
+        L.off_wmem = L.total;
+        L.off_wtime = align256(L.off_wmem + n_configs * 3 * 4 * L.np * 8);
+        L.off_wx = align256(L.off_wtime + n_configs * L.n_masks * 3 * 3 * L.np * 8);
+        L.total = align256(L.off_wx + n_configs * 4 * 8);
+    }
     return L;
 }
 
@@ -147,6 +159,18 @@ hipError_t launch_type_dp(const void *d_image, const hapmoe_candidate *d_cand, i
                           int n_micro, int umax, int ppmax, const TablesLayout &L, const void *d_tables, int64_t first,
                           int64_t count, hapmoe_dp_result *d_res, uint8_t *d_types, int32_t *d_stats, void *d_ws,
                           bool exact, hipStream_t s);
+// Per-stage data-parallel widths (stage_types = 3): the width tables (run after
+// the cost tables on the same stream) and the DP over (stage, end layer,
+// half-groups used).
+constexpr int64_t kWidthDpMaxSlots = 512;   // workgroups with a state slice each
+hipError_t launch_width_tables(const void *d_image, const hapmoe_candidate *d_cand, int64_t per_config,
+                               const TablesLayout &L, int64_t cfg_lo, int64_t n_cfg, void *d_tables, hipStream_t s);
+int64_t width_dp_slot_bytes(int n_layers, int ppmax);
+int64_t width_dp_ws_bytes(int n_layers, int ppmax, int64_t n_cand);
+hipError_t launch_width_dp(const void *d_image, const hapmoe_candidate *d_cand, int n_layers, int ppmax,
+                           const TablesLayout &L, const void *d_tables, int64_t first, int64_t count,
+                           hapmoe_dp_result *d_res, uint8_t *d_types, uint8_t *d_widths, int32_t *d_stats, void *d_ws,
+                           hipStream_t s);
 // bytes of the winner record in the best-plan workspace (result, candidate, stage layout)
 constexpr int64_t kWinnerBytes = 256;
 static_assert(sizeof(hapmoe_dp_result) + sizeof(hapmoe_candidate) + sizeof(KeyInfo) <= kWinnerBytes, "winner");

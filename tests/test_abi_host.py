@@ -125,7 +125,7 @@ def test_free_stage_types_enumeration_and_limits():
         assert binding.tables_layout(q)["n_orders"] == o.n_orders()
     q = variant(workloads.config(2), **{"space.stage_types": 1})
     assert binding.tables_layout(q)["n_orders"] == 420   # 8! / (4! 2! 2!)
-    for bad in (3, -1):
+    for bad in (4, -1):
         with pytest.raises(binding.HapmoeError):
             binding.validate(variant(q, **{"space.stage_types": bad}))
     # 4 types x 64 devices at PP = 16: 16! / (4!)^4 sequences
@@ -166,7 +166,7 @@ def test_device_count_dp_space_and_limits():
         binding.validate(variant(workloads.config(4), **{"space.stage_types": 2}))
     binding.validate(variant(workloads.config(4), **{"space.stage_types": 2, "space.pp_max": 16}))
     with pytest.raises(binding.HapmoeError):
-        binding.validate(variant(workloads.config(3), **{"space.stage_types": 3}))
+        binding.validate(variant(workloads.config(3), **{"space.stage_types": 4}))
 
 
 def test_noalloc_best_plan_rejects_problems_beyond_its_workspace():

@@ -163,7 +163,7 @@ def test_empty_slots_are_infeasible():
 
 def test_stage_types_field_is_checked():
     with pytest.raises(ValueError):
-        orc.Oracle(variant(workloads.config(1), **{"space.stage_types": 3}))
+        orc.Oracle(variant(workloads.config(1), **{"space.stage_types": 4}))
 
 
 # ---------------------------------------------------------------------------
