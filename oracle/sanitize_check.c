@@ -110,23 +110,37 @@ static int run_problem(const orc_problem *p, const char *name)
     orc_enumerate(p, cfgs, ncfg);
     int64_t *cost = malloc(sizeof(int64_t) * (size_t)ORC_MAX_STAGES * (T + 1) * T * W * W);
     uint8_t *rf = malloc((size_t)ORC_MAX_STAGES * (T + 1) * T * W * W);
+    const int widths = p->stage_types == 3;
+    int64_t *wcost = malloc(sizeof(int64_t) * (size_t)p->pp_max * (2 * p->pp_max + 1) * 3 * W * W);
+    uint8_t *wrf = malloc((size_t)p->pp_max * (2 * p->pp_max + 1) * 3 * W * W);
     for (int64_t i = 0; i < n; i++) {
         orc_result a, b, c, d;
-        if (orc_solve(p, i, &a) || orc_solve_brute(p, i, &b) || orc_solve_exact(p, i, &c) ||
-            orc_solve_exact_brute(p, i, &d)) {
+        if (orc_solve(p, i, &a) || orc_solve_brute(p, i, &b) ||
+            (!widths && (orc_solve_exact(p, i, &c) || orc_solve_exact_brute(p, i, &d)))) {
             printf("%s: solve failed at %lld\n", name, (long long)i);
             return 1;
         }
-        if (a.status != b.status || a.opt != b.opt || c.status != d.status || c.opt != d.opt) {
+        if (a.status != b.status || a.opt != b.opt || (!widths && (c.status != d.status || c.opt != d.opt))) {
             printf("%s: dp and brute force differ at %lld\n", name, (long long)i);
             return 1;
+        }
+        if (p->stage_types == 0) {   /* the least 1F1B latency and its brute force */
+            if (orc_solve_latency(p, i, &c) || orc_solve_latency_brute(p, i, &d) || c.status != d.status ||
+                c.opt != d.opt) {
+                printf("%s: least latency differs at %lld\n", name, (long long)i);
+                return 1;
+            }
         }
         feasible += a.status == 0;
         if (p->stage_types == 2)
             orc_type_costs(p, i, cost, rf);
+        else if (widths)
+            orc_width_costs(p, i, wcost, wrf);
         else
             orc_segment_costs(p, i, cost, rf);
     }
+    free(wcost);
+    free(wrf);
     for (int64_t k = 0; k < ncfg; k++) {
         orc_pi_terms pt;
         orc_pi_terms_eval(p, &cfgs[k], &pt);
@@ -162,7 +176,7 @@ int main(void)
     orc_problem p;
     int bad = 0;
     for (int seed = 1; seed <= 3; seed++)
-        for (int mode = 0; mode <= 2; mode++) {
+        for (int mode = 0; mode <= 3; mode++) {
             char name[64];
             snprintf(name, sizeof(name), "two types, seed %d, stage_types %d", seed, mode);
             make_problem(&p, &A, (uint64_t)seed, 6, 2, c2, mode);

@@ -137,6 +137,11 @@ int run_problem(const hapmoe_problem &p, const char *name)
     if (int e = hapmoe_debug_layout(&p, dlay)) bad |= fail("debug layout", e);
     if (p.space.stage_types == 2) {
         if (int e = hapmoe_stage_dp_types_ws_bytes(&p, &ws)) bad |= fail("types ws", e);
+    } else if (p.space.stage_types == 3) {
+        if (int e = hapmoe_stage_dp_widths_ws_bytes(&p, n, &ws)) bad |= fail("widths ws", e);
+        if (hapmoe_stage_dp_widths(&p, nullptr, nullptr, n, nullptr, 0, 0, n, nullptr, nullptr, nullptr, nullptr,
+                                   nullptr, 0, nullptr) == HAPMOE_OK)
+            bad |= fail("widths null", 0);
     } else if (int e = hapmoe_stage_dp_ws_bytes(&p, &ws)) {
         bad |= fail("dp ws", e);
     }
@@ -168,7 +173,7 @@ int main()
     hapmoe_problem p;
     int bad = 0;
     for (int seed = 1; seed <= 4; ++seed)
-        for (int st = 0; st <= 2; ++st) {
+        for (int st = 0; st <= 3; ++st) {
             char name[80];
             std::snprintf(name, sizeof(name), "2 types seed %d stage_types %d", seed, st);
             make_problem(p, A, (uint64_t)seed, 12, 2, c2, st);
@@ -198,7 +203,7 @@ int main()
     p = base; p.space.pp_max = 33; expect_inval(p);
     p = base; p.space.n_micro = 0; expect_inval(p);
     p = base; p.space.micro[0] = 5000; expect_inval(p);
-    p = base; p.space.stage_types = 3; expect_inval(p);
+    p = base; p.space.stage_types = 4; expect_inval(p);
     p = base; p.model.is_moe = nullptr; expect_inval(p);
     if (hapmoe_validate(nullptr) != HAPMOE_E_INVAL) bad |= fail("null problem", 0);
     if (refused != cases) bad |= fail("malformed problems accepted", cases - refused);

@@ -131,7 +131,7 @@ def test_never_worse_than_uniform_without_windows(n):
     nb = len(base["space"]["micro"])
     per_u, per_w = ou.n_orders() * nb, ow.n_orders() * nb
     lower = 0
-    for k in range(0, len(cw), max(1, len(cw) // 30)):
+    for k in range(0, len(cw), max(1, len(cw) // 12)):
         for j in range(per_w):
             d, u = ow.solve(k * per_w + j), ou.solve(cu.index(cw[k]) * per_u + j)
             assert (d["status"] == 0) >= (u["status"] == 0)

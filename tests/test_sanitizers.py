@@ -35,7 +35,7 @@ def test_oracle_under_sanitizers():
                         os.path.join(ROOT, "oracle", "sanitize_check.c"),
                         os.path.join(ROOT, "oracle", "hapmoe_oracle.c"), "-lm"], check=True)
         out = _run(exe)
-    assert out.count("dp = brute force") == 19
+    assert out.count("dp = brute force") == 25
 
 
 @pytest.mark.skipif(not os.path.exists("/opt/rocm/bin/hipcc"), reason="hipcc missing")
@@ -53,4 +53,4 @@ def test_library_host_code_under_sanitizers():
                *[os.path.join(csrc, s) for s in build.SOURCES]]
         subprocess.run(cmd, check=True, capture_output=True)
         out = _run(exe)
-    assert out.count("candidates,") == 36 and "12 malformed problems refused" in out
+    assert out.count("candidates,") == 48 and "12 malformed problems refused" in out
