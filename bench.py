@@ -273,6 +273,47 @@ def host_cpu():
     return {"nproc": usable, "cpu_count": os.cpu_count(), "cpu_model": model}
 
 
+def leg_widths(torch, binding, workloads, dev, stream, steps, warmup, cpu_sample):
+    """Per-stage data-parallel widths (non-uniform PP/DP, hapmoe_stage_dp_widths)
+    on the 32- and 61-layer workloads: the same candidates' best objective with
+    uniform widths beside it."""
+    import copy
+    import numpy as np
+    out = {}
+    for n_config in (2, 3):
+        base = workloads.config(n_config)
+        wp = copy.deepcopy(base)
+        wp["space"]["stage_types"] = 3
+        pw = binding.Planner(wp, dev)
+        pw.eval_cost_tables()
+        pw.stage_dp(stats=True)
+        st = pw.stats()
+        plan, elapsed, dp_ms = _timed_steps(torch, pw, stream, steps, warmup)
+        res = pw.results()
+        # the uniform plan of the same candidates (block layout, same configurations)
+        pu = binding.Planner(base, dev)
+        pu.run()
+        ures = pu.results()
+        keep = {tuple(c) for c in np.stack([pw.cand_host[f] for f in ("pp", "tp", "cp", "dp", "ep", "tpe")], 1)}
+        ukey = [tuple(c) in keep for c in np.stack([pu.cand_host[f] for f in ("pp", "tp", "cp", "dp", "ep", "tpe")], 1)]
+        uobj = np.where(ures["status"] == 0, ures["objective"], np.iinfo(np.int64).max)[np.array(ukey)]
+        relax = int(st[:, 1].astype(np.int64).sum())
+        rec = {"workload": f"config {n_config}: {WORKLOADS[n_config]}, per-stage data-parallel widths",
+               "value": pw.n * steps / elapsed, "unit": "candidates/s", "ms_per_step": elapsed * 1e3 / steps,
+               "stage_dp_ms": dp_ms, "candidates": pw.n, "feasible_candidates": int((res["status"] == 0).sum()),
+               "dp_passes_per_candidate": {"mean": float(st[:, 0].mean()), "max": int(st[:, 0].max())},
+               "relaxations_per_launch": relax,
+               "roofline": alu_roofline(relax, 0, dp_ms, "width_dp"),
+               "best_objective_ns": plan["objective"], "uniform_widths_best_ns": int(uobj.min()),
+               "gain_over_uniform_widths": 1.0 - plan["objective"] / int(uobj.min()),
+               "best_plan": {"config": plan["config"], "order": plan["order"], "B": plan["n_micro"],
+                             "widths": plan["widths"], "layers": plan["layers"]}}
+        if n_config == 2 and cpu_sample:
+            rec["cpu_baseline"], _ = cpu_baseline(wp, pw.n, cpu_sample)
+        out[f"config{n_config}"] = rec
+    return out
+
+
 def cpu_baseline(problem, n_total, n_sample, exact=False):
     """The oracle as it stands, single thread, on a fixed stride sample (exact:
     its 1F1B re-scoring of the frontier)."""
@@ -308,6 +349,8 @@ def main():
     ap.add_argument("--section-clocks", action="store_true",
                     help="diagnostic build: report where the stage-DP kernel's cycles go (slightly slower kernel)")
     ap.add_argument("--cpu-sample-free", type=int, default=40)
+    ap.add_argument("--no-widths", action="store_true", help="skip the per-stage data-parallel width legs")
+    ap.add_argument("--cpu-sample-widths", type=int, default=200)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (counter scaling for HBM traffic)")
     args = ap.parse_args()
@@ -411,6 +454,9 @@ def main():
     if not args.no_free_types:
         out["free_stage_types"] = leg_free_types(torch, binding, workloads, dev, stream, args.steps, args.warmup,
                                                  0 if args.no_cpu_baseline else args.cpu_sample_free)
+    if not args.no_widths:
+        out["per_stage_widths"] = leg_widths(torch, binding, workloads, dev, stream, args.steps, args.warmup,
+                                             0 if args.no_cpu_baseline else args.cpu_sample_widths)
     if calib is not None:
         out["copy_calibration_bytes"] = calib
     if not args.no_cpu_baseline:
