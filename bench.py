@@ -208,11 +208,13 @@ def _timed_steps(torch, pl, stream, steps, warmup):
 def leg_free_types(torch, binding, workloads, dev, stream, steps, warmup, cpu_sample):
     """Free per-stage device types: every stage-type sequence as its own candidate
     (config 2), and the DP over device counts (configs 2 and 3, pipelines up to
-    16 stages); each with the best objective of the block orderings beside it."""
+    16 stages, and config 4, up to 32 stages and 9^4 count states); each with the
+    best objective of the block orderings beside it."""
     import copy
     import numpy as np
     out = {}
-    for name, n_config, mode in (("sequences", 2, 1), ("device_count_dp", 2, 2), ("device_count_dp", 3, 2)):
+    for name, n_config, mode in (("sequences", 2, 1), ("device_count_dp", 2, 2), ("device_count_dp", 3, 2),
+                                 ("device_count_dp", 4, 2)):
         base = workloads.config(n_config)
         free = copy.deepcopy(base)
         free["space"]["stage_types"] = mode

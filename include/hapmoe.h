@@ -135,7 +135,7 @@ typedef struct hapmoe_space {
                             2: free per-stage type chosen by the DP over device counts (the
                             state m of Section 3.4): the same configurations as 1, one order
                             slot each (order 0 lays out the first sequence), solved by
-                            hapmoe_stage_dp_types; at most 4096 count states prod_h (k_h + 1)
+                            hapmoe_stage_dp_types; at most 8192 count states prod_h (k_h + 1)
                             per pipeline, k_h = m_h / (G/PP).
                             3: per-stage data-parallel widths (the non-uniform PP/DP of
                             Section 1): the block orderings of 0, but stage i takes the next

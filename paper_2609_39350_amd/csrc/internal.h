@@ -143,10 +143,10 @@ enum {
 int32_t stage_dp_section_clocks(uint64_t *out, bool clear);
 
 // Device-count DP (free per-stage device types by the DP state of device counts).
-constexpr int kMaxTypeStates = 4096;                        // states u = prod_h (k_h + 1) per pipeline
+constexpr int kMaxTypeStates = 8192;                        // states u = prod_h (k_h + 1) per pipeline
 constexpr int64_t kTypeDpMaxSlots = 512;                    // workgroups with a state slice each
 constexpr int64_t kTypeDpMaxSlotBytes = int64_t(8) << 30;   // all slices together
-constexpr int kTypeDpMaxLds = 64 * 1024;
+constexpr int kTypeDpMaxLds = 160 * 1024;                   // the LDS of one gfx950 CU
 struct TypeLds {
     int umax;
     int off_t0, off_t1, off_mw, off_moe, off_inc, off_path, off_ctl, off_ulist, off_bounds, bytes;

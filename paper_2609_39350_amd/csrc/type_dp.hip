@@ -647,9 +647,18 @@ hipError_t launch_type_dp(const void *d_image, const hapmoe_candidate *d_cand, i
     const auto *img = static_cast<const unsigned char *>(d_image);
     const auto *tab = static_cast<const unsigned char *>(d_tables);
     const dim3 grid3((unsigned)grid), block(kThreads);
+    // more than 64 KB of LDS a workgroup (the count states of 32-stage pipelines
+    // on four types) has to be allowed per kernel
 #define HAPMOE_TYPE_DP(ST, EX)                                                                                 \
-    hipLaunchKernelGGL((k_type_dp<ST, EX>), grid3, block, S.bytes, s, img, d_cand, L, tab, first, count, key_lo, \
-                       n_keys, S, slot_base, slot_bytes, d_res, d_types, d_stats, queue)
+    do {                                                                                                       \
+        if (S.bytes > 65536) {                                                                                 \
+            const hipError_t e_ = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_type_dp<ST, EX>),     \
+                                                      hipFuncAttributeMaxDynamicSharedMemorySize, S.bytes);    \
+            if (e_ != hipSuccess) return e_;                                                                   \
+        }                                                                                                      \
+        hipLaunchKernelGGL((k_type_dp<ST, EX>), grid3, block, S.bytes, s, img, d_cand, L, tab, first, count,     \
+                           key_lo, n_keys, S, slot_base, slot_bytes, d_res, d_types, d_stats, queue);          \
+    } while (0)
     if (d_stats && exact)
         HAPMOE_TYPE_DP(true, true);
     else if (d_stats)

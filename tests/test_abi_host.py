@@ -159,12 +159,11 @@ def test_device_count_dp_space_and_limits():
         # the fixed-type stage DP refuses the mode (before any device work)
         assert binding.lib().hapmoe_stage_dp(hp.ref, None, None, 0, None, 0, 0, 0, None, None, None, 0,
                                              None) == -1
-    # 4 types x 64 devices at PP = 16: 5^4 count states, fine; a 4 x 256-device
-    # cluster at PP = 32 has 9^4 = 6561, past the 4096 limit (PP <= 16 is fine)
+    # 4 types x 64 devices at PP = 16: 5^4 count states; a 4 x 256-device cluster
+    # at PP = 32 has 9^4 = 6561, inside the 8192 limit (the most four types allow
+    # at 32 stages)
     binding.validate(variant(workloads.config(3), **{"space.stage_types": 2}))
-    with pytest.raises(binding.HapmoeError):
-        binding.validate(variant(workloads.config(4), **{"space.stage_types": 2}))
-    binding.validate(variant(workloads.config(4), **{"space.stage_types": 2, "space.pp_max": 16}))
+    binding.validate(variant(workloads.config(4), **{"space.stage_types": 2}))
     with pytest.raises(binding.HapmoeError):
         binding.validate(variant(workloads.config(3), **{"space.stage_types": 4}))
 

@@ -140,11 +140,12 @@ def test_count_dp_config3_sampled(torch):
     compare_types(p, pl, idx, slow=True)
 
 
-@pytest.mark.parametrize("n", [3, 5])
+@pytest.mark.parametrize("n", [3, 5, 4])
 def test_count_dp_full_space_properties(torch, n):
-    # PP up to 16 (5^4 count states): every result is a valid plan whose stage
-    # costs, evaluated by the oracle, give its sum, largest stage and objective,
-    # and no block ordering of the same (pi, B) does better
+    # PP up to 16 (5^4 count states; on the 96-layer workload up to 32 stages and
+    # 9^4 = 6,561 states): every result is a valid plan whose stage costs,
+    # evaluated by the oracle, give its sum, largest stage and objective, and no
+    # block ordering of the same (pi, B) does better
     base = workloads.config(n)
     p = count_dp(base)
     print(f"device-count DP, config {n}: properties", flush=True)
@@ -173,14 +174,18 @@ def test_count_dp_full_space_properties(torch, n):
             feasible += 1
             assert int(res[i]["objective"]) <= best_block, (cfg, j)
     assert feasible > 0
-    # a stride sample re-evaluated from the oracle's cost tensor
-    for i in range(0, pl.n, max(1, pl.n // 24)):
+    # a stride sample re-evaluated from the oracle's cost tensor (and every
+    # pipeline depth's last candidate)
+    pps = pl.cand_host["pp"]
+    sample = set(range(0, pl.n, max(1, pl.n // 24))) | {int(np.nonzero(pps == d)[0][-1]) for d in np.unique(pps)}
+    for i in sorted(sample):
         if res[i]["status"] != 0:
             continue
         cost, rf = o.type_costs(i)
         pp, B = cfgs[i // nB][0], p["space"]["micro"][i % nB]
         types = [int(m).bit_length() - 1 for m in ty[i][:pp]]
-        assert sorted(types) == sorted(h for h in range(4) for _ in range(64 // (256 // pp)))
+        g = int(sum(base["cluster"]["count"])) // pp
+        assert sorted(types) == sorted(h for h in range(4) for _ in range(int(base["cluster"]["count"][h]) // g))
         a, cs, rs = 0, [], []
         for s in range(pp):
             b = a + int(res[i]["layers"][s])
