@@ -41,6 +41,9 @@ WORKLOADS = {
 }
 
 
+# training batch (sequences) for the fixed-batch arg-min of each workload: B * DP * mbs
+GLOBAL_BATCH = {1: 16, 2: 256, 3: 1024, 4: 2048, 5: 1024}
+
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "stage_dp_moe96_traffic.json")
 STAGE_DP_SOURCE = os.path.join(ROOT, "paper_2609_39350_amd", "csrc", "stage_dp.hip")
 
@@ -445,6 +448,18 @@ def main():
                       "layers": plan["layers"], "recompute": plan["recompute"]},
     }
     out["side_rooflines"] = side_rooflines(binding, pl, ms)
+    # the same results with the training batch fixed (B * DP * mbs = global batch):
+    # the arg-min over candidates that do the same work
+    gbs = GLOBAL_BATCH.get(args.config)
+    if gbs:
+        import copy
+        fixed = copy.deepcopy(problem)
+        fixed["space"]["global_batch"] = gbs
+        fp = binding.best_plan(binding.HostProblem(fixed), pl.d_cand, pl.d_tables, pl.d_res, pl.n, pl.d_ws)
+        out["best_plan_fixed_global_batch"] = {
+            "global_batch_sequences": gbs, "instance": fp["instance"], "objective_ns": fp["objective"],
+            "config": fp["config"], "order": fp["order"], "B": fp["n_micro"], "layers": fp["layers"],
+            "recompute": fp["recompute"]}
     if clocks is not None:
         clocks["steps"] = args.steps
         out["stage_dp_section_clocks"] = clocks

@@ -148,6 +148,12 @@ typedef struct hapmoe_space {
                             HAPMOE_E_INVAL */
     int32_t n_micro;     /* entries of micro[] */
     int32_t micro[HAPMOE_MAX_MICRO]; /* microbatch counts B, 1..1024 */
+    int32_t global_batch; /* 0: every B of micro[] competes in hapmoe_best_plan's arg-min (each
+                             candidate's objective is the latency of its own B micro-batches);
+                             > 0: the training batch is fixed (Section 3.1 input) at this many
+                             sequences, and the arg-min (per configuration and global) only
+                             takes candidates whose B * DP * micro_batch_size equals it.  The
+                             stage DP itself is unaffected. */
 } hapmoe_space;
 
 typedef struct hapmoe_problem {

@@ -57,7 +57,7 @@ class Params(C.Structure):
 class Space(C.Structure):
     _fields_ = [("pp_max", C.c_int32), ("tp_mask", C.c_int32), ("cp_mask", C.c_int32), ("ep_max", C.c_int32),
                 ("tpe_mask", C.c_int32), ("mode", C.c_int32), ("stage_types", C.c_int32), ("n_micro", C.c_int32),
-                ("micro", C.c_int32 * MAX_MICRO)]
+                ("micro", C.c_int32 * MAX_MICRO), ("global_batch", C.c_int32)]
 
 
 class Problem(C.Structure):
@@ -175,6 +175,7 @@ class HostProblem:
         for f in ("pp_max", "tp_mask", "cp_mask", "ep_max", "tpe_mask", "mode"):
             setattr(p.space, f, int(sp[f]))
         p.space.stage_types = int(sp.get("stage_types", 0))
+        p.space.global_batch = int(sp.get("global_batch", 0))
         micro = list(sp["micro"])
         p.space.n_micro = len(micro)
         for i, b in enumerate(micro[:MAX_MICRO]):

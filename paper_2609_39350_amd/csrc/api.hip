@@ -70,6 +70,7 @@ int32_t check_fields(const hapmoe_problem *p)
     for (int i = 0; i < s.n_micro; ++i)
         if (s.micro[i] < 1 || s.micro[i] > kMaxMicroValue) return HAPMOE_E_INVAL;
     if (s.stage_types < 0 || s.stage_types > 3) return HAPMOE_E_INVAL;
+    if (s.global_batch < 0) return HAPMOE_E_INVAL;
     return HAPMOE_OK;
 }
 
@@ -648,7 +649,8 @@ int32_t best_plan_any(const hapmoe_problem *p, const hapmoe_candidate *d_cand, c
     }
     hipStream_t s = (hipStream_t)stream;
     const auto *tab = static_cast<const unsigned char *>(d_tables);
-    if (launch_best_plan(d_res, d_cand, tab + L.off_key, d_types, p->space.n_micro, n, per, ncfg, d_config_best,
+    if (launch_best_plan(d_res, d_cand, tab + L.off_key, d_types, p->space.n_micro, n, per, ncfg,
+                         p->space.global_batch, p->model.micro_batch_size, d_config_best,
                          d_ws, s) != hipSuccess)
         return HAPMOE_E_HIP;
     // one copy: the global (objective, index) pair and the winner's records

@@ -63,8 +63,11 @@ __device__ inline Best block_min(Best v, Best *sh)
 }
 
 // level 1: chunk ch of configuration cfg -> partial[cfg * chunks + ch]
-__global__ __launch_bounds__(kThreads) void k_seg_partial(const hapmoe_dp_result *__restrict__ res, int64_t n,
-                                                          int64_t per, int64_t chunks, Best *__restrict__ partial)
+// (with a fixed global batch gbs > 0 only the candidates whose B * DP * mbs equals it)
+__global__ __launch_bounds__(kThreads) void k_seg_partial(const hapmoe_dp_result *__restrict__ res,
+                                                          const hapmoe_candidate *__restrict__ cand, int64_t n,
+                                                          int64_t per, int64_t chunks, int64_t gbs, int64_t mbs,
+                                                          Best *__restrict__ partial)
 {
     __shared__ Best sh[kThreads / 64];
     const int64_t cfg = blockIdx.x, ch = blockIdx.y;
@@ -74,7 +77,9 @@ __global__ __launch_bounds__(kThreads) void k_seg_partial(const hapmoe_dp_result
     Best v = {kInf, INT64_MAX};
     for (int64_t i = lo + threadIdx.x; i < hi; i += kThreads) {
         const hapmoe_dp_result &r = res[i];
-        const Best o = {r.status == HAPMOE_STATUS_OK ? r.objective : kInf, i};
+        bool take = r.status == HAPMOE_STATUS_OK;
+        if (gbs > 0) take = take && (int64_t)cand[i].n_micro * cand[i].dp * mbs == gbs;
+        const Best o = {take ? r.objective : kInf, i};
         if (better(o, v)) v = o;
     }
     v = block_min(v, sh);
@@ -169,16 +174,16 @@ int64_t best_plan_ws_bytes(int64_t n, int64_t per_config, int64_t n_configs)
 
 hipError_t launch_best_plan(const hapmoe_dp_result *d_res, const hapmoe_candidate *d_cand,
                             const unsigned char *d_key_info, const uint8_t *d_types, int64_t n_micro, int64_t n,
-                            int64_t per_config, int64_t n_configs, int64_t *d_config_best, void *d_ws,
-                            hipStream_t s)
+                            int64_t per_config, int64_t n_configs, int64_t global_batch, int64_t mbs,
+                            int64_t *d_config_best, void *d_ws, hipStream_t s)
 {
     const int64_t chunks = chunks_per_config(per_config);
     Best *glob = static_cast<Best *>(d_ws);
     auto *winner = reinterpret_cast<uint32_t *>(static_cast<unsigned char *>(d_ws) + sizeof(Best));
     Best *cfg_best = reinterpret_cast<Best *>(static_cast<unsigned char *>(d_ws) + sizeof(Best) + kWinnerBytes);
     Best *partial = cfg_best + n_configs;
-    hipLaunchKernelGGL(k_seg_partial, dim3((unsigned)n_configs, (unsigned)chunks), dim3(kThreads), 0, s, d_res, n,
-                       per_config, chunks, partial);
+    hipLaunchKernelGGL(k_seg_partial, dim3((unsigned)n_configs, (unsigned)chunks), dim3(kThreads), 0, s, d_res,
+                       d_cand, n, per_config, chunks, global_batch, mbs, partial);
     hipLaunchKernelGGL(k_seg_final, dim3((unsigned)((n_configs + kThreads - 1) / kThreads)), dim3(kThreads), 0, s,
                        partial, n_configs, chunks, cfg_best, d_config_best);
     hipLaunchKernelGGL(k_global, dim3(1), dim3(1024), 0, s, cfg_best, n_configs, glob);

@@ -178,8 +178,8 @@ static_assert(sizeof(hapmoe_dp_result) % 4 == 0 && sizeof(hapmoe_candidate) % 4 
               "word copies");
 hipError_t launch_best_plan(const hapmoe_dp_result *d_res, const hapmoe_candidate *d_cand,
                             const unsigned char *d_key_info, const uint8_t *d_types, int64_t n_micro, int64_t n,
-                            int64_t per_config, int64_t n_configs, int64_t *d_config_best, void *d_ws,
-                            hipStream_t s);
+                            int64_t per_config, int64_t n_configs, int64_t global_batch, int64_t mbs,
+                            int64_t *d_config_best, void *d_ws, hipStream_t s);
 int64_t best_plan_ws_bytes(int64_t n, int64_t per_config, int64_t n_configs);
 // device address and size of the fixed workspace of hapmoe_best_plan_noalloc on the current device
 hipError_t best_plan_scratch(void **ptr, int64_t *bytes);

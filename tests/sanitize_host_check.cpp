@@ -204,6 +204,7 @@ int main()
     p = base; p.space.n_micro = 0; expect_inval(p);
     p = base; p.space.micro[0] = 5000; expect_inval(p);
     p = base; p.space.stage_types = 4; expect_inval(p);
+    p = base; p.space.global_batch = -1; expect_inval(p);
     p = base; p.model.is_moe = nullptr; expect_inval(p);
     if (hapmoe_validate(nullptr) != HAPMOE_E_INVAL) bad |= fail("null problem", 0);
     if (refused != cases) bad |= fail("malformed problems accepted", cases - refused);

@@ -437,6 +437,37 @@ def test_1f1b_random_and_tied_every_candidate(torch):
     assert total > 100
 
 
+@pytest.mark.parametrize("n,gbs", [(1, 16), (4, 2048)])
+def test_fixed_global_batch_arg_min(torch, n, gbs):
+    """With the training batch fixed at gbs sequences, the arg-min takes only the
+    candidates with B * DP * mbs = gbs (per configuration and global); the stage
+    DP results do not change."""
+    p = workloads.config(n)
+    pl = binding.Planner(p, "cuda:0")
+    pl.run()
+    free = pl.results().copy()
+    q = variant(p, **{"space.global_batch": gbs})
+    ql = binding.Planner(q, "cuda:0")
+    plan = ql.run()
+    res = ql.results()
+    assert np.array_equal(res, free)
+    c = ql.cand_host
+    keep = (res["status"] == 0) & (c["n_micro"].astype(np.int64) * c["dp"] * p["model"]["micro_batch_size"] == gbs)
+    assert keep.any()
+    obj = np.where(keep, res["objective"], np.iinfo(np.int64).max)
+    assert plan["instance"] == int(np.argmin(obj)) and plan["objective"] == int(obj.min())
+    assert plan["n_micro"] * plan["config"][3] * p["model"]["micro_batch_size"] == gbs
+    per = ql.n // ql.n_configs
+    seg = obj.reshape(ql.n_configs, per)
+    exp = np.where(seg.min(axis=1) == np.iinfo(np.int64).max, -1, np.arange(ql.n_configs) * per + seg.argmin(axis=1))
+    assert (ql.config_best() == exp).all()
+    if n == 1:   # the oracle's own minimum over the same subset
+        o = orc.Oracle(p)
+        ref = [o.solve(i) for i in range(o.n_instances())]
+        best = min((r["opt"], i) for i, r in enumerate(ref) if r["status"] == 0 and keep[i])
+        assert (plan["objective"], plan["instance"]) == best
+
+
 def test_1f1b_feasibility_equals_threshold_objective(torch):
     """Both objectives search the same feasible partitions: the same candidates
     are feasible (the bench launch, 3.86 M candidates)."""

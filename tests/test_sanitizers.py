@@ -53,4 +53,4 @@ def test_library_host_code_under_sanitizers():
                *[os.path.join(csrc, s) for s in build.SOURCES]]
         subprocess.run(cmd, check=True, capture_output=True)
         out = _run(exe)
-    assert out.count("candidates,") == 48 and "12 malformed problems refused" in out
+    assert out.count("candidates,") == 48 and "13 malformed problems refused" in out
