@@ -260,6 +260,41 @@ def leg_free_types(torch, binding, workloads, dev, stream, steps, warmup, cpu_sa
     return out
 
 
+def per_depth(torch, binding, pl, stream, reps=5, clocks=False):
+    """Diagnostic: the stage-DP kernel on each pipeline depth's candidates alone
+    (a sub-range launch each), with its executed relaxations and split-point
+    evaluations and its fraction of the VALU roofline (clocks: the diagnostic
+    build's section clocks of each depth's launches)."""
+    import numpy as np
+    pp = pl.cand_host["pp"]
+    rows = []
+    for d in np.unique(pp):
+        at = np.nonzero(pp == d)[0]
+        first, count = int(at[0]), int(len(at))
+        pl.stage_dp(first=first, count=count, stats=True)
+        st = pl.stats()[first:first + count]
+        relax, evals = int(st[:, 1].astype(np.int64).sum()), int(st[:, 2].astype(np.int64).sum())
+        slots = int(st[:, 3].astype(np.int64).sum())
+        torch.cuda.synchronize()
+        if clocks:
+            binding.section_clocks(clear=True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            pl.stage_dp(first=first, count=count)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        roof = alu_roofline(relax, evals, ms, "stage_dp")
+        row = {"pp": int(d), "candidates": count, "ms": ms, "relaxations": relax, "evaluations": evals,
+               "lane_utilisation": relax / max(slots, 1),
+               "passes_per_candidate": float(st[:, 0].mean()), "frac": roof["frac"]}
+        if clocks:
+            row["section_clocks"] = binding.section_clocks(clear=True)
+        rows.append(row)
+    return rows
+
+
 def host_cpu():
     """Host cores and CPU model, for the CPU-baseline record."""
     model = None
@@ -355,6 +390,8 @@ def main():
                     help="diagnostic build: report where the stage-DP kernel's cycles go (slightly slower kernel)")
     ap.add_argument("--cpu-sample-free", type=int, default=40)
     ap.add_argument("--no-widths", action="store_true", help="skip the per-stage data-parallel width legs")
+    ap.add_argument("--per-depth", action="store_true",
+                    help="diagnostic: stage-DP time, work and roofline fraction of each pipeline depth alone")
     ap.add_argument("--cpu-sample-widths", type=int, default=200)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (counter scaling for HBM traffic)")
@@ -448,6 +485,8 @@ def main():
                       "layers": plan["layers"], "recompute": plan["recompute"]},
     }
     out["side_rooflines"] = side_rooflines(binding, pl, ms)
+    if args.per_depth:
+        out["stage_dp_per_depth"] = per_depth(torch, binding, pl, stream, clocks=args.section_clocks)
     # the same results with the training batch fixed (B * DP * mbs = global batch):
     # the arg-min over candidates that do the same work
     gbs = GLOBAL_BATCH.get(args.config)
