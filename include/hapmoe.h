@@ -319,6 +319,35 @@ int32_t hapmoe_stage_dp_1f1b(const hapmoe_problem *p, const void *d_image,
                              hapmoe_dp_result *d_res, int32_t *d_stats,
                              void *d_ws, int64_t ws_bytes, void *stream);
 
+/* The least 1F1B iteration latency over every partition (Appendix B, Eq. 5,
+ * with the steady-state term of Eq. 4), exact rather than a re-scoring of the
+ * threshold DP's frontier:
+ *   T = sum_i c_i + sum_{i <= s} ceil(c_i / 3) + max(0, B - s - 1) * max_i c_i,
+ * s the first (1-based) stage of largest cost, minimised over every partition
+ * that passes the three prunings (stage costs, recomputation and memory as in
+ * hapmoe_stage_dp).  For every distinct stage cost t, ascending, a DP over
+ * (stage, end layer, bottleneck placed yet) gives the least T with largest
+ * stage exactly t; the sweep stops once F_inf + ceil(t / 3) +
+ * max(0, B - PP - 1) t, F_inf the least stage sum, reaches the best T.  Ties:
+ * least T, then the lower largest stage, then the lexicographically smallest
+ * (b_PP-1, ..., b_1) of the stage end layers.  For each candidate of
+ * [first, first + count) writes d_res[i - first]: objective = T + C, stage_sum
+ * and t_max of the chosen partition, its recomputation mask and stage lengths.
+ * One workgroup per candidate, 64 KB of LDS.  Its stage-cost table holds, for
+ * every stage, end layer b of the stage's band (the end layers its windows
+ * allow) and split point of its window, an 8-byte cost and a 1-byte
+ * recomputation flag (the flags rounded up to 16 bytes), plus 16 bytes of DP
+ * state for every (stage, b); a candidate whose table exceeds 63,744 bytes gets
+ * HAPMOE_STATUS_OVERFLOW.  d_stats (may be NULL): thresholds swept and DP
+ * relaxations of each candidate (columns 2, 3 zero).  No workspace.  Not for
+ * stage_types = 2 or 3 (HAPMOE_E_INVAL); ranges and errors as hapmoe_stage_dp.
+ * Asynchronous. */
+int32_t hapmoe_stage_dp_latency(const hapmoe_problem *p, const void *d_image,
+                                const hapmoe_candidate *d_cand, int64_t n_cand,
+                                const void *d_tables, int64_t tables_bytes,
+                                int64_t first, int64_t count,
+                                hapmoe_dp_result *d_res, int32_t *d_stats, void *stream);
+
 /* Workspace of hapmoe_stage_dp_types: the work-queue counter and one slice of
  * DP states per workgroup (F as int64 and the back-trace pointer as int16 per
  * state (u, b, h')); HAPMOE_E_INVAL unless stage_types = 2. */

@@ -98,6 +98,7 @@ def lib():
         L.hapmoe_eval_cost_tables.argtypes = [P(Problem), vp, vp, i64, i64, i64, vp, i64, vp, i64, vp]
         L.hapmoe_stage_dp.argtypes = [P(Problem), vp, vp, i64, vp, i64, i64, i64, vp, vp, vp, i64, vp]
         L.hapmoe_stage_dp_1f1b.argtypes = [P(Problem), vp, vp, i64, vp, i64, i64, i64, vp, vp, vp, i64, vp]
+        L.hapmoe_stage_dp_latency.argtypes = [P(Problem), vp, vp, i64, vp, i64, i64, i64, vp, vp, vp]
         L.hapmoe_stage_dp_ws_bytes.argtypes = [P(Problem), P(i64)]
         L.hapmoe_tables_layout.argtypes = [P(Problem), P(i64)]
         L.hapmoe_debug_layout.argtypes = [P(Problem), P(i64)]
@@ -115,7 +116,7 @@ def lib():
                   "hapmoe_tables_bytes", "hapmoe_debug_bytes", "hapmoe_tables_layout", "hapmoe_debug_layout", "hapmoe_eval_cost_tables", "hapmoe_stage_dp", "hapmoe_stage_dp_1f1b", "hapmoe_stage_dp_ws_bytes",
                   "hapmoe_best_plan_ws_bytes", "hapmoe_best_plan", "hapmoe_best_plan_noalloc", "hapmoe_stage_dp_types",
                   "hapmoe_stage_dp_types_ws_bytes", "hapmoe_stage_dp_types_1f1b", "hapmoe_stage_dp_widths",
-                  "hapmoe_stage_dp_widths_ws_bytes"):
+                  "hapmoe_stage_dp_widths_ws_bytes", "hapmoe_stage_dp_latency"):
             getattr(L, f).restype = C.c_int32
         _LIB = L
     return _LIB
@@ -333,6 +334,13 @@ def stage_dp_1f1b(problem, d_image, d_cand, n_cand, d_tables, first, count, d_re
            "hapmoe_stage_dp_1f1b")
 
 
+def stage_dp_latency(problem, d_image, d_cand, n_cand, d_tables, first, count, d_res, d_stats=None, stream=None):
+    """The least 1F1B latency over every partition (no workspace)."""
+    _check(lib().hapmoe_stage_dp_latency(_hp(problem).ref, _dptr(d_image), _dptr(d_cand), int(n_cand),
+                                         _dptr(d_tables), _nbytes(d_tables), int(first), int(count), _dptr(d_res),
+                                         _dptr(d_stats), _stream(stream)), "hapmoe_stage_dp_latency")
+
+
 def stage_dp_types_ws_bytes(problem) -> int:
     n = C.c_int64(0)
     _check(lib().hapmoe_stage_dp_types_ws_bytes(_hp(problem).ref, C.byref(n)), "hapmoe_stage_dp_types_ws_bytes")
@@ -449,8 +457,10 @@ class Planner:
 
     def stage_dp(self, first=0, count=None, stats=False, stream=None, objective="threshold"):
         """objective "threshold": sum + (B-1) max (hapmoe_stage_dp); "1f1b": the
-        appendix's 1F1B latency over the Pareto frontier (hapmoe_stage_dp_1f1b)."""
-        if objective not in ("threshold", "1f1b"):
+        appendix's 1F1B latency over the Pareto frontier (hapmoe_stage_dp_1f1b);
+        "latency": the least 1F1B latency over every partition
+        (hapmoe_stage_dp_latency)."""
+        if objective not in ("threshold", "1f1b", "latency"):
             raise ValueError(objective)
         count = self.n - first if count is None else count
         d_stats = None
@@ -459,6 +469,11 @@ class Planner:
             self.d_stats = d_stats
         res = self.d_res[first * RESULT_DTYPE.itemsize:]
         st = None if d_stats is None else d_stats[4 * first:]
+        if objective == "latency":
+            if self.width_dp or self.device_count_dp:
+                raise ValueError("least latency: stage_types 0 or 1 only")
+            stage_dp_latency(self.hp, self.d_image, self.d_cand, self.n, self.d_tables, first, count, res, st, stream)
+            return
         if self.width_dp:
             if objective != "threshold":
                 raise ValueError("per-stage widths: threshold objective only")

@@ -5,7 +5,7 @@ import subprocess
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 LIB = os.path.join(PKG, "libhapmoe.so")
-SOURCES = ["api.hip", "cost_tables.hip", "stage_dp.hip", "type_dp.hip", "width_dp.hip", "best_plan.hip"]
+SOURCES = ["api.hip", "cost_tables.hip", "stage_dp.hip", "type_dp.hip", "width_dp.hip", "latency_dp.hip", "best_plan.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

@@ -518,6 +518,28 @@ int32_t hapmoe_stage_dp_1f1b(const hapmoe_problem *p, const void *d_image, const
                         ws_bytes, stream, true);
 }
 
+int32_t hapmoe_stage_dp_latency(const hapmoe_problem *p, const void *d_image, const hapmoe_candidate *d_cand,
+                                int64_t n_cand, const void *d_tables, int64_t tables_bytes, int64_t first,
+                                int64_t count, hapmoe_dp_result *d_res, int32_t *d_stats, void *stream)
+{
+    if (const int32_t e = check_problem(p)) return e;
+    if (!d_image || !d_cand || !d_tables || !d_res) return HAPMOE_E_INVAL;
+    if (p->space.stage_types >= 2) return HAPMOE_E_INVAL;
+    Space S;
+    build_space(p, S);
+    const int64_t per = per_config(p, S);
+    if (n_cand != (int64_t)S.cfg.size() * per) return HAPMOE_E_INVAL;
+    if (first < 0 || count < 0 || first + count > n_cand) return HAPMOE_E_RANGE;
+    const TablesLayout L = tables_layout((int64_t)S.cfg.size(), (int)S.n_orders, p->cluster.n_types,
+                                         p->model.n_layers);
+    if (tables_bytes < L.total) return HAPMOE_E_WORKSPACE;
+    if (const int e = check_arch()) return e;
+    if (launch_latency_dp(d_image, d_cand, L, d_tables, first, count, d_res, d_stats, (hipStream_t)stream) !=
+        hipSuccess)
+        return HAPMOE_E_HIP;
+    return HAPMOE_OK;
+}
+
 int32_t hapmoe_stage_dp_types_ws_bytes(const hapmoe_problem *p, int64_t *bytes)
 {
     if (const int32_t e = check_problem(p)) return e;

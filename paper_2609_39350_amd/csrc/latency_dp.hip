@@ -1,0 +1,386 @@
+// Least 1F1B iteration latency over every partition (Appendix B, Eq. 5, with
+// the steady-state term of Eq. 4): for each candidate the partition, with the
+// Section 3.4 prunings and per-stage recomputation, that minimises
+//     T = sum_i c_i + sum_{i <= s} ceil(c_i / 3) + max(0, B - s - 1) * t,
+// t = max_i c_i and s the first (1-based) stage whose cost is t (a stage's
+// forward part is ceil(c / 3), its backward part the rest).
+//
+// For a threshold t the least T among partitions whose largest stage is
+// exactly t is a DP over (stage, end layer, z), z = 1 once the bottleneck
+// stage is placed: before it a stage needs c < t and weighs c + ceil(c / 3);
+// the bottleneck stage s has c = t and weighs t + ceil(t / 3) +
+// max(0, B - s - 1) t; after it a stage needs c <= t and weighs c.  The
+// thresholds are the distinct finite stage costs, taken in ascending order;
+// the sweep stops at the first t where F_inf + ceil(t / 3) +
+// max(0, B - PP - 1) t (a lower bound of T for this and every larger t,
+// F_inf the least stage sum) reaches the best T found.  Ties: the least T,
+// then the lower largest stage (the first threshold reaching it), then the
+// lexicographically smallest (b_{PP-1}, ..., b_1): the back-trace keeps the
+// set of (end layer, z) states on optimal paths and at every stage takes the
+// smallest split point through which one continues optimally.
+//
+// Mapping: one wave64 workgroup per candidate (grid-stride).  The candidate's
+// stage costs -- every (stage, end layer b in the stage's band, split point a
+// in the window) with the memory test of its stored micro-batch count,
+// recomputation and prunings 1 and 3, exactly as the threshold DP prices them
+// -- are evaluated once into LDS; a pass spreads the (end layer, z) states of
+// a stage over the lanes, each lane taking the minimum over its window.  The
+// next threshold is a wave-wide minimum over the cost table.  Integer min-plus
+// work: no MFMA.
+#include "internal.h"
+
+namespace hapmoe {
+namespace {
+
+constexpr int64_t kLBig = int64_t(1) << 62;   // "no path" inside the DP, far from overflow
+constexpr int kLatLds = 64 * 1024;            // LDS of one workgroup (two fit a CU)
+constexpr int kLatBlocks = 2048;              // grid-stride launch width
+
+struct LatStage {
+    int blo, wd;     // band of end layers [blo, blo + wd)
+    int lo, win;     // window: n = b - a in [lo, lo + win)
+    int plo, phi;    // band of the previous stage's end layers (split points)
+    int coff, voff;  // offsets into the cost table and the DP states
+};
+
+struct LatHead {
+    LatStage st[kMaxStages];
+    int64_t red[64];         // wave reductions through LDS
+    int32_t len[kMaxStages]; // best partition: layers per stage
+    int32_t flag[kMaxStages];
+};
+
+// the stage-cost table may use 64 KB less the header: 63,744 bytes (documented)
+static_assert(sizeof(LatHead) == 1792, "LDS header size is part of the documented table limit");
+
+__device__ inline int64_t ceil3(int64_t c) { return (c + 2) / 3; }
+
+// Wave-wide minimum of an int64 through LDS (every lane gets it).
+__device__ inline int64_t lat_min(int64_t v, int64_t *red, int lane)
+{
+    red[lane] = v;
+    __syncthreads();
+    for (int o = 32; o >= 1; o >>= 1) {
+        if (lane < o) red[lane] = red[lane + o] < red[lane] ? red[lane + o] : red[lane];
+        __syncthreads();
+    }
+    const int64_t m = red[0];
+    __syncthreads();
+    return m;
+}
+
+__device__ inline int64_t lat_sum(int64_t v, int64_t *red, int lane)
+{
+    red[lane] = v;
+    __syncthreads();
+    for (int o = 32; o >= 1; o >>= 1) {
+        if (lane < o) red[lane] += red[lane + o];
+        __syncthreads();
+    }
+    const int64_t m = red[0];
+    __syncthreads();
+    return m;
+}
+
+__device__ inline void lat_write(hapmoe_dp_result *out, int status, int64_t obj, int64_t sum, int64_t tmax,
+                                 uint32_t rmask, const int32_t *len, int pp)
+{
+    out->objective = obj;
+    out->stage_sum = sum;
+    out->t_max = tmax;
+    out->status = status;
+    out->recompute_mask = rmask;
+    for (int s = 0; s < kMaxStages; ++s) out->layers[s] = (uint8_t)(len && s < pp ? len[s] : 0);
+}
+
+template <bool STATS>
+__global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, const hapmoe_candidate *cand,
+                                                   const unsigned char *tab, TablesLayout L, int64_t first,
+                                                   int64_t count, hapmoe_dp_result *res, int32_t *stats)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    const ImageHeader &H = *reinterpret_cast<const ImageHeader *>(img);
+    LatHead &D = *reinterpret_cast<LatHead *>(smem);
+    unsigned char *dyn = smem + ((sizeof(LatHead) + 15) & ~size_t(15));
+    const int dyn_bytes = kLatLds - (int)((sizeof(LatHead) + 15) & ~size_t(15));
+    const int lane = threadIdx.x;
+    const int N = H.n_layers, nB = H.n_micro;
+    const int64_t np = L.np;
+
+    for (int64_t i = blockIdx.x; i < count; i += gridDim.x) {
+        const int64_t inst = first + i;
+        const int64_t key = inst / nB, cfg = key / H.n_orders;
+        const int PP = cand[inst].pp;
+        const int64_t B = cand[inst].n_micro;
+        hapmoe_dp_result *out = res + i;
+        int32_t *st_out = STATS ? stats + 4 * i : nullptr;
+        const PiInfo *pi = reinterpret_cast<const PiInfo *>(tab + L.off_pi) + cfg;
+        const KeyInfo *ki = reinterpret_cast<const KeyInfo *>(tab + L.off_key) + key;
+        const int64_t *mem = reinterpret_cast<const int64_t *>(tab + L.off_mem) + cfg * 4 * np;
+        const int64_t *time = reinterpret_cast<const int64_t *>(tab + L.off_time) + cfg * L.n_masks * 3 * np;
+        auto finish = [&](int status) {   // a result without a partition
+            if (lane == 0) {
+                lat_write(out, status, kInf, kInf, kInf, 0, nullptr, PP);
+                if (STATS) st_out[0] = st_out[1] = st_out[2] = st_out[3] = 0;
+            }
+            __syncthreads();
+        };
+        if (pi->status != HAPMOE_STATUS_OK) {
+            finish(HAPMOE_STATUS_OVERFLOW);
+            continue;
+        }
+
+        // ---- stage layout: bands of end layers under the pruning-1 windows ----
+        int totlo = 0, tothi = 0, cumlo = 0, cumhi = 0;
+        for (int s = 0; s < PP; ++s) {
+            totlo += ki->lo[s];
+            tothi += ki->hi[s];
+            if (s <= lane) {
+                cumlo += ki->lo[s];
+                cumhi += ki->hi[s];
+            }
+        }
+        int wd = 0;
+        if (lane < PP) {
+            int blo = N - (tothi - cumhi), bhi = N - (totlo - cumlo);
+            blo = blo > cumlo ? blo : cumlo;
+            bhi = bhi < cumhi ? bhi : cumhi;
+            wd = bhi >= blo ? bhi - blo + 1 : 0;
+            D.st[lane].blo = blo;
+            D.st[lane].wd = wd;
+            D.st[lane].lo = ki->lo[lane];
+            D.st[lane].win = ki->hi[lane] - ki->lo[lane] + 1;
+        }
+        const bool shape = totlo <= N && tothi >= N && !__any(lane < PP && wd == 0);
+        __syncthreads();
+        if (!shape) {
+            finish(HAPMOE_STATUS_INFEASIBLE);
+            continue;
+        }
+        if (lane == 0) {
+            int coff = 0, voff = 0;
+            for (int s = 0; s < PP; ++s) {
+                LatStage &S = D.st[s];
+                S.plo = s ? D.st[s - 1].blo : 0;
+                S.phi = s ? D.st[s - 1].blo + D.st[s - 1].wd - 1 : 0;
+                S.coff = coff;
+                S.voff = voff;
+                coff += S.wd * S.win;
+                voff += S.wd;
+            }
+            D.red[0] = coff;
+            D.red[1] = voff;
+        }
+        __syncthreads();
+        const int ncost = (int)D.red[0], nv = (int)D.red[1];
+        __syncthreads();
+        // LDS: cost table [ncost] int64 | DP states [nv][2] int64 | recomputation flags [ncost] u8
+        const int need = ncost * 8 + nv * 16 + ((ncost + 15) & ~15);
+        if (need > dyn_bytes) {
+            finish(HAPMOE_STATUS_OVERFLOW);
+            continue;
+        }
+        int64_t *Cst = reinterpret_cast<int64_t *>(dyn);
+        int64_t *V = Cst + ncost;
+        uint8_t *R = reinterpret_cast<uint8_t *>(V + 2 * nv);
+
+        // ---- every stage cost of the candidate, once ----
+        const int64_t X = pi->x_bytes, eta_tbar = (int64_t)H.eta_prune * pi->tbar;
+        const bool prune_het = H.prune_hetero != 0, recomp = H.allow_recompute != 0;
+        for (int e = lane; e < ncost; e += 64) {
+            int s = 0;
+            while (s + 1 < PP && D.st[s + 1].coff <= e) ++s;
+            const LatStage S = D.st[s];
+            const int k = (e - S.coff) / S.win, j = (e - S.coff) - k * S.win;
+            const int b = S.blo + k, a = b - S.lo - j;
+            int64_t c = kLBig;
+            uint8_t r = 0;
+            if (a >= S.plo && a <= S.phi && a >= 0) {
+                const int mask = ki->mask[s];
+                int64_t cap = kInf;
+                for (int h = 0; h < H.n_types; ++h)
+                    if ((mask >> h) & 1) cap = H.mem_bytes[h] < cap ? H.mem_bytes[h] : cap;
+                const bool inner = s < PP - 1;
+                const int bp = ki->bpair[s];
+                const int64_t p2p = inner ? pi->p2p[(bp >> 2) * kMaxTypes + (bp & 3)] : 0;
+                const bool bdiff = inner && ((bp >> 2) != (bp & 3));
+                const bool mixed = __popc(mask) > 1;
+                const int64_t *tm = time + (int64_t)(mask - 1) * 3 * np;
+                const int64_t ms = (PP - s) < B ? (PP - s) : B;   // stored micro-batches
+                const int64_t base = mem[b] - mem[a] + ((mem[3 * np + b] - mem[3 * np + a]) > 0 ? X : 0);
+                const int64_t hc = (mixed ? tm[2 * np + b] - tm[2 * np + a] : 0) + (bdiff ? p2p : 0);
+                if (!prune_het || hc <= eta_tbar) {
+                    if (base + ms * (mem[np + b] - mem[np + a]) <= cap) {
+                        c = tm[b] - tm[a] + p2p;
+                    } else if (recomp && base + ms * (mem[2 * np + b] - mem[2 * np + a]) <= cap) {
+                        c = tm[np + b] - tm[np + a] + p2p;
+                        r = 1;
+                    }
+                }
+            }
+            Cst[e] = c;
+            R[e] = r;
+        }
+        __syncthreads();
+
+        // One pass over the stages.  lat = false: the least stage sum (state z = 0
+        // only); lat = true: the least latency weight with the largest stage
+        // exactly t, states z = 0 / 1.  Returns the relaxations this lane made.
+        auto pass = [&](bool lat, int64_t t) -> int64_t {
+            int64_t nrel = 0;
+            for (int s = 0; s < PP; ++s) {
+                const LatStage S = D.st[s];
+                const LatStage P = D.st[s ? s - 1 : 0];
+                const int64_t steady = B - s - 2 > 0 ? B - s - 2 : 0;   // stage s + 1 (1-based) as bottleneck
+                for (int e = lane; e < 2 * S.wd; e += 64) {
+                    const int k = e >> 1, z = e & 1;
+                    const int b = S.blo + k;
+                    int64_t best = kLBig;
+                    if (lat || z == 0) {
+                        for (int j = 0; j < S.win; ++j) {
+                            const int64_t c = Cst[S.coff + k * S.win + j];
+                            if (c >= kLBig) continue;
+                            const int a = b - S.lo - j;
+                            const int64_t v0 = s ? V[2 * (P.voff + a - P.blo)] : (a == 0 ? 0 : kLBig);
+                            if (!lat) {
+                                if (v0 < kLBig && v0 + c < best) best = v0 + c;
+                                continue;
+                            }
+                            if (STATS) ++nrel;
+                            if (z == 0) {
+                                if (v0 < kLBig && c < t && v0 + c + ceil3(c) < best) best = v0 + c + ceil3(c);
+                            } else {
+                                const int64_t v1 = s ? V[2 * (P.voff + a - P.blo) + 1] : kLBig;
+                                if (v0 < kLBig && c == t && v0 + c + ceil3(c) + steady * c < best)
+                                    best = v0 + c + ceil3(c) + steady * c;
+                                if (v1 < kLBig && c <= t && v1 + c < best) best = v1 + c;
+                            }
+                        }
+                    }
+                    V[2 * (S.voff + k) + z] = best;
+                }
+                __syncthreads();
+            }
+            return nrel;
+        };
+
+        pass(false, 0);
+        const LatStage SL = D.st[PP - 1];
+        const int64_t finf = V[2 * (SL.voff + (N - SL.blo))];
+        __syncthreads();
+        if (finf >= kLBig) {
+            finish(HAPMOE_STATUS_INFEASIBLE);
+            continue;
+        }
+        const int64_t steady_min = B - PP - 1 > 0 ? B - PP - 1 : 0;
+        int64_t best = kLBig, tbest = 0, bsum = 0, tprev = -1, relax = 0;
+        uint32_t brm = 0;
+        int swept = 0;
+        for (;;) {
+            // the next distinct stage cost above tprev (stage costs are positive)
+            int64_t tn = kLBig;
+            for (int e = lane; e < ncost; e += 64) {
+                const int64_t c = Cst[e];
+                if (c > tprev && c < tn) tn = c;
+            }
+            const int64_t t = lat_min(tn, D.red, lane);
+            if (t >= kLBig) break;
+            if (finf + ceil3(t) + steady_min * t >= best) break;
+            relax += pass(true, t);
+            ++swept;
+            tprev = t;
+            const int64_t v = V[2 * (SL.voff + (N - SL.blo)) + 1];
+            __syncthreads();
+            if (v >= best) continue;
+            best = v;
+            tbest = t;
+            // back-trace: the smallest split point through which a live state
+            // continues optimally, stage by stage from the last
+            int b = N;
+            bool live0 = false, live1 = true;
+            int64_t sum = 0;
+            uint32_t rmask = 0;
+            for (int s = PP - 1; s >= 0; --s) {
+                const LatStage S = D.st[s];
+                const LatStage P = D.st[s ? s - 1 : 0];
+                const int64_t steady = B - s - 2 > 0 ? B - s - 2 : 0;
+                const int k = b - S.blo;
+                const int64_t tg0 = V[2 * (S.voff + k)], tg1 = V[2 * (S.voff + k) + 1];
+                int64_t amin = kLBig;
+                bool m0 = false, m1 = false;
+                int aj = -1;
+                for (int j = lane; j < S.win; j += 64) {
+                    const int64_t c = Cst[S.coff + k * S.win + j];
+                    if (c >= kLBig) continue;
+                    const int a = b - S.lo - j;
+                    const int64_t v0 = s ? V[2 * (P.voff + a - P.blo)] : (a == 0 ? 0 : kLBig);
+                    const int64_t v1 = s ? V[2 * (P.voff + a - P.blo) + 1] : kLBig;
+                    const bool f0 = v0 < kLBig && ((live0 && c < t && v0 + c + ceil3(c) == tg0) ||
+                                                   (live1 && c == t && v0 + c + ceil3(c) + steady * c == tg1));
+                    const bool f1 = v1 < kLBig && live1 && c <= t && v1 + c == tg1;
+                    if ((f0 || f1) && a < amin) {   // one lane may hold two split points (j, j + 64)
+                        amin = a;
+                        m0 = f0;
+                        m1 = f1;
+                        aj = j;
+                    }
+                }
+                const int64_t na = lat_min(amin, D.red, lane);
+                const bool mine = amin == na && na < kLBig;
+                const uint64_t b0 = __ballot(mine && m0), b1 = __ballot(mine && m1);
+                const uint64_t who = __ballot(mine);
+                const int src = who ? __ffsll((unsigned long long)who) - 1 : 0;
+                const int jj = __shfl(aj, src, 64);
+                if (na >= kLBig || jj < 0) {   // cannot happen on an optimal path
+                    live0 = live1 = false;
+                    break;
+                }
+                const int e = S.coff + k * S.win + jj;
+                sum += Cst[e];
+                if (R[e]) rmask |= 1u << s;
+                if (lane == 0) D.len[s] = b - (int)na;
+                b = (int)na;
+                live0 = b0 != 0;
+                live1 = b1 != 0;
+            }
+            bsum = sum;
+            brm = rmask;
+            __syncthreads();
+        }
+        if (best >= kLBig) {
+            finish(HAPMOE_STATUS_INFEASIBLE);
+            continue;
+        }
+        const int64_t nrel = STATS ? lat_sum(relax, D.red, lane) : 0;
+        if (lane == 0) {
+            lat_write(out, HAPMOE_STATUS_OK, best + ki->dp_const, bsum, tbest, brm, D.len, PP);
+            if (STATS) {
+                st_out[0] = swept;
+                st_out[1] = (int32_t)(nrel < INT32_MAX ? nrel : INT32_MAX);
+                st_out[2] = st_out[3] = 0;
+            }
+        }
+        __syncthreads();
+    }
+}
+
+}  // namespace
+
+hipError_t launch_latency_dp(const void *d_image, const hapmoe_candidate *d_cand, const TablesLayout &L,
+                             const void *d_tables, int64_t first, int64_t count, hapmoe_dp_result *d_res,
+                             int32_t *d_stats, hipStream_t stream)
+{
+    if (count == 0) return hipSuccess;
+    const int grid = (int)(count < kLatBlocks ? count : kLatBlocks);
+    const auto *img = static_cast<const unsigned char *>(d_image);
+    const auto *tab = static_cast<const unsigned char *>(d_tables);
+    if (d_stats)
+        hipLaunchKernelGGL(k_latency_dp<true>, dim3(grid), dim3(64), kLatLds, stream, img, d_cand, tab, L, first,
+                           count, d_res, d_stats);
+    else
+        hipLaunchKernelGGL(k_latency_dp<false>, dim3(grid), dim3(64), kLatLds, stream, img, d_cand, tab, L, first,
+                           count, d_res, d_stats);
+    return hipGetLastError();
+}
+
+}  // namespace hapmoe

@@ -111,6 +111,28 @@ def test_device_calls_refuse_bad_sizes_before_touching_the_gpu():
     assert f(hp.ref, 1, 1, 90, 1, 10**9, 0, 1, 1, None, None, 256, None) == -1
 
 
+def test_least_latency_entry_checks_before_the_gpu():
+    """hapmoe_stage_dp_latency validates its arguments before any HIP call:
+    range, table size and the modes it does not cover."""
+    import ctypes as C
+    p = workloads.config(1)
+    hp = binding.HostProblem(p)
+    n = len(binding.enumerate_candidates(p))
+    fake = C.c_void_p(1 << 20)   # never dereferenced: every call below returns before device work
+    tb = binding.tables_bytes(p)
+    f = binding.lib().hapmoe_stage_dp_latency
+    assert f(hp.ref, fake, fake, n, fake, tb, n - 5, 6, fake, None, None) == -7
+    assert f(hp.ref, fake, fake, n, fake, tb, -1, 1, fake, None, None) == -7
+    assert f(hp.ref, fake, fake, n, fake, tb - 1, 0, 1, fake, None, None) == -3
+    assert f(hp.ref, fake, fake, n + 1, fake, tb, 0, 1, fake, None, None) == -1
+    assert f(hp.ref, fake, fake, n, fake, tb, 0, 1, None, None, None) == -1
+    for mode in (2, 3):
+        q = variant(p, **{"space.stage_types": mode})
+        hq = binding.HostProblem(q)
+        assert f(hq.ref, fake, fake, 0, fake, 1 << 40, 0, 0, fake, None, None) == -1
+    assert f(hp.ref, fake, fake, n, fake, tb, 0, 1, fake, None, None) in (-4, -5)   # no usable device here
+
+
 def test_free_stage_types_enumeration_and_limits():
     # free per-stage types: the same candidate set as the oracle, and sequence
     # counts past the library's limit refused up front
