@@ -147,6 +147,59 @@ def leg_1f1b(torch, pl, stream, steps, warmup):
                           "layers": plan["layers"]}}
 
 
+def leg_latency(torch, binding, workloads, dev, stream, cpu_sample):
+    """The least 1F1B latency over every partition (hapmoe_stage_dp_latency) on
+    configurations 2 and 3, whole launches, with the frontier re-scoring's best
+    plan beside it (the exact minimum can only be lower)."""
+    import numpy as np
+    out = {}
+    for n_config in (2, 3):
+        p = workloads.config(n_config)
+        pl = binding.Planner(p, dev)
+        pl.eval_cost_tables()
+        pl.stage_dp(stats=True, objective="latency")   # statistics, and warm
+        st = pl.stats()
+        res = pl.results()
+        ok = res["status"] == 0
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        e0.record(stream)
+        pl.stage_dp(objective="latency")
+        e1.record(stream)
+        plan = pl.best_plan()
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+        ms = e0.elapsed_time(e1)
+        relax = int(st[:, 1].astype(np.int64).sum())
+        plan_f = pl.run(objective="1f1b")
+        rec = {"workload": f"config {n_config}: {WORKLOADS[n_config]}", "candidates": pl.n,
+               "value": pl.n / elapsed, "unit": "candidates/s", "stage_dp_ms": ms,
+               "feasible_candidates": int(ok.sum()),
+               "thresholds_per_candidate": {"mean": float(st[ok, 0].mean()) if ok.any() else 0.0,
+                                            "max": int(st[:, 0].max())},
+               "relaxations_per_launch": relax,
+               "roofline": alu_roofline(relax, 0, ms, "latency_dp"),
+               "best_objective_ns": plan["objective"], "frontier_rescoring_best_ns": plan_f["objective"],
+               "best_plan": {"config": plan["config"], "order": plan["order"], "B": plan["n_micro"],
+                             "layers": plan["layers"], "recompute": plan["recompute"]}}
+        if cpu_sample and n_config == 2:
+            from oracle.oracle import Oracle
+            o = Oracle(p)
+            stride = max(1, pl.n // cpu_sample)
+            idx = list(range(stride // 2, pl.n, stride))[:cpu_sample]
+            t0 = time.perf_counter()
+            o.solve_latency_many(idx)
+            dt = time.perf_counter() - t0
+            rec["cpu_baseline"] = {"value": len(idx) / dt, "unit": "candidates/s", "cores": 1, "kind": "oracle",
+                                   "host": host_cpu(),
+                                   "sample": f"{len(idx)} candidates at stride {stride} of {pl.n}, {dt:.1f} s "
+                                             f"on one host core"}
+        out[f"config{n_config}"] = rec
+        progress(f"least latency config {n_config}")
+    return out
+
+
 FP64_PEAK_FLOPS = 78.6e12            # MI355X vector fp64
 HBM_PEAK_BYTES = 8.0e12
 COST_FLOPS_PER_ENTRY = 40            # fp64 operations per (configuration, type set, layer) entry
@@ -407,6 +460,8 @@ def main():
     ap.add_argument("--per-depth", action="store_true",
                     help="diagnostic: stage-DP time, work and roofline fraction of each pipeline depth alone")
     ap.add_argument("--cpu-sample-widths", type=int, default=200)
+    ap.add_argument("--no-latency", action="store_true", help="skip the least-latency legs")
+    ap.add_argument("--cpu-sample-latency", type=int, default=2000)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (counter scaling for HBM traffic)")
     args = ap.parse_args()
@@ -530,6 +585,9 @@ def main():
         out["free_stage_types"] = leg_free_types(torch, binding, workloads, dev, stream, args.steps, args.warmup,
                                                  0 if args.no_cpu_baseline else args.cpu_sample_free)
         progress("free stage-type legs")
+    if not args.no_latency:
+        out["least_latency"] = leg_latency(torch, binding, workloads, dev, stream,
+                                           0 if args.no_cpu_baseline else args.cpu_sample_latency)
     if not args.no_widths:
         out["per_stage_widths"] = leg_widths(torch, binding, workloads, dev, stream, args.steps, args.warmup,
                                              0 if args.no_cpu_baseline else args.cpu_sample_widths)

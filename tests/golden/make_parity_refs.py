@@ -8,6 +8,11 @@ Contents (each an index array and a uint32 digest array, tests/parity_digest.py)
   cfg4_threshold   one candidate per (configuration, ordering) key, B rotating 1..64
   cfg4_1f1b        one candidate per configuration, ordering and B rotating
   cfg3_types16     device-count DP, 16 candidates of 16-stage pipelines
+  cfg3_latency, cfg5_latency   the least 1F1B latency, every 97th candidate
+  cfg4_latency     the least 1F1B latency, one candidate of every 6th
+                   configuration (ordering and B rotating)
+With "latency" as a further argument only the least-latency entries are
+(re)computed and merged into the existing file.
 """
 import copy
 import os
@@ -38,7 +43,7 @@ def _problem(name):
 def _work(args):
     name, mode, idx = args
     o = orc.Oracle(_problem(name))
-    res = {"threshold": o.solve_many, "1f1b": o.solve_exact_many}[mode](idx)
+    res = {"threshold": o.solve_many, "1f1b": o.solve_exact_many, "latency": o.solve_latency_many}[mode](idx)
     return parity_digest.of_oracle(res, with_types=name == "cfg3_types")
 
 
@@ -68,11 +73,37 @@ def types16_samples():
     return np.array(idx[:: max(1, len(idx) // 16)][:16])
 
 
-def main():
-    workers = int(sys.argv[1]) if len(sys.argv) > 1 else (os.cpu_count() or 1)
+def latency_samples():
+    """Stride samples for the least-latency references (its oracle takes 20 ms to
+    1 s a candidate on these workloads)."""
     out = {}
-    thr4, f1b4 = cfg4_samples()
+    for n in (3, 5):
+        out[n] = np.arange(0, orc.Oracle(workloads.config(n)).n_instances(), 97)
+    o = orc.Oracle(workloads.config(4))
+    n_ord, n_b = o.n_orders(), len(workloads.config(4)["space"]["micro"])
+    cfg = np.arange(0, len(o.configs()), 6)
+    out[4] = (cfg * n_ord + (cfg // 6) % n_ord) * n_b + (cfg * 11) % n_b
+    return out
+
+
+def main():
+    args = [a for a in sys.argv[1:] if a != "latency"]
+    workers = int(args[0]) if args else (os.cpu_count() or 1)
+    only_latency = "latency" in sys.argv[1:]
+    out = {}
+    if only_latency:
+        with np.load(OUT) as f:
+            out = {k: f[k] for k in f.files}
+    lat = latency_samples()
     with get_context("spawn").Pool(workers) as pool:
+        for n, chunk in ((3, 40), (5, 40), (4, 4)):
+            out[f"cfg{n}_latency_idx"] = lat[n]
+            out[f"cfg{n}_latency"] = run(pool, f"cfg{n}", "latency", lat[n], chunk)
+        if only_latency:
+            np.savez_compressed(OUT, **out)
+            print("wrote", OUT, os.path.getsize(OUT), "bytes")
+            return
+        thr4, f1b4 = cfg4_samples()
         for n in (3, 5):
             N = orc.Oracle(workloads.config(n)).n_instances()
             idx = np.arange(N)

@@ -6,7 +6,8 @@ the oracle's results, written by tests/golden/make_parity_refs.py from oracle/
 alone: configurations 3 and 5 in full under both objectives, configuration 4
 with one candidate of every (configuration, ordering) key (B rotating over
 1..64) and one of every configuration under the 1F1B re-scoring, and 16
-sixteen-stage candidates of configuration 3 under the device-count DP.  A digest
+sixteen-stage candidates of configuration 3 under the device-count DP, and
+stride samples of configurations 3, 4 and 5 under the least 1F1B latency.  A digest
 covers status, objective, stage sum, largest stage, recomputation mask, stage
 lengths (and stage types); a mismatch is re-checked against the oracle itself
 and reported field by field.
@@ -45,7 +46,7 @@ def _explain(problem, res, idx, objective, types=None):
     o = orc.Oracle(problem)
     out = []
     for i in idx[:3]:
-        r = o.solve(int(i)) if objective == "threshold" else o.solve_exact(int(i))
+        r = {"threshold": o.solve, "1f1b": o.solve_exact, "latency": o.solve_latency}[objective](int(i))
         g = res[int(i)]
         out.append((int(i), {"gpu": (int(g["status"]), int(g["objective"]), int(g["stage_sum"]), int(g["t_max"]),
                                      list(g["layers"][:r["pp"]])),
@@ -99,3 +100,20 @@ def test_device_count_dp_sixteen_stages(torch, refs):
     got = parity_digest.of_gpu(res, idx, types)
     assert np.array_equal(got, refs["cfg3_types16"]), np.nonzero(got != refs["cfg3_types16"])[0]
     assert (res["status"][idx] == 0).any()
+
+
+@pytest.mark.parametrize("n", [3, 5, 4])
+def test_least_latency_samples(torch, refs, n):
+    """The least 1F1B latency (hapmoe_stage_dp_latency) on every 97th candidate
+    of configurations 3 and 5 and one candidate of every 6th configuration of
+    configuration 4, each from a one-candidate launch."""
+    p = workloads.config(n)
+    print(f"config {n}, least latency: stride sample", flush=True)
+    pl = binding.Planner(p, "cuda:0")
+    pl.eval_cost_tables()
+    idx = refs[f"cfg{n}_latency_idx"]
+    for i in idx:
+        pl.stage_dp(first=int(i), count=1, objective="latency")
+    res = pl.results()
+    assert _check(p, res, refs, f"cfg{n}_latency", "latency") == len(idx)
+    assert (res["status"][idx] == 0).sum() > 10
