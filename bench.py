@@ -524,6 +524,13 @@ def main():
     progress(f"timed {args.steps} steps")
 
     clocks = binding.section_clocks(clear=True) if args.section_clocks else None
+    if clocks is not None:
+        # one launch alone: its longest key and when its waves finish (wall clock)
+        pl.stage_dp()
+        torch.cuda.synchronize()
+        one = binding.section_clocks(clear=True)
+        clocks["single_launch_wall"] = {k: one[k] for k in ("longest_key_us", "longest_key_pp",
+                                                           "first_wave_done_us", "last_wave_done_us") if k in one}
     dp_s = ms["stage_dp"] / 1e3
     achieved = (relax * OPS_PER_RELAXATION + evals * OPS_PER_EVALUATION) / dp_s
     out = {

@@ -203,8 +203,18 @@ def section_clocks(clear=True) -> dict:
     _check(lib().hapmoe_section_clocks(out, 1 if clear else 0), "hapmoe_section_clocks")
     v = list(out)
     total = max(v[5], 1)
-    return {"share": {n: v[i] / total for i, n in enumerate(SECTION_NAMES)}, "wave_cycles": v[5],
-            "keys": v[6], "segment_batches": v[7], "passes": v[8]}
+    out = {"share": {n: v[i] / total for i, n in enumerate(SECTION_NAMES)}, "wave_cycles": v[5],
+           "keys": v[6], "segment_batches": v[7], "passes": v[8]}
+    khz = v[13]
+    if khz and v[12]:
+        us = 1e3 / khz   # microseconds a tick
+        start, end_min, end_max = (~v[10]) & (2**64 - 1), (~v[11]) & (2**64 - 1), v[12]
+        # wall-clock view of the last launch (the maxima span every launch since the clear)
+        out["longest_key_us"] = (v[9] >> 6) * us
+        out["longest_key_pp"] = v[9] & 63
+        out["first_wave_done_us"] = (end_min - start) * us
+        out["last_wave_done_us"] = (end_max - start) * us
+    return out
 
 
 def _hp(problem):

@@ -1,6 +1,8 @@
 // Segmented arg-min over the stage-DP results (the outer min of Eq. 1 over pi
 // and the candidate's ordering and B): per configuration pi the best of its
 // candidates, then the global best.  Order: objective, then candidate index.
+// Two kernels: the streaming partial minima over 4,096-candidate chunks, then
+// one workgroup for the per-configuration and global minima and the winner.
 // Reading the 8-byte objective of every 64-byte result record, this is a
 // streaming (HBM-bound) reduction.
 #include <mutex>
@@ -86,48 +88,36 @@ __global__ __launch_bounds__(kThreads) void k_seg_partial(const hapmoe_dp_result
     if (threadIdx.x == 0) partial[cfg * chunks + ch] = v;
 }
 
-// level 2: per configuration over its chunks
-__global__ __launch_bounds__(kThreads) void k_seg_final(const Best *__restrict__ partial, int64_t n_configs,
-                                                        int64_t chunks, Best *__restrict__ cfg_best,
-                                                        int64_t *__restrict__ config_best)
-{
-    const int64_t cfg = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (cfg >= n_configs) return;
-    Best v = {kInf, INT64_MAX};
-    for (int64_t k = 0; k < chunks; ++k) {
-        const Best o = partial[cfg * chunks + k];
-        if (better(o, v)) v = o;
-    }
-    cfg_best[cfg] = v;
-    if (config_best) config_best[cfg] = v.obj == kInf ? -1 : v.idx;
-}
-
-// level 3: global best over configurations (one workgroup)
-__global__ __launch_bounds__(1024) void k_global(const Best *__restrict__ cfg_best, int64_t n_configs,
-                                                 Best *__restrict__ out)
-{
-    __shared__ Best sh[1024 / 64];
-    Best v = {kInf, INT64_MAX};
-    for (int64_t i = threadIdx.x; i < n_configs; i += blockDim.x) {
-        const Best o = cfg_best[i];
-        if (better(o, v)) v = o;
-    }
-    v = block_min(v, sh);
-    if (threadIdx.x == 0) *out = v;
-}
-
 int64_t chunks_per_config(int64_t per) { return (per + kChunk - 1) / kChunk; }
 
-// The winner's result, candidate and stage layout, copied next to the global
-// best so that the host reads everything with one copy.
-__global__ __launch_bounds__(64) void k_gather(const Best *__restrict__ glob, const hapmoe_dp_result *__restrict__ res,
-                                               const hapmoe_candidate *__restrict__ cand,
-                                               const unsigned char *__restrict__ key_info,
-                                               const uint8_t *__restrict__ types, int64_t n_micro,
-                                               uint32_t *__restrict__ out)
+constexpr int kFinishThreads = 1024;
+
+// levels 2 and 3 in one workgroup: per configuration over its chunks (into
+// config_best), the global best over configurations, then the winner's result,
+// candidate and stage layout copied next to it, so that the host reads
+// everything with one copy.
+__global__ __launch_bounds__(kFinishThreads) void k_finish(const Best *__restrict__ partial, int64_t n_configs,
+                                                           int64_t chunks, int64_t *__restrict__ config_best,
+                                                           const hapmoe_dp_result *__restrict__ res,
+                                                           const hapmoe_candidate *__restrict__ cand,
+                                                           const unsigned char *__restrict__ key_info,
+                                                           const uint8_t *__restrict__ types, int64_t n_micro,
+                                                           Best *__restrict__ glob, uint32_t *__restrict__ out)
 {
-    const Best b = *glob;
-    if (b.obj == kInf) return;
+    __shared__ Best sh[kFinishThreads / 64];
+    Best v = {kInf, INT64_MAX};
+    for (int64_t cfg = threadIdx.x; cfg < n_configs; cfg += kFinishThreads) {
+        Best c = {kInf, INT64_MAX};
+        for (int64_t k = 0; k < chunks; ++k) {
+            const Best o = partial[cfg * chunks + k];
+            if (better(o, c)) c = o;
+        }
+        if (config_best) config_best[cfg] = c.obj == kInf ? -1 : c.idx;
+        if (better(c, v)) v = c;
+    }
+    const Best b = block_min(v, sh);
+    if (threadIdx.x == 0) *glob = b;
+    if (b.obj == kInf || threadIdx.x >= 64) return;
     const int w = threadIdx.x;
     constexpr int kRes = (int)sizeof(hapmoe_dp_result) / 4, kCand = (int)sizeof(hapmoe_candidate) / 4;
     constexpr int kKey = (int)sizeof(KeyInfo) / 4;
@@ -163,13 +153,13 @@ hipError_t best_plan_scratch(void **ptr, int64_t *bytes)
     return hipSuccess;
 }
 
-// workspace: [global Best][winner: result | candidate | stage layout][cfg_best
-// n_configs][partial n_configs * chunks]
+// workspace: [global Best][winner: result | candidate | stage layout][partial
+// n_configs * chunks]
 int64_t best_plan_ws_bytes(int64_t n, int64_t per_config, int64_t n_configs)
 {
     (void)n;
     const int64_t chunks = chunks_per_config(per_config);
-    return (int64_t)sizeof(Best) * (1 + n_configs + n_configs * chunks) + kWinnerBytes;
+    return (int64_t)sizeof(Best) * (1 + n_configs * chunks) + kWinnerBytes;
 }
 
 hipError_t launch_best_plan(const hapmoe_dp_result *d_res, const hapmoe_candidate *d_cand,
@@ -180,14 +170,11 @@ hipError_t launch_best_plan(const hapmoe_dp_result *d_res, const hapmoe_candidat
     const int64_t chunks = chunks_per_config(per_config);
     Best *glob = static_cast<Best *>(d_ws);
     auto *winner = reinterpret_cast<uint32_t *>(static_cast<unsigned char *>(d_ws) + sizeof(Best));
-    Best *cfg_best = reinterpret_cast<Best *>(static_cast<unsigned char *>(d_ws) + sizeof(Best) + kWinnerBytes);
-    Best *partial = cfg_best + n_configs;
+    Best *partial = reinterpret_cast<Best *>(static_cast<unsigned char *>(d_ws) + sizeof(Best) + kWinnerBytes);
     hipLaunchKernelGGL(k_seg_partial, dim3((unsigned)n_configs, (unsigned)chunks), dim3(kThreads), 0, s, d_res,
                        d_cand, n, per_config, chunks, global_batch, mbs, partial);
-    hipLaunchKernelGGL(k_seg_final, dim3((unsigned)((n_configs + kThreads - 1) / kThreads)), dim3(kThreads), 0, s,
-                       partial, n_configs, chunks, cfg_best, d_config_best);
-    hipLaunchKernelGGL(k_global, dim3(1), dim3(1024), 0, s, cfg_best, n_configs, glob);
-    hipLaunchKernelGGL(k_gather, dim3(1), dim3(64), 0, s, glob, d_res, d_cand, d_key_info, d_types, n_micro, winner);
+    hipLaunchKernelGGL(k_finish, dim3(1), dim3(kFinishThreads), 0, s, partial, n_configs, chunks, d_config_best,
+                       d_res, d_cand, d_key_info, d_types, n_micro, glob, winner);
     return hipGetLastError();
 }
 

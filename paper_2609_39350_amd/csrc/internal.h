@@ -142,7 +142,11 @@ hipError_t launch_latency_dp(const void *d_image, const hapmoe_candidate *d_cand
 // section clocks of the stage-DP kernel (libraries built with HAPMOE_SECTION_CLOCKS)
 enum {
     kClockSetup, kClockScan, kClockRelax, kClockTrace, kClockControl, kClockTotal,
-    kCountKeys, kCountBatches, kCountPasses, kSectionClocks
+    kCountKeys, kCountBatches, kCountPasses,
+    // wall-clock (constant-rate counter) records: the longest key of any wave
+    // (ticks << 6 | its pipeline depth), the earliest wave start and end
+    // (stored complemented, so that all three are maxima), the latest wave end
+    kKeyMax, kWaveStartMinC, kWaveEndMinC, kWaveEndMax, kWallClockKHz, kSectionClocks
 };
 int32_t stage_dp_section_clocks(uint64_t *out, bool clear);
 

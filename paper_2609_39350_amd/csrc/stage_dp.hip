@@ -76,7 +76,10 @@ __device__ unsigned long long g_section_clocks[kSectionClocks];
 #define HAPMOE_CLOCK_VARS                                                           \
     unsigned long long clk_acc[kSectionClocks] = {};                                \
     const unsigned long long clk_start = clock64();                                 \
-    unsigned long long clk_last = clk_start
+    unsigned long long clk_last = clk_start;                                        \
+    const unsigned long long wall_start = wall_clock64();                           \
+    unsigned long long key_start = 0;                                               \
+    int key_pp = 0
 #define HAPMOE_CLOCK(sec)                                                           \
     do {                                                                            \
         const unsigned long long clk_now = clock64();                               \
@@ -84,17 +87,34 @@ __device__ unsigned long long g_section_clocks[kSectionClocks];
         clk_last = clk_now;                                                         \
     } while (0)
 #define HAPMOE_CLOCK_RESTART() (clk_last = clock64())
+// at the top of the key loop: the previous key of this wave has ended
+#define HAPMOE_KEY_MARK(lane)                                                       \
+    do {                                                                            \
+        const unsigned long long now_ = wall_clock64();                             \
+        if (key_start && (lane) == 0)                                               \
+            atomicMax(&g_section_clocks[kKeyMax], ((now_ - key_start) << 6) | (unsigned long long)key_pp); \
+        key_start = now_;                                                           \
+    } while (0)
+#define HAPMOE_KEY_PP(pp) (key_pp = (pp))
 #define HAPMOE_COUNT(sec) (++clk_acc[sec])
 #define HAPMOE_CLOCK_FLUSH(lane)                                                    \
     do {                                                                            \
         clk_acc[kClockTotal] = clock64() - clk_start;                               \
         if ((lane) == 0)                                                            \
-            for (int i_ = 0; i_ < kSectionClocks; ++i_) atomicAdd(&g_section_clocks[i_], clk_acc[i_]); \
+            for (int i_ = 0; i_ < kCountPasses + 1; ++i_) atomicAdd(&g_section_clocks[i_], clk_acc[i_]); \
+        const unsigned long long wend_ = wall_clock64();                            \
+        if ((lane) == 0) {                                                          \
+            atomicMax(&g_section_clocks[kWaveStartMinC], ~wall_start);              \
+            atomicMax(&g_section_clocks[kWaveEndMinC], ~wend_);                     \
+            atomicMax(&g_section_clocks[kWaveEndMax], wend_);                       \
+        }                                                                           \
     } while (0)
 #else
 #define HAPMOE_CLOCK_VARS
 #define HAPMOE_CLOCK(sec)
 #define HAPMOE_CLOCK_RESTART()
+#define HAPMOE_KEY_MARK(lane)
+#define HAPMOE_KEY_PP(pp)
 #define HAPMOE_COUNT(sec)
 #define HAPMOE_CLOCK_FLUSH(lane)
 #endif
@@ -396,6 +416,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
     // soon and costs more in balance than it saves, at every depth measured.
     for (;;) {
         HAPMOE_CLOCK_RESTART();
+        HAPMOE_KEY_MARK(lane);
         uint32_t qi = 0;
         if (lane == 0) qi = atomicAdd(queue, 1u);
         // wave-uniform from here on: everything indexed by the key stays scalar
@@ -405,6 +426,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
         const int64_t cfg = key / H.n_orders;
         const int64_t idx0 = key * nB;
         const int PP = __builtin_amdgcn_readfirstlane(cand[idx0].pp);
+        HAPMOE_KEY_PP(PP);
         const PiInfo *pi = reinterpret_cast<const PiInfo *>(tab + L.off_pi) + cfg;
         const KeyInfo *ki = reinterpret_cast<const KeyInfo *>(tab + L.off_key) + key;
         // The configuration's memory prefix sums (stored to LDS for the class
@@ -1492,6 +1514,11 @@ int32_t stage_dp_section_clocks(uint64_t *out, bool clear)
 #ifdef HAPMOE_SECTION_CLOCKS
     if (hipMemcpyFromSymbol(out, HIP_SYMBOL(g_section_clocks), sizeof(uint64_t) * kSectionClocks) != hipSuccess)
         return HAPMOE_E_HIP;
+    int dev = 0, khz = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess)
+        return HAPMOE_E_HIP;
+    out[kWallClockKHz] = (uint64_t)khz;
     if (clear) {
         const uint64_t z[kSectionClocks] = {};
         if (hipMemcpyToSymbol(HIP_SYMBOL(g_section_clocks), z, sizeof(z)) != hipSuccess) return HAPMOE_E_HIP;
