@@ -308,15 +308,21 @@ __device__ inline uint64_t step_bit(int m, int mtop)
 }
 
 // Entry e of a stage's (segment, end layer) list: segment q = e / wd and
-// k = e % wd.  The fp32 quotient is off by at most one for e < 2^10 and is
-// corrected by one integer step.
-__device__ inline void split_entry(int e, int wd, float inv_wd, int &q, int &k)
+// k = e % wd, as q = (e * ceil(2^16 / wd)) >> 16.  For 1 <= wd <= 128 this is
+// the exact floor for every e < 4 wd + 64 (checked exhaustively), which covers
+// the entries of up to four segments plus the lanes past the last one.
+struct DivMulTable {
+    uint32_t m[129];
+    constexpr DivMulTable() : m()
+    {
+        for (int d = 1; d <= 128; ++d) m[d] = (65536u + (uint32_t)d - 1u) / (uint32_t)d;
+    }
+};
+__constant__ DivMulTable kDivMul = DivMulTable();
+
+__device__ inline void split_entry(int e, int wd, uint32_t mul, int &q, int &k)
 {
-    q = (int)((float)e * inv_wd);
-    if (q * wd > e)
-        --q;
-    else if ((q + 1) * wd <= e)
-        ++q;
+    q = (int)(__umul24((uint32_t)e, mul) >> 16);
     k = e - q * wd;
 }
 
@@ -874,13 +880,12 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                     // stage, and a wave-uniform split-point loop: a lane with less to
                     // do runs masked (clamped, in-range loads; predicated stores only)
                     const int total = nq * wd_s;
-                    // approximate reciprocal: split_entry corrects the quotient
-                    const float inv_wd = nq > 1 ? __builtin_amdgcn_rcpf((float)wd_s) : 0.0f;
+                    const uint32_t mul_wd = kDivMul.m[wd_s];   // wd_s <= N - PP + 1 <= 127
                     for (int e0 = 0; e0 < total; e0 += 64) {
                         const int e = e0 + lane;
                         const bool act = e < total;
                         int qi = 0, k = act ? e : 0;
-                        if (nq > 1) split_entry(k, wd_s, inv_wd, qi, k);   // wave-uniform branch
+                        if (nq > 1) split_entry(k, wd_s, mul_wd, qi, k);   // wave-uniform branch
                         const int q = (qmap >> (2 * qi)) & 3;
                         const int64_t t = CTL[q].t;
                         const uint8_t *const AMq = REG + ((cmap >> (2 * q)) & 3) * arr_bytes;   // class
