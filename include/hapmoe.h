@@ -325,7 +325,8 @@ int32_t hapmoe_stage_dp_1f1b(const hapmoe_problem *p, const void *d_image,
  *   T = sum_i c_i + sum_{i <= s} ceil(c_i / 3) + max(0, B - s - 1) * max_i c_i,
  * s the first (1-based) stage of largest cost, minimised over every partition
  * that passes the three prunings (stage costs, recomputation and memory as in
- * hapmoe_stage_dp).  For every distinct stage cost t, ascending, a DP over
+ * hapmoe_stage_dp).  For every distinct stage cost t, ascending from the least
+ * possible largest stage (the thresholds below it admit no partition), a DP over
  * (stage, end layer, bottleneck placed yet) gives the least T with largest
  * stage exactly t; the sweep stops once F_inf + ceil(t / 3) +
  * max(0, B - PP - 1) t, F_inf the least stage sum, reaches the best T.  Ties:
@@ -333,12 +334,13 @@ int32_t hapmoe_stage_dp_1f1b(const hapmoe_problem *p, const void *d_image,
  * (b_PP-1, ..., b_1) of the stage end layers.  For each candidate of
  * [first, first + count) writes d_res[i - first]: objective = T + C, stage_sum
  * and t_max of the chosen partition, its recomputation mask and stage lengths.
- * One workgroup per candidate, 64 KB of LDS.  Its stage-cost table holds, for
- * every stage, end layer b of the stage's band (the end layers its windows
- * allow) and split point of its window, an 8-byte cost and a 1-byte
- * recomputation flag (the flags rounded up to 16 bytes), plus 16 bytes of DP
- * state for every (stage, b); a candidate whose table exceeds 63,744 bytes gets
- * HAPMOE_STATUS_OVERFLOW.  d_stats (may be NULL): thresholds swept and DP
+ * One workgroup per candidate.  Its stage-cost table holds, for every stage,
+ * end layer b of the stage's band (the end layers its windows allow) and split
+ * point of its window, an 8-byte cost and a 1-byte recomputation flag (the
+ * flags rounded up to 16 bytes), plus 16 bytes of DP state for every (stage, b).
+ * Two launches: every candidate with 24 KB of LDS a workgroup, then those whose
+ * table did not fit (over 22,784 bytes) with 160 KB; a candidate whose table
+ * exceeds 162,048 bytes gets HAPMOE_STATUS_OVERFLOW.  d_stats (may be NULL): thresholds swept and DP
  * relaxations of each candidate (columns 2, 3 zero).  No workspace.  Not for
  * stage_types = 2 or 3 (HAPMOE_E_INVAL); ranges and errors as hapmoe_stage_dp.
  * Asynchronous. */

@@ -10,8 +10,9 @@
 // stage is placed: before it a stage needs c < t and weighs c + ceil(c / 3);
 // the bottleneck stage s has c = t and weighs t + ceil(t / 3) +
 // max(0, B - s - 1) t; after it a stage needs c <= t and weighs c.  The
-// thresholds are the distinct finite stage costs, taken in ascending order;
-// the sweep stops at the first t where F_inf + ceil(t / 3) +
+// thresholds are the distinct finite stage costs, taken in ascending order
+// from t_bot, the least possible largest stage (one min-max pass: below it no
+// partition exists, so those passes would change nothing); the sweep stops at the first t where F_inf + ceil(t / 3) +
 // max(0, B - PP - 1) t (a lower bound of T for this and every larger t,
 // F_inf the least stage sum) reaches the best T found.  Ties: the least T,
 // then the lower largest stage (the first threshold reaching it), then the
@@ -19,7 +20,9 @@
 // set of (end layer, z) states on optimal paths and at every stage takes the
 // smallest split point through which one continues optimally.
 //
-// Mapping: one wave64 workgroup per candidate (grid-stride).  The candidate's
+// Mapping: one wave64 workgroup per candidate (grid-stride); a first launch
+// with 24 KB of LDS a workgroup, a second with 160 KB for the candidates whose
+// tables did not fit.  The candidate's
 // stage costs -- every (stage, end layer b in the stage's band, split point a
 // in the window) with the memory test of its stored micro-batch count,
 // recomputation and prunings 1 and 3, exactly as the threshold DP prices them
@@ -33,8 +36,12 @@ namespace hapmoe {
 namespace {
 
 constexpr int64_t kLBig = int64_t(1) << 62;   // "no path" inside the DP, far from overflow
-constexpr int kLatLds = 64 * 1024;            // LDS of one workgroup (two fit a CU)
+// Two launches: every candidate with a 24 KB workgroup (six fit a CU), then the
+// candidates whose table did not fit, with 160 KB (one a CU).
+constexpr int kLatLdsSmall = 24 * 1024;
+constexpr int kLatLdsLarge = 160 * 1024;
 constexpr int kLatBlocks = 2048;              // grid-stride launch width
+constexpr int32_t kStatusRetry = 3;           // between the two launches only: table too big for the first
 
 struct LatStage {
     int blo, wd;     // band of end layers [blo, blo + wd)
@@ -50,36 +57,35 @@ struct LatHead {
     int32_t flag[kMaxStages];
 };
 
-// the stage-cost table may use 64 KB less the header: 63,744 bytes (documented)
+// the stage-cost table may use 160 KB less the header: 162,048 bytes (documented)
 static_assert(sizeof(LatHead) == 1792, "LDS header size is part of the documented table limit");
 
 __device__ inline int64_t ceil3(int64_t c) { return (c + 2) / 3; }
 
-// Wave-wide minimum of an int64 through LDS (every lane gets it).
-__device__ inline int64_t lat_min(int64_t v, int64_t *red, int lane)
+__device__ inline int64_t shfl_xor64(int64_t v, int d)
 {
-    red[lane] = v;
-    __syncthreads();
-    for (int o = 32; o >= 1; o >>= 1) {
-        if (lane < o) red[lane] = red[lane + o] < red[lane] ? red[lane + o] : red[lane];
-        __syncthreads();
-    }
-    const int64_t m = red[0];
-    __syncthreads();
-    return m;
+    const int lo = __shfl_xor((int)(uint32_t)(uint64_t)v, d, 64);
+    const int hi = __shfl_xor((int)(uint32_t)((uint64_t)v >> 32), d, 64);
+    return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
 }
 
-__device__ inline int64_t lat_sum(int64_t v, int64_t *red, int lane)
+// Wave-wide minimum and sum of an int64 (every lane gets the result; call with
+// every lane of the wave active).
+__device__ inline int64_t lat_min(int64_t v)
 {
-    red[lane] = v;
-    __syncthreads();
-    for (int o = 32; o >= 1; o >>= 1) {
-        if (lane < o) red[lane] += red[lane + o];
-        __syncthreads();
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) {
+        const int64_t o = shfl_xor64(v, d);
+        v = o < v ? o : v;
     }
-    const int64_t m = red[0];
-    __syncthreads();
-    return m;
+    return v;
+}
+
+__device__ inline int64_t lat_sum(int64_t v)
+{
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) v += shfl_xor64(v, d);
+    return v;
 }
 
 __device__ inline void lat_write(hapmoe_dp_result *out, int status, int64_t obj, int64_t sum, int64_t tmax,
@@ -93,16 +99,20 @@ __device__ inline void lat_write(hapmoe_dp_result *out, int status, int64_t obj,
     for (int s = 0; s < kMaxStages; ++s) out->layers[s] = (uint8_t)(len && s < pp ? len[s] : 0);
 }
 
+// lds_bytes: the workgroup's LDS; retry: process only the candidates the first
+// launch marked kStatusRetry (last: no larger launch follows, so a table that
+// does not fit is HAPMOE_STATUS_OVERFLOW)
 template <bool STATS>
 __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, const hapmoe_candidate *cand,
                                                    const unsigned char *tab, TablesLayout L, int64_t first,
-                                                   int64_t count, hapmoe_dp_result *res, int32_t *stats)
+                                                   int64_t count, hapmoe_dp_result *res, int32_t *stats,
+                                                   int lds_bytes, int retry, int last)
 {
     extern __shared__ __align__(16) unsigned char smem[];
     const ImageHeader &H = *reinterpret_cast<const ImageHeader *>(img);
     LatHead &D = *reinterpret_cast<LatHead *>(smem);
     unsigned char *dyn = smem + ((sizeof(LatHead) + 15) & ~size_t(15));
-    const int dyn_bytes = kLatLds - (int)((sizeof(LatHead) + 15) & ~size_t(15));
+    const int dyn_bytes = lds_bytes - (int)((sizeof(LatHead) + 15) & ~size_t(15));
     const int lane = threadIdx.x;
     const int N = H.n_layers, nB = H.n_micro;
     const int64_t np = L.np;
@@ -113,6 +123,7 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
         const int PP = cand[inst].pp;
         const int64_t B = cand[inst].n_micro;
         hapmoe_dp_result *out = res + i;
+        if (retry && out->status != kStatusRetry) continue;   // wave-uniform
         int32_t *st_out = STATS ? stats + 4 * i : nullptr;
         const PiInfo *pi = reinterpret_cast<const PiInfo *>(tab + L.off_pi) + cfg;
         const KeyInfo *ki = reinterpret_cast<const KeyInfo *>(tab + L.off_key) + key;
@@ -177,7 +188,7 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
         // LDS: cost table [ncost] int64 | DP states [nv][2] int64 | recomputation flags [ncost] u8
         const int need = ncost * 8 + nv * 16 + ((ncost + 15) & ~15);
         if (need > dyn_bytes) {
-            finish(HAPMOE_STATUS_OVERFLOW);
+            finish(last ? HAPMOE_STATUS_OVERFLOW : kStatusRetry);
             continue;
         }
         int64_t *Cst = reinterpret_cast<int64_t *>(dyn);
@@ -226,7 +237,13 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
         // One pass over the stages.  lat = false: the least stage sum (state z = 0
         // only); lat = true: the least latency weight with the largest stage
         // exactly t, states z = 0 / 1.  Returns the relaxations this lane made.
-        auto pass = [&](bool lat, int64_t t) -> int64_t {
+        // One pass over the stages, every (end layer, z) state of a stage on its own
+        // lane.  mode 0: the least stage sum (state z = 0 only); 1: the least
+        // latency weight with the largest stage exactly t (states z = 0 / 1); 2:
+        // the least possible largest stage (z = 0 only).  Returns the latency
+        // relaxations this lane made.
+        auto pass = [&](int mode, int64_t t) -> int64_t {
+            const bool lat = mode == 1;
             int64_t nrel = 0;
             for (int s = 0; s < PP; ++s) {
                 const LatStage S = D.st[s];
@@ -242,8 +259,13 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
                             if (c >= kLBig) continue;
                             const int a = b - S.lo - j;
                             const int64_t v0 = s ? V[2 * (P.voff + a - P.blo)] : (a == 0 ? 0 : kLBig);
-                            if (!lat) {
+                            if (mode == 0) {
                                 if (v0 < kLBig && v0 + c < best) best = v0 + c;
+                                continue;
+                            }
+                            if (mode == 2) {
+                                const int64_t m = v0 > c ? v0 : c;
+                                if (v0 < kLBig && m < best) best = m;
                                 continue;
                             }
                             if (STATS) ++nrel;
@@ -264,7 +286,7 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
             return nrel;
         };
 
-        pass(false, 0);
+        pass(0, 0);
         const LatStage SL = D.st[PP - 1];
         const int64_t finf = V[2 * (SL.voff + (N - SL.blo))];
         __syncthreads();
@@ -272,8 +294,13 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
             finish(HAPMOE_STATUS_INFEASIBLE);
             continue;
         }
+        // no partition has a largest stage below t_bot: the sweep starts there
+        // (the passes below it find no path and change nothing)
+        pass(2, 0);
+        const int64_t tbot = V[2 * (SL.voff + (N - SL.blo))];
+        __syncthreads();
         const int64_t steady_min = B - PP - 1 > 0 ? B - PP - 1 : 0;
-        int64_t best = kLBig, tbest = 0, bsum = 0, tprev = -1, relax = 0;
+        int64_t best = kLBig, tbest = 0, bsum = 0, tprev = tbot - 1, relax = 0;
         uint32_t brm = 0;
         int swept = 0;
         for (;;) {
@@ -283,10 +310,10 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
                 const int64_t c = Cst[e];
                 if (c > tprev && c < tn) tn = c;
             }
-            const int64_t t = lat_min(tn, D.red, lane);
+            const int64_t t = lat_min(tn);
             if (t >= kLBig) break;
             if (finf + ceil3(t) + steady_min * t >= best) break;
-            relax += pass(true, t);
+            relax += pass(1, t);
             ++swept;
             tprev = t;
             const int64_t v = V[2 * (SL.voff + (N - SL.blo)) + 1];
@@ -325,7 +352,7 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
                         aj = j;
                     }
                 }
-                const int64_t na = lat_min(amin, D.red, lane);
+                const int64_t na = lat_min(amin);
                 const bool mine = amin == na && na < kLBig;
                 const uint64_t b0 = __ballot(mine && m0), b1 = __ballot(mine && m1);
                 const uint64_t who = __ballot(mine);
@@ -351,7 +378,7 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
             finish(HAPMOE_STATUS_INFEASIBLE);
             continue;
         }
-        const int64_t nrel = STATS ? lat_sum(relax, D.red, lane) : 0;
+        const int64_t nrel = STATS ? lat_sum(relax) : 0;
         if (lane == 0) {
             lat_write(out, HAPMOE_STATUS_OK, best + ki->dp_const, bsum, tbest, brm, D.len, PP);
             if (STATS) {
@@ -374,13 +401,17 @@ hipError_t launch_latency_dp(const void *d_image, const hapmoe_candidate *d_cand
     const int grid = (int)(count < kLatBlocks ? count : kLatBlocks);
     const auto *img = static_cast<const unsigned char *>(d_image);
     const auto *tab = static_cast<const unsigned char *>(d_tables);
-    if (d_stats)
-        hipLaunchKernelGGL(k_latency_dp<true>, dim3(grid), dim3(64), kLatLds, stream, img, d_cand, tab, L, first,
-                           count, d_res, d_stats);
-    else
-        hipLaunchKernelGGL(k_latency_dp<false>, dim3(grid), dim3(64), kLatLds, stream, img, d_cand, tab, L, first,
-                           count, d_res, d_stats);
-    return hipGetLastError();
+    auto go = [&](auto kern) -> hipError_t {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, kLatLdsLarge);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(kern, dim3(grid), dim3(64), kLatLdsSmall, stream, img, d_cand, tab, L, first, count,
+                           d_res, d_stats, kLatLdsSmall, 0, 0);
+        hipLaunchKernelGGL(kern, dim3(grid), dim3(64), kLatLdsLarge, stream, img, d_cand, tab, L, first, count,
+                           d_res, d_stats, kLatLdsLarge, 1, 1);
+        return hipGetLastError();
+    };
+    return d_stats ? go(k_latency_dp<true>) : go(k_latency_dp<false>);
 }
 
 }  // namespace hapmoe
