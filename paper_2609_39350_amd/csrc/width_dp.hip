@@ -25,9 +25,9 @@
 // the incumbent)).  The incumbent is replaced by a lower sum + (B-1) max, or an
 // equal one with a lower max, so the result is the least objective, the least
 // threshold reaching it and the back-trace there.  Plain int64 min-plus work on
-// the VALU; F and the back-trace pointers live in the workgroup's slice of the
-// workspace, the memory prefix sums and the stage layouts of the half-group
-// ranges in LDS.
+// the VALU; F of two levels, the memory prefix sums and the stage layouts of the
+// half-group ranges live in LDS, the back-trace pointers in the workgroup's
+// slice of the workspace.
 #include "internal.h"
 
 namespace hapmoe {
@@ -244,7 +244,10 @@ __global__ __launch_bounds__(kThreads) void k_width_dp(const unsigned char *__re
     __shared__ uint8_t s_plen[kMaxStages], s_pw[kMaxStages], s_pmask[kMaxStages];
     __shared__ uint32_t s_relax;
 
-    int64_t *F = reinterpret_cast<int64_t *>(slots + (int64_t)blockIdx.x * slot_bytes);
+    // F of two levels in LDS; the back-trace pointers in the workgroup's slice
+    extern __shared__ __align__(16) unsigned char w_dyn[];
+    int64_t *F = reinterpret_cast<int64_t *>(w_dyn);
+    int16_t *const ARG = reinterpret_cast<int16_t *>(slots + (int64_t)blockIdx.x * slot_bytes);
     for (;;) {
         if (tid == 0) ctl.qi = atomicAdd(queue, 1u);
         __syncthreads();
@@ -261,7 +264,6 @@ __global__ __launch_bounds__(kThreads) void k_width_dp(const unsigned char *__re
         const KeyInfo *ki = reinterpret_cast<const KeyInfo *>(tab + L.off_key) + key;
         hapmoe_dp_result *out = res + k;
         uint8_t *tout = types_out + k * kMaxStages, *wout = widths_out + k * kMaxStages;
-        int16_t *ARG = reinterpret_cast<int16_t *>(F + 2 * (int64_t)W * UP);
         if (pi->status != HAPMOE_STATUS_OK) {
             if (tid == 0) {
                 out->objective = out->stage_sum = out->t_max = kInf;
@@ -411,14 +413,31 @@ __global__ __launch_bounds__(kThreads) void k_width_dp(const unsigned char *__re
                         if (u0 < i - 1 || u0 > 3 * (i - 1)) continue;
                         const WStage &x = s_st[u0][w - 1];
                         if (x.mask == 0) continue;
-                        int alo = b - x.hi, ahi = b - x.lo;
+                        int alo = b - x.hi, ahi = b - x.lo;   // the window: n = b - a in [lo, hi]
                         alo = alo < i - 1 ? i - 1 : alo;
+                        // stage_cost with its end-layer terms read once per (b, w)
+                        const int wi = w - 1;
+                        const int64_t ms = (int64_t)(PP - (i - 1)) < B ? (int64_t)(PP - (i - 1)) : B;
+                        const int64_t *P = wtime + ((int64_t)(x.mask - 1) * 3 + wi) * 3 * np;
+                        const int64_t p0b = P[b], p1b = P[np + b], p2b = (x.flags & 1) ? P[2 * np + b] : 0;
+                        const int64_t mwb = s_mw[wi][b], ma0b = s_ma0[wi][b], ma1b = s_ma1[wi][b];
+                        const int moeb = s_moe[b];
+                        const int64_t xw = s_x[wi], hc_b = (x.flags & 2) ? x.p2p : 0;
                         for (int a = alo; a <= ahi; ++a) {
                             const int64_t prev = Fp[(int64_t)a * UP + u0];
                             if (prev == kNone) continue;
-                            int rf;
-                            const int64_t cst = stage_cost(i - 1, u0, w, a, b, &rf);
-                            if (cst == kNone || cst > t) continue;
+                            const int64_t ex = (moeb - s_moe[a]) > 0 ? xw : 0;
+                            const int64_t dw = mwb - s_mw[wi][a];
+                            int64_t cst;
+                            if (dw + ms * (ma0b - s_ma0[wi][a]) + ex <= x.cap)
+                                cst = p0b - P[a];
+                            else if (recomp && dw + ms * (ma1b - s_ma1[wi][a]) + ex <= x.cap)
+                                cst = p1b - P[np + a];
+                            else
+                                continue;
+                            if (prune_het && ((x.flags & 1) ? p2b - P[2 * np + a] : 0) + hc_b > eta_tbar) continue;
+                            cst += x.p2p;
+                            if (cst > t) continue;
                             if (STATS) ++relax;
                             const int64_t v = prev + cst;
                             if (v < best || (v == best && (a < ba || (a == ba && w < bwid)))) {
@@ -541,12 +560,19 @@ hipError_t launch_width_tables(const void *d_image, const hapmoe_candidate *d_ca
     return hipGetLastError();
 }
 
-// one workgroup's slice: F of two levels (int64) and the back-trace pointers of
-// every level (int16), [levels][end layer][half-groups used]
+// one workgroup's slice: the back-trace pointers of every level (int16),
+// [levels][end layer][half-groups used]
 int64_t width_dp_slot_bytes(int n_layers, int ppmax)
 {
     const int64_t W = n_layers + 1, UP = 2 * ppmax + 1;
-    return align256(2 * W * UP * 8 + (ppmax + 1) * W * UP * 2);
+    return align256((ppmax + 1) * W * UP * 2);
+}
+
+// LDS of one workgroup beyond its static arrays: F of two levels (int64),
+// [end layer][half-groups used]; at most 2 x 128 x 65 x 8 = 133,120 bytes
+int width_dp_lds_bytes(int n_layers, int ppmax)
+{
+    return 2 * (n_layers + 1) * (2 * ppmax + 1) * 8;
 }
 
 int64_t width_dp_ws_bytes(int n_layers, int ppmax, int64_t n_cand)
@@ -570,13 +596,18 @@ hipError_t launch_width_dp(const void *d_image, const hapmoe_candidate *d_cand, 
     hipLaunchKernelGGL(k_width_reset, dim3(1), dim3(1), 0, s, queue);
     const auto *img = static_cast<const unsigned char *>(d_image);
     const auto *tab = static_cast<const unsigned char *>(d_tables);
-    if (d_stats)
-        hipLaunchKernelGGL(k_width_dp<true>, dim3((unsigned)grid), dim3(kThreads), 0, s, img, d_cand, L, tab, first,
-                           count, slots, slot, d_res, d_types, d_widths, d_stats, queue);
-    else
-        hipLaunchKernelGGL(k_width_dp<false>, dim3((unsigned)grid), dim3(kThreads), 0, s, img, d_cand, L, tab, first,
-                           count, slots, slot, d_res, d_types, d_widths, d_stats, queue);
-    return hipGetLastError();
+    const int lds = width_dp_lds_bytes(n_layers, ppmax);
+    auto go = [&](auto kern) -> hipError_t {
+        if (lds > 65536) {
+            const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+            if (e != hipSuccess) return e;
+        }
+        hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kThreads), lds, s, img, d_cand, L, tab, first, count,
+                           slots, slot, d_res, d_types, d_widths, d_stats, queue);
+        return hipGetLastError();
+    };
+    return d_stats ? go(k_width_dp<true>) : go(k_width_dp<false>);
 }
 
 }  // namespace hapmoe
