@@ -419,7 +419,8 @@ int32_t hapmoe_stage_dp_widths_ws_bytes(const hapmoe_problem *p, int64_t count, 
  * like hapmoe_stage_dp, d_types[32 * (0 .. count)] the device-type set of each
  * stage and d_widths[32 * (0 .. count)] each w_i (0 past PP and for infeasible
  * candidates).  d_stats (may be NULL): passes of the candidate's sweep and its
- * relaxations (columns 2, 3 zero).  The tables must come from
+ * relaxations, counted on the first candidate of the key that shares the sweep
+ * (those with equal min(B, PP) share every pass; columns 2, 3 zero).  The tables must come from
  * hapmoe_eval_cost_tables on the same problem (which adds the width tables).
  * d_ws (hapmoe_stage_dp_widths_ws_bytes for count) is the kernel's: calls that
  * may overlap need their own.  Asynchronous. */

@@ -243,35 +243,54 @@ __global__ __launch_bounds__(kThreads) void k_width_dp(const unsigned char *__re
     __shared__ uint32_t s_prm;
     __shared__ uint8_t s_plen[kMaxStages], s_pw[kMaxStages], s_pmask[kMaxStages];
     __shared__ uint32_t s_relax;
+    // the candidates of the key's current group (equal min(B, PP)): their B index
+    // j and their incumbents, and the next threshold each still needs
+    __shared__ int32_t s_mj[HAPMOE_MAX_MICRO];
+    __shared__ int64_t s_best[HAPMOE_MAX_MICRO], s_bestM[HAPMOE_MAX_MICRO], s_bestF[HAPMOE_MAX_MICRO];
+    __shared__ int64_t s_next[HAPMOE_MAX_MICRO];
+    __shared__ uint32_t s_brm[HAPMOE_MAX_MICRO];
+    __shared__ uint8_t s_blen[HAPMOE_MAX_MICRO][kMaxStages], s_bw[HAPMOE_MAX_MICRO][kMaxStages],
+        s_bmask[HAPMOE_MAX_MICRO][kMaxStages];
+    __shared__ int s_nmem, s_vj;
 
     // F of two levels in LDS; the back-trace pointers in the workgroup's slice
     extern __shared__ __align__(16) unsigned char w_dyn[];
     int64_t *F = reinterpret_cast<int64_t *>(w_dyn);
     int16_t *const ARG = reinterpret_cast<int16_t *>(slots + (int64_t)blockIdx.x * slot_bytes);
+    // the (configuration, ordering) keys holding candidates [first, first + count)
+    const int64_t key_lo = first / H.n_micro, n_keys = (first + count - 1) / H.n_micro - key_lo + 1;
     for (;;) {
         if (tid == 0) ctl.qi = atomicAdd(queue, 1u);
         __syncthreads();
         const int64_t k = ctl.qi;
         __syncthreads();
-        if (k >= count) break;   // every workgroup exits once the queue is drained
-        const int64_t idx = first + k;
-        const hapmoe_candidate c = cand[idx];
-        const int64_t key = idx / H.n_micro, cfg = key / H.n_orders;
+        if (k >= n_keys) break;   // every workgroup exits once the queue is drained
+        const int64_t key = key_lo + k;
+        const int nB = H.n_micro;
+        const hapmoe_candidate c = cand[key * nB];
+        const int64_t cfg = key / H.n_orders;
         const int o = (int)(key - cfg * H.n_orders);
         const int PP = c.pp, U = 2 * PP, UP = U + 1;
-        const int64_t B = c.n_micro;
         const PiInfo *pi = reinterpret_cast<const PiInfo *>(tab + L.off_pi) + cfg;
         const KeyInfo *ki = reinterpret_cast<const KeyInfo *>(tab + L.off_key) + key;
-        hapmoe_dp_result *out = res + k;
-        uint8_t *tout = types_out + k * kMaxStages, *wout = widths_out + k * kMaxStages;
+        // candidate j of the key, when it lies in [first, first + count)
+        auto in_range = [&](int j) {
+            const int64_t idx = key * nB + j;
+            return idx >= first && idx < first + count;
+        };
         if (pi->status != HAPMOE_STATUS_OK) {
-            if (tid == 0) {
-                out->objective = out->stage_sum = out->t_max = kInf;
-                out->status = HAPMOE_STATUS_OVERFLOW;
-                out->recompute_mask = 0;
-                if (STATS) stats[4 * k] = stats[4 * k + 1] = stats[4 * k + 2] = stats[4 * k + 3] = 0;
+            for (int j = 0; j < nB; ++j) {
+                if (!in_range(j)) continue;
+                const int64_t r = key * nB + j - first;
+                hapmoe_dp_result *out = res + r;
+                if (tid == 0) {
+                    out->objective = out->stage_sum = out->t_max = kInf;
+                    out->status = HAPMOE_STATUS_OVERFLOW;
+                    out->recompute_mask = 0;
+                    if (STATS) stats[4 * r] = stats[4 * r + 1] = stats[4 * r + 2] = stats[4 * r + 3] = 0;
+                }
+                if (tid < kMaxStages) out->layers[tid] = types_out[r * kMaxStages + tid] = widths_out[r * kMaxStages + tid] = 0;
             }
-            if (tid < kMaxStages) out->layers[tid] = tout[tid] = wout[tid] = 0;
             __syncthreads();
             continue;
         }
@@ -358,6 +377,7 @@ __global__ __launch_bounds__(kThreads) void k_width_dp(const unsigned char *__re
         const int64_t *wtime = reinterpret_cast<const int64_t *>(tab + L.off_wtime) + cfg * L.n_masks * 3 * 3 * np;
         const int64_t eta_tbar = (int64_t)H.eta_prune * pi->tbar;
         const bool prune_het = H.prune_hetero != 0, recomp = H.allow_recompute != 0;
+        int64_t B = 1;   // the current group's min(B, PP): every stage's stored micro-batches
 
         // cost of stage s on half-groups [u0, u0 + w) and layers [a, b), kNone if
         // pruned; *rf = 1 if it needs recomputation
@@ -366,7 +386,7 @@ __global__ __launch_bounds__(kThreads) void k_width_dp(const unsigned char *__re
             const int n = b - a;
             if (n < x.lo || n > x.hi) return kNone;
             const int wi = w - 1;
-            const int64_t ms = (int64_t)(PP - s) < B ? (int64_t)(PP - s) : B;
+            const int64_t ms = (int64_t)(PP - s) < B ? (int64_t)(PP - s) : B;   // B: the group's min(B, PP)
             const int64_t ex = (s_moe[b] - s_moe[a]) > 0 ? s_x[wi] : 0;
             const int64_t dw = s_mw[wi][b] - s_mw[wi][a];
             const int64_t *P = wtime + ((int64_t)(x.mask - 1) * 3 + wi) * 3 * np;
@@ -483,66 +503,108 @@ __global__ __launch_bounds__(kThreads) void k_width_dp(const unsigned char *__re
             __syncthreads();
         };
 
-        // ---- the descending Pareto sweep ----
-        int64_t best = kInf, bestM = kInf, bestF = kInf;
-        uint32_t brm = 0;
-        uint8_t blen[kMaxStages], bw[kMaxStages], bmask[kMaxStages];
-        int passes = 0;
-        int64_t t = kInf;
-        for (;;) {
-            pass(t);
-            ++passes;
-            const int64_t f = s_pF, m = s_pM;
-            if (f == kNone) break;
-            const int64_t obj = f + (B - 1) * m;
-            if (obj < best || (obj == best && m < bestM)) {
-                best = obj;
-                bestM = m;
-                bestF = f;
-                brm = s_prm;
-                for (int s = 0; s < PP; ++s) {
-                    blen[s] = s_plen[s];
-                    bw[s] = s_pw[s];
-                    bmask[s] = s_pmask[s];
+        // ---- the descending Pareto sweep, one per group of the key's candidates
+        // with equal min(B, PP) (their stored micro-batch counts, hence every DP
+        // pass, are the same); one incumbent per candidate, replaced by a lower
+        // sum + (B-1) max or an equal one with a lower max.  The next threshold is
+        // the largest any member still needs: a member skips only points that
+        // cannot beat its own incumbent, so each gets the result of its own sweep.
+        for (int g = 0; g < nB; ++g) {
+            // group g: the candidates whose min(B, PP) equals that of the g-th B,
+            // taken at its first occurrence
+            if (tid == 0) {
+                const int vg = H.micro[g] < PP ? H.micro[g] : PP;
+                bool firstv = true;
+                for (int j = 0; j < g; ++j) firstv = firstv && (H.micro[j] < PP ? H.micro[j] : PP) != vg;
+                int nm = 0;
+                if (firstv)
+                    for (int j = g; j < nB; ++j)
+                        if ((H.micro[j] < PP ? H.micro[j] : PP) == vg && in_range(j)) s_mj[nm++] = j;
+                s_nmem = nm;
+                s_vj = vg;
+                s_relax = 0;
+            }
+            __syncthreads();
+            const int nmem = s_nmem;
+            B = s_vj;
+            __syncthreads();   // every thread has read them before thread 0 moves on
+            if (nmem == 0) continue;   // uniform
+            for (int m = tid; m < nmem; m += kThreads) {
+                s_best[m] = s_bestM[m] = s_bestF[m] = kInf;
+                s_brm[m] = 0;
+            }
+            int passes = 0;
+            int64_t t = kInf;
+            for (;;) {
+                pass(t);
+                ++passes;
+                const int64_t f = s_pF, mx = s_pM;
+                if (f == kNone) break;
+                for (int m = tid; m < nmem; m += kThreads) {
+                    const int64_t Bm = H.micro[s_mj[m]];
+                    const int64_t obj = f + (Bm - 1) * mx;
+                    if (obj < s_best[m] || (obj == s_best[m] && mx < s_bestM[m])) {
+                        s_best[m] = obj;
+                        s_bestM[m] = mx;
+                        s_bestF[m] = f;
+                        s_brm[m] = s_prm;
+                        for (int q = 0; q < PP; ++q) {
+                            s_blen[m][q] = s_plen[q];
+                            s_bw[m][q] = s_pw[q];
+                            s_bmask[m][q] = s_pmask[q];
+                        }
+                    }
+                    // a lower threshold t' gives a sum >= f: it can win only if
+                    // f + (B-1) t' <= best (equal objectives go to the lower max)
+                    int64_t next = mx - 1;
+                    if (Bm > 1) {
+                        const int64_t lim = floor_div(s_best[m] - f, Bm - 1);
+                        next = lim < next ? lim : next;
+                    } else if (f > s_best[m]) {
+                        next = -1;
+                    }
+                    s_next[m] = next;
+                }
+                __syncthreads();
+                int64_t next = -1;
+                for (int m = 0; m < nmem; ++m) next = s_next[m] > next ? s_next[m] : next;
+                __syncthreads();
+                if (next < 0) break;
+                t = next;
+            }
+            __syncthreads();
+            for (int m = 0; m < nmem; ++m) {
+                const int64_t r = key * nB + s_mj[m] - first;
+                hapmoe_dp_result *out = res + r;
+                uint8_t *tout = types_out + r * kMaxStages, *wout = widths_out + r * kMaxStages;
+                const int64_t best = s_best[m];
+                if (tid == 0) {
+                    if (best == kInf) {
+                        out->objective = out->stage_sum = out->t_max = kInf;
+                        out->status = HAPMOE_STATUS_INFEASIBLE;
+                        out->recompute_mask = 0;
+                    } else {
+                        out->objective = best + ki->dp_const;
+                        out->stage_sum = s_bestF[m];
+                        out->t_max = s_bestM[m];
+                        out->status = HAPMOE_STATUS_OK;
+                        out->recompute_mask = s_brm[m];
+                    }
+                    if (STATS) {   // the shared sweep's relaxations on its first candidate
+                        stats[4 * r] = passes;
+                        stats[4 * r + 1] = m == 0 ? (int32_t)s_relax : 0;
+                        stats[4 * r + 2] = 0;
+                        stats[4 * r + 3] = 0;
+                    }
+                }
+                if (tid < kMaxStages) {
+                    const bool on = best != kInf && tid < PP;
+                    out->layers[tid] = on ? s_blen[m][tid] : 0;
+                    tout[tid] = on ? s_bmask[m][tid] : 0;
+                    wout[tid] = on ? s_bw[m][tid] : 0;
                 }
             }
-            // a lower threshold t' gives a sum >= f: it can win only if
-            // f + (B-1) t' <= best (equal objectives go to the lower max)
-            int64_t next = m - 1;
-            if (B > 1) {
-                const int64_t lim = floor_div(best - f, B - 1);
-                next = lim < next ? lim : next;
-            } else if (f > best) {
-                next = -1;
-            }
-            if (next < 0) break;
-            t = next;
-        }
-        __syncthreads();
-        if (tid == 0) {
-            if (best == kInf) {
-                out->objective = out->stage_sum = out->t_max = kInf;
-                out->status = HAPMOE_STATUS_INFEASIBLE;
-                out->recompute_mask = 0;
-            } else {
-                out->objective = best + ki->dp_const;
-                out->stage_sum = bestF;
-                out->t_max = bestM;
-                out->status = HAPMOE_STATUS_OK;
-                out->recompute_mask = brm;
-            }
-            for (int s = 0; s < kMaxStages; ++s) {
-                const bool on = best != kInf && s < PP;
-                out->layers[s] = on ? blen[s] : 0;
-                tout[s] = on ? bmask[s] : 0;
-                wout[s] = on ? bw[s] : 0;
-            }
-            if (STATS) {
-                stats[4 * k] = passes;
-                stats[4 * k + 1] = (int32_t)s_relax;
-                stats[4 * k + 2] = 0;
-                stats[4 * k + 3] = 0;
-            }
+            __syncthreads();
         }
         __syncthreads();
     }
