@@ -340,8 +340,11 @@ int32_t hapmoe_stage_dp_1f1b(const hapmoe_problem *p, const void *d_image,
  * flags rounded up to 16 bytes), plus 16 bytes of DP state for every (stage, b).
  * Two launches: every candidate with 24 KB of LDS a workgroup, then those whose
  * table did not fit (over 22,784 bytes) with 160 KB; a candidate whose table
- * exceeds 162,048 bytes gets HAPMOE_STATUS_OVERFLOW.  d_stats (may be NULL): thresholds swept and DP
- * relaxations of each candidate (columns 2, 3 zero).  No workspace.  Not for
+ * exceeds 162,048 bytes gets HAPMOE_STATUS_OVERFLOW.  The candidates of a (configuration, ordering) key
+ * with B >= PP + 1 share one sweep (their latencies at a threshold t differ by
+ * (B - B') t); d_stats (may be NULL): thresholds swept for the candidate, and
+ * DP relaxations counted on the first candidate of each shared sweep (columns
+ * 2, 3 zero).  No workspace.  Not for
  * stage_types = 2 or 3 (HAPMOE_E_INVAL); ranges and errors as hapmoe_stage_dp.
  * Asynchronous. */
 int32_t hapmoe_stage_dp_latency(const hapmoe_problem *p, const void *d_image,

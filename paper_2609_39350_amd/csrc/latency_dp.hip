@@ -20,9 +20,11 @@
 // set of (end layer, z) states on optimal paths and at every stage takes the
 // smallest split point through which one continues optimally.
 //
-// Mapping: one wave64 workgroup per candidate (grid-stride); a first launch
-// with 24 KB of LDS a workgroup, a second with 160 KB for the candidates whose
-// tables did not fit.  The candidate's
+// Mapping: one wave64 workgroup per (configuration, ordering) key (grid-stride),
+// lane j holding the key's j-th candidate and its incumbent; the candidates
+// with B >= PP + 1 share one sweep, the others run one each.  A first launch
+// with 24 KB of LDS a workgroup, a second with 160 KB for the keys whose tables
+// did not fit.  The candidate's
 // stage costs -- every (stage, end layer b in the stage's band, split point a
 // in the window) with the memory test of its stored micro-batch count,
 // recomputation and prunings 1 and 3, exactly as the threshold DP prices them
@@ -99,9 +101,9 @@ __device__ inline void lat_write(hapmoe_dp_result *out, int status, int64_t obj,
     for (int s = 0; s < kMaxStages; ++s) out->layers[s] = (uint8_t)(len && s < pp ? len[s] : 0);
 }
 
-// lds_bytes: the workgroup's LDS; retry: process only the candidates the first
-// launch marked kStatusRetry (last: no larger launch follows, so a table that
-// does not fit is HAPMOE_STATUS_OVERFLOW)
+// lds_bytes: the workgroup's LDS; retry: process only the keys whose candidates
+// the first launch marked kStatusRetry (last: no larger launch follows, so a
+// table that does not fit is HAPMOE_STATUS_OVERFLOW)
 template <bool STATS>
 __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, const hapmoe_candidate *cand,
                                                    const unsigned char *tab, TablesLayout L, int64_t first,
@@ -116,28 +118,31 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
     const int lane = threadIdx.x;
     const int N = H.n_layers, nB = H.n_micro;
     const int64_t np = L.np;
+    // the (configuration, ordering) keys holding candidates [first, first + count)
+    const int64_t key_lo = first / nB, n_keys = (first + count - 1) / nB - key_lo + 1;
 
-    for (int64_t i = blockIdx.x; i < count; i += gridDim.x) {
-        const int64_t inst = first + i;
-        const int64_t key = inst / nB, cfg = key / H.n_orders;
-        const int PP = cand[inst].pp;
-        const int64_t B = cand[inst].n_micro;
-        hapmoe_dp_result *out = res + i;
-        if (retry && out->status != kStatusRetry) continue;   // wave-uniform
-        int32_t *st_out = STATS ? stats + 4 * i : nullptr;
+    for (int64_t kq = blockIdx.x; kq < n_keys; kq += gridDim.x) {
+        const int64_t key = key_lo + kq, cfg = key / H.n_orders;
+        const int PP = cand[key * nB].pp;
+        // lane j holds the key's j-th candidate (B = micro[j])
+        const int64_t inst = key * nB + lane;
+        const bool inr = lane < nB && inst >= first && inst < first + count;
+        const int64_t Bj = lane < nB ? H.micro[lane] : 1;
+        hapmoe_dp_result *out = res + (inst - first);   // dereferenced only where inr
+        int32_t *st_out = STATS ? stats + 4 * (inst - first) : nullptr;
+        if (retry && __ballot(inr && out->status == kStatusRetry) == 0) continue;   // wave-uniform
         const PiInfo *pi = reinterpret_cast<const PiInfo *>(tab + L.off_pi) + cfg;
         const KeyInfo *ki = reinterpret_cast<const KeyInfo *>(tab + L.off_key) + key;
         const int64_t *mem = reinterpret_cast<const int64_t *>(tab + L.off_mem) + cfg * 4 * np;
         const int64_t *time = reinterpret_cast<const int64_t *>(tab + L.off_time) + cfg * L.n_masks * 3 * np;
-        auto finish = [&](int status) {   // a result without a partition
-            if (lane == 0) {
+        auto finish_if = [&](bool mine, int status) {   // a result without a partition
+            if (mine) {
                 lat_write(out, status, kInf, kInf, kInf, 0, nullptr, PP);
                 if (STATS) st_out[0] = st_out[1] = st_out[2] = st_out[3] = 0;
             }
-            __syncthreads();
         };
         if (pi->status != HAPMOE_STATUS_OK) {
-            finish(HAPMOE_STATUS_OVERFLOW);
+            finish_if(inr, HAPMOE_STATUS_OVERFLOW);
             continue;
         }
 
@@ -165,7 +170,8 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
         const bool shape = totlo <= N && tothi >= N && !__any(lane < PP && wd == 0);
         __syncthreads();
         if (!shape) {
-            finish(HAPMOE_STATUS_INFEASIBLE);
+            finish_if(inr, HAPMOE_STATUS_INFEASIBLE);
+            __syncthreads();
             continue;
         }
         if (lane == 0) {
@@ -187,56 +193,18 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
         __syncthreads();
         // LDS: cost table [ncost] int64 | DP states [nv][2] int64 | recomputation flags [ncost] u8
         const int need = ncost * 8 + nv * 16 + ((ncost + 15) & ~15);
-        if (need > dyn_bytes) {
-            finish(last ? HAPMOE_STATUS_OVERFLOW : kStatusRetry);
+        if (need > dyn_bytes) {   // the table does not depend on B: the whole key
+            finish_if(inr, last ? HAPMOE_STATUS_OVERFLOW : kStatusRetry);
             continue;
         }
         int64_t *Cst = reinterpret_cast<int64_t *>(dyn);
         int64_t *V = Cst + ncost;
         uint8_t *R = reinterpret_cast<uint8_t *>(V + 2 * nv);
-
-        // ---- every stage cost of the candidate, once ----
         const int64_t X = pi->x_bytes, eta_tbar = (int64_t)H.eta_prune * pi->tbar;
         const bool prune_het = H.prune_hetero != 0, recomp = H.allow_recompute != 0;
-        for (int e = lane; e < ncost; e += 64) {
-            int s = 0;
-            while (s + 1 < PP && D.st[s + 1].coff <= e) ++s;
-            const LatStage S = D.st[s];
-            const int k = (e - S.coff) / S.win, j = (e - S.coff) - k * S.win;
-            const int b = S.blo + k, a = b - S.lo - j;
-            int64_t c = kLBig;
-            uint8_t r = 0;
-            if (a >= S.plo && a <= S.phi && a >= 0) {
-                const int mask = ki->mask[s];
-                int64_t cap = kInf;
-                for (int h = 0; h < H.n_types; ++h)
-                    if ((mask >> h) & 1) cap = H.mem_bytes[h] < cap ? H.mem_bytes[h] : cap;
-                const bool inner = s < PP - 1;
-                const int bp = ki->bpair[s];
-                const int64_t p2p = inner ? pi->p2p[(bp >> 2) * kMaxTypes + (bp & 3)] : 0;
-                const bool bdiff = inner && ((bp >> 2) != (bp & 3));
-                const bool mixed = __popc(mask) > 1;
-                const int64_t *tm = time + (int64_t)(mask - 1) * 3 * np;
-                const int64_t ms = (PP - s) < B ? (PP - s) : B;   // stored micro-batches
-                const int64_t base = mem[b] - mem[a] + ((mem[3 * np + b] - mem[3 * np + a]) > 0 ? X : 0);
-                const int64_t hc = (mixed ? tm[2 * np + b] - tm[2 * np + a] : 0) + (bdiff ? p2p : 0);
-                if (!prune_het || hc <= eta_tbar) {
-                    if (base + ms * (mem[np + b] - mem[np + a]) <= cap) {
-                        c = tm[b] - tm[a] + p2p;
-                    } else if (recomp && base + ms * (mem[2 * np + b] - mem[2 * np + a]) <= cap) {
-                        c = tm[np + b] - tm[np + a] + p2p;
-                        r = 1;
-                    }
-                }
-            }
-            Cst[e] = c;
-            R[e] = r;
-        }
-        __syncthreads();
+        const LatStage SL = D.st[PP - 1];
+        int64_t B = 1;   // the current group's reference B (see below)
 
-        // One pass over the stages.  lat = false: the least stage sum (state z = 0
-        // only); lat = true: the least latency weight with the largest stage
-        // exactly t, states z = 0 / 1.  Returns the relaxations this lane made.
         // One pass over the stages, every (end layer, z) state of a stage on its own
         // lane.  mode 0: the least stage sum (state z = 0 only); 1: the least
         // latency weight with the largest stage exactly t (states z = 0 / 1); 2:
@@ -286,108 +254,183 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
             return nrel;
         };
 
-        pass(0, 0);
-        const LatStage SL = D.st[PP - 1];
-        const int64_t finf = V[2 * (SL.voff + (N - SL.blo))];
-        __syncthreads();
-        if (finf >= kLBig) {
-            finish(HAPMOE_STATUS_INFEASIBLE);
-            continue;
-        }
-        // no partition has a largest stage below t_bot: the sweep starts there
-        // (the passes below it find no path and change nothing)
-        pass(2, 0);
-        const int64_t tbot = V[2 * (SL.voff + (N - SL.blo))];
-        __syncthreads();
-        const int64_t steady_min = B - PP - 1 > 0 ? B - PP - 1 : 0;
-        int64_t best = kLBig, tbest = 0, bsum = 0, tprev = tbot - 1, relax = 0;
-        uint32_t brm = 0;
-        int swept = 0;
-        for (;;) {
-            // the next distinct stage cost above tprev (stage costs are positive)
-            int64_t tn = kLBig;
+        // Groups of the key's candidates that share one sweep: all those with
+        // B >= PP + 1, then each one with B <= PP alone.  With B >= PP + 1 no
+        // stage's steady-state count max(0, B - s - 1) is clamped and every stage
+        // stores PP - s + 1 micro-batches, so the DP at a threshold t differs
+        // between two such B only by (B - B') t on the states past the bottleneck:
+        // the same least-latency paths, latencies shifted by a constant.  One
+        // sweep with the group's smallest B serves them all, each member keeping
+        // its own incumbent and stopping bound; a member's bound says that no
+        // larger threshold can beat its incumbent, so the extra thresholds the
+        // others need change nothing for it.
+        const uint64_t shared = __ballot(inr && Bj >= PP + 1);
+        uint64_t pending = __ballot(inr);
+        while (pending) {
+            const uint64_t grp = (pending & shared) ? (pending & shared)
+                                                    : (uint64_t(1) << (__ffsll((unsigned long long)pending) - 1));
+            pending &= ~grp;
+            const bool member = (grp >> lane) & 1;
+            const int lead = __ffsll((unsigned long long)grp) - 1;
+            B = lat_min(member ? Bj : kLBig);
+            const int64_t dB = Bj - B;
+
+            // ---- every stage cost of the group (stored micro-batches min(PP - s, B)) ----
             for (int e = lane; e < ncost; e += 64) {
-                const int64_t c = Cst[e];
-                if (c > tprev && c < tn) tn = c;
-            }
-            const int64_t t = lat_min(tn);
-            if (t >= kLBig) break;
-            if (finf + ceil3(t) + steady_min * t >= best) break;
-            relax += pass(1, t);
-            ++swept;
-            tprev = t;
-            const int64_t v = V[2 * (SL.voff + (N - SL.blo)) + 1];
-            __syncthreads();
-            if (v >= best) continue;
-            best = v;
-            tbest = t;
-            // back-trace: the smallest split point through which a live state
-            // continues optimally, stage by stage from the last
-            int b = N;
-            bool live0 = false, live1 = true;
-            int64_t sum = 0;
-            uint32_t rmask = 0;
-            for (int s = PP - 1; s >= 0; --s) {
+                int s = 0;
+                while (s + 1 < PP && D.st[s + 1].coff <= e) ++s;
                 const LatStage S = D.st[s];
-                const LatStage P = D.st[s ? s - 1 : 0];
-                const int64_t steady = B - s - 2 > 0 ? B - s - 2 : 0;
-                const int k = b - S.blo;
-                const int64_t tg0 = V[2 * (S.voff + k)], tg1 = V[2 * (S.voff + k) + 1];
-                int64_t amin = kLBig;
-                bool m0 = false, m1 = false;
-                int aj = -1;
-                for (int j = lane; j < S.win; j += 64) {
-                    const int64_t c = Cst[S.coff + k * S.win + j];
-                    if (c >= kLBig) continue;
-                    const int a = b - S.lo - j;
-                    const int64_t v0 = s ? V[2 * (P.voff + a - P.blo)] : (a == 0 ? 0 : kLBig);
-                    const int64_t v1 = s ? V[2 * (P.voff + a - P.blo) + 1] : kLBig;
-                    const bool f0 = v0 < kLBig && ((live0 && c < t && v0 + c + ceil3(c) == tg0) ||
-                                                   (live1 && c == t && v0 + c + ceil3(c) + steady * c == tg1));
-                    const bool f1 = v1 < kLBig && live1 && c <= t && v1 + c == tg1;
-                    if ((f0 || f1) && a < amin) {   // one lane may hold two split points (j, j + 64)
-                        amin = a;
-                        m0 = f0;
-                        m1 = f1;
-                        aj = j;
+                const int k = (e - S.coff) / S.win, j = (e - S.coff) - k * S.win;
+                const int b = S.blo + k, a = b - S.lo - j;
+                int64_t c = kLBig;
+                uint8_t r = 0;
+                if (a >= S.plo && a <= S.phi && a >= 0) {
+                    const int mask = ki->mask[s];
+                    int64_t cap = kInf;
+                    for (int h = 0; h < H.n_types; ++h)
+                        if ((mask >> h) & 1) cap = H.mem_bytes[h] < cap ? H.mem_bytes[h] : cap;
+                    const bool inner = s < PP - 1;
+                    const int bp = ki->bpair[s];
+                    const int64_t p2p = inner ? pi->p2p[(bp >> 2) * kMaxTypes + (bp & 3)] : 0;
+                    const bool bdiff = inner && ((bp >> 2) != (bp & 3));
+                    const bool mixed = __popc(mask) > 1;
+                    const int64_t *tm = time + (int64_t)(mask - 1) * 3 * np;
+                    const int64_t ms = (PP - s) < B ? (PP - s) : B;   // stored micro-batches
+                    const int64_t base = mem[b] - mem[a] + ((mem[3 * np + b] - mem[3 * np + a]) > 0 ? X : 0);
+                    const int64_t hc = (mixed ? tm[2 * np + b] - tm[2 * np + a] : 0) + (bdiff ? p2p : 0);
+                    if (!prune_het || hc <= eta_tbar) {
+                        if (base + ms * (mem[np + b] - mem[np + a]) <= cap) {
+                            c = tm[b] - tm[a] + p2p;
+                        } else if (recomp && base + ms * (mem[2 * np + b] - mem[2 * np + a]) <= cap) {
+                            c = tm[np + b] - tm[np + a] + p2p;
+                            r = 1;
+                        }
                     }
                 }
-                const int64_t na = lat_min(amin);
-                const bool mine = amin == na && na < kLBig;
-                const uint64_t b0 = __ballot(mine && m0), b1 = __ballot(mine && m1);
-                const uint64_t who = __ballot(mine);
-                const int src = who ? __ffsll((unsigned long long)who) - 1 : 0;
-                const int jj = __shfl(aj, src, 64);
-                if (na >= kLBig || jj < 0) {   // cannot happen on an optimal path
-                    live0 = live1 = false;
-                    break;
-                }
-                const int e = S.coff + k * S.win + jj;
-                sum += Cst[e];
-                if (R[e]) rmask |= 1u << s;
-                if (lane == 0) D.len[s] = b - (int)na;
-                b = (int)na;
-                live0 = b0 != 0;
-                live1 = b1 != 0;
+                Cst[e] = c;
+                R[e] = r;
             }
-            bsum = sum;
-            brm = rmask;
+            __syncthreads();
+
+            pass(0, 0);
+            const int64_t finf = V[2 * (SL.voff + (N - SL.blo))];
+            __syncthreads();
+            if (finf >= kLBig) {
+                finish_if(member, HAPMOE_STATUS_INFEASIBLE);
+                __syncthreads();
+                continue;
+            }
+            // no partition has a largest stage below t_bot: the sweep starts there
+            // (the passes below it find no path and change nothing)
+            pass(2, 0);
+            const int64_t tbot = V[2 * (SL.voff + (N - SL.blo))];
+            __syncthreads();
+            const int64_t steady_min = Bj - PP - 1 > 0 ? Bj - PP - 1 : 0;
+            // this lane's incumbent (members only): latency, largest stage, sum,
+            // recomputation mask and the stage lengths, four to a word
+            int64_t best = kLBig, tbest = 0, bsum = 0;
+            uint32_t brm = 0, lw[kMaxStages / 4] = {};
+            int64_t tprev = tbot - 1, relax = 0;
+            int swept = 0;
+            for (;;) {
+                // the next distinct stage cost above tprev (stage costs are positive)
+                int64_t tn = kLBig;
+                for (int e = lane; e < ncost; e += 64) {
+                    const int64_t c = Cst[e];
+                    if (c > tprev && c < tn) tn = c;
+                }
+                const int64_t t = lat_min(tn);
+                if (t >= kLBig) break;
+                if (__ballot(member && finf + ceil3(t) + steady_min * t < best) == 0) break;
+                relax += pass(1, t);
+                ++swept;
+                tprev = t;
+                const int64_t v = V[2 * (SL.voff + (N - SL.blo)) + 1];
+                __syncthreads();
+                const bool gain = member && v < kLBig && v + dB * t < best;
+                if (__ballot(gain) == 0) continue;
+                // back-trace: the smallest split point through which a live state
+                // continues optimally, stage by stage from the last
+                int b = N;
+                bool live0 = false, live1 = true;
+                int64_t sum = 0;
+                uint32_t rmask = 0;
+                for (int s = PP - 1; s >= 0; --s) {
+                    const LatStage S = D.st[s];
+                    const LatStage P = D.st[s ? s - 1 : 0];
+                    const int64_t steady = B - s - 2 > 0 ? B - s - 2 : 0;
+                    const int k = b - S.blo;
+                    const int64_t tg0 = V[2 * (S.voff + k)], tg1 = V[2 * (S.voff + k) + 1];
+                    int64_t amin = kLBig;
+                    bool m0 = false, m1 = false;
+                    int aj = -1;
+                    for (int j = lane; j < S.win; j += 64) {
+                        const int64_t c = Cst[S.coff + k * S.win + j];
+                        if (c >= kLBig) continue;
+                        const int a = b - S.lo - j;
+                        const int64_t v0 = s ? V[2 * (P.voff + a - P.blo)] : (a == 0 ? 0 : kLBig);
+                        const int64_t v1 = s ? V[2 * (P.voff + a - P.blo) + 1] : kLBig;
+                        const bool f0 = v0 < kLBig && ((live0 && c < t && v0 + c + ceil3(c) == tg0) ||
+                                                       (live1 && c == t && v0 + c + ceil3(c) + steady * c == tg1));
+                        const bool f1 = v1 < kLBig && live1 && c <= t && v1 + c == tg1;
+                        if ((f0 || f1) && a < amin) {   // one lane may hold two split points (j, j + 64)
+                            amin = a;
+                            m0 = f0;
+                            m1 = f1;
+                            aj = j;
+                        }
+                    }
+                    const int64_t na = lat_min(amin);
+                    const bool mine = amin == na && na < kLBig;
+                    const uint64_t b0 = __ballot(mine && m0), b1 = __ballot(mine && m1);
+                    const uint64_t who = __ballot(mine);
+                    const int src = who ? __ffsll((unsigned long long)who) - 1 : 0;
+                    const int jj = __shfl(aj, src, 64);
+                    if (na >= kLBig || jj < 0) {   // cannot happen on an optimal path
+                        live0 = live1 = false;
+                        break;
+                    }
+                    const int e = S.coff + k * S.win + jj;
+                    sum += Cst[e];
+                    if (R[e]) rmask |= 1u << s;
+                    if (lane == 0) D.len[s] = b - (int)na;
+                    b = (int)na;
+                    live0 = b0 != 0;
+                    live1 = b1 != 0;
+                }
+                __syncthreads();
+                if (gain) {
+                    best = v + dB * t;
+                    tbest = t;
+                    bsum = sum;
+                    brm = rmask;
+#pragma unroll
+                    for (int w = 0; w < kMaxStages / 4; ++w) {
+                        uint32_t x = 0;
+                        for (int q = 0; q < 4; ++q)
+                            if (4 * w + q < PP) x |= (uint32_t)(uint8_t)D.len[4 * w + q] << (8 * q);
+                        lw[w] = x;
+                    }
+                }
+                __syncthreads();
+            }
+            const int64_t nrel = STATS ? lat_sum(relax) : 0;
+            if (member) {
+                if (best >= kLBig) {
+                    lat_write(out, HAPMOE_STATUS_INFEASIBLE, kInf, kInf, kInf, 0, nullptr, PP);
+                } else {
+                    int32_t len[kMaxStages];
+                    for (int q = 0; q < kMaxStages; ++q) len[q] = (lw[q / 4] >> (8 * (q % 4))) & 0xff;
+                    lat_write(out, HAPMOE_STATUS_OK, best + ki->dp_const, bsum, tbest, brm, len, PP);
+                }
+                if (STATS) {   // the group's thresholds; its relaxations on its first candidate
+                    st_out[0] = best >= kLBig ? 0 : swept;
+                    st_out[1] = best >= kLBig || lane != lead ? 0 : (int32_t)(nrel < INT32_MAX ? nrel : INT32_MAX);
+                    st_out[2] = st_out[3] = 0;
+                }
+            }
             __syncthreads();
         }
-        if (best >= kLBig) {
-            finish(HAPMOE_STATUS_INFEASIBLE);
-            continue;
-        }
-        const int64_t nrel = STATS ? lat_sum(relax) : 0;
-        if (lane == 0) {
-            lat_write(out, HAPMOE_STATUS_OK, best + ki->dp_const, bsum, tbest, brm, D.len, PP);
-            if (STATS) {
-                st_out[0] = swept;
-                st_out[1] = (int32_t)(nrel < INT32_MAX ? nrel : INT32_MAX);
-                st_out[2] = st_out[3] = 0;
-            }
-        }
-        __syncthreads();
     }
 }
 

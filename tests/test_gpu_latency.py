@@ -130,7 +130,10 @@ def test_latency_sub_range_and_stats(torch):
     assert (raw[:first] == 0x5A).all() and (raw[first + count:] == 0x5A).all()
     st = pl.stats()[first:first + count]
     ok = whole[first:first + count]["status"] == 0
-    assert (st[ok, 0] >= 1).all() and (st[~ok, 0] == 0).all() and (st[ok, 1] > 0).all()
+    assert (st[ok, 0] >= 1).all() and (st[~ok, 0] == 0).all() and (st[:, 1] >= 0).all()
+    # relaxations are counted once per shared sweep: on the first candidate of
+    # each (key, group) -- with B in {8, 16, 32} and PP <= 8, B = 16 and 32 share
+    assert st[ok, 1].sum() > 0 and (st[ok, 1] > 0).sum() < ok.sum()
 
 
 def test_latency_lower_bound_of_the_frontier_rescoring(torch):
