@@ -298,7 +298,24 @@ def leg_free_types(torch, binding, workloads, dev, stream, steps, warmup, cpu_sa
                "best_plan": {"config": plan["config"], "order": plan["order"], "B": plan["n_micro"],
                              "stage_types": plan["stage_types"], "layers": plan["layers"]}}
         if mode == 1:
+            # every configuration has the same number of order slots (the largest
+            # arrangement count); a pipeline's own stage-type sequences fill the
+            # first PP! / prod_h k_h! of them, the rest are padding that the cost
+            # tables mark infeasible without DP work
+            from math import factorial
+            counts = [int(x) for x in free["cluster"]["count"]]
+            G = sum(counts)
+            real = 0
+            for pp in pf.cand_host["pp"][::int(binding.tables_layout(free)["n_orders"]) * len(free["space"]["micro"])]:
+                g = G // int(pp)
+                arr = factorial(int(pp))
+                for m in counts:
+                    arr //= factorial(m // g)
+                real += arr * len(free["space"]["micro"])
             rec["sequences_per_config"] = int(binding.tables_layout(free)["n_orders"])
+            rec["real_sequence_candidates"] = real
+            rec["padding_candidates"] = pf.n - real
+            rec["value_real_sequences"] = real * k_steps / elapsed
         if mode == 2:   # the 1F1B re-scoring of the same DP (hapmoe_stage_dp_types_1f1b)
             if k_warm:
                 pf.stage_dp(objective="1f1b")
