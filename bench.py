@@ -149,11 +149,11 @@ def leg_1f1b(torch, pl, stream, steps, warmup):
 
 def leg_latency(torch, binding, workloads, dev, stream, cpu_sample):
     """The least 1F1B latency over every partition (hapmoe_stage_dp_latency) on
-    configurations 2 and 3, whole launches, with the frontier re-scoring's best
-    plan beside it (the exact minimum can only be lower)."""
+    configurations 2, 3 and 4, whole launches, with the frontier re-scoring's
+    best plan beside it (the exact minimum can only be lower)."""
     import numpy as np
     out = {}
-    for n_config in (2, 3):
+    for n_config in (2, 3, 4):   # configuration 4: about 8 s a launch
         p = workloads.config(n_config)
         pl = binding.Planner(p, dev)
         pl.eval_cost_tables()
