@@ -56,7 +56,7 @@ struct LatHead {
     LatStage st[kMaxStages];
     int64_t red[64];         // wave reductions through LDS
     int32_t len[kMaxStages]; // best partition: layers per stage
-    int32_t flag[kMaxStages];
+    int32_t pad[kMaxStages];  // keeps the header at the documented 1,792 bytes
 };
 
 // the stage-cost table may use 160 KB less the header: 162,048 bytes (documented)
