@@ -7,6 +7,7 @@
 // layout queries -- on seeded problems of each stage-type mode, then the bad
 // inputs each must refuse (the device calls included, which must return their
 // error before any HIP call).  Exit status 0 on success.
+#include <cstdint>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
@@ -155,6 +156,24 @@ int run_problem(const hapmoe_problem &p, const char *name)
     if (hapmoe_stage_dp_types(&p, nullptr, nullptr, n, nullptr, 0, 0, n, nullptr, nullptr, nullptr, nullptr, 0,
                               nullptr) == HAPMOE_OK)
         bad |= fail("types null", 0);
+    if (hapmoe_stage_dp_latency(&p, nullptr, nullptr, n, nullptr, 0, 0, n, nullptr, nullptr, nullptr) ==
+        HAPMOE_OK)
+        bad |= fail("latency null", 0);
+    {   // range and table-size checks with stand-in pointers (never dereferenced)
+        void *fake = reinterpret_cast<void *>(uintptr_t(1) << 20);
+        const auto *fc = static_cast<const hapmoe_candidate *>(fake);
+        auto *fr = static_cast<hapmoe_dp_result *>(fake);
+        if (p.space.stage_types < 2) {
+            if (hapmoe_stage_dp_latency(&p, fake, fc, n, fake, tab, n, 1, fr, nullptr, nullptr) != HAPMOE_E_RANGE)
+                bad |= fail("latency range", 0);
+            if (hapmoe_stage_dp_latency(&p, fake, fc, n, fake, tab - 1, 0, 1, fr, nullptr, nullptr) !=
+                HAPMOE_E_WORKSPACE)
+                bad |= fail("latency tables", 0);
+        } else if (hapmoe_stage_dp_latency(&p, fake, fc, n, fake, tab, 0, 1, fr, nullptr, nullptr) !=
+                   HAPMOE_E_INVAL) {
+            bad |= fail("latency mode", 0);
+        }
+    }
     hapmoe_plan plan;
     if (hapmoe_best_plan(&p, nullptr, nullptr, 0, nullptr, nullptr, n, nullptr, nullptr, 0, &plan, nullptr) ==
         HAPMOE_OK)
