@@ -20,6 +20,10 @@
 // set of (end layer, z) states on optimal paths and at every stage takes the
 // smallest split point through which one continues optimally.
 //
+// Thresholds are taken up to kLatSlots at a time and run side by side in one
+// pass (a slot of DP states each), then examined in ascending order with the
+// stop test; a pass past the stop is discarded.
+//
 // Mapping: one wave64 workgroup per (configuration, ordering) key (grid-stride),
 // lane j holding the key's j-th candidate and its incumbent; the candidates
 // with B >= PP + 1 share one sweep, the others run one each.  A first launch
@@ -43,6 +47,7 @@ constexpr int64_t kLBig = int64_t(1) << 62;   // "no path" inside the DP, far fr
 constexpr int kLatLdsSmall = 24 * 1024;
 constexpr int kLatLdsLarge = 160 * 1024;
 constexpr int kLatBlocks = 2048;              // grid-stride launch width
+constexpr int kLatSlots = 8;                  // thresholds a latency pass may run side by side
 constexpr int32_t kStatusRetry = 3;           // between the two launches only: table too big for the first
 
 struct LatStage {
@@ -191,15 +196,23 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
         __syncthreads();
         const int ncost = (int)D.red[0], nv = (int)D.red[1];
         __syncthreads();
-        // LDS: cost table [ncost] int64 | DP states [nv][2] int64 | recomputation flags [ncost] u8
-        const int need = ncost * 8 + nv * 16 + ((ncost + 15) & ~15);
+        // LDS: cost table [ncost] int64 | recomputation flags [ncost] u8 | DP states
+        // [nslot][nv][2] int64, one slot per threshold of a pass (at least one)
+        const int fixed = ncost * 8 + ((ncost + 15) & ~15);
+        const int need = fixed + nv * 16;
         if (need > dyn_bytes) {   // the table does not depend on B: the whole key
             finish_if(inr, last ? HAPMOE_STATUS_OVERFLOW : kStatusRetry);
             continue;
         }
+        // thresholds a latency pass runs side by side, as many as the LDS allows (at
+        // most kLatSlots): a stage's (slot, end layer, z) states are spread over the
+        // lanes together, so narrow bands fill the wave instead of a few lanes
+        int nslot = (dyn_bytes - fixed) / (nv * 16);
+        nslot = nslot < kLatSlots ? nslot : kLatSlots;
+        nslot = nslot > 1 ? nslot : 1;
         int64_t *Cst = reinterpret_cast<int64_t *>(dyn);
-        int64_t *V = Cst + ncost;
-        uint8_t *R = reinterpret_cast<uint8_t *>(V + 2 * nv);
+        uint8_t *R = reinterpret_cast<uint8_t *>(Cst + ncost);
+        int64_t *V = reinterpret_cast<int64_t *>(dyn + fixed);
         const int64_t X = pi->x_bytes, eta_tbar = (int64_t)H.eta_prune * pi->tbar;
         const bool prune_het = H.prune_hetero != 0, recomp = H.allow_recompute != 0;
         const LatStage SL = D.st[PP - 1];
@@ -207,26 +220,31 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
 
         // One pass over the stages, every (end layer, z) state of a stage on its own
         // lane.  mode 0: the least stage sum (state z = 0 only); 1: the least
-        // latency weight with the largest stage exactly t (states z = 0 / 1); 2:
-        // the least possible largest stage (z = 0 only).  Returns the latency
+        // latency weight with the largest stage exactly t (states z = 0 / 1), for
+        // nt thresholds D.red[8 + k] side by side, slot k's states at V + 2 nv k;
+        // 2: the least possible largest stage (z = 0 only).  Returns the latency
         // relaxations this lane made.
-        auto pass = [&](int mode, int64_t t) -> int64_t {
+        auto pass = [&](int mode, int nt) -> int64_t {
             const bool lat = mode == 1;
             int64_t nrel = 0;
             for (int s = 0; s < PP; ++s) {
                 const LatStage S = D.st[s];
                 const LatStage P = D.st[s ? s - 1 : 0];
                 const int64_t steady = B - s - 2 > 0 ? B - s - 2 : 0;   // stage s + 1 (1-based) as bottleneck
-                for (int e = lane; e < 2 * S.wd; e += 64) {
-                    const int k = e >> 1, z = e & 1;
+                const int per = 2 * S.wd;
+                for (int e = lane; e < nt * per; e += 64) {
+                    const int ks = e / per, r = e - ks * per;
+                    const int k = r >> 1, z = r & 1;
                     const int b = S.blo + k;
+                    const int64_t t = lat ? D.red[8 + ks] : 0;
+                    int64_t *Vk = V + 2 * (int64_t)nv * ks;
                     int64_t best = kLBig;
                     if (lat || z == 0) {
                         for (int j = 0; j < S.win; ++j) {
                             const int64_t c = Cst[S.coff + k * S.win + j];
                             if (c >= kLBig) continue;
                             const int a = b - S.lo - j;
-                            const int64_t v0 = s ? V[2 * (P.voff + a - P.blo)] : (a == 0 ? 0 : kLBig);
+                            const int64_t v0 = s ? Vk[2 * (P.voff + a - P.blo)] : (a == 0 ? 0 : kLBig);
                             if (mode == 0) {
                                 if (v0 < kLBig && v0 + c < best) best = v0 + c;
                                 continue;
@@ -240,18 +258,69 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
                             if (z == 0) {
                                 if (v0 < kLBig && c < t && v0 + c + ceil3(c) < best) best = v0 + c + ceil3(c);
                             } else {
-                                const int64_t v1 = s ? V[2 * (P.voff + a - P.blo) + 1] : kLBig;
+                                const int64_t v1 = s ? Vk[2 * (P.voff + a - P.blo) + 1] : kLBig;
                                 if (v0 < kLBig && c == t && v0 + c + ceil3(c) + steady * c < best)
                                     best = v0 + c + ceil3(c) + steady * c;
                                 if (v1 < kLBig && c <= t && v1 + c < best) best = v1 + c;
                             }
                         }
                     }
-                    V[2 * (S.voff + k) + z] = best;
+                    Vk[2 * (S.voff + k) + z] = best;
                 }
                 __syncthreads();
             }
             return nrel;
+        };
+
+        // Back-trace of the latency pass at threshold t with states Vt: the
+        // smallest split point through which a live state continues optimally,
+        // stage by stage from the last (lengths into D.len; sum and recomputation
+        // mask returned).
+        auto trace = [&](const int64_t *Vt, int64_t t, int64_t &sum, uint32_t &rmask) {
+            int b = N;
+            bool live0 = false, live1 = true;
+            sum = 0;
+            rmask = 0;
+            for (int s = PP - 1; s >= 0; --s) {
+                const LatStage S = D.st[s];
+                const LatStage P = D.st[s ? s - 1 : 0];
+                const int64_t steady = B - s - 2 > 0 ? B - s - 2 : 0;
+                const int k = b - S.blo;
+                const int64_t tg0 = Vt[2 * (S.voff + k)], tg1 = Vt[2 * (S.voff + k) + 1];
+                int64_t amin = kLBig;
+                bool m0 = false, m1 = false;
+                int aj = -1;
+                for (int j = lane; j < S.win; j += 64) {
+                    const int64_t c = Cst[S.coff + k * S.win + j];
+                    if (c >= kLBig) continue;
+                    const int a = b - S.lo - j;
+                    const int64_t v0 = s ? Vt[2 * (P.voff + a - P.blo)] : (a == 0 ? 0 : kLBig);
+                    const int64_t v1 = s ? Vt[2 * (P.voff + a - P.blo) + 1] : kLBig;
+                    const bool f0 = v0 < kLBig && ((live0 && c < t && v0 + c + ceil3(c) == tg0) ||
+                                                   (live1 && c == t && v0 + c + ceil3(c) + steady * c == tg1));
+                    const bool f1 = v1 < kLBig && live1 && c <= t && v1 + c == tg1;
+                    if ((f0 || f1) && a < amin) {   // one lane may hold two split points (j, j + 64)
+                        amin = a;
+                        m0 = f0;
+                        m1 = f1;
+                        aj = j;
+                    }
+                }
+                const int64_t na = lat_min(amin);
+                const bool mine = amin == na && na < kLBig;
+                const uint64_t b0 = __ballot(mine && m0), b1 = __ballot(mine && m1);
+                const uint64_t who = __ballot(mine);
+                const int src = who ? __ffsll((unsigned long long)who) - 1 : 0;
+                const int jj = __shfl(aj, src, 64);
+                if (na >= kLBig || jj < 0) break;   // cannot happen on an optimal path
+                const int e = S.coff + k * S.win + jj;
+                sum += Cst[e];
+                if (R[e]) rmask |= 1u << s;
+                if (lane == 0) D.len[s] = b - (int)na;
+                b = (int)na;
+                live0 = b0 != 0;
+                live1 = b1 != 0;
+            }
         };
 
         // Groups of the key's candidates that share one sweep: all those with
@@ -312,7 +381,7 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
             }
             __syncthreads();
 
-            pass(0, 0);
+            pass(0, 1);
             const int64_t finf = V[2 * (SL.voff + (N - SL.blo))];
             __syncthreads();
             if (finf >= kLBig) {
@@ -322,7 +391,7 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
             }
             // no partition has a largest stage below t_bot: the sweep starts there
             // (the passes below it find no path and change nothing)
-            pass(2, 0);
+            pass(2, 1);
             const int64_t tbot = V[2 * (SL.voff + (N - SL.blo))];
             __syncthreads();
             const int64_t steady_min = Bj - PP - 1 > 0 ? Bj - PP - 1 : 0;
@@ -332,87 +401,59 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
             uint32_t brm = 0, lw[kMaxStages / 4] = {};
             int64_t tprev = tbot - 1, relax = 0;
             int swept = 0;
-            for (;;) {
-                // the next distinct stage cost above tprev (stage costs are positive)
-                int64_t tn = kLBig;
-                for (int e = lane; e < ncost; e += 64) {
-                    const int64_t c = Cst[e];
-                    if (c > tprev && c < tn) tn = c;
-                }
-                const int64_t t = lat_min(tn);
-                if (t >= kLBig) break;
-                if (__ballot(member && finf + ceil3(t) + steady_min * t < best) == 0) break;
-                relax += pass(1, t);
-                ++swept;
-                tprev = t;
-                const int64_t v = V[2 * (SL.voff + (N - SL.blo)) + 1];
-                __syncthreads();
-                const bool gain = member && v < kLBig && v + dB * t < best;
-                if (__ballot(gain) == 0) continue;
-                // back-trace: the smallest split point through which a live state
-                // continues optimally, stage by stage from the last
-                int b = N;
-                bool live0 = false, live1 = true;
-                int64_t sum = 0;
-                uint32_t rmask = 0;
-                for (int s = PP - 1; s >= 0; --s) {
-                    const LatStage S = D.st[s];
-                    const LatStage P = D.st[s ? s - 1 : 0];
-                    const int64_t steady = B - s - 2 > 0 ? B - s - 2 : 0;
-                    const int k = b - S.blo;
-                    const int64_t tg0 = V[2 * (S.voff + k)], tg1 = V[2 * (S.voff + k) + 1];
-                    int64_t amin = kLBig;
-                    bool m0 = false, m1 = false;
-                    int aj = -1;
-                    for (int j = lane; j < S.win; j += 64) {
-                        const int64_t c = Cst[S.coff + k * S.win + j];
-                        if (c >= kLBig) continue;
-                        const int a = b - S.lo - j;
-                        const int64_t v0 = s ? V[2 * (P.voff + a - P.blo)] : (a == 0 ? 0 : kLBig);
-                        const int64_t v1 = s ? V[2 * (P.voff + a - P.blo) + 1] : kLBig;
-                        const bool f0 = v0 < kLBig && ((live0 && c < t && v0 + c + ceil3(c) == tg0) ||
-                                                       (live1 && c == t && v0 + c + ceil3(c) + steady * c == tg1));
-                        const bool f1 = v1 < kLBig && live1 && c <= t && v1 + c == tg1;
-                        if ((f0 || f1) && a < amin) {   // one lane may hold two split points (j, j + 64)
-                            amin = a;
-                            m0 = f0;
-                            m1 = f1;
-                            aj = j;
-                        }
+            for (bool more = true; more;) {
+                // the next nslot distinct stage costs above tprev (stage costs are
+                // positive), run side by side; then taken in ascending order, each
+                // with the stop test against the incumbents as they stand there (a
+                // pass past the stop is discarded)
+                int nt = 0;
+                for (int64_t lo_t = tprev; nt < nslot; ++nt) {
+                    int64_t tn = kLBig;
+                    for (int e = lane; e < ncost; e += 64) {
+                        const int64_t c = Cst[e];
+                        if (c > lo_t && c < tn) tn = c;
                     }
-                    const int64_t na = lat_min(amin);
-                    const bool mine = amin == na && na < kLBig;
-                    const uint64_t b0 = __ballot(mine && m0), b1 = __ballot(mine && m1);
-                    const uint64_t who = __ballot(mine);
-                    const int src = who ? __ffsll((unsigned long long)who) - 1 : 0;
-                    const int jj = __shfl(aj, src, 64);
-                    if (na >= kLBig || jj < 0) {   // cannot happen on an optimal path
-                        live0 = live1 = false;
+                    const int64_t t = lat_min(tn);
+                    if (t >= kLBig) break;
+                    if (lane == 0) D.red[8 + nt] = t;
+                    lo_t = t;
+                }
+                __syncthreads();
+                if (nt == 0) break;
+                if (__ballot(member && finf + ceil3(D.red[8]) + steady_min * D.red[8] < best) == 0) break;
+                relax += pass(1, nt);
+                for (int ks = 0; ks < nt; ++ks) {
+                    const int64_t t = D.red[8 + ks];
+                    if (ks > 0 && __ballot(member && finf + ceil3(t) + steady_min * t < best) == 0) {
+                        more = false;
                         break;
                     }
-                    const int e = S.coff + k * S.win + jj;
-                    sum += Cst[e];
-                    if (R[e]) rmask |= 1u << s;
-                    if (lane == 0) D.len[s] = b - (int)na;
-                    b = (int)na;
-                    live0 = b0 != 0;
-                    live1 = b1 != 0;
-                }
-                __syncthreads();
-                if (gain) {
-                    best = v + dB * t;
-                    tbest = t;
-                    bsum = sum;
-                    brm = rmask;
+                    ++swept;
+                    tprev = t;
+                    const int64_t *Vt = V + 2 * (int64_t)nv * ks;
+                    const int64_t v = Vt[2 * (SL.voff + (N - SL.blo)) + 1];
+                    const bool gain = member && v < kLBig && v + dB * t < best;
+                    if (__ballot(gain) == 0) continue;
+                    int64_t sum = 0;
+                    uint32_t rmask = 0;
+                    trace(Vt, t, sum, rmask);
+                    __syncthreads();
+                    if (gain) {
+                        best = v + dB * t;
+                        tbest = t;
+                        bsum = sum;
+                        brm = rmask;
 #pragma unroll
-                    for (int w = 0; w < kMaxStages / 4; ++w) {
-                        uint32_t x = 0;
-                        for (int q = 0; q < 4; ++q)
-                            if (4 * w + q < PP) x |= (uint32_t)(uint8_t)D.len[4 * w + q] << (8 * q);
-                        lw[w] = x;
+                        for (int w = 0; w < kMaxStages / 4; ++w) {
+                            uint32_t x = 0;
+                            for (int q = 0; q < 4; ++q)
+                                if (4 * w + q < PP) x |= (uint32_t)(uint8_t)D.len[4 * w + q] << (8 * q);
+                            lw[w] = x;
+                        }
                     }
+                    __syncthreads();
                 }
-                __syncthreads();
+                __syncthreads();   // the thresholds of the next chunk overwrite D.red
             }
             const int64_t nrel = STATS ? lat_sum(relax) : 0;
             if (member) {
