@@ -338,9 +338,9 @@ int32_t hapmoe_stage_dp_1f1b(const hapmoe_problem *p, const void *d_image,
  * end layer b of the stage's band (the end layers its windows allow) and split
  * point of its window, an 8-byte cost and a 1-byte recomputation flag (the
  * flags rounded up to 16 bytes), plus 16 bytes of DP state for every (stage, b).
- * Two launches: every candidate with 24 KB of LDS a workgroup, then those whose
- * table did not fit (over 22,784 bytes) with 160 KB; a candidate whose table
- * exceeds 162,048 bytes gets HAPMOE_STATUS_OVERFLOW.  The candidates of a (configuration, ordering) key
+ * Launches in tiers of LDS a workgroup: every candidate with 24 KB, then those
+ * whose table did not fit (over 22,784 bytes) with 40, 80 and 160 KB; a
+ * candidate whose table exceeds 162,048 bytes gets HAPMOE_STATUS_OVERFLOW.  The candidates of a (configuration, ordering) key
  * with B >= PP + 1 share one sweep (their latencies at a threshold t differ by
  * (B - B') t); d_stats (may be NULL): thresholds swept for the candidate, and
  * DP relaxations counted on the first candidate of each shared sweep (columns

@@ -27,8 +27,8 @@
 // Mapping: one wave64 workgroup per (configuration, ordering) key (grid-stride),
 // lane j holding the key's j-th candidate and its incumbent; the candidates
 // with B >= PP + 1 share one sweep, the others run one each.  A first launch
-// with 24 KB of LDS a workgroup, a second with 160 KB for the keys whose tables
-// did not fit.  The candidate's
+// with 24 KB of LDS a workgroup, then 40, 80 and 160 KB for the keys whose tables
+// did not fit the previous one (more LDS also holds more threshold slots).  The candidate's
 // stage costs -- every (stage, end layer b in the stage's band, split point a
 // in the window) with the memory test of its stored micro-batch count,
 // recomputation and prunings 1 and 3, exactly as the threshold DP prices them
@@ -42,10 +42,11 @@ namespace hapmoe {
 namespace {
 
 constexpr int64_t kLBig = int64_t(1) << 62;   // "no path" inside the DP, far from overflow
-// Two launches: every candidate with a 24 KB workgroup (six fit a CU), then the
-// candidates whose table did not fit, with 160 KB (one a CU).
-constexpr int kLatLdsSmall = 24 * 1024;
-constexpr int kLatLdsLarge = 160 * 1024;
+// Launches in tiers of LDS a workgroup: every key with 24 KB (six workgroups fit
+// a CU), then the keys whose table did not fit with 40 KB (four), 80 KB (two)
+// and 160 KB (one).
+constexpr int kLatTiers = 4;
+constexpr int kLatLdsTiers[kLatTiers] = {24 * 1024, 40 * 1024, 80 * 1024, 160 * 1024};
 constexpr int kLatBlocks = 2048;              // grid-stride launch width
 constexpr int kLatSlots = 8;                  // thresholds a latency pass may run side by side
 constexpr int32_t kStatusRetry = 3;           // between the two launches only: table too big for the first
@@ -487,12 +488,12 @@ hipError_t launch_latency_dp(const void *d_image, const hapmoe_candidate *d_cand
     const auto *tab = static_cast<const unsigned char *>(d_tables);
     auto go = [&](auto kern) -> hipError_t {
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, kLatLdsLarge);
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, kLatLdsTiers[kLatTiers - 1]);
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(kern, dim3(grid), dim3(64), kLatLdsSmall, stream, img, d_cand, tab, L, first, count,
-                           d_res, d_stats, kLatLdsSmall, 0, 0);
-        hipLaunchKernelGGL(kern, dim3(grid), dim3(64), kLatLdsLarge, stream, img, d_cand, tab, L, first, count,
-                           d_res, d_stats, kLatLdsLarge, 1, 1);
+        for (int tier = 0; tier < kLatTiers; ++tier)
+            hipLaunchKernelGGL(kern, dim3(grid), dim3(64), kLatLdsTiers[tier], stream, img, d_cand, tab, L, first,
+                               count, d_res, d_stats, kLatLdsTiers[tier], tier > 0 ? 1 : 0,
+                               tier == kLatTiers - 1 ? 1 : 0);
         return hipGetLastError();
     };
     return d_stats ? go(k_latency_dp<true>) : go(k_latency_dp<false>);

@@ -168,7 +168,7 @@ def test_latency_lower_bound_of_the_frontier_rescoring(torch):
 
 
 LDS_SMALL_BYTES = 22784    # first launch: 24 KB less the kernel's 1,792-byte header
-LDS_TABLE_BYTES = 162048   # second launch: 160 KB less the header
+LDS_TABLE_BYTES = 162048   # last launch: 160 KB less the header
 
 
 def table_bytes(problem, o):
@@ -193,11 +193,11 @@ def table_bytes(problem, o):
 
 
 def test_latency_oversized_table_reports_overflow(torch):
-    """Tables too big for the first launch's 24 KB workgroups go to the second
-    launch (160 KB) with the same results; a candidate whose table exceeds that
-    too gets HAPMOE_STATUS_OVERFLOW, not a wrong answer.  127 layers, windows
+    """Tables too big for the first launch's 24 KB workgroups go to the later
+    launches (up to 160 KB) with the same results; a candidate whose table
+    exceeds that too gets HAPMOE_STATUS_OVERFLOW, not a wrong answer.  127 layers, windows
     opened to delta = 0.999 and memory that always fits: the one-stage pipelines
-    fit the first launch, the two-stage ones only the second, the four-stage
+    fit the first launch, the two-stage ones only a later one, the four-stage
     ones neither."""
     p = workloads.random_tiny(11, n_layers=127, max_pp=4)
     p["params"]["delta_num"], p["params"]["delta_den"] = 999, 1000
