@@ -22,7 +22,10 @@
 // objective or an equal one with a lower largest stage: the result is the
 // least sum + (B-1) max, the smallest threshold reaching it, and the
 // back-trace there.  B enters through min(B, PP) (memory) and the objective
-// weight: the B values with one min(B, PP) share every pass.
+// weight: the B values with one min(B, PP) share every pass, and so do
+// neighbouring values of min(B, PP) whose feasible split intervals agree at
+// every (stage, type, end layer) -- one sweep per such class, one incumbent
+// per B.
 //
 // Mapping: one 1024-thread workgroup per configuration, pulled from an atomic
 // queue (largest PP first).  States of one level (equal sum u) are
@@ -66,6 +69,7 @@ struct TypeCtl {   // workgroup-uniform scalars set by thread 0
     int32_t start[kMaxStages + 2];
     int32_t wmax[kMaxStages + 2];  // widest end-layer band of a level
     uint32_t relax;
+    int32_t diff;   // a later group's feasible intervals differ from the class's
 };
 
 // one state vector u of a level: u | 6-bit digits u_h | band start | band width
@@ -443,14 +447,6 @@ __global__ __launch_bounds__(kThreads) void k_type_dp(const unsigned char *__res
                 if (vj > v_prev && vj < v) v = vj;
             }
             if (v == 1 << 30) break;
-            v_prev = v;
-            auto member = [&](int j) { return j < nB && (H.micro[j] < PP ? H.micro[j] : PP) == v; };
-            if (tid < nB && member(tid)) {
-                inc[tid].obj = kNone;
-                inc[tid].M = kNone;
-                inc[tid].passes = 0;
-            }
-            if (tid == 0) C.relax = 0;
             // feasible split points of every (stage, type, end layer) for this group:
             // memory only falls as the split point a rises, so they form a suffix of
             // the pruning-1 window; scan it downwards
@@ -473,6 +469,57 @@ __global__ __launch_bounds__(kThreads) void k_type_dp(const unsigned char *__res
                     }
                     bounds[i] = (uint16_t)(amin | (a0 << 8));
                 }
+            __syncthreads();
+            // The next group values join this class while their feasible split
+            // intervals are the same at every (stage, type, end layer): then every
+            // DP pass and back-trace is the same too (memory enters nothing else),
+            // so one sweep serves them all, one incumbent per B.
+            int vmax = v;
+            for (;;) {
+                int v2 = 1 << 30;
+                for (int j = 0; j < nB; ++j) {
+                    const int vj = H.micro[j] < PP ? H.micro[j] : PP;
+                    if (vj > vmax && vj < v2) v2 = vj;
+                }
+                if (v2 == 1 << 30 || !shape_ok) break;   // uniform
+                if (tid == 0) C.diff = 0;
+                __syncthreads();
+                for (int i = tid; i < PP * T * W; i += kThreads) {
+                    const int b = i % W, sh = i / W, h = sh % T, st = sh / T;
+                    const int64_t ms = (PP - st) < v2 ? (PP - st) : v2;
+                    const int64_t cap = H.mem_bytes[h];
+                    int amin = b, a0 = b;
+                    const int top = b - (h == 0 ? lo[0] : h == 1 ? lo[1] : h == 2 ? lo[2] : lo[3]);
+                    const int bot = b - (h == 0 ? hi[0] : h == 1 ? hi[1] : h == 2 ? hi[2] : hi[3]);
+                    for (int a = top; a >= 0 && a >= bot; --a) {
+                        const int64_t dw = sMW[b] - sMW[a];
+                        const int64_t ex = (sMOE[b] - sMOE[a]) > 0 ? X : 0;
+                        const bool fit0 = dw + ms * (sMA0[b] - sMA0[a]) + ex <= cap;
+                        const bool fit1 = recomp && dw + ms * (sMA1[b] - sMA1[a]) + ex <= cap;
+                        if (!(fit0 || fit1)) break;
+                        amin = a;
+                        if (fit0) a0 = a;
+                    }
+                    if (bounds[i] != (uint16_t)(amin | (a0 << 8))) C.diff = 1;
+                }
+                __syncthreads();
+                const int differ = C.diff;
+                __syncthreads();
+                if (differ) break;
+                vmax = v2;
+            }
+            v_prev = vmax;
+            auto member = [&](int j) {
+                if (j >= nB) return false;
+                const int vj = H.micro[j] < PP ? H.micro[j] : PP;
+                return vj >= v && vj <= vmax;
+            };
+            if (tid < nB && member(tid)) {
+                inc[tid].obj = kNone;
+                inc[tid].M = kNone;
+                inc[tid].passes = 0;
+            }
+            if (tid == 0) C.relax = 0;
             __syncthreads();
             int passes = 0;
             if (shape_ok && !EXACT) {
