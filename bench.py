@@ -279,7 +279,7 @@ def leg_free_types(torch, binding, workloads, dev, stream, steps, warmup, cpu_sa
         pf.eval_cost_tables()
         pf.stage_dp(stats=True)
         st = pf.stats()
-        # the 96-layer count DP runs about 11 s a launch: one timed launch after
+        # the 96-layer count DP runs about 2.4 s a launch: one timed launch after
         # the statistics launch (which also warms it)
         k_steps, k_warm = (1, 0) if n_config == 4 and mode == 2 else (steps, warmup)
         plan, elapsed, dp_ms = _timed_steps(torch, pf, stream, k_steps, k_warm)
