@@ -11,6 +11,9 @@ Contents (each an index array and a uint32 digest array, tests/parity_digest.py)
   cfg3_latency, cfg5_latency   the least 1F1B latency, every 97th candidate
   cfg4_latency     the least 1F1B latency, one candidate of every 6th
                    configuration (ordering and B rotating)
+  cfg4_types       device-count DP, eight candidates of 8-stage and four of
+                   4-stage pipelines (written with "types4" as a further
+                   argument, merged into the existing file)
 With "latency" as a further argument only the least-latency entries are
 (re)computed and merged into the existing file.
 """
@@ -33,8 +36,8 @@ OUT = os.path.join(os.path.dirname(os.path.abspath(__file__)), "parity_refs.npz"
 
 
 def _problem(name):
-    if name == "cfg3_types":
-        p = copy.deepcopy(workloads.config(3))
+    if name in ("cfg3_types", "cfg4_types"):
+        p = copy.deepcopy(workloads.config(int(name[3])))
         p["space"]["stage_types"] = 2
         return p
     return workloads.config(int(name[3]))
@@ -44,7 +47,7 @@ def _work(args):
     name, mode, idx = args
     o = orc.Oracle(_problem(name))
     res = {"threshold": o.solve_many, "1f1b": o.solve_exact_many, "latency": o.solve_latency_many}[mode](idx)
-    return parity_digest.of_oracle(res, with_types=name == "cfg3_types")
+    return parity_digest.of_oracle(res, with_types=name in ("cfg3_types", "cfg4_types"))
 
 
 def run(pool, name, mode, idx, chunk):
@@ -73,6 +76,35 @@ def types16_samples():
     return np.array(idx[:: max(1, len(idx) // 16)][:16])
 
 
+def types4_samples():
+    """Device-count DP on the 96-layer workload: eight candidates of 8-stage and
+    four of 4-stage pipelines, B rotating, from configurations where the
+    oracle's block-ordering DP (stage types fixed) finds a feasible partition, so
+    that the device-count DP has one too (the oracle's ascending sweep over every
+    distinct stage cost takes minutes a candidate at 8 stages and hours at 16
+    or 32)."""
+    p = _problem("cfg4_types")
+    o = orc.Oracle(p)
+    base = orc.Oracle(workloads.config(4))
+    nB = len(p["space"]["micro"])
+    per = o.n_orders() * nB
+    per_base = base.n_orders() * nB
+    out = []
+    for pp, n in ((4, 4), (8, 8)):
+        cfgs = [k for k, c in enumerate(o.configs()) if c[0] == pp]
+        where = {c: i for i, c in enumerate(base.configs())}
+        picked = 0
+        for k in cfgs[::7]:
+            j = (k * 13 + 7 * pp) % nB
+            if base.solve(where[o.configs()[k]] * per_base + j)["status"] != 0:   # ordering 0, same B
+                continue
+            out.append(k * per + j)
+            picked += 1
+            if picked == n:
+                break
+    return np.array(out)
+
+
 def latency_samples():
     """Stride samples for the least-latency references (its oracle takes 20 ms to
     1 s a candidate on these workloads)."""
@@ -87,13 +119,22 @@ def latency_samples():
 
 
 def main():
-    args = [a for a in sys.argv[1:] if a != "latency"]
+    args = [a for a in sys.argv[1:] if a not in ("latency", "types4")]
     workers = int(args[0]) if args else (os.cpu_count() or 1)
     only_latency = "latency" in sys.argv[1:]
+    only_types4 = "types4" in sys.argv[1:]
     out = {}
-    if only_latency:
+    if only_latency or only_types4:
         with np.load(OUT) as f:
             out = {k: f[k] for k in f.files}
+    if only_types4:
+        t4 = types4_samples()
+        with get_context("spawn").Pool(workers) as pool:
+            out["cfg4_types_idx"] = t4
+            out["cfg4_types"] = run(pool, "cfg4_types", "threshold", t4, 1)
+        np.savez_compressed(OUT, **out)
+        print("wrote", OUT, os.path.getsize(OUT), "bytes")
+        return
     lat = latency_samples()
     with get_context("spawn").Pool(workers) as pool:
         for n, chunk in ((3, 40), (5, 40), (4, 4)):

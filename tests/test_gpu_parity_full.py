@@ -6,7 +6,8 @@ the oracle's results, written by tests/golden/make_parity_refs.py from oracle/
 alone: configurations 3 and 5 in full under both objectives, configuration 4
 with one candidate of every (configuration, ordering) key (B rotating over
 1..64) and one of every configuration under the 1F1B re-scoring, and 16
-sixteen-stage candidates of configuration 3 under the device-count DP, and
+sixteen-stage candidates of configuration 3 and twelve 4- and 8-stage ones of
+configuration 4 under the device-count DP, and
 stride samples of configurations 3, 4 and 5 under the least 1F1B latency.  A digest
 covers status, objective, stage sum, largest stage, recomputation mask, stage
 lengths (and stage types); a mismatch is re-checked against the oracle itself
@@ -117,3 +118,22 @@ def test_least_latency_samples(torch, refs, n):
     res = pl.results()
     assert _check(p, res, refs, f"cfg{n}_latency", "latency") == len(idx)
     assert (res["status"][idx] == 0).sum() > 10
+
+
+def test_device_count_dp_config4_samples(torch, refs):
+    """The device-count DP on the 96-layer workload (96,128 candidates, pipelines
+    up to 32 stages, one launch): twelve 4- and 8-stage candidates against the
+    stored oracle results, stage types included (the oracle's sweep takes hours
+    a candidate at 16 or 32 stages; those are checked by the properties of
+    tests/test_gpu_free_types.py)."""
+    p = copy.deepcopy(workloads.config(4))
+    p["space"]["stage_types"] = 2
+    print("config 4, device-count DP: 4- and 8-stage samples", flush=True)
+    pl = binding.Planner(p, "cuda:0")
+    pl.run()
+    res, types = pl.results(), pl.stage_types()
+    idx = refs["cfg4_types_idx"]
+    assert set(pl.cand_host["pp"][idx]) == {4, 8} and len(idx) == 12
+    got = parity_digest.of_gpu(res, idx, types)
+    assert np.array_equal(got, refs["cfg4_types"]), np.nonzero(got != refs["cfg4_types"])[0]
+    assert (res["status"][idx] == 0).sum() >= 6
