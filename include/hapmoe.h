@@ -398,7 +398,7 @@ int32_t hapmoe_stage_dp_types_1f1b(const hapmoe_problem *p, const void *d_image,
 
 /* Workspace of hapmoe_stage_dp_widths for a launch over `count` candidates: the
  * work-queue counter and one slice of back-trace pointers per workgroup (at
- * most 512; the DP values themselves live in the workgroup's LDS).
+ * most 1024; the DP values themselves live in the workgroup's LDS).
  * HAPMOE_E_INVAL unless stage_types = 3. */
 int32_t hapmoe_stage_dp_widths_ws_bytes(const hapmoe_problem *p, int64_t count, int64_t *bytes);
 

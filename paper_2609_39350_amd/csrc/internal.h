@@ -170,7 +170,7 @@ hipError_t launch_type_dp(const void *d_image, const hapmoe_candidate *d_cand, i
 // Per-stage data-parallel widths (stage_types = 3): the width tables (run after
 // the cost tables on the same stream) and the DP over (stage, end layer,
 // half-groups used).
-constexpr int64_t kWidthDpMaxSlots = 512;   // workgroups with a state slice each
+constexpr int64_t kWidthDpMaxSlots = 1024;   // workgroups with a state slice each
 hipError_t launch_width_tables(const void *d_image, const hapmoe_candidate *d_cand, int64_t per_config,
                                const TablesLayout &L, int64_t cfg_lo, int64_t n_cfg, void *d_tables, hipStream_t s);
 int64_t width_dp_slot_bytes(int n_layers, int ppmax);
