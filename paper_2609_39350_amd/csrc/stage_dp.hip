@@ -310,15 +310,12 @@ __device__ inline uint64_t step_bit(int m, int mtop)
 // Entry e of a stage's (segment, end layer) list: segment q = e / wd and
 // k = e % wd, as q = (e * ceil(2^16 / wd)) >> 16.  For 1 <= wd <= 128 this is
 // the exact floor for every e < 4 wd + 64 (checked exhaustively), which covers
-// the entries of up to four segments plus the lanes past the last one.
-struct DivMulTable {
-    uint32_t m[129];
-    constexpr DivMulTable() : m()
-    {
-        for (int d = 1; d <= 128; ++d) m[d] = (65536u + (uint32_t)d - 1u) / (uint32_t)d;
-    }
-};
-__constant__ DivMulTable kDivMul = DivMulTable();
+// the entries of up to four segments plus the lanes past the last one.  The
+// multiplier of each stage is computed once a key, in the stage's lane.
+__device__ inline uint32_t split_mul(int wd)
+{
+    return wd > 0 ? (65536u + (uint32_t)wd - 1u) / (uint32_t)wd : 0u;
+}
 
 __device__ inline void split_entry(int e, int wd, uint32_t mul, int &q, int &k)
 {
@@ -326,19 +323,22 @@ __device__ inline void split_entry(int e, int wd, uint32_t mul, int &q, int &k)
     k = e - q * wd;
 }
 
-// Per-segment values held in registers, selected / updated without dynamic
-// register indexing.
-// floor(x / d) for x >= 0, d > 0: below 2^52 through the correctly rounded
-// double quotient, whose truncation is the floor or one more than it
-__device__ inline int64_t div_nonneg(int64_t x, int64_t d)
+// floor(x / d) for x >= 0 and d >= 1, with rd = 1 / d rounded to double: below
+// 2^52 through the double product x * rd, whose truncation is within one of the
+// floor (d = 1: exact; d >= 2: the two roundings leave an error below x / d *
+// 2^-52 < 1/2), corrected by one integer step either way
+__device__ inline int64_t div_recip(int64_t x, int64_t d, double rd)
 {
     if (x < (int64_t(1) << 52)) {
-        const int64_t q = (int64_t)((double)x / (double)d);
-        return q * d > x ? q - 1 : q;
+        const int64_t q = (int64_t)((double)x * rd);
+        const int64_t r = x - q * d;
+        return r < 0 ? q - 1 : (r >= d ? q + 1 : q);
     }
     return x / d;
 }
 
+// Per-segment values held in registers, selected / updated without dynamic
+// register indexing.
 __device__ inline int sel4(const int (&v)[4], int q)
 {
     return q == 0 ? v[0] : q == 1 ? v[1] : q == 2 ? v[2] : v[3];
@@ -529,6 +529,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
         // woff | wd << 16 (woff <= 32 * 128, wd <= 128)
         const int pk1 = (blo & 0xff) | ((bhi & 0xff) << 8) | ((lo & 0xff) << 16) | (slot << 24);
         const int pk2 = woff | (wd << 16);
+        const int pkm = (int)split_mul(wd);   // the entry split's multiplier
         // and hi | mask << 8 | mixed << 16 | bdiff << 17, for the stage-flattened scans
         const int pk3 = (hi & 0xff) | (mask << 8) | (mixed << 16) | (bdiff << 17);
         // The classification and feasibility scans spread the (stage, end layer)
@@ -880,7 +881,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                     // stage, and a wave-uniform split-point loop: a lane with less to
                     // do runs masked (clamped, in-range loads; predicated stores only)
                     const int total = nq * wd_s;
-                    const uint32_t mul_wd = kDivMul.m[wd_s];   // wd_s <= N - PP + 1 <= 127
+                    const uint32_t mul_wd = (uint32_t)rl32(pkm, s);
                     for (int e0 = 0; e0 < total; e0 += 64) {
                         const int e = e0 + lane;
                         const bool act = e < total;
@@ -888,9 +889,10 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                         if (nq > 1) split_entry(k, wd_s, mul_wd, qi, k);   // wave-uniform branch
                         const int q = (qmap >> (2 * qi)) & 3;
                         const int64_t t = CTL[q].t;
-                        const uint8_t *const AMq = REG + ((cmap >> (2 * q)) & 3) * arr_bytes;   // class
-                        uint8_t *const ARq = REG + q * arr_bytes + 2 * sumwd;                   // slot
-                        unsigned char *const RWq = REG + off_rows + q * row_bytes;
+                        // (24-bit products: full-rate multiplies; every region offset is far below 2^24)
+                        const uint8_t *const AMq = REG + __umul24((cmap >> (2 * q)) & 3, arr_bytes);   // class
+                        uint8_t *const ARq = REG + __umul24(q, arr_bytes) + 2 * sumwd;                   // slot
+                        unsigned char *const RWq = REG + off_rows + __umul24(q, row_bytes);
                         const int64_t *Fp = reinterpret_cast<const int64_t *>(RWq + poff);
                         int64_t *Fc = reinterpret_cast<int64_t *>(RWq + coff);
                         const I64x2 *Gp = reinterpret_cast<const I64x2 *>(RWq + poff);
@@ -1130,6 +1132,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
             uint32_t pw[8] = {0, 0, 0, 0, 0, 0, 0, 0};
             uint32_t prm = 0, pok = 0;
             const int64_t Bm = (int64_t)Bj - 1;
+            const double rBm = Bm > 0 ? 1.0 / (double)Bm : 0.0;   // for the sweep bound below
             // offer the segment's last pass: a lower objective wins, and on equal
             // objectives the lower largest stage (the least threshold reaching the
             // optimum), whatever order the passes ran in; equal (objective, M)
@@ -1328,7 +1331,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                 const int64_t cF = CTL[slot].cF, ct = CTL[slot].ct;
                 if (!sweeping || done || cF + Bm * tbot > bs) return -1;
                 if (Bm == 0 || cF + Bm * ct <= bs) return ct;   // ct binds: no division
-                const int64_t lim = div_nonneg(bs - cF, Bm);
+                const int64_t lim = div_recip(bs - cF, Bm, rBm);
                 return lim < ct ? lim : ct;
             };
             // the chains' passes: offer them, and move the chains on

@@ -19,3 +19,29 @@ def test_ceil_third_matches_definition():
     """ceil(c / 3) as (c + 2) // 3 for the non-negative stage costs."""
     for c in list(range(0, 1000)) + [10**12 + k for k in range(6)]:
         assert (c + 2) // 3 == -(-c // 3)
+
+
+def test_reciprocal_floor_division_is_exact():
+    """The stage DP's sweep bound floor(x / d), d = B - 1 in 1..63, taken as the
+    truncated double product x * RN(1 / d) corrected by one integer step either
+    way, equals the floor for x below 2^52 (IEEE double products on both sides:
+    numpy's float64 multiply rounds to nearest like the GPU's)."""
+    import numpy as np
+
+    rng = np.random.default_rng(7)
+    xs = np.concatenate([
+        np.arange(0, 4096, dtype=np.int64),
+        rng.integers(0, 1 << 52, size=200_000, dtype=np.int64),
+        (1 << 52) - 1 - np.arange(0, 4096, dtype=np.int64),
+    ])
+    for d in range(1, 64):
+        rd = np.float64(1.0) / np.float64(d)
+        # near-multiples of d, where a truncation error would show first
+        k = rng.integers(0, ((1 << 52) - 1) // d, size=20_000, dtype=np.int64)
+        x = np.concatenate([xs, k * d, k * d - 1, k * d + d - 1])
+        x = x[(x >= 0) & (x < (1 << 52))]
+        q = (x.astype(np.float64) * rd).astype(np.int64)
+        r = x - q * d
+        assert np.all(np.abs(q - x // d) <= 1), d
+        q = np.where(r < 0, q - 1, np.where(r >= d, q + 1, q))
+        assert np.array_equal(q, x // d), d
