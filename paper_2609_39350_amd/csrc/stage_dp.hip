@@ -975,16 +975,20 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                     for (int w = 0; w < 8; ++w) CTL[sg].bt[w] = 0;
                 }
                 if (PP >= kParallelTrace) {
-                    // Deep pipelines: lane 0 of each segment only follows the chain of
+                    // Deep pipelines: the lanes of each segment only follow the chain of
                     // split points (one byte load a stage) into CTL.sb; then every
                     // (segment, stage) entry recomputes its stage cost on its own lane
                     // and the segment's largest stage, recomputation mask and layer
                     // counts are combined with LDS atomics.  Same results as the
                     // stage-by-stage trace below.
                     {
+                        // Every lane of a segment follows the segment's chain (with the
+                        // same values), so the loop holds no branch and no store: lane ll
+                        // keeps stage ll's split point and stage ll + W's (PP <= 2 W),
+                        // stored once the chain is done -- one LDS round trip a stage.
                         uint8_t *const sbb = reinterpret_cast<uint8_t *>(CTL[segi].sb);
-                        bool ok = tracer && fin < kBig;
-                        int b = N;
+                        bool ok = on && fin < kBig;
+                        int b = N, sv0 = 0, sv1 = 0;
                         for (int s = PP - 1; s >= 0; --s) {   // wave-uniform; clamped, in-range indices
                             const int q1 = rl32(pk1, s), q2 = rl32(pk2, s);
                             const int wdn = q2 >> 16;
@@ -992,10 +996,15 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                             k = k < 0 ? 0 : (k >= wdn ? wdn - 1 : k);
                             const int a = ARG[(q2 & 0xffff) + k];
                             ok = ok && a < b;
-                            if (tracer) sbb[s] = (uint8_t)a;
+                            sv0 = s == ll ? a : sv0;
+                            sv1 = s == ll + W ? a : sv1;
                             b = ok ? a : b;
                         }
                         ok = ok && b == 0;
+                        if (on) {
+                            if (ll < PP) sbb[ll] = (uint8_t)sv0;
+                            if (ll + W < PP) sbb[ll + W] = (uint8_t)sv1;
+                        }
                         if (tracer) {
                             CTL[sg].ok = ok ? 1u : 0u;
                             CTL[sg].M = 0;
