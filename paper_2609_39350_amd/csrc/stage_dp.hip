@@ -859,10 +859,13 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
                         FM1[0] = 0;
                 }
                 // the running segments, in order (wave-uniform)
-                int nq = 0, qmap = 0;
+                // (all four flags are read at once -- one LDS round trip -- and masked)
+                int nq = 0, qmap = 0, onq[kMaxSeg];
+#pragma unroll
+                for (int q = 0; q < kMaxSeg; ++q) onq[q] = CTL[q].on;
 #pragma unroll
                 for (int q = 0; q < kMaxSeg; ++q) {
-                    const int o = q < nseg ? __builtin_amdgcn_readfirstlane(CTL[q].on) : 0;
+                    const int o = __builtin_amdgcn_readfirstlane(onq[q]) & -(int)(q < nseg);
                     if (o) {
                         qmap |= q << (2 * nq);
                         ++nq;
