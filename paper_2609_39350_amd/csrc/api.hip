@@ -534,8 +534,8 @@ int32_t hapmoe_stage_dp_latency(const hapmoe_problem *p, const void *d_image, co
                                          p->model.n_layers);
     if (tables_bytes < L.total) return HAPMOE_E_WORKSPACE;
     if (const int e = check_arch()) return e;
-    if (launch_latency_dp(d_image, d_cand, L, d_tables, first, count, d_res, d_stats, (hipStream_t)stream) !=
-        hipSuccess)
+    if (launch_latency_dp(d_image, d_cand, p->space.n_micro, L, d_tables, first, count, d_res, d_stats,
+                          (hipStream_t)stream) != hipSuccess)
         return HAPMOE_E_HIP;
     return HAPMOE_OK;
 }

@@ -136,9 +136,9 @@ hipError_t launch_stage_dp(const void *d_image, const hapmoe_candidate *d_cand, 
                            bool exact, hipStream_t s);
 int64_t stage_dp_ws_bytes();
 // the least 1F1B latency over every partition: one workgroup per candidate
-hipError_t launch_latency_dp(const void *d_image, const hapmoe_candidate *d_cand, const TablesLayout &L,
-                             const void *d_tables, int64_t first, int64_t count, hapmoe_dp_result *d_res,
-                             int32_t *d_stats, hipStream_t stream);
+hipError_t launch_latency_dp(const void *d_image, const hapmoe_candidate *d_cand, int n_micro,
+                             const TablesLayout &L, const void *d_tables, int64_t first, int64_t count,
+                             hapmoe_dp_result *d_res, int32_t *d_stats, hipStream_t stream);
 // section clocks of the stage-DP kernel (libraries built with HAPMOE_SECTION_CLOCKS)
 enum {
     kClockSetup, kClockScan, kClockRelax, kClockTrace, kClockControl, kClockTotal,

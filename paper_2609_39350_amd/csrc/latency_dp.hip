@@ -24,7 +24,7 @@
 // pass (a slot of DP states each), then examined in ascending order with the
 // stop test; a pass past the stop is discarded.
 //
-// Mapping: one wave64 workgroup per (configuration, ordering) key (grid-stride),
+// Mapping: one wave64 workgroup per (configuration, ordering) key, deepest first,
 // lane j holding the key's j-th candidate and its incumbent; the candidates
 // with B >= PP + 1 share one sweep, the others run one each.  A first launch
 // with 24 KB of LDS a workgroup, then 40, 80 and 160 KB for the keys whose tables
@@ -47,7 +47,7 @@ constexpr int64_t kLBig = int64_t(1) << 62;   // "no path" inside the DP, far fr
 // and 160 KB (one).
 constexpr int kLatTiers = 4;
 constexpr int kLatLdsTiers[kLatTiers] = {24 * 1024, 40 * 1024, 80 * 1024, 160 * 1024};
-constexpr int kLatBlocks = 2048;              // grid-stride launch width
+constexpr int64_t kLatMaxGrid = int64_t(1) << 30;   // workgroups a launch (keys beyond: grid-stride)
 constexpr int kLatSlots = 8;                  // thresholds a latency pass may run side by side
 constexpr int32_t kStatusRetry = 3;           // between the two launches only: table too big for the first
 
@@ -128,7 +128,8 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
     const int64_t key_lo = first / nB, n_keys = (first + count - 1) / nB - key_lo + 1;
 
     for (int64_t kq = blockIdx.x; kq < n_keys; kq += gridDim.x) {
-        const int64_t key = key_lo + kq, cfg = key / H.n_orders;
+        // keys are PP-ascending: the deepest pipelines (the most work) go first
+        const int64_t key = key_lo + n_keys - 1 - kq, cfg = key / H.n_orders;
         const int PP = cand[key * nB].pp;
         // lane j holds the key's j-th candidate (B = micro[j])
         const int64_t inst = key * nB + lane;
@@ -478,22 +479,26 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
 
 }  // namespace
 
-hipError_t launch_latency_dp(const void *d_image, const hapmoe_candidate *d_cand, const TablesLayout &L,
-                             const void *d_tables, int64_t first, int64_t count, hapmoe_dp_result *d_res,
-                             int32_t *d_stats, hipStream_t stream)
+hipError_t launch_latency_dp(const void *d_image, const hapmoe_candidate *d_cand, int n_micro,
+                             const TablesLayout &L, const void *d_tables, int64_t first, int64_t count,
+                             hapmoe_dp_result *d_res, int32_t *d_stats, hipStream_t stream)
 {
     if (count == 0) return hipSuccess;
-    const int grid = (int)(count < kLatBlocks ? count : kLatBlocks);
+    const int64_t n_keys = (first + count - 1) / n_micro - first / n_micro + 1;
     const auto *img = static_cast<const unsigned char *>(d_image);
     const auto *tab = static_cast<const unsigned char *>(d_tables);
     auto go = [&](auto kern) -> hipError_t {
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, kLatLdsTiers[kLatTiers - 1]);
         if (e != hipSuccess) return e;
-        for (int tier = 0; tier < kLatTiers; ++tier)
-            hipLaunchKernelGGL(kern, dim3(grid), dim3(64), kLatLdsTiers[tier], stream, img, d_cand, tab, L, first,
-                               count, d_res, d_stats, kLatLdsTiers[tier], tier > 0 ? 1 : 0,
+        for (int tier = 0; tier < kLatTiers; ++tier) {
+            // one workgroup a key: the dispatcher hands the next key to whichever
+            // CU slot frees first, which balances keys of very different work
+            const int64_t grid = n_keys < kLatMaxGrid ? n_keys : kLatMaxGrid;
+            hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(64), kLatLdsTiers[tier], stream, img, d_cand, tab, L,
+                               first, count, d_res, d_stats, kLatLdsTiers[tier], tier > 0 ? 1 : 0,
                                tier == kLatTiers - 1 ? 1 : 0);
+        }
         return hipGetLastError();
     };
     return d_stats ? go(k_latency_dp<true>) : go(k_latency_dp<false>);
