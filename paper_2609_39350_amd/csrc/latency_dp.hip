@@ -70,6 +70,15 @@ static_assert(sizeof(LatHead) == 1792, "LDS header size is part of the documente
 
 __device__ inline int64_t ceil3(int64_t c) { return (c + 2) / 3; }
 
+// The cost table holds each stage cost c as w = c + ceil(c / 3), the weight of a
+// stage before the bottleneck (kLBig: no such stage).  w is strictly increasing
+// in c, so comparisons with a threshold t can be made as w against t +
+// ceil(t / 3), and c comes back without a division: c = 3m, 3m + 1, 3m + 2 give
+// w = 4m, 4m + 2, 4m + 3, so c = 3 (w >> 2) + ((w & 3) + 1) / 2.  (Stage costs
+// stay below 2^60, so w stays below kLBig.)
+__device__ inline int64_t cost_weight(int64_t c) { return c >= kLBig ? kLBig : c + ceil3(c); }
+__device__ inline int64_t weight_cost(int64_t w) { return 3 * (w >> 2) + (((w & 3) + 1) >> 1); }
+
 __device__ inline int64_t shfl_xor64(int64_t v, int d)
 {
     const int lo = __shfl_xor((int)(uint32_t)(uint64_t)v, d, 64);
@@ -207,7 +216,7 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
             continue;
         }
         // thresholds a latency pass runs side by side, as many as the LDS allows (at
-        // most kLatSlots): a stage's (slot, end layer, z) states are spread over the
+        // most kLatSlots): a stage's (slot, end layer) entries are spread over the
         // lanes together, so narrow bands fill the wave instead of a few lanes
         int nslot = (dyn_bytes - fixed) / (nv * 16);
         nslot = nslot < kLatSlots ? nslot : kLatSlots;
@@ -233,41 +242,66 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
                 const LatStage S = D.st[s];
                 const LatStage P = D.st[s ? s - 1 : 0];
                 const int64_t steady = B - s - 2 > 0 ? B - s - 2 : 0;   // stage s + 1 (1-based) as bottleneck
-                const int per = 2 * S.wd;
+                const int per = S.wd;
                 for (int e = lane; e < nt * per; e += 64) {
-                    const int ks = e / per, r = e - ks * per;
-                    const int k = r >> 1, z = r & 1;
+                    // one lane an (end layer, threshold slot): both states z = 0 / 1 of
+                    // the end layer from the same loads
+                    const int ks = e / per, k = e - ks * per;
                     const int b = S.blo + k;
                     const int64_t t = lat ? D.red[8 + ks] : 0;
                     int64_t *Vk = V + 2 * (int64_t)nv * ks;
-                    int64_t best = kLBig;
-                    if (lat || z == 0) {
-                        for (int j = 0; j < S.win; ++j) {
-                            const int64_t c = Cst[S.coff + k * S.win + j];
-                            if (c >= kLBig) continue;
-                            const int a = b - S.lo - j;
-                            const int64_t v0 = s ? Vk[2 * (P.voff + a - P.blo)] : (a == 0 ? 0 : kLBig);
-                            if (mode == 0) {
-                                if (v0 < kLBig && v0 + c < best) best = v0 + c;
-                                continue;
-                            }
-                            if (mode == 2) {
-                                const int64_t m = v0 > c ? v0 : c;
-                                if (v0 < kLBig && m < best) best = m;
-                                continue;
-                            }
-                            if (STATS) ++nrel;
-                            if (z == 0) {
-                                if (v0 < kLBig && c < t && v0 + c + ceil3(c) < best) best = v0 + c + ceil3(c);
-                            } else {
-                                const int64_t v1 = s ? Vk[2 * (P.voff + a - P.blo) + 1] : kLBig;
-                                if (v0 < kLBig && c == t && v0 + c + ceil3(c) + steady * c < best)
-                                    best = v0 + c + ceil3(c) + steady * c;
-                                if (v1 < kLBig && c <= t && v1 + c < best) best = v1 + c;
-                            }
+                    // a stage of cost t weighs wt before the bottleneck and wb as it
+                    const int64_t wt = lat ? t + ceil3(t) : 0, wb = wt + steady * t;
+                    const int64_t *Wp = Cst + S.coff + k * S.win;
+                    int64_t best0 = kLBig, best1 = kLBig;
+                    // the previous stage's states at split point a (stage 0: layer 0 at
+                    // cost 0); a split point outside its band has no cost (w = kLBig),
+                    // and the clamped index keeps the read inside the band
+                    auto states = [&](int a, int64_t &v0, int64_t &v1) {
+                        v0 = a == 0 ? 0 : kLBig;
+                        v1 = kLBig;
+                        if (s) {   // wave-uniform
+                            int q = a - P.blo;
+                            q = q < 0 ? 0 : (q >= P.wd ? P.wd - 1 : q);
+                            const int64_t *vp = Vk + 2 * (P.voff + q);
+                            v0 = vp[0];
+                            v1 = vp[1];
                         }
+                    };
+                    auto relax = [&](int64_t w, int64_t v0, int64_t v1) {
+                        const bool live = w < kLBig && v0 < kLBig;
+                        if (mode == 0) {
+                            const int64_t x = v0 + weight_cost(w);
+                            best0 = live && x < best0 ? x : best0;
+                        } else if (mode == 2) {
+                            const int64_t c = weight_cost(w), m = v0 > c ? v0 : c;
+                            best0 = live && m < best0 ? m : best0;
+                        } else {
+                            if (STATS) nrel += w < kLBig ? 2 : 0;   // both states
+                            const int64_t x0 = v0 + w, x1 = v0 + wb, y = v1 + weight_cost(w);
+                            best0 = live && w < wt && x0 < best0 ? x0 : best0;
+                            best1 = live && w == wt && x1 < best1 ? x1 : best1;
+                            best1 = v1 < kLBig && w <= wt && y < best1 ? y : best1;
+                        }
+                    };
+                    // two split points a trip, every load issued before either is used
+                    const int a0 = b - S.lo;
+                    int j = 0;
+                    for (; j + 1 < S.win; j += 2) {
+                        const int64_t wa = Wp[j], wb2 = Wp[j + 1];
+                        int64_t va0, va1, vb0, vb1;
+                        states(a0 - j, va0, va1);
+                        states(a0 - j - 1, vb0, vb1);
+                        relax(wa, va0, va1);
+                        relax(wb2, vb0, vb1);
                     }
-                    Vk[2 * (S.voff + k) + z] = best;
+                    if (j < S.win) {
+                        int64_t v0, v1;
+                        states(a0 - j, v0, v1);
+                        relax(Wp[j], v0, v1);
+                    }
+                    Vk[2 * (S.voff + k)] = best0;
+                    Vk[2 * (S.voff + k) + 1] = best1;
                 }
                 __syncthreads();
             }
@@ -293,8 +327,9 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
                 bool m0 = false, m1 = false;
                 int aj = -1;
                 for (int j = lane; j < S.win; j += 64) {
-                    const int64_t c = Cst[S.coff + k * S.win + j];
-                    if (c >= kLBig) continue;
+                    const int64_t w = Cst[S.coff + k * S.win + j];
+                    if (w >= kLBig) continue;
+                    const int64_t c = weight_cost(w);
                     const int a = b - S.lo - j;
                     const int64_t v0 = s ? Vt[2 * (P.voff + a - P.blo)] : (a == 0 ? 0 : kLBig);
                     const int64_t v1 = s ? Vt[2 * (P.voff + a - P.blo) + 1] : kLBig;
@@ -316,7 +351,7 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
                 const int jj = __shfl(aj, src, 64);
                 if (na >= kLBig || jj < 0) break;   // cannot happen on an optimal path
                 const int e = S.coff + k * S.win + jj;
-                sum += Cst[e];
+                sum += weight_cost(Cst[e]);
                 if (R[e]) rmask |= 1u << s;
                 if (lane == 0) D.len[s] = b - (int)na;
                 b = (int)na;
@@ -378,7 +413,7 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
                         }
                     }
                 }
-                Cst[e] = c;
+                Cst[e] = cost_weight(c);
                 R[e] = r;
             }
             __syncthreads();
@@ -410,13 +445,16 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
                 // pass past the stop is discarded)
                 int nt = 0;
                 for (int64_t lo_t = tprev; nt < nslot; ++nt) {
-                    int64_t tn = kLBig;
+                    // in weights: the least w above lo_t's is the least cost above lo_t
+                    const int64_t wlo = lo_t + ceil3(lo_t);
+                    int64_t wn = kLBig;
                     for (int e = lane; e < ncost; e += 64) {
-                        const int64_t c = Cst[e];
-                        if (c > lo_t && c < tn) tn = c;
+                        const int64_t w = Cst[e];
+                        if (w > wlo && w < wn) wn = w;
                     }
-                    const int64_t t = lat_min(tn);
-                    if (t >= kLBig) break;
+                    const int64_t wmin = lat_min(wn);
+                    if (wmin >= kLBig) break;
+                    const int64_t t = weight_cost(wmin);
                     if (lane == 0) D.red[8 + nt] = t;
                     lo_t = t;
                 }
