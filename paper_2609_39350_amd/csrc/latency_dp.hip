@@ -278,7 +278,11 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
                             best0 = live && m < best0 ? m : best0;
                         } else {
                             if (STATS) nrel += w < kLBig ? 2 : 0;   // both states
-                            const int64_t x0 = v0 + w, x1 = v0 + wb, y = v1 + weight_cost(w);
+                            // (unsigned sums: a state or cost of kLBig gives a value that
+                            // is not used, without a signed overflow)
+                            const int64_t x0 = (int64_t)((uint64_t)v0 + (uint64_t)w);
+                            const int64_t x1 = (int64_t)((uint64_t)v0 + (uint64_t)wb);
+                            const int64_t y = (int64_t)((uint64_t)v1 + (uint64_t)weight_cost(w));
                             best0 = live && w < wt && x0 < best0 ? x0 : best0;
                             best1 = live && w == wt && x1 < best1 ? x1 : best1;
                             best1 = v1 < kLBig && w <= wt && y < best1 ? y : best1;
