@@ -293,8 +293,15 @@ __device__ inline int cap_count(int64_t room, int64_t act)
     if (room < 0) return -1;
     if (act <= 0 || room >= act * 64) return 64;
     if (room < act) return 0;
-    int m = (int)((float)room / (float)act);
-    m = m > 63 ? 63 : m;
+    // act <= room < 64 act, so the quotient lies in [1, 63].  Both are shifted
+    // right until room fits 32 bits (act then keeps at least 25), and the fp32
+    // product with act's approximate reciprocal is within one of the floor.
+    const uint32_t rh = (uint32_t)((uint64_t)room >> 32);
+    const int sh = rh ? 32 - __clz(rh) : 0;
+    const float q = (float)(uint32_t)((uint64_t)room >> sh) *
+                    __builtin_amdgcn_rcpf((float)(uint32_t)((uint64_t)act >> sh));
+    int m = (int)q;
+    m = m > 63 ? 63 : (m < 1 ? 1 : m);
     if ((int64_t)m * act > room)
         --m;
     else if ((int64_t)(m + 1) * act <= room)
@@ -435,6 +442,15 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
         HAPMOE_KEY_PP(PP);
         const PiInfo *pi = reinterpret_cast<const PiInfo *>(tab + L.off_pi) + cfg;
         const KeyInfo *ki = reinterpret_cast<const KeyInfo *>(tab + L.off_key) + key;
+        // stage s's layout fields in lane s, loaded with PP (the arrays hold
+        // kMaxStages entries; lanes from PP on are cleared below)
+        int mask = 0, lo = 0, hi = 0, bp = 0;
+        if (lane < kMaxStages) {
+            mask = ki->mask[lane];
+            lo = ki->lo[lane];
+            hi = ki->hi[lane];
+            bp = ki->bpair[lane];
+        }
         // The configuration's memory prefix sums (stored to LDS for the class
         // split) and, below, the slots' time prefix sums are loaded as soon as
         // their addresses are known, so that their latency overlaps the stage
@@ -475,13 +491,7 @@ __global__ __launch_bounds__(64) void k_stage_dp(const unsigned char *__restrict
         }
 
         // ---- stage s lives in lane s ----
-        int mask = 0, lo = 0, hi = 0, bp = 0;
-        if (lane < PP) {
-            mask = ki->mask[lane];
-            lo = ki->lo[lane];
-            hi = ki->hi[lane];
-            bp = ki->bpair[lane];
-        }
+        if (lane >= PP) mask = lo = hi = bp = 0;
         const uint64_t used = wave_or64(lane < PP ? (uint64_t(1) << mask) : 0);
         const int nslot = __popcll(used);
         const int slot = __popcll(used & ((uint64_t(1) << mask) - 1));

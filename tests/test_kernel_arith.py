@@ -45,3 +45,34 @@ def test_reciprocal_floor_division_is_exact():
         assert np.all(np.abs(q - x // d) <= 1), d
         q = np.where(r < 0, q - 1, np.where(r >= d, q + 1, q))
         assert np.array_equal(q, x // d), d
+
+
+def test_cap_count_estimate_is_corrected_to_the_floor():
+    """The class split's count floor(room / act), act <= room < 64 act: both
+    shifted right until room fits 32 bits, an fp32 product with act's
+    approximate reciprocal (taken here with a relative error of 2^-20 either
+    way, well beyond the hardware's), clamped to [1, 63], then corrected by one
+    integer step either way, equals the floor."""
+    import numpy as np
+
+    rng = np.random.default_rng(11)
+    n = 200_000
+    act = rng.integers(1, 1 << 45, size=n, dtype=np.int64)
+    mult = rng.uniform(1.0, 64.0, size=n)
+    room = np.minimum((act.astype(np.float64) * mult).astype(np.int64), act * 64 - 1)
+    # exact multiples and their neighbours, where the estimate's error shows first
+    k = rng.integers(1, 64, size=n, dtype=np.int64)
+    act = np.concatenate([act, act, act])
+    room = np.concatenate([room, np.minimum(k * act[:n], act[:n] * 64 - 1), np.maximum(k * act[:n] - 1, act[:n])])
+    ok = (room >= act) & (room < 64 * act)
+    room, act = room[ok], act[ok]
+    hi = (room.astype(np.uint64) >> np.uint64(32)).astype(np.int64)
+    sh = np.where(hi > 0, np.floor(np.log2(np.maximum(hi, 1))).astype(np.int64) + 1, 0)
+    r32 = (room >> sh).astype(np.float32)
+    a32 = (act >> sh).astype(np.float32)
+    for err in (1.0 - 2.0 ** -20, 1.0 + 2.0 ** -20):
+        rcp = (np.float32(1.0) / a32) * np.float32(err)
+        m = (r32 * rcp).astype(np.float32).astype(np.int64)
+        m = np.clip(m, 1, 63)
+        m = np.where(m * act > room, m - 1, np.where((m + 1) * act <= room, m + 1, m))
+        assert np.array_equal(m, room // act)
