@@ -334,10 +334,12 @@ int32_t hapmoe_stage_dp_1f1b(const hapmoe_problem *p, const void *d_image,
  * (b_PP-1, ..., b_1) of the stage end layers.  For each candidate of
  * [first, first + count) writes d_res[i - first]: objective = T + C, stage_sum
  * and t_max of the chosen partition, its recomputation mask and stage lengths.
- * One workgroup per candidate.  Its stage-cost table holds, for every stage,
- * end layer b of the stage's band (the end layers its windows allow) and split
- * point of its window, an 8-byte cost and a 1-byte recomputation flag (the
- * flags rounded up to 16 bytes), plus 16 bytes of DP state for every (stage, b).
+ * One workgroup per (configuration, ordering) key, lane j holding the key's
+ * j-th candidate, the deepest pipelines first.  Its stage-cost table holds, for
+ * every stage, end layer b of the stage's band (the end layers its windows
+ * allow) and split point of its window, an 8-byte cost c (kept as
+ * c + ceil(c / 3)) and a 1-byte recomputation flag (the flags rounded up to 16
+ * bytes), plus 16 bytes of DP state for every (stage, b).
  * Launches in tiers of LDS a workgroup: every candidate with 24 KB, then those
  * whose table did not fit (over 22,784 bytes) with 40, 80 and 160 KB; a
  * candidate whose table exceeds 162,048 bytes gets HAPMOE_STATUS_OVERFLOW.  The candidates of a (configuration, ordering) key

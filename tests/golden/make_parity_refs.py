@@ -14,7 +14,10 @@ Contents (each an index array and a uint32 digest array, tests/parity_digest.py)
   cfg4_types       device-count DP, eight candidates of 8-stage and four of
                    4-stage pipelines (written with "types4" as a further
                    argument, merged into the existing file)
-With "latency" as a further argument only the least-latency entries are
+  cfg3_latency_all, cfg5_latency_all   the least 1F1B latency, every candidate
+                   (written with "latency_all" as a further argument, merged
+                   into the existing file; about 2 CPU-hours each)
+With "latency" as a further argument only the least-latency samples are
 (re)computed and merged into the existing file.
 """
 import copy
@@ -119,14 +122,24 @@ def latency_samples():
 
 
 def main():
-    args = [a for a in sys.argv[1:] if a not in ("latency", "types4")]
+    args = [a for a in sys.argv[1:] if a not in ("latency", "types4", "latency_all")]
     workers = int(args[0]) if args else (os.cpu_count() or 1)
     only_latency = "latency" in sys.argv[1:]
     only_types4 = "types4" in sys.argv[1:]
+    latency_all = "latency_all" in sys.argv[1:]
     out = {}
-    if only_latency or only_types4:
+    if only_latency or only_types4 or latency_all:
         with np.load(OUT) as f:
             out = {k: f[k] for k in f.files}
+    if latency_all:
+        with get_context("spawn").Pool(workers) as pool:
+            for n in (3, 5):
+                idx = np.arange(orc.Oracle(workloads.config(n)).n_instances())
+                out[f"cfg{n}_latency_all_idx"] = idx
+                out[f"cfg{n}_latency_all"] = run(pool, f"cfg{n}", "latency", idx, 100)
+                np.savez_compressed(OUT, **out)   # each workload as soon as it is done
+                print("wrote", OUT, os.path.getsize(OUT), "bytes", flush=True)
+        return
     if only_types4:
         t4 = types4_samples()
         with get_context("spawn").Pool(workers) as pool:

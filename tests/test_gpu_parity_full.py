@@ -8,7 +8,8 @@ with one candidate of every (configuration, ordering) key (B rotating over
 1..64) and one of every configuration under the 1F1B re-scoring, and 16
 sixteen-stage candidates of configuration 3 and twelve 4- and 8-stage ones of
 configuration 4 under the device-count DP, and
-stride samples of configurations 3, 4 and 5 under the least 1F1B latency.  A digest
+stride samples of configurations 3, 4 and 5 and every candidate of
+configurations 3 and 5 under the least 1F1B latency.  A digest
 covers status, objective, stage sum, largest stage, recomputation mask, stage
 lengths (and stage types); a mismatch is re-checked against the oracle itself
 and reported field by field.
@@ -118,6 +119,22 @@ def test_least_latency_samples(torch, refs, n):
     res = pl.results()
     assert _check(p, res, refs, f"cfg{n}_latency", "latency") == len(idx)
     assert (res["status"][idx] == 0).sum() > 10
+
+
+@pytest.mark.parametrize("n", [3, 5])
+def test_least_latency_every_candidate(torch, refs, n):
+    """The least 1F1B latency on every candidate of configurations 3 and 5 (one
+    launch over the whole workload, as the bench runs it), against stored oracle
+    digests; skipped if the references were written without them."""
+    if f"cfg{n}_latency_all" not in refs:
+        pytest.skip("no full least-latency references in parity_refs.npz")
+    p = workloads.config(n)
+    print(f"config {n}, least latency: every candidate", flush=True)
+    pl = binding.Planner(p, "cuda:0")
+    pl.eval_cost_tables()
+    pl.stage_dp(objective="latency")
+    res = pl.results()
+    assert _check(p, res, refs, f"cfg{n}_latency_all", "latency") == pl.n
 
 
 def test_device_count_dp_config4_samples(torch, refs):
