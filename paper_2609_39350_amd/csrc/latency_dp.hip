@@ -229,8 +229,8 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
         const LatStage SL = D.st[PP - 1];
         int64_t B = 1;   // the current group's reference B (see below)
 
-        // One pass over the stages, every (end layer, z) state of a stage on its own
-        // lane.  mode 0: the least stage sum (state z = 0 only); 1: the least
+        // One pass over the stages, every end layer of a stage (both its states z =
+        // 0 / 1) on its own lane.  mode 0: the least stage sum (state z = 0 only); 1: the least
         // latency weight with the largest stage exactly t (states z = 0 / 1), for
         // nt thresholds D.red[8 + k] side by side, slot k's states at V + 2 nv k;
         // 2: the least possible largest stage (z = 0 only).  Returns the latency
@@ -292,12 +292,12 @@ __global__ __launch_bounds__(64) void k_latency_dp(const unsigned char *img, con
                     const int a0 = b - S.lo;
                     int j = 0;
                     for (; j + 1 < S.win; j += 2) {
-                        const int64_t wa = Wp[j], wb2 = Wp[j + 1];
-                        int64_t va0, va1, vb0, vb1;
-                        states(a0 - j, va0, va1);
-                        states(a0 - j - 1, vb0, vb1);
-                        relax(wa, va0, va1);
-                        relax(wb2, vb0, vb1);
+                        const int64_t w1 = Wp[j], w2 = Wp[j + 1];
+                        int64_t p0, p1, q0, q1;
+                        states(a0 - j, p0, p1);
+                        states(a0 - j - 1, q0, q1);
+                        relax(w1, p0, p1);
+                        relax(w2, q0, q1);
                     }
                     if (j < S.win) {
                         int64_t v0, v1;

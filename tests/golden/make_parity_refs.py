@@ -16,7 +16,8 @@ Contents (each an index array and a uint32 digest array, tests/parity_digest.py)
                    argument, merged into the existing file)
   cfg3_latency_all, cfg5_latency_all   the least 1F1B latency, every candidate
                    (written with "latency_all" as a further argument, merged
-                   into the existing file; about 2 CPU-hours each)
+                   into the existing file; about 3 CPU-hours each, half an
+                   hour on seven cores)
 With "latency" as a further argument only the least-latency samples are
 (re)computed and merged into the existing file.
 """
