@@ -14,6 +14,9 @@ Contents (each an index array and a uint32 digest array, tests/parity_digest.py)
   cfg4_types       device-count DP, eight candidates of 8-stage and four of
                    4-stage pipelines (written with "types4" as a further
                    argument, merged into the existing file)
+  cfg2_widths      per-stage widths, every candidate of configuration 2
+                   (stage type sets and widths in the digest; "widths2" as a
+                   further argument, merged into the existing file)
   cfg3_latency_all, cfg5_latency_all   the least 1F1B latency, every candidate
                    (written with "latency_all" as a further argument, merged
                    into the existing file; about 3 CPU-hours each, half an
@@ -44,6 +47,10 @@ def _problem(name):
         p = copy.deepcopy(workloads.config(int(name[3])))
         p["space"]["stage_types"] = 2
         return p
+    if name == "cfg2_widths":
+        p = copy.deepcopy(workloads.config(2))
+        p["space"]["stage_types"] = 3
+        return p
     return workloads.config(int(name[3]))
 
 
@@ -51,7 +58,8 @@ def _work(args):
     name, mode, idx = args
     o = orc.Oracle(_problem(name))
     res = {"threshold": o.solve_many, "1f1b": o.solve_exact_many, "latency": o.solve_latency_many}[mode](idx)
-    return parity_digest.of_oracle(res, with_types=name in ("cfg3_types", "cfg4_types"))
+    return parity_digest.of_oracle(res, with_types=name in ("cfg3_types", "cfg4_types", "cfg2_widths"),
+                                   with_widths=name == "cfg2_widths")
 
 
 def run(pool, name, mode, idx, chunk):
@@ -123,15 +131,24 @@ def latency_samples():
 
 
 def main():
-    args = [a for a in sys.argv[1:] if a not in ("latency", "types4", "latency_all")]
+    args = [a for a in sys.argv[1:] if a not in ("latency", "types4", "latency_all", "widths2")]
     workers = int(args[0]) if args else (os.cpu_count() or 1)
     only_latency = "latency" in sys.argv[1:]
     only_types4 = "types4" in sys.argv[1:]
     latency_all = "latency_all" in sys.argv[1:]
+    widths2 = "widths2" in sys.argv[1:]
     out = {}
-    if only_latency or only_types4 or latency_all:
+    if only_latency or only_types4 or latency_all or widths2:
         with np.load(OUT) as f:
             out = {k: f[k] for k in f.files}
+    if widths2:
+        with get_context("spawn").Pool(workers) as pool:
+            idx = np.arange(orc.Oracle(_problem("cfg2_widths")).n_instances())
+            out["cfg2_widths_idx"] = idx
+            out["cfg2_widths"] = run(pool, "cfg2_widths", "threshold", idx, 50)
+        np.savez_compressed(OUT, **out)
+        print("wrote", OUT, os.path.getsize(OUT), "bytes")
+        return
     if latency_all:
         with get_context("spawn").Pool(workers) as pool:
             for n in (3, 5):

@@ -8,6 +8,7 @@ import pytest
 
 from oracle import oracle as orc
 from paper_2609_39350_amd import binding, workloads
+from tests import parity_digest
 from tests.problems import worked_problem_w2
 
 pytestmark = pytest.mark.gpu
@@ -96,6 +97,27 @@ def test_config2_sampled(torch, window):
     idx = sorted(set(list(range(3, pl.n, max(1, pl.n // 160))) + [plan["instance"]]))
     from tests.test_gpu_parity import oracle_many
     assert compare(p, pl, idx, ref=oracle_many(p, idx, pool=True)) > 0
+
+
+def test_config2_every_candidate(torch):
+    """Every candidate of configuration 2 (10,584, one launch) against stored
+    oracle digests of status, objective, stage sum, largest stage,
+    recomputation mask, stage lengths, stage type sets and widths
+    (tests/golden/parity_refs.npz, written from oracle/ alone)."""
+    import os
+    refs_path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "parity_refs.npz")
+    with np.load(refs_path) as f:
+        if "cfg2_widths" not in f.files:
+            pytest.skip("no per-stage widths references in parity_refs.npz")
+        idx, ref = f["cfg2_widths_idx"], f["cfg2_widths"]
+    p = widths(workloads.config(2))
+    print("widths: config 2, every candidate against stored oracle digests", flush=True)
+    pl, plan = _run(p)
+    assert len(idx) == pl.n
+    got = parity_digest.of_gpu(pl.results(), idx, pl.stage_types(), pl.widths())
+    bad = np.nonzero(got != ref)[0]
+    assert len(bad) == 0, f"{len(bad)} of {len(idx)} differ, first: {idx[bad][:5]}"
+    assert (pl.results()["status"] == 0).sum() > 1000
 
 
 def test_config2_sub_ranges_equal_one_launch(torch):
