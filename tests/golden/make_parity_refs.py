@@ -14,6 +14,11 @@ Contents (each an index array and a uint32 digest array, tests/parity_digest.py)
   cfg4_types       device-count DP, eight candidates of 8-stage and four of
                    4-stage pipelines (written with "types4" as a further
                    argument, merged into the existing file)
+  cfg3_types_shallow   device-count DP, every candidate of configuration 3
+                   with at most 8 stages ("types3" as a further argument,
+                   merged into the file: about 3 CPU-hours, the feasible
+                   8-stage candidates half a minute each; the 16-stage ones
+                   take minutes to hours)
   cfg2_widths      per-stage widths, every candidate of configuration 2
                    (stage type sets and widths in the digest; "widths2" as a
                    further argument, merged into the existing file)
@@ -131,16 +136,28 @@ def latency_samples():
 
 
 def main():
-    args = [a for a in sys.argv[1:] if a not in ("latency", "types4", "latency_all", "widths2")]
+    args = [a for a in sys.argv[1:] if a not in ("latency", "types4", "latency_all", "widths2", "types3")]
     workers = int(args[0]) if args else (os.cpu_count() or 1)
     only_latency = "latency" in sys.argv[1:]
     only_types4 = "types4" in sys.argv[1:]
     latency_all = "latency_all" in sys.argv[1:]
     widths2 = "widths2" in sys.argv[1:]
+    types3 = "types3" in sys.argv[1:]
     out = {}
-    if only_latency or only_types4 or latency_all or widths2:
+    if only_latency or only_types4 or latency_all or widths2 or types3:
         with np.load(OUT) as f:
             out = {k: f[k] for k in f.files}
+    if types3:
+        with get_context("spawn").Pool(workers) as pool:
+            o = orc.Oracle(_problem("cfg3_types"))
+            per = o.n_orders() * len(_problem("cfg3_types")["space"]["micro"])
+            pp = np.array([c[0] for c in o.configs()])
+            idx = np.array([i for i in range(o.n_instances()) if pp[i // per] <= 8])
+            out["cfg3_types_shallow_idx"] = idx
+            out["cfg3_types_shallow"] = run(pool, "cfg3_types", "threshold", idx, 4)
+        np.savez_compressed(OUT, **out)
+        print("wrote", OUT, os.path.getsize(OUT), "bytes")
+        return
     if widths2:
         with get_context("spawn").Pool(workers) as pool:
             idx = np.arange(orc.Oracle(_problem("cfg2_widths")).n_instances())

@@ -6,8 +6,9 @@ the oracle's results, written by tests/golden/make_parity_refs.py from oracle/
 alone: configurations 3 and 5 in full under both objectives, configuration 4
 with one candidate of every (configuration, ordering) key (B rotating over
 1..64) and one of every configuration under the 1F1B re-scoring, and 16
-sixteen-stage candidates of configuration 3 and twelve 4- and 8-stage ones of
-configuration 4 under the device-count DP, and
+sixteen-stage candidates and every candidate of up to 8 stages of configuration
+3 and twelve 4- and 8-stage ones of configuration 4 under the device-count DP,
+and
 stride samples of configurations 3, 4 and 5 and every candidate of
 configurations 3 and 5 under the least 1F1B latency.  A digest
 covers status, objective, stage sum, largest stage, recomputation mask, stage
@@ -135,6 +136,26 @@ def test_least_latency_every_candidate(torch, refs, n):
     pl.stage_dp(objective="latency")
     res = pl.results()
     assert _check(p, res, refs, f"cfg{n}_latency_all", "latency") == pl.n
+
+
+def test_device_count_dp_shallow_every_candidate(torch, refs):
+    """The device-count DP on every candidate of configuration 3 with at most 8
+    stages (one launch over the whole workload), stage types included, against
+    stored oracle digests; skipped if the references were written without them."""
+    if "cfg3_types_shallow" not in refs:
+        pytest.skip("no shallow device-count references in parity_refs.npz")
+    p = copy.deepcopy(workloads.config(3))
+    p["space"]["stage_types"] = 2
+    print("config 3, device-count DP: every candidate of up to 8 stages", flush=True)
+    pl = binding.Planner(p, "cuda:0")
+    pl.run()
+    res, types = pl.results(), pl.stage_types()
+    idx = refs["cfg3_types_shallow_idx"]
+    assert (pl.cand_host["pp"][idx] <= 8).all() and len(idx) > 1000
+    got = parity_digest.of_gpu(res, idx, types)
+    bad = np.nonzero(got != refs["cfg3_types_shallow"])[0]
+    assert len(bad) == 0, f"{len(bad)} of {len(idx)} differ, first: {idx[bad][:5]}"
+    assert (res["status"][idx] == 0).sum() > 100
 
 
 def test_device_count_dp_config4_samples(torch, refs):
