@@ -90,12 +90,29 @@ __device__ inline int64_t shfl_xor64(int64_t v, int d)
 // every lane of the wave active).
 __device__ inline int64_t lat_min(int64_t v)
 {
+    // each 16-lane row by DPP row rotations (no LDS round trip), then the four
+    // rows' results from lanes 0, 16, 32 and 48
+#define LAT_ROT_MIN(CTRL)                                                                              \
+    do {                                                                                               \
+        const int lo_ = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(uint64_t)v, CTRL, 0xf, 0xf, false); \
+        const int hi_ = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)((uint64_t)v >> 32), CTRL, 0xf, 0xf, false); \
+        const int64_t o_ = (int64_t)(((uint64_t)(uint32_t)hi_ << 32) | (uint32_t)lo_);                \
+        v = o_ < v ? o_ : v;                                                                           \
+    } while (0)
+    LAT_ROT_MIN(0x128);   // row_ror 8
+    LAT_ROT_MIN(0x124);   // row_ror 4
+    LAT_ROT_MIN(0x122);   // row_ror 2
+    LAT_ROT_MIN(0x121);   // row_ror 1
+#undef LAT_ROT_MIN
+    int64_t m = kLBig + kLBig / 2;   // above every value
 #pragma unroll
-    for (int d = 32; d >= 1; d >>= 1) {
-        const int64_t o = shfl_xor64(v, d);
-        v = o < v ? o : v;
+    for (int r = 0; r < 64; r += 16) {
+        const int lo = __builtin_amdgcn_readlane((int)(uint32_t)(uint64_t)v, r);
+        const int hi = __builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)v >> 32), r);
+        const int64_t o = (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+        m = o < m ? o : m;
     }
-    return v;
+    return m;
 }
 
 __device__ inline int64_t lat_sum(int64_t v)
