@@ -1,6 +1,6 @@
 """Writes tests/golden/parity_refs.npz: digests of the oracle's results on the
-large workloads, for the GPU parity tests (which cannot afford to run the
-oracle over them on the GPU machine).  Calls only oracle/ and the seeded
+large workloads, for the GPU parity tests (the oracle needs hours for them,
+far beyond a test's time limit).  Calls only oracle/ and the seeded
 workload generators.  Run: python tests/golden/make_parity_refs.py [workers]
 
 Contents (each an index array and a uint32 digest array, tests/parity_digest.py):
