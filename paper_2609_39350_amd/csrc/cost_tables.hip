@@ -147,6 +147,9 @@ __global__ __launch_bounds__(kThreads, 8) void k_cost_tables(const unsigned char
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const hapmoe_candidate c = cand[cfg * per_config];
     const int N = H.n_layers, T = H.n_types;
+    // MoE flags of layers 2 lane and 2 lane + 1, the layers this lane takes in the
+    // prefix sums and for every device-type set
+    const bool moe2[2] = {2 * lane < N && is_moe[2 * lane] != 0, 2 * lane + 1 < N && is_moe[2 * lane + 1] != 0};
     double *dcfg = dbg ? dbg + cfg * D.per_cfg : nullptr;
 
     __shared__ int64_t s_qce[kMaxTypes][kLayerSlots];   // q(comp) + q(expert) per type, layer
@@ -158,6 +161,7 @@ __global__ __launch_bounds__(kThreads, 8) void k_cost_tables(const unsigned char
     __shared__ unsigned s_used, s_flag;
     __shared__ int64_t s_tbar;
     __shared__ int32_t s_ospd[kMaxOrders][kMaxStages];   // block orderings: speed of each stage
+    __shared__ int32_t s_perm[kMaxOrders][kMaxTypes], s_count[kMaxTypes], s_speed[kMaxTypes];   // orderings, devices
     __shared__ uint8_t s_omask[kMaxOrders][kMaxStages];  //   and its device-type set
     __shared__ int64_t s_osum[kMaxOrders];               //   summed stage speeds
 
@@ -184,6 +188,12 @@ __global__ __launch_bounds__(kThreads, 8) void k_cost_tables(const unsigned char
     // device-type set
     for (int l = tid; l < N; l += kThreads) s_skew[l] = reinterpret_cast<const double *>(tab + L.off_layer)[l];
     if (tid >= 1 && tid < (1 << T)) set_link(H, tid, s_link_a[tid], s_link_b[tid]);
+    // the orderings, device counts and speeds, read by every (ordering, stage) pair below
+    if (tid < kMaxOrders * kMaxTypes) s_perm[tid / kMaxTypes][tid % kMaxTypes] = H.perm[tid / kMaxTypes][tid % kMaxTypes];
+    if (tid < kMaxTypes) {
+        s_count[tid] = H.count[tid];
+        s_speed[tid] = H.speed[tid];
+    }
     __syncthreads();
 
     // ---- stage layout of the block orderings: (ordering, stage) pairs over the threads ----
@@ -192,27 +202,35 @@ __global__ __launch_bounds__(kThreads, 8) void k_cost_tables(const unsigned char
         const int nord = H.n_orders, PP = c.pp, g = H.total_devices / PP, npair = nord * PP;
         for (int i = tid; i < npair; i += kThreads) {
             const int o = i / PP, s = i - o * PP;
-            int pos_type[kMaxTypes], pos_end[kMaxTypes];
+            // (loops over all kMaxTypes positions, unrolled, so that the arrays stay in
+            // registers; positions j >= T take no part)
+            int pos_type[kMaxTypes], pos_cnt[kMaxTypes], pos_end[kMaxTypes];
             int acc = 0;
-            for (int j = 0; j < T; ++j) {
-                pos_type[j] = H.perm[o][j];
-                acc += H.count[pos_type[j]];
+#pragma unroll
+            for (int j = 0; j < kMaxTypes; ++j) {
+                pos_type[j] = j < T ? s_perm[o][j] : 0;
+                pos_cnt[j] = j < T ? s_count[pos_type[j]] : 0;
+                acc += pos_cnt[j];
                 pos_end[j] = acc;
             }
+            // the type of device d: that of the first block ending past d, else the last block's
             auto type_of = [&](int d) {
-                int t = pos_type[T - 1];
-                for (int j = T - 1; j >= 0; --j)
-                    if (d < pos_end[j]) t = pos_type[j];
+                int t = 0;
+#pragma unroll
+                for (int j = kMaxTypes - 1; j >= 0; --j)
+                    if (j == T - 1 || (j < T && d < pos_end[j])) t = pos_type[j];
                 return t;
             };
             const int d0 = s * g, d1 = d0 + g;
             int mask = 0;
-            for (int j = 0; j < T; ++j)
-                if (pos_end[j] - H.count[pos_type[j]] < d1 && pos_end[j] > d0) mask |= 1 << pos_type[j];
+#pragma unroll
+            for (int j = 0; j < kMaxTypes; ++j)
+                if (j < T && pos_end[j] - pos_cnt[j] < d1 && pos_end[j] > d0) mask |= 1 << pos_type[j];
             const int bpair = s < PP - 1 ? (type_of(d1 - 1) << 2) | type_of(d1) : 0;
             int sp = 0;
-            for (int h = 0; h < T; ++h)
-                if ((mask >> h) & 1) sp = (sp == 0 || H.speed[h] < sp) ? H.speed[h] : sp;
+#pragma unroll
+            for (int h = 0; h < kMaxTypes; ++h)
+                if (h < T && ((mask >> h) & 1)) sp = (sp == 0 || s_speed[h] < sp) ? s_speed[h] : sp;
             KeyInfo *K = reinterpret_cast<KeyInfo *>(tab + L.off_key) + (cfg * L.n_orders + o);
             K->mask[s] = (uint8_t)mask;
             K->bpair[s] = (uint8_t)bpair;
@@ -414,7 +432,7 @@ __global__ __launch_bounds__(kThreads, 8) void k_cost_tables(const unsigned char
             v[0][k] = ok ? s_w[l] : 0;
             v[1][k] = ok ? s_a0[l] : 0;
             v[2][k] = ok ? s_a1[l] : 0;
-            v[3][k] = ok ? (int64_t)(is_moe[l] != 0) : 0;
+            v[3][k] = ok ? (int64_t)moe2[k] : 0;
         }
         for (int f = 0; f < 4; ++f) {
             const int64_t ex = wave_excl_scan(v[f][0] + v[f][1], lane);
@@ -432,8 +450,7 @@ __global__ __launch_bounds__(kThreads, 8) void k_cost_tables(const unsigned char
     for (int m = 1; m <= (int)L.n_masks; ++m) {
         if (!((used >> (m - 1)) & 1)) continue;
         if ((k++ & 3) != wave) continue;
-        double alpha, bw;
-        set_link(H, m, alpha, bw);
+        const double alpha = s_link_a[m], bw = s_link_b[m];
         int64_t *P = reinterpret_cast<int64_t *>(tab + L.off_time) + (cfg * L.n_masks + (m - 1)) * 3 * np;
         int64_t v[3][2];
         for (int kk = 0; kk < 2; ++kk) {
@@ -441,7 +458,7 @@ __global__ __launch_bounds__(kThreads, 8) void k_cost_tables(const unsigned char
             v[0][kk] = v[1][kk] = v[2][kk] = 0;
             if (l >= N) continue;
             double a2a, tp;
-            if (!is_moe[l]) {
+            if (!moe2[kk]) {
                 a2a = 0.0;
                 tp = 4.0 * ring_ar(Dact, c.tp, alpha, bw);
             } else {
@@ -478,23 +495,24 @@ __global__ __launch_bounds__(kThreads, 8) void k_cost_tables(const unsigned char
         }
     }
 
-    __syncthreads();
-
-    // ---- per-configuration record (after every overflow flag is in) ----
-    if (tid == 0) {
-        PiInfo *pi = reinterpret_cast<PiInfo *>(tab + L.off_pi) + cfg;
-        // boundary transfer: activation forward + gradient back, tokens*H*beta/TP each way
-        for (int h = 0; h < kMaxTypes; ++h)
-            for (int g = 0; g < kMaxTypes; ++g) {
-                int64_t v = 0;
-                if (h < T && g < T) {
-                    const double a = H.alpha[h * kMaxTypes + g], b = H.bw[h * kMaxTypes + g];
-                    v = qterm(2.0 * (a + (Dact / (double)c.tp) / b), &s_flag);
-                }
-                pi->p2p[h * kMaxTypes + g] = v;
-            }
+    // ---- per-configuration record ----
+    PiInfo *pi = reinterpret_cast<PiInfo *>(tab + L.off_pi) + cfg;
+    if (tid < kMaxTypes * kMaxTypes) {
+        // boundary transfer: activation forward + gradient back, tokens*H*beta/TP each
+        // way; one (h, g) link a thread
+        const int h = tid / kMaxTypes, g = tid % kMaxTypes;
+        int64_t v = 0;
+        if (h < T && g < T) {
+            const double a = H.alpha[h * kMaxTypes + g], b = H.bw[h * kMaxTypes + g];
+            v = qterm(2.0 * (a + (Dact / (double)c.tp) / b), &s_flag);
+        }
+        pi->p2p[tid] = v;
+    } else if (tid == kMaxTypes * kMaxTypes) {
         // routing metadata (8 bytes per token and choice) + dispatch and combine buffers
         pi->x_bytes = qterm(((8.0 * tok) * (double)H.top_k) + 2.0 * dmoe, &s_flag);
+    }
+    __syncthreads();   // every overflow flag is in
+    if (tid == 0) {
         pi->tbar = s_tbar;
         pi->used_masks = s_used;
         pi->status = s_flag ? HAPMOE_STATUS_OVERFLOW : HAPMOE_STATUS_OK;
