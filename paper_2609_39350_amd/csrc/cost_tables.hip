@@ -35,17 +35,21 @@ __device__ inline int64_t qterm(double x, unsigned *flag)
 // over all (h, h') pairs of the set.
 __device__ inline void set_link(const ImageHeader &H, int mask, double &alpha, double &bw)
 {
+    // (unrolled over all kMaxTypes x kMaxTypes pairs so that every load is issued at
+    // once; pairs outside the set take no part)
     bool first = true;
     alpha = 0.0;
     bw = 0.0;
-    for (int h = 0; h < H.n_types; ++h) {
-        if (!((mask >> h) & 1)) continue;
-        for (int g = 0; g < H.n_types; ++g) {
-            if (!((mask >> g) & 1)) continue;
+#pragma unroll
+    for (int h = 0; h < kMaxTypes; ++h) {
+#pragma unroll
+        for (int g = 0; g < kMaxTypes; ++g) {
             const double a = H.alpha[h * kMaxTypes + g], b = H.bw[h * kMaxTypes + g];
-            if (first || a > alpha) alpha = a;
-            if (first || b < bw) bw = b;
-            first = false;
+            if (h < H.n_types && g < H.n_types && ((mask >> h) & 1) && ((mask >> g) & 1)) {
+                if (first || a > alpha) alpha = a;
+                if (first || b < bw) bw = b;
+                first = false;
+            }
         }
     }
 }
@@ -176,9 +180,11 @@ __global__ __launch_bounds__(kThreads, 8) void k_cost_tables(const unsigned char
     }
     if (wave == 0) {   // parameters per device, averaged over the stages (exact int64 sums)
         int64_t pd = 0, pe = 0;
-        for (int l = lane; l < N; l += 64) {
-            pd += pdense[l];
-            pe += pexp[l];
+#pragma unroll
+        for (int r = 0; r < kLayerSlots / 64; ++r) {   // N < kLayerSlots: every load at once
+            const int l = lane + 64 * r;
+            pd += l < N ? pdense[l] : 0;
+            pe += l < N ? pexp[l] : 0;
         }
         pd = wave_sum(pd);
         pe = wave_sum(pe);
@@ -473,8 +479,9 @@ __global__ __launch_bounds__(kThreads, 8) void k_cost_tables(const unsigned char
                                          : 3.0 * ((double)(c.cp - 1) * (alpha + ((2.0 * Dact) / (double)c.tp) / bw));
             const int64_t comm = qterm(a2a, &s_flag) + qterm(tp, &s_flag) + qterm(cpt, &s_flag);
             int64_t ce = 0;
-            for (int h = 0; h < T; ++h)
-                if ((m >> h) & 1) ce = s_qce[h][l] > ce ? s_qce[h][l] : ce;
+#pragma unroll
+            for (int h = 0; h < kMaxTypes; ++h)
+                if (h < T && ((m >> h) & 1)) ce = s_qce[h][l] > ce ? s_qce[h][l] : ce;
             const int64_t t0 = ce + comm;
             v[0][kk] = t0;
             v[1][kk] = qterm(H.rc_time * (double)t0, &s_flag);
