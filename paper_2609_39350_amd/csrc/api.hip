@@ -143,23 +143,25 @@ void build_space(const hapmoe_problem *p, Space &S)
             if (!whole) continue;
         }
         bool any = false;
+        // TP, CP, EP and TPE are powers of two, so every divisibility test below is
+        // a mask test: x % d == (x & (d - 1)) for x >= 0
         for (int TP : tps) {
-            if (g % TP || m.hidden % TP) continue;
+            if ((g & (TP - 1)) || (m.hidden & (TP - 1))) continue;
             for (int CP : cps) {
-                if (m.seq_len % CP) continue;
+                if (m.seq_len & (CP - 1)) continue;
                 for (int EP : eps)
                     for (int TPE : tpes) {
                         int DP;
                         if (sp.mode == 0) {
-                            if (g % (TP * CP) || g % (EP * TPE)) continue;
+                            if ((g & (TP * CP - 1)) || (g & (EP * TPE - 1))) continue;
                             DP = g / (TP * CP);
                         } else {
                             const int prod = TP * CP * EP * TPE;
-                            if (g % prod) continue;
+                            if (g & (prod - 1)) continue;
                             DP = g / prod;
                         }
                         // per-stage widths: half a group holds whole replicas and expert groups
-                        if (widths && (DP % 2 || (g / 2) % (EP * TPE))) continue;
+                        if (widths && ((DP & 1) || ((g / 2) & (EP * TPE - 1)))) continue;
                         S.cfg.push_back({PP, TP, CP, DP, EP, TPE});
                         any = true;
                     }
