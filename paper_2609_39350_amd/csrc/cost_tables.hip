@@ -194,7 +194,7 @@ __global__ __launch_bounds__(kThreads, 8) void k_cost_tables(const unsigned char
     // device-type set
     for (int l = tid; l < N; l += kThreads) s_skew[l] = reinterpret_cast<const double *>(tab + L.off_layer)[l];
     if (tid >= 1 && tid < (1 << T)) set_link(H, tid, s_link_a[tid], s_link_b[tid]);
-    // the orderings, device counts and speeds, read by every (ordering, stage) pair below
+    // the orderings, device counts and speeds, read by the stage layouts below
     if (tid < kMaxOrders * kMaxTypes) s_perm[tid / kMaxTypes][tid % kMaxTypes] = H.perm[tid / kMaxTypes][tid % kMaxTypes];
     if (tid < kMaxTypes) {
         s_count[tid] = H.count[tid];
@@ -296,7 +296,7 @@ __global__ __launch_bounds__(kThreads, 8) void k_cost_tables(const unsigned char
             int64_t M = 1;   // multinomial of the counts so far; it never falls, and stays <= 2^20
             int r = 0;
             for (int h = 0; h < kMaxTypes; ++h) {
-                k[h] = h < T ? H.count[h] / g : 0;
+                k[h] = h < T ? s_count[h] / g : 0;
                 for (int i = 1; i <= k[h]; ++i) M = M * ++r / i;
             }
             if (o >= M) {   // past this pipeline's sequences: no partition is feasible
@@ -326,9 +326,9 @@ __global__ __launch_bounds__(kThreads, 8) void k_cost_tables(const unsigned char
         int pos_type[kMaxTypes], pos_start[kMaxTypes], pos_end[kMaxTypes];
         int acc = 0;
         for (int j = 0; j < T; ++j) {
-            pos_type[j] = H.stage_types ? j : H.perm[o][j];   // perm holds |H|! <= 24 rows
+            pos_type[j] = H.stage_types ? j : s_perm[o][j];   // perm holds |H|! <= 24 rows
             pos_start[j] = acc;
-            acc += H.count[pos_type[j]];
+            acc += s_count[pos_type[j]];
             pos_end[j] = acc;
         }
         auto type_of = [&](int d) {
@@ -353,7 +353,7 @@ __global__ __launch_bounds__(kThreads, 8) void k_cost_tables(const unsigned char
             }
             int sp = 0;
             for (int h = 0; h < T; ++h)
-                if ((mask >> h) & 1) sp = (sp == 0 || H.speed[h] < sp) ? H.speed[h] : sp;
+                if ((mask >> h) & 1) sp = (sp == 0 || s_speed[h] < sp) ? s_speed[h] : sp;
             spd[s] = sp;
             sum_speed += sp;
             double a, b;
