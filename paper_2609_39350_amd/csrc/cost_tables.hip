@@ -62,15 +62,25 @@ __device__ inline double ring_ar(double bytes, int w, double alpha, double bw)
     return steps * alpha + ((steps * bytes) / (double)w) / bw;
 }
 
-__device__ inline int64_t wave_excl_scan(int64_t x, int lane)
+// K exclusive wave scans side by side (their shuffles overlap): x[f] becomes the
+// sum of x[f] over the lower lanes
+template <int K>
+__device__ inline void wave_excl_scan_k(int64_t (&x)[K], int lane)
 {
-    int64_t inc = x;
+    int64_t inc[K];
+#pragma unroll
+    for (int f = 0; f < K; ++f) inc[f] = x[f];
 #pragma unroll
     for (int d = 1; d < 64; d <<= 1) {
-        const int64_t y = __shfl_up(inc, d, 64);
-        if (lane >= d) inc += y;
+        int64_t y[K];
+#pragma unroll
+        for (int f = 0; f < K; ++f) y[f] = __shfl_up(inc[f], d, 64);
+#pragma unroll
+        for (int f = 0; f < K; ++f)
+            if (lane >= d) inc[f] += y[f];
     }
-    return inc - x;
+#pragma unroll
+    for (int f = 0; f < K; ++f) x[f] = inc[f] - x[f];
 }
 
 __device__ inline int64_t wave_sum(int64_t x)
@@ -440,8 +450,13 @@ __global__ __launch_bounds__(kThreads, 8) void k_cost_tables(const unsigned char
             v[2][k] = ok ? s_a1[l] : 0;
             v[3][k] = ok ? (int64_t)moe2[k] : 0;
         }
+        int64_t exs[4];
+#pragma unroll
+        for (int f = 0; f < 4; ++f) exs[f] = v[f][0] + v[f][1];
+        wave_excl_scan_k(exs, lane);
+#pragma unroll
         for (int f = 0; f < 4; ++f) {
-            const int64_t ex = wave_excl_scan(v[f][0] + v[f][1], lane);
+            const int64_t ex = exs[f];
             if (lane == 0) mem[f * np] = 0;
             if (l0 < N) mem[f * np + l0 + 1] = ex + v[f][0];
             if (l1 < N) mem[f * np + l1 + 1] = ex + v[f][0] + v[f][1];
@@ -494,8 +509,13 @@ __global__ __launch_bounds__(kThreads, 8) void k_cost_tables(const unsigned char
             }
         }
         const int l0 = 2 * lane, l1 = 2 * lane + 1;
+        int64_t exs[3];
+#pragma unroll
+        for (int f = 0; f < 3; ++f) exs[f] = v[f][0] + v[f][1];
+        wave_excl_scan_k(exs, lane);
+#pragma unroll
         for (int f = 0; f < 3; ++f) {
-            const int64_t ex = wave_excl_scan(v[f][0] + v[f][1], lane);
+            const int64_t ex = exs[f];
             if (lane == 0) P[f * np] = 0;
             if (l0 < N) P[f * np + l0 + 1] = ex + v[f][0];
             if (l1 < N) P[f * np + l1 + 1] = ex + v[f][0] + v[f][1];
